@@ -1,0 +1,37 @@
+"""CPU oracle for LLMCad's token-tree verification pass (arXiv 2309.04255, §3.2).
+
+TEST INFRASTRUCTURE ONLY.  This package is a plain, slow, obviously correct
+NumPy (float64) statement of what the verification pass computes.  Only the
+test suite, the package entry's smoke check and the benchmark's CPU-baseline
+leg may import it.  It shares no code with the HIP path: it imports neither
+the library package nor its binding, and the library never imports it.
+
+Contents
+  model.py  the decoder forward as the plain causal definition, and the
+            tree-masked forward over every node of a token tree
+            (§3.2 "Tree decoder" masking table; "Batched non-autoregressive
+            verification")
+  walk.py   greedy acceptance: branch correct sequences, the correct token
+            tree and its depth-first longest path (§3.2 "Depth-first verified
+            sequence searching")
+
+Every function is pinned by tests/test_oracle_*.py against something other
+than itself: brute force, an independent library implementation
+(transformers' LLaMA), closed forms, invariants or hand-built cases.  The
+readings taken where the paper is silent or garbled are listed with the
+build's design notes.
+"""
+
+from .model import (  # noqa: F401
+    OracleConfig,
+    OracleWeights,
+    bf16_round,
+    rmsnorm,
+    rope,
+    silu,
+    causal_forward,
+    prefill_kv,
+    tree_forward,
+    verify_tree,
+)
+from .walk import accept_walk, branch_sequences, correct_sequences  # noqa: F401

@@ -1,0 +1,79 @@
+"""Model shapes and verification workloads.
+
+Shapes are LLaMA-style decoder-only stacks (the paper's phone targets are
+LLaMa2 / Vicuna 7B and 13B, Table 3; its memory-wall table adds 33B, Table 1).
+The paper names the layer kinds only generically (embedding, masked
+self-attention, norm, linear; §2.1).  The concrete block is RMSNorm, rotary
+positions, multi-head attention with as many K/V heads as query heads, a
+SwiGLU feed-forward, no biases, an untied LM head.
+"""
+
+from dataclasses import dataclass, field
+
+
+@dataclass(frozen=True)
+class ModelShape:
+    name: str
+    n_layers: int
+    d_model: int
+    n_heads: int
+    head_dim: int
+    d_ffn: int
+    vocab: int
+    rms_eps: float = 1e-6
+    rope_theta: float = 10000.0
+    weight_std: float = 0.02
+    seed: int = 0
+
+    def params(self) -> int:
+        d, f, v, l = self.d_model, self.d_ffn, self.vocab, self.n_layers
+        return l * (4 * d * d + 3 * d * f + 2 * d) + 2 * v * d + d
+
+
+MODELS = {
+    "tiny": ModelShape("tiny", 2, 256, 4, 64, 688, 1024, seed=0x5EED0001),
+    "llama7b": ModelShape("llama7b", 32, 4096, 32, 128, 11008, 32000, seed=0x5EED0007),
+    "llama13b": ModelShape("llama13b", 40, 5120, 40, 128, 13824, 32000, seed=0x5EED0013),
+    "llama30b": ModelShape("llama30b", 60, 6656, 52, 128, 17920, 32000, seed=0x5EED0030),
+}
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One verification workload: a model, a prefix length and a tree recipe.
+
+    tree: ("complete", (b1, b2, ...)) -> root plus levels with branching b_k;
+          ("random", n, max_parent_depth) -> parent of node i uniform over
+          earlier nodes whose depth is at most max_parent_depth;
+          ("chain", n) -> a single branch.
+    """
+
+    name: str
+    model: str
+    prefix_len: int
+    tree: tuple
+    seed: int = 1234
+    notes: str = ""
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def shape(self) -> ModelShape:
+        return MODELS[self.model]
+
+
+WORKLOADS = {
+    "tiny_p32_n15": Workload("tiny_p32_n15", "tiny", 32, ("complete", (2, 2, 2))),
+    "llama7b_p512_n31": Workload("llama7b_p512_n31", "llama7b", 512, ("complete", (2, 2, 2, 2))),
+    "llama7b_p2048_n41": Workload("llama7b_p2048_n41", "llama7b", 2048, ("complete", (4, 3, 2))),
+    "llama13b_p1024_n41": Workload("llama13b_p1024_n41", "llama13b", 1024, ("complete", (4, 3, 2))),
+    "llama30b_p1024_n1": Workload("llama30b_p1024_n1", "llama30b", 1024, ("random", 1, 7)),
+    "llama30b_p1024_n8": Workload("llama30b_p1024_n8", "llama30b", 1024, ("random", 8, 7)),
+    "llama30b_p1024_n32": Workload("llama30b_p1024_n32", "llama30b", 1024, ("random", 32, 7)),
+    "llama30b_p1024_n128": Workload("llama30b_p1024_n128", "llama30b", 1024, ("random", 128, 7)),
+}
+
+
+def get_workload(name: str) -> Workload:
+    if name not in WORKLOADS:
+        raise KeyError(f"unknown workload {name!r}; known: {sorted(WORKLOADS)}")
+    return WORKLOADS[name]
