@@ -1,0 +1,270 @@
+#!/usr/bin/env python3
+"""Token-tree verification benchmark on one MI355X.
+
+A step is one verification pass (§3.2 of arXiv 2309.04255): the target
+model's forward over every node of a draft token tree against the prefix KV
+cache, the per-node argmax and the accept walk, all in libllmcad's HIP
+kernels.  Default workload: LLaMA-7B shape (32 layers, d 4096, 32x128 heads,
+F 11008, V 32000), random bf16 weights, 512-token prefix, 31-node tree
+(root + complete binary tree of depth 4), uniform tokens.
+
+Prints one JSON line (rank 0):
+  value            passes/s over the timed steps (inputs resident in HBM)
+  hbm_roofline_frac  algorithmic bytes of a pass / (time per pass * 8 TB/s)
+  roofline         the dominant kernel (gate/up GEMM + SwiGLU): algorithmic
+                   bytes per launch / mean launch time (HIP events on the
+                   pass's stream), against 8 TB/s
+  cpu_baseline     the CPU oracle timed on this host on a bounded sample
+Progress goes to stderr.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
+METRIC = "tree-verify passes/sec + % HBM roofline, LLaMA-7B shape, 31-node tree"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_gemm_traffic.json")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2309_04255_amd", "csrc", "gemm.hip")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def pass_bytes(shape, P, n):
+    """Algorithmic HBM bytes of one pass: every weight byte once (embedding: n
+    rows), prefix K+V read once, tree K/V written, embedding rows, fp32 logits."""
+    L, d, F, V = shape.n_layers, shape.d_model, shape.d_ffn, shape.vocab
+    weights = 2 * (L * (4 * d * d + 3 * d * F + 2 * d) + V * d + d)
+    return weights + 4 * L * P * d + 4 * L * n * d + 2 * n * d + 4 * n * V
+
+
+def gate_up_bytes(shape, n):
+    """Algorithmic bytes of one gate/up launch: W_gate and W_up (bf16) once,
+    the fp32 residual rows read once, the bf16 SwiGLU product written once."""
+    d, F = shape.d_model, shape.d_ffn
+    return 2 * (2 * F * d) + 4 * n * d + 2 * n * F
+
+
+def source_hash():
+    with open(GEMM_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(n_expected):
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("gemm_source_sha256_16") != source_hash() or t.get("tree_nodes") != n_expected:
+        return None  # the kernel changed since the counters were taken
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(shape, P, n, seed):
+    """Time the CPU oracle on a bounded sample: tree_forward with 1 and 2 of the
+    model's layers (+ embedding and LM head); one pass = t1 + (L-1)(t2 - t1)."""
+    import numpy as np
+
+    import oracle
+    import workloads
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # threadpoolctl missing: report the visible cores
+        threads = os.cpu_count() or 1
+    gen = workloads.make_weights(shape, "cpu")
+
+    def np64(t):
+        return t.float().numpy().astype(np.float64)
+
+    t0 = time.perf_counter()
+    layers = {l: {k: np64(v) for k, v in gen.layer(l).items()} for l in (0, 1)}
+    emb, fin, head = np64(gen.tok_embed()), np64(gen.final_norm()), np64(gen.lm_head())
+    log(f"cpu baseline: weights for 2 layers converted in {time.perf_counter() - t0:.1f}s")
+    rng = np.random.default_rng(seed)
+    H, Dh = shape.n_heads, shape.head_dim
+    pk = oracle.bf16_round(rng.standard_normal((2, P, H, Dh)))
+    pv = oracle.bf16_round(rng.standard_normal((2, P, H, Dh)))
+    parent, tok = workloads.make_tree(("complete", (2, 2, 2, 2)), shape.vocab, seed) \
+        if n == 31 else workloads.make_tree(("random", n, 7), shape.vocab, seed)
+
+    def run(nl):
+        cfg = oracle.OracleConfig(nl, shape.d_model, shape.n_heads, shape.head_dim, shape.d_ffn,
+                                  shape.vocab, shape.rms_eps, shape.rope_theta)
+        w = oracle.OracleWeights(cfg, emb, fin, head, lambda l: layers[l])
+        w.layer(0)
+        if nl > 1:
+            w.layer(1)
+        t = time.perf_counter()
+        oracle.tree_forward(w, pk[:nl], pv[:nl], tok, parent, rounding=True)
+        return time.perf_counter() - t
+
+    reps = []
+    for _ in range(3):
+        t1, t2 = run(1), run(2)
+        reps.append((t1, t2))
+    t1 = statistics.median(r[0] for r in reps)
+    t2 = statistics.median(r[1] for r in reps)
+    per_pass = t1 + (shape.n_layers - 1) * max(t2 - t1, 0.0)
+    log(f"cpu baseline: 1 layer {t1:.2f}s, 2 layers {t2:.2f}s -> {per_pass:.1f}s per pass")
+    return {
+        "value": 1.0 / per_pass,
+        "unit": "passes/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"oracle.tree_forward (float64 NumPy, bf16 storage rounding) with layers 0 and 1 "
+                   f"of the {shape.n_layers}-layer model plus embedding and LM head, P={P}, n={n}; "
+                   f"median of 3; pass = t(1 layer) + {shape.n_layers - 1} x (t(2) - t(1)); "
+                   f"host cores visible: {os.cpu_count()}"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama7b_p512_n31")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures a single GPU: this build has no multi-GPU path "
+              "(run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import workloads
+    from paper_2309_04255_amd import binding
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    wl = workloads.get_workload(args.workload)
+    shape = wl.shape
+    P = wl.prefix_len
+    parent, tok = workloads.make_tree(wl.tree, shape.vocab, wl.seed)
+    n = len(parent)
+    prefix = workloads.draw_tokens(P, shape.vocab, seed=wl.seed)
+
+    t0 = time.perf_counter()
+    sess = binding.Session(shape, capacity=P + max(n, 128), max_n=128)
+    gen = workloads.make_weights(shape, "cuda")
+    binding.pack_globals(sess.cfg, gen.tok_embed(), gen.final_norm(), gen.lm_head(), sess.packed)
+    for l in range(shape.n_layers):
+        binding.pack_layer(sess.cfg, l, gen.layer(l), sess.packed)
+        torch.cuda.synchronize()
+        if l % 8 == 7:
+            log(f"packed layer {l + 1}/{shape.n_layers}")
+    torch.cuda.empty_cache()
+    sess.prefill(prefix, 0)
+    torch.cuda.synchronize()
+    log(f"setup (weights, packing, {P}-token prefill) {time.perf_counter() - t0:.1f}s")
+
+    def one_pass():
+        binding.verify_tree(sess.cfg, sess.packed, sess.k_cache, sess.v_cache, P, tok, parent,
+                            sess.logits, sess.path, sess.accept_len, sess.next_token, sess.workspace)
+
+    for _ in range(args.warmup):
+        one_pass()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        one_pass()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    gpu_s = ev0.elapsed_time(ev1) / 1e3
+    elapsed = max(wall, gpu_s)
+    ms_per_pass = 1e3 * elapsed / args.steps
+    value = args.steps / elapsed
+    log(f"timed {args.steps} passes: wall {wall * 1e3:.1f} ms, events {gpu_s * 1e3:.1f} ms "
+        f"-> {ms_per_pass:.3f} ms/pass")
+
+    # Dominant kernel: gate/up GEMM, timed per launch with HIP events on the same
+    # stream, over the same number of passes in the same launch configuration.
+    launches = args.steps * shape.n_layers
+    binding.timing_enable(binding.KERNEL_GATE_UP, launches)
+    for _ in range(args.steps):
+        one_pass()
+    torch.cuda.synchronize()
+    tot_ms, nl = binding.timing_read(binding.KERNEL_GATE_UP)
+    binding.timing_enable(-1, 0)
+    gu_ms = tot_ms / max(nl, 1)
+    gu_alg = gate_up_bytes(shape, n)
+    gu_achieved = gu_alg / (gu_ms / 1e3)
+    log(f"gate/up GEMM: {nl} launches, mean {gu_ms * 1e3:.1f} us, {gu_achieved / 1e9:.0f} GB/s")
+
+    # Latency of a pass when the decode loop waits for the accepted path.
+    lat = []
+    for _ in range(min(args.steps, 20)):
+        t = time.perf_counter()
+        one_pass()
+        sess.accept_len.cpu()
+        lat.append(time.perf_counter() - t)
+
+    B = pass_bytes(shape, P, n)
+    frac = B / (elapsed / args.steps) / HBM_PEAK
+    traffic = load_traffic(n)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "passes/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_pass, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic: random-init bf16 weights (counter-hash Irwin-Hall, std 0.02), uniform tokens",
+        "config": {
+            "workload": wl.name,
+            "shape": f"L{shape.n_layers} d{shape.d_model} H{shape.n_heads}x{shape.head_dim} "
+                     f"F{shape.d_ffn} V{shape.vocab}",
+            "prefix_len": P,
+            "tree_nodes": n,
+            "tree": str(wl.tree),
+        },
+        "tree_tokens_per_s": round(value * n, 1),
+        "hbm_roofline_frac": round(frac, 4),
+        "pass_alg_bytes": B,
+        "ms_per_pass_with_readback": round(1e3 * statistics.median(lat), 4),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "gate/up GEMM + SwiGLU (gemm_kernel PRO_NORM EPI_SWIGLU)",
+            "achieved": round(gu_achieved / 1e9, 1),
+            "peak": HBM_PEAK / 1e9,
+            "unit": "GB/s",
+            "frac": round(gu_achieved / HBM_PEAK, 4),
+            "traffic": traffic,
+            "alg_bytes_per_launch": gu_alg,
+            "mean_launch_us": round(gu_ms * 1e3, 2),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle (bounded sample)")
+        out["cpu_baseline"] = cpu_baseline(shape, P, n, wl.seed)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

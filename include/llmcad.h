@@ -1,0 +1,190 @@
+/*
+ * llmcad.h — C ABI of the MI355X (gfx950) token-tree verification library.
+ *
+ * The library computes the target model's side of LLMCad's
+ * generate-then-verify decoding (arXiv 2309.04255):
+ *
+ *   §3.2 "Token tree verification and rectification": one non-autoregressive
+ *   pass of the target model over every node of a draft token tree, where a
+ *   node only sees the accepted prefix and its own branch (the masking table of
+ *   §3.2 "Tree decoder"), followed by the greedy acceptance of the longest
+ *   root path whose draft tokens equal the target's output (branch correct
+ *   sequences and the depth-first verified-sequence search of §3.2).
+ *
+ * The model is a LLaMA-style decoder (the paper names only embedding, masked
+ * self-attention, norm and linear layers, §2.1): RMSNorm, rotary positions
+ * (rotate-half pairing), multi-head attention, SwiGLU feed-forward, untied LM
+ * head, no biases.  Weights and the KV cache are bf16; matrix products
+ * accumulate in fp32; the residual stream and logits are fp32.
+ *
+ * Conventions shared by every entry point
+ *  - All device buffers are owned by the caller; the library never allocates,
+ *    frees or synchronises.  Work is enqueued on `stream` (a hipStream_t passed
+ *    as void*; NULL = the null stream) and results are valid once the caller
+ *    has synchronised that stream.
+ *  - Return value: LLMCAD_OK (0) or a negative status (see below).  Every
+ *    argument check happens on the host before anything is enqueued; on error
+ *    nothing is enqueued and no device buffer (in particular the KV cache) is
+ *    touched.  Device faults surface at the caller's synchronisation.
+ *  - Calls that share a workspace must not overlap (same stream serialises).
+ *
+ * Data layouts (row-major, bf16 = IEEE bfloat16 bit pattern)
+ *  - Plain weights, W[out][in]:
+ *      tok_embed [V][d], final_norm [d], lm_head [V][d]
+ *      per layer: attn_norm [d], w_qkv [3d][d] (rows q, then k, then v),
+ *                 w_o [d][d], ffn_norm [d],
+ *                 w_gate_up [2F][d] (rows gate, then up), w_down [d][F]
+ *  - Packed weights: an opaque device image of llmcad_packed_bytes() bytes
+ *    written by llmcad_pack_globals / llmcad_pack_layer (MFMA-fragment order,
+ *    4 KiB contiguous per 64 output columns x 32 inputs).  The globals sit
+ *    first, then layer 0, 1, ...; an image packed for L layers also serves a
+ *    configuration with fewer layers.
+ *  - KV cache: k_cache and v_cache are bf16 [L][H][capacity][Dh] each.  Slot p
+ *    holds position p of the accepted sequence for p < prefix_len.
+ */
+#ifndef LLMCAD_H
+#define LLMCAD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define LLMCAD_OK 0
+#define LLMCAD_EARG (-1)       /* NULL pointer, bad config value, bad layer index   */
+#define LLMCAD_ETREE (-2)      /* n < 1 or n > max, parent[0] != -1, parent[i] not
+                                  in [0, i), token outside [0, V)                    */
+#define LLMCAD_ECAPACITY (-3)  /* prefix_len < 0 or prefix_len + n > capacity       */
+#define LLMCAD_ESHAPE (-4)     /* unsupported shape (see llmcad_check_config)       */
+#define LLMCAD_EHIP (-5)       /* a HIP launch or runtime call failed               */
+#define LLMCAD_EWORKSPACE (-6) /* workspace or packed image smaller than required   */
+
+/* Largest tree (number of nodes) one verification pass accepts; also the
+ * largest chunk a prefill pass processes at once. */
+#define LLMCAD_MAX_NODES 128
+
+typedef struct llmcad_config {
+  int32_t n_layers;  /* L                                            */
+  int32_t d_model;   /* d = n_heads * head_dim, a multiple of 64     */
+  int32_t n_heads;   /* H (as many K/V heads as query heads)         */
+  int32_t head_dim;  /* Dh, 64 or 128                                */
+  int32_t d_ffn;     /* F (SwiGLU hidden width), any value >= 1      */
+  int32_t vocab;     /* V                                            */
+  float rms_eps;     /* RMSNorm epsilon                              */
+  float rope_theta;  /* rotary base: pair j rotates at theta^(-2j/Dh) */
+} llmcad_config;
+
+typedef struct llmcad_layer_weights {
+  const void* attn_norm; /* device bf16 [d]      */
+  const void* w_qkv;     /* device bf16 [3d][d]  */
+  const void* w_o;       /* device bf16 [d][d]   */
+  const void* ffn_norm;  /* device bf16 [d]      */
+  const void* w_gate_up; /* device bf16 [2F][d]  */
+  const void* w_down;    /* device bf16 [d][F]   */
+} llmcad_layer_weights;
+
+/* Checks a configuration: LLMCAD_OK, LLMCAD_EARG (non-positive sizes, bad
+ * eps/theta) or LLMCAD_ESHAPE (head_dim not 64/128, d != H*Dh, d % 64 != 0). */
+int llmcad_check_config(const llmcad_config* cfg);
+
+/* Bytes of the packed weight image for cfg (0 if cfg is invalid). */
+size_t llmcad_packed_bytes(const llmcad_config* cfg);
+
+/* Re-lays the model-wide tensors (embedding, final norm, LM head) from the
+ * plain layouts above into the packed image.  Source buffers may be freed
+ * once the stream has passed this call. */
+int llmcad_pack_globals(const llmcad_config* cfg, const void* tok_embed, const void* final_norm,
+                        const void* lm_head, void* packed, size_t packed_bytes, void* stream);
+
+/* Re-lays one layer's weights (layer in [0, L)) into the packed image. */
+int llmcad_pack_layer(const llmcad_config* cfg, int32_t layer, const llmcad_layer_weights* src,
+                      void* packed, size_t packed_bytes, void* stream);
+
+/* Bytes of workspace for passes of up to max_n nodes (max_n in [1, 128]). */
+size_t llmcad_workspace_bytes(const llmcad_config* cfg, int32_t max_n);
+
+/* Clears the workspace's synchronisation counters.  Call once after
+ * allocating a workspace (a zero-filled allocation needs no call); every pass
+ * leaves them cleared again. */
+int llmcad_workspace_init(const llmcad_config* cfg, int32_t max_n, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/*
+ * One verification pass over a token tree (§3.2).
+ *
+ * Tree (host arrays, read before the call returns): n nodes in topological
+ * order; tree_tokens[0] is the root, the last accepted token, which is not yet
+ * in the KV cache; parent[0] = -1 and 0 <= parent[i] < i.  Node i sits at
+ * position prefix_len + depth(i) and attends to cache slots [0, prefix_len)
+ * plus its ancestors and itself.
+ *
+ * Effects and outputs (device buffers):
+ *  - K/V of node i (every layer) are written to cache slot prefix_len + i; slots
+ *    [0, prefix_len) are only read.  Calling again with the same arguments gives
+ *    the same results.
+ *  - logits: fp32 [n][V], row i = the target's logits after node i's branch
+ *    (NULL: not stored).
+ *  - path: int32 [n]; path[0] = 0 and path[1..accept_len] are the accepted
+ *    draft nodes root-first; entries past accept_len are -1.
+ *  - accept_len: int32 [1], number of accepted draft nodes (root excluded):
+ *    the deepest node whose whole branch matches the target's greedy tokens
+ *    (lowest node index among equally deep ones; lowest vocabulary index among
+ *    equal logits).
+ *  - next_token: int32 [1], the target's greedy token after the last accepted
+ *    node (a rectification if that node has children, else a bonus token).
+ * Requires n <= the max_n the workspace was sized for.
+ */
+int llmcad_verify_tree(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                       int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens,
+                       const int32_t* parent, int32_t n, float* logits, int32_t* path,
+                       int32_t* accept_len, int32_t* next_token, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/*
+ * Prefill: runs tokens[0..n_tokens) (host array) as positions
+ * [start_pos, start_pos + n_tokens) against cache slots [0, start_pos),
+ * writing their K/V to slots [start_pos, start_pos + n_tokens).  Processed in
+ * chains of at most max_n tokens (the workspace's size).  last_logits (device
+ * fp32 [V], NULL = not needed) receives the logits after the last token.
+ */
+int llmcad_prefill(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                   int32_t capacity, const int32_t* tokens, int32_t n_tokens, int32_t start_pos,
+                   float* last_logits, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static text for a status code. */
+const char* llmcad_status_string(int status);
+
+/* Byte offset and size of a named intermediate buffer inside a workspace
+ * sized for max_n (for diagnostics): 0 residual stream fp32 [Mp][d],
+ * 1 rotated queries bf16 [Mp][d], 2 attention output bf16 [Mp][d],
+ * 3 SwiGLU product bf16 [Mp][Fp], 4 per-node greedy token int32 [Mp];
+ * Mp = max_n rounded up to 16, Fp = F rounded up to 32. */
+int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t which, size_t* offset,
+                            size_t* bytes);
+
+/* Kernel classes of a pass, for llmcad_timing_enable. */
+#define LLMCAD_KERNEL_QKV 0       /* RMSNorm + QKV projection + rotary + KV write */
+#define LLMCAD_KERNEL_ATTENTION 1 /* tree-masked attention                        */
+#define LLMCAD_KERNEL_O_PROJ 2    /* output projection + residual                 */
+#define LLMCAD_KERNEL_GATE_UP 3   /* RMSNorm + gate/up projection + SwiGLU        */
+#define LLMCAD_KERNEL_DOWN 4      /* down projection + residual                   */
+#define LLMCAD_KERNEL_LM_HEAD 5   /* final RMSNorm + LM head + argmax + walk      */
+#define LLMCAD_KERNEL_EMBED 6     /* tree preparation + embedding                 */
+
+/* Diagnostics (measurement only, process-wide, not thread-safe): after
+ * llmcad_timing_enable(c, m), the next m launches of kernel class c made by
+ * passes are each bracketed by a pair of HIP events on the pass's stream.
+ * kernel_class < 0 disables and releases the events.  llmcad_timing_read
+ * waits for the recorded events, returns the summed milliseconds and the
+ * number of bracketed launches, and makes the slots available again. */
+int llmcad_timing_enable(int32_t kernel_class, int32_t max_launches);
+int llmcad_timing_read(int32_t kernel_class, double* total_ms, int32_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LLMCAD_H */

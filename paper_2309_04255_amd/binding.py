@@ -1,0 +1,272 @@
+"""ctypes binding of libllmcad (the C ABI in include/llmcad.h).
+
+Argument marshalling only: every step of a pass runs in the library's HIP
+kernels.  Device buffers are torch tensors on a ROCm device (torch provides
+memory and streams); tree arrays are host int32 arrays.  Importing this module
+fails loudly if the library has not been built.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libllmcad.so")
+
+OK = 0
+EARG = -1
+ETREE = -2
+ECAPACITY = -3
+ESHAPE = -4
+EHIP = -5
+EWORKSPACE = -6
+MAX_NODES = 128
+
+SYMBOLS = (
+    "llmcad_check_config",
+    "llmcad_packed_bytes",
+    "llmcad_pack_globals",
+    "llmcad_pack_layer",
+    "llmcad_workspace_bytes",
+    "llmcad_workspace_init",
+    "llmcad_verify_tree",
+    "llmcad_prefill",
+    "llmcad_status_string",
+    "llmcad_workspace_region",
+    "llmcad_timing_enable",
+    "llmcad_timing_read",
+)
+
+KERNEL_QKV, KERNEL_ATTENTION, KERNEL_O_PROJ, KERNEL_GATE_UP, KERNEL_DOWN, KERNEL_LM_HEAD, \
+    KERNEL_EMBED = range(7)
+
+
+class LlmcadConfig(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32),
+        ("d_model", ctypes.c_int32),
+        ("n_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("d_ffn", ctypes.c_int32),
+        ("vocab", ctypes.c_int32),
+        ("rms_eps", ctypes.c_float),
+        ("rope_theta", ctypes.c_float),
+    ]
+
+
+class LlmcadLayerWeights(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in
+                ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")]
+
+
+class LlmcadError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(
+            f"{_LIB_PATH} is missing: build it with `python -m paper_2309_04255_amd.build` "
+            "(there is no fallback implementation)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    CFG = ctypes.POINTER(LlmcadConfig)
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    sig = {
+        "llmcad_check_config": (ctypes.c_int, [CFG]),
+        "llmcad_packed_bytes": (SZ, [CFG]),
+        "llmcad_pack_globals": (ctypes.c_int, [CFG, P, P, P, P, SZ, P]),
+        "llmcad_pack_layer": (ctypes.c_int, [CFG, I32, ctypes.POINTER(LlmcadLayerWeights), P, SZ, P]),
+        "llmcad_workspace_bytes": (SZ, [CFG, I32]),
+        "llmcad_workspace_init": (ctypes.c_int, [CFG, I32, P, SZ, P]),
+        "llmcad_verify_tree": (ctypes.c_int, [CFG, P, P, P, I32, I32, I32P, I32P, I32, P, P, P, P,
+                                              P, SZ, P]),
+        "llmcad_prefill": (ctypes.c_int, [CFG, P, P, P, I32, I32P, I32, I32, P, P, SZ, P]),
+        "llmcad_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "llmcad_workspace_region": (ctypes.c_int, [CFG, I32, I32, ctypes.POINTER(SZ),
+                                                   ctypes.POINTER(SZ)]),
+        "llmcad_timing_enable": (ctypes.c_int, [I32, I32]),
+        "llmcad_timing_read": (ctypes.c_int, [I32, ctypes.POINTER(ctypes.c_double), I32P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def lib():
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return _lib.llmcad_status_string(int(status)).decode()
+
+
+def make_config(shape) -> LlmcadConfig:
+    """From any object with n_layers, d_model, n_heads, head_dim, d_ffn, vocab, rms_eps, rope_theta."""
+    return LlmcadConfig(shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim, shape.d_ffn,
+                        shape.vocab, float(shape.rms_eps), float(shape.rope_theta))
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _i32(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _check(rc, what):
+    if rc != OK:
+        raise LlmcadError(rc, what)
+
+
+def check_config(cfg: LlmcadConfig) -> int:
+    return _lib.llmcad_check_config(ctypes.byref(cfg))
+
+
+def packed_bytes(cfg: LlmcadConfig) -> int:
+    return _lib.llmcad_packed_bytes(ctypes.byref(cfg))
+
+
+def workspace_bytes(cfg: LlmcadConfig, max_n: int) -> int:
+    return _lib.llmcad_workspace_bytes(ctypes.byref(cfg), int(max_n))
+
+
+def pack_globals(cfg, tok_embed, final_norm, lm_head, packed, stream=None):
+    _check(_lib.llmcad_pack_globals(ctypes.byref(cfg), _ptr(tok_embed), _ptr(final_norm),
+                                    _ptr(lm_head), _ptr(packed), packed.numel() * packed.element_size(),
+                                    _stream(stream)), "llmcad_pack_globals")
+
+
+def pack_layer(cfg, layer: int, w: dict, packed, stream=None):
+    src = LlmcadLayerWeights(*(w[k].data_ptr() for k in
+                               ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")))
+    _check(_lib.llmcad_pack_layer(ctypes.byref(cfg), int(layer), ctypes.byref(src), _ptr(packed),
+                                  packed.numel() * packed.element_size(), _stream(stream)),
+           "llmcad_pack_layer")
+
+
+def workspace_init(cfg, max_n: int, workspace, stream=None):
+    _check(_lib.llmcad_workspace_init(ctypes.byref(cfg), int(max_n), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), _stream(stream)),
+           "llmcad_workspace_init")
+
+
+def verify_tree(cfg, packed, k_cache, v_cache, prefix_len: int, tree_tokens, parent, logits, path,
+                accept_len, next_token, workspace, stream=None, raise_on_error=True) -> int:
+    """Enqueue one verification pass; returns the status (raises on error by default)."""
+    tok, tok_p = _i32(tree_tokens)
+    par, par_p = _i32(parent)
+    n = len(tok)
+    if len(par) != n:
+        raise ValueError("tree_tokens and parent differ in length")
+    cap = k_cache.shape[-2]
+    rc = _lib.llmcad_verify_tree(
+        ctypes.byref(cfg), _ptr(packed), _ptr(k_cache), _ptr(v_cache), int(cap), int(prefix_len),
+        tok_p, par_p, int(n), _ptr(logits), _ptr(path), _ptr(accept_len), _ptr(next_token),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+    if raise_on_error:
+        _check(rc, "llmcad_verify_tree")
+    return rc
+
+
+def prefill(cfg, packed, k_cache, v_cache, tokens, start_pos: int, last_logits, workspace,
+            stream=None, raise_on_error=True) -> int:
+    tok, tok_p = _i32(tokens)
+    cap = k_cache.shape[-2]
+    rc = _lib.llmcad_prefill(
+        ctypes.byref(cfg), _ptr(packed), _ptr(k_cache), _ptr(v_cache), int(cap), tok_p, int(len(tok)),
+        int(start_pos), _ptr(last_logits), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream))
+    if raise_on_error:
+        _check(rc, "llmcad_prefill")
+    return rc
+
+
+def workspace_region(cfg, n: int, which: int):
+    off, size = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(_lib.llmcad_workspace_region(ctypes.byref(cfg), int(n), int(which), ctypes.byref(off),
+                                        ctypes.byref(size)), "llmcad_workspace_region")
+    return off.value, size.value
+
+
+def timing_enable(kernel_class: int, max_launches: int):
+    _check(_lib.llmcad_timing_enable(int(kernel_class), int(max_launches)), "llmcad_timing_enable")
+
+
+def timing_read(kernel_class: int):
+    """(summed milliseconds, launches) of the bracketed launches since the last read."""
+    ms, n = ctypes.c_double(), ctypes.c_int32()
+    _check(_lib.llmcad_timing_read(int(kernel_class), ctypes.byref(ms), ctypes.byref(n)),
+           "llmcad_timing_read")
+    return ms.value, n.value
+
+
+class Session:
+    """Owns the device buffers of one target model: packed weights, KV cache,
+    workspace and output buffers (all torch tensors), and forwards calls."""
+
+    def __init__(self, shape, capacity: int, max_n: int = MAX_NODES, device="cuda"):
+        self.cfg = make_config(shape)
+        rc = check_config(self.cfg)
+        if rc != OK:
+            raise LlmcadError(rc, "config")
+        self.shape = shape
+        self.device = torch.device(device)
+        self.max_n = int(max_n)
+        self.capacity = int(capacity)
+        L, H, Dh = shape.n_layers, shape.n_heads, shape.head_dim
+        self.packed = torch.empty(packed_bytes(self.cfg), dtype=torch.uint8, device=self.device)
+        self.k_cache = torch.zeros((L, H, capacity, Dh), dtype=torch.bfloat16, device=self.device)
+        self.v_cache = torch.zeros((L, H, capacity, Dh), dtype=torch.bfloat16, device=self.device)
+        self.workspace = torch.zeros(workspace_bytes(self.cfg, self.max_n), dtype=torch.uint8,
+                                     device=self.device)
+        self.logits = torch.empty((self.max_n, shape.vocab), dtype=torch.float32, device=self.device)
+        self.path = torch.empty(self.max_n, dtype=torch.int32, device=self.device)
+        self.accept_len = torch.empty(1, dtype=torch.int32, device=self.device)
+        self.next_token = torch.empty(1, dtype=torch.int32, device=self.device)
+        self.last_logits = torch.empty(shape.vocab, dtype=torch.float32, device=self.device)
+
+    def load_weights(self, gen, layers=None):
+        """Pack weights from a generator with tok_embed(), final_norm(), lm_head(), layer(l)
+        returning plain-layout bf16 tensors on this device."""
+        pack_globals(self.cfg, gen.tok_embed(), gen.final_norm(), gen.lm_head(), self.packed)
+        for l in range(self.shape.n_layers) if layers is None else layers:
+            pack_layer(self.cfg, l, gen.layer(l), self.packed)
+            torch.cuda.current_stream().synchronize()  # let the plain layer be freed
+
+    def prefill(self, tokens, start_pos=0, want_logits=False):
+        prefill(self.cfg, self.packed, self.k_cache, self.v_cache, tokens, start_pos,
+                self.last_logits if want_logits else None, self.workspace)
+        return self.last_logits if want_logits else None
+
+    def verify_tree(self, prefix_len, tree_tokens, parent, want_logits=True):
+        n = len(tree_tokens)
+        verify_tree(self.cfg, self.packed, self.k_cache, self.v_cache, prefix_len, tree_tokens,
+                    parent, self.logits if want_logits else None, self.path, self.accept_len,
+                    self.next_token, self.workspace)
+        return n
+
+    def results(self, n):
+        """Synchronise and return (logits [n, V] fp32 cpu, path list, accept_len, next_token)."""
+        torch.cuda.current_stream().synchronize()
+        acc = int(self.accept_len.item())
+        return (self.logits[:n].cpu(), [int(x) for x in self.path[: acc + 1].cpu()], acc,
+                int(self.next_token.item()))

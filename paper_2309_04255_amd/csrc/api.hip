@@ -1,0 +1,511 @@
+// Host side of the C ABI: argument checks, packing, launch sequencing.
+//
+// A verification pass (§3.2, "Batched non-autoregressive verification" and
+// "Depth-first verified sequence searching") is enqueued as
+//   embed+tree prep, then per layer: QKV GEMM (RMSNorm prologue, rotary +
+//   KV-write epilogue) -> tree attention -> O GEMM (+residual) -> gate/up GEMM
+//   (RMSNorm prologue, SwiGLU epilogue) -> down GEMM (+residual),
+//   then the LM-head GEMM (final RMSNorm prologue, argmax epilogue) whose last
+//   workgroup performs the accept walk.
+// Prefill runs the same sequence on chains of tokens (a chain's ancestor mask
+// is the causal mask and its depth is its offset).
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "kernels.h"
+#include "layout.h"
+#include "llmcad.h"
+
+using namespace llmcad;
+
+namespace {
+
+int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  if (v == nullptr || *v == 0) return dflt;
+  int x = atoi(v);
+  return x > 0 ? x : dflt;
+}
+
+// Workgroup-count targets for the GEMM split-K and the attention position
+// splits (read once per pass; the environment variables tune launch shapes).
+struct LaunchTargets {
+  int gemm_wgs, attn_wgs;
+  LaunchTargets()
+      : gemm_wgs(env_int("LLMCAD_GEMM_WGS", 1024)), attn_wgs(env_int("LLMCAD_ATTN_WGS", 512)) {}
+};
+
+int choose_ksplit(const LaunchTargets& lt, int tiles, int ksteps) {
+  int ks = cdiv(lt.gemm_wgs, tiles);
+  int max_split = ksteps / 8;
+  if (max_split < 1) max_split = 1;
+  if (ks > max_split) ks = max_split;
+  if (ks < 1) ks = 1;
+  while (ks > 1 && tiles * ks > kGemmMaxWgs) --ks;
+  return ks;
+}
+
+int check_cfg(const llmcad_config* c) {
+  if (c == nullptr) return LLMCAD_EARG;
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->head_dim < 1 || c->d_ffn < 1 ||
+      c->vocab < 1)
+    return LLMCAD_EARG;
+  if (!(c->rms_eps > 0.0f) || !(c->rope_theta > 1.0f)) return LLMCAD_EARG;
+  if (c->head_dim != 64 && c->head_dim != 128) return LLMCAD_ESHAPE;
+  if ((long)c->n_heads * c->head_dim != c->d_model) return LLMCAD_ESHAPE;
+  if (c->d_model % 64 != 0) return LLMCAD_ESHAPE;
+  if (c->n_layers > 4096 || c->d_model > 65536 || c->d_ffn > (1 << 20) || c->vocab > (1 << 24))
+    return LLMCAD_ESHAPE;
+  return LLMCAD_OK;
+}
+
+hipError_t g_last_error = hipSuccess;
+
+// Diagnostics: optional HIP event pairs around every launch of one kernel
+// class (see llmcad_timing_enable).  Not used unless enabled.
+struct Timing {
+  int kclass = -1;
+  int capacity = 0;
+  int used = 0;
+  hipEvent_t* ev = nullptr;  // [capacity][2]
+} g_timing;
+
+struct TimedLaunch {
+  bool on;
+  hipStream_t st;
+  int slot;
+  TimedLaunch(int kclass, hipStream_t s) : on(false), st(s), slot(-1) {
+    if (g_timing.kclass == kclass && g_timing.used < g_timing.capacity) {
+      on = true;
+      slot = g_timing.used++;
+      (void)hipEventRecord(g_timing.ev[2 * slot], st);
+    }
+  }
+  ~TimedLaunch() {
+    if (on) (void)hipEventRecord(g_timing.ev[2 * slot + 1], st);
+  }
+};
+
+#define HIP_TRY(expr)                 \
+  do {                                \
+    hipError_t e_ = (expr);           \
+    if (e_ != hipSuccess) {           \
+      g_last_error = e_;              \
+      return LLMCAD_EHIP;             \
+    }                                 \
+  } while (0)
+
+struct Pass {
+  const llmcad_config* cfg;
+  const char* packed;
+  char* k_cache;
+  char* v_cache;
+  int cap;
+  int prefix_len;
+  int n;
+  float* logits;
+  int row_lo;
+  int* path;
+  int* accept_len;
+  int* next_token;
+  char* ws;
+  hipStream_t st;
+};
+
+int run_pass(const Pass& a, const TreeArgs& tree) {
+  const Shape s(*a.cfg);
+  const PackedLayout P(s);
+  const WorkspaceLayout W(s, a.n);
+  const int Mp = W.Mp, MB = Mp / 16;
+  char* ws = a.ws;
+  float* x = (float*)(ws + W.x);
+  float* ssq = (float*)(ws + W.ssq);
+  int* wtree = (int*)(ws + W.tree);
+  int* gemm_counters = (int*)(ws + W.counters);
+  int* attn_counters = gemm_counters + W.n_gemm_counters;
+  int* lm_counter = attn_counters + W.n_attn_counters;
+  const float eps = a.cfg->rms_eps;
+  const float log2_theta = (float)log2((double)a.cfg->rope_theta);
+  const LaunchTargets lt;
+
+  {
+    TimedLaunch tl(LLMCAD_KERNEL_EMBED, a.st);
+    HIP_TRY(launch_embed(tree, a.n, Mp, s.d, a.prefix_len, a.packed + P.embed, wtree, x, ssq, a.st));
+  }
+
+  const int total = a.prefix_len + a.n;
+  const int nchunks = cdiv(total, kAttnChunk);
+  int splits = cdiv(lt.attn_wgs, s.H);
+  if (splits > attn_max_splits(s.H)) splits = attn_max_splits(s.H);
+  if (splits > nchunks) splits = nchunks;
+  if (splits < 1) splits = 1;
+
+  GemmParams base;
+  memset(&base, 0, sizeof(base));
+  base.n = a.n;
+  base.Mp = Mp;
+  base.part = (float*)(ws + W.gemm_part);
+  base.counters = gemm_counters;
+  base.x = x;
+  base.ssq = ssq;
+  base.ssq_tiles = s.d_tiles;
+  base.eps = eps;
+  base.inv_d = 1.0f / (float)s.d;
+  base.d = s.d;
+
+  const size_t kv_layer = (size_t)s.H * a.cap * s.Dh * 2;
+  for (int l = 0; l < s.L; ++l) {
+    const char* lw = a.packed + P.layer(l);
+    char* kc = a.k_cache + (size_t)l * kv_layer;
+    char* vc = a.v_cache + (size_t)l * kv_layer;
+
+    GemmParams g = base;  // QKV
+    g.w = lw + P.w_qkv;
+    g.ksteps = s.ks_d;
+    g.tiles = s.qkv_tiles;
+    g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
+    g.gain = lw + P.attn_norm;
+    g.q_out = ws + W.q;
+    g.k_cache = kc;
+    g.v_cache = vc;
+    g.cap = a.cap;
+    g.prefix_len = a.prefix_len;
+    g.H = s.H;
+    g.Dh = s.Dh;
+    g.pos = wtree + 384;
+    g.log2_theta = log2_theta;
+    {
+      TimedLaunch tl(LLMCAD_KERNEL_QKV, a.st);
+      HIP_TRY(launch_gemm(PRO_NORM, EPI_QKV, MB, g, a.st));
+    }
+
+    AttnParams at;
+    at.q = ws + W.q;
+    at.k_cache = kc;
+    at.v_cache = vc;
+    at.o_out = ws + W.o;
+    at.part_o = (float*)(ws + W.attn_o);
+    at.part_ml = (float*)(ws + W.attn_ml);
+    at.counters = attn_counters;
+    at.anc = (const uint32_t*)(wtree + 512);
+    at.n = a.n;
+    at.Mp = Mp;
+    at.H = s.H;
+    at.Dh = s.Dh;
+    at.cap = a.cap;
+    at.prefix_len = a.prefix_len;
+    at.splits = splits;
+    at.nchunks = nchunks;
+    at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.Dh));
+    {
+      TimedLaunch tl(LLMCAD_KERNEL_ATTENTION, a.st);
+      HIP_TRY(launch_attention(MB, at, a.st));
+    }
+
+    g = base;  // O projection + residual
+    g.w = lw + P.w_o;
+    g.ksteps = s.ks_d;
+    g.tiles = s.d_tiles;
+    g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
+    g.a = ws + W.o;
+    g.lda = s.d;
+    g.x_out = x;
+    g.ssq_out = ssq;
+    {
+      TimedLaunch tl(LLMCAD_KERNEL_O_PROJ, a.st);
+      HIP_TRY(launch_gemm(PRO_BF16, EPI_RESID, MB, g, a.st));
+    }
+
+    g = base;  // gate/up + SwiGLU
+    g.w = lw + P.w_gate_up;
+    g.ksteps = s.ks_d;
+    g.tiles = s.gu_tiles;
+    g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
+    g.gain = lw + P.ffn_norm;
+    g.h_out = ws + W.h;
+    g.ldh = s.Fp;
+    {
+      TimedLaunch tl(LLMCAD_KERNEL_GATE_UP, a.st);
+      HIP_TRY(launch_gemm(PRO_NORM, EPI_SWIGLU, MB, g, a.st));
+    }
+
+    g = base;  // down projection + residual
+    g.w = lw + P.w_down;
+    g.ksteps = s.ks_f;
+    g.tiles = s.d_tiles;
+    g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
+    g.a = ws + W.h;
+    g.lda = s.Fp;
+    g.x_out = x;
+    g.ssq_out = ssq;
+    {
+      TimedLaunch tl(LLMCAD_KERNEL_DOWN, a.st);
+      HIP_TRY(launch_gemm(PRO_BF16, EPI_RESID, MB, g, a.st));
+    }
+  }
+
+  GemmParams g = base;  // final norm + LM head + argmax + accept walk
+  g.w = a.packed + P.lm_head;
+  g.ksteps = s.ks_d;
+  g.tiles = s.v_tiles;
+  g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
+  g.gain = a.packed + P.final_norm;
+  g.logits = a.logits;
+  g.V = s.V;
+  g.row_lo = a.row_lo;
+  g.lm_val = (float*)(ws + W.lm_val);
+  g.lm_idx = (int*)(ws + W.lm_idx);
+  g.lm_counter = lm_counter;
+  g.amax = (int*)(ws + W.amax);
+  g.tree_tok = wtree;
+  g.tree_parent = wtree + 128;
+  g.tree_depth = wtree + 256;
+  g.path = a.path;
+  g.accept_len = a.accept_len;
+  g.next_token = a.next_token;
+  {
+    TimedLaunch tl(LLMCAD_KERNEL_LM_HEAD, a.st);
+    HIP_TRY(launch_gemm(PRO_NORM, EPI_LOGITS, MB, g, a.st));
+  }
+  return LLMCAD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int llmcad_check_config(const llmcad_config* cfg) { return check_cfg(cfg); }
+
+size_t llmcad_packed_bytes(const llmcad_config* cfg) {
+  if (check_cfg(cfg) != LLMCAD_OK) return 0;
+  return PackedLayout(Shape(*cfg)).total;
+}
+
+int llmcad_pack_globals(const llmcad_config* cfg, const void* tok_embed, const void* final_norm,
+                        const void* lm_head, void* packed, size_t packed_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!tok_embed || !final_norm || !lm_head || !packed) return LLMCAD_EARG;
+  const Shape s(*cfg);
+  const PackedLayout P(s);
+  if (packed_bytes < P.total) return LLMCAD_EWORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  char* out = (char*)packed;
+  HIP_TRY(hipMemcpyAsync(out + P.embed, tok_embed, (size_t)s.V * s.d * 2, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(out + P.final_norm, final_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(launch_pack(lm_head, s.V, s.d, out + P.lm_head, s.v_tiles, s.ks_d, PACK_PLAIN, s.H, s.Dh,
+                      s.F, st));
+  return LLMCAD_OK;
+}
+
+int llmcad_pack_layer(const llmcad_config* cfg, int32_t layer, const llmcad_layer_weights* src,
+                      void* packed, size_t packed_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!src || !packed || layer < 0 || layer >= cfg->n_layers) return LLMCAD_EARG;
+  if (!src->attn_norm || !src->w_qkv || !src->w_o || !src->ffn_norm || !src->w_gate_up ||
+      !src->w_down)
+    return LLMCAD_EARG;
+  const Shape s(*cfg);
+  const PackedLayout P(s);
+  if (packed_bytes < P.total) return LLMCAD_EWORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  char* out = (char*)packed + P.layer(layer);
+  HIP_TRY(hipMemcpyAsync(out + P.attn_norm, src->attn_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(out + P.ffn_norm, src->ffn_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(launch_pack(src->w_qkv, 3 * s.d, s.d, out + P.w_qkv, s.qkv_tiles, s.ks_d, PACK_QKV_ROPE,
+                      s.H, s.Dh, s.F, st));
+  HIP_TRY(launch_pack(src->w_o, s.d, s.d, out + P.w_o, s.d_tiles, s.ks_d, PACK_PLAIN, s.H, s.Dh,
+                      s.F, st));
+  HIP_TRY(launch_pack(src->w_gate_up, 2 * s.F, s.d, out + P.w_gate_up, s.gu_tiles, s.ks_d,
+                      PACK_GATE_UP, s.H, s.Dh, s.F, st));
+  HIP_TRY(launch_pack(src->w_down, s.d, s.F, out + P.w_down, s.d_tiles, s.ks_f, PACK_PLAIN, s.H,
+                      s.Dh, s.F, st));
+  return LLMCAD_OK;
+}
+
+size_t llmcad_workspace_bytes(const llmcad_config* cfg, int32_t max_n) {
+  if (check_cfg(cfg) != LLMCAD_OK || max_n < 1 || max_n > kMaxNodes) return 0;
+  return WorkspaceLayout(Shape(*cfg), max_n).total;
+}
+
+int llmcad_workspace_init(const llmcad_config* cfg, int32_t max_n, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!workspace || max_n < 1 || max_n > kMaxNodes) return LLMCAD_EARG;
+  const WorkspaceLayout W(Shape(*cfg), max_n);
+  if (workspace_bytes < W.total) return LLMCAD_EWORKSPACE;
+  HIP_TRY(hipMemsetAsync((char*)workspace + W.counters, 0, W.counters_bytes, (hipStream_t)stream));
+  return LLMCAD_OK;
+}
+
+int llmcad_verify_tree(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                       int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens,
+                       const int32_t* parent, int32_t n, float* logits, int32_t* path,
+                       int32_t* accept_len, int32_t* next_token, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!packed || !k_cache || !v_cache || !tree_tokens || !parent || !path || !accept_len ||
+      !next_token || !workspace)
+    return LLMCAD_EARG;
+  if (n < 1 || n > kMaxNodes) return LLMCAD_ETREE;
+  if (parent[0] != -1) return LLMCAD_ETREE;
+  for (int i = 0; i < n; ++i) {
+    if (tree_tokens[i] < 0 || tree_tokens[i] >= cfg->vocab) return LLMCAD_ETREE;
+    if (i > 0 && (parent[i] < 0 || parent[i] >= i)) return LLMCAD_ETREE;
+  }
+  if (capacity < 1 || prefix_len < 0 || (long)prefix_len + n > capacity) return LLMCAD_ECAPACITY;
+  const Shape s(*cfg);
+  if (workspace_bytes < WorkspaceLayout(s, n).total) return LLMCAD_EWORKSPACE;
+  TreeArgs tree;
+  memset(&tree, 0, sizeof(tree));
+  for (int i = 0; i < n; ++i) {
+    tree.tok[i] = tree_tokens[i];
+    tree.parent[i] = parent[i];
+  }
+  Pass a;
+  a.cfg = cfg;
+  a.packed = (const char*)packed;
+  a.k_cache = (char*)k_cache;
+  a.v_cache = (char*)v_cache;
+  a.cap = capacity;
+  a.prefix_len = prefix_len;
+  a.n = n;
+  a.logits = logits;
+  a.row_lo = 0;
+  a.path = path;
+  a.accept_len = accept_len;
+  a.next_token = next_token;
+  a.ws = (char*)workspace;
+  a.st = (hipStream_t)stream;
+  return run_pass(a, tree);
+}
+
+int llmcad_prefill(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                   int32_t capacity, const int32_t* tokens, int32_t n_tokens, int32_t start_pos,
+                   float* last_logits, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!packed || !k_cache || !v_cache || !tokens || !workspace) return LLMCAD_EARG;
+  if (n_tokens < 1) return LLMCAD_ETREE;
+  for (int i = 0; i < n_tokens; ++i)
+    if (tokens[i] < 0 || tokens[i] >= cfg->vocab) return LLMCAD_ETREE;
+  if (capacity < 1 || start_pos < 0 || (long)start_pos + n_tokens > capacity) return LLMCAD_ECAPACITY;
+  const Shape s(*cfg);
+  // Largest chain the workspace holds.
+  int chunk = 0;
+  for (int m = kMaxNodes; m >= 1; --m)
+    if (WorkspaceLayout(s, m).total <= workspace_bytes) {
+      chunk = m;
+      break;
+    }
+  if (chunk == 0) return LLMCAD_EWORKSPACE;
+  const WorkspaceLayout W(s, 1);
+  int* sink = (int*)((char*)workspace + W.scratch_out);  // path/len/next are not needed
+  for (int off = 0; off < n_tokens; off += chunk) {
+    const int len = (n_tokens - off) < chunk ? (n_tokens - off) : chunk;
+    TreeArgs tree;
+    memset(&tree, 0, sizeof(tree));
+    for (int i = 0; i < len; ++i) {
+      tree.tok[i] = tokens[off + i];
+      tree.parent[i] = i - 1;
+    }
+    const bool last = off + len == n_tokens;
+    Pass a;
+    a.cfg = cfg;
+    a.packed = (const char*)packed;
+    a.k_cache = (char*)k_cache;
+    a.v_cache = (char*)v_cache;
+    a.cap = capacity;
+    a.prefix_len = start_pos + off;
+    a.n = len;
+    a.logits = last ? last_logits : nullptr;
+    a.row_lo = len - 1;
+    a.path = sink;
+    a.accept_len = sink + 128;
+    a.next_token = sink + 129;
+    a.ws = (char*)workspace;
+    a.st = (hipStream_t)stream;
+    rc = run_pass(a, tree);
+    if (rc != LLMCAD_OK) return rc;
+  }
+  return LLMCAD_OK;
+}
+
+int llmcad_timing_enable(int32_t kernel_class, int32_t max_launches) {
+  if (g_timing.ev != nullptr) {
+    for (int i = 0; i < 2 * g_timing.capacity; ++i) (void)hipEventDestroy(g_timing.ev[i]);
+    free(g_timing.ev);
+    g_timing = Timing();
+  }
+  if (kernel_class < 0) return LLMCAD_OK;
+  if (kernel_class > LLMCAD_KERNEL_EMBED || max_launches < 1) return LLMCAD_EARG;
+  g_timing.ev = (hipEvent_t*)calloc((size_t)2 * max_launches, sizeof(hipEvent_t));
+  if (g_timing.ev == nullptr) return LLMCAD_EARG;
+  for (int i = 0; i < 2 * max_launches; ++i) {
+    hipError_t e = hipEventCreate(&g_timing.ev[i]);
+    if (e != hipSuccess) {
+      g_last_error = e;
+      g_timing.capacity = i / 2;
+      return LLMCAD_EHIP;
+    }
+  }
+  g_timing.capacity = max_launches;
+  g_timing.kclass = kernel_class;
+  return LLMCAD_OK;
+}
+
+int llmcad_timing_read(int32_t kernel_class, double* total_ms, int32_t* launches) {
+  if (!total_ms || !launches) return LLMCAD_EARG;
+  *total_ms = 0.0;
+  *launches = 0;
+  if (kernel_class != g_timing.kclass) return LLMCAD_OK;
+  double sum = 0.0;
+  for (int i = 0; i < g_timing.used; ++i) {
+    HIP_TRY(hipEventSynchronize(g_timing.ev[2 * i + 1]));
+    float ms = 0.0f;
+    HIP_TRY(hipEventElapsedTime(&ms, g_timing.ev[2 * i], g_timing.ev[2 * i + 1]));
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = g_timing.used;
+  g_timing.used = 0;
+  return LLMCAD_OK;
+}
+
+const char* llmcad_status_string(int status) {
+  switch (status) {
+    case LLMCAD_OK: return "ok";
+    case LLMCAD_EARG: return "invalid argument";
+    case LLMCAD_ETREE: return "invalid token tree";
+    case LLMCAD_ECAPACITY: return "KV cache capacity exceeded";
+    case LLMCAD_ESHAPE: return "unsupported model shape";
+    case LLMCAD_EHIP: return hipGetErrorString(g_last_error);
+    case LLMCAD_EWORKSPACE: return "workspace or packed image too small";
+    default: return "unknown status";
+  }
+}
+
+int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t which, size_t* offset,
+                            size_t* bytes) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!offset || !bytes || max_n < 1 || max_n > kMaxNodes) return LLMCAD_EARG;
+  const Shape s(*cfg);
+  const WorkspaceLayout W(s, max_n);
+  switch (which) {
+    case 0: *offset = W.x; *bytes = (size_t)W.Mp * s.d * 4; break;
+    case 1: *offset = W.q; *bytes = (size_t)W.Mp * s.d * 2; break;
+    case 2: *offset = W.o; *bytes = (size_t)W.Mp * s.d * 2; break;
+    case 3: *offset = W.h; *bytes = (size_t)W.Mp * s.Fp * 2; break;
+    case 4: *offset = W.amax; *bytes = (size_t)W.Mp * 4; break;
+    default: return LLMCAD_EARG;
+  }
+  return LLMCAD_OK;
+}
+
+}  // extern "C"

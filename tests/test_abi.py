@@ -1,0 +1,114 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, sizes
+its buffers, and rejects bad arguments on the host before touching a device."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "llmcad.h")
+
+
+@pytest.fixture(scope="module")
+def binding():
+    from paper_2309_04255_amd import binding
+
+    return binding
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(llmcad_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol(binding):
+    names = declared_functions()
+    assert len(names) >= 10
+    lib = binding.lib()
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(binding.SYMBOLS) == set(names)
+
+
+def test_config_checks(binding):
+    ok = binding.make_config(workloads.MODELS["llama7b"])
+    assert binding.check_config(ok) == binding.OK
+    bad = binding.make_config(workloads.MODELS["llama7b"])
+    bad.head_dim = 96
+    assert binding.check_config(bad) == binding.ESHAPE
+    bad = binding.make_config(workloads.MODELS["llama7b"])
+    bad.n_heads = 31
+    assert binding.check_config(bad) == binding.ESHAPE
+    bad = binding.make_config(workloads.MODELS["llama7b"])
+    bad.vocab = 0
+    assert binding.check_config(bad) == binding.EARG
+    assert binding.packed_bytes(bad) == 0
+    assert binding.lib().llmcad_check_config(None) == binding.EARG
+
+
+def test_sizes(binding):
+    s = workloads.MODELS["llama7b"]
+    cfg = binding.make_config(s)
+    weight_bytes = 2 * (s.n_layers * (4 * s.d_model ** 2 + 3 * s.d_model * s.d_ffn + 2 * s.d_model)
+                        + 2 * s.vocab * s.d_model + s.d_model)
+    pb = binding.packed_bytes(cfg)
+    assert weight_bytes <= pb <= weight_bytes * 1.001
+    assert binding.workspace_bytes(cfg, 31) < binding.workspace_bytes(cfg, 128)
+    assert binding.workspace_bytes(cfg, 0) == 0 and binding.workspace_bytes(cfg, 129) == 0
+    off, size = binding.workspace_region(cfg, 31, 0)
+    assert size == 32 * s.d_model * 4 and off + size <= binding.workspace_bytes(cfg, 31)
+
+
+def _call_verify(binding, cfg, tok, par, prefix_len=10, cap=64, ws_bytes=1 << 30, packed=16):
+    lib = binding.lib()
+    tok = np.ascontiguousarray(tok, dtype=np.int32)
+    par = np.ascontiguousarray(par, dtype=np.int32)
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    fake = ctypes.c_void_p(256)  # never dereferenced: every case below fails a host check
+    return lib.llmcad_verify_tree(
+        ctypes.byref(cfg), ctypes.c_void_p(packed) if packed else None, fake, fake, cap, prefix_len,
+        tok.ctypes.data_as(I32P), par.ctypes.data_as(I32P), len(tok), fake, fake, fake, fake, fake,
+        ws_bytes, None)
+
+
+def test_host_validation(binding):
+    cfg = binding.make_config(workloads.MODELS["tiny"])
+    V = cfg.vocab
+    assert _call_verify(binding, cfg, [1, 2], [0, 0]) == binding.ETREE
+    assert _call_verify(binding, cfg, [1, 2, 3], [-1, 0, 2]) == binding.ETREE
+    assert _call_verify(binding, cfg, [1, 2, 3], [-1, 0, -1]) == binding.ETREE
+    assert _call_verify(binding, cfg, [1, V], [-1, 0]) == binding.ETREE
+    assert _call_verify(binding, cfg, [-1, 3], [-1, 0]) == binding.ETREE
+    assert _call_verify(binding, cfg, np.zeros(129), np.arange(-1, 128)) == binding.ETREE
+    assert _call_verify(binding, cfg, [1, 2], [-1, 0], prefix_len=63, cap=64) == binding.ECAPACITY
+    assert _call_verify(binding, cfg, [1, 2], [-1, 0], prefix_len=-1) == binding.ECAPACITY
+    assert _call_verify(binding, cfg, [1, 2], [-1, 0], ws_bytes=1000) == binding.EWORKSPACE
+    assert _call_verify(binding, cfg, [1, 2], [-1, 0], packed=0) == binding.EARG
+    bad = binding.make_config(workloads.MODELS["tiny"])
+    bad.head_dim = 32
+    bad.n_heads = 8
+    assert _call_verify(binding, bad, [1, 2], [-1, 0]) == binding.ESHAPE
+    assert binding.status_string(binding.ETREE) == "invalid token tree"
+
+
+def test_prefill_validation(binding):
+    cfg = binding.make_config(workloads.MODELS["tiny"])
+    lib = binding.lib()
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    fake = ctypes.c_void_p(256)
+    toks = np.array([1, 2, cfg.vocab], dtype=np.int32)
+    rc = lib.llmcad_prefill(ctypes.byref(cfg), fake, fake, fake, 64, toks.ctypes.data_as(I32P), 3, 0,
+                            None, fake, 1 << 30, None)
+    assert rc == binding.ETREE
+    toks = np.array([1, 2, 3], dtype=np.int32)
+    rc = lib.llmcad_prefill(ctypes.byref(cfg), fake, fake, fake, 64, toks.ctypes.data_as(I32P), 3, 62,
+                            None, fake, 1 << 30, None)
+    assert rc == binding.ECAPACITY
+    rc = lib.llmcad_prefill(ctypes.byref(cfg), fake, fake, fake, 64, toks.ctypes.data_as(I32P), 3, 0,
+                            None, fake, 100, None)
+    assert rc == binding.EWORKSPACE

@@ -1,0 +1,219 @@
+"""GPU parity of the HIP verification pass against the oracle (through the C ABI).
+
+Models: the tiny 2-layer shape (head_dim 64, F = 688 not a multiple of 32) and a
+small head_dim-128 shape with ragged F and V (V = 2000 leaves a partial
+64-column tile).  Norm gains are jittered so that the gain path is exercised.
+Trees span one to eight 16-row blocks with ragged tails (n = 1 ... 128), and
+the prefix (100) is not a multiple of the 64-position attention chunk.
+"""
+
+import os
+import types
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from tests import parity
+from tests.util import oracle_weights
+
+pytestmark = pytest.mark.gpu
+
+P = 100
+SHAPES = {
+    "tiny": workloads.MODELS["tiny"],
+    "small128": workloads.ModelShape("small128", 2, 512, 4, 128, 1000, 2000, seed=0x5EED0128),
+}
+TREES = {
+    "single": workloads.chain_tree(1),
+    "binary_d3_n15": workloads.complete_tree((2, 2, 2)),
+    "random_n20": workloads.random_tree(20, 7, 5),
+    "chain_n9": workloads.chain_tree(9),
+    "binary_d4_n31": workloads.complete_tree((2, 2, 2, 2)),
+    "b432_n41": workloads.complete_tree((4, 3, 2)),
+    "random_n77": workloads.random_tree(77, 7, 8),
+    "random_n128": workloads.random_tree(128, 7, 9),
+}
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2309_04255_amd import binding
+
+    return binding
+
+
+@pytest.fixture(scope="module", params=sorted(SHAPES))
+def model(request):
+    binding = _gpu()
+    shape = SHAPES[request.param]
+    print(f"\n[model] {shape.name}", flush=True)
+    gen = workloads.make_weights(shape, "cuda", gain_jitter=0.1)
+    sess = binding.Session(shape, capacity=P + 200, max_n=128)
+    binding.workspace_init(sess.cfg, 128, sess.workspace)
+    sess.load_weights(gen)
+    ow = oracle_weights(shape, gain_jitter=0.1)
+    prefix = workloads.draw_tokens(P, shape.vocab, seed=3)
+    ok, ov = oracle.prefill_kv(ow, prefix, rounding=True)
+    sess.prefill(prefix, 0)
+    torch.cuda.synchronize()
+    return types.SimpleNamespace(shape=shape, sess=sess, ow=ow, prefix=prefix, ok=ok, ov=ov,
+                                 binding=binding, gen=gen)
+
+
+def _gpu_amax(m, n):
+    off, size = m.binding.workspace_region(m.sess.cfg, n, 4)
+    return m.sess.workspace[off:off + 4 * n].view(torch.int32).cpu().numpy()
+
+
+def _run(m, parent, tok):
+    n = len(parent)
+    m.sess.verify_tree(P, tok, parent)
+    logits, path, acc, nxt = m.sess.results(n)
+    return logits.numpy(), path, acc, nxt, _gpu_amax(m, n)
+
+
+def _check_all(m, parent, tok, what):
+    logits, path, acc, nxt, amax = _run(m, parent, tok)
+    ref, _, _ = oracle.tree_forward(m.ow, m.ok, m.ov, tok, parent, rounding=True)
+    err, rel = parity.check_logits(logits, ref, what)
+    np.testing.assert_array_equal(amax, np.argmax(logits, axis=1))
+    parity.check_argmax(amax, ref, what)
+    parity.check_walk(parent, tok, amax, path, acc, nxt, ref, what)
+    print(f"[{what}] max_abs={err:.2e} rel={rel:.2e}", flush=True)
+    return logits
+
+
+def test_weights_identical_on_cpu_and_gpu(model):
+    cpu = workloads.make_weights(model.shape, "cpu", gain_jitter=0.1).layer(1)
+    gpu = model.gen.layer(1)
+    for k in cpu:
+        assert torch.equal(cpu[k], gpu[k].cpu()), k
+
+
+@pytest.mark.parametrize("tree", list(TREES))
+def test_verify_matches_oracle(model, tree):
+    parent = TREES[tree]
+    tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=101, stream=len(parent))
+    _check_all(model, parent, tok, f"{model.shape.name}/{tree}")
+
+
+def test_launch_shape_variants(model, monkeypatch):
+    # Unsplit GEMMs, maximal split-K, and attention splits that each span
+    # several key chunks all meet the oracle bar.
+    parent = TREES["b432_n41"]
+    tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=7)
+    _check_all(model, parent, tok, "default")
+    for env in ({"LLMCAD_GEMM_WGS": "1", "LLMCAD_ATTN_WGS": "1"},
+                {"LLMCAD_GEMM_WGS": "100000", "LLMCAD_ATTN_WGS": "8"}):
+        for k, v in env.items():
+            monkeypatch.setenv(k, v)
+        _check_all(model, parent, tok, str(env))
+
+
+def test_deterministic_and_prefix_untouched(model):
+    parent = TREES["random_n77"]
+    tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=5)
+    before = model.sess.k_cache[:, :, :P].clone(), model.sess.v_cache[:, :, :P].clone()
+    a = _run(model, parent, tok)
+    b = _run(model, parent, tok)
+    np.testing.assert_array_equal(a[0], b[0])
+    assert a[1:4] == b[1:4]
+    assert torch.equal(model.sess.k_cache[:, :, :P], before[0])
+    assert torch.equal(model.sess.v_cache[:, :, :P], before[1])
+
+
+def test_tree_kv_written_to_node_slots(model):
+    parent = TREES["binary_d3_n15"]
+    n = len(parent)
+    tok = workloads.draw_tokens(n, model.shape.vocab, seed=9)
+    _run(model, parent, tok)
+    _, tk, tv = oracle.tree_forward(model.ow, model.ok, model.ov, tok, parent, rounding=True)
+    # cache [L][H][cap][Dh] vs oracle [L][n][H][Dh]
+    gk = model.sess.k_cache[:, :, P:P + n].float().cpu().numpy().transpose(0, 2, 1, 3)
+    gv = model.sess.v_cache[:, :, P:P + n].float().cpu().numpy().transpose(0, 2, 1, 3)
+    for g, r in ((gk, tk), (gv, tv)):
+        scale = np.abs(r).max()
+        assert np.abs(g - r).max() <= 2e-2 * scale
+
+
+def test_isolated_prefix_kv(model):
+    # Upload the oracle's bf16 prefix K/V instead of the GPU prefill's.
+    s = model.sess
+    saved = s.k_cache[:, :, :P].clone(), s.v_cache[:, :, :P].clone()
+    try:
+        s.k_cache[:, :, :P] = torch.from_numpy(model.ok.transpose(0, 2, 1, 3).astype(np.float32)).to(
+            torch.bfloat16).cuda()
+        s.v_cache[:, :, :P] = torch.from_numpy(model.ov.transpose(0, 2, 1, 3).astype(np.float32)).to(
+            torch.bfloat16).cuda()
+        parent = TREES["binary_d4_n31"]
+        tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=13)
+        _check_all(model, parent, tok, "isolated")
+    finally:
+        s.k_cache[:, :, :P] = saved[0]
+        s.v_cache[:, :, :P] = saved[1]
+
+
+def test_prefill_last_logits(model):
+    binding = model.binding
+    s = model.sess
+    toks = workloads.draw_tokens(150, model.shape.vocab, seed=21)
+    k = torch.zeros_like(s.k_cache)
+    v = torch.zeros_like(s.v_cache)
+    out = torch.empty(model.shape.vocab, dtype=torch.float32, device="cuda")
+    binding.prefill(s.cfg, s.packed, k, v, toks, 0, out, s.workspace)
+    torch.cuda.synchronize()
+    ref, _, _ = oracle.causal_forward(model.ow, toks, rounding=True)
+    parity.check_logits(out.cpu().numpy()[None], ref[-1:], "prefill")
+
+
+def test_planted_tree(model):
+    # Plant the oracle's greedy continuation along the last branch of a 41-node
+    # tree; the GPU must accept exactly K nodes and return the next greedy token.
+    parent = TREES["b432_n41"]
+    n = len(parent)
+    tok = workloads.draw_tokens(n, model.shape.vocab, seed=17)
+    K = 2
+    seq = [int(x) for x in np.concatenate([model.prefix, tok[:1]])]
+    cont = []
+    for _ in range(K + 1):
+        lg, _, _ = oracle.causal_forward(model.ow, seq, rounding=True)
+        cont.append(int(np.argmax(lg[-1])))
+        seq.append(cont[-1])
+    tok_p = workloads.plant_path(parent, tok, n - 1, cont, model.shape.vocab)
+    ref = oracle.verify_tree(model.ow, model.ok, model.ov, tok_p, parent, rounding=True)
+    assert ref["accept_len"] == K
+    logits, path, acc, nxt, amax = _run(model, parent, tok_p)
+    confident = parity.check_walk(parent, tok_p, amax, path, acc, nxt, ref["logits"], "planted")
+    if confident:
+        assert acc == K and nxt == cont[K]
+
+
+def test_host_errors_leave_cache_untouched(model):
+    binding = model.binding
+    s = model.sess
+    before = s.k_cache.clone()
+    V = model.shape.vocab
+    cases = [
+        ([1, 2], [0, 0], binding.ETREE),          # parent[0] != -1
+        ([1, 2, 3], [-1, 0, 2], binding.ETREE),   # parent[i] >= i
+        ([1, V], [-1, 0], binding.ETREE),          # token out of range
+        ([], [], binding.ETREE),                   # empty tree
+    ]
+    for tok, par, want in cases:
+        rc = binding.verify_tree(s.cfg, s.packed, s.k_cache, s.v_cache, P, tok, par, s.logits, s.path,
+                                 s.accept_len, s.next_token, s.workspace, raise_on_error=False)
+        assert rc == want, (tok, par, rc)
+    rc = binding.verify_tree(s.cfg, s.packed, s.k_cache, s.v_cache, s.capacity - 1, [1, 2], [-1, 0],
+                             s.logits, s.path, s.accept_len, s.next_token, s.workspace,
+                             raise_on_error=False)
+    assert rc == binding.ECAPACITY
+    big = workloads.chain_tree(129)
+    rc = binding.verify_tree(s.cfg, s.packed, s.k_cache, s.v_cache, P, np.zeros(129), big, s.logits,
+                             s.path, s.accept_len, s.next_token, s.workspace, raise_on_error=False)
+    assert rc == binding.ETREE
+    torch.cuda.synchronize()
+    assert torch.equal(s.k_cache, before)
