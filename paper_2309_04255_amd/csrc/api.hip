@@ -34,7 +34,7 @@ int env_int(const char* name, int dflt) {
 struct LaunchTargets {
   int gemm_wgs, attn_wgs;
   LaunchTargets()
-      : gemm_wgs(env_int("LLMCAD_GEMM_WGS", 1024)), attn_wgs(env_int("LLMCAD_ATTN_WGS", 512)) {}
+      : gemm_wgs(env_int("LLMCAD_GEMM_WGS", 256)), attn_wgs(env_int("LLMCAD_ATTN_WGS", 512)) {}
 };
 
 int choose_ksplit(const LaunchTargets& lt, int tiles, int ksteps) {

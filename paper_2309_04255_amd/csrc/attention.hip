@@ -33,9 +33,14 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnParams p) {
   constexpr int DB = DH / 16;      // 16-wide output column blocks
   constexpr int KST = DH + 8;      // LDS row stride of K (bf16)
   constexpr int VST = CH + 8;      // LDS row stride of V^T (bf16)
-  __shared__ __attribute__((aligned(16))) bf16 Ks[CH * KST];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VST];
+  // LDS: the K and V^T tiles of the chunk loop, reused by the split merge.
+  constexpr int KS_BYTES = CH * KST * 2, VT_BYTES = DH * VST * 2;
+  constexpr int MERGE_BYTES = 2 * kAttnMaxSplits * kMaxNodes * 4;
+  constexpr int LDS_BYTES = KS_BYTES + VT_BYTES > MERGE_BYTES ? KS_BYTES + VT_BYTES : MERGE_BYTES;
+  __shared__ __attribute__((aligned(16))) char lds_raw[LDS_BYTES];
   __shared__ int flag;
+  bf16* Ks = reinterpret_cast<bf16*>(lds_raw);
+  bf16* Vt = reinterpret_cast<bf16*>(lds_raw + KS_BYTES);
 
   const int h = blockIdx.x / p.splits, sp = blockIdx.x % p.splits;
   const int c_begin = sp * p.nchunks / p.splits, c_end = (sp + 1) * p.nchunks / p.splits;
@@ -177,31 +182,67 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnParams p) {
     const int rb = wave + 4 * r;
     if (rb >= MB) continue;
     const int row = 16 * rb + li;
-    if (g == 0) {
-      p.part_ml[(split_base + row) * 2 + 0] = m_run[r];
-      p.part_ml[(split_base + row) * 2 + 1] = l_run[r];
-    }
+    if (g == 0) st_coherent2(&p.part_ml[(split_base + row) * 2], m_run[r], l_run[r]);
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
-      *(f32x4*)&p.part_o[(split_base + row) * DH + 16 * db + 4 * g] = oacc[r][db];
+    for (int db = 0; db < DB; ++db) {
+      float* dst = &p.part_o[(split_base + row) * DH + 16 * db + 4 * g];
+      st_coherent2(dst, oacc[r][db][0], oacc[r][db][1]);
+      st_coherent2(dst + 2, oacc[r][db][2], oacc[r][db][3]);
+    }
   }
 
   if (!arrive_last(&p.counters[h], p.splits, &flag)) return;
 
-  // Merge the splits of head h in split order.
-  for (int idx = threadIdx.x; idx < p.n * DH; idx += 256) {
-    const int i = idx / DH, dd = idx % DH;
+  // Merge the splits of head h in split order: per-row weights first (in
+  // LDS), then every output element as a weighted sum of the split outputs.
+  float (*wgt)[kMaxNodes] = reinterpret_cast<float (*)[kMaxNodes]>(lds_raw);
+  float (*lsum)[kMaxNodes] = wgt + kAttnMaxSplits;
+  const int S = p.splits;
+  const size_t head_base = (size_t)h * S * p.Mp;
+  for (int idx = threadIdx.x; idx < S * p.n; idx += 256) {
+    const int s = idx / p.n, i = idx % p.n;
+    const float2 ml = ld_coherent2(&p.part_ml[(head_base + (size_t)s * p.Mp + i) * 2]);
+    wgt[s][i] = ml.x;
+    lsum[s][i] = ml.y;
+  }
+  __syncthreads();
+  if (threadIdx.x < p.n) {
+    const int i = threadIdx.x;
     float M = -INFINITY;
-    for (int s = 0; s < p.splits; ++s)
-      M = fmaxf(M, p.part_ml[(((size_t)h * p.splits + s) * p.Mp + i) * 2]);
-    float L = 0.0f, O = 0.0f;
-    for (int s = 0; s < p.splits; ++s) {
-      const size_t b = ((size_t)h * p.splits + s) * p.Mp + i;
-      const float w = exp2f(p.part_ml[b * 2] - M);
-      L += p.part_ml[b * 2 + 1] * w;
-      O += p.part_o[b * DH + dd] * w;
+    for (int s = 0; s < S; ++s) M = fmaxf(M, wgt[s][i]);
+    float L = 0.0f;
+    for (int s = 0; s < S; ++s) {
+      const float w = exp2f(wgt[s][i] - M);
+      wgt[s][i] = w;
+      L += lsum[s][i] * w;
     }
-    ((bf16*)p.o_out)[(size_t)i * d + h * DH + dd] = f2bf(O / L);
+    const float inv = 1.0f / L;
+    for (int s = 0; s < S; ++s) wgt[s][i] *= inv;
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < p.n * (DH / 2); idx += 256) {
+    const int i = idx / (DH / 2), dd = 2 * (idx % (DH / 2));
+    float o0 = 0.0f, o1 = 0.0f;
+    int s = 0;
+    for (; s + 4 <= S; s += 4) {  // four loads in flight, sums in split order
+      float2 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        v[u] = ld_coherent2(&p.part_o[(head_base + (size_t)(s + u) * p.Mp + i) * DH + dd]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        o0 += v[u].x * wgt[s + u][i];
+        o1 += v[u].y * wgt[s + u][i];
+      }
+    }
+    for (; s < S; ++s) {
+      const float2 v = ld_coherent2(&p.part_o[(head_base + (size_t)s * p.Mp + i) * DH + dd]);
+      o0 += v.x * wgt[s][i];
+      o1 += v.y * wgt[s][i];
+    }
+    bf16* dst = (bf16*)p.o_out + (size_t)i * d + h * DH + dd;
+    dst[0] = f2bf(o0);
+    dst[1] = f2bf(o1);
   }
 }
 

@@ -50,23 +50,53 @@ __device__ __forceinline__ void wave_argmax(float& v, int& idx) {
   }
 }
 
-// Device-scope release of this workgroup's prior global writes, then an
-// atomic arrival on `counter`.  Returns true (to every thread) in the last of
-// `expected` arriving workgroups, after an acquire, and resets the counter.
-// Must be called by all threads of the workgroup.
+// Hand-off between workgroups of one launch without L2 maintenance.
+//
+// A full device-scope fence on this GPU writes back and invalidates the
+// XCD's L2, which costs far more than the data it protects.  Instead, data
+// read by another workgroup of the same launch is written with
+// device-coherent stores and read with device-coherent loads (relaxed
+// device-scope atomics: they bypass non-coherent L2 state), and
+// arrive_last only has to wait until this workgroup's stores have completed
+// before counting its arrival with a device-scope atomic.
+__device__ __forceinline__ void st_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coherent(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coherent2(float* p, float a, float b) {  // p 8-byte aligned
+  const uint64_t bits = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
+  __hip_atomic_store((uint64_t*)p, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int ld_coherent(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 ld_coherent2(const float* p) {  // p 8-byte aligned
+  const uint64_t bits = __hip_atomic_load((const uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)bits), __uint_as_float((uint32_t)(bits >> 32)));
+}
+
+// Counts this workgroup's arrival on `counter`; returns true (to every
+// thread) in the last of `expected` arriving workgroups, which also resets
+// the counter.  The caller's cross-workgroup data must have been written
+// with st_coherent*; the last workgroup reads it with ld_coherent*.  Must be
+// called by all threads of the workgroup.
 __device__ __forceinline__ bool arrive_last(int* counter, int expected, int* lds_flag) {
-  __threadfence();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);  // keep the stores above in program order
+  __builtin_amdgcn_s_waitcnt(0);            // and wait until they have completed
   __syncthreads();
   if (threadIdx.x == 0) {
-    int old = __hip_atomic_fetch_add(counter, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    int last = (old == expected - 1);
+    const int old = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = (old == expected - 1);
     if (last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *lds_flag = last;
   }
   __syncthreads();
-  bool last = *lds_flag != 0;
-  if (last) __threadfence();
-  return last;
+  return *lds_flag != 0;
 }
 
 }  // namespace llmcad

@@ -57,6 +57,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
   __shared__ float tileS[ROWS][TS];
   __shared__ int flag;
   __shared__ int reach[EPI == EPI_LOGITS ? kMaxNodes : 1];
+  __shared__ int amax_s[EPI == EPI_LOGITS ? kMaxNodes : 1];
 
   const int tile = blockIdx.x / p.ksplit;
   const int split = blockIdx.x - tile * p.ksplit;
@@ -69,11 +70,34 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
 
   float rstd[MB];
   if constexpr (PRO == PRO_NORM) {
+    // rstd(row) from the per-tile sums of squares: the block's threads split
+    // the tiles into CH contiguous chunks, then the chunks are added in
+    // order, so every workgroup forms the same value.
+    constexpr int CH = 256 / ROWS;
+    __shared__ float part_ss[CH][ROWS];
+    if (threadIdx.x < CH * ROWS) {
+      const int r = threadIdx.x % ROWS, c = threadIdx.x / ROWS;
+      const int t0 = c * p.ssq_tiles / CH, t1 = (c + 1) * p.ssq_tiles / CH;
+      float ss = 0.0f;
+      int t = t0;
+      for (; t + 4 <= t1; t += 4) {
+        const float v0 = p.ssq[(size_t)t * p.Mp + r], v1 = p.ssq[(size_t)(t + 1) * p.Mp + r];
+        const float v2 = p.ssq[(size_t)(t + 2) * p.Mp + r], v3 = p.ssq[(size_t)(t + 3) * p.Mp + r];
+        ss += v0;
+        ss += v1;
+        ss += v2;
+        ss += v3;
+      }
+      for (; t < t1; ++t) ss += p.ssq[(size_t)t * p.Mp + r];
+      part_ss[c][r] = ss;
+    }
+    __syncthreads();
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb) {
       const int row = 16 * rb + lrow;
       float ss = 0.0f;
-      for (int t = 0; t < p.ssq_tiles; ++t) ss += p.ssq[(size_t)t * p.Mp + row];
+#pragma unroll
+      for (int c = 0; c < CH; ++c) ss += part_ss[c][row];
       rstd[rb] = 1.0f / sqrtf(ss * p.inv_d + p.eps);
     }
   }
@@ -160,13 +184,30 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
 
   if (p.ksplit > 1) {
     float* mine = p.part + (size_t)blockIdx.x * ROWS * 64;
-    for (int idx = threadIdx.x; idx < ROWS * 64; idx += 256) mine[idx] = tileS[idx >> 6][idx & 63];
+    for (int idx = 2 * threadIdx.x; idx < ROWS * 64; idx += 512)
+      st_coherent2(mine + idx, tileS[idx >> 6][idx & 63], tileS[idx >> 6][(idx & 63) + 1]);
     if (!arrive_last(&p.counters[tile], p.ksplit, &flag)) return;
     const float* base = p.part + (size_t)tile * p.ksplit * ROWS * 64;
-    for (int idx = threadIdx.x; idx < ROWS * 64; idx += 256) {
-      float s = 0.0f;
-      for (int sp = 0; sp < p.ksplit; ++sp) s += base[(size_t)sp * ROWS * 64 + idx];
-      tileS[idx >> 6][idx & 63] = s;
+    for (int idx = 2 * threadIdx.x; idx < ROWS * 64; idx += 512) {
+      float s0 = 0.0f, s1 = 0.0f;
+      int sp = 0;
+      for (; sp + 4 <= p.ksplit; sp += 4) {  // four loads in flight, sums in split order
+        float2 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = ld_coherent2(base + (size_t)(sp + u) * ROWS * 64 + idx);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          s0 += v[u].x;
+          s1 += v[u].y;
+        }
+      }
+      for (; sp < p.ksplit; ++sp) {
+        const float2 v = ld_coherent2(base + (size_t)sp * ROWS * 64 + idx);
+        s0 += v.x;
+        s1 += v.y;
+      }
+      tileS[idx >> 6][idx & 63] = s0;
+      tileS[idx >> 6][(idx & 63) + 1] = s1;
     }
     __syncthreads();
   }
@@ -231,8 +272,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
       int mi = valid ? col : 0x7fffffff;
       wave_argmax(mv, mi);
       if (lane == 0) {
-        p.lm_val[(size_t)tile * p.Mp + r] = mv;
-        p.lm_idx[(size_t)tile * p.Mp + r] = mi;
+        st_coherent(&p.lm_val[(size_t)tile * p.Mp + r], mv);
+        st_coherent(&p.lm_idx[(size_t)tile * p.Mp + r], mi);
       }
     }
     if (!arrive_last(p.lm_counter, p.tiles, &flag)) return;
@@ -240,16 +281,27 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
     for (int r = wave; r < p.n; r += 4) {
       float mv = -INFINITY;
       int mi = 0x7fffffff;
-      for (int t = lane; t < p.tiles; t += 64) {
-        const float v = p.lm_val[(size_t)t * p.Mp + r];
-        const int i = p.lm_idx[(size_t)t * p.Mp + r];
-        if (v > mv || (v == mv && i < mi)) {
-          mv = v;
-          mi = i;
+      for (int t0 = 0; t0 < p.tiles; t0 += 4 * 64) {  // four loads per lane in flight
+        float v[4];
+        int ix[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int t = t0 + 64 * u + lane;
+          v[u] = t < p.tiles ? ld_coherent(&p.lm_val[(size_t)t * p.Mp + r]) : -INFINITY;
+          ix[u] = t < p.tiles ? ld_coherent(&p.lm_idx[(size_t)t * p.Mp + r]) : 0x7fffffff;
         }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (v[u] > mv || (v[u] == mv && ix[u] < mi)) {
+            mv = v[u];
+            mi = ix[u];
+          }
       }
       wave_argmax(mv, mi);
-      if (lane == 0) p.amax[r] = mi;
+      if (lane == 0) {
+        p.amax[r] = mi;
+        amax_s[r] = mi;
+      }
     }
     __syncthreads();
     // Accept walk (§3.2): node i is reachable when its parent is reachable and
@@ -260,7 +312,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
       reach[0] = 1;
       for (int i = 1; i < p.n; ++i) {
         const int par = p.tree_parent[i];
-        const int ok = reach[par] && (p.tree_tok[i] == p.amax[par]);
+        const int ok = reach[par] && (p.tree_tok[i] == amax_s[par]);
         reach[i] = ok;
         const int dep = p.tree_depth[i];
         if (ok && dep > best_depth) {
@@ -271,7 +323,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
       for (int k = 0; k < p.n; ++k) p.path[k] = -1;
       for (int i = best; i >= 0; i = p.tree_parent[i]) p.path[p.tree_depth[i]] = i;
       *p.accept_len = best_depth;
-      *p.next_token = p.amax[best];
+      *p.next_token = amax_s[best];
     }
   }
 }

@@ -84,8 +84,10 @@ struct PackedLayout {
 // Split of an attention pass over key positions: every head's positions
 // [0, P + n) are cut into 64-wide chunks, and each workgroup takes a
 // contiguous run of chunks.
+constexpr int kAttnMaxSplits = 32;  // position splits per head
 inline int attn_max_splits(int H) {
   int s = kAttnMaxWgs / H;
+  if (s > kAttnMaxSplits) s = kAttnMaxSplits;
   return s < 1 ? 1 : s;
 }
 

@@ -19,34 +19,30 @@ __global__ __launch_bounds__(256) void embed_kernel(TreeArgs tree, int n, int Mp
                                                     float* __restrict__ x,
                                                     float* __restrict__ ssq) {
   const int m = blockIdx.x;
-  if (m == 0 && threadIdx.x == 0) {
-    int* tok = ws_tree;
-    int* par = ws_tree + 128;
-    int* depth = ws_tree + 256;
-    int* pos = ws_tree + 384;
-    uint32_t* anc = (uint32_t*)(ws_tree + 512);
-    for (int i = 0; i < 128; ++i) {
-      if (i < n) {
-        const int p = tree.parent[i];
-        const int dep = (i == 0) ? 0 : depth[p] + 1;
-        uint32_t a[4] = {0u, 0u, 0u, 0u};
-        if (i > 0) {
-          for (int w = 0; w < 4; ++w) a[w] = anc[p * 4 + w];
-        }
-        a[i >> 5] |= 1u << (i & 31);
-        tok[i] = tree.tok[i];
-        par[i] = p;
-        depth[i] = dep;
-        pos[i] = prefix_len + dep;
-        for (int w = 0; w < 4; ++w) anc[i * 4 + w] = a[w];
-      } else {
-        tok[i] = 0;
-        par[i] = -1;
-        depth[i] = 0;
-        pos[i] = prefix_len;
-        for (int w = 0; w < 4; ++w) anc[i * 4 + w] = 0u;
+  __shared__ int par_s[128];
+  if (m == 0) {
+    if (threadIdx.x < 128) par_s[threadIdx.x] = threadIdx.x < n ? tree.parent[threadIdx.x] : -1;
+    __syncthreads();
+  }
+  if (m == 0 && threadIdx.x < 128) {
+    // Each node walks its own ancestor chain (all nodes in parallel).
+    const int i = threadIdx.x;
+    int dep = 0;
+    uint32_t a[4] = {0u, 0u, 0u, 0u};
+    if (i < n) {
+      for (int j = i; j >= 0; j = par_s[j]) {
+        a[j >> 5] |= 1u << (j & 31);
+        ++dep;
       }
+      --dep;
     }
+    ws_tree[i] = i < n ? tree.tok[i] : 0;
+    ws_tree[128 + i] = par_s[i];
+    ws_tree[256 + i] = dep;
+    ws_tree[384 + i] = prefix_len + dep;
+    uint32_t* anc = (uint32_t*)(ws_tree + 512);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) anc[i * 4 + w] = a[w];
   }
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const bool valid = m < n;
