@@ -160,8 +160,12 @@ const char* llmcad_status_string(int status);
 /* Byte offset and size of a named intermediate buffer inside a workspace
  * sized for max_n (for diagnostics): 0 residual stream fp32 [Mp][d],
  * 1 rotated queries bf16 [Mp][d], 2 attention output bf16 [Mp][d],
- * 3 SwiGLU product bf16 [Mp][Fp], 4 per-node greedy token int32 [Mp];
- * Mp = max_n rounded up to 16, Fp = F rounded up to 32. */
+ * 3 SwiGLU product bf16 [Mp][Fp], 4 per-node greedy token int32 [Mp],
+ * 5 pass status int32 (0 = ok; 1 = a grid wait of the single-launch pass ran
+ * out of its bounded spin: the pass's outputs are invalid, and the workspace
+ * must be cleared with llmcad_workspace_init before the next pass);
+ * Mp = max_n rounded up to 16, Fp = F rounded up to 32.  Offsets describe a
+ * pass over max_n nodes (call with max_n = that pass's n). */
 int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t which, size_t* offset,
                             size_t* bytes);
 
@@ -173,6 +177,7 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
 #define LLMCAD_KERNEL_DOWN 4      /* down projection + residual                   */
 #define LLMCAD_KERNEL_LM_HEAD 5   /* final RMSNorm + LM head + argmax + walk      */
 #define LLMCAD_KERNEL_EMBED 6     /* tree preparation + embedding                 */
+#define LLMCAD_KERNEL_PASS 7      /* the whole pass as one persistent launch      */
 
 /* Diagnostics (measurement only, process-wide, not thread-safe): after
  * llmcad_timing_enable(c, m), the next m launches of kernel class c made by

@@ -39,7 +39,7 @@ SYMBOLS = (
 )
 
 KERNEL_QKV, KERNEL_ATTENTION, KERNEL_O_PROJ, KERNEL_GATE_UP, KERNEL_DOWN, KERNEL_LM_HEAD, \
-    KERNEL_EMBED = range(7)
+    KERNEL_EMBED, KERNEL_PASS = range(8)
 
 
 class LlmcadConfig(ctypes.Structure):

@@ -114,7 +114,26 @@ struct Pass {
   hipStream_t st;
 };
 
+// Device facts for the persistent pass, looked up once per device.
+struct DeviceInfo {
+  int cus = 0;
+};
+DeviceInfo device_info() {
+  static DeviceInfo cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DeviceInfo();
+  if (cache[dev].cus == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+      cache[dev].cus = cus;
+  }
+  return cache[dev];
+}
+
+int run_pass_persistent(const Pass& a, const TreeArgs& tree);
+
 int run_pass(const Pass& a, const TreeArgs& tree) {
+  if (env_int("LLMCAD_PERSISTENT", 0) != 0) return run_pass_persistent(a, tree);
   const Shape s(*a.cfg);
   const PackedLayout P(s);
   const WorkspaceLayout W(s, a.n);
@@ -272,6 +291,98 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   return LLMCAD_OK;
 }
 
+int run_pass_persistent(const Pass& a, const TreeArgs& tree) {
+  const Shape s(*a.cfg);
+  const PackedLayout P(s);
+  const WorkspaceLayout W(s, a.n);
+  const int MB = W.Mp / 16;
+  const DeviceInfo dev = device_info();
+  const int occ = pass_occupancy(MB, s.Dh);
+  if (dev.cus <= 0 || occ <= 0) {
+    g_last_error = hipErrorInvalidConfiguration;
+    return LLMCAD_EHIP;
+  }
+  int per_cu = env_int("LLMCAD_PASS_WGS_PER_CU", 1);
+  if (per_cu > occ) per_cu = occ;
+  int G = dev.cus * per_cu;
+  if (G > kPassMaxGrid) G = kPassMaxGrid;
+  char* ws = a.ws;
+  int* counters = (int*)(ws + W.counters);
+
+  PassParams p;
+  memset(&p, 0, sizeof(p));
+  p.L = s.L;
+  p.d = s.d;
+  p.H = s.H;
+  p.Dh = s.Dh;
+  p.F = s.F;
+  p.Fp = s.Fp;
+  p.V = s.V;
+  p.eps = a.cfg->rms_eps;
+  p.inv_d = 1.0f / (float)s.d;
+  p.log2_theta = (float)log2((double)a.cfg->rope_theta);
+  p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.Dh));
+  p.n = a.n;
+  p.Mp = W.Mp;
+  p.prefix_len = a.prefix_len;
+  p.cap = a.cap;
+  p.G = G;
+  p.packed = a.packed;
+  p.o_embed = (long long)P.embed;
+  p.o_final_norm = (long long)P.final_norm;
+  p.o_lm = (long long)P.lm_head;
+  p.layer0 = (long long)P.globals_end;
+  p.layer_bytes = (long long)P.layer_bytes;
+  p.o_attn_norm = (long long)P.attn_norm;
+  p.o_qkv = (long long)P.w_qkv;
+  p.o_o = (long long)P.w_o;
+  p.o_ffn_norm = (long long)P.ffn_norm;
+  p.o_gu = (long long)P.w_gate_up;
+  p.o_down = (long long)P.w_down;
+  p.ks_d = s.ks_d;
+  p.ks_f = s.ks_f;
+  p.qkv_tiles = s.qkv_tiles;
+  p.d_tiles = s.d_tiles;
+  p.gu_tiles = s.gu_tiles;
+  p.v_tiles = s.v_tiles;
+  p.k_cache = (bf16*)a.k_cache;
+  p.v_cache = (bf16*)a.v_cache;
+  p.tree = (int*)(ws + W.tree);
+  p.x = (float*)(ws + W.xs);
+  p.ssq = (float*)(ws + W.ssqs);
+  p.q = (bf16*)(ws + W.qs);
+  p.o = (bf16*)(ws + W.os);
+  p.h = (bf16*)(ws + W.hs);
+  p.part = (float*)(ws + W.part_sk);
+  p.attn_o = (float*)(ws + W.attn_o);
+  p.attn_ml = (float*)(ws + W.attn_ml);
+  const int T = a.prefix_len + a.n;
+  int S = G / s.H;
+  if (S > kAttnMaxSplits) S = kAttnMaxSplits;
+  if (S > cdiv(T, 16)) S = cdiv(T, 16);
+  if (S < 1) S = 1;
+  p.attn_splits = S;
+  p.tile_cnt = counters;
+  p.head_cnt = counters + W.n_gemm_counters;
+  p.lm_cnt = p.head_cnt + W.n_attn_counters;
+  p.bar = (int*)(ws + W.bar);
+  p.exit_cnt = p.lm_cnt + 1;
+  p.status = p.exit_cnt + 1;
+  p.lm_val = (float*)(ws + W.lm_val);
+  p.lm_idx = (int*)(ws + W.lm_idx);
+  p.amax = (int*)(ws + W.amax);
+  p.logits = a.logits;
+  p.row_lo = a.row_lo;
+  p.path = a.path;
+  p.accept_len = a.accept_len;
+  p.next_token = a.next_token;
+  p.spin_limit = env_int("LLMCAD_SPIN_LIMIT", 4000000);
+  p.trace = env_int("LLMCAD_TRACE", 0) ? (long long*)(ws + W.trace) : nullptr;
+  TimedLaunch tl(LLMCAD_KERNEL_PASS, a.st);
+  HIP_TRY(launch_pass(MB, p, tree, a.st));
+  return LLMCAD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -339,6 +450,7 @@ int llmcad_workspace_init(const llmcad_config* cfg, int32_t max_n, void* workspa
   const WorkspaceLayout W(Shape(*cfg), max_n);
   if (workspace_bytes < W.total) return LLMCAD_EWORKSPACE;
   HIP_TRY(hipMemsetAsync((char*)workspace + W.counters, 0, W.counters_bytes, (hipStream_t)stream));
+  HIP_TRY(hipMemsetAsync((char*)workspace + W.bar, 0, 16 * 32 * 4, (hipStream_t)stream));
   return LLMCAD_OK;
 }
 
@@ -443,7 +555,7 @@ int llmcad_timing_enable(int32_t kernel_class, int32_t max_launches) {
     g_timing = Timing();
   }
   if (kernel_class < 0) return LLMCAD_OK;
-  if (kernel_class > LLMCAD_KERNEL_EMBED || max_launches < 1) return LLMCAD_EARG;
+  if (kernel_class > LLMCAD_KERNEL_PASS || max_launches < 1) return LLMCAD_EARG;
   g_timing.ev = (hipEvent_t*)calloc((size_t)2 * max_launches, sizeof(hipEvent_t));
   if (g_timing.ev == nullptr) return LLMCAD_EARG;
   for (int i = 0; i < 2 * max_launches; ++i) {
@@ -503,6 +615,8 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
     case 2: *offset = W.o; *bytes = (size_t)W.Mp * s.d * 2; break;
     case 3: *offset = W.h; *bytes = (size_t)W.Mp * s.Fp * 2; break;
     case 4: *offset = W.amax; *bytes = (size_t)W.Mp * 4; break;
+    case 6: *offset = W.trace; *bytes = (size_t)8 * (2 + 5 * s.L) * 6 * 8; break;
+    case 5: *offset = W.counters + (size_t)(W.n_gemm_counters + W.n_attn_counters + 2) * 4; *bytes = 4; break;
     default: return LLMCAD_EARG;
   }
   return LLMCAD_OK;

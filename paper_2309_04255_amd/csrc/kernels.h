@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "device.h"
+
 namespace llmcad {
 
 // ---- weight packing (pack.hip)
@@ -91,5 +93,46 @@ struct AttnParams {
   float scale_log2;  // log2(e) / sqrt(Dh)
 };
 hipError_t launch_attention(int mb, const AttnParams& p, hipStream_t st);
+
+// ---- persistent single-launch pass (pass.hip)
+struct PassParams {  // see pass.hip for the phase structure
+  int L, d, H, Dh, F, Fp, V;
+  float eps, inv_d, log2_theta, scale_log2;
+  int n, Mp, prefix_len, cap, G;
+  const char* packed;
+  long long o_embed, o_final_norm, o_lm, layer0, layer_bytes;
+  long long o_attn_norm, o_qkv, o_o, o_ffn_norm, o_gu, o_down;
+  int ks_d, ks_f, qkv_tiles, d_tiles, gu_tiles, v_tiles;
+  bf16* k_cache;
+  bf16* v_cache;
+  int* tree;
+  float* x;    // [2L+1][Mp][d]
+  float* ssq;  // [2L+1][d_tiles][Mp]
+  bf16* q;     // [L][Mp][d]
+  bf16* o;     // [L][Mp][d]
+  bf16* h;     // [L][Mp][Fp]
+  float* part; // [G][2][Mp][64]
+  float* attn_o;
+  float* attn_ml;
+  int attn_splits;
+  int* tile_cnt;
+  int* head_cnt;
+  int* lm_cnt;
+  int* bar;
+  int* exit_cnt;
+  int* status;
+  float* lm_val;
+  int* lm_idx;
+  int* amax;
+  float* logits;
+  int row_lo;
+  int* path;
+  int* accept_len;
+  int* next_token;
+  int spin_limit;
+  long long* trace;  // diagnostics: [8][2 + 5L][3] phase timestamps, or null
+};
+hipError_t launch_pass(int mb, const PassParams& p, const TreeArgs& tree, hipStream_t st);
+int pass_occupancy(int mb, int dh);  // resident workgroups per CU (0 if unavailable)
 
 }  // namespace llmcad

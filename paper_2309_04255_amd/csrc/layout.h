@@ -85,6 +85,7 @@ struct PackedLayout {
 // [0, P + n) are cut into 64-wide chunks, and each workgroup takes a
 // contiguous run of chunks.
 constexpr int kAttnMaxSplits = 32;  // position splits per head
+constexpr int kPassMaxGrid = 1024;  // workgroups of the persistent pass
 inline int attn_max_splits(int H) {
   int s = kAttnMaxWgs / H;
   if (s > kAttnMaxSplits) s = kAttnMaxSplits;
@@ -107,7 +108,16 @@ struct WorkspaceLayout {
   size_t attn_o;     // fp32 [H][S][Mp][Dh] per-split unnormalised outputs
   size_t attn_ml;    // fp32 [H][S][Mp][2]  per-split running max and sum
   size_t scratch_out;  // int32 [128 + 2]  path/len/next sink for prefill
-  size_t counters;   // int32 [ncounters]
+  // persistent pass: one buffer per producing phase (written once per pass)
+  size_t xs;         // fp32 [2L+1][Mp][d]        residual stream versions
+  size_t ssqs;       // fp32 [2L+1][d/64][Mp]     their per-tile sums of squares
+  size_t qs;         // bf16 [L][Mp][d]
+  size_t os;         // bf16 [L][Mp][d]
+  size_t hs;         // bf16 [L][Mp][Fp]
+  size_t part_sk;    // fp32 [kPassMaxGrid][2][Mp][64] stream-K partial tiles
+  size_t trace;      // int64 [8][2 + 5L][6] phase timestamps (diagnostics)
+  size_t bar;        // int32 [16][32] grid-barrier slots, one per 128-byte line
+  size_t counters;   // int32 [ncounters]: gemm tiles | heads | lm | barrier | exit | status
   int n_gemm_counters, n_attn_counters;
   size_t counters_bytes;
   size_t total;
@@ -127,8 +137,9 @@ struct WorkspaceLayout {
     if (s.gu_tiles > max_tiles) max_tiles = s.gu_tiles;
     n_gemm_counters = max_tiles;
     n_attn_counters = s.H;
-    counters_bytes = (size_t)(n_gemm_counters + n_attn_counters + 1) * 4;
+    counters_bytes = (size_t)(n_gemm_counters + n_attn_counters + 4) * 4;
     counters = take(counters_bytes);
+    bar = take(16 * 32 * 4);
     scratch_out = take((128 + 2) * 4);
     tree = take(4 * 128 * 4 + 128 * 4 * 4);
     x = take((size_t)Mp * s.d * 4);
@@ -142,6 +153,13 @@ struct WorkspaceLayout {
     gemm_part = take((size_t)kGemmMaxWgs * Mp * 64 * 4);
     attn_o = take((size_t)s.H * S * Mp * s.Dh * 4);
     attn_ml = take((size_t)s.H * S * Mp * 2 * 4);
+    xs = take((size_t)(2 * s.L + 1) * Mp * s.d * 4);
+    ssqs = take((size_t)(2 * s.L + 1) * s.d_tiles * Mp * 4);
+    qs = take((size_t)s.L * Mp * s.d * 2);
+    os = take((size_t)s.L * Mp * s.d * 2);
+    hs = take((size_t)s.L * Mp * s.Fp * 2);
+    part_sk = take((size_t)kPassMaxGrid * 2 * Mp * 64 * 4);
+    trace = take((size_t)8 * (2 + 5 * s.L) * 6 * 8);
     total = o_;
   }
 };
