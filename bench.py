@@ -11,9 +11,9 @@ F 11008, V 32000), random bf16 weights, 512-token prefix, 31-node tree
 Prints one JSON line (rank 0):
   value            passes/s over the timed steps (inputs resident in HBM)
   hbm_roofline_frac  algorithmic bytes of a pass / (time per pass * 8 TB/s)
-  roofline         the dominant kernel (gate/up GEMM + SwiGLU): algorithmic
-                   bytes per launch / mean launch time (HIP events on the
-                   pass's stream), against 8 TB/s
+  roofline         the dominant kernel, which is the whole pass (one
+                   persistent launch): algorithmic bytes per launch / mean
+                   launch time (HIP events on the pass's stream), against 8 TB/s
   cpu_baseline     the CPU oracle timed on this host on a bounded sample
 Progress goes to stderr.
 """
@@ -31,8 +31,9 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
 METRIC = "tree-verify passes/sec + % HBM roofline, LLaMA-7B shape, 31-node tree"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_gemm_traffic.json")
-GEMM_SOURCE = os.path.join(ROOT, "paper_2309_04255_amd", "csrc", "gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pass_kernel_traffic.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2309_04255_amd", "csrc", f)
+                  for f in ("pass.hip", "device.h", "layout.h", "kernels.h")]
 
 
 def log(msg):
@@ -47,26 +48,25 @@ def pass_bytes(shape, P, n):
     return weights + 4 * L * P * d + 4 * L * n * d + 2 * n * d + 4 * n * V
 
 
-def gate_up_bytes(shape, n):
-    """Algorithmic bytes of one gate/up launch: W_gate and W_up (bf16) once,
-    the fp32 residual rows read once, the bf16 SwiGLU product written once."""
-    d, F = shape.d_model, shape.d_ffn
-    return 2 * (2 * F * d) + 4 * n * d + 2 * n * F
-
-
 def source_hash():
-    with open(GEMM_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
-def load_traffic(n_expected):
+def load_traffic(workload):
+    """Measured HBM bytes per pass-kernel launch (FETCH_SIZE + WRITE_SIZE,
+    calibrated against a copy kernel), or None when the counters were taken
+    on other kernel sources or another workload."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("gemm_source_sha256_16") != source_hash() or t.get("tree_nodes") != n_expected:
-        return None  # the kernel changed since the counters were taken
+    if t.get("kernel_sources_sha256_16") != source_hash() or t.get("workload") != workload:
+        return None
     return t.get("bytes_per_launch")
 
 
@@ -198,19 +198,19 @@ def main():
     log(f"timed {args.steps} passes: wall {wall * 1e3:.1f} ms, events {gpu_s * 1e3:.1f} ms "
         f"-> {ms_per_pass:.3f} ms/pass")
 
-    # Dominant kernel: gate/up GEMM, timed per launch with HIP events on the same
-    # stream, over the same number of passes in the same launch configuration.
-    launches = args.steps * shape.n_layers
-    binding.timing_enable(binding.KERNEL_GATE_UP, launches)
+    # Dominant kernel: the pass kernel itself, timed per launch with HIP events
+    # recorded by the library on the stream it launches on, over the same
+    # number of passes in the same launch configuration.
+    B = pass_bytes(shape, P, n)
+    binding.timing_enable(binding.KERNEL_PASS, args.steps)
     for _ in range(args.steps):
         one_pass()
     torch.cuda.synchronize()
-    tot_ms, nl = binding.timing_read(binding.KERNEL_GATE_UP)
+    tot_ms, nl = binding.timing_read(binding.KERNEL_PASS)
     binding.timing_enable(-1, 0)
-    gu_ms = tot_ms / max(nl, 1)
-    gu_alg = gate_up_bytes(shape, n)
-    gu_achieved = gu_alg / (gu_ms / 1e3)
-    log(f"gate/up GEMM: {nl} launches, mean {gu_ms * 1e3:.1f} us, {gu_achieved / 1e9:.0f} GB/s")
+    k_ms = tot_ms / max(nl, 1)
+    k_achieved = B / (k_ms / 1e3)
+    log(f"pass kernel: {nl} launches, mean {k_ms * 1e3:.1f} us, {k_achieved / 1e9:.0f} GB/s")
 
     # Latency of a pass when the decode loop waits for the accepted path.
     lat = []
@@ -220,9 +220,8 @@ def main():
         sess.accept_len.cpu()
         lat.append(time.perf_counter() - t)
 
-    B = pass_bytes(shape, P, n)
     frac = B / (elapsed / args.steps) / HBM_PEAK
-    traffic = load_traffic(n)
+    traffic = load_traffic(wl.name)
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -250,14 +249,14 @@ def main():
         "ms_per_pass_with_readback": round(1e3 * statistics.median(lat), 4),
         "roofline": {
             "bound": "hbm",
-            "kernel": "gate/up GEMM + SwiGLU (gemm_kernel PRO_NORM EPI_SWIGLU)",
-            "achieved": round(gu_achieved / 1e9, 1),
+            "kernel": "pass_kernel (persistent: embed, per layer QKV / attention / O / gate-up / down, LM head, walk)",
+            "achieved": round(k_achieved / 1e9, 1),
             "peak": HBM_PEAK / 1e9,
             "unit": "GB/s",
-            "frac": round(gu_achieved / HBM_PEAK, 4),
+            "frac": round(k_achieved / HBM_PEAK, 4),
             "traffic": traffic,
-            "alg_bytes_per_launch": gu_alg,
-            "mean_launch_us": round(gu_ms * 1e3, 2),
+            "alg_bytes_per_launch": B,
+            "mean_launch_us": round(k_ms * 1e3, 2),
         },
     }
     if not args.no_cpu_baseline:

@@ -35,8 +35,9 @@
  *                 w_o [d][d], ffn_norm [d],
  *                 w_gate_up [2F][d] (rows gate, then up), w_down [d][F]
  *  - Packed weights: an opaque device image of llmcad_packed_bytes() bytes
- *    written by llmcad_pack_globals / llmcad_pack_layer (MFMA-fragment order,
- *    4 KiB contiguous per 64 output columns x 32 inputs).  The globals sit
+ *    written by llmcad_pack_globals / llmcad_pack_layer (MFMA-fragment order:
+ *    1 KiB contiguous per 16 output columns x 32 inputs, consecutive inputs
+ *    consecutive).  The globals sit
  *    first, then layer 0, 1, ...; an image packed for L layers also serves a
  *    configuration with fewer layers.
  *  - KV cache: k_cache and v_cache are bf16 [L][H][capacity][Dh] each.  Slot p
@@ -158,26 +159,23 @@ int llmcad_prefill(const llmcad_config* cfg, const void* packed, void* k_cache, 
 const char* llmcad_status_string(int status);
 
 /* Byte offset and size of a named intermediate buffer inside a workspace
- * sized for max_n (for diagnostics): 0 residual stream fp32 [Mp][d],
- * 1 rotated queries bf16 [Mp][d], 2 attention output bf16 [Mp][d],
- * 3 SwiGLU product bf16 [Mp][Fp], 4 per-node greedy token int32 [Mp],
+ * sized for max_n (for diagnostics): 0 final residual stream fp32 [Mp][d],
+ * 1 layer 0's q and k before the rotary embedding fp32 [Mp][2d], 2 layer
+ * 0's attention output bf16 [Mp][d], 3 layer 0's SwiGLU product bf16
+ * [Mp][Fp], 4 per-node greedy token int32 [Mp],
  * 5 pass status int32 (0 = ok; 1 = a grid wait of the single-launch pass ran
  * out of its bounded spin: the pass's outputs are invalid, and the workspace
- * must be cleared with llmcad_workspace_init before the next pass);
+ * must be cleared with llmcad_workspace_init before the next pass),
+ * 6 phase timestamps int64 [8][2 + 5L][6] (written when the environment
+ * variable LLMCAD_TRACE is 1);
  * Mp = max_n rounded up to 16, Fp = F rounded up to 32.  Offsets describe a
  * pass over max_n nodes (call with max_n = that pass's n). */
 int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t which, size_t* offset,
                             size_t* bytes);
 
-/* Kernel classes of a pass, for llmcad_timing_enable. */
-#define LLMCAD_KERNEL_QKV 0       /* RMSNorm + QKV projection + rotary + KV write */
-#define LLMCAD_KERNEL_ATTENTION 1 /* tree-masked attention                        */
-#define LLMCAD_KERNEL_O_PROJ 2    /* output projection + residual                 */
-#define LLMCAD_KERNEL_GATE_UP 3   /* RMSNorm + gate/up projection + SwiGLU        */
-#define LLMCAD_KERNEL_DOWN 4      /* down projection + residual                   */
-#define LLMCAD_KERNEL_LM_HEAD 5   /* final RMSNorm + LM head + argmax + walk      */
-#define LLMCAD_KERNEL_EMBED 6     /* tree preparation + embedding                 */
-#define LLMCAD_KERNEL_PASS 7      /* the whole pass as one persistent launch      */
+/* Kernel classes for llmcad_timing_enable.  A verification or prefill pass
+ * is one persistent launch. */
+#define LLMCAD_KERNEL_PASS 0
 
 /* Diagnostics (measurement only, process-wide, not thread-safe): after
  * llmcad_timing_enable(c, m), the next m launches of kernel class c made by

@@ -38,8 +38,7 @@ SYMBOLS = (
     "llmcad_timing_read",
 )
 
-KERNEL_QKV, KERNEL_ATTENTION, KERNEL_O_PROJ, KERNEL_GATE_UP, KERNEL_DOWN, KERNEL_LM_HEAD, \
-    KERNEL_EMBED, KERNEL_PASS = range(8)
+KERNEL_PASS = 0  # the whole pass is one persistent launch
 
 
 class LlmcadConfig(ctypes.Structure):

@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libllmcad.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "pass.hip", "gemm.hip", "attention.hip", "tree.hip", "pack.hip"]
+SOURCES = ["api.hip", "pass.hip", "pack.hip"]
 
 
 def hipcc() -> str:

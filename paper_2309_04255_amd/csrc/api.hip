@@ -29,24 +29,6 @@ int env_int(const char* name, int dflt) {
   return x > 0 ? x : dflt;
 }
 
-// Workgroup-count targets for the GEMM split-K and the attention position
-// splits (read once per pass; the environment variables tune launch shapes).
-struct LaunchTargets {
-  int gemm_wgs, attn_wgs;
-  LaunchTargets()
-      : gemm_wgs(env_int("LLMCAD_GEMM_WGS", 256)), attn_wgs(env_int("LLMCAD_ATTN_WGS", 512)) {}
-};
-
-int choose_ksplit(const LaunchTargets& lt, int tiles, int ksteps) {
-  int ks = cdiv(lt.gemm_wgs, tiles);
-  int max_split = ksteps / 8;
-  if (max_split < 1) max_split = 1;
-  if (ks > max_split) ks = max_split;
-  if (ks < 1) ks = 1;
-  while (ks > 1 && tiles * ks > kGemmMaxWgs) --ks;
-  return ks;
-}
-
 int check_cfg(const llmcad_config* c) {
   if (c == nullptr) return LLMCAD_EARG;
   if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->head_dim < 1 || c->d_ffn < 1 ||
@@ -114,7 +96,7 @@ struct Pass {
   hipStream_t st;
 };
 
-// Device facts for the persistent pass, looked up once per device.
+// Device facts for the pass, looked up once per device.
 struct DeviceInfo {
   int cus = 0;
 };
@@ -130,168 +112,7 @@ DeviceInfo device_info() {
   return cache[dev];
 }
 
-int run_pass_persistent(const Pass& a, const TreeArgs& tree);
-
 int run_pass(const Pass& a, const TreeArgs& tree) {
-  if (env_int("LLMCAD_PERSISTENT", 0) != 0) return run_pass_persistent(a, tree);
-  const Shape s(*a.cfg);
-  const PackedLayout P(s);
-  const WorkspaceLayout W(s, a.n);
-  const int Mp = W.Mp, MB = Mp / 16;
-  char* ws = a.ws;
-  float* x = (float*)(ws + W.x);
-  float* ssq = (float*)(ws + W.ssq);
-  int* wtree = (int*)(ws + W.tree);
-  int* gemm_counters = (int*)(ws + W.counters);
-  int* attn_counters = gemm_counters + W.n_gemm_counters;
-  int* lm_counter = attn_counters + W.n_attn_counters;
-  const float eps = a.cfg->rms_eps;
-  const float log2_theta = (float)log2((double)a.cfg->rope_theta);
-  const LaunchTargets lt;
-
-  {
-    TimedLaunch tl(LLMCAD_KERNEL_EMBED, a.st);
-    HIP_TRY(launch_embed(tree, a.n, Mp, s.d, a.prefix_len, a.packed + P.embed, wtree, x, ssq, a.st));
-  }
-
-  const int total = a.prefix_len + a.n;
-  const int nchunks = cdiv(total, kAttnChunk);
-  int splits = cdiv(lt.attn_wgs, s.H);
-  if (splits > attn_max_splits(s.H)) splits = attn_max_splits(s.H);
-  if (splits > nchunks) splits = nchunks;
-  if (splits < 1) splits = 1;
-
-  GemmParams base;
-  memset(&base, 0, sizeof(base));
-  base.n = a.n;
-  base.Mp = Mp;
-  base.part = (float*)(ws + W.gemm_part);
-  base.counters = gemm_counters;
-  base.x = x;
-  base.ssq = ssq;
-  base.ssq_tiles = s.d_tiles;
-  base.eps = eps;
-  base.inv_d = 1.0f / (float)s.d;
-  base.d = s.d;
-
-  const size_t kv_layer = (size_t)s.H * a.cap * s.Dh * 2;
-  for (int l = 0; l < s.L; ++l) {
-    const char* lw = a.packed + P.layer(l);
-    char* kc = a.k_cache + (size_t)l * kv_layer;
-    char* vc = a.v_cache + (size_t)l * kv_layer;
-
-    GemmParams g = base;  // QKV
-    g.w = lw + P.w_qkv;
-    g.ksteps = s.ks_d;
-    g.tiles = s.qkv_tiles;
-    g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
-    g.gain = lw + P.attn_norm;
-    g.q_out = ws + W.q;
-    g.k_cache = kc;
-    g.v_cache = vc;
-    g.cap = a.cap;
-    g.prefix_len = a.prefix_len;
-    g.H = s.H;
-    g.Dh = s.Dh;
-    g.pos = wtree + 384;
-    g.log2_theta = log2_theta;
-    {
-      TimedLaunch tl(LLMCAD_KERNEL_QKV, a.st);
-      HIP_TRY(launch_gemm(PRO_NORM, EPI_QKV, MB, g, a.st));
-    }
-
-    AttnParams at;
-    at.q = ws + W.q;
-    at.k_cache = kc;
-    at.v_cache = vc;
-    at.o_out = ws + W.o;
-    at.part_o = (float*)(ws + W.attn_o);
-    at.part_ml = (float*)(ws + W.attn_ml);
-    at.counters = attn_counters;
-    at.anc = (const uint32_t*)(wtree + 512);
-    at.n = a.n;
-    at.Mp = Mp;
-    at.H = s.H;
-    at.Dh = s.Dh;
-    at.cap = a.cap;
-    at.prefix_len = a.prefix_len;
-    at.splits = splits;
-    at.nchunks = nchunks;
-    at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.Dh));
-    {
-      TimedLaunch tl(LLMCAD_KERNEL_ATTENTION, a.st);
-      HIP_TRY(launch_attention(MB, at, a.st));
-    }
-
-    g = base;  // O projection + residual
-    g.w = lw + P.w_o;
-    g.ksteps = s.ks_d;
-    g.tiles = s.d_tiles;
-    g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
-    g.a = ws + W.o;
-    g.lda = s.d;
-    g.x_out = x;
-    g.ssq_out = ssq;
-    {
-      TimedLaunch tl(LLMCAD_KERNEL_O_PROJ, a.st);
-      HIP_TRY(launch_gemm(PRO_BF16, EPI_RESID, MB, g, a.st));
-    }
-
-    g = base;  // gate/up + SwiGLU
-    g.w = lw + P.w_gate_up;
-    g.ksteps = s.ks_d;
-    g.tiles = s.gu_tiles;
-    g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
-    g.gain = lw + P.ffn_norm;
-    g.h_out = ws + W.h;
-    g.ldh = s.Fp;
-    {
-      TimedLaunch tl(LLMCAD_KERNEL_GATE_UP, a.st);
-      HIP_TRY(launch_gemm(PRO_NORM, EPI_SWIGLU, MB, g, a.st));
-    }
-
-    g = base;  // down projection + residual
-    g.w = lw + P.w_down;
-    g.ksteps = s.ks_f;
-    g.tiles = s.d_tiles;
-    g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
-    g.a = ws + W.h;
-    g.lda = s.Fp;
-    g.x_out = x;
-    g.ssq_out = ssq;
-    {
-      TimedLaunch tl(LLMCAD_KERNEL_DOWN, a.st);
-      HIP_TRY(launch_gemm(PRO_BF16, EPI_RESID, MB, g, a.st));
-    }
-  }
-
-  GemmParams g = base;  // final norm + LM head + argmax + accept walk
-  g.w = a.packed + P.lm_head;
-  g.ksteps = s.ks_d;
-  g.tiles = s.v_tiles;
-  g.ksplit = choose_ksplit(lt, g.tiles, g.ksteps);
-  g.gain = a.packed + P.final_norm;
-  g.logits = a.logits;
-  g.V = s.V;
-  g.row_lo = a.row_lo;
-  g.lm_val = (float*)(ws + W.lm_val);
-  g.lm_idx = (int*)(ws + W.lm_idx);
-  g.lm_counter = lm_counter;
-  g.amax = (int*)(ws + W.amax);
-  g.tree_tok = wtree;
-  g.tree_parent = wtree + 128;
-  g.tree_depth = wtree + 256;
-  g.path = a.path;
-  g.accept_len = a.accept_len;
-  g.next_token = a.next_token;
-  {
-    TimedLaunch tl(LLMCAD_KERNEL_LM_HEAD, a.st);
-    HIP_TRY(launch_gemm(PRO_NORM, EPI_LOGITS, MB, g, a.st));
-  }
-  return LLMCAD_OK;
-}
-
-int run_pass_persistent(const Pass& a, const TreeArgs& tree) {
   const Shape s(*a.cfg);
   const PackedLayout P(s);
   const WorkspaceLayout W(s, a.n);
@@ -341,33 +162,36 @@ int run_pass_persistent(const Pass& a, const TreeArgs& tree) {
   p.o_down = (long long)P.w_down;
   p.ks_d = s.ks_d;
   p.ks_f = s.ks_f;
-  p.qkv_tiles = s.qkv_tiles;
-  p.d_tiles = s.d_tiles;
-  p.gu_tiles = s.gu_tiles;
-  p.v_tiles = s.v_tiles;
+  p.qkv_nb = s.qkv_nb;
+  p.d_nb = s.d_nb;
+  p.gu_nb = s.gu_nb;
+  p.v_nb = s.v_nb;
   p.k_cache = (bf16*)a.k_cache;
   p.v_cache = (bf16*)a.v_cache;
   p.tree = (int*)(ws + W.tree);
   p.x = (float*)(ws + W.xs);
   p.ssq = (float*)(ws + W.ssqs);
-  p.q = (bf16*)(ws + W.qs);
+  p.qk = (float*)(ws + W.qk);
   p.o = (bf16*)(ws + W.os);
   p.h = (bf16*)(ws + W.hs);
-  p.part = (float*)(ws + W.part_sk);
+  p.part = (float*)(ws + W.part);
   p.attn_o = (float*)(ws + W.attn_o);
   p.attn_ml = (float*)(ws + W.attn_ml);
+  // Position splits per head: enough (head, split) units for the grid, at
+  // least 16 positions each.
   const int T = a.prefix_len + a.n;
-  int S = G / s.H;
+  int S = env_int("LLMCAD_ATTN_SPLITS", G / s.H);
   if (S > kAttnMaxSplits) S = kAttnMaxSplits;
   if (S > cdiv(T, 16)) S = cdiv(T, 16);
+  if (s.H * S > G) S = G / s.H;
   if (S < 1) S = 1;
   p.attn_splits = S;
   p.tile_cnt = counters;
-  p.head_cnt = counters + W.n_gemm_counters;
-  p.lm_cnt = p.head_cnt + W.n_attn_counters;
+  p.head_cnt = counters + W.n_tile_counters;
+  p.lm_cnt = (int*)(ws + W.lm_cnt());
+  p.exit_cnt = (int*)(ws + W.exit_cnt());
+  p.status = (int*)(ws + W.status());
   p.bar = (int*)(ws + W.bar);
-  p.exit_cnt = p.lm_cnt + 1;
-  p.status = p.exit_cnt + 1;
   p.lm_val = (float*)(ws + W.lm_val);
   p.lm_idx = (int*)(ws + W.lm_idx);
   p.amax = (int*)(ws + W.amax);
@@ -406,8 +230,7 @@ int llmcad_pack_globals(const llmcad_config* cfg, const void* tok_embed, const v
   char* out = (char*)packed;
   HIP_TRY(hipMemcpyAsync(out + P.embed, tok_embed, (size_t)s.V * s.d * 2, hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipMemcpyAsync(out + P.final_norm, final_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(launch_pack(lm_head, s.V, s.d, out + P.lm_head, s.v_tiles, s.ks_d, PACK_PLAIN, s.H, s.Dh,
-                      s.F, st));
+  HIP_TRY(launch_pack(lm_head, s.V, s.d, out + P.lm_head, s.v_nb, s.ks_d, PACK_PLAIN, s.F, st));
   return LLMCAD_OK;
 }
 
@@ -426,14 +249,11 @@ int llmcad_pack_layer(const llmcad_config* cfg, int32_t layer, const llmcad_laye
   char* out = (char*)packed + P.layer(layer);
   HIP_TRY(hipMemcpyAsync(out + P.attn_norm, src->attn_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipMemcpyAsync(out + P.ffn_norm, src->ffn_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(launch_pack(src->w_qkv, 3 * s.d, s.d, out + P.w_qkv, s.qkv_tiles, s.ks_d, PACK_QKV_ROPE,
-                      s.H, s.Dh, s.F, st));
-  HIP_TRY(launch_pack(src->w_o, s.d, s.d, out + P.w_o, s.d_tiles, s.ks_d, PACK_PLAIN, s.H, s.Dh,
+  HIP_TRY(launch_pack(src->w_qkv, 3 * s.d, s.d, out + P.w_qkv, s.qkv_nb, s.ks_d, PACK_PLAIN, s.F, st));
+  HIP_TRY(launch_pack(src->w_o, s.d, s.d, out + P.w_o, s.d_nb, s.ks_d, PACK_PLAIN, s.F, st));
+  HIP_TRY(launch_pack(src->w_gate_up, 2 * s.F, s.d, out + P.w_gate_up, s.gu_nb, s.ks_d, PACK_GATE_UP,
                       s.F, st));
-  HIP_TRY(launch_pack(src->w_gate_up, 2 * s.F, s.d, out + P.w_gate_up, s.gu_tiles, s.ks_d,
-                      PACK_GATE_UP, s.H, s.Dh, s.F, st));
-  HIP_TRY(launch_pack(src->w_down, s.d, s.F, out + P.w_down, s.d_tiles, s.ks_f, PACK_PLAIN, s.H,
-                      s.Dh, s.F, st));
+  HIP_TRY(launch_pack(src->w_down, s.d, s.F, out + P.w_down, s.d_nb, s.ks_f, PACK_PLAIN, s.F, st));
   return LLMCAD_OK;
 }
 
@@ -450,7 +270,8 @@ int llmcad_workspace_init(const llmcad_config* cfg, int32_t max_n, void* workspa
   const WorkspaceLayout W(Shape(*cfg), max_n);
   if (workspace_bytes < W.total) return LLMCAD_EWORKSPACE;
   HIP_TRY(hipMemsetAsync((char*)workspace + W.counters, 0, W.counters_bytes, (hipStream_t)stream));
-  HIP_TRY(hipMemsetAsync((char*)workspace + W.bar, 0, 16 * 32 * 4, (hipStream_t)stream));
+  HIP_TRY(hipMemsetAsync((char*)workspace + W.bar, 0, (size_t)kBarSlots * kBarStride * 4,
+                          (hipStream_t)stream));
   return LLMCAD_OK;
 }
 
@@ -610,13 +431,13 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
   const Shape s(*cfg);
   const WorkspaceLayout W(s, max_n);
   switch (which) {
-    case 0: *offset = W.x; *bytes = (size_t)W.Mp * s.d * 4; break;
-    case 1: *offset = W.q; *bytes = (size_t)W.Mp * s.d * 2; break;
-    case 2: *offset = W.o; *bytes = (size_t)W.Mp * s.d * 2; break;
-    case 3: *offset = W.h; *bytes = (size_t)W.Mp * s.Fp * 2; break;
+    case 0: *offset = W.xs + (size_t)2 * s.L * W.Mp * s.d * 4; *bytes = (size_t)W.Mp * s.d * 4; break;
+    case 1: *offset = W.qk; *bytes = (size_t)W.Mp * 2 * s.d * 4; break;
+    case 2: *offset = W.os; *bytes = (size_t)W.Mp * s.d * 2; break;
+    case 3: *offset = W.hs; *bytes = (size_t)W.Mp * s.Fp * 2; break;
     case 4: *offset = W.amax; *bytes = (size_t)W.Mp * 4; break;
+    case 5: *offset = W.status(); *bytes = 4; break;
     case 6: *offset = W.trace; *bytes = (size_t)8 * (2 + 5 * s.L) * 6 * 8; break;
-    case 5: *offset = W.counters + (size_t)(W.n_gemm_counters + W.n_attn_counters + 2) * 4; *bytes = 4; break;
     default: return LLMCAD_EARG;
   }
   return LLMCAD_OK;

@@ -22,6 +22,18 @@ __device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Index of this thread's wavefront as a wave-uniform (scalar) value.  Every
+// guard of a matrix-core instruction must be uniform in this sense: a guard
+// the compiler sees as lane-divergent becomes an EXEC mask, the compiler may
+// drop the skip branch around a short masked block, and a matrix instruction
+// issued with EXEC all zero still updates its accumulator.
+__device__ __forceinline__ int wave_index() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+}
+// A value the caller knows is the same in every lane of the wave, made
+// scalar so that branches on it are scalar branches.
+__device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 __device__ __forceinline__ float bf2f(bf16 x) { return (float)x; }
 __device__ __forceinline__ bf16 f2bf(float x) { return (bf16)x; }  // round to nearest even
 

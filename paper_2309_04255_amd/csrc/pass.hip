@@ -1,32 +1,37 @@
 // The whole verification pass (§3.2 of arXiv 2309.04255) as one persistent
 // launch.
 //
-// Why one launch: a pass is a chain of ~5 dependent steps per layer, each
-// streaming tens to hundreds of MB of weights.  As separate kernels every step
-// pays a ramp-up and a drain; here every workgroup (one per CU, all resident:
-// cooperative launch) walks the phases in order and meets the others at a
-// grid barrier between phases.  Weights never depend on the previous phase,
-// so each workgroup issues the first weight loads of its next phase *before*
-// waiting at the barrier, and HBM keeps streaming while the barrier settles.
+// Why one launch: a pass is a chain of five dependent steps per layer, each
+// streaming tens to hundreds of MB of weights.  As separate kernels every
+// step pays a ramp-up and a drain; here every workgroup (one per CU, all
+// resident: cooperative launch) walks the phases in order and meets the
+// others at a grid barrier between phases.  Weights never depend on the
+// previous phase, so each workgroup issues the first weight loads of its next
+// phase before waiting at the barrier, and HBM keeps streaming meanwhile.
 //
-// Phases: embed + tree prep; per layer QKV (+RMSNorm, rotary, KV write) ->
-// tree attention -> O (+residual) -> gate/up (+RMSNorm, SwiGLU) -> down
-// (+residual); then final RMSNorm + LM head + argmax, and the accept walk in
-// the last tile to finish.
+// Phases: embed + tree prep; per layer QKV projection (RMSNorm prologue) ->
+// tree attention (rotary embedding at each node's position, ancestor mask) ->
+// O projection (+residual) -> gate/up (RMSNorm prologue, SwiGLU epilogue) ->
+// down projection (+residual); then final RMSNorm + LM head + argmax, and the
+// accept walk in the workgroup that completes the argmax.
 //
-// GEMM phases are stream-K: the (64-column tile, 32-wide k-step) grid of a
-// matrix is cut into G equal contiguous runs, one per workgroup, so every
-// workgroup streams the same number of weight bytes.  A tile covered by
-// several runs is finished by the last contributor, which adds the partials
-// in k order (bit-reproducible).
+// GEMM phases: the output columns are 16-wide n-blocks (one MFMA each).
+// Workgroup g owns c = N_blocks / G whole n-blocks over the full K, so its
+// epilogue needs nothing from other workgroups; the remaining R = N_blocks mod
+// G n-blocks are shared stream-K style (every workgroup gets an equal run of
+// their k-steps), finished by the last contributor, which adds the partials
+// in k order (bit-reproducible).  Runs over the remainder come first so their
+// hand-off latency overlaps the main block's streaming.  Inside a workgroup
+// the four waves take interleaved k-steps and their partial sums are added in
+// LDS in a fixed order.
 //
 // Coherence without cache maintenance: every buffer handed from one phase to
 // the next is written once per pass at its own address with device-coherent
-// stores and read after the barrier with ordinary (cacheable) loads, so no L2
-// can hold an older copy; buffers reused within a pass (partials) are read
-// with device-coherent loads.  Barriers and per-head joins are monotonic
-// counters polled with bounded spins: a wait that exceeds its bound records
-// an error status and the workgroup leaves the pass, so no wave can hang.
+// stores and read after the barrier with ordinary loads, so no L2 can hold an
+// older copy; buffers reused within a pass (partials) are read with
+// device-coherent loads.  Barriers and per-head joins are counters polled
+// with bounded spins: a wait that exceeds its bound records an error status
+// and the workgroup leaves the pass, so no wave can hang.
 #include <math.h>
 
 #include "device.h"
@@ -39,6 +44,10 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
+
+// How a GEMM phase forms its A operand, and what its epilogue does.
+enum Prologue { PRO_BF16 = 0, PRO_NORM = 1 };  // bf16 activations | RMSNorm of fp32 x
+enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 constexpr int kTraceWgs = 8;  // workgroups that record phase timestamps
 
 __device__ __forceinline__ void st_coherent_bf2(bf16* p, float a, float b) {  // p 4-byte aligned
@@ -47,32 +56,27 @@ __device__ __forceinline__ void st_coherent_bf2(bf16* p, float a, float b) {  //
   __hip_atomic_store((uint32_t*)p, lo | (hi << 16), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// ------------------------------------------------------------------ barrier
+// ------------------------------------------------------------------ sync
 
 struct Sync {
   int* bar;
   int* status;
   int limit;
   int* lds_flag;
-  long long* trace;  // [phase][3] timestamps of this workgroup, or null
+  long long* trace;  // [phase][6] timestamps of this workgroup, or null
 };
 
-// Diagnostics: wall-clock (100 MHz) marks per phase: 0 = barrier wait entered,
-// 1 = wait over, 2 = phase work done; GEMM phases also mark 3 = operand
-// prologue done, 4 = weight streaming of the last segment done, 5 = last
-// epilogue done.
+// Diagnostics: wall-clock (100 MHz) marks per phase: 0 = barrier wait
+// entered, 1 = wait over, 2 = phase work done; GEMM phases also mark 3 =
+// operand prologue done, 4 = weight streaming of the last segment done,
+// 5 = last epilogue done.
 __device__ __forceinline__ void trace_mark(const Sync& s, int phase, int k) {
   if (s.trace != nullptr && threadIdx.x == 0) s.trace[phase * 6 + k] = (long long)wall_clock64();
 }
 
-// The grid barrier is spread over kBarSlots counters (one per 128-byte line)
-// so that arrivals do not serialise on one address: workgroup g counts on
-// slot g % kBarSlots, and a waiter polls all slots with one wave.
-constexpr int kBarSlots = 16;
-constexpr int kBarStride = 32;  // ints between slots
-
-// Arrival at the end of a phase: this workgroup's stores are complete, then
-// one device-scope increment.
+// End of a phase: this workgroup's stores have completed, then one
+// device-scope increment on its barrier counter (workgroup g counts on
+// counter g % kBarSlots, so arrivals do not serialise on one address).
 __device__ __forceinline__ void grid_arrive(const Sync& s, int phase) {
   trace_mark(s, phase, 2);
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -83,15 +87,15 @@ __device__ __forceinline__ void grid_arrive(const Sync& s, int phase) {
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Waits until every barrier slot has seen `phase` arrivals from each of its
-// workgroups; false (to all threads) if the bounded spin ran out.
+// Waits until all G workgroups have arrived `phase` times; one wave polls all
+// counters.  False (to all threads) if the bounded spin ran out.
 __device__ __forceinline__ bool grid_wait(const Sync& s, int phase, int G) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
     const int slots = G < kBarSlots ? G : kBarSlots;
     const int per = G / kBarSlots + (lane < G % kBarSlots ? 1 : 0);
     const int want = lane < slots ? phase * (G < kBarSlots ? 1 : per) : 0;
-    int* slot = s.bar + (lane < slots ? lane : 0) * kBarStride;
+    const int* slot = s.bar + (lane < slots ? lane : 0) * kBarStride;
     int ok = 1, spins = 0;
     while (true) {
       const int v = lane < slots ? ld_coherent(slot) : 0;
@@ -111,12 +115,12 @@ __device__ __forceinline__ bool grid_wait(const Sync& s, int phase, int G) {
   return ok;
 }
 
-// Waits until *c >= target; false (to all threads) if the bounded spin ran out.
-__device__ __forceinline__ bool wait_at_least(const Sync& s, int* c, int target) {
+// Waits until *c >= target (one poller); false if the bounded spin ran out.
+__device__ __forceinline__ bool wait_at_least(const Sync& s, const int* c, int target) {
   if (threadIdx.x == 0) {
     int ok = 1, spins = 0;
     while (ld_coherent(c) < target) {
-      __builtin_amdgcn_s_sleep(2);
+      __builtin_amdgcn_s_sleep(1);
       if (++spins > s.limit) {
         st_coherent(s.status, 1);
         ok = 0;
@@ -134,14 +138,24 @@ __device__ __forceinline__ bool wait_at_least(const Sync& s, int* c, int target)
 // ------------------------------------------------------------------ GEMM
 
 struct GemmDesc {
-  const bf16x8* w;  // packed matrix
-  int tiles, ks;    // 64-column tiles, 32-wide k-steps per tile
-  // A operand
-  const bf16* a;    // PRO_BF16: [Mp][lda]
+  const bf16x8* w;   // packed matrix, n-block major
+  int nbt, ks;       // n-blocks, k-steps per n-block
+  const bf16* a;     // PRO_BF16: [Mp][lda]
   int lda;
-  const float* x;   // PRO_NORM: [Mp][d]
-  const float* ssq; // PRO_NORM: [d/64][Mp]
-  const bf16* gain; // PRO_NORM: [d]
+  const float* x;    // PRO_NORM: [Mp][d]
+  const float* ssq;  // PRO_NORM: [d/16][Mp]
+  const bf16* gain;  // PRO_NORM: [d]
+};
+
+struct EpiArgs {
+  float* qk;          // EPI_QKV: [Mp][2d] q then k, before the rotary embedding
+  bf16* vc;           // EPI_QKV: V cache of this layer [H][cap][Dh]
+  const float* x_in;  // EPI_RESID: [Mp][d]
+  float* x_out;       // EPI_RESID: [Mp][d]
+  float* ssq_out;     // EPI_RESID: [d/16][Mp]
+  bf16* h;            // EPI_SWIGLU: [Mp][Fp]
+  float* logits;      // EPI_LOGITS: rows [row_lo, n), or null
+  int row_lo;
 };
 
 template <int MB, int PRO>
@@ -156,35 +170,46 @@ struct AStage<MB, PRO_NORM> {
   bf16x8 g;
 };
 
-template <int MB, int PRO, int D>
+// Register pipeline depth: ~192 VGPRs of stages, 2..16 k-steps.
+template <int MB, int PRO, int C>
+constexpr int pipe_depth() {
+  constexpr int per = 4 * C + (PRO == PRO_BF16 ? 4 * MB : 8 * MB + 4);
+  constexpr int d = 192 / per;
+  return d < 2 ? 2 : (d > 16 ? 16 : d);
+}
+
+template <int MB, int PRO, int C>
 struct Pipe {
-  bf16x8 bw[D][4];
+  static constexpr int D = pipe_depth<MB, PRO, C>();
+  bf16x8 bw[D][C];
   AStage<MB, PRO> as[D];
-  const bf16x8* wt;  // tile base + lane
-  int s0, ns;        // this wave's first k-step, number of k-steps
+  const bf16x8* wt;  // first n-block's blocks + lane
+  int ks;            // blocks between consecutive n-blocks
+  int s0, ns;        // this wave's first k-step and number of k-steps
 };
 
-template <int MB, int PRO, int D>
-__device__ __forceinline__ void pipe_setup(Pipe<MB, PRO, D>& P, const GemmDesc& g, int tile, int k0,
+template <int MB, int PRO, int C>
+__device__ __forceinline__ void pipe_setup(Pipe<MB, PRO, C>& P, const GemmDesc& g, int nb0, int k0,
                                            int k1) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  P.wt = g.w + (size_t)tile * g.ks * 256 + lane;
-  P.s0 = k0 + wave;
-  P.ns = P.s0 < k1 ? (k1 - P.s0 + kWaves - 1) / kWaves : 0;
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  P.wt = g.w + (size_t)nb0 * g.ks * 64 + lane;
+  P.ks = g.ks;
+  P.s0 = wave_uniform(k0 + wave);
+  P.ns = wave_uniform(P.s0 < k1 ? (k1 - P.s0 + kWaves - 1) / kWaves : 0);
 }
 
-template <int MB, int PRO, int D>
-__device__ __forceinline__ void pipe_load_b(Pipe<MB, PRO, D>& P, int slot, int i) {
+template <int MB, int PRO, int C>
+__device__ __forceinline__ void pipe_load_b(Pipe<MB, PRO, C>& P, int slot, int i) {
   const int s = P.s0 + kWaves * i;
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) P.bw[slot][nb] = P.wt[(size_t)s * 256 + nb * 64];
+  for (int c = 0; c < C; ++c) P.bw[slot][c] = P.wt[((size_t)c * P.ks + s) * 64];
 }
 
-template <int MB, int PRO, int D>
-__device__ __forceinline__ void pipe_load_a(Pipe<MB, PRO, D>& P, const GemmDesc& g, int d, int slot,
+template <int MB, int PRO, int C>
+__device__ __forceinline__ void pipe_load_a(Pipe<MB, PRO, C>& P, const GemmDesc& g, int d, int slot,
                                             int i) {
   const int lane = threadIdx.x & 63, lrow = lane & 15, kg = lane >> 4;
-  const int k = 32 * (P.s0 + kWaves * i) + 8 * kg;
+  const int k = kStepK * (P.s0 + kWaves * i) + 8 * kg;
   if constexpr (PRO == PRO_BF16) {
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb)
@@ -200,8 +225,8 @@ __device__ __forceinline__ void pipe_load_a(Pipe<MB, PRO, D>& P, const GemmDesc&
   }
 }
 
-template <int MB, int PRO, int D>
-__device__ __forceinline__ void pipe_compute(Pipe<MB, PRO, D>& P, int slot, f32x4 (&acc)[MB][4],
+template <int MB, int PRO, int C>
+__device__ __forceinline__ void pipe_compute(Pipe<MB, PRO, C>& P, int slot, f32x4 (&acc)[MB][C],
                                              const float (&rstd)[MB]) {
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb) {
@@ -216,25 +241,30 @@ __device__ __forceinline__ void pipe_compute(Pipe<MB, PRO, D>& P, int slot, f32x
       for (int e = 0; e < 8; ++e) a[e] = f2bf(xs[e] * rstd[rb] * bf2f(P.as[slot].g[e]));
     }
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) acc[rb][nb] = mfma16x16x32(a, P.bw[slot][nb], acc[rb][nb]);
+    for (int c = 0; c < C; ++c) acc[rb][c] = mfma16x16x32(a, P.bw[slot][c], acc[rb][c]);
   }
 }
 
-// Runs the wave's k-steps.  If b_ready, the first D weight stages were issued
-// before (across a barrier).  Loads are issued unconditionally (clamped to the
-// last step) so the number in flight is the same on every path.
-template <int MB, int PRO, int D>
-__device__ __forceinline__ void pipe_run(Pipe<MB, PRO, D>& P, const GemmDesc& g, int d, bool b_ready,
-                                         f32x4 (&acc)[MB][4], const float (&rstd)[MB]) {
+// Issues the first D weight stages (done before a barrier for the first segment).
+template <int MB, int PRO, int C>
+__device__ __forceinline__ void pipe_prefetch_b(Pipe<MB, PRO, C>& P) {
+  if (P.ns == 0) return;
+#pragma unroll
+  for (int u = 0; u < Pipe<MB, PRO, C>::D; ++u) pipe_load_b(P, u, u < P.ns ? u : P.ns - 1);
+}
+
+// Runs the wave's k-steps.  Loads are issued unconditionally (clamped to the
+// last step) so that the number in flight is the same on every path.
+template <int MB, int PRO, int C>
+__device__ __forceinline__ void pipe_run(Pipe<MB, PRO, C>& P, const GemmDesc& g, int d, bool b_ready,
+                                         f32x4 (&acc)[MB][C], const float (&rstd)[MB]) {
+  constexpr int D = Pipe<MB, PRO, C>::D;
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) acc[rb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < C; ++c) acc[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (P.ns == 0) return;
-  if (!b_ready) {
-#pragma unroll
-    for (int u = 0; u < D; ++u) pipe_load_b(P, u, u < P.ns ? u : P.ns - 1);
-  }
+  if (!b_ready) pipe_prefetch_b(P);
 #pragma unroll
   for (int u = 0; u < D; ++u) pipe_load_a(P, g, d, u, u < P.ns ? u : P.ns - 1);
   for (int i = 0; i < P.ns; i += D) {
@@ -248,20 +278,21 @@ __device__ __forceinline__ void pipe_run(Pipe<MB, PRO, D>& P, const GemmDesc& g,
   }
 }
 
-// Sum the waves' partial tiles into tileS (fixed wave order).
-template <int MB>
-__device__ __forceinline__ void reduce_waves(float (*tileS)[68], const f32x4 (&acc)[MB][4]) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lrow = lane & 15, kg = lane >> 4;
+// Sum the waves' partial tiles into tileS [16 MB][16 C (+4)] in wave order.
+template <int MB, int C>
+__device__ __forceinline__ void reduce_waves(float* tileS, const f32x4 (&acc)[MB][C]) {
+  constexpr int TS = 16 * C + 4;
+  const int wave = wave_index(), lane = threadIdx.x & 63, lrow = lane & 15, kg = lane >> 4;
   for (int w = 0; w < kWaves; ++w) {
     if (wave == w) {
 #pragma unroll
       for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
+        for (int c = 0; c < C; ++c)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            float* dst = &tileS[16 * rb + 4 * kg + i][16 * nb + lrow];
-            *dst = (w == 0) ? acc[rb][nb][i] : *dst + acc[rb][nb][i];
+            float* dst = &tileS[(16 * rb + 4 * kg + i) * TS + 16 * c + lrow];
+            *dst = (w == 0) ? acc[rb][c][i] : *dst + acc[rb][c][i];
           }
     }
     __syncthreads();
@@ -273,74 +304,256 @@ __device__ __forceinline__ int owner_of(long q, long W, int G) {
   return (int)(((q + 1) * G + W - 1) / W) - 1;
 }
 
-// ------------------------------------------------------------------ epilogues
-
-struct EpiQkv {
-  bf16* q;        // [Mp][d]
-  bf16* kc;       // [H][cap][Dh] of this layer
-  bf16* vc;
-  const int* pos; // [n]
-};
-struct EpiResid {
-  const float* x_in;  // [Mp][d]
-  float* x_out;       // [Mp][d]
-  float* ssq_out;     // [d/64][Mp]
-};
-struct EpiSwiglu {
-  bf16* h;  // [Mp][Fp]
-};
-struct EpiLogits {
-  float* logits;
-  int row_lo;
-};
-
-}  // namespace
-
-namespace {
-
-template <int MB>
-struct PassLds {
-  float tileS[MB * 16][68];
-  float part_ss[256 / (MB * 16) > 0 ? 256 / (MB * 16) : 1][MB * 16];
+struct GemmLds {
+  float part_ss[256];         // rstd prologue: [256 / ROWS][ROWS]
+  float red_v[kMaxNodes][8];  // argmax per (row, n-block)
+  int red_i[kMaxNodes][8];
   int reach[kMaxNodes];
   int amax[kMaxNodes];
+  float best_v[kMaxNodes];  // LM head: the workgroup's best column per row
+  int best_i[kMaxNodes];
 };
 
-// One GEMM phase.  Issues this workgroup's first weight loads, then waits for
-// `target` arrivals at the grid barrier, then runs its stream-K run.
-template <int MB, int PRO, int EPI, int D>
-__device__ __forceinline__ bool gemm_phase(const PassParams& p, const GemmDesc& g, const Sync& sy,
-                                           int target, PassLds<MB>& lds, int layer, const void* epi) {
-  constexpr int ROWS = MB * 16;
-  const int G = p.G;
-  const long W = (long)g.tiles * g.ks;
-  const long begin = (long)blockIdx.x * W / G, end = (long)(blockIdx.x + 1) * W / G;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lrow = lane & 15;
-
-  Pipe<MB, PRO, D> P;
-  long pos = begin;
-  if (pos < end) {
-    const int t = (int)(pos / g.ks), k0 = (int)(pos % g.ks);
-    const int k1 = (int)((long)k0 + (end - pos) < g.ks ? k0 + (end - pos) : g.ks);
-    pipe_setup(P, g, t, k0, k1);
-    if (P.ns > 0) {
+// Epilogue of C n-blocks [nb0, nb0 + C) held in tileS: writes the phase's
+// outputs with device-coherent stores.  lm_entry: argmax partial slot.
+template <int MB, int EPI, int C>
+__device__ __forceinline__ void epilogue(const PassParams& p, const EpiArgs& e, float* tileS, int nb0,
+                                         int lm_entry, GemmLds& gl) {
+  constexpr int ROWS = 16 * MB, COLS = 16 * C, TS = COLS + 4;
+  const int lane = threadIdx.x & 63;
+  if constexpr (EPI == EPI_QKV) {
+    const int d = p.d;
+    for (int idx = threadIdx.x; idx < ROWS * COLS; idx += kThreads) {
+      const int r = idx / COLS, cc = idx % COLS;
+      const int col = kNB * nb0 + cc;
+      const float v = tileS[r * TS + cc];
+      const float nxt = __shfl_down(v, 1, kWave);
+      if (r >= p.n) continue;
+      if (col < 2 * d) {
+        st_coherent(&e.qk[(size_t)r * 2 * d + col], v);
+      } else if ((cc & 1) == 0) {
+        const int j = col - 2 * d, hh = j / p.Dh, dd = j % p.Dh;
+        st_coherent_bf2(e.vc + ((size_t)hh * p.cap + p.prefix_len + r) * p.Dh + dd, v, nxt);
+      }
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    for (int idx = threadIdx.x; idx < ROWS * COLS; idx += kThreads) {
+      const int r = idx / COLS, cc = idx % COLS;
+      const int col = kNB * nb0 + cc;
+      float xn = 0.0f;
+      if (r < p.n) {
+        xn = e.x_in[(size_t)r * p.d + col] + tileS[r * TS + cc];
+        st_coherent(&e.x_out[(size_t)r * p.d + col], xn);
+      }
+      // sum of squares over the 16 columns of this n-block (16 consecutive lanes)
+      float s = xn * xn;
+      s += __shfl_xor(s, 8, kWave);
+      s += __shfl_xor(s, 4, kWave);
+      s += __shfl_xor(s, 2, kWave);
+      s += __shfl_xor(s, 1, kWave);
+      if ((lane & 15) == 0) st_coherent(&e.ssq_out[(size_t)(nb0 + cc / kNB) * p.Mp + r], s);
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    for (int idx = threadIdx.x; idx < ROWS * C * 8; idx += kThreads) {
+      const int r = idx / (C * 8), rem = idx % (C * 8), i = rem / 8, j = rem % 8;
+      const float gt = tileS[r * TS + kNB * i + j], up = tileS[r * TS + kNB * i + 8 + j];
+      const float hv = gt / (1.0f + expf(-gt)) * up;
+      const float nxt = __shfl_down(hv, 1, kWave);
+      if (r < p.n && (j & 1) == 0) st_coherent_bf2(e.h + (size_t)r * p.Fp + 8 * (nb0 + i) + j, hv, nxt);
+    }
+  } else {  // EPI_LOGITS
+    for (int idx = threadIdx.x; idx < ROWS * COLS; idx += kThreads) {
+      const int r = idx / COLS, cc = idx % COLS;
+      const int col = kNB * nb0 + cc;
+      const bool valid = r < p.n && col < p.V;
+      const float v = tileS[r * TS + cc];
+      if (valid && e.logits != nullptr && r >= e.row_lo) e.logits[(size_t)(r - e.row_lo) * p.V + col] = v;
+      float mv = valid ? v : -INFINITY;
+      int mi = valid ? col : 0x7fffffff;
 #pragma unroll
-      for (int u = 0; u < D; ++u) pipe_load_b(P, u, u < P.ns ? u : P.ns - 1);
+      for (int off = 8; off >= 1; off >>= 1) {  // argmax over the n-block's 16 columns
+        const float ov = __shfl_xor(mv, off, kWave);
+        const int oi = __shfl_xor(mi, off, kWave);
+        if (ov > mv || (ov == mv && oi < mi)) {
+          mv = ov;
+          mi = oi;
+        }
+      }
+      if ((lane & 15) == 0) {
+        gl.red_v[r][cc / kNB] = mv;
+        gl.red_i[r][cc / kNB] = mi;
+      }
+    }
+    __syncthreads();
+    for (int r = threadIdx.x; r < ROWS; r += kThreads) {
+      float mv = -INFINITY;
+      int mi = 0x7fffffff;
+      for (int c = 0; c < C; ++c) {
+        const float v = gl.red_v[r][c];
+        const int i = gl.red_i[r][c];
+        if (v > mv || (v == mv && i < mi)) {
+          mv = v;
+          mi = i;
+        }
+      }
+      if (lm_entry >= 0) {  // a remainder n-block: its own argmax entry
+        st_coherent(&p.lm_val[(size_t)lm_entry * p.Mp + r], mv);
+        st_coherent(&p.lm_idx[(size_t)lm_entry * p.Mp + r], mi);
+      } else if (lm_entry == -2 || mv > gl.best_v[r] || (mv == gl.best_v[r] && mi < gl.best_i[r])) {
+        gl.best_v[r] = mv;  // main block: best over its sub-blocks (-2: first sub-block)
+        gl.best_i[r] = mi;
+      }
     }
   }
-  trace_mark(sy, target / p.G, 0);
-  if (!grid_wait(sy, target / p.G, p.G)) return false;
-  trace_mark(sy, target / p.G, 1);
+}
+
+// After all argmax partials are in: greedy token per node and the accept walk
+// (§3.2): node i is reachable when its parent is and its draft token equals
+// the target's token after the parent; the result is the deepest reachable
+// node (lowest index among equally deep ones).
+__device__ __forceinline__ void finish_walk(const PassParams& p, int entries, GemmLds& gl) {
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  for (int r = wave; r < p.n; r += kWaves) {
+    float mv = -INFINITY;
+    int mi = 0x7fffffff;
+    for (int t0 = 0; t0 < entries; t0 += 4 * 64) {
+      float v[4];
+      int ix[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int t = t0 + 64 * u + lane;
+        v[u] = t < entries ? ld_coherent(&p.lm_val[(size_t)t * p.Mp + r]) : -INFINITY;
+        ix[u] = t < entries ? ld_coherent(&p.lm_idx[(size_t)t * p.Mp + r]) : 0x7fffffff;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (v[u] > mv || (v[u] == mv && ix[u] < mi)) {
+          mv = v[u];
+          mi = ix[u];
+        }
+    }
+    wave_argmax(mv, mi);
+    if (lane == 0) {
+      p.amax[r] = mi;
+      gl.amax[r] = mi;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int* tok = p.tree;
+    const int* par = p.tree + 128;
+    const int* dep = p.tree + 256;
+    int best = 0, best_depth = 0;
+    gl.reach[0] = 1;
+    for (int i = 1; i < p.n; ++i) {
+      const int pr = par[i];
+      const int ok = gl.reach[pr] && (tok[i] == gl.amax[pr]);
+      gl.reach[i] = ok;
+      if (ok && dep[i] > best_depth) {
+        best = i;
+        best_depth = dep[i];
+      }
+    }
+    for (int k = 0; k < p.n; ++k) p.path[k] = -1;
+    for (int i = best; i >= 0; i = par[i]) p.path[dep[i]] = i;
+    *p.accept_len = best_depth;
+    *p.next_token = gl.amax[best];
+  }
+  __syncthreads();
+}
+
+// Warms L2 with the first 16 KiB of weights each wave will read: blocks of
+// n-blocks [nb0, nb0 + nbs) at the wave's k-steps k0 + wave, + 4, ... (< k1),
+// in the order the pipeline consumes them, so that HBM keeps streaming while
+// the workgroup waits at a barrier.  The loaded values are folded into a
+// token after the wait (prefetch_fold) so the loads stay live.
+struct Prefetch {
+  bf16x8 v[16];
+};
+__device__ __forceinline__ void l2_prefetch(Prefetch& pf, const bf16x8* w, int ks, int nb0, int nbs,
+                                            int k0, int k1) {
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  const int s0 = k0 + wave;
+  const int ns = s0 < k1 ? (k1 - s0 + kWaves - 1) / kWaves : 0;
+  const int total = ns * nbs;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int it = i < total ? i : (total > 0 ? total - 1 : 0);
+    const int c = it % nbs, s = s0 + kWaves * (it / nbs);
+    const size_t blk = total > 0 ? ((size_t)(nb0 + c) * ks + s) : 0;
+    pf.v[i] = w[blk * 64 + lane];
+  }
+}
+__device__ __forceinline__ uint32_t prefetch_fold(const Prefetch& pf) {
+  uint32_t tok = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) tok ^= __builtin_bit_cast(uint32_t, (__bf16 __attribute__((ext_vector_type(2)))){pf.v[i][0], pf.v[i][1]});
+  return tok;
+}
+
+// Main-block widths: the largest allowed width <= remaining.
+template <int EPI>
+__device__ __forceinline__ int next_width(int rem) {
+  if (rem >= 4) return 4;
+  if (EPI == EPI_QKV && rem == 3) return 3;
+  if (rem >= 2) return 2;
+  return 1;
+}
+
+template <int MB, int PRO, int EPI, int CM>
+__device__ __forceinline__ void main_subblock(const PassParams& p, const GemmDesc& g, const EpiArgs& e,
+                                              int nb0, const float (&rstd)[MB], float* tileS,
+                                              GemmLds& gl, int lm_entry) {
+  Pipe<MB, PRO, CM> P;
+  pipe_setup(P, g, nb0, 0, g.ks);
+  f32x4 acc[MB][CM];
+  pipe_run(P, g, p.d, false, acc, rstd);
+  reduce_waves<MB, CM>(tileS, acc);
+  epilogue<MB, EPI, CM>(p, e, tileS, nb0, lm_entry, gl);
+  __syncthreads();
+}
+
+// One GEMM phase: warm L2 with the first weights, wait at the barrier, then
+// the remainder runs (stream-K, one n-block per segment) and the main block
+// (whole n-blocks over the full K, in sub-blocks of 4, 3, 2 or 1 n-blocks).
+template <int MB, int PRO, int EPI>
+__device__ __attribute__((noinline)) bool gemm_phase(const PassParams& p, const GemmDesc& g,
+                                                     const EpiArgs& e, const Sync& sy, int phase,
+                                                     float* tileS, GemmLds& gl) {
+  constexpr int ROWS = 16 * MB;
+  const int G = p.G, gi = blockIdx.x;
+  const int c = g.nbt / G, R = g.nbt - c * G;
+  const long Wr = (long)R * g.ks;
+  const long rbeg = (long)gi * Wr / G, rend = (long)(gi + 1) * Wr / G;
+  const int lrow = (threadIdx.x & 63) & 15;
+
+  {
+    Prefetch pf;
+    if (rbeg < rend) {
+      const int t = (int)(rbeg / g.ks), k0 = (int)(rbeg % g.ks);
+      const int k1 = (int)(k0 + (rend - rbeg) < g.ks ? k0 + (rend - rbeg) : g.ks);
+      l2_prefetch(pf, g.w, g.ks, c * G + t, 1, k0, k1);
+    } else if (c > 0) {
+      l2_prefetch(pf, g.w, g.ks, gi * c, next_width<EPI>(c), 0, g.ks);
+    } else {
+      l2_prefetch(pf, g.w, g.ks, 0, 1, 0, 0);
+    }
+    trace_mark(sy, phase, 0);
+    if (!grid_wait(sy, phase, G)) return false;
+    trace_mark(sy, phase, 1);
+    const uint32_t tok = prefetch_fold(pf);
+    if (tok == 0x9e3779b9u && p.G < 0) p.status[1] = (int)tok;  // keeps the prefetch loads
+  }
 
   float rstd[MB];
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb) rstd[rb] = 1.0f;
   if constexpr (PRO == PRO_NORM) {
-    constexpr int CH = 256 / ROWS;
-    const int dt = p.d_tiles;
-    if (threadIdx.x < CH * ROWS) {
-      const int r = threadIdx.x % ROWS, c = threadIdx.x / ROWS;
-      const int t0 = c * dt / CH, t1 = (c + 1) * dt / CH;
+    constexpr int CHK = 256 / ROWS;
+    const int dn = p.d_nb;
+    if (threadIdx.x < CHK * ROWS) {
+      const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
+      const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
       float ss = 0.0f;
       int t = t0;
       for (; t + 4 <= t1; t += 4) {
@@ -352,7 +565,7 @@ __device__ __forceinline__ bool gemm_phase(const PassParams& p, const GemmDesc& 
         ss += v3;
       }
       for (; t < t1; ++t) ss += g.ssq[(size_t)t * p.Mp + r];
-      lds.part_ss[c][r] = ss;
+      gl.part_ss[ch * ROWS + r] = ss;
     }
     __syncthreads();
 #pragma unroll
@@ -360,258 +573,223 @@ __device__ __forceinline__ bool gemm_phase(const PassParams& p, const GemmDesc& 
       const int row = 16 * rb + lrow;
       float ss = 0.0f;
 #pragma unroll
-      for (int c = 0; c < CH; ++c) ss += lds.part_ss[c][row];
+      for (int ch = 0; ch < CHK; ++ch) ss += gl.part_ss[ch * ROWS + row];
       rstd[rb] = 1.0f / sqrtf(ss * p.inv_d + p.eps);
     }
   }
+  trace_mark(sy, phase, 3);
 
-  const int ph = target / G;
-  trace_mark(sy, ph, 3);
-  bool first = true;
-  while (pos < end) {
+  // Remainder n-blocks (stream-K), one n-block per segment.
+  for (long pos = rbeg; pos < rend;) {
     const int t = (int)(pos / g.ks), k0 = (int)(pos % g.ks);
-    const int k1 = (int)((long)k0 + (end - pos) < g.ks ? k0 + (end - pos) : g.ks);
-    if (!first) pipe_setup(P, g, t, k0, k1);
-    f32x4 acc[MB][4];
-    pipe_run(P, g, p.d, first, acc, rstd);
-    trace_mark(sy, ph, 4);
-    reduce_waves<MB>(lds.tileS, acc);
+    const int k1 = (int)(k0 + (rend - pos) < g.ks ? k0 + (rend - pos) : g.ks);
+    const int nb = c * G + t;
+    {
+      Pipe<MB, PRO, 1> P1;
+      pipe_setup(P1, g, nb, k0, k1);
+      f32x4 acc[MB][1];
+      pipe_run(P1, g, p.d, false, acc, rstd);
+      reduce_waves<MB, 1>(tileS, acc);
+    }
+    constexpr int TS = 16 + 4;
     bool finish = true;
     if (!(k0 == 0 && k1 == g.ks)) {
-      // Partial tile: store it, count the arrival, the last contributor sums.
-      const int slot = (pos == begin) ? 0 : 1;
-      float* mine = p.part + ((size_t)blockIdx.x * 2 + slot) * ROWS * 64;
-      for (int idx = 2 * threadIdx.x; idx < ROWS * 64; idx += 512)
-        st_coherent2(mine + idx, lds.tileS[idx >> 6][idx & 63], lds.tileS[idx >> 6][(idx & 63) + 1]);
+      const int slot = (pos == rbeg) ? 0 : 1;
+      float* mine = p.part + ((size_t)gi * 2 + slot) * ROWS * kNB;
+      for (int idx = 2 * threadIdx.x; idx < ROWS * kNB; idx += 2 * kThreads)
+        st_coherent2(mine + idx, tileS[(idx / kNB) * TS + idx % kNB], tileS[(idx / kNB) * TS + idx % kNB + 1]);
       const long tile_lo = (long)t * g.ks, tile_hi = tile_lo + g.ks - 1;
-      const int g_lo = owner_of(tile_lo, W, G), g_hi = owner_of(tile_hi, W, G);
-      int contributors = 0;  // workgroups with a non-empty run inside the tile
+      const int g_lo = owner_of(tile_lo, Wr, G), g_hi = owner_of(tile_hi, Wr, G);
+      int contributors = 0;
       for (int gg = g_lo; gg <= g_hi; ++gg)
-        contributors += ((long)gg * W / G < (long)(gg + 1) * W / G) ? 1 : 0;
-      finish = arrive_last(&p.tile_cnt[t], contributors, sy.lds_flag);
+        contributors += ((long)gg * Wr / G < (long)(gg + 1) * Wr / G) ? 1 : 0;
+      finish = arrive_last(&p.tile_cnt[nb], contributors, sy.lds_flag);
       if (finish) {
-        for (int idx = 2 * threadIdx.x; idx < ROWS * 64; idx += 512) {
+        for (int idx = 2 * threadIdx.x; idx < ROWS * kNB; idx += 2 * kThreads) {
           float s0 = 0.0f, s1 = 0.0f;
           for (int gg = g_lo; gg <= g_hi; ++gg) {
-            const long gb = (long)gg * W / G;
-            if (gb == (long)(gg + 1) * W / G) continue;  // empty run
+            const long gb = (long)gg * Wr / G;
+            if (gb == (long)(gg + 1) * Wr / G) continue;  // empty run
             const int sl = (gg == g_lo && gb < tile_lo) ? 1 : 0;
-            const float2 v = ld_coherent2(p.part + ((size_t)gg * 2 + sl) * ROWS * 64 + idx);
+            const float2 v = ld_coherent2(p.part + ((size_t)gg * 2 + sl) * ROWS * kNB + idx);
             s0 += v.x;
             s1 += v.y;
           }
-          lds.tileS[idx >> 6][idx & 63] = s0;
-          lds.tileS[idx >> 6][(idx & 63) + 1] = s1;
+          tileS[(idx / kNB) * TS + idx % kNB] = s0;
+          tileS[(idx / kNB) * TS + idx % kNB + 1] = s1;
         }
         __syncthreads();
       }
     }
     if (finish) {
-      if constexpr (EPI == EPI_QKV) {
-        const EpiQkv& e = *(const EpiQkv*)epi;
-        const int tiles_per_head = p.Dh / 64;
-        const int per_part = p.H * tiles_per_head;
-        const int part = t / per_part, rr = t % per_part;
-        const int hh = rr / tiles_per_head, b = rr % tiles_per_head;
-        const int half = p.Dh / 2;
-        const int jj = 32 * b + (lane & 31);
-        const int j = lane < 32 ? jj : half + jj;
-        const float inv_freq = exp2f(-(2.0f * (float)jj / (float)p.Dh) * p.log2_theta);
-        for (int r = wave; r < p.n; r += kWaves) {
-          const float v = lds.tileS[r][lane];
-          float out = v;
-          if (part < 2) {
-            const float partner = lds.tileS[r][lane ^ 32];
-            float sn, cs;
-            sincosf((float)e.pos[r] * inv_freq, &sn, &cs);
-            out = lane < 32 ? v * cs - partner * sn : v * cs + partner * sn;
-          }
-          const float nxt = __shfl_down(out, 1, kWave);
-          if ((lane & 1) == 0) {
-            bf16* dst;
-            if (part == 0)
-              dst = e.q + (size_t)r * p.d + hh * p.Dh + j;
-            else
-              dst = (part == 1 ? e.kc : e.vc) + ((size_t)hh * p.cap + p.prefix_len + r) * p.Dh + j;
-            st_coherent_bf2(dst, out, nxt);
-          }
-        }
-      } else if constexpr (EPI == EPI_RESID) {
-        const EpiResid& e = *(const EpiResid*)epi;
-        const int col = 64 * t + lane;
-        for (int r = wave; r < ROWS; r += kWaves) {
-          float xn = 0.0f;
-          if (r < p.n) {
-            xn = e.x_in[(size_t)r * p.d + col] + lds.tileS[r][lane];
-            st_coherent(&e.x_out[(size_t)r * p.d + col], xn);
-          }
-          const float s = wave_sum(xn * xn);
-          if (lane == 0) st_coherent(&e.ssq_out[(size_t)t * p.Mp + r], s);
-        }
-      } else if constexpr (EPI == EPI_SWIGLU) {
-        const EpiSwiglu& e = *(const EpiSwiglu*)epi;
-        const int c = lane & 31;
-        for (int r = wave; r < p.n; r += kWaves) {
-          const float gt = lds.tileS[r][c], up = lds.tileS[r][32 + c];
-          const float hv = gt / (1.0f + expf(-gt)) * up;
-          const float nxt = __shfl_down(hv, 1, kWave);
-          if (lane < 32 && (lane & 1) == 0) st_coherent_bf2(e.h + (size_t)r * p.Fp + 32 * t + c, hv, nxt);
-        }
-      } else {  // EPI_LOGITS
-        const EpiLogits& e = *(const EpiLogits*)epi;
-        const int col = 64 * t + lane;
-        for (int r = wave; r < ROWS; r += kWaves) {
-          const bool valid = r < p.n && col < p.V;
-          const float v = lds.tileS[r][lane];
-          if (valid && e.logits != nullptr && r >= e.row_lo) e.logits[(size_t)(r - e.row_lo) * p.V + col] = v;
-          float mv = valid ? v : -INFINITY;
-          int mi = valid ? col : 0x7fffffff;
-          wave_argmax(mv, mi);
-          if (lane == 0) {
-            st_coherent(&p.lm_val[(size_t)t * p.Mp + r], mv);
-            st_coherent(&p.lm_idx[(size_t)t * p.Mp + r], mi);
-          }
-        }
-        if (arrive_last(p.lm_cnt, g.tiles, sy.lds_flag)) {
-          for (int r = wave; r < p.n; r += kWaves) {
-            float mv = -INFINITY;
-            int mi = 0x7fffffff;
-            for (int t0 = 0; t0 < g.tiles; t0 += 4 * 64) {
-              float v[4];
-              int ix[4];
-#pragma unroll
-              for (int u = 0; u < 4; ++u) {
-                const int tt = t0 + 64 * u + lane;
-                v[u] = tt < g.tiles ? ld_coherent(&p.lm_val[(size_t)tt * p.Mp + r]) : -INFINITY;
-                ix[u] = tt < g.tiles ? ld_coherent(&p.lm_idx[(size_t)tt * p.Mp + r]) : 0x7fffffff;
-              }
-#pragma unroll
-              for (int u = 0; u < 4; ++u)
-                if (v[u] > mv || (v[u] == mv && ix[u] < mi)) {
-                  mv = v[u];
-                  mi = ix[u];
-                }
-            }
-            wave_argmax(mv, mi);
-            if (lane == 0) {
-              p.amax[r] = mi;
-              lds.amax[r] = mi;
-            }
-          }
-          __syncthreads();
-          if (threadIdx.x == 0) {
-            const int* tok = p.tree;
-            const int* par = p.tree + 128;
-            const int* dep = p.tree + 256;
-            int best = 0, best_depth = 0;
-            lds.reach[0] = 1;
-            for (int i = 1; i < p.n; ++i) {
-              const int pr = par[i];
-              const int ok = lds.reach[pr] && (tok[i] == lds.amax[pr]);
-              lds.reach[i] = ok;
-              if (ok && dep[i] > best_depth) {
-                best = i;
-                best_depth = dep[i];
-              }
-            }
-            for (int k = 0; k < p.n; ++k) p.path[k] = -1;
-            for (int i = best; i >= 0; i = par[i]) p.path[dep[i]] = i;
-            *p.accept_len = best_depth;
-            *p.next_token = lds.amax[best];
-          }
-        }
+      epilogue<MB, EPI, 1>(p, e, tileS, nb, G + t, gl);
+      if constexpr (EPI == EPI_LOGITS) {
+        if (arrive_last(p.lm_cnt, G + R, sy.lds_flag)) finish_walk(p, G + R, gl);
       }
-      __syncthreads();
     }
-    trace_mark(sy, ph, 5);
+    __syncthreads();
     pos += k1 - k0;
-    first = false;
   }
-  (void)layer;
+
+  // Main block: n-blocks [gi c, (gi + 1) c) over the full K.  For the LM head
+  // the workgroup's argmax entry is the best over its sub-blocks.
+  for (int done = 0; done < c;) {
+    const int w = next_width<EPI>(c - done);
+    const int nb0 = gi * c + done;
+    const int lm = done == 0 ? -2 : -1;
+    if (w == 4) {
+      main_subblock<MB, PRO, EPI, 4>(p, g, e, nb0, rstd, tileS, gl, lm);
+    } else if (w == 3) {
+      if constexpr (EPI == EPI_QKV) main_subblock<MB, PRO, EPI, 3>(p, g, e, nb0, rstd, tileS, gl, lm);
+    } else if (w == 2) {
+      main_subblock<MB, PRO, EPI, 2>(p, g, e, nb0, rstd, tileS, gl, lm);
+    } else {
+      main_subblock<MB, PRO, EPI, 1>(p, g, e, nb0, rstd, tileS, gl, lm);
+    }
+    done += w;
+  }
+  trace_mark(sy, phase, 4);
+  if constexpr (EPI == EPI_LOGITS) {
+    for (int r = threadIdx.x; r < ROWS; r += kThreads) {
+      const size_t at = (size_t)gi * p.Mp + r;
+      st_coherent(&p.lm_val[at], c > 0 ? gl.best_v[r] : -INFINITY);
+      st_coherent(&p.lm_idx[at], c > 0 ? gl.best_i[r] : 0x7fffffff);
+    }
+    if (arrive_last(p.lm_cnt, G + R, sy.lds_flag)) finish_walk(p, G + R, gl);
+  }
+  trace_mark(sy, phase, 5);
   return true;
 }
 
 // ------------------------------------------------------------------ attention
 
-template <int MB, int DH>
-struct AttnLds {
-  static constexpr int CH = kAttnChunk;
-  static constexpr int KST = DH + 8;
-  static constexpr int VST = CH + 8;
-  static constexpr int KS_BYTES = CH * KST * 2, VT_BYTES = DH * VST * 2;
-  static constexpr int MERGE_BYTES = 2 * kAttnMaxSplits * kMaxNodes * 4;
-  static constexpr int BYTES = KS_BYTES + VT_BYTES > MERGE_BYTES ? KS_BYTES + VT_BYTES : MERGE_BYTES;
+template <int DH>
+struct AttnGeom {
+  static constexpr int CH = kAttnChunk;  // key positions per LDS tile
+  static constexpr int KST = DH + 8;     // K row stride (bf16)
+  static constexpr int VST = CH + 8;     // V^T row stride (bf16)
+  static constexpr int KS_BYTES = CH * KST * 2;
+  static constexpr int VT_BYTES = DH * VST * 2;
+  static constexpr int BYTES = KS_BYTES + VT_BYTES;
 };
 
-// Stage key positions [p0, p0 + 64) of head h into LDS (K row-major, V
-// transposed); positions outside [lo, hi) are zero.
+__device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) {
+  return exp2f(-(2.0f * (float)j / (float)Dh) * log2_theta);
+}
+
+// Stage key positions [p0, p0 + CH) ∩ [lo, hi) of head h into LDS: K row-major,
+// V transposed; other rows zero.  Prefix keys come from the cache; tree keys
+// (position >= prefix_len) are rotated here from the QKV phase's raw k at the
+// node's position and also written to the node's cache slot.
 template <int DH>
-__device__ __forceinline__ void attn_stage(char* lds, const bf16* kc, const bf16* vc, int p0, int lo,
+__device__ __forceinline__ void attn_stage(const PassParams& p, char* lds, const bf16* kc, bf16* kc_w,
+                                           const bf16* vc, const float* kraw, int h, int p0, int lo,
                                            int hi) {
-  constexpr int CH = kAttnChunk, KST = DH + 8, VST = CH + 8;
+  using Gm = AttnGeom<DH>;
   bf16* Ks = reinterpret_cast<bf16*>(lds);
-  bf16* Vt = reinterpret_cast<bf16*>(lds + CH * KST * 2);
-  for (int idx = threadIdx.x; idx < CH * DH / 8; idx += kThreads) {
-    const int j = idx / (DH / 8), dc = (idx % (DH / 8)) * 8;
+  bf16* Vt = reinterpret_cast<bf16*>(lds + Gm::KS_BYTES);
+  constexpr int HALF = DH / 2;
+  // (position, 8-dim chunk of the first half); the chunk's rotary partner
+  // (+DH/2) is handled by the same thread.
+  for (int idx = threadIdx.x; idx < Gm::CH * (HALF / 8); idx += kThreads) {
+    const int j = idx / (HALF / 8), dc = (idx % (HALF / 8)) * 8;
     const int pos = p0 + j;
-    bf16x8 kv, vv;
+    bf16x8 k0, k1, v0, v1;
     if (pos >= lo && pos < hi) {
-      kv = *(const bf16x8*)(kc + (size_t)pos * DH + dc);
-      vv = *(const bf16x8*)(vc + (size_t)pos * DH + dc);
+      v0 = *(const bf16x8*)(vc + (size_t)pos * DH + dc);
+      v1 = *(const bf16x8*)(vc + (size_t)pos * DH + dc + HALF);
+      if (pos < p.prefix_len) {
+        k0 = *(const bf16x8*)(kc + (size_t)pos * DH + dc);
+        k1 = *(const bf16x8*)(kc + (size_t)pos * DH + dc + HALF);
+      } else {
+        const int node = pos - p.prefix_len;
+        const float* kr = kraw + (size_t)node * 2 * p.d + h * DH;
+        const float4 a0 = *(const float4*)(kr + dc), a1 = *(const float4*)(kr + dc + 4);
+        const float4 b0 = *(const float4*)(kr + dc + HALF), b1 = *(const float4*)(kr + dc + HALF + 4);
+        const float xa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        const float xb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+        const float npos = (float)p.tree[384 + node];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float sn, cs;
+          sincosf(npos * rope_inv_freq(dc + e, DH, p.log2_theta), &sn, &cs);
+          k0[e] = f2bf(xa[e] * cs - xb[e] * sn);
+          k1[e] = f2bf(xb[e] * cs + xa[e] * sn);
+        }
+        *(bf16x8*)(kc_w + (size_t)pos * DH + dc) = k0;
+        *(bf16x8*)(kc_w + (size_t)pos * DH + dc + HALF) = k1;
+      }
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        kv[e] = (bf16)0.0f;
-        vv[e] = (bf16)0.0f;
+        k0[e] = (bf16)0.0f;
+        k1[e] = (bf16)0.0f;
+        v0[e] = (bf16)0.0f;
+        v1[e] = (bf16)0.0f;
       }
     }
-    *(bf16x8*)&Ks[j * KST + dc] = kv;
+    *(bf16x8*)&Ks[j * Gm::KST + dc] = k0;
+    *(bf16x8*)&Ks[j * Gm::KST + dc + HALF] = k1;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) Vt[(dc + e) * VST + j] = vv[e];
+    for (int e = 0; e < 8; ++e) {
+      Vt[(dc + e) * Gm::VST + j] = v0[e];
+      Vt[(dc + HALF + e) * Gm::VST + j] = v1[e];
+    }
   }
 }
 
-// Tree attention phase: unit (head, split) per workgroup; positions of a split
-// are [s * T / S, (s + 1) * T / S) rounded to 16, T = prefix_len + n.
+// Tree attention phase: unit (head, split) per workgroup; split s of a head
+// covers positions [s T / S, (s + 1) T / S) rounded down to 16, T = prefix_len
+// + n.  Node i attends to the prefix and to the cache slots of its
+// ancestors-or-self (a 128-bit set per node).  Per unit: S^T = K q^T on the
+// matrix cores, online softmax in the log2 domain, O^T += V^T P^T with P split
+// into two bf16 halves (P never leaves registers: the S result's lane layout
+// is the PV product's k-slot order).  Then the head's splits join and each
+// merges its share of the rows.
 template <int MB, int DH>
-__device__ __forceinline__ bool attn_phase(const PassParams& p, int layer, const Sync& sy, int target,
-                                           char* lds) {
-  constexpr int CH = kAttnChunk, KSTEPS = DH / 32, DB = DH / 16, KST = DH + 8, VST = CH + 8;
+__device__ __attribute__((noinline)) bool attn_phase(const PassParams& p, int layer, const Sync& sy,
+                                                     int phase, char* lds) {
+  using Gm = AttnGeom<DH>;
+  constexpr int CH = Gm::CH, KSTEPS = DH / 32, DB = DH / 16, KST = Gm::KST, VST = Gm::VST;
   constexpr int RPW = MB > 4 ? 2 : 1;
-  const int S = p.attn_splits;
-  const int units = p.H * S;
-  const int total = p.prefix_len + p.n;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, li = lane & 15, g = lane >> 4;
-  const int d = p.H * DH;
+  constexpr int HALF = DH / 2;
+  const int S = wave_uniform(p.attn_splits);
+  const int units = wave_uniform(p.H) * S;
+  const int total = wave_uniform(p.prefix_len + p.n);
+  const int wave = wave_index(), lane = threadIdx.x & 63, li = lane & 15, g = lane >> 4;
+  const int MBr = wave_uniform(p.Mp / 16);
   const size_t kv_layer = (size_t)p.H * p.cap * DH;
-  const bf16* kcl = p.k_cache + (size_t)layer * kv_layer;
+  bf16* kcl = p.k_cache + (size_t)layer * kv_layer;
   const bf16* vcl = p.v_cache + (size_t)layer * kv_layer;
+  const float* qk = p.qk + (size_t)layer * p.Mp * 2 * p.d;
   bf16* Ks = reinterpret_cast<bf16*>(lds);
-  bf16* Vt = reinterpret_cast<bf16*>(lds + CH * KST * 2);
+  bf16* Vt = reinterpret_cast<bf16*>(lds + Gm::KS_BYTES);
 
-  // Units of this workgroup: blockIdx.x, blockIdx.x + G, ...  The first
-  // chunk of the first unit is staged before the barrier when it only holds
-  // prefix positions (which this pass does not write).
+  // The first tile of the first unit is staged before the barrier when it
+  // only holds prefix keys (which this pass does not write).
   int u = blockIdx.x;
   bool staged = false;
   if (u < units) {
     const int h = u / S, s = u % S;
     const int lo = (s * total / S) & ~15, hi = s + 1 == S ? total : ((s + 1) * total / S) & ~15;
-    if (lo < hi && hi <= p.prefix_len) {
-      attn_stage<DH>(lds, kcl + (size_t)h * p.cap * DH, vcl + (size_t)h * p.cap * DH, lo, lo, hi);
+    const int hi0 = lo + CH < hi ? lo + CH : hi;
+    if (lo < hi && hi0 <= p.prefix_len) {
+      attn_stage<DH>(p, lds, kcl + (size_t)h * p.cap * DH, kcl + (size_t)h * p.cap * DH,
+                     vcl + (size_t)h * p.cap * DH, qk + p.d, h, lo, lo, hi0);
       staged = true;
     }
   }
-  trace_mark(sy, target / p.G, 0);
-  if (!grid_wait(sy, target / p.G, p.G)) return false;
-  trace_mark(sy, target / p.G, 1);
+  trace_mark(sy, phase, 0);
+  if (!grid_wait(sy, phase, p.G)) return false;
+  trace_mark(sy, phase, 1);
 
-  const bf16* qbase = p.q + (size_t)layer * p.Mp * d;
   for (; u < units; u += p.G) {
     const int h = u / S, s = u % S;
     const int lo = (s * total / S) & ~15, hi = s + 1 == S ? total : ((s + 1) * total / S) & ~15;
-    const bf16* kc = kcl + (size_t)h * p.cap * DH;
+    bf16* kc = kcl + (size_t)h * p.cap * DH;
     const bf16* vc = vcl + (size_t)h * p.cap * DH;
+    // Query fragments (B operand of S^T = K q^T): lane holds row 16 rb + li,
+    // dims 32 ks + 8 g + e; rotated here at the node's position.
     bf16x8 qf[RPW][KSTEPS];
     uint32_t anc[RPW][4];
     float m_run[RPW], l_run[RPW];
@@ -619,10 +797,24 @@ __device__ __forceinline__ bool attn_phase(const PassParams& p, int layer, const
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
       const int rb = wave + 4 * r;
-      const int row = 16 * (rb < MB ? rb : 0) + li;
-      const bf16* qr = qbase + (size_t)row * d + h * DH;
+      const int row = 16 * (rb < MBr ? rb : 0) + li;
+      const float* qr = qk + (size_t)row * 2 * p.d + h * DH;
+      const float npos = (float)p.tree[384 + row];
 #pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) qf[r][ks] = *(const bf16x8*)(qr + 32 * ks + 8 * g);
+      for (int ks = 0; ks < KSTEPS / 2; ++ks) {
+        const int j0 = 32 * ks + 8 * g;
+        const float4 a0 = *(const float4*)(qr + j0), a1 = *(const float4*)(qr + j0 + 4);
+        const float4 b0 = *(const float4*)(qr + j0 + HALF), b1 = *(const float4*)(qr + j0 + HALF + 4);
+        const float xa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        const float xb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float sn, cs;
+          sincosf(npos * rope_inv_freq(j0 + e, DH, p.log2_theta), &sn, &cs);
+          qf[r][ks][e] = f2bf(xa[e] * cs - xb[e] * sn);
+          qf[r][ks + KSTEPS / 2][e] = f2bf(xb[e] * cs + xa[e] * sn);
+        }
+      }
       const uint32_t* ap = (const uint32_t*)(p.tree + 512) + row * 4;
 #pragma unroll
       for (int w = 0; w < 4; ++w) anc[r][w] = ap[w];
@@ -632,84 +824,87 @@ __device__ __forceinline__ bool attn_phase(const PassParams& p, int layer, const
       for (int db = 0; db < DB; ++db) oacc[r][db] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     for (int p0 = lo; p0 < hi; p0 += CH) {
+      const int hi_t = p0 + CH < hi ? p0 + CH : hi;
       if (!staged) {
         __syncthreads();
-        attn_stage<DH>(lds, kc, vc, p0, lo, hi);
+        attn_stage<DH>(p, lds, kc, kc, vc, qk + p.d, h, p0, p0, hi_t);
       }
       staged = false;
       __syncthreads();
 #pragma unroll
       for (int r = 0; r < RPW; ++r) {
         const int rb = wave + 4 * r;
-        if (rb >= MB) continue;
-        f32x4 sc[4];
+        if (rb >= MBr) continue;
+        for (int c0 = 0; c0 < CH && p0 + c0 < hi_t; c0 += 64) {  // 64 keys per softmax step
+          f32x4 sc[4];
 #pragma unroll
-        for (int jb = 0; jb < 4; ++jb) {
-          sc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+          for (int jb = 0; jb < 4; ++jb) {
+            sc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int ks = 0; ks < KSTEPS; ++ks) {
-            const bf16x8 a = *(const bf16x8*)&Ks[(16 * jb + li) * KST + 32 * ks + 8 * g];
-            sc[jb] = mfma16x16x32(a, qf[r][ks], sc[jb]);
+            for (int ks = 0; ks < KSTEPS; ++ks) {
+              const bf16x8 a = *(const bf16x8*)&Ks[(c0 + 16 * jb + li) * KST + 32 * ks + 8 * g];
+              sc[jb] = mfma16x16x32(a, qf[r][ks], sc[jb]);
+            }
           }
-        }
-        float mx = -INFINITY;
+          float mx = -INFINITY;
 #pragma unroll
-        for (int jb = 0; jb < 4; ++jb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int pos = p0 + 16 * jb + 4 * g + e;
-            const int t = pos - p.prefix_len;
-            const bool vis = pos < hi && (pos < p.prefix_len ||
-                                          (t < p.n && ((anc[r][t >> 5] >> (t & 31)) & 1u)));
-            const float sv = vis ? sc[jb][e] * p.scale_log2 : -INFINITY;
-            sc[jb][e] = sv;
-            mx = fmaxf(mx, sv);
-          }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-        const float m_new = fmaxf(m_run[r], mx);
-        const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
-        const float alpha = exp2f(m_run[r] - m_use);
-        bf16 ph[4][4], pl[4][4];
-        float psum = 0.0f;
-#pragma unroll
-        for (int jb = 0; jb < 4; ++jb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float pe = exp2f(sc[jb][e] - m_use);
-            ph[jb][e] = f2bf(pe);
-            pl[jb][e] = f2bf(pe - bf2f(ph[jb][e]));
-            psum += pe;
-          }
-        psum += __shfl_xor(psum, 16, kWave);
-        psum += __shfl_xor(psum, 32, kWave);
-        l_run[r] = l_run[r] * alpha + psum;
-        m_run[r] = m_new;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) oacc[r][db] = oacc[r][db] * alpha;
-#pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2) {
-          bf16x8 bph, bpl;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            bph[e] = ph[2 * t2][e];
-            bph[4 + e] = ph[2 * t2 + 1][e];
-            bpl[e] = pl[2 * t2][e];
-            bpl[4 + e] = pl[2 * t2 + 1][e];
-          }
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const bf16* vrow = &Vt[(16 * db + li) * VST + 32 * t2 + 4 * g];
-            const bf16x4 lo4 = *(const bf16x4*)vrow;
-            const bf16x4 hi4 = *(const bf16x4*)(vrow + 16);
-            bf16x8 av;
+          for (int jb = 0; jb < 4; ++jb)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              av[e] = lo4[e];
-              av[4 + e] = hi4[e];
+              const int pos = p0 + c0 + 16 * jb + 4 * g + e;
+              const int t = pos - p.prefix_len;
+              const bool vis = pos < hi_t && (pos < p.prefix_len ||
+                                              (t < p.n && ((anc[r][t >> 5] >> (t & 31)) & 1u)));
+              const float sv = vis ? sc[jb][e] * p.scale_log2 : -INFINITY;
+              sc[jb][e] = sv;
+              mx = fmaxf(mx, sv);
             }
-            oacc[r][db] = mfma16x16x32(av, bph, oacc[r][db]);
-            oacc[r][db] = mfma16x16x32(av, bpl, oacc[r][db]);
+          mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+          mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+          const float m_new = fmaxf(m_run[r], mx);
+          const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
+          const float alpha = exp2f(m_run[r] - m_use);
+          bf16 ph[4][4], pl[4][4];
+          float psum = 0.0f;
+#pragma unroll
+          for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float pe = exp2f(sc[jb][e] - m_use);
+              ph[jb][e] = f2bf(pe);
+              pl[jb][e] = f2bf(pe - bf2f(ph[jb][e]));
+              psum += pe;
+            }
+          psum += __shfl_xor(psum, 16, kWave);
+          psum += __shfl_xor(psum, 32, kWave);
+          l_run[r] = l_run[r] * alpha + psum;
+          m_run[r] = m_new;
+#pragma unroll
+          for (int db = 0; db < DB; ++db) oacc[r][db] = oacc[r][db] * alpha;
+#pragma unroll
+          for (int t2 = 0; t2 < 2; ++t2) {
+            bf16x8 bph, bpl;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              bph[e] = ph[2 * t2][e];
+              bph[4 + e] = ph[2 * t2 + 1][e];
+              bpl[e] = pl[2 * t2][e];
+              bpl[4 + e] = pl[2 * t2 + 1][e];
+            }
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+              const bf16* vrow = &Vt[(16 * db + li) * VST + c0 + 32 * t2 + 4 * g];
+              const bf16x4 lo4 = *(const bf16x4*)vrow;
+              const bf16x4 hi4 = *(const bf16x4*)(vrow + 16);
+              bf16x8 av;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                av[e] = lo4[e];
+                av[4 + e] = hi4[e];
+              }
+              oacc[r][db] = mfma16x16x32(av, bph, oacc[r][db]);
+              oacc[r][db] = mfma16x16x32(av, bpl, oacc[r][db]);
+            }
           }
         }
       }
@@ -721,7 +916,7 @@ __device__ __forceinline__ bool attn_phase(const PassParams& p, int layer, const
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
       const int rb = wave + 4 * r;
-      if (rb >= MB) continue;
+      if (rb >= MBr) continue;
       const int row = 16 * rb + li;
       if (g == 0) st_coherent2(&p.attn_ml[(split_base + row) * 2], m_run[r], l_run[r]);
 #pragma unroll
@@ -763,7 +958,7 @@ __device__ __forceinline__ bool attn_phase(const PassParams& p, int layer, const
       for (int ss = 0; ss < S; ++ss) wgt[ss][i] *= inv;
     }
     __syncthreads();
-    bf16* obase = p.o + (size_t)layer * p.Mp * d;
+    bf16* obase = p.o + (size_t)layer * p.Mp * p.d;
     for (int idx = threadIdx.x; idx < nr * (DH / 2); idx += kThreads) {
       const int i = r_lo + idx / (DH / 2), dd = 2 * (idx % (DH / 2));
       float o0 = 0.0f, o1 = 0.0f;
@@ -784,7 +979,7 @@ __device__ __forceinline__ bool attn_phase(const PassParams& p, int layer, const
         o0 += v.x * wgt[ss][i];
         o1 += v.y * wgt[ss][i];
       }
-      st_coherent_bf2(obase + (size_t)i * d + h * DH + dd, o0, o1);
+      st_coherent_bf2(obase + (size_t)i * p.d + h * DH + dd, o0, o1);
     }
     __syncthreads();
   }
@@ -793,8 +988,10 @@ __device__ __forceinline__ bool attn_phase(const PassParams& p, int layer, const
 
 // ------------------------------------------------------------------ embed
 
-__device__ __forceinline__ void embed_phase(const PassParams& p, const TreeArgs& tree) {
-  __shared__ int par_s[128];
+// Tree preparation (every node's depth, position prefix_len + depth, and
+// ancestor-or-self set: its row of the tree masking table) and the residual
+// stream's first version: the nodes' embedding rows.
+__device__ __forceinline__ void embed_phase(const PassParams& p, const TreeArgs& tree, int* par_s) {
   const bf16* E = (const bf16*)(p.packed + p.o_embed);
   if (blockIdx.x == 0) {
     if (threadIdx.x < 128) par_s[threadIdx.x] = threadIdx.x < p.n ? tree.parent[threadIdx.x] : -1;
@@ -818,16 +1015,19 @@ __device__ __forceinline__ void embed_phase(const PassParams& p, const TreeArgs&
       for (int w = 0; w < 4; ++w) st_coherent(&p.tree[512 + i * 4 + w], (int)a[w]);
     }
   }
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63;
   for (int m = blockIdx.x; m < p.Mp; m += p.G) {
     const bool valid = m < p.n;
     const bf16* row = E + (size_t)(valid ? tree.tok[m] : 0) * p.d;
-    for (int t = wave; t < p.d_tiles; t += kWaves) {
-      const int c = 64 * t + lane;
+    for (int c = threadIdx.x; c < p.d; c += kThreads) {
       const float v = valid ? bf2f(row[c]) : 0.0f;
       st_coherent(&p.x[(size_t)m * p.d + c], v);
-      const float s = wave_sum(v * v);
-      if (lane == 0) st_coherent(&p.ssq[(size_t)t * p.Mp + m], s);
+      float s = v * v;
+      s += __shfl_xor(s, 8, kWave);
+      s += __shfl_xor(s, 4, kWave);
+      s += __shfl_xor(s, 2, kWave);
+      s += __shfl_xor(s, 1, kWave);
+      if ((lane & 15) == 0) st_coherent(&p.ssq[(size_t)(c / kNB) * p.Mp + m], s);
     }
   }
 }
@@ -835,86 +1035,103 @@ __device__ __forceinline__ void embed_phase(const PassParams& p, const TreeArgs&
 // ------------------------------------------------------------------ kernel
 
 template <int MB, int DH>
+constexpr int pass_lds_bytes() {
+  constexpr int attn = AttnGeom<DH>::BYTES;
+  constexpr int merge = 2 * kAttnMaxSplits * kMaxNodes * 4;
+  constexpr int tile = 16 * MB * (16 * 4 + 4) * 4;
+  constexpr int m1 = attn > merge ? attn : merge;
+  return m1 > tile ? m1 : tile;
+}
+
+template <int MB, int DH>
 __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p, const TreeArgs tree) {
-  constexpr int D = MB <= 2 ? 4 : (MB <= 4 ? 3 : 2);
-  __shared__ __attribute__((aligned(16))) char attn_lds[AttnLds<MB, DH>::BYTES];
-  __shared__ PassLds<MB> lds;
+  __shared__ __attribute__((aligned(16))) char lds_raw[pass_lds_bytes<MB, DH>()];
+  __shared__ GemmLds gl;
+  __shared__ int par_s[128];
   __shared__ int flag;
   const Sync sy{p.bar, p.status, p.spin_limit, &flag,
                 p.trace != nullptr && (int)blockIdx.x < kTraceWgs
                     ? p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 6
                     : nullptr};
-  const int G = p.G;
-  const size_t xsz = (size_t)p.Mp * p.d, ssz = (size_t)p.d_tiles * p.Mp;
+  float* tileS = reinterpret_cast<float*>(lds_raw);
+  const size_t xsz = (size_t)p.Mp * p.d, ssz = (size_t)p.d_nb * p.Mp;
+  const size_t kv_layer = (size_t)p.H * p.cap * p.Dh;
   int phase = 0;
   bool ok = true;
 
-  embed_phase(p, tree);
+  embed_phase(p, tree, par_s);
   grid_arrive(sy, phase);
   ++phase;
 
   for (int l = 0; l < p.L && ok; ++l) {
     const char* lw = p.packed + p.layer0 + (long long)l * p.layer_bytes;
-    const float* x_a = p.x + (size_t)(2 * l) * xsz;       // layer input
-    float* x_b = p.x + (size_t)(2 * l + 1) * xsz;         // after attention
-    float* x_c = p.x + (size_t)(2 * l + 2) * xsz;         // after feed-forward
+    const float* x_a = p.x + (size_t)(2 * l) * xsz;  // layer input
+    float* x_b = p.x + (size_t)(2 * l + 1) * xsz;    // after attention
+    float* x_c = p.x + (size_t)(2 * l + 2) * xsz;    // after the feed-forward block
     const float* ss_a = p.ssq + (size_t)(2 * l) * ssz;
     float* ss_b = p.ssq + (size_t)(2 * l + 1) * ssz;
     float* ss_c = p.ssq + (size_t)(2 * l + 2) * ssz;
-    bf16* q_l = p.q + (size_t)l * p.Mp * p.d;
-    bf16* o_l = p.o + (size_t)l * p.Mp * p.d;
-    bf16* h_l = p.h + (size_t)l * p.Mp * p.Fp;
-    const size_t kv_layer = (size_t)p.H * p.cap * p.Dh;
-
-    {  // QKV
-      GemmDesc g{(const bf16x8*)(lw + p.o_qkv), p.qkv_tiles, p.ks_d, nullptr, 0, x_a, ss_a,
-                 (const bf16*)(lw + p.o_attn_norm)};
-      EpiQkv e{q_l, p.k_cache + (size_t)l * kv_layer, p.v_cache + (size_t)l * kv_layer, p.tree + 384};
-      ok = gemm_phase<MB, PRO_NORM, EPI_QKV, D>(p, g, sy, G * phase, lds, l, &e);
+    {  // QKV projection
+      const GemmDesc g{(const bf16x8*)(lw + p.o_qkv), p.qkv_nb, p.ks_d, nullptr, 0, x_a, ss_a,
+                       (const bf16*)(lw + p.o_attn_norm)};
+      EpiArgs e{};
+      e.qk = p.qk + (size_t)l * p.Mp * 2 * p.d;
+      e.vc = p.v_cache + (size_t)l * kv_layer;
+      ok = gemm_phase<MB, PRO_NORM, EPI_QKV>(p, g, e, sy, phase, tileS, gl);
       if (!ok) break;
       grid_arrive(sy, phase);
       ++phase;
     }
-    ok = attn_phase<MB, DH>(p, l, sy, G * phase, attn_lds);
+    ok = attn_phase<MB, DH>(p, l, sy, phase, lds_raw);
     if (!ok) break;
     grid_arrive(sy, phase);
     ++phase;
     {  // O projection + residual
-      GemmDesc g{(const bf16x8*)(lw + p.o_o), p.d_tiles, p.ks_d, o_l, p.d, nullptr, nullptr, nullptr};
-      EpiResid e{x_a, x_b, ss_b};
-      ok = gemm_phase<MB, PRO_BF16, EPI_RESID, D>(p, g, sy, G * phase, lds, l, &e);
+      const GemmDesc g{(const bf16x8*)(lw + p.o_o), p.d_nb, p.ks_d, p.o + (size_t)l * p.Mp * p.d, p.d,
+                       nullptr, nullptr, nullptr};
+      EpiArgs e{};
+      e.x_in = x_a;
+      e.x_out = x_b;
+      e.ssq_out = ss_b;
+      ok = gemm_phase<MB, PRO_BF16, EPI_RESID>(p, g, e, sy, phase, tileS, gl);
       if (!ok) break;
       grid_arrive(sy, phase);
       ++phase;
     }
     {  // gate/up + SwiGLU
-      GemmDesc g{(const bf16x8*)(lw + p.o_gu), p.gu_tiles, p.ks_d, nullptr, 0, x_b, ss_b,
-                 (const bf16*)(lw + p.o_ffn_norm)};
-      EpiSwiglu e{h_l};
-      ok = gemm_phase<MB, PRO_NORM, EPI_SWIGLU, D>(p, g, sy, G * phase, lds, l, &e);
+      const GemmDesc g{(const bf16x8*)(lw + p.o_gu), p.gu_nb, p.ks_d, nullptr, 0, x_b, ss_b,
+                       (const bf16*)(lw + p.o_ffn_norm)};
+      EpiArgs e{};
+      e.h = p.h + (size_t)l * p.Mp * p.Fp;
+      ok = gemm_phase<MB, PRO_NORM, EPI_SWIGLU>(p, g, e, sy, phase, tileS, gl);
       if (!ok) break;
       grid_arrive(sy, phase);
       ++phase;
     }
     {  // down projection + residual
-      GemmDesc g{(const bf16x8*)(lw + p.o_down), p.d_tiles, p.ks_f, h_l, p.Fp, nullptr, nullptr, nullptr};
-      EpiResid e{x_b, x_c, ss_c};
-      ok = gemm_phase<MB, PRO_BF16, EPI_RESID, D>(p, g, sy, G * phase, lds, l, &e);
+      const GemmDesc g{(const bf16x8*)(lw + p.o_down), p.d_nb, p.ks_f, p.h + (size_t)l * p.Mp * p.Fp,
+                       p.Fp, nullptr, nullptr, nullptr};
+      EpiArgs e{};
+      e.x_in = x_b;
+      e.x_out = x_c;
+      e.ssq_out = ss_c;
+      ok = gemm_phase<MB, PRO_BF16, EPI_RESID>(p, g, e, sy, phase, tileS, gl);
       if (!ok) break;
       grid_arrive(sy, phase);
       ++phase;
     }
   }
   if (ok) {  // final norm + LM head + argmax + accept walk
-    GemmDesc g{(const bf16x8*)(p.packed + p.o_lm), p.v_tiles, p.ks_d, nullptr, 0,
-               p.x + (size_t)(2 * p.L) * xsz, p.ssq + (size_t)(2 * p.L) * ssz,
-               (const bf16*)(p.packed + p.o_final_norm)};
-    EpiLogits e{p.logits, p.row_lo};
-    if (gemm_phase<MB, PRO_NORM, EPI_LOGITS, D>(p, g, sy, G * phase, lds, p.L, &e))
-      trace_mark(sy, phase, 2);
+    const GemmDesc g{(const bf16x8*)(p.packed + p.o_lm), p.v_nb, p.ks_d, nullptr, 0,
+                     p.x + (size_t)(2 * p.L) * xsz, p.ssq + (size_t)(2 * p.L) * ssz,
+                     (const bf16*)(p.packed + p.o_final_norm)};
+    EpiArgs e{};
+    e.logits = p.logits;
+    e.row_lo = p.row_lo;
+    if (gemm_phase<MB, PRO_NORM, EPI_LOGITS>(p, g, e, sy, phase, tileS, gl)) trace_mark(sy, phase, 2);
   }
   // Leave the pass: the last workgroup out resets the barrier and join counters.
-  if (arrive_last(p.exit_cnt, G, &flag)) {
+  if (arrive_last(p.exit_cnt, p.G, &flag)) {
     if (threadIdx.x < kBarSlots)
       __hip_atomic_store(p.bar + threadIdx.x * kBarStride, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     for (int h = threadIdx.x; h < p.H; h += kThreads)
@@ -950,9 +1167,6 @@ hipError_t launch_pass(int mb, const PassParams& p, const TreeArgs& tree, hipStr
     LLMCAD_PASS_CASE(2)
     LLMCAD_PASS_CASE(3)
     LLMCAD_PASS_CASE(4)
-    LLMCAD_PASS_CASE(5)
-    LLMCAD_PASS_CASE(6)
-    LLMCAD_PASS_CASE(7)
     LLMCAD_PASS_CASE(8)
     default:
       return hipErrorInvalidValue;
@@ -969,9 +1183,6 @@ int pass_occupancy(int mb, int dh) {
     LLMCAD_OCC_CASE(2)
     LLMCAD_OCC_CASE(3)
     LLMCAD_OCC_CASE(4)
-    LLMCAD_OCC_CASE(5)
-    LLMCAD_OCC_CASE(6)
-    LLMCAD_OCC_CASE(7)
     LLMCAD_OCC_CASE(8)
     default:
       return 0;

@@ -102,16 +102,27 @@ def test_verify_matches_oracle(model, tree):
 
 
 def test_launch_shape_variants(model, monkeypatch):
-    # Unsplit GEMMs, maximal split-K, and attention splits that each span
-    # several key chunks all meet the oracle bar.
+    # One position split per head (every split spans several 128-key tiles),
+    # three splits, and two workgroups per CU (a different stream-K cut and
+    # main-block width) all meet the oracle bar.
     parent = TREES["b432_n41"]
     tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=7)
     _check_all(model, parent, tok, "default")
-    for env in ({"LLMCAD_GEMM_WGS": "1", "LLMCAD_ATTN_WGS": "1"},
-                {"LLMCAD_GEMM_WGS": "100000", "LLMCAD_ATTN_WGS": "8"}):
+    for env in ({"LLMCAD_ATTN_SPLITS": "1"}, {"LLMCAD_ATTN_SPLITS": "3"},
+                {"LLMCAD_PASS_WGS_PER_CU": "2"}):
         for k, v in env.items():
             monkeypatch.setenv(k, v)
         _check_all(model, parent, tok, str(env))
+        for k in env:
+            monkeypatch.delenv(k)
+
+
+def test_pass_status_ok(model):
+    parent = TREES["binary_d3_n15"]
+    tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=3)
+    _run(model, parent, tok)
+    off, _ = model.binding.workspace_region(model.sess.cfg, len(parent), 5)
+    assert int(model.sess.workspace[off:off + 4].view(torch.int32).item()) == 0
 
 
 def test_deterministic_and_prefix_untouched(model):
