@@ -165,10 +165,13 @@ const char* llmcad_status_string(int status);
  * [Mp][Fp], 4 per-node greedy token int32 [Mp],
  * 5 pass status int32 (0 = ok; 1 = a grid wait of the single-launch pass ran
  * out of its bounded spin: the pass's outputs are invalid, and the workspace
- * must be cleared with llmcad_workspace_init before the next pass),
+ * must be cleared with llmcad_workspace_init before the next pass; 3 = the
+ * kernel did not find its parameter block where it reads it, and did
+ * nothing),
  * 6 phase timestamps int64 [8][2 + 5L][6] (written when the environment
  * variable LLMCAD_TRACE is 1);
- * Mp = max_n rounded up to 16, Fp = F rounded up to 32.  Offsets describe a
+ * Mp = max_n rounded up to 16 (to 128 when max_n > 64), Fp = F rounded up
+ * to 32.  Offsets describe a
  * pass over max_n nodes (call with max_n = that pass's n). */
 int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t which, size_t* offset,
                             size_t* bytes);

@@ -132,6 +132,7 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
 
   PassParams p;
   memset(&p, 0, sizeof(p));
+  p.magic = kPassMagic;
   p.L = s.L;
   p.d = s.d;
   p.H = s.H;

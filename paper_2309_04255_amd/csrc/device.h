@@ -34,6 +34,30 @@ __device__ __forceinline__ int wave_index() {
 // scalar so that branches on it are scalar branches.
 __device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Global-memory access.  Pointers that reach a device function through a
+// structure or a reference are generic to the compiler, and a generic access
+// is a FLAT instruction, which counts on both the vector-memory and the
+// out-of-order LDS/scalar counters: every wait for one of them then drains all
+// loads in flight.  These casts make the access a global one (in-order vector
+// counter only, so a pipeline can wait for its oldest stage alone).
+// (The host pass of a HIP compile only type-checks device code; address
+// spaces mean nothing there.)
+#if defined(__HIP_DEVICE_COMPILE__)
+#define LLMCAD_GLOBAL __attribute__((address_space(1)))
+#define LLMCAD_CONSTANT __attribute__((address_space(4)))
+#else
+#define LLMCAD_GLOBAL
+#define LLMCAD_CONSTANT
+#endif
+template <class T>
+__device__ __forceinline__ T ldg(const T* p) {
+  return *(const LLMCAD_GLOBAL T*)p;
+}
+template <class T>
+__device__ __forceinline__ void stg(T* p, const T& v) {
+  *(LLMCAD_GLOBAL T*)p = v;
+}
+
 __device__ __forceinline__ float bf2f(bf16 x) { return (float)x; }
 __device__ __forceinline__ bf16 f2bf(float x) { return (bf16)x; }  // round to nearest even
 
@@ -72,24 +96,35 @@ __device__ __forceinline__ void wave_argmax(float& v, int& idx) {
 // arrive_last only has to wait until this workgroup's stores have completed
 // before counting its arrival with a device-scope atomic.
 __device__ __forceinline__ void st_coherent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store((LLMCAD_GLOBAL float*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void st_coherent(int* p, int v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store((LLMCAD_GLOBAL int*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void st_coherent2(float* p, float a, float b) {  // p 8-byte aligned
   const uint64_t bits = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
-  __hip_atomic_store((uint64_t*)p, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store((LLMCAD_GLOBAL uint64_t*)p, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coherent_bf2(bf16* p, float a, float b) {  // p 4-byte aligned
+  const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, f2bf(a));
+  const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, f2bf(b));
+  __hip_atomic_store((LLMCAD_GLOBAL uint32_t*)p, lo | (hi << 16), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ float ld_coherent(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_load((const LLMCAD_GLOBAL float*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ int ld_coherent(const int* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_load((const LLMCAD_GLOBAL int*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ float2 ld_coherent2(const float* p) {  // p 8-byte aligned
-  const uint64_t bits = __hip_atomic_load((const uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t bits =
+      __hip_atomic_load((const LLMCAD_GLOBAL uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   return make_float2(__uint_as_float((uint32_t)bits), __uint_as_float((uint32_t)(bits >> 32)));
+}
+// Device-scope counter updates.
+__device__ __forceinline__ int atomic_add_dev(int* p, int v) {
+  return __hip_atomic_fetch_add((LLMCAD_GLOBAL int*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Counts this workgroup's arrival on `counter`; returns true (to every
@@ -102,9 +137,9 @@ __device__ __forceinline__ bool arrive_last(int* counter, int expected, int* lds
   __builtin_amdgcn_s_waitcnt(0);            // and wait until they have completed
   __syncthreads();
   if (threadIdx.x == 0) {
-    const int old = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int old = atomic_add_dev(counter, 1);
     const int last = (old == expected - 1);
-    if (last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (last) st_coherent(counter, 0);
     *lds_flag = last;
   }
   __syncthreads();

@@ -20,7 +20,13 @@ struct TreeArgs {
   int32_t parent[128];
 };
 
+// Set in PassParams::magic by the host; the kernel checks it where it reads
+// the parameters in place.
+constexpr int kPassMagic = 0x4c4d4341;
+
+// Must stay the first kernel argument of the pass kernel.
 struct PassParams {
+  int magic;
   // model
   int L, d, H, Dh, F, Fp, V;
   float eps, inv_d, log2_theta, scale_log2;

@@ -50,10 +50,18 @@ enum Prologue { PRO_BF16 = 0, PRO_NORM = 1 };  // bf16 activations | RMSNorm of 
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 constexpr int kTraceWgs = 8;  // workgroups that record phase timestamps
 
-__device__ __forceinline__ void st_coherent_bf2(bf16* p, float a, float b) {  // p 4-byte aligned
-  const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, f2bf(a));
-  const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, f2bf(b));
-  __hip_atomic_store((uint32_t*)p, lo | (hi << 16), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// The launch parameters, read in place from the kernel-argument segment
+// (constant memory): loads through a wave-uniform address of it are scalar
+// loads, their values are wave-uniform, and no store can alias them.
+typedef const LLMCAD_CONSTANT PassParams KParams;
+
+// Inside a non-inlined function the compiler no longer knows that the
+// parameter block's address is the same in every lane; re-establish it.
+__device__ __forceinline__ KParams& uniform_params(KParams& p) {
+  const uint64_t v = (uint64_t)&p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return *(KParams*)(((uint64_t)hi << 32) | lo);
 }
 
 // ------------------------------------------------------------------ sync
@@ -66,12 +74,24 @@ struct Sync {
   long long* trace;  // [phase][6] timestamps of this workgroup, or null
 };
 
+__device__ __forceinline__ Sync make_sync(KParams& p, int* lds_flag) {
+  Sync s;
+  s.bar = p.bar;
+  s.status = p.status;
+  s.limit = p.spin_limit;
+  s.lds_flag = lds_flag;
+  s.trace = p.trace != nullptr && (int)blockIdx.x < kTraceWgs
+                ? p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 6
+                : nullptr;
+  return s;
+}
+
 // Diagnostics: wall-clock (100 MHz) marks per phase: 0 = barrier wait
 // entered, 1 = wait over, 2 = phase work done; GEMM phases also mark 3 =
 // operand prologue done, 4 = weight streaming of the last segment done,
 // 5 = last epilogue done.
 __device__ __forceinline__ void trace_mark(const Sync& s, int phase, int k) {
-  if (s.trace != nullptr && threadIdx.x == 0) s.trace[phase * 6 + k] = (long long)wall_clock64();
+  if (s.trace != nullptr && threadIdx.x == 0) stg(s.trace + phase * 6 + k, (long long)wall_clock64());
 }
 
 // End of a phase: this workgroup's stores have completed, then one
@@ -83,8 +103,7 @@ __device__ __forceinline__ void grid_arrive(const Sync& s, int phase) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0)
-    __hip_atomic_fetch_add(s.bar + (blockIdx.x % kBarSlots) * kBarStride, 1, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+    atomic_add_dev(s.bar + (blockIdx.x % kBarSlots) * kBarStride, 1);
 }
 
 // Waits until all G workgroups have arrived `phase` times; one wave polls all
@@ -202,7 +221,7 @@ template <int MB, int PRO, int C>
 __device__ __forceinline__ void pipe_load_b(Pipe<MB, PRO, C>& P, int slot, int i) {
   const int s = P.s0 + kWaves * i;
 #pragma unroll
-  for (int c = 0; c < C; ++c) P.bw[slot][c] = P.wt[((size_t)c * P.ks + s) * 64];
+  for (int c = 0; c < C; ++c) P.bw[slot][c] = ldg(P.wt + ((size_t)c * P.ks + s) * 64);
 }
 
 template <int MB, int PRO, int C>
@@ -213,15 +232,15 @@ __device__ __forceinline__ void pipe_load_a(Pipe<MB, PRO, C>& P, const GemmDesc&
   if constexpr (PRO == PRO_BF16) {
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb)
-      P.as[slot].a[rb] = *(const bf16x8*)(g.a + (size_t)(16 * rb + lrow) * g.lda + k);
+      P.as[slot].a[rb] = ldg((const bf16x8*)(g.a + (size_t)(16 * rb + lrow) * g.lda + k));
   } else {
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb) {
       const float* xr = g.x + (size_t)(16 * rb + lrow) * d + k;
-      P.as[slot].x[rb][0] = *(const float4*)xr;
-      P.as[slot].x[rb][1] = *(const float4*)(xr + 4);
+      P.as[slot].x[rb][0] = ldg((const float4*)xr);
+      P.as[slot].x[rb][1] = ldg((const float4*)(xr + 4));
     }
-    P.as[slot].g = *(const bf16x8*)(g.gain + k);
+    P.as[slot].g = ldg((const bf16x8*)(g.gain + k));
   }
 }
 
@@ -245,37 +264,42 @@ __device__ __forceinline__ void pipe_compute(Pipe<MB, PRO, C>& P, int slot, f32x
   }
 }
 
-// Issues the first D weight stages (done before a barrier for the first segment).
+// Runs the wave's k-steps as a software pipeline of D register stages.
+// Every stage is loaded (weights, then the A operand) D steps ahead of its
+// use, and loads are issued unconditionally (clamped to the last step) so
+// the number in flight is the same on every path.  The scheduling fences keep
+// each stage's compute after the previous stage's reload: the compiler's
+// wait before a compute then only covers that stage's own loads, and the
+// (D - 1) younger stages stay in flight.
 template <int MB, int PRO, int C>
-__device__ __forceinline__ void pipe_prefetch_b(Pipe<MB, PRO, C>& P) {
-  if (P.ns == 0) return;
-#pragma unroll
-  for (int u = 0; u < Pipe<MB, PRO, C>::D; ++u) pipe_load_b(P, u, u < P.ns ? u : P.ns - 1);
-}
-
-// Runs the wave's k-steps.  Loads are issued unconditionally (clamped to the
-// last step) so that the number in flight is the same on every path.
-template <int MB, int PRO, int C>
-__device__ __forceinline__ void pipe_run(Pipe<MB, PRO, C>& P, const GemmDesc& g, int d, bool b_ready,
+__device__ __forceinline__ void pipe_run(Pipe<MB, PRO, C>& P, const GemmDesc& g, int d,
                                          f32x4 (&acc)[MB][C], const float (&rstd)[MB]) {
   constexpr int D = Pipe<MB, PRO, C>::D;
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
     for (int c = 0; c < C; ++c) acc[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (P.ns == 0) return;
-  if (!b_ready) pipe_prefetch_b(P);
+  const int ns = P.ns;  // wave-uniform
+  if (ns == 0) return;
 #pragma unroll
-  for (int u = 0; u < D; ++u) pipe_load_a(P, g, d, u, u < P.ns ? u : P.ns - 1);
-  for (int i = 0; i < P.ns; i += D) {
+  for (int u = 0; u < D; ++u) {
+    const int st = u < ns ? u : ns - 1;
+    pipe_load_b(P, u, st);
+    pipe_load_a(P, g, d, u, st);
+    __builtin_amdgcn_sched_barrier(0);  // stages issue in order
+  }
+  for (int i = 0; i < ns; i += D) {
 #pragma unroll
     for (int u = 0; u < D; ++u) {
-      if (i + u < P.ns) pipe_compute(P, u, acc, rstd);
-      const int nx = i + u + D < P.ns ? i + u + D : P.ns - 1;
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + u < ns) pipe_compute(P, u, acc, rstd);
+      __builtin_amdgcn_sched_barrier(0);
+      const int nx = i + u + D < ns ? i + u + D : ns - 1;
       pipe_load_b(P, u, nx);
       pipe_load_a(P, g, d, u, nx);
     }
   }
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 // Sum the waves' partial tiles into tileS [16 MB][16 C (+4)] in wave order.
@@ -310,6 +334,10 @@ struct GemmLds {
   int red_i[kMaxNodes][8];
   int reach[kMaxNodes];
   int amax[kMaxNodes];
+  int tok[kMaxNodes];  // accept walk: the tree, staged from the workspace
+  int par[kMaxNodes];
+  int dep[kMaxNodes];
+  int walk_len;
   float best_v[kMaxNodes];  // LM head: the workgroup's best column per row
   int best_i[kMaxNodes];
 };
@@ -317,7 +345,7 @@ struct GemmLds {
 // Epilogue of C n-blocks [nb0, nb0 + C) held in tileS: writes the phase's
 // outputs with device-coherent stores.  lm_entry: argmax partial slot.
 template <int MB, int EPI, int C>
-__device__ __forceinline__ void epilogue(const PassParams& p, const EpiArgs& e, float* tileS, int nb0,
+__device__ __forceinline__ void epilogue(KParams& p, const EpiArgs& e, float* tileS, int nb0,
                                          int lm_entry, GemmLds& gl) {
   constexpr int ROWS = 16 * MB, COLS = 16 * C, TS = COLS + 4;
   const int lane = threadIdx.x & 63;
@@ -342,7 +370,7 @@ __device__ __forceinline__ void epilogue(const PassParams& p, const EpiArgs& e, 
       const int col = kNB * nb0 + cc;
       float xn = 0.0f;
       if (r < p.n) {
-        xn = e.x_in[(size_t)r * p.d + col] + tileS[r * TS + cc];
+        xn = ldg(e.x_in + (size_t)r * p.d + col) + tileS[r * TS + cc];
         st_coherent(&e.x_out[(size_t)r * p.d + col], xn);
       }
       // sum of squares over the 16 columns of this n-block (16 consecutive lanes)
@@ -367,7 +395,7 @@ __device__ __forceinline__ void epilogue(const PassParams& p, const EpiArgs& e, 
       const int col = kNB * nb0 + cc;
       const bool valid = r < p.n && col < p.V;
       const float v = tileS[r * TS + cc];
-      if (valid && e.logits != nullptr && r >= e.row_lo) e.logits[(size_t)(r - e.row_lo) * p.V + col] = v;
+      if (valid && e.logits != nullptr && r >= e.row_lo) stg(e.logits + (size_t)(r - e.row_lo) * p.V + col, v);
       float mv = valid ? v : -INFINITY;
       int mi = valid ? col : 0x7fffffff;
 #pragma unroll
@@ -411,7 +439,7 @@ __device__ __forceinline__ void epilogue(const PassParams& p, const EpiArgs& e, 
 // (§3.2): node i is reachable when its parent is and its draft token equals
 // the target's token after the parent; the result is the deepest reachable
 // node (lowest index among equally deep ones).
-__device__ __forceinline__ void finish_walk(const PassParams& p, int entries, GemmLds& gl) {
+__device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl) {
   const int wave = wave_index(), lane = threadIdx.x & 63;
   for (int r = wave; r < p.n; r += kWaves) {
     float mv = -INFINITY;
@@ -434,15 +462,20 @@ __device__ __forceinline__ void finish_walk(const PassParams& p, int entries, Ge
     }
     wave_argmax(mv, mi);
     if (lane == 0) {
-      p.amax[r] = mi;
+      stg(p.amax + r, mi);
       gl.amax[r] = mi;
     }
   }
+  for (int i = threadIdx.x; i < p.n; i += kThreads) {
+    gl.tok[i] = ldg(p.tree + i);
+    gl.par[i] = ldg(p.tree + 128 + i);
+    gl.dep[i] = ldg(p.tree + 256 + i);
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
-    const int* tok = p.tree;
-    const int* par = p.tree + 128;
-    const int* dep = p.tree + 256;
+    const int* tok = gl.tok;
+    const int* par = gl.par;
+    const int* dep = gl.dep;
     int best = 0, best_depth = 0;
     gl.reach[0] = 1;
     for (int i = 1; i < p.n; ++i) {
@@ -454,10 +487,18 @@ __device__ __forceinline__ void finish_walk(const PassParams& p, int entries, Ge
         best_depth = dep[i];
       }
     }
-    for (int k = 0; k < p.n; ++k) p.path[k] = -1;
-    for (int i = best; i >= 0; i = par[i]) p.path[dep[i]] = i;
-    *p.accept_len = best_depth;
-    *p.next_token = gl.amax[best];
+    for (int i = best; i >= 0; i = par[i]) gl.reach[dep[i]] = -1 - i;  // path by depth, encoded
+    gl.walk_len = best_depth;
+    stg(p.accept_len, best_depth);
+    stg(p.next_token, gl.amax[best]);
+  }
+  __syncthreads();
+  {
+    const int best_depth = gl.walk_len;
+    for (int k = threadIdx.x; k < p.n; k += kThreads) {
+      const int v = gl.reach[k];
+      stg(p.path + k, (k <= best_depth && v < 0) ? -1 - v : -1);
+    }
   }
   __syncthreads();
 }
@@ -481,7 +522,7 @@ __device__ __forceinline__ void l2_prefetch(Prefetch& pf, const bf16x8* w, int k
     const int it = i < total ? i : (total > 0 ? total - 1 : 0);
     const int c = it % nbs, s = s0 + kWaves * (it / nbs);
     const size_t blk = total > 0 ? ((size_t)(nb0 + c) * ks + s) : 0;
-    pf.v[i] = w[blk * 64 + lane];
+    pf.v[i] = ldg(w + blk * 64 + lane);
   }
 }
 __device__ __forceinline__ uint32_t prefetch_fold(const Prefetch& pf) {
@@ -501,13 +542,13 @@ __device__ __forceinline__ int next_width(int rem) {
 }
 
 template <int MB, int PRO, int EPI, int CM>
-__device__ __forceinline__ void main_subblock(const PassParams& p, const GemmDesc& g, const EpiArgs& e,
+__device__ __forceinline__ void main_subblock(KParams& p, const GemmDesc& g, const EpiArgs& e,
                                               int nb0, const float (&rstd)[MB], float* tileS,
                                               GemmLds& gl, int lm_entry) {
   Pipe<MB, PRO, CM> P;
   pipe_setup(P, g, nb0, 0, g.ks);
   f32x4 acc[MB][CM];
-  pipe_run(P, g, p.d, false, acc, rstd);
+  pipe_run(P, g, p.d, acc, rstd);
   reduce_waves<MB, CM>(tileS, acc);
   epilogue<MB, EPI, CM>(p, e, tileS, nb0, lm_entry, gl);
   __syncthreads();
@@ -516,10 +557,76 @@ __device__ __forceinline__ void main_subblock(const PassParams& p, const GemmDes
 // One GEMM phase: warm L2 with the first weights, wait at the barrier, then
 // the remainder runs (stream-K, one n-block per segment) and the main block
 // (whole n-blocks over the full K, in sub-blocks of 4, 3, 2 or 1 n-blocks).
+// The GEMM steps of the pass and their operands.
+enum Step { STEP_QKV = 0, STEP_O = 1, STEP_GATE_UP = 2, STEP_DOWN = 3, STEP_LM = 4 };
+
+__device__ __forceinline__ void step_operands(KParams& p, int step, int l, GemmDesc& g, EpiArgs& e) {
+  const size_t xsz = (size_t)p.Mp * p.d, ssz = (size_t)p.d_nb * p.Mp;
+  const char* lw = p.packed + p.layer0 + (long long)l * p.layer_bytes;
+  g = GemmDesc{};
+  e = EpiArgs{};
+  switch (step) {
+    case STEP_QKV:  // RMSNorm(x_2l) -> q, k (raw) and v (to the cache)
+      g.w = (const bf16x8*)(lw + p.o_qkv);
+      g.nbt = p.qkv_nb;
+      g.ks = p.ks_d;
+      g.x = p.x + (size_t)(2 * l) * xsz;
+      g.ssq = p.ssq + (size_t)(2 * l) * ssz;
+      g.gain = (const bf16*)(lw + p.o_attn_norm);
+      e.qk = p.qk + (size_t)l * p.Mp * 2 * p.d;
+      e.vc = p.v_cache + (size_t)l * p.H * p.cap * p.Dh;
+      break;
+    case STEP_O:  // x_2l+1 = x_2l + o W_o^T
+      g.w = (const bf16x8*)(lw + p.o_o);
+      g.nbt = p.d_nb;
+      g.ks = p.ks_d;
+      g.a = p.o + (size_t)l * p.Mp * p.d;
+      g.lda = p.d;
+      e.x_in = p.x + (size_t)(2 * l) * xsz;
+      e.x_out = p.x + (size_t)(2 * l + 1) * xsz;
+      e.ssq_out = p.ssq + (size_t)(2 * l + 1) * ssz;
+      break;
+    case STEP_GATE_UP:  // h = SwiGLU(RMSNorm(x_2l+1))
+      g.w = (const bf16x8*)(lw + p.o_gu);
+      g.nbt = p.gu_nb;
+      g.ks = p.ks_d;
+      g.x = p.x + (size_t)(2 * l + 1) * xsz;
+      g.ssq = p.ssq + (size_t)(2 * l + 1) * ssz;
+      g.gain = (const bf16*)(lw + p.o_ffn_norm);
+      e.h = p.h + (size_t)l * p.Mp * p.Fp;
+      break;
+    case STEP_DOWN:  // x_2l+2 = x_2l+1 + h W_down^T
+      g.w = (const bf16x8*)(lw + p.o_down);
+      g.nbt = p.d_nb;
+      g.ks = p.ks_f;
+      g.a = p.h + (size_t)l * p.Mp * p.Fp;
+      g.lda = p.Fp;
+      e.x_in = p.x + (size_t)(2 * l + 1) * xsz;
+      e.x_out = p.x + (size_t)(2 * l + 2) * xsz;
+      e.ssq_out = p.ssq + (size_t)(2 * l + 2) * ssz;
+      break;
+    default:  // STEP_LM: logits = RMSNorm(x_2L) W_lm^T
+      g.w = (const bf16x8*)(p.packed + p.o_lm);
+      g.nbt = p.v_nb;
+      g.ks = p.ks_d;
+      g.x = p.x + (size_t)(2 * p.L) * xsz;
+      g.ssq = p.ssq + (size_t)(2 * p.L) * ssz;
+      g.gain = (const bf16*)(p.packed + p.o_final_norm);
+      e.logits = p.logits;
+      e.row_lo = p.row_lo;
+      break;
+  }
+}
+
 template <int MB, int PRO, int EPI>
-__device__ __attribute__((noinline)) bool gemm_phase(const PassParams& p, const GemmDesc& g,
-                                                     const EpiArgs& e, const Sync& sy, int phase,
-                                                     float* tileS, GemmLds& gl) {
+__device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& pin, int step, int layer, int phase,
+                                                     float* tileS, GemmLds& gl, int* lds_flag) {
+  KParams& p = uniform_params(pin);
+  const Sync sy = make_sync(p, lds_flag);
+  GemmDesc g;
+  EpiArgs e;
+  step_operands(p, wave_uniform(step), wave_uniform(layer), g, e);
+  phase = wave_uniform(phase);
   constexpr int ROWS = 16 * MB;
   const int G = p.G, gi = blockIdx.x;
   const int c = g.nbt / G, R = g.nbt - c * G;
@@ -542,7 +649,7 @@ __device__ __attribute__((noinline)) bool gemm_phase(const PassParams& p, const 
     if (!grid_wait(sy, phase, G)) return false;
     trace_mark(sy, phase, 1);
     const uint32_t tok = prefetch_fold(pf);
-    if (tok == 0x9e3779b9u && p.G < 0) p.status[1] = (int)tok;  // keeps the prefetch loads
+    if (tok == 0x9e3779b9u && p.G < 0) stg(p.status + 1, (int)tok);  // keeps the prefetch loads
   }
 
   float rstd[MB];
@@ -557,14 +664,14 @@ __device__ __attribute__((noinline)) bool gemm_phase(const PassParams& p, const 
       float ss = 0.0f;
       int t = t0;
       for (; t + 4 <= t1; t += 4) {
-        const float v0 = g.ssq[(size_t)t * p.Mp + r], v1 = g.ssq[(size_t)(t + 1) * p.Mp + r];
-        const float v2 = g.ssq[(size_t)(t + 2) * p.Mp + r], v3 = g.ssq[(size_t)(t + 3) * p.Mp + r];
+        const float v0 = ldg(g.ssq + (size_t)t * p.Mp + r), v1 = ldg(g.ssq + (size_t)(t + 1) * p.Mp + r);
+        const float v2 = ldg(g.ssq + (size_t)(t + 2) * p.Mp + r), v3 = ldg(g.ssq + (size_t)(t + 3) * p.Mp + r);
         ss += v0;
         ss += v1;
         ss += v2;
         ss += v3;
       }
-      for (; t < t1; ++t) ss += g.ssq[(size_t)t * p.Mp + r];
+      for (; t < t1; ++t) ss += ldg(g.ssq + (size_t)t * p.Mp + r);
       gl.part_ss[ch * ROWS + r] = ss;
     }
     __syncthreads();
@@ -588,7 +695,7 @@ __device__ __attribute__((noinline)) bool gemm_phase(const PassParams& p, const 
       Pipe<MB, PRO, 1> P1;
       pipe_setup(P1, g, nb, k0, k1);
       f32x4 acc[MB][1];
-      pipe_run(P1, g, p.d, false, acc, rstd);
+      pipe_run(P1, g, p.d, acc, rstd);
       reduce_waves<MB, 1>(tileS, acc);
     }
     constexpr int TS = 16 + 4;
@@ -682,7 +789,7 @@ __device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) 
 // (position >= prefix_len) are rotated here from the QKV phase's raw k at the
 // node's position and also written to the node's cache slot.
 template <int DH>
-__device__ __forceinline__ void attn_stage(const PassParams& p, char* lds, const bf16* kc, bf16* kc_w,
+__device__ __forceinline__ void attn_stage(KParams& p, char* lds, const bf16* kc, bf16* kc_w,
                                            const bf16* vc, const float* kraw, int h, int p0, int lo,
                                            int hi) {
   using Gm = AttnGeom<DH>;
@@ -696,19 +803,19 @@ __device__ __forceinline__ void attn_stage(const PassParams& p, char* lds, const
     const int pos = p0 + j;
     bf16x8 k0, k1, v0, v1;
     if (pos >= lo && pos < hi) {
-      v0 = *(const bf16x8*)(vc + (size_t)pos * DH + dc);
-      v1 = *(const bf16x8*)(vc + (size_t)pos * DH + dc + HALF);
+      v0 = ldg((const bf16x8*)(vc + (size_t)pos * DH + dc));
+      v1 = ldg((const bf16x8*)(vc + (size_t)pos * DH + dc + HALF));
       if (pos < p.prefix_len) {
-        k0 = *(const bf16x8*)(kc + (size_t)pos * DH + dc);
-        k1 = *(const bf16x8*)(kc + (size_t)pos * DH + dc + HALF);
+        k0 = ldg((const bf16x8*)(kc + (size_t)pos * DH + dc));
+        k1 = ldg((const bf16x8*)(kc + (size_t)pos * DH + dc + HALF));
       } else {
         const int node = pos - p.prefix_len;
         const float* kr = kraw + (size_t)node * 2 * p.d + h * DH;
-        const float4 a0 = *(const float4*)(kr + dc), a1 = *(const float4*)(kr + dc + 4);
-        const float4 b0 = *(const float4*)(kr + dc + HALF), b1 = *(const float4*)(kr + dc + HALF + 4);
+        const float4 a0 = ldg((const float4*)(kr + dc)), a1 = ldg((const float4*)(kr + dc + 4));
+        const float4 b0 = ldg((const float4*)(kr + dc + HALF)), b1 = ldg((const float4*)(kr + dc + HALF + 4));
         const float xa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
         const float xb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-        const float npos = (float)p.tree[384 + node];
+        const float npos = (float)ldg(p.tree + 384 + node);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           float sn, cs;
@@ -716,8 +823,8 @@ __device__ __forceinline__ void attn_stage(const PassParams& p, char* lds, const
           k0[e] = f2bf(xa[e] * cs - xb[e] * sn);
           k1[e] = f2bf(xb[e] * cs + xa[e] * sn);
         }
-        *(bf16x8*)(kc_w + (size_t)pos * DH + dc) = k0;
-        *(bf16x8*)(kc_w + (size_t)pos * DH + dc + HALF) = k1;
+        stg((bf16x8*)(kc_w + (size_t)pos * DH + dc), k0);
+        stg((bf16x8*)(kc_w + (size_t)pos * DH + dc + HALF), k1);
       }
     } else {
 #pragma unroll
@@ -747,8 +854,12 @@ __device__ __forceinline__ void attn_stage(const PassParams& p, char* lds, const
 // is the PV product's k-slot order).  Then the head's splits join and each
 // merges its share of the rows.
 template <int MB, int DH>
-__device__ __attribute__((noinline)) bool attn_phase(const PassParams& p, int layer, const Sync& sy,
-                                                     int phase, char* lds) {
+__device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& pin, int layer, int phase, char* lds,
+                                                     int* lds_flag) {
+  KParams& p = uniform_params(pin);
+  const Sync sy = make_sync(p, lds_flag);
+  layer = wave_uniform(layer);
+  phase = wave_uniform(phase);
   using Gm = AttnGeom<DH>;
   constexpr int CH = Gm::CH, KSTEPS = DH / 32, DB = DH / 16, KST = Gm::KST, VST = Gm::VST;
   constexpr int RPW = MB > 4 ? 2 : 1;
@@ -799,12 +910,12 @@ __device__ __attribute__((noinline)) bool attn_phase(const PassParams& p, int la
       const int rb = wave + 4 * r;
       const int row = 16 * (rb < MBr ? rb : 0) + li;
       const float* qr = qk + (size_t)row * 2 * p.d + h * DH;
-      const float npos = (float)p.tree[384 + row];
+      const float npos = (float)ldg(p.tree + 384 + row);
 #pragma unroll
       for (int ks = 0; ks < KSTEPS / 2; ++ks) {
         const int j0 = 32 * ks + 8 * g;
-        const float4 a0 = *(const float4*)(qr + j0), a1 = *(const float4*)(qr + j0 + 4);
-        const float4 b0 = *(const float4*)(qr + j0 + HALF), b1 = *(const float4*)(qr + j0 + HALF + 4);
+        const float4 a0 = ldg((const float4*)(qr + j0)), a1 = ldg((const float4*)(qr + j0 + 4));
+        const float4 b0 = ldg((const float4*)(qr + j0 + HALF)), b1 = ldg((const float4*)(qr + j0 + HALF + 4));
         const float xa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
         const float xb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
 #pragma unroll
@@ -817,7 +928,7 @@ __device__ __attribute__((noinline)) bool attn_phase(const PassParams& p, int la
       }
       const uint32_t* ap = (const uint32_t*)(p.tree + 512) + row * 4;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) anc[r][w] = ap[w];
+      for (int w = 0; w < 4; ++w) anc[r][w] = ldg(ap + w);
       m_run[r] = -INFINITY;
       l_run[r] = 0.0f;
 #pragma unroll
@@ -930,7 +1041,7 @@ __device__ __attribute__((noinline)) bool attn_phase(const PassParams& p, int la
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0)
-      __hip_atomic_fetch_add(&p.head_cnt[h], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      atomic_add_dev(&p.head_cnt[h], 1);
     if (!wait_at_least(sy, &p.head_cnt[h], S * (layer + 1))) return false;
 
     const int r_lo = s * p.n / S, r_hi = (s + 1) * p.n / S;
@@ -991,7 +1102,7 @@ __device__ __attribute__((noinline)) bool attn_phase(const PassParams& p, int la
 // Tree preparation (every node's depth, position prefix_len + depth, and
 // ancestor-or-self set: its row of the tree masking table) and the residual
 // stream's first version: the nodes' embedding rows.
-__device__ __forceinline__ void embed_phase(const PassParams& p, const TreeArgs& tree, int* par_s) {
+__device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, int* par_s) {
   const bf16* E = (const bf16*)(p.packed + p.o_embed);
   if (blockIdx.x == 0) {
     if (threadIdx.x < 128) par_s[threadIdx.x] = threadIdx.x < p.n ? tree.parent[threadIdx.x] : -1;
@@ -1020,7 +1131,7 @@ __device__ __forceinline__ void embed_phase(const PassParams& p, const TreeArgs&
     const bool valid = m < p.n;
     const bf16* row = E + (size_t)(valid ? tree.tok[m] : 0) * p.d;
     for (int c = threadIdx.x; c < p.d; c += kThreads) {
-      const float v = valid ? bf2f(row[c]) : 0.0f;
+      const float v = valid ? bf2f(ldg(row + c)) : 0.0f;
       st_coherent(&p.x[(size_t)m * p.d + c], v);
       float s = v * v;
       s += __shfl_xor(s, 8, kWave);
@@ -1044,18 +1155,19 @@ constexpr int pass_lds_bytes() {
 }
 
 template <int MB, int DH>
-__global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p, const TreeArgs tree) {
+__global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_arg, const TreeArgs tree) {
   __shared__ __attribute__((aligned(16))) char lds_raw[pass_lds_bytes<MB, DH>()];
   __shared__ GemmLds gl;
   __shared__ int par_s[128];
   __shared__ int flag;
-  const Sync sy{p.bar, p.status, p.spin_limit, &flag,
-                p.trace != nullptr && (int)blockIdx.x < kTraceWgs
-                    ? p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 6
-                    : nullptr};
+  // The parameter block is the first kernel argument: read it in place.
+  KParams& p = *(KParams*)__builtin_amdgcn_kernarg_segment_ptr();
+  if (p.magic != kPassMagic || p.G != p_arg.G || p.n != p_arg.n) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) stg(p_arg.status, 3);
+    return;  // (uniform over the grid: no workgroup reaches a barrier)
+  }
+  const Sync sy = make_sync(p, &flag);
   float* tileS = reinterpret_cast<float*>(lds_raw);
-  const size_t xsz = (size_t)p.Mp * p.d, ssz = (size_t)p.d_nb * p.Mp;
-  const size_t kv_layer = (size_t)p.H * p.cap * p.Dh;
   int phase = 0;
   bool ok = true;
 
@@ -1064,83 +1176,35 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p, c
   ++phase;
 
   for (int l = 0; l < p.L && ok; ++l) {
-    const char* lw = p.packed + p.layer0 + (long long)l * p.layer_bytes;
-    const float* x_a = p.x + (size_t)(2 * l) * xsz;  // layer input
-    float* x_b = p.x + (size_t)(2 * l + 1) * xsz;    // after attention
-    float* x_c = p.x + (size_t)(2 * l + 2) * xsz;    // after the feed-forward block
-    const float* ss_a = p.ssq + (size_t)(2 * l) * ssz;
-    float* ss_b = p.ssq + (size_t)(2 * l + 1) * ssz;
-    float* ss_c = p.ssq + (size_t)(2 * l + 2) * ssz;
-    {  // QKV projection
-      const GemmDesc g{(const bf16x8*)(lw + p.o_qkv), p.qkv_nb, p.ks_d, nullptr, 0, x_a, ss_a,
-                       (const bf16*)(lw + p.o_attn_norm)};
-      EpiArgs e{};
-      e.qk = p.qk + (size_t)l * p.Mp * 2 * p.d;
-      e.vc = p.v_cache + (size_t)l * kv_layer;
-      ok = gemm_phase<MB, PRO_NORM, EPI_QKV>(p, g, e, sy, phase, tileS, gl);
-      if (!ok) break;
-      grid_arrive(sy, phase);
-      ++phase;
-    }
-    ok = attn_phase<MB, DH>(p, l, sy, phase, lds_raw);
+    ok = gemm_phase<MB, PRO_NORM, EPI_QKV>(p, STEP_QKV, l, phase, tileS, gl, &flag);
     if (!ok) break;
-    grid_arrive(sy, phase);
-    ++phase;
-    {  // O projection + residual
-      const GemmDesc g{(const bf16x8*)(lw + p.o_o), p.d_nb, p.ks_d, p.o + (size_t)l * p.Mp * p.d, p.d,
-                       nullptr, nullptr, nullptr};
-      EpiArgs e{};
-      e.x_in = x_a;
-      e.x_out = x_b;
-      e.ssq_out = ss_b;
-      ok = gemm_phase<MB, PRO_BF16, EPI_RESID>(p, g, e, sy, phase, tileS, gl);
-      if (!ok) break;
-      grid_arrive(sy, phase);
-      ++phase;
-    }
-    {  // gate/up + SwiGLU
-      const GemmDesc g{(const bf16x8*)(lw + p.o_gu), p.gu_nb, p.ks_d, nullptr, 0, x_b, ss_b,
-                       (const bf16*)(lw + p.o_ffn_norm)};
-      EpiArgs e{};
-      e.h = p.h + (size_t)l * p.Mp * p.Fp;
-      ok = gemm_phase<MB, PRO_NORM, EPI_SWIGLU>(p, g, e, sy, phase, tileS, gl);
-      if (!ok) break;
-      grid_arrive(sy, phase);
-      ++phase;
-    }
-    {  // down projection + residual
-      const GemmDesc g{(const bf16x8*)(lw + p.o_down), p.d_nb, p.ks_f, p.h + (size_t)l * p.Mp * p.Fp,
-                       p.Fp, nullptr, nullptr, nullptr};
-      EpiArgs e{};
-      e.x_in = x_b;
-      e.x_out = x_c;
-      e.ssq_out = ss_c;
-      ok = gemm_phase<MB, PRO_BF16, EPI_RESID>(p, g, e, sy, phase, tileS, gl);
-      if (!ok) break;
-      grid_arrive(sy, phase);
-      ++phase;
-    }
+    grid_arrive(sy, phase++);
+    ok = attn_phase<MB, DH>(p, l, phase, lds_raw, &flag);
+    if (!ok) break;
+    grid_arrive(sy, phase++);
+    ok = gemm_phase<MB, PRO_BF16, EPI_RESID>(p, STEP_O, l, phase, tileS, gl, &flag);
+    if (!ok) break;
+    grid_arrive(sy, phase++);
+    ok = gemm_phase<MB, PRO_NORM, EPI_SWIGLU>(p, STEP_GATE_UP, l, phase, tileS, gl, &flag);
+    if (!ok) break;
+    grid_arrive(sy, phase++);
+    ok = gemm_phase<MB, PRO_BF16, EPI_RESID>(p, STEP_DOWN, l, phase, tileS, gl, &flag);
+    if (!ok) break;
+    grid_arrive(sy, phase++);
   }
   if (ok) {  // final norm + LM head + argmax + accept walk
-    const GemmDesc g{(const bf16x8*)(p.packed + p.o_lm), p.v_nb, p.ks_d, nullptr, 0,
-                     p.x + (size_t)(2 * p.L) * xsz, p.ssq + (size_t)(2 * p.L) * ssz,
-                     (const bf16*)(p.packed + p.o_final_norm)};
-    EpiArgs e{};
-    e.logits = p.logits;
-    e.row_lo = p.row_lo;
-    if (gemm_phase<MB, PRO_NORM, EPI_LOGITS>(p, g, e, sy, phase, tileS, gl)) trace_mark(sy, phase, 2);
+    if (gemm_phase<MB, PRO_NORM, EPI_LOGITS>(p, STEP_LM, 0, phase, tileS, gl, &flag))
+      trace_mark(sy, phase, 2);
   }
   // Leave the pass: the last workgroup out resets the barrier and join counters.
   if (arrive_last(p.exit_cnt, p.G, &flag)) {
-    if (threadIdx.x < kBarSlots)
-      __hip_atomic_store(p.bar + threadIdx.x * kBarStride, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    for (int h = threadIdx.x; h < p.H; h += kThreads)
-      __hip_atomic_store(&p.head_cnt[h], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x < kBarSlots) st_coherent(p.bar + threadIdx.x * kBarStride, 0);
+    for (int h = threadIdx.x; h < p.H; h += kThreads) st_coherent(&p.head_cnt[h], 0);
   }
 }
 
 template <int MB, int DH>
-hipError_t launch_pass_mb(const PassParams& p, const TreeArgs& tree, hipStream_t st) {
+hipError_t launch_pass_mb(KParams& p, const TreeArgs& tree, hipStream_t st) {
   void* args[] = {(void*)&p, (void*)&tree};
   return hipLaunchCooperativeKernel((const void*)pass_kernel<MB, DH>, dim3(p.G), dim3(kThreads), args,
                                     0, st);
@@ -1157,7 +1221,7 @@ int occupancy_mb() {
 
 }  // namespace
 
-hipError_t launch_pass(int mb, const PassParams& p, const TreeArgs& tree, hipStream_t st) {
+hipError_t launch_pass(int mb, KParams& p, const TreeArgs& tree, hipStream_t st) {
 #define LLMCAD_PASS_CASE(M)                                                 \
   case M:                                                                   \
     return p.Dh == 128 ? launch_pass_mb<M, 128>(p, tree, st)                \
