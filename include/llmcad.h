@@ -160,7 +160,7 @@ const char* llmcad_status_string(int status);
 
 /* Byte offset and size of a named intermediate buffer inside a workspace
  * sized for max_n (for diagnostics): 0 final residual stream fp32 [Mp][d],
- * 1 layer 0's q and k before the rotary embedding fp32 [Mp][2d], 2 layer
+ * 1 layer 0's queries after the rotary embedding bf16 [Mp][d], 2 layer
  * 0's attention output bf16 [Mp][d], 3 layer 0's SwiGLU product bf16
  * [Mp][Fp], 4 per-node greedy token int32 [Mp],
  * 5 pass status int32 (0 = ok; 1 = a grid wait of the single-launch pass ran

@@ -172,7 +172,7 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.tree = (int*)(ws + W.tree);
   p.x = (float*)(ws + W.xs);
   p.ssq = (float*)(ws + W.ssqs);
-  p.qk = (float*)(ws + W.qk);
+  p.q = (bf16*)(ws + W.qs);
   p.o = (bf16*)(ws + W.os);
   p.h = (bf16*)(ws + W.hs);
   p.part = (float*)(ws + W.part);
@@ -250,7 +250,8 @@ int llmcad_pack_layer(const llmcad_config* cfg, int32_t layer, const llmcad_laye
   char* out = (char*)packed + P.layer(layer);
   HIP_TRY(hipMemcpyAsync(out + P.attn_norm, src->attn_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipMemcpyAsync(out + P.ffn_norm, src->ffn_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(launch_pack(src->w_qkv, 3 * s.d, s.d, out + P.w_qkv, s.qkv_nb, s.ks_d, PACK_PLAIN, s.F, st));
+  HIP_TRY(launch_pack(src->w_qkv, 3 * s.d, s.d, out + P.w_qkv, s.qkv_nb, s.ks_d, PACK_QKV_ROPE, s.Dh,
+                      st));
   HIP_TRY(launch_pack(src->w_o, s.d, s.d, out + P.w_o, s.d_nb, s.ks_d, PACK_PLAIN, s.F, st));
   HIP_TRY(launch_pack(src->w_gate_up, 2 * s.F, s.d, out + P.w_gate_up, s.gu_nb, s.ks_d, PACK_GATE_UP,
                       s.F, st));
@@ -433,7 +434,7 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
   const WorkspaceLayout W(s, max_n);
   switch (which) {
     case 0: *offset = W.xs + (size_t)2 * s.L * W.Mp * s.d * 4; *bytes = (size_t)W.Mp * s.d * 4; break;
-    case 1: *offset = W.qk; *bytes = (size_t)W.Mp * 2 * s.d * 4; break;
+    case 1: *offset = W.qs; *bytes = (size_t)W.Mp * s.d * 2; break;
     case 2: *offset = W.os; *bytes = (size_t)W.Mp * s.d * 2; break;
     case 3: *offset = W.hs; *bytes = (size_t)W.Mp * s.Fp * 2; break;
     case 4: *offset = W.amax; *bytes = (size_t)W.Mp * 4; break;

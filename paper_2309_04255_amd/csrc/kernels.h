@@ -10,9 +10,11 @@
 namespace llmcad {
 
 // ---- weight packing (pack.hip)
-enum PackKind { PACK_PLAIN = 0, PACK_GATE_UP = 1 };
+// aux: F (the FFN width) for PACK_GATE_UP, the head dimension for
+// PACK_QKV_ROPE, unused for PACK_PLAIN.
+enum PackKind { PACK_PLAIN = 0, PACK_GATE_UP = 1, PACK_QKV_ROPE = 2 };
 hipError_t launch_pack(const void* w, int N, int K, void* out, int nblocks, int ksteps, int kind,
-                       int F, hipStream_t st);
+                       int aux, hipStream_t st);
 
 // ---- the verification pass as one persistent launch (pass.hip)
 struct TreeArgs {
@@ -44,7 +46,7 @@ struct PassParams {
   int* tree;       // tok | parent | depth | pos | anc
   float* x;        // [2L+1][Mp][d]
   float* ssq;      // [2L+1][d/16][Mp]
-  float* qk;       // [L][Mp][2d]
+  bf16* q;        // [L][Mp][d]   queries after the rotary embedding
   bf16* o;         // [L][Mp][d]
   bf16* h;         // [L][Mp][Fp]
   float* part;     // [G][2][Mp][16]

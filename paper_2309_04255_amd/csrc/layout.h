@@ -107,7 +107,7 @@ struct WorkspaceLayout {
   size_t lm_idx;       // int32 [G + v_nb][Mp]    argmax partials (column)
   size_t xs;           // fp32 [2L+1][Mp][d]      residual stream versions
   size_t ssqs;         // fp32 [2L+1][d/16][Mp]   their per-n-block sums of squares
-  size_t qk;           // fp32 [L][Mp][2d]        q and k before the rotary embedding
+  size_t qs;           // bf16 [L][Mp][d]         queries after the rotary embedding
   size_t os;           // bf16 [L][Mp][d]         attention output
   size_t hs;           // bf16 [L][Mp][Fp]        SwiGLU product
   size_t part;         // fp32 [kPassMaxGrid][2][Mp][16] stream-K partial n-blocks
@@ -140,7 +140,7 @@ struct WorkspaceLayout {
     lm_idx = take((size_t)(kPassMaxGrid + s.v_nb) * Mp * 4);
     xs = take((size_t)(2 * s.L + 1) * Mp * s.d * 4);
     ssqs = take((size_t)(2 * s.L + 1) * s.d_nb * Mp * 4);
-    qk = take((size_t)s.L * Mp * 2 * s.d * 4);
+    qs = take((size_t)s.L * Mp * s.d * 2);
     os = take((size_t)s.L * Mp * s.d * 2);
     hs = take((size_t)s.L * Mp * s.Fp * 2);
     part = take((size_t)kPassMaxGrid * 2 * Mp * kNB * 4);

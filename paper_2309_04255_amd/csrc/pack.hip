@@ -13,14 +13,28 @@
 //  PACK_GATE_UP   n-block i holds gate rows [8i, 8i+8) then up rows
 //                 [8i, 8i+8), so the SwiGLU product of 8 columns is formed
 //                 inside one n-block; F is padded to a multiple of 32 with zeros.
+//  PACK_QKV_ROPE  the fused [q; k; v] projection (N = 3d rows).  In the q and
+//                 k parts, n-block t of a head (Dh / 16 per head) holds that
+//                 head's dims [8t, 8t+8) then [8t + Dh/2, 8t + Dh/2 + 8): the
+//                 pairs the rotary embedding mixes (rotate-half pairing, dim j
+//                 with j + Dh/2) sit 8 columns apart inside one n-block.  The
+//                 v part is plain.
 #include "device.h"
 #include "kernels.h"
 #include "layout.h"
 
 namespace llmcad {
 
-__device__ __forceinline__ int packed_col_to_row(int c, int N, int kind, int F) {
+__device__ __forceinline__ int packed_col_to_row(int c, int N, int kind, int aux) {
   if (kind == PACK_PLAIN) return c < N ? c : -1;
+  if (kind == PACK_QKV_ROPE) {
+    const int d = N / 3, dh = aux;
+    if (c >= 2 * d) return c < N ? c : -1;
+    const int part = c / d, cq = c % d, head = cq / dh, w = cq % dh;
+    const int t = w / kNB, ci = w % kNB;
+    return part * d + head * dh + 8 * t + (ci % 8) + (ci < 8 ? 0 : dh / 2);
+  }
+  const int F = aux;
   const int nb = c / kNB, cc = c % kNB;
   const int f = 8 * nb + (cc % 8);
   if (f >= F) return -1;
@@ -28,14 +42,14 @@ __device__ __forceinline__ int packed_col_to_row(int c, int N, int kind, int F) 
 }
 
 __global__ void pack_kernel(const bf16* __restrict__ w, int N, int K, bf16x8* __restrict__ out,
-                            long total_chunks, int ksteps, int kind, int F) {
+                            long total_chunks, int ksteps, int kind, int aux) {
   for (long ch = blockIdx.x * (long)blockDim.x + threadIdx.x; ch < total_chunks;
        ch += (long)gridDim.x * blockDim.x) {
     const int lane = (int)(ch % 64);
     const long blk = ch / 64;  // nb * ksteps + s
     const int s = (int)(blk % ksteps);
     const int nb = (int)(blk / ksteps);
-    const int row = packed_col_to_row(kNB * nb + lane % 16, N, kind, F);
+    const int row = packed_col_to_row(kNB * nb + lane % 16, N, kind, aux);
     const int k0 = kStepK * s + 8 * (lane / 16);
     bf16x8 v;
 #pragma unroll
@@ -48,12 +62,12 @@ __global__ void pack_kernel(const bf16* __restrict__ w, int N, int K, bf16x8* __
 }
 
 hipError_t launch_pack(const void* w, int N, int K, void* out, int nblocks, int ksteps, int kind,
-                       int F, hipStream_t st) {
+                       int aux, hipStream_t st) {
   const long total = (long)nblocks * ksteps * 64;
   long blocks = (total + 255) / 256;
   if (blocks > 65536) blocks = 65536;
   pack_kernel<<<dim3((unsigned)blocks), dim3(256), 0, st>>>((const bf16*)w, N, K, (bf16x8*)out,
-                                                             total, ksteps, kind, F);
+                                                             total, ksteps, kind, aux);
   return hipGetLastError();
 }
 

@@ -167,7 +167,8 @@ struct GemmDesc {
 };
 
 struct EpiArgs {
-  float* qk;          // EPI_QKV: [Mp][2d] q then k, before the rotary embedding
+  bf16* q;            // EPI_QKV: [Mp][d] queries after the rotary embedding
+  bf16* kc;           // EPI_QKV: K cache of this layer [H][cap][Dh]
   bf16* vc;           // EPI_QKV: V cache of this layer [H][cap][Dh]
   const float* x_in;  // EPI_RESID: [Mp][d]
   float* x_out;       // EPI_RESID: [Mp][d]
@@ -271,23 +272,30 @@ __device__ __forceinline__ void pipe_compute(Pipe<MB, PRO, C>& P, int slot, f32x
 // each stage's compute after the previous stage's reload: the compiler's
 // wait before a compute then only covers that stage's own loads, and the
 // (D - 1) younger stages stay in flight.
-template <int MB, int PRO, int C>
+// `hook` runs (in every wave) once the first stages are in flight; the first
+// pipeline of a phase computes the RMSNorm scales there, so their loads
+// overlap the weight stream.
+template <int MB, int PRO, int C, class Hook>
 __device__ __forceinline__ void pipe_run(Pipe<MB, PRO, C>& P, const GemmDesc& g, int d,
-                                         f32x4 (&acc)[MB][C], const float (&rstd)[MB]) {
+                                         f32x4 (&acc)[MB][C], const float (&rstd)[MB], Hook&& hook) {
   constexpr int D = Pipe<MB, PRO, C>::D;
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
     for (int c = 0; c < C; ++c) acc[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int ns = P.ns;  // wave-uniform
-  if (ns == 0) return;
+  if (ns > 0) {
 #pragma unroll
-  for (int u = 0; u < D; ++u) {
-    const int st = u < ns ? u : ns - 1;
-    pipe_load_b(P, u, st);
-    pipe_load_a(P, g, d, u, st);
-    __builtin_amdgcn_sched_barrier(0);  // stages issue in order
+    for (int u = 0; u < D; ++u) {
+      const int st = u < ns ? u : ns - 1;
+      pipe_load_b(P, u, st);
+      pipe_load_a(P, g, d, u, st);
+      __builtin_amdgcn_sched_barrier(0);  // stages issue in order
+    }
   }
+  hook();
+  __builtin_amdgcn_sched_barrier(0);
+  if (ns == 0) return;
   for (int i = 0; i < ns; i += D) {
 #pragma unroll
     for (int u = 0; u < D; ++u) {
@@ -342,6 +350,11 @@ struct GemmLds {
   int best_i[kMaxNodes];
 };
 
+// Rotary embedding frequency of dim pair (j, j + Dh/2): theta^(-2j/Dh).
+__device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) {
+  return exp2f(-(2.0f * (float)j / (float)Dh) * log2_theta);
+}
+
 // Epilogue of C n-blocks [nb0, nb0 + C) held in tileS: writes the phase's
 // outputs with device-coherent stores.  lm_entry: argmax partial slot.
 template <int MB, int EPI, int C>
@@ -350,18 +363,40 @@ __device__ __forceinline__ void epilogue(KParams& p, const EpiArgs& e, float* ti
   constexpr int ROWS = 16 * MB, COLS = 16 * C, TS = COLS + 4;
   const int lane = threadIdx.x & 63;
   if constexpr (EPI == EPI_QKV) {
-    const int d = p.d;
-    for (int idx = threadIdx.x; idx < ROWS * COLS; idx += kThreads) {
-      const int r = idx / COLS, cc = idx % COLS;
+    // One thread per (row, column pair cc, cc + 8) of an n-block.  q and k
+    // n-blocks hold rotary pairs 8 columns apart (PACK_QKV_ROPE): rotate at
+    // the node's position, then store q, and k into the node's cache slot.
+    // v n-blocks are plain.  Stores go out in adjacent pairs of dims (this
+    // lane and the next).
+    const int d = p.d, dh = p.Dh, half = dh / 2;
+    for (int idx = threadIdx.x; idx < ROWS * (COLS / 2); idx += kThreads) {
+      const int r = idx / (COLS / 2), ps = idx % (COLS / 2);
+      const int cc = kNB * (ps / 8) + (ps % 8);
       const int col = kNB * nb0 + cc;
-      const float v = tileS[r * TS + cc];
-      const float nxt = __shfl_down(v, 1, kWave);
-      if (r >= p.n) continue;
+      const float a = tileS[r * TS + cc], b = tileS[r * TS + cc + 8];
+      const bool store = r < p.n && (ps & 1) == 0;
       if (col < 2 * d) {
-        st_coherent(&e.qk[(size_t)r * 2 * d + col], v);
-      } else if ((cc & 1) == 0) {
-        const int j = col - 2 * d, hh = j / p.Dh, dd = j % p.Dh;
-        st_coherent_bf2(e.vc + ((size_t)hh * p.cap + p.prefix_len + r) * p.Dh + dd, v, nxt);
+        const int part = col / d, cq = col % d, hh = cq / dh, w = cq % dh;
+        const int j = 8 * (w / kNB) + (w % kNB);  // < Dh/2
+        const int pos = r < p.n ? ldg(p.tree + 384 + r) : 0;
+        float sn, cs;
+        sincosf((float)pos * rope_inv_freq(j, dh, p.log2_theta), &sn, &cs);
+        const float lo = a * cs - b * sn, hi = b * cs + a * sn;
+        const float lo1 = __shfl_down(lo, 1, kWave), hi1 = __shfl_down(hi, 1, kWave);
+        if (store) {
+          bf16* dst = part == 0 ? e.q + (size_t)r * d + hh * dh
+                                : e.kc + ((size_t)hh * p.cap + p.prefix_len + r) * dh;
+          st_coherent_bf2(dst + j, lo, lo1);
+          st_coherent_bf2(dst + j + half, hi, hi1);
+        }
+      } else {
+        const int j = col - 2 * d, hh = j / dh, dd = j % dh;
+        const float a1 = __shfl_down(a, 1, kWave), b1 = __shfl_down(b, 1, kWave);
+        if (store) {
+          bf16* dst = e.vc + ((size_t)hh * p.cap + p.prefix_len + r) * dh + dd;
+          st_coherent_bf2(dst, a, a1);
+          st_coherent_bf2(dst + 8, b, b1);
+        }
       }
     }
   } else if constexpr (EPI == EPI_RESID) {
@@ -532,31 +567,7 @@ __device__ __forceinline__ uint32_t prefetch_fold(const Prefetch& pf) {
   return tok;
 }
 
-// Main-block widths: the largest allowed width <= remaining.
-template <int EPI>
-__device__ __forceinline__ int next_width(int rem) {
-  if (rem >= 4) return 4;
-  if (EPI == EPI_QKV && rem == 3) return 3;
-  if (rem >= 2) return 2;
-  return 1;
-}
 
-template <int MB, int PRO, int EPI, int CM>
-__device__ __forceinline__ void main_subblock(KParams& p, const GemmDesc& g, const EpiArgs& e,
-                                              int nb0, const float (&rstd)[MB], float* tileS,
-                                              GemmLds& gl, int lm_entry) {
-  Pipe<MB, PRO, CM> P;
-  pipe_setup(P, g, nb0, 0, g.ks);
-  f32x4 acc[MB][CM];
-  pipe_run(P, g, p.d, acc, rstd);
-  reduce_waves<MB, CM>(tileS, acc);
-  epilogue<MB, EPI, CM>(p, e, tileS, nb0, lm_entry, gl);
-  __syncthreads();
-}
-
-// One GEMM phase: warm L2 with the first weights, wait at the barrier, then
-// the remainder runs (stream-K, one n-block per segment) and the main block
-// (whole n-blocks over the full K, in sub-blocks of 4, 3, 2 or 1 n-blocks).
 // The GEMM steps of the pass and their operands.
 enum Step { STEP_QKV = 0, STEP_O = 1, STEP_GATE_UP = 2, STEP_DOWN = 3, STEP_LM = 4 };
 
@@ -573,7 +584,8 @@ __device__ __forceinline__ void step_operands(KParams& p, int step, int l, GemmD
       g.x = p.x + (size_t)(2 * l) * xsz;
       g.ssq = p.ssq + (size_t)(2 * l) * ssz;
       g.gain = (const bf16*)(lw + p.o_attn_norm);
-      e.qk = p.qk + (size_t)l * p.Mp * 2 * p.d;
+      e.q = p.q + (size_t)l * p.Mp * p.d;
+      e.kc = p.k_cache + (size_t)l * p.H * p.cap * p.Dh;
       e.vc = p.v_cache + (size_t)l * p.H * p.cap * p.Dh;
       break;
     case STEP_O:  // x_2l+1 = x_2l + o W_o^T
@@ -618,6 +630,105 @@ __device__ __forceinline__ void step_operands(KParams& p, int step, int l, GemmD
   }
 }
 
+// RMSNorm scales of the rows (this lane's row 16 rb + lane % 16 for each row
+// block rb): 1 / sqrt(mean of squares + eps), from the per-n-block sums of
+// squares the producing phase wrote.
+template <int MB>
+__device__ __forceinline__ void row_scales(KParams& p, const GemmDesc& g, GemmLds& gl, float (&rstd)[MB]) {
+  constexpr int ROWS = 16 * MB, CHK = 256 / ROWS;
+  const int lrow = threadIdx.x & 15;
+  const int dn = p.d_nb;
+  if (threadIdx.x < CHK * ROWS) {
+    const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
+    const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
+    float ss = 0.0f;
+    int t = t0;
+    for (; t + 4 <= t1; t += 4) {
+      const float v0 = ldg(g.ssq + (size_t)t * p.Mp + r), v1 = ldg(g.ssq + (size_t)(t + 1) * p.Mp + r);
+      const float v2 = ldg(g.ssq + (size_t)(t + 2) * p.Mp + r), v3 = ldg(g.ssq + (size_t)(t + 3) * p.Mp + r);
+      ss += v0;
+      ss += v1;
+      ss += v2;
+      ss += v3;
+    }
+    for (; t < t1; ++t) ss += ldg(g.ssq + (size_t)t * p.Mp + r);
+    gl.part_ss[ch * ROWS + r] = ss;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb) {
+    const int row = 16 * rb + lrow;
+    float ss = 0.0f;
+#pragma unroll
+    for (int ch = 0; ch < CHK; ++ch) ss += gl.part_ss[ch * ROWS + row];
+    rstd[rb] = 1.0f / sqrtf(ss * p.inv_d + p.eps);
+  }
+  __syncthreads();
+}
+
+template <int MB>
+struct RowScale {
+  float v[MB];
+};
+
+// Widest main-block sub-block (n-blocks streamed together, sharing one pass
+// over the A operand) that the registers allow at MB row blocks.
+template <int MB>
+constexpr int max_width() {
+  return MB <= 2 ? 8 : (MB <= 4 ? 4 : 2);
+}
+
+// CM whole n-blocks [nb0, nb0 + CM) over the full K.  A function of its own
+// per width, so each width gets its own register allocation.  When need_rs
+// is set the RMSNorm scales are computed here, once the first weight stages
+// are in flight; the scales used are returned.
+template <int MB, int PRO, int EPI, int CM>
+__device__ __attribute__((noinline, not_tail_called)) RowScale<MB> main_block(
+    KParams& pin, int step, int layer, int nb0, RowScale<MB> rs, int need_rs, float* tileS, GemmLds& gl,
+    int lm_entry) {
+  KParams& p = uniform_params(pin);
+  GemmDesc g;
+  EpiArgs e;
+  step_operands(p, wave_uniform(step), wave_uniform(layer), g, e);
+  nb0 = wave_uniform(nb0);
+  lm_entry = wave_uniform(lm_entry);
+  bool need = wave_uniform(need_rs) != 0;
+  float rstd[MB];
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb) rstd[rb] = rs.v[rb];
+  auto hook = [&]() {
+    if constexpr (PRO == PRO_NORM) {
+      if (need) row_scales<MB>(p, g, gl, rstd);
+    }
+  };
+  Pipe<MB, PRO, CM> P;
+  pipe_setup(P, g, nb0, 0, g.ks);
+  f32x4 acc[MB][CM];
+  pipe_run(P, g, p.d, acc, rstd, hook);
+  reduce_waves<MB, CM>(tileS, acc);
+  epilogue<MB, EPI, CM>(p, e, tileS, nb0, lm_entry, gl);
+  __syncthreads();
+  RowScale<MB> out;
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb) out.v[rb] = rstd[rb];
+  return out;
+}
+
+template <int MB, int PRO, int EPI, int W>
+__device__ __forceinline__ RowScale<MB> main_dispatch(int w, KParams& p, int step, int layer, int nb0,
+                                                      RowScale<MB> rs, int need_rs, float* tileS,
+                                                      GemmLds& gl, int lm) {
+  if constexpr (W >= 1) {
+    if (w == W) return main_block<MB, PRO, EPI, W>(p, step, layer, nb0, rs, need_rs, tileS, gl, lm);
+    return main_dispatch<MB, PRO, EPI, W - 1>(w, p, step, layer, nb0, rs, need_rs, tileS, gl, lm);
+  } else {
+    return rs;
+  }
+}
+
+// One GEMM phase: warm L2 with the first weights, wait at the barrier, then
+// the remainder runs (stream-K, one n-block per segment) and the main block
+// (whole n-blocks over the full K, in sub-blocks of 4, 3, 2 or 1 n-blocks).
 template <int MB, int PRO, int EPI>
 __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& pin, int step, int layer, int phase,
                                                      float* tileS, GemmLds& gl, int* lds_flag) {
@@ -632,7 +743,6 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   const int c = g.nbt / G, R = g.nbt - c * G;
   const long Wr = (long)R * g.ks;
   const long rbeg = (long)gi * Wr / G, rend = (long)(gi + 1) * Wr / G;
-  const int lrow = (threadIdx.x & 63) & 15;
 
   {
     Prefetch pf;
@@ -641,7 +751,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
       const int k1 = (int)(k0 + (rend - rbeg) < g.ks ? k0 + (rend - rbeg) : g.ks);
       l2_prefetch(pf, g.w, g.ks, c * G + t, 1, k0, k1);
     } else if (c > 0) {
-      l2_prefetch(pf, g.w, g.ks, gi * c, next_width<EPI>(c), 0, g.ks);
+      l2_prefetch(pf, g.w, g.ks, gi * c, c < max_width<MB>() ? c : max_width<MB>(), 0, g.ks);
     } else {
       l2_prefetch(pf, g.w, g.ks, 0, 1, 0, 0);
     }
@@ -655,36 +765,16 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   float rstd[MB];
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb) rstd[rb] = 1.0f;
-  if constexpr (PRO == PRO_NORM) {
-    constexpr int CHK = 256 / ROWS;
-    const int dn = p.d_nb;
-    if (threadIdx.x < CHK * ROWS) {
-      const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
-      const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
-      float ss = 0.0f;
-      int t = t0;
-      for (; t + 4 <= t1; t += 4) {
-        const float v0 = ldg(g.ssq + (size_t)t * p.Mp + r), v1 = ldg(g.ssq + (size_t)(t + 1) * p.Mp + r);
-        const float v2 = ldg(g.ssq + (size_t)(t + 2) * p.Mp + r), v3 = ldg(g.ssq + (size_t)(t + 3) * p.Mp + r);
-        ss += v0;
-        ss += v1;
-        ss += v2;
-        ss += v3;
-      }
-      for (; t < t1; ++t) ss += ldg(g.ssq + (size_t)t * p.Mp + r);
-      gl.part_ss[ch * ROWS + r] = ss;
+  // RMSNorm scales: computed by the first pipeline of the phase once its
+  // first stages are in flight.
+  bool need_rstd = PRO == PRO_NORM;
+  auto rstd_hook = [&]() {
+    if constexpr (PRO == PRO_NORM) {
+      if (!need_rstd) return;
+      need_rstd = false;
+      row_scales<MB>(p, g, gl, rstd);
     }
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < MB; ++rb) {
-      const int row = 16 * rb + lrow;
-      float ss = 0.0f;
-#pragma unroll
-      for (int ch = 0; ch < CHK; ++ch) ss += gl.part_ss[ch * ROWS + row];
-      rstd[rb] = 1.0f / sqrtf(ss * p.inv_d + p.eps);
-    }
-  }
-  trace_mark(sy, phase, 3);
+  };
 
   // Remainder n-blocks (stream-K), one n-block per segment.
   for (long pos = rbeg; pos < rend;) {
@@ -695,7 +785,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
       Pipe<MB, PRO, 1> P1;
       pipe_setup(P1, g, nb, k0, k1);
       f32x4 acc[MB][1];
-      pipe_run(P1, g, p.d, acc, rstd);
+      pipe_run(P1, g, p.d, acc, rstd, rstd_hook);
       reduce_waves<MB, 1>(tileS, acc);
     }
     constexpr int TS = 16 + 4;
@@ -740,19 +830,19 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
 
   // Main block: n-blocks [gi c, (gi + 1) c) over the full K.  For the LM head
   // the workgroup's argmax entry is the best over its sub-blocks.
+  trace_mark(sy, phase, 3);
   for (int done = 0; done < c;) {
-    const int w = next_width<EPI>(c - done);
+    const int w = c - done < max_width<MB>() ? c - done : max_width<MB>();
     const int nb0 = gi * c + done;
     const int lm = done == 0 ? -2 : -1;
-    if (w == 4) {
-      main_subblock<MB, PRO, EPI, 4>(p, g, e, nb0, rstd, tileS, gl, lm);
-    } else if (w == 3) {
-      if constexpr (EPI == EPI_QKV) main_subblock<MB, PRO, EPI, 3>(p, g, e, nb0, rstd, tileS, gl, lm);
-    } else if (w == 2) {
-      main_subblock<MB, PRO, EPI, 2>(p, g, e, nb0, rstd, tileS, gl, lm);
-    } else {
-      main_subblock<MB, PRO, EPI, 1>(p, g, e, nb0, rstd, tileS, gl, lm);
-    }
+    RowScale<MB> rs;
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) rs.v[rb] = rstd[rb];
+    rs = main_dispatch<MB, PRO, EPI, max_width<MB>()>(w, p, step, layer, nb0, rs, need_rstd ? 1 : 0,
+                                                       tileS, gl, lm);
+    need_rstd = false;
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) rstd[rb] = rs.v[rb];
     done += w;
   }
   trace_mark(sy, phase, 4);
@@ -780,68 +870,33 @@ struct AttnGeom {
   static constexpr int BYTES = KS_BYTES + VT_BYTES;
 };
 
-__device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) {
-  return exp2f(-(2.0f * (float)j / (float)Dh) * log2_theta);
-}
-
-// Stage key positions [p0, p0 + CH) ∩ [lo, hi) of head h into LDS: K row-major,
-// V transposed; other rows zero.  Prefix keys come from the cache; tree keys
-// (position >= prefix_len) are rotated here from the QKV phase's raw k at the
-// node's position and also written to the node's cache slot.
+// Stage key positions [p0, p0 + CH) ∩ [lo, hi) of one head into LDS: K
+// row-major, V transposed; other rows zero.  Every key comes from the cache:
+// the tree's keys and values were written to their slots, already rotated,
+// by the QKV phase.
 template <int DH>
-__device__ __forceinline__ void attn_stage(KParams& p, char* lds, const bf16* kc, bf16* kc_w,
-                                           const bf16* vc, const float* kraw, int h, int p0, int lo,
+__device__ __forceinline__ void attn_stage(char* lds, const bf16* kc, const bf16* vc, int p0, int lo,
                                            int hi) {
   using Gm = AttnGeom<DH>;
   bf16* Ks = reinterpret_cast<bf16*>(lds);
   bf16* Vt = reinterpret_cast<bf16*>(lds + Gm::KS_BYTES);
-  constexpr int HALF = DH / 2;
-  // (position, 8-dim chunk of the first half); the chunk's rotary partner
-  // (+DH/2) is handled by the same thread.
-  for (int idx = threadIdx.x; idx < Gm::CH * (HALF / 8); idx += kThreads) {
-    const int j = idx / (HALF / 8), dc = (idx % (HALF / 8)) * 8;
+  for (int idx = threadIdx.x; idx < Gm::CH * (DH / 8); idx += kThreads) {
+    const int j = idx / (DH / 8), dc = (idx % (DH / 8)) * 8;
     const int pos = p0 + j;
-    bf16x8 k0, k1, v0, v1;
+    bf16x8 k0, v0;
     if (pos >= lo && pos < hi) {
+      k0 = ldg((const bf16x8*)(kc + (size_t)pos * DH + dc));
       v0 = ldg((const bf16x8*)(vc + (size_t)pos * DH + dc));
-      v1 = ldg((const bf16x8*)(vc + (size_t)pos * DH + dc + HALF));
-      if (pos < p.prefix_len) {
-        k0 = ldg((const bf16x8*)(kc + (size_t)pos * DH + dc));
-        k1 = ldg((const bf16x8*)(kc + (size_t)pos * DH + dc + HALF));
-      } else {
-        const int node = pos - p.prefix_len;
-        const float* kr = kraw + (size_t)node * 2 * p.d + h * DH;
-        const float4 a0 = ldg((const float4*)(kr + dc)), a1 = ldg((const float4*)(kr + dc + 4));
-        const float4 b0 = ldg((const float4*)(kr + dc + HALF)), b1 = ldg((const float4*)(kr + dc + HALF + 4));
-        const float xa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-        const float xb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-        const float npos = (float)ldg(p.tree + 384 + node);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          float sn, cs;
-          sincosf(npos * rope_inv_freq(dc + e, DH, p.log2_theta), &sn, &cs);
-          k0[e] = f2bf(xa[e] * cs - xb[e] * sn);
-          k1[e] = f2bf(xb[e] * cs + xa[e] * sn);
-        }
-        stg((bf16x8*)(kc_w + (size_t)pos * DH + dc), k0);
-        stg((bf16x8*)(kc_w + (size_t)pos * DH + dc + HALF), k1);
-      }
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         k0[e] = (bf16)0.0f;
-        k1[e] = (bf16)0.0f;
         v0[e] = (bf16)0.0f;
-        v1[e] = (bf16)0.0f;
       }
     }
     *(bf16x8*)&Ks[j * Gm::KST + dc] = k0;
-    *(bf16x8*)&Ks[j * Gm::KST + dc + HALF] = k1;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      Vt[(dc + e) * Gm::VST + j] = v0[e];
-      Vt[(dc + HALF + e) * Gm::VST + j] = v1[e];
-    }
+    for (int e = 0; e < 8; ++e) Vt[(dc + e) * Gm::VST + j] = v0[e];
   }
 }
 
@@ -863,7 +918,6 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
   using Gm = AttnGeom<DH>;
   constexpr int CH = Gm::CH, KSTEPS = DH / 32, DB = DH / 16, KST = Gm::KST, VST = Gm::VST;
   constexpr int RPW = MB > 4 ? 2 : 1;
-  constexpr int HALF = DH / 2;
   const int S = wave_uniform(p.attn_splits);
   const int units = wave_uniform(p.H) * S;
   const int total = wave_uniform(p.prefix_len + p.n);
@@ -872,7 +926,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
   const size_t kv_layer = (size_t)p.H * p.cap * DH;
   bf16* kcl = p.k_cache + (size_t)layer * kv_layer;
   const bf16* vcl = p.v_cache + (size_t)layer * kv_layer;
-  const float* qk = p.qk + (size_t)layer * p.Mp * 2 * p.d;
+  const bf16* qb = p.q + (size_t)layer * p.Mp * p.d;
   bf16* Ks = reinterpret_cast<bf16*>(lds);
   bf16* Vt = reinterpret_cast<bf16*>(lds + Gm::KS_BYTES);
 
@@ -885,8 +939,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
     const int lo = (s * total / S) & ~15, hi = s + 1 == S ? total : ((s + 1) * total / S) & ~15;
     const int hi0 = lo + CH < hi ? lo + CH : hi;
     if (lo < hi && hi0 <= p.prefix_len) {
-      attn_stage<DH>(p, lds, kcl + (size_t)h * p.cap * DH, kcl + (size_t)h * p.cap * DH,
-                     vcl + (size_t)h * p.cap * DH, qk + p.d, h, lo, lo, hi0);
+      attn_stage<DH>(lds, kcl + (size_t)h * p.cap * DH, vcl + (size_t)h * p.cap * DH, lo, lo, hi0);
       staged = true;
     }
   }
@@ -900,7 +953,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
     bf16* kc = kcl + (size_t)h * p.cap * DH;
     const bf16* vc = vcl + (size_t)h * p.cap * DH;
     // Query fragments (B operand of S^T = K q^T): lane holds row 16 rb + li,
-    // dims 32 ks + 8 g + e; rotated here at the node's position.
+    // dims 32 ks + 8 g + e (queries were rotated by the QKV phase).
     bf16x8 qf[RPW][KSTEPS];
     uint32_t anc[RPW][4];
     float m_run[RPW], l_run[RPW];
@@ -909,23 +962,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
     for (int r = 0; r < RPW; ++r) {
       const int rb = wave + 4 * r;
       const int row = 16 * (rb < MBr ? rb : 0) + li;
-      const float* qr = qk + (size_t)row * 2 * p.d + h * DH;
-      const float npos = (float)ldg(p.tree + 384 + row);
+      const bf16* qrow = qb + (size_t)row * p.d + h * DH;
 #pragma unroll
-      for (int ks = 0; ks < KSTEPS / 2; ++ks) {
-        const int j0 = 32 * ks + 8 * g;
-        const float4 a0 = ldg((const float4*)(qr + j0)), a1 = ldg((const float4*)(qr + j0 + 4));
-        const float4 b0 = ldg((const float4*)(qr + j0 + HALF)), b1 = ldg((const float4*)(qr + j0 + HALF + 4));
-        const float xa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-        const float xb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          float sn, cs;
-          sincosf(npos * rope_inv_freq(j0 + e, DH, p.log2_theta), &sn, &cs);
-          qf[r][ks][e] = f2bf(xa[e] * cs - xb[e] * sn);
-          qf[r][ks + KSTEPS / 2][e] = f2bf(xb[e] * cs + xa[e] * sn);
-        }
-      }
+      for (int ks = 0; ks < KSTEPS; ++ks) qf[r][ks] = ldg((const bf16x8*)(qrow + 32 * ks + 8 * g));
       const uint32_t* ap = (const uint32_t*)(p.tree + 512) + row * 4;
 #pragma unroll
       for (int w = 0; w < 4; ++w) anc[r][w] = ldg(ap + w);
@@ -934,11 +973,12 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
 #pragma unroll
       for (int db = 0; db < DB; ++db) oacc[r][db] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+    trace_mark(sy, phase, 3);
     for (int p0 = lo; p0 < hi; p0 += CH) {
       const int hi_t = p0 + CH < hi ? p0 + CH : hi;
       if (!staged) {
         __syncthreads();
-        attn_stage<DH>(p, lds, kc, kc, vc, qk + p.d, h, p0, p0, hi_t);
+        attn_stage<DH>(lds, kc, vc, p0, p0, hi_t);
       }
       staged = false;
       __syncthreads();
@@ -1042,7 +1082,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
     __syncthreads();
     if (threadIdx.x == 0)
       atomic_add_dev(&p.head_cnt[h], 1);
+    trace_mark(sy, phase, 4);
     if (!wait_at_least(sy, &p.head_cnt[h], S * (layer + 1))) return false;
+    trace_mark(sy, phase, 5);
 
     const int r_lo = s * p.n / S, r_hi = (s + 1) * p.n / S;
     const int nr = r_hi - r_lo;
@@ -1149,7 +1191,7 @@ template <int MB, int DH>
 constexpr int pass_lds_bytes() {
   constexpr int attn = AttnGeom<DH>::BYTES;
   constexpr int merge = 2 * kAttnMaxSplits * kMaxNodes * 4;
-  constexpr int tile = 16 * MB * (16 * 4 + 4) * 4;
+  constexpr int tile = 16 * MB * (16 * max_width<MB>() + 4) * 4;
   constexpr int m1 = attn > merge ? attn : merge;
   return m1 > tile ? m1 : tile;
 }
