@@ -36,7 +36,7 @@
  *                 w_gate_up [2F][d] (rows gate, then up), w_down [d][F]
  *  - Packed weights: an opaque device image of llmcad_packed_bytes() bytes
  *    written by llmcad_pack_globals / llmcad_pack_layer (MFMA-fragment order:
- *    1 KiB contiguous per 16 output columns x 32 inputs, consecutive inputs
+ *    1 KiB contiguous per 32 output columns x 16 inputs, consecutive inputs
  *    consecutive).  The globals sit
  *    first, then layer 0, 1, ...; an image packed for L layers also serves a
  *    configuration with fewer layers.
@@ -104,12 +104,15 @@ int llmcad_pack_globals(const llmcad_config* cfg, const void* tok_embed, const v
 int llmcad_pack_layer(const llmcad_config* cfg, int32_t layer, const llmcad_layer_weights* src,
                       void* packed, size_t packed_bytes, void* stream);
 
-/* Bytes of workspace for passes of up to max_n nodes (max_n in [1, 128]). */
+/* Bytes of workspace for passes of up to max_n nodes (max_n in [1, 128]) on
+ * the current device (the split of the work, and so the size, depends on its
+ * compute-unit count). */
 size_t llmcad_workspace_bytes(const llmcad_config* cfg, int32_t max_n);
 
-/* Clears the workspace's synchronisation counters.  Call once after
- * allocating a workspace (a zero-filled allocation needs no call); every pass
- * leaves them cleared again. */
+/* Clears the workspace's synchronisation counters and its zero block.  Call
+ * once after allocating a workspace (a zero-filled allocation needs no call);
+ * every pass leaves the counters cleared again and never writes the zero
+ * block. */
 int llmcad_workspace_init(const llmcad_config* cfg, int32_t max_n, void* workspace,
                           size_t workspace_bytes, void* stream);
 
@@ -169,9 +172,11 @@ const char* llmcad_status_string(int status);
  * kernel did not find its parameter block where it reads it, and did
  * nothing),
  * 6 phase timestamps int64 [8][2 + 5L][6] (written when the environment
- * variable LLMCAD_TRACE is 1);
- * Mp = max_n rounded up to 16 (to 128 when max_n > 64), Fp = F rounded up
- * to 32.  Offsets describe a
+ * variable LLMCAD_TRACE is 1), 7 every residual stream version fp32
+ * [2L+1][Mp][d], 8 their per-32-column sums of squares fp32 [2L+1][d/32][Mp],
+ * 9 every layer's queries bf16 [L][Mp][d], 10 attention outputs bf16
+ * [L][Mp][d], 11 SwiGLU products bf16 [L][Mp][Fp];
+ * Mp = max_n rounded up to 32, 64 or 128, Fp = F rounded up to 16.  Offsets describe a
  * pass over max_n nodes (call with max_n = that pass's n). */
 int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t which, size_t* offset,
                             size_t* bytes);

@@ -112,23 +112,31 @@ DeviceInfo device_info() {
   return cache[dev];
 }
 
+// Workgroups of a pass on the current device: one per CU, at most
+// kPassMaxGrid; LLMCAD_PASS_GRID (diagnostics) asks for fewer.  Without a
+// device (sizing on a host with no GPU) the MI355X count, 256, stands in.
+int pass_grid() {
+  const DeviceInfo dev = device_info();
+  int G = dev.cus > 0 ? dev.cus : 256;
+  const int want = env_int("LLMCAD_PASS_GRID", 0);
+  if (want > 0 && want < G) G = want;
+  return G > kPassMaxGrid ? kPassMaxGrid : G;
+}
+
 int run_pass(const Pass& a, const TreeArgs& tree) {
   const Shape s(*a.cfg);
   const PackedLayout P(s);
-  const WorkspaceLayout W(s, a.n);
-  const int MB = W.Mp / 16;
-  const DeviceInfo dev = device_info();
+  const int G = pass_grid();
+  const WorkspaceLayout W(s, a.n, G);
+  const int MB = W.Mp / 32;
   const int occ = pass_occupancy(MB, s.Dh);
-  if (dev.cus <= 0 || occ <= 0) {
+  if (device_info().cus <= 0 || occ * device_info().cus < G) {
     g_last_error = hipErrorInvalidConfiguration;
     return LLMCAD_EHIP;
   }
-  int per_cu = env_int("LLMCAD_PASS_WGS_PER_CU", 1);
-  if (per_cu > occ) per_cu = occ;
-  int G = dev.cus * per_cu;
-  if (G > kPassMaxGrid) G = kPassMaxGrid;
+  const PassPlans plans(s, MB, G);
+  if (!plans.ok()) return LLMCAD_ESHAPE;
   char* ws = a.ws;
-  int* counters = (int*)(ws + W.counters);
 
   PassParams p;
   memset(&p, 0, sizeof(p));
@@ -152,24 +160,31 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.packed = a.packed;
   p.o_embed = (long long)P.embed;
   p.o_final_norm = (long long)P.final_norm;
-  p.o_lm = (long long)P.lm_head;
   p.layer0 = (long long)P.globals_end;
   p.layer_bytes = (long long)P.layer_bytes;
   p.o_attn_norm = (long long)P.attn_norm;
-  p.o_qkv = (long long)P.w_qkv;
-  p.o_o = (long long)P.w_o;
   p.o_ffn_norm = (long long)P.ffn_norm;
-  p.o_gu = (long long)P.w_gate_up;
-  p.o_down = (long long)P.w_down;
-  p.ks_d = s.ks_d;
-  p.ks_f = s.ks_f;
-  p.qkv_nb = s.qkv_nb;
   p.d_nb = s.d_nb;
-  p.gu_nb = s.gu_nb;
-  p.v_nb = s.v_nb;
+  const long long w_off[kSteps] = {(long long)P.w_qkv, (long long)P.w_o, (long long)P.w_gate_up,
+                                   (long long)P.w_down, (long long)P.lm_head};
+  for (int i = 0; i < kSteps; ++i) {
+    const GemmPlan& g = plans.g[i];
+    StepPlan& sp = p.step[i];
+    sp.S = g.S;
+    sp.groups = g.groups;
+    sp.cw = g.cw;
+    sp.n_hi = g.n_hi;
+    sp.nblocks = g.nblocks;
+    sp.ksteps = g.ksteps;
+    sp.w_off = w_off[i];
+    sp.layer_rel = i == STEP_LM ? 0 : 1;
+    sp.group_cnt = (int*)(ws + W.group_counters(i));
+  }
   p.k_cache = (bf16*)a.k_cache;
   p.v_cache = (bf16*)a.v_cache;
   p.tree = (int*)(ws + W.tree);
+  p.zero = ws + W.zero;
+  p.rope = (float*)(ws + W.rope);
   p.x = (float*)(ws + W.xs);
   p.ssq = (float*)(ws + W.ssqs);
   p.q = (bf16*)(ws + W.qs);
@@ -187,8 +202,7 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   if (s.H * S > G) S = G / s.H;
   if (S < 1) S = 1;
   p.attn_splits = S;
-  p.tile_cnt = counters;
-  p.head_cnt = counters + W.n_tile_counters;
+  p.head_cnt = (int*)(ws + W.head_counters());
   p.lm_cnt = (int*)(ws + W.lm_cnt());
   p.exit_cnt = (int*)(ws + W.exit_cnt());
   p.status = (int*)(ws + W.status());
@@ -261,7 +275,7 @@ int llmcad_pack_layer(const llmcad_config* cfg, int32_t layer, const llmcad_laye
 
 size_t llmcad_workspace_bytes(const llmcad_config* cfg, int32_t max_n) {
   if (check_cfg(cfg) != LLMCAD_OK || max_n < 1 || max_n > kMaxNodes) return 0;
-  return WorkspaceLayout(Shape(*cfg), max_n).total;
+  return WorkspaceLayout(Shape(*cfg), max_n, pass_grid()).total;
 }
 
 int llmcad_workspace_init(const llmcad_config* cfg, int32_t max_n, void* workspace,
@@ -269,9 +283,10 @@ int llmcad_workspace_init(const llmcad_config* cfg, int32_t max_n, void* workspa
   int rc = check_cfg(cfg);
   if (rc != LLMCAD_OK) return rc;
   if (!workspace || max_n < 1 || max_n > kMaxNodes) return LLMCAD_EARG;
-  const WorkspaceLayout W(Shape(*cfg), max_n);
+  const WorkspaceLayout W(Shape(*cfg), max_n, pass_grid());
   if (workspace_bytes < W.total) return LLMCAD_EWORKSPACE;
   HIP_TRY(hipMemsetAsync((char*)workspace + W.counters, 0, W.counters_bytes, (hipStream_t)stream));
+  HIP_TRY(hipMemsetAsync((char*)workspace + W.zero, 0, kZeroBytes, (hipStream_t)stream));
   HIP_TRY(hipMemsetAsync((char*)workspace + W.bar, 0, (size_t)kBarSlots * kBarStride * 4,
                           (hipStream_t)stream));
   return LLMCAD_OK;
@@ -295,7 +310,7 @@ int llmcad_verify_tree(const llmcad_config* cfg, const void* packed, void* k_cac
   }
   if (capacity < 1 || prefix_len < 0 || (long)prefix_len + n > capacity) return LLMCAD_ECAPACITY;
   const Shape s(*cfg);
-  if (workspace_bytes < WorkspaceLayout(s, n).total) return LLMCAD_EWORKSPACE;
+  if (workspace_bytes < WorkspaceLayout(s, n, pass_grid()).total) return LLMCAD_EWORKSPACE;
   TreeArgs tree;
   memset(&tree, 0, sizeof(tree));
   for (int i = 0; i < n; ++i) {
@@ -333,13 +348,14 @@ int llmcad_prefill(const llmcad_config* cfg, const void* packed, void* k_cache, 
   const Shape s(*cfg);
   // Largest chain the workspace holds.
   int chunk = 0;
+  const int G = pass_grid();
   for (int m = kMaxNodes; m >= 1; --m)
-    if (WorkspaceLayout(s, m).total <= workspace_bytes) {
+    if (WorkspaceLayout(s, m, G).total <= workspace_bytes) {
       chunk = m;
       break;
     }
   if (chunk == 0) return LLMCAD_EWORKSPACE;
-  const WorkspaceLayout W(s, 1);
+  const WorkspaceLayout W(s, 1, G);
   int* sink = (int*)((char*)workspace + W.scratch_out);  // path/len/next are not needed
   for (int off = 0; off < n_tokens; off += chunk) {
     const int len = (n_tokens - off) < chunk ? (n_tokens - off) : chunk;
@@ -431,7 +447,7 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
   if (rc != LLMCAD_OK) return rc;
   if (!offset || !bytes || max_n < 1 || max_n > kMaxNodes) return LLMCAD_EARG;
   const Shape s(*cfg);
-  const WorkspaceLayout W(s, max_n);
+  const WorkspaceLayout W(s, max_n, pass_grid());
   switch (which) {
     case 0: *offset = W.xs + (size_t)2 * s.L * W.Mp * s.d * 4; *bytes = (size_t)W.Mp * s.d * 4; break;
     case 1: *offset = W.qs; *bytes = (size_t)W.Mp * s.d * 2; break;
@@ -440,6 +456,11 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
     case 4: *offset = W.amax; *bytes = (size_t)W.Mp * 4; break;
     case 5: *offset = W.status(); *bytes = 4; break;
     case 6: *offset = W.trace; *bytes = (size_t)8 * (2 + 5 * s.L) * 6 * 8; break;
+    case 7: *offset = W.xs; *bytes = (size_t)(2 * s.L + 1) * W.Mp * s.d * 4; break;
+    case 8: *offset = W.ssqs; *bytes = (size_t)(2 * s.L + 1) * s.d_nb * W.Mp * 4; break;
+    case 9: *offset = W.qs; *bytes = (size_t)s.L * W.Mp * s.d * 2; break;
+    case 10: *offset = W.os; *bytes = (size_t)s.L * W.Mp * s.d * 2; break;
+    case 11: *offset = W.hs; *bytes = (size_t)s.L * W.Mp * s.Fp * 2; break;
     default: return LLMCAD_EARG;
   }
   return LLMCAD_OK;

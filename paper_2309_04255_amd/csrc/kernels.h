@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include "device.h"
+#include "layout.h"
 
 namespace llmcad {
 
@@ -24,7 +25,16 @@ struct TreeArgs {
 
 // Set in PassParams::magic by the host; the kernel checks it where it reads
 // the parameters in place.
-constexpr int kPassMagic = 0x4c4d4341;
+constexpr int kPassMagic = 0x4c4d4342;
+
+// One GEMM step's tiling (see GemmPlan) and where its weights live.
+struct StepPlan {
+  int S, groups, cw, n_hi;
+  int nblocks, ksteps;
+  long long w_off;     // packed matrix: offset from the packed image (globals) or the layer start
+  int layer_rel;       // 1 if w_off is relative to the layer's start
+  int* group_cnt;      // [nblocks] arrival counters of the groups
+};
 
 // Must stay the first kernel argument of the pass kernel.
 struct PassParams {
@@ -36,44 +46,47 @@ struct PassParams {
   int n, Mp, prefix_len, cap, G;
   // packed weights
   const char* packed;
-  long long o_embed, o_final_norm, o_lm, layer0, layer_bytes;
-  long long o_attn_norm, o_qkv, o_o, o_ffn_norm, o_gu, o_down;
-  int ks_d, ks_f, qkv_nb, d_nb, gu_nb, v_nb;
+  long long o_embed, o_final_norm, layer0, layer_bytes;
+  long long o_attn_norm, o_ffn_norm;
+  int d_nb;
+  StepPlan step[kSteps];
   // KV cache [L][H][cap][Dh]
   bf16* k_cache;
   bf16* v_cache;
   // workspace
-  int* tree;       // tok | parent | depth | pos | anc
-  float* x;        // [2L+1][Mp][d]
-  float* ssq;      // [2L+1][d/16][Mp]
-  bf16* q;        // [L][Mp][d]   queries after the rotary embedding
-  bf16* o;         // [L][Mp][d]
-  bf16* h;         // [L][Mp][Fp]
-  float* part;     // [G][2][Mp][16]
-  float* attn_o;   // [H][S][Mp][Dh]
-  float* attn_ml;  // [H][S][Mp][2]
+  int* tree;        // tok | parent | depth | pos | anc
+  const char* zero; // kZeroBytes of zeros
+  float* rope;      // [Mp][Dh/2][2] cos, sin of every node's rotary angles
+  float* x;         // [2L+1][Mp][d]
+  float* ssq;       // [2L+1][d/32][Mp]
+  bf16* q;          // [L][Mp][d]   queries after the rotary embedding
+  bf16* o;          // [L][Mp][d]
+  bf16* h;          // [L][Mp][Fp]
+  float* part;      // split-K partial tiles
+  float* attn_o;    // [H][S][Mp][Dh]
+  float* attn_ml;   // [H][S][Mp][2]
   int attn_splits;
-  int* tile_cnt;
   int* head_cnt;
   int* lm_cnt;
   int* exit_cnt;
   int* status;
-  int* bar;        // [kBarSlots][kBarStride]
-  float* lm_val;   // [G + v_nb][Mp]
+  int* bar;         // [kBarSlots][kBarStride]
+  float* lm_val;    // [v_nb][Mp]
   int* lm_idx;
-  int* amax;       // [Mp]
+  int* amax;        // [Mp]
   // outputs
-  float* logits;   // rows [row_lo, n) x V, or null
+  float* logits;    // rows [row_lo, n) x V, or null
   int row_lo;
   int* path;
   int* accept_len;
   int* next_token;
   // control
-  int spin_limit;   // bound of every wait loop (polls)
-  long long* trace; // diagnostics: [8][2 + 5L][6] phase timestamps, or null
+  int spin_limit;    // bound of every wait loop (polls)
+  long long* trace;  // diagnostics: [8][2 + 5L][6] phase timestamps, or null
 };
 
-hipError_t launch_pass(int mb, const PassParams& p, const TreeArgs& tree, hipStream_t st);
-int pass_occupancy(int mb, int dh);  // resident workgroups per CU (0 if unavailable)
+hipError_t launch_pass(int mb32, const PassParams& p, const TreeArgs& tree, hipStream_t st);
+int pass_occupancy(int mb32, int dh);  // resident workgroups per CU (0 if unavailable)
+size_t pass_lds_bytes(int mb32, int dh);
 
 }  // namespace llmcad

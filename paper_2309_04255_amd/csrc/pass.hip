@@ -6,24 +6,28 @@
 // step pays a ramp-up and a drain; here every workgroup (one per CU, all
 // resident: cooperative launch) walks the phases in order and meets the
 // others at a grid barrier between phases.  Weights never depend on the
-// previous phase, so each workgroup issues the first weight loads of its next
-// phase before waiting at the barrier, and HBM keeps streaming meanwhile.
+// previous phase, so each workgroup issues the first weight loads of its
+// next tile before it waits at the barrier, and HBM keeps streaming
+// meanwhile.
 //
-// Phases: embed + tree prep; per layer QKV projection (RMSNorm prologue) ->
-// tree attention (rotary embedding at each node's position, ancestor mask) ->
-// O projection (+residual) -> gate/up (RMSNorm prologue, SwiGLU epilogue) ->
-// down projection (+residual); then final RMSNorm + LM head + argmax, and the
-// accept walk in the workgroup that completes the argmax.
+// Phases: embed + tree prep; per layer QKV projection (RMSNorm applied to
+// the staged activations; rotary embedding and K/V cache write in the
+// epilogue) -> tree attention (ancestor mask) -> O projection (+residual) ->
+// gate/up (RMSNorm; SwiGLU epilogue) -> down projection (+residual); then
+// final RMSNorm + LM head + argmax, and the accept walk in the workgroup that
+// completes the argmax.
 //
-// GEMM phases: the output columns are 16-wide n-blocks (one MFMA each).
-// Workgroup g owns c = N_blocks / G whole n-blocks over the full K, so its
-// epilogue needs nothing from other workgroups; the remaining R = N_blocks mod
-// G n-blocks are shared stream-K style (every workgroup gets an equal run of
-// their k-steps), finished by the last contributor, which adds the partials
-// in k order (bit-reproducible).  Runs over the remainder come first so their
-// hand-off latency overlaps the main block's streaming.  Inside a workgroup
-// the four waves take interleaved k-steps and their partial sums are added in
-// LDS in a fixed order.
+// GEMM phases (activations X [Mp rows x K], packed weights W [N x K]): the
+// host cuts every step into tiles (GemmPlan): a tile is a group of up to 16
+// consecutive 32-column n-blocks times a slice of the k-steps.  A tile's
+// activation slice is copied once into LDS with direct global->LDS loads, in
+// exactly the lane order of the 32x32x16 MFMA A operand, while the weights
+// stream from HBM through a register pipeline (non-temporal loads); the
+// activations are never re-read from L2 per n-block.  The four waves take
+// interleaved k-steps and their partial tiles are added in LDS in wave
+// order.  When a group's k-steps are split over S tiles, each tile stores its
+// partial sum and the workgroup that completes the group last adds the S
+// partials in slice order (bit-reproducible) and runs the epilogue.
 //
 // Coherence without cache maintenance: every buffer handed from one phase to
 // the next is written once per pass at its own address with device-coherent
@@ -45,10 +49,19 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 
-// How a GEMM phase forms its A operand, and what its epilogue does.
-enum Prologue { PRO_BF16 = 0, PRO_NORM = 1 };  // bf16 activations | RMSNorm of fp32 x
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 constexpr int kTraceWgs = 8;  // workgroups that record phase timestamps
+
+// D = A(32x16) * B(16x32) + C on the matrix cores, bf16 inputs, fp32
+// accumulate.  Lane l holds A row l % 32 and B column l % 32, k-slots
+// 8 (l / 32) .. + 7 of both; D element i of lane l is row
+// 8 (i / 4) + 4 (l / 32) + i % 4, column l % 32.
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 
 // The launch parameters, read in place from the kernel-argument segment
 // (constant memory): loads through a wave-uniform address of it are scalar
@@ -62,6 +75,17 @@ __device__ __forceinline__ KParams& uniform_params(KParams& p) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
   return *(KParams*)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ bf16x8 ldg_nt(const bf16x8* p) {
+  return __builtin_nontemporal_load((const LLMCAD_GLOBAL bf16x8*)p);
+}
+
+// Direct global -> LDS copy of 16 bytes per lane: lane l's bytes land at
+// lds + 16 l.  `lds` must be the same in every lane.
+__device__ __forceinline__ void dma16(const void* src, char* lds) {
+  __builtin_amdgcn_global_load_lds((const LLMCAD_GLOBAL void*)src,
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
 // ------------------------------------------------------------------ sync
@@ -88,8 +112,7 @@ __device__ __forceinline__ Sync make_sync(KParams& p, int* lds_flag) {
 
 // Diagnostics: wall-clock (100 MHz) marks per phase: 0 = barrier wait
 // entered, 1 = wait over, 2 = phase work done; GEMM phases also mark 3 =
-// operand prologue done, 4 = weight streaming of the last segment done,
-// 5 = last epilogue done.
+// activations staged, 4 = weight streaming done, 5 = epilogue done.
 __device__ __forceinline__ void trace_mark(const Sync& s, int phase, int k) {
   if (s.trace != nullptr && threadIdx.x == 0) stg(s.trace + phase * 6 + k, (long long)wall_clock64());
 }
@@ -102,12 +125,13 @@ __device__ __forceinline__ void grid_arrive(const Sync& s, int phase) {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  if (threadIdx.x == 0)
-    atomic_add_dev(s.bar + (blockIdx.x % kBarSlots) * kBarStride, 1);
+  if (threadIdx.x == 0) atomic_add_dev(s.bar + (blockIdx.x % kBarSlots) * kBarStride, 1);
 }
 
 // Waits until all G workgroups have arrived `phase` times; one wave polls all
-// counters.  False (to all threads) if the bounded spin ran out.
+// counters.  False (to all threads) if the bounded spin ran out.  The total
+// is exact only because every workgroup waits at every phase before it
+// arrives again: no workgroup can then be more than one arrival ahead.
 __device__ __forceinline__ bool grid_wait(const Sync& s, int phase, int G) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
@@ -156,302 +180,436 @@ __device__ __forceinline__ bool wait_at_least(const Sync& s, const int* c, int t
 
 // ------------------------------------------------------------------ GEMM
 
-struct GemmDesc {
-  const bf16x8* w;   // packed matrix, n-block major
-  int nbt, ks;       // n-blocks, k-steps per n-block
-  const bf16* a;     // PRO_BF16: [Mp][lda]
-  int lda;
-  const float* x;    // PRO_NORM: [Mp][d]
-  const float* ssq;  // PRO_NORM: [d/16][Mp]
-  const bf16* gain;  // PRO_NORM: [d]
-};
-
-struct EpiArgs {
-  bf16* q;            // EPI_QKV: [Mp][d] queries after the rotary embedding
-  bf16* kc;           // EPI_QKV: K cache of this layer [H][cap][Dh]
-  bf16* vc;           // EPI_QKV: V cache of this layer [H][cap][Dh]
-  const float* x_in;  // EPI_RESID: [Mp][d]
-  float* x_out;       // EPI_RESID: [Mp][d]
-  float* ssq_out;     // EPI_RESID: [d/16][Mp]
-  bf16* h;            // EPI_SWIGLU: [Mp][Fp]
-  float* logits;      // EPI_LOGITS: rows [row_lo, n), or null
-  int row_lo;
-};
-
-template <int MB, int PRO>
-struct AStage;
-template <int MB>
-struct AStage<MB, PRO_BF16> {
-  bf16x8 a[MB];
-};
-template <int MB>
-struct AStage<MB, PRO_NORM> {
-  float4 x[MB][2];
-  bf16x8 g;
-};
-
-// Register pipeline depth: ~192 VGPRs of stages, 2..16 k-steps.
-template <int MB, int PRO, int C>
-constexpr int pipe_depth() {
-  constexpr int per = 4 * C + (PRO == PRO_BF16 ? 4 * MB : 8 * MB + 4);
-  constexpr int d = 192 / per;
-  return d < 2 ? 2 : (d > 16 ? 16 : d);
-}
-
-template <int MB, int PRO, int C>
-struct Pipe {
-  static constexpr int D = pipe_depth<MB, PRO, C>();
-  bf16x8 bw[D][C];
-  AStage<MB, PRO> as[D];
-  const bf16x8* wt;  // first n-block's blocks + lane
-  int ks;            // blocks between consecutive n-blocks
-  int s0, ns;        // this wave's first k-step and number of k-steps
-};
-
-template <int MB, int PRO, int C>
-__device__ __forceinline__ void pipe_setup(Pipe<MB, PRO, C>& P, const GemmDesc& g, int nb0, int k0,
-                                           int k1) {
-  const int wave = wave_index(), lane = threadIdx.x & 63;
-  P.wt = g.w + (size_t)nb0 * g.ks * 64 + lane;
-  P.ks = g.ks;
-  P.s0 = wave_uniform(k0 + wave);
-  P.ns = wave_uniform(P.s0 < k1 ? (k1 - P.s0 + kWaves - 1) / kWaves : 0);
-}
-
-template <int MB, int PRO, int C>
-__device__ __forceinline__ void pipe_load_b(Pipe<MB, PRO, C>& P, int slot, int i) {
-  const int s = P.s0 + kWaves * i;
-#pragma unroll
-  for (int c = 0; c < C; ++c) P.bw[slot][c] = ldg(P.wt + ((size_t)c * P.ks + s) * 64);
-}
-
-template <int MB, int PRO, int C>
-__device__ __forceinline__ void pipe_load_a(Pipe<MB, PRO, C>& P, const GemmDesc& g, int d, int slot,
-                                            int i) {
-  const int lane = threadIdx.x & 63, lrow = lane & 15, kg = lane >> 4;
-  const int k = kStepK * (P.s0 + kWaves * i) + 8 * kg;
-  if constexpr (PRO == PRO_BF16) {
-#pragma unroll
-    for (int rb = 0; rb < MB; ++rb)
-      P.as[slot].a[rb] = ldg((const bf16x8*)(g.a + (size_t)(16 * rb + lrow) * g.lda + k));
-  } else {
-#pragma unroll
-    for (int rb = 0; rb < MB; ++rb) {
-      const float* xr = g.x + (size_t)(16 * rb + lrow) * d + k;
-      P.as[slot].x[rb][0] = ldg((const float4*)xr);
-      P.as[slot].x[rb][1] = ldg((const float4*)(xr + 4));
-    }
-    P.as[slot].g = ldg((const bf16x8*)(g.gain + k));
-  }
-}
-
-template <int MB, int PRO, int C>
-__device__ __forceinline__ void pipe_compute(Pipe<MB, PRO, C>& P, int slot, f32x4 (&acc)[MB][C],
-                                             const float (&rstd)[MB]) {
-#pragma unroll
-  for (int rb = 0; rb < MB; ++rb) {
-    bf16x8 a;
-    if constexpr (PRO == PRO_BF16) {
-      a = P.as[slot].a[rb];
-    } else {
-      const float xs[8] = {P.as[slot].x[rb][0].x, P.as[slot].x[rb][0].y, P.as[slot].x[rb][0].z,
-                           P.as[slot].x[rb][0].w, P.as[slot].x[rb][1].x, P.as[slot].x[rb][1].y,
-                           P.as[slot].x[rb][1].z, P.as[slot].x[rb][1].w};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) a[e] = f2bf(xs[e] * rstd[rb] * bf2f(P.as[slot].g[e]));
-    }
-#pragma unroll
-    for (int c = 0; c < C; ++c) acc[rb][c] = mfma16x16x32(a, P.bw[slot][c], acc[rb][c]);
-  }
-}
-
-// Runs the wave's k-steps as a software pipeline of D register stages.
-// Every stage is loaded (weights, then the A operand) D steps ahead of its
-// use, and loads are issued unconditionally (clamped to the last step) so
-// the number in flight is the same on every path.  The scheduling fences keep
-// each stage's compute after the previous stage's reload: the compiler's
-// wait before a compute then only covers that stage's own loads, and the
-// (D - 1) younger stages stay in flight.
-// `hook` runs (in every wave) once the first stages are in flight; the first
-// pipeline of a phase computes the RMSNorm scales there, so their loads
-// overlap the weight stream.
-template <int MB, int PRO, int C, class Hook>
-__device__ __forceinline__ void pipe_run(Pipe<MB, PRO, C>& P, const GemmDesc& g, int d,
-                                         f32x4 (&acc)[MB][C], const float (&rstd)[MB], Hook&& hook) {
-  constexpr int D = Pipe<MB, PRO, C>::D;
-#pragma unroll
-  for (int rb = 0; rb < MB; ++rb)
-#pragma unroll
-    for (int c = 0; c < C; ++c) acc[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int ns = P.ns;  // wave-uniform
-  if (ns > 0) {
-#pragma unroll
-    for (int u = 0; u < D; ++u) {
-      const int st = u < ns ? u : ns - 1;
-      pipe_load_b(P, u, st);
-      pipe_load_a(P, g, d, u, st);
-      __builtin_amdgcn_sched_barrier(0);  // stages issue in order
-    }
-  }
-  hook();
-  __builtin_amdgcn_sched_barrier(0);
-  if (ns == 0) return;
-  for (int i = 0; i < ns; i += D) {
-#pragma unroll
-    for (int u = 0; u < D; ++u) {
-      __builtin_amdgcn_sched_barrier(0);
-      if (i + u < ns) pipe_compute(P, u, acc, rstd);
-      __builtin_amdgcn_sched_barrier(0);
-      const int nx = i + u + D < ns ? i + u + D : ns - 1;
-      pipe_load_b(P, u, nx);
-      pipe_load_a(P, g, d, u, nx);
-    }
-  }
-  __builtin_amdgcn_sched_barrier(0);
-}
-
-// Sum the waves' partial tiles into tileS [16 MB][16 C (+4)] in wave order.
-template <int MB, int C>
-__device__ __forceinline__ void reduce_waves(float* tileS, const f32x4 (&acc)[MB][C]) {
-  constexpr int TS = 16 * C + 4;
-  const int wave = wave_index(), lane = threadIdx.x & 63, lrow = lane & 15, kg = lane >> 4;
-  for (int w = 0; w < kWaves; ++w) {
-    if (wave == w) {
-#pragma unroll
-      for (int rb = 0; rb < MB; ++rb)
-#pragma unroll
-        for (int c = 0; c < C; ++c)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            float* dst = &tileS[(16 * rb + 4 * kg + i) * TS + 16 * c + lrow];
-            *dst = (w == 0) ? acc[rb][c][i] : *dst + acc[rb][c][i];
-          }
-    }
-    __syncthreads();
-  }
-}
-
-// Workgroup whose stream-K run contains flat k-step position q.
-__device__ __forceinline__ int owner_of(long q, long W, int G) {
-  return (int)(((q + 1) * G + W - 1) / W) - 1;
-}
-
 struct GemmLds {
-  float part_ss[256];         // rstd prologue: [256 / ROWS][ROWS]
-  float red_v[kMaxNodes][8];  // argmax per (row, n-block)
-  int red_i[kMaxNodes][8];
+  float rstd[kMaxNodes];          // RMSNorm scale per row of the current tile
+  float part_ss[256];             // their partial sums
+  float red_v[kMaxNodes][kMaxCW]; // LM head: argmax per (row, n-block)
+  int red_i[kMaxNodes][kMaxCW];
   int reach[kMaxNodes];
   int amax[kMaxNodes];
   int tok[kMaxNodes];  // accept walk: the tree, staged from the workspace
   int par[kMaxNodes];
   int dep[kMaxNodes];
   int walk_len;
-  float best_v[kMaxNodes];  // LM head: the workgroup's best column per row
-  int best_i[kMaxNodes];
 };
+
+// What one GEMM step reads and writes in a given layer.
+struct StepIo {
+  const bf16x8* w;   // packed matrix
+  int ks;            // k-steps per n-block (K / 16)
+  bool norm;         // activations: RMSNorm(x) with gain, else bf16 a
+  const bf16* a;     // [Mp][lda]
+  int lda;
+  const float* x;    // [Mp][d]
+  const float* ssq;  // [d/32][Mp]
+  const bf16* gain;  // [d]
+  // epilogue
+  bf16* q;           // QKV: [Mp][d] queries after the rotary embedding
+  bf16* kc;          // QKV: K cache of this layer [H][cap][Dh]
+  bf16* vc;          // QKV: V cache of this layer [H][cap][Dh]
+  const float* x_in; // RESID: [Mp][d]
+  float* x_out;      // RESID: [Mp][d]
+  float* ssq_out;    // RESID: [d/32][Mp]
+  bf16* h;           // SWIGLU: [Mp][Fp]
+};
+
+__device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
+  const size_t xsz = (size_t)p.Mp * p.d, ssz = (size_t)p.d_nb * p.Mp;
+  const char* lw = p.packed + p.layer0 + (long long)l * p.layer_bytes;
+  const StepPlan& sp = p.step[step];
+  StepIo io{};
+  io.w = (const bf16x8*)((sp.layer_rel ? lw : p.packed) + sp.w_off);
+  io.ks = sp.ksteps;
+  switch (step) {
+    case STEP_QKV:
+      io.norm = true;
+      io.x = p.x + (size_t)(2 * l) * xsz;
+      io.ssq = p.ssq + (size_t)(2 * l) * ssz;
+      io.gain = (const bf16*)(lw + p.o_attn_norm);
+      io.q = p.q + (size_t)l * p.Mp * p.d;
+      io.kc = p.k_cache + (size_t)l * p.H * p.cap * p.Dh;
+      io.vc = p.v_cache + (size_t)l * p.H * p.cap * p.Dh;
+      break;
+    case STEP_O:
+      io.norm = false;
+      io.a = p.o + (size_t)l * p.Mp * p.d;
+      io.lda = p.d;
+      io.x_in = p.x + (size_t)(2 * l) * xsz;
+      io.x_out = p.x + (size_t)(2 * l + 1) * xsz;
+      io.ssq_out = p.ssq + (size_t)(2 * l + 1) * ssz;
+      break;
+    case STEP_GATE_UP:
+      io.norm = true;
+      io.x = p.x + (size_t)(2 * l + 1) * xsz;
+      io.ssq = p.ssq + (size_t)(2 * l + 1) * ssz;
+      io.gain = (const bf16*)(lw + p.o_ffn_norm);
+      io.h = p.h + (size_t)l * p.Mp * p.Fp;
+      break;
+    case STEP_DOWN:
+      io.norm = false;
+      io.a = p.h + (size_t)l * p.Mp * p.Fp;
+      io.lda = p.Fp;
+      io.x_in = p.x + (size_t)(2 * l + 1) * xsz;
+      io.x_out = p.x + (size_t)(2 * l + 2) * xsz;
+      io.ssq_out = p.ssq + (size_t)(2 * l + 2) * ssz;
+      break;
+    default:  // STEP_LM
+      io.norm = true;
+      io.x = p.x + (size_t)(2 * p.L) * xsz;
+      io.ssq = p.ssq + (size_t)(2 * p.L) * ssz;
+      io.gain = (const bf16*)(p.packed + p.o_final_norm);
+      break;
+  }
+  return io;
+}
+
+// Copies the tile's activation slice (k-steps [k0, k0 + kt), all Mp rows)
+// into LDS in MFMA A-operand lane order.  bf16: unit (kk, mb) = 1 KiB at
+// (kk MB + mb) KiB, lane l's 16 bytes = row 32 mb + l % 32, inputs
+// 16 (k0 + kk) + 8 (l / 32) .. + 7.  Norm (fp32 x): unit ((kk MB + mb) 2 + h)
+// holds inputs + 4 h .. + 3 of the same lane; then the gains, 32 bytes per
+// k-step (16 per lane half).  Rows >= n read zeros.  Waves take units in
+// turn; the caller waits for the loads.
+template <int MB>
+__device__ __forceinline__ void stage_activations(KParams& p, const StepIo& io, int k0, int kt, char* A) {
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  const int lrow = lane & 31, khalf = lane >> 5;
+  const char* zero = p.zero + lane * 16;
+  if (!io.norm) {
+    const int units = kt * MB;
+    for (int u = wave; u < units; u += kWaves) {
+      const int kk = u / MB, mb = u % MB;
+      const int r = 32 * mb + lrow;
+      const void* src = r < p.n ? (const void*)(io.a + (size_t)r * io.lda + 16 * (k0 + kk) + 8 * khalf)
+                                : (const void*)zero;
+      dma16(src, A + (size_t)u * 1024);
+    }
+  } else {
+    const int units = kt * MB * 2;
+    for (int u = wave; u < units; u += kWaves) {
+      const int kk = u / (2 * MB), mb = (u / 2) % MB, hh = u & 1;
+      const int r = 32 * mb + lrow;
+      const void* src = r < p.n
+                            ? (const void*)(io.x + (size_t)r * p.d + 16 * (k0 + kk) + 8 * khalf + 4 * hh)
+                            : (const void*)zero;
+      dma16(src, A + (size_t)u * 1024);
+    }
+    char* G = A + (size_t)kt * MB * 2048;
+    for (int j = wave; j * 32 < kt; j += kWaves) {
+      const int kk = 32 * j + (lane >> 1);
+      const void* src = kk < kt ? (const void*)(io.gain + 16 * (k0 + kk) + 8 * (lane & 1)) : (const void*)zero;
+      dma16(src, G + (size_t)j * 1024);
+    }
+  }
+}
+
+// RMSNorm scales of rows [0, Mp): 1 / sqrt(mean of squares + eps) from the
+// per-n-block sums of squares the producing phase wrote (added in n-block
+// order); 0 for rows >= n.  Loads are issued here, the sums are formed by
+// finish_row_scales after the caller's wait.
+template <int MB>
+struct SsqLoads {
+  static constexpr int ROWS = 32 * MB, CHK = 256 / ROWS, PER = 16;
+  float v[PER];
+};
+template <int MB>
+__device__ __forceinline__ void row_scale_loads(KParams& p, const StepIo& io, SsqLoads<MB>& L, int pass) {
+  constexpr int ROWS = 32 * MB, CHK = 256 / ROWS, PER = SsqLoads<MB>::PER;
+  const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
+  const int dn = p.d_nb;
+  const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int t = t0 + pass * PER + i;
+    L.v[i] = (r < p.n && t < t1) ? ldg(io.ssq + (size_t)t * p.Mp + r) : 0.0f;
+  }
+}
+template <int MB>
+__device__ __forceinline__ void row_scales(KParams& p, const StepIo& io, GemmLds& gl) {
+  constexpr int ROWS = 32 * MB, CHK = 256 / ROWS, PER = SsqLoads<MB>::PER;
+  const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
+  const int dn = p.d_nb;
+  const int len = (ch + 1) * dn / CHK - ch * dn / CHK;
+  float ss = 0.0f;
+  for (int pass = 0; pass * PER < len; ++pass) {
+    SsqLoads<MB> L;
+    row_scale_loads<MB>(p, io, L, pass);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) ss += L.v[i];
+  }
+  gl.part_ss[ch * ROWS + r] = ss;
+  __syncthreads();
+  if (threadIdx.x < ROWS) {
+    float t = 0.0f;
+    for (int c = 0; c < CHK; ++c) t += gl.part_ss[c * ROWS + threadIdx.x];
+    gl.rstd[threadIdx.x] = threadIdx.x < p.n ? 1.0f / sqrtf(t * p.inv_d + p.eps) : 0.0f;
+  }
+  __syncthreads();
+}
+
+// Weight stages per wave: about 160 VGPRs, 2 to 16 k-steps; one stage for
+// the widest tiles, whose accumulators fill the AGPRs.
+template <int CW>
+constexpr int tile_depth() {
+  constexpr int d = 40 / CW;
+  return CW >= 12 ? 1 : (d < 2 ? 2 : (d > 16 ? 16 : d));
+}
+
+// One tile: n-blocks [nb0, nb0 + CW) x k-steps [k0, k1) of a step.  Issues
+// the first weight stages, then (wait_phase >= 0) waits at the grid barrier
+// for the step's inputs, stages the activations into LDS, streams the
+// weights and leaves the tile's sum in LDS at T = A:
+// fp32 [CW][MB][64 lanes][16] (MFMA accumulator order).  False if a wait
+// ran out.
+template <int MB, int CW, bool NORM>
+__device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams& pin, int step, int layer,
+                                                                       int nb0, int k0, int k1,
+                                                                       int wait_phase, char* A,
+                                                                       GemmLds& gl, int* lds_flag) {
+  KParams& p = uniform_params(pin);
+  step = wave_uniform(step);
+  layer = wave_uniform(layer);
+  nb0 = wave_uniform(nb0);
+  k0 = wave_uniform(k0);
+  k1 = wave_uniform(k1);
+  wait_phase = wave_uniform(wait_phase);
+  const StepIo io = step_io(p, step, layer);
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  const int kt = k1 - k0;
+  const int ns = wave_uniform(wave < kt ? (kt - wave + kWaves - 1) / kWaves : 0);
+  constexpr int D = tile_depth<CW>();
+  // this wave's k-steps: k0 + wave + 4 i
+  const bf16x8* wt = io.w + ((size_t)nb0 * io.ks + k0 + wave) * 64 + lane;
+  const size_t cstride = (size_t)io.ks * 64;
+  bf16x8 bw[D][CW];
+  auto load_stage = [&](int slot, int i) {
+#pragma unroll
+    for (int c = 0; c < CW; ++c) bw[slot][c] = ldg_nt(wt + c * cstride + (size_t)(kWaves * i) * 64);
+  };
+  if (ns > 0) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      load_stage(u, u < ns ? u : ns - 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  if (wait_phase >= 0) {
+    const Sync sy = make_sync(p, lds_flag);
+    trace_mark(sy, wait_phase, 0);
+    if (!grid_wait(sy, wait_phase, p.G)) return false;
+    trace_mark(sy, wait_phase, 1);
+  }
+  stage_activations<MB>(p, io, k0, kt, A);
+  if constexpr (NORM) row_scales<MB>(p, io, gl);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (wait_phase >= 0 && p.trace != nullptr && (int)blockIdx.x < kTraceWgs && threadIdx.x == 0)
+    stg(p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 6 + wait_phase * 6 + 3, (long long)wall_clock64());
+
+  float rs[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) rs[mb] = NORM ? gl.rstd[32 * mb + (lane & 31)] : 1.0f;
+  const char* G = A + (size_t)kt * MB * 2048;
+  f32x16 acc[MB][CW];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int c = 0; c < CW; ++c) acc[mb][c] = f32x16{};
+  for (int i = 0; i < ns; i += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + u < ns) {
+        const int kk = wave + kWaves * (i + u);
+        bf16x8 a[MB];
+        if constexpr (NORM) {
+          const bf16x8 g = *(const bf16x8*)(G + kk * 32 + (lane >> 5) * 16);
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const char* base = A + (size_t)(kk * MB + mb) * 2048 + lane * 16;
+            const float4 x0 = *(const float4*)base;
+            const float4 x1 = *(const float4*)(base + 1024);
+            const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) a[mb][e] = f2bf(xs[e] * rs[mb] * bf2f(g[e]));
+          }
+        } else {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) a[mb] = *(const bf16x8*)(A + (size_t)(kk * MB + mb) * 1024 + lane * 16);
+        }
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int c = 0; c < CW; ++c) acc[mb][c] = mfma32(a[mb], bw[u][c], acc[mb][c]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      const int nx = i + u + D < ns ? i + u + D : ns - 1;
+      load_stage(u, nx);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  __syncthreads();  // every wave is done reading the activations
+  // Wave partials -> T (the activation region), added in wave order.
+  float* T = reinterpret_cast<float*>(A);
+  for (int w = 0; w < kWaves; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int c = 0; c < CW; ++c)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          float4* dst = reinterpret_cast<float4*>(T + ((size_t)(c * MB + mb) * 64 + lane) * 16);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            float4 v = make_float4(acc[mb][c][4 * j], acc[mb][c][4 * j + 1], acc[mb][c][4 * j + 2],
+                                   acc[mb][c][4 * j + 3]);
+            if (w > 0) {
+              const float4 o = dst[j];
+              v.x += o.x;
+              v.y += o.y;
+              v.z += o.z;
+              v.w += o.w;
+            }
+            dst[j] = v;
+          }
+        }
+    }
+    __syncthreads();
+  }
+  return true;
+}
+
+template <int MB, bool NORM, int CW>
+__device__ __forceinline__ bool tile_dispatch(int cw, KParams& p, int step, int layer, int nb0, int k0,
+                                              int k1, int wait_phase, char* A, GemmLds& gl, int* flag) {
+  if constexpr (CW >= 1) {
+    if (cw == CW) return tile_compute<MB, CW, NORM>(p, step, layer, nb0, k0, k1, wait_phase, A, gl, flag);
+    return tile_dispatch<MB, NORM, CW - 1>(cw, p, step, layer, nb0, k0, k1, wait_phase, A, gl, flag);
+  } else {
+    return false;
+  }
+}
 
 // Rotary embedding frequency of dim pair (j, j + Dh/2): theta^(-2j/Dh).
 __device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) {
   return exp2f(-(2.0f * (float)j / (float)Dh) * log2_theta);
 }
 
-// Epilogue of C n-blocks [nb0, nb0 + C) held in tileS: writes the phase's
-// outputs with device-coherent stores.  lm_entry: argmax partial slot.
-template <int MB, int EPI, int C>
-__device__ __forceinline__ void epilogue(KParams& p, const EpiArgs& e, float* tileS, int nb0,
-                                         int lm_entry, GemmLds& gl) {
-  constexpr int ROWS = 16 * MB, COLS = 16 * C, TS = COLS + 4;
-  const int lane = threadIdx.x & 63;
-  if constexpr (EPI == EPI_QKV) {
-    // One thread per (row, column pair cc, cc + 8) of an n-block.  q and k
-    // n-blocks hold rotary pairs 8 columns apart (PACK_QKV_ROPE): rotate at
-    // the node's position, then store q, and k into the node's cache slot.
-    // v n-blocks are plain.  Stores go out in adjacent pairs of dims (this
-    // lane and the next).
-    const int d = p.d, dh = p.Dh, half = dh / 2;
-    for (int idx = threadIdx.x; idx < ROWS * (COLS / 2); idx += kThreads) {
-      const int r = idx / (COLS / 2), ps = idx % (COLS / 2);
-      const int cc = kNB * (ps / 8) + (ps % 8);
-      const int col = kNB * nb0 + cc;
-      const float a = tileS[r * TS + cc], b = tileS[r * TS + cc + 8];
-      const bool store = r < p.n && (ps & 1) == 0;
+// Epilogue of a complete group held in T (fp32 [cw][MB][64][16]): each
+// wave takes (n-block, row block) units in turn, one accumulator tile per
+// unit, and writes the step's outputs with device-coherent stores.
+template <int MB, int EPI>
+__device__ __forceinline__ void epilogue(KParams& p, const StepIo& io, const float* T, int nb0, int cw, int group,
+                                         GemmLds& gl) {
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  const int j = lane & 31;
+  for (int unit = wave; unit < cw * MB; unit += kWaves) {
+    const int c = unit / MB, mb = unit % MB;
+    const int nb = nb0 + c;
+    float v[16];
+    {
+      const float4* src = reinterpret_cast<const float4*>(T + ((size_t)unit * 64 + lane) * 16);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 f = src[q];
+        v[4 * q] = f.x;
+        v[4 * q + 1] = f.y;
+        v[4 * q + 2] = f.z;
+        v[4 * q + 3] = f.w;
+      }
+    }
+    if constexpr (EPI == EPI_QKV) {
+      const int d = p.d, dh = p.Dh;
+      const int col = kNB * nb + j;
       if (col < 2 * d) {
-        const int part = col / d, cq = col % d, hh = cq / dh, w = cq % dh;
-        const int j = 8 * (w / kNB) + (w % kNB);  // < Dh/2
-        const int pos = r < p.n ? ldg(p.tree + 384 + r) : 0;
-        float sn, cs;
-        sincosf((float)pos * rope_inv_freq(j, dh, p.log2_theta), &sn, &cs);
-        const float lo = a * cs - b * sn, hi = b * cs + a * sn;
-        const float lo1 = __shfl_down(lo, 1, kWave), hi1 = __shfl_down(hi, 1, kWave);
-        if (store) {
-          bf16* dst = part == 0 ? e.q + (size_t)r * d + hh * dh
-                                : e.kc + ((size_t)hh * p.cap + p.prefix_len + r) * dh;
-          st_coherent_bf2(dst + j, lo, lo1);
-          st_coherent_bf2(dst + j + half, hi, hi1);
+        // q or k: this n-block holds dims [16t, 16t+16) (lanes j < 16) and
+        // their rotary partners + Dh/2 (lanes j >= 16) of one head.
+        const int part = col / d, cq = (kNB * nb) % d, hh = cq / dh, t = (cq % dh) / kNB;
+        const int jj = 16 * t + (j & 15);  // pair index < Dh/2
+        const int dim = jj + (j < 16 ? 0 : dh / 2);
+        bf16* base = part == 0 ? io.q + hh * dh : io.kc + (size_t)hh * p.cap * dh;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = 32 * mb + acc_row(i, lane);
+          const float partner = __shfl_xor(v[i], 16, kWave);
+          const float2 cssn = r < p.n ? ldg((const float2*)p.rope + (size_t)r * (dh / 2) + jj) : make_float2(1.0f, 0.0f);
+          const float cs = cssn.x, sn = cssn.y;
+          const float outv = j < 16 ? v[i] * cs - partner * sn : v[i] * cs + partner * sn;
+          const float nxt = __shfl_down(outv, 1, kWave);
+          if (r < p.n && (j & 1) == 0) {
+            bf16* dst = part == 0 ? base + (size_t)r * d : base + (size_t)(p.prefix_len + r) * dh;
+            st_coherent_bf2(dst + dim, outv, nxt);
+          }
         }
       } else {
-        const int j = col - 2 * d, hh = j / dh, dd = j % dh;
-        const float a1 = __shfl_down(a, 1, kWave), b1 = __shfl_down(b, 1, kWave);
-        if (store) {
-          bf16* dst = e.vc + ((size_t)hh * p.cap + p.prefix_len + r) * dh + dd;
-          st_coherent_bf2(dst, a, a1);
-          st_coherent_bf2(dst + 8, b, b1);
-        }
-      }
-    }
-  } else if constexpr (EPI == EPI_RESID) {
-    for (int idx = threadIdx.x; idx < ROWS * COLS; idx += kThreads) {
-      const int r = idx / COLS, cc = idx % COLS;
-      const int col = kNB * nb0 + cc;
-      float xn = 0.0f;
-      if (r < p.n) {
-        xn = ldg(e.x_in + (size_t)r * p.d + col) + tileS[r * TS + cc];
-        st_coherent(&e.x_out[(size_t)r * p.d + col], xn);
-      }
-      // sum of squares over the 16 columns of this n-block (16 consecutive lanes)
-      float s = xn * xn;
-      s += __shfl_xor(s, 8, kWave);
-      s += __shfl_xor(s, 4, kWave);
-      s += __shfl_xor(s, 2, kWave);
-      s += __shfl_xor(s, 1, kWave);
-      if ((lane & 15) == 0) st_coherent(&e.ssq_out[(size_t)(nb0 + cc / kNB) * p.Mp + r], s);
-    }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    for (int idx = threadIdx.x; idx < ROWS * C * 8; idx += kThreads) {
-      const int r = idx / (C * 8), rem = idx % (C * 8), i = rem / 8, j = rem % 8;
-      const float gt = tileS[r * TS + kNB * i + j], up = tileS[r * TS + kNB * i + 8 + j];
-      const float hv = gt / (1.0f + expf(-gt)) * up;
-      const float nxt = __shfl_down(hv, 1, kWave);
-      if (r < p.n && (j & 1) == 0) st_coherent_bf2(e.h + (size_t)r * p.Fp + 8 * (nb0 + i) + j, hv, nxt);
-    }
-  } else {  // EPI_LOGITS
-    for (int idx = threadIdx.x; idx < ROWS * COLS; idx += kThreads) {
-      const int r = idx / COLS, cc = idx % COLS;
-      const int col = kNB * nb0 + cc;
-      const bool valid = r < p.n && col < p.V;
-      const float v = tileS[r * TS + cc];
-      if (valid && e.logits != nullptr && r >= e.row_lo) stg(e.logits + (size_t)(r - e.row_lo) * p.V + col, v);
-      float mv = valid ? v : -INFINITY;
-      int mi = valid ? col : 0x7fffffff;
+        const int cv = col - 2 * d, hh = cv / dh, dim = cv % dh;
 #pragma unroll
-      for (int off = 8; off >= 1; off >>= 1) {  // argmax over the n-block's 16 columns
-        const float ov = __shfl_xor(mv, off, kWave);
-        const int oi = __shfl_xor(mi, off, kWave);
-        if (ov > mv || (ov == mv && oi < mi)) {
-          mv = ov;
-          mi = oi;
+        for (int i = 0; i < 16; ++i) {
+          const int r = 32 * mb + acc_row(i, lane);
+          const float nxt = __shfl_down(v[i], 1, kWave);
+          if (r < p.n && (j & 1) == 0)
+            st_coherent_bf2(io.vc + ((size_t)hh * p.cap + p.prefix_len + r) * dh + dim, v[i], nxt);
         }
       }
-      if ((lane & 15) == 0) {
-        gl.red_v[r][cc / kNB] = mv;
-        gl.red_i[r][cc / kNB] = mi;
+    } else if constexpr (EPI == EPI_RESID) {
+      const int col = kNB * nb + j;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = 32 * mb + acc_row(i, lane);
+        float xn = 0.0f;
+        if (r < p.n) {
+          xn = ldg(io.x_in + (size_t)r * p.d + col) + v[i];
+          st_coherent(io.x_out + (size_t)r * p.d + col, xn);
+        }
+        float s = xn * xn;  // sum of squares over the n-block's 32 columns
+        s += __shfl_xor(s, 16, kWave);
+        s += __shfl_xor(s, 8, kWave);
+        s += __shfl_xor(s, 4, kWave);
+        s += __shfl_xor(s, 2, kWave);
+        s += __shfl_xor(s, 1, kWave);
+        if (j == 0 && r < p.n) st_coherent(io.ssq_out + (size_t)nb * p.Mp + r, s);
+      }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      const int f = 16 * nb + (j & 15);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = 32 * mb + acc_row(i, lane);
+        const float up = __shfl_xor(v[i], 16, kWave);
+        const float hv = v[i] / (1.0f + expf(-v[i])) * up;
+        const float nxt = __shfl_down(hv, 1, kWave);
+        if (r < p.n && j < 16 && (j & 1) == 0) st_coherent_bf2(io.h + (size_t)r * p.Fp + f, hv, nxt);
+      }
+    } else {  // EPI_LOGITS
+      const int col = kNB * nb + j;
+      const bool vcol = col < p.V;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = 32 * mb + acc_row(i, lane);
+        const bool valid = vcol && r < p.n;
+        if (valid && p.logits != nullptr && r >= p.row_lo) stg(p.logits + (size_t)(r - p.row_lo) * p.V + col, v[i]);
+        float mv = valid ? v[i] : -INFINITY;
+        int mi = valid ? col : 0x7fffffff;
+#pragma unroll
+        for (int off = 16; off >= 1; off >>= 1) {  // argmax over the n-block's 32 columns
+          const float ov = __shfl_xor(mv, off, kWave);
+          const int oi = __shfl_xor(mi, off, kWave);
+          if (ov > mv || (ov == mv && oi < mi)) {
+            mv = ov;
+            mi = oi;
+          }
+        }
+        if (j == 0) {
+          gl.red_v[r][c] = mv;
+          gl.red_i[r][c] = mi;
+        }
       }
     }
+  }
+  if constexpr (EPI == EPI_LOGITS) {
     __syncthreads();
-    for (int r = threadIdx.x; r < ROWS; r += kThreads) {
+    for (int r = threadIdx.x; r < 32 * MB; r += kThreads) {
       float mv = -INFINITY;
       int mi = 0x7fffffff;
-      for (int c = 0; c < C; ++c) {
+      for (int c = 0; c < cw; ++c) {
         const float v = gl.red_v[r][c];
         const int i = gl.red_i[r][c];
         if (v > mv || (v == mv && i < mi)) {
@@ -459,13 +617,8 @@ __device__ __forceinline__ void epilogue(KParams& p, const EpiArgs& e, float* ti
           mi = i;
         }
       }
-      if (lm_entry >= 0) {  // a remainder n-block: its own argmax entry
-        st_coherent(&p.lm_val[(size_t)lm_entry * p.Mp + r], mv);
-        st_coherent(&p.lm_idx[(size_t)lm_entry * p.Mp + r], mi);
-      } else if (lm_entry == -2 || mv > gl.best_v[r] || (mv == gl.best_v[r] && mi < gl.best_i[r])) {
-        gl.best_v[r] = mv;  // main block: best over its sub-blocks (-2: first sub-block)
-        gl.best_i[r] = mi;
-      }
+      st_coherent(&p.lm_val[(size_t)group * p.Mp + r], mv);
+      st_coherent(&p.lm_idx[(size_t)group * p.Mp + r], mi);
     }
   }
 }
@@ -538,321 +691,97 @@ __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl
   __syncthreads();
 }
 
-// Warms L2 with the first 16 KiB of weights each wave will read: blocks of
-// n-blocks [nb0, nb0 + nbs) at the wave's k-steps k0 + wave, + 4, ... (< k1),
-// in the order the pipeline consumes them, so that HBM keeps streaming while
-// the workgroup waits at a barrier.  The loaded values are folded into a
-// token after the wait (prefetch_fold) so the loads stay live.
-struct Prefetch {
-  bf16x8 v[16];
-};
-__device__ __forceinline__ void l2_prefetch(Prefetch& pf, const bf16x8* w, int ks, int nb0, int nbs,
-                                            int k0, int k1) {
-  const int wave = wave_index(), lane = threadIdx.x & 63;
-  const int s0 = k0 + wave;
-  const int ns = s0 < k1 ? (k1 - s0 + kWaves - 1) / kWaves : 0;
-  const int total = ns * nbs;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int it = i < total ? i : (total > 0 ? total - 1 : 0);
-    const int c = it % nbs, s = s0 + kWaves * (it / nbs);
-    const size_t blk = total > 0 ? ((size_t)(nb0 + c) * ks + s) : 0;
-    pf.v[i] = ldg(w + blk * 64 + lane);
-  }
-}
-__device__ __forceinline__ uint32_t prefetch_fold(const Prefetch& pf) {
-  uint32_t tok = 0;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) tok ^= __builtin_bit_cast(uint32_t, (__bf16 __attribute__((ext_vector_type(2)))){pf.v[i][0], pf.v[i][1]});
-  return tok;
-}
-
-
-// The GEMM steps of the pass and their operands.
-enum Step { STEP_QKV = 0, STEP_O = 1, STEP_GATE_UP = 2, STEP_DOWN = 3, STEP_LM = 4 };
-
-__device__ __forceinline__ void step_operands(KParams& p, int step, int l, GemmDesc& g, EpiArgs& e) {
-  const size_t xsz = (size_t)p.Mp * p.d, ssz = (size_t)p.d_nb * p.Mp;
-  const char* lw = p.packed + p.layer0 + (long long)l * p.layer_bytes;
-  g = GemmDesc{};
-  e = EpiArgs{};
-  switch (step) {
-    case STEP_QKV:  // RMSNorm(x_2l) -> q, k (raw) and v (to the cache)
-      g.w = (const bf16x8*)(lw + p.o_qkv);
-      g.nbt = p.qkv_nb;
-      g.ks = p.ks_d;
-      g.x = p.x + (size_t)(2 * l) * xsz;
-      g.ssq = p.ssq + (size_t)(2 * l) * ssz;
-      g.gain = (const bf16*)(lw + p.o_attn_norm);
-      e.q = p.q + (size_t)l * p.Mp * p.d;
-      e.kc = p.k_cache + (size_t)l * p.H * p.cap * p.Dh;
-      e.vc = p.v_cache + (size_t)l * p.H * p.cap * p.Dh;
-      break;
-    case STEP_O:  // x_2l+1 = x_2l + o W_o^T
-      g.w = (const bf16x8*)(lw + p.o_o);
-      g.nbt = p.d_nb;
-      g.ks = p.ks_d;
-      g.a = p.o + (size_t)l * p.Mp * p.d;
-      g.lda = p.d;
-      e.x_in = p.x + (size_t)(2 * l) * xsz;
-      e.x_out = p.x + (size_t)(2 * l + 1) * xsz;
-      e.ssq_out = p.ssq + (size_t)(2 * l + 1) * ssz;
-      break;
-    case STEP_GATE_UP:  // h = SwiGLU(RMSNorm(x_2l+1))
-      g.w = (const bf16x8*)(lw + p.o_gu);
-      g.nbt = p.gu_nb;
-      g.ks = p.ks_d;
-      g.x = p.x + (size_t)(2 * l + 1) * xsz;
-      g.ssq = p.ssq + (size_t)(2 * l + 1) * ssz;
-      g.gain = (const bf16*)(lw + p.o_ffn_norm);
-      e.h = p.h + (size_t)l * p.Mp * p.Fp;
-      break;
-    case STEP_DOWN:  // x_2l+2 = x_2l+1 + h W_down^T
-      g.w = (const bf16x8*)(lw + p.o_down);
-      g.nbt = p.d_nb;
-      g.ks = p.ks_f;
-      g.a = p.h + (size_t)l * p.Mp * p.Fp;
-      g.lda = p.Fp;
-      e.x_in = p.x + (size_t)(2 * l + 1) * xsz;
-      e.x_out = p.x + (size_t)(2 * l + 2) * xsz;
-      e.ssq_out = p.ssq + (size_t)(2 * l + 2) * ssz;
-      break;
-    default:  // STEP_LM: logits = RMSNorm(x_2L) W_lm^T
-      g.w = (const bf16x8*)(p.packed + p.o_lm);
-      g.nbt = p.v_nb;
-      g.ks = p.ks_d;
-      g.x = p.x + (size_t)(2 * p.L) * xsz;
-      g.ssq = p.ssq + (size_t)(2 * p.L) * ssz;
-      g.gain = (const bf16*)(p.packed + p.o_final_norm);
-      e.logits = p.logits;
-      e.row_lo = p.row_lo;
-      break;
-  }
-}
-
-// RMSNorm scales of the rows (this lane's row 16 rb + lane % 16 for each row
-// block rb): 1 / sqrt(mean of squares + eps), from the per-n-block sums of
-// squares the producing phase wrote.
-template <int MB>
-__device__ __forceinline__ void row_scales(KParams& p, const GemmDesc& g, GemmLds& gl, float (&rstd)[MB]) {
-  constexpr int ROWS = 16 * MB, CHK = 256 / ROWS;
-  const int lrow = threadIdx.x & 15;
-  const int dn = p.d_nb;
-  if (threadIdx.x < CHK * ROWS) {
-    const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
-    const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
-    float ss = 0.0f;
-    int t = t0;
-    for (; t + 4 <= t1; t += 4) {
-      const float v0 = ldg(g.ssq + (size_t)t * p.Mp + r), v1 = ldg(g.ssq + (size_t)(t + 1) * p.Mp + r);
-      const float v2 = ldg(g.ssq + (size_t)(t + 2) * p.Mp + r), v3 = ldg(g.ssq + (size_t)(t + 3) * p.Mp + r);
-      ss += v0;
-      ss += v1;
-      ss += v2;
-      ss += v3;
-    }
-    for (; t < t1; ++t) ss += ldg(g.ssq + (size_t)t * p.Mp + r);
-    gl.part_ss[ch * ROWS + r] = ss;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int rb = 0; rb < MB; ++rb) {
-    const int row = 16 * rb + lrow;
-    float ss = 0.0f;
-#pragma unroll
-    for (int ch = 0; ch < CHK; ++ch) ss += gl.part_ss[ch * ROWS + row];
-    rstd[rb] = 1.0f / sqrtf(ss * p.inv_d + p.eps);
-  }
-  __syncthreads();
-}
-
-template <int MB>
-struct RowScale {
-  float v[MB];
-};
-
-// Widest main-block sub-block (n-blocks streamed together, sharing one pass
-// over the A operand) that the registers allow at MB row blocks.
-template <int MB>
-constexpr int max_width() {
-  return MB <= 2 ? 8 : (MB <= 4 ? 4 : 2);
-}
-
-// CM whole n-blocks [nb0, nb0 + CM) over the full K.  A function of its own
-// per width, so each width gets its own register allocation.  When need_rs
-// is set the RMSNorm scales are computed here, once the first weight stages
-// are in flight; the scales used are returned.
-template <int MB, int PRO, int EPI, int CM>
-__device__ __attribute__((noinline, not_tail_called)) RowScale<MB> main_block(
-    KParams& pin, int step, int layer, int nb0, RowScale<MB> rs, int need_rs, float* tileS, GemmLds& gl,
-    int lm_entry) {
+// One GEMM phase: this workgroup's tiles, each followed by its share of the
+// group hand-off and, in the group's last workgroup, the epilogue.
+template <int MB, int EPI>
+__device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& pin, int step, int layer,
+                                                                     int phase, char* A, GemmLds& gl,
+                                                                     int* lds_flag) {
   KParams& p = uniform_params(pin);
-  GemmDesc g;
-  EpiArgs e;
-  step_operands(p, wave_uniform(step), wave_uniform(layer), g, e);
-  nb0 = wave_uniform(nb0);
-  lm_entry = wave_uniform(lm_entry);
-  bool need = wave_uniform(need_rs) != 0;
-  float rstd[MB];
-#pragma unroll
-  for (int rb = 0; rb < MB; ++rb) rstd[rb] = rs.v[rb];
-  auto hook = [&]() {
-    if constexpr (PRO == PRO_NORM) {
-      if (need) row_scales<MB>(p, g, gl, rstd);
-    }
-  };
-  Pipe<MB, PRO, CM> P;
-  pipe_setup(P, g, nb0, 0, g.ks);
-  f32x4 acc[MB][CM];
-  pipe_run(P, g, p.d, acc, rstd, hook);
-  reduce_waves<MB, CM>(tileS, acc);
-  epilogue<MB, EPI, CM>(p, e, tileS, nb0, lm_entry, gl);
-  __syncthreads();
-  RowScale<MB> out;
-#pragma unroll
-  for (int rb = 0; rb < MB; ++rb) out.v[rb] = rstd[rb];
-  return out;
-}
-
-template <int MB, int PRO, int EPI, int W>
-__device__ __forceinline__ RowScale<MB> main_dispatch(int w, KParams& p, int step, int layer, int nb0,
-                                                      RowScale<MB> rs, int need_rs, float* tileS,
-                                                      GemmLds& gl, int lm) {
-  if constexpr (W >= 1) {
-    if (w == W) return main_block<MB, PRO, EPI, W>(p, step, layer, nb0, rs, need_rs, tileS, gl, lm);
-    return main_dispatch<MB, PRO, EPI, W - 1>(w, p, step, layer, nb0, rs, need_rs, tileS, gl, lm);
-  } else {
-    return rs;
-  }
-}
-
-// One GEMM phase: warm L2 with the first weights, wait at the barrier, then
-// the remainder runs (stream-K, one n-block per segment) and the main block
-// (whole n-blocks over the full K, in sub-blocks of 4, 3, 2 or 1 n-blocks).
-template <int MB, int PRO, int EPI>
-__device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& pin, int step, int layer, int phase,
-                                                     float* tileS, GemmLds& gl, int* lds_flag) {
-  KParams& p = uniform_params(pin);
-  const Sync sy = make_sync(p, lds_flag);
-  GemmDesc g;
-  EpiArgs e;
-  step_operands(p, wave_uniform(step), wave_uniform(layer), g, e);
+  step = wave_uniform(step);
+  layer = wave_uniform(layer);
   phase = wave_uniform(phase);
-  constexpr int ROWS = 16 * MB;
-  const int G = p.G, gi = blockIdx.x;
-  const int c = g.nbt / G, R = g.nbt - c * G;
-  const long Wr = (long)R * g.ks;
-  const long rbeg = (long)gi * Wr / G, rend = (long)(gi + 1) * Wr / G;
-
-  {
-    Prefetch pf;
-    if (rbeg < rend) {
-      const int t = (int)(rbeg / g.ks), k0 = (int)(rbeg % g.ks);
-      const int k1 = (int)(k0 + (rend - rbeg) < g.ks ? k0 + (rend - rbeg) : g.ks);
-      l2_prefetch(pf, g.w, g.ks, c * G + t, 1, k0, k1);
-    } else if (c > 0) {
-      l2_prefetch(pf, g.w, g.ks, gi * c, c < max_width<MB>() ? c : max_width<MB>(), 0, g.ks);
-    } else {
-      l2_prefetch(pf, g.w, g.ks, 0, 1, 0, 0);
-    }
+  const Sync sy = make_sync(p, lds_flag);
+  const StepPlan& sp = p.step[step];
+  const int S = sp.S, tiles = sp.groups * sp.S;
+  const StepIo io = step_io(p, step, layer);
+  constexpr bool NORM = EPI != EPI_RESID;
+  constexpr int CWM = kMaxCW / MB;
+  // The barrier counts arrivals: it is exact only if every workgroup waits
+  // at every phase before it arrives again, tile or no tile.
+  if ((int)blockIdx.x >= tiles) {
     trace_mark(sy, phase, 0);
-    if (!grid_wait(sy, phase, G)) return false;
+    const bool ok = grid_wait(sy, phase, p.G);
     trace_mark(sy, phase, 1);
-    const uint32_t tok = prefetch_fold(pf);
-    if (tok == 0x9e3779b9u && p.G < 0) stg(p.status + 1, (int)tok);  // keeps the prefetch loads
+    return ok;
   }
-
-  float rstd[MB];
-#pragma unroll
-  for (int rb = 0; rb < MB; ++rb) rstd[rb] = 1.0f;
-  // RMSNorm scales: computed by the first pipeline of the phase once its
-  // first stages are in flight.
-  bool need_rstd = PRO == PRO_NORM;
-  auto rstd_hook = [&]() {
-    if constexpr (PRO == PRO_NORM) {
-      if (!need_rstd) return;
-      need_rstd = false;
-      row_scales<MB>(p, g, gl, rstd);
-    }
-  };
-
-  // Remainder n-blocks (stream-K), one n-block per segment.
-  for (long pos = rbeg; pos < rend;) {
-    const int t = (int)(pos / g.ks), k0 = (int)(pos % g.ks);
-    const int k1 = (int)(k0 + (rend - pos) < g.ks ? k0 + (rend - pos) : g.ks);
-    const int nb = c * G + t;
-    {
-      Pipe<MB, PRO, 1> P1;
-      pipe_setup(P1, g, nb, k0, k1);
-      f32x4 acc[MB][1];
-      pipe_run(P1, g, p.d, acc, rstd, rstd_hook);
-      reduce_waves<MB, 1>(tileS, acc);
-    }
-    constexpr int TS = 16 + 4;
+  bool first = true;
+  for (int t = blockIdx.x; t < tiles; t += p.G) {
+    const int g = t / S, s = t % S;
+    const int nb0 = g * sp.cw + (g < sp.n_hi ? g : sp.n_hi);
+    const int cw = sp.cw + (g < sp.n_hi ? 1 : 0);
+    const int k0 = (int)((long)s * sp.ksteps / S), k1 = (int)((long)(s + 1) * sp.ksteps / S);
+    if (!tile_dispatch<MB, NORM, CWM>(cw, p, step, layer, nb0, k0, k1, first ? phase : -1, A, gl, lds_flag))
+      return false;
+    if (first) trace_mark(sy, phase, 4);
+    first = false;
+    float* T = reinterpret_cast<float*>(A);
+    const int tile_words = cw * MB * 1024;
     bool finish = true;
-    if (!(k0 == 0 && k1 == g.ks)) {
-      const int slot = (pos == rbeg) ? 0 : 1;
-      float* mine = p.part + ((size_t)gi * 2 + slot) * ROWS * kNB;
-      for (int idx = 2 * threadIdx.x; idx < ROWS * kNB; idx += 2 * kThreads)
-        st_coherent2(mine + idx, tileS[(idx / kNB) * TS + idx % kNB], tileS[(idx / kNB) * TS + idx % kNB + 1]);
-      const long tile_lo = (long)t * g.ks, tile_hi = tile_lo + g.ks - 1;
-      const int g_lo = owner_of(tile_lo, Wr, G), g_hi = owner_of(tile_hi, Wr, G);
-      int contributors = 0;
-      for (int gg = g_lo; gg <= g_hi; ++gg)
-        contributors += ((long)gg * Wr / G < (long)(gg + 1) * Wr / G) ? 1 : 0;
-      finish = arrive_last(&p.tile_cnt[nb], contributors, sy.lds_flag);
+    if (S > 1) {
+      // Store this slice's partial; the group's last workgroup adds all S.
+      float* part_g = p.part + (size_t)(nb0 * S) * MB * 1024;
+      float* mine = part_g + (size_t)s * tile_words;
+      for (int w = 2 * threadIdx.x; w < tile_words; w += 2 * kThreads) st_coherent2(mine + w, T[w], T[w + 1]);
+      finish = arrive_last(sp.group_cnt + g, S, lds_flag);
       if (finish) {
-        for (int idx = 2 * threadIdx.x; idx < ROWS * kNB; idx += 2 * kThreads) {
-          float s0 = 0.0f, s1 = 0.0f;
-          for (int gg = g_lo; gg <= g_hi; ++gg) {
-            const long gb = (long)gg * Wr / G;
-            if (gb == (long)(gg + 1) * Wr / G) continue;  // empty run
-            const int sl = (gg == g_lo && gb < tile_lo) ? 1 : 0;
-            const float2 v = ld_coherent2(p.part + ((size_t)gg * 2 + sl) * ROWS * kNB + idx);
-            s0 += v.x;
-            s1 += v.y;
+        // T = sum of the S partials in slice order.  Loads go out in batches
+        // of 4 slices x 8 pairs per thread, so a group costs about S / 4
+        // round trips.
+        constexpr int B = 8;
+        const int pairs = tile_words / 2;
+        for (int base = threadIdx.x; base < pairs; base += kThreads * B) {
+          float2 acc[B];
+#pragma unroll
+          for (int j = 0; j < B; ++j) acc[j] = make_float2(0.0f, 0.0f);
+          for (int s0 = 0; s0 < S; s0 += 4) {
+            float2 v[4][B];
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+              for (int j = 0; j < B; ++j) {
+                const int idx = base + j * kThreads;
+                v[k][j] = (s0 + k < S && idx < pairs)
+                              ? ld_coherent2(part_g + (size_t)(s0 + k) * tile_words + 2 * idx)
+                              : make_float2(0.0f, 0.0f);
+              }
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+              for (int j = 0; j < B; ++j) {
+                acc[j].x += v[k][j].x;
+                acc[j].y += v[k][j].y;
+              }
           }
-          tileS[(idx / kNB) * TS + idx % kNB] = s0;
-          tileS[(idx / kNB) * TS + idx % kNB + 1] = s1;
+#pragma unroll
+          for (int j = 0; j < B; ++j) {
+            const int idx = base + j * kThreads;
+            if (idx < pairs) {
+              T[2 * idx] = acc[j].x;
+              T[2 * idx + 1] = acc[j].y;
+            }
+          }
         }
         __syncthreads();
       }
     }
     if (finish) {
-      epilogue<MB, EPI, 1>(p, e, tileS, nb, G + t, gl);
+      epilogue<MB, EPI>(p, io, T, nb0, cw, g, gl);
       if constexpr (EPI == EPI_LOGITS) {
-        if (arrive_last(p.lm_cnt, G + R, sy.lds_flag)) finish_walk(p, G + R, gl);
+        if (arrive_last(p.lm_cnt, sp.groups, lds_flag)) finish_walk(p, sp.groups, gl);
       }
     }
     __syncthreads();
-    pos += k1 - k0;
-  }
-
-  // Main block: n-blocks [gi c, (gi + 1) c) over the full K.  For the LM head
-  // the workgroup's argmax entry is the best over its sub-blocks.
-  trace_mark(sy, phase, 3);
-  for (int done = 0; done < c;) {
-    const int w = c - done < max_width<MB>() ? c - done : max_width<MB>();
-    const int nb0 = gi * c + done;
-    const int lm = done == 0 ? -2 : -1;
-    RowScale<MB> rs;
-#pragma unroll
-    for (int rb = 0; rb < MB; ++rb) rs.v[rb] = rstd[rb];
-    rs = main_dispatch<MB, PRO, EPI, max_width<MB>()>(w, p, step, layer, nb0, rs, need_rstd ? 1 : 0,
-                                                       tileS, gl, lm);
-    need_rstd = false;
-#pragma unroll
-    for (int rb = 0; rb < MB; ++rb) rstd[rb] = rs.v[rb];
-    done += w;
-  }
-  trace_mark(sy, phase, 4);
-  if constexpr (EPI == EPI_LOGITS) {
-    for (int r = threadIdx.x; r < ROWS; r += kThreads) {
-      const size_t at = (size_t)gi * p.Mp + r;
-      st_coherent(&p.lm_val[at], c > 0 ? gl.best_v[r] : -INFINITY);
-      st_coherent(&p.lm_idx[at], c > 0 ? gl.best_i[r] : 0x7fffffff);
-    }
-    if (arrive_last(p.lm_cnt, G + R, sy.lds_flag)) finish_walk(p, G + R, gl);
   }
   trace_mark(sy, phase, 5);
   return true;
@@ -910,7 +839,7 @@ __device__ __forceinline__ void attn_stage(char* lds, const bf16* kc, const bf16
 // merges its share of the rows.
 template <int MB, int DH>
 __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& pin, int layer, int phase, char* lds,
-                                                     int* lds_flag) {
+                                                                     int* lds_flag) {
   KParams& p = uniform_params(pin);
   const Sync sy = make_sync(p, lds_flag);
   layer = wave_uniform(layer);
@@ -1080,8 +1009,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0)
-      atomic_add_dev(&p.head_cnt[h], 1);
+    if (threadIdx.x == 0) atomic_add_dev(&p.head_cnt[h], 1);
     trace_mark(sy, phase, 4);
     if (!wait_at_least(sy, &p.head_cnt[h], S * (layer + 1))) return false;
     trace_mark(sy, phase, 5);
@@ -1143,7 +1071,8 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
 
 // Tree preparation (every node's depth, position prefix_len + depth, and
 // ancestor-or-self set: its row of the tree masking table) and the residual
-// stream's first version: the nodes' embedding rows.
+// stream's first version: the nodes' embedding rows, with the sums of
+// squares of every 32-column n-block.
 __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, int* par_s) {
   const bf16* E = (const bf16*)(p.packed + p.o_embed);
   if (blockIdx.x == 0) {
@@ -1169,18 +1098,27 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
     }
   }
   const int lane = threadIdx.x & 63;
-  for (int m = blockIdx.x; m < p.Mp; m += p.G) {
-    const bool valid = m < p.n;
-    const bf16* row = E + (size_t)(valid ? tree.tok[m] : 0) * p.d;
+  for (int m = blockIdx.x; m < p.n; m += p.G) {
+    // rotary table row m: (cos, sin) of pos(m) * theta^(-2j/Dh), j < Dh/2
+    if (threadIdx.x < p.Dh / 2) {
+      int dep = 0;
+      for (int j = tree.parent[m]; j >= 0; j = tree.parent[j]) ++dep;
+      const int jj = threadIdx.x;
+      float sn, cs;
+      sincosf((float)(p.prefix_len + dep) * rope_inv_freq(jj, p.Dh, p.log2_theta), &sn, &cs);
+      st_coherent2(p.rope + ((size_t)m * (p.Dh / 2) + jj) * 2, cs, sn);
+    }
+    const bf16* row = E + (size_t)tree.tok[m] * p.d;
     for (int c = threadIdx.x; c < p.d; c += kThreads) {
-      const float v = valid ? bf2f(ldg(row + c)) : 0.0f;
+      const float v = bf2f(ldg(row + c));
       st_coherent(&p.x[(size_t)m * p.d + c], v);
       float s = v * v;
+      s += __shfl_xor(s, 16, kWave);
       s += __shfl_xor(s, 8, kWave);
       s += __shfl_xor(s, 4, kWave);
       s += __shfl_xor(s, 2, kWave);
       s += __shfl_xor(s, 1, kWave);
-      if ((lane & 15) == 0) st_coherent(&p.ssq[(size_t)(c / kNB) * p.Mp + m], s);
+      if ((lane & 31) == 0) st_coherent(&p.ssq[(size_t)(c / kNB) * p.Mp + m], s);
     }
   }
 }
@@ -1188,17 +1126,8 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
 // ------------------------------------------------------------------ kernel
 
 template <int MB, int DH>
-constexpr int pass_lds_bytes() {
-  constexpr int attn = AttnGeom<DH>::BYTES;
-  constexpr int merge = 2 * kAttnMaxSplits * kMaxNodes * 4;
-  constexpr int tile = 16 * MB * (16 * max_width<MB>() + 4) * 4;
-  constexpr int m1 = attn > merge ? attn : merge;
-  return m1 > tile ? m1 : tile;
-}
-
-template <int MB, int DH>
 __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_arg, const TreeArgs tree) {
-  __shared__ __attribute__((aligned(16))) char lds_raw[pass_lds_bytes<MB, DH>()];
+  extern __shared__ __attribute__((aligned(16))) char lds_raw[];
   __shared__ GemmLds gl;
   __shared__ int par_s[128];
   __shared__ int flag;
@@ -1209,7 +1138,6 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
     return;  // (uniform over the grid: no workgroup reaches a barrier)
   }
   const Sync sy = make_sync(p, &flag);
-  float* tileS = reinterpret_cast<float*>(lds_raw);
   int phase = 0;
   bool ok = true;
 
@@ -1218,25 +1146,24 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
   ++phase;
 
   for (int l = 0; l < p.L && ok; ++l) {
-    ok = gemm_phase<MB, PRO_NORM, EPI_QKV>(p, STEP_QKV, l, phase, tileS, gl, &flag);
+    ok = gemm_phase<MB, EPI_QKV>(p, STEP_QKV, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
-    ok = attn_phase<MB, DH>(p, l, phase, lds_raw, &flag);
+    ok = attn_phase<2 * MB, DH>(p, l, phase, lds_raw, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
-    ok = gemm_phase<MB, PRO_BF16, EPI_RESID>(p, STEP_O, l, phase, tileS, gl, &flag);
+    ok = gemm_phase<MB, EPI_RESID>(p, STEP_O, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
-    ok = gemm_phase<MB, PRO_NORM, EPI_SWIGLU>(p, STEP_GATE_UP, l, phase, tileS, gl, &flag);
+    ok = gemm_phase<MB, EPI_SWIGLU>(p, STEP_GATE_UP, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
-    ok = gemm_phase<MB, PRO_BF16, EPI_RESID>(p, STEP_DOWN, l, phase, tileS, gl, &flag);
+    ok = gemm_phase<MB, EPI_RESID>(p, STEP_DOWN, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
   }
   if (ok) {  // final norm + LM head + argmax + accept walk
-    if (gemm_phase<MB, PRO_NORM, EPI_LOGITS>(p, STEP_LM, 0, phase, tileS, gl, &flag))
-      trace_mark(sy, phase, 2);
+    if (gemm_phase<MB, EPI_LOGITS>(p, STEP_LM, 0, phase, lds_raw, gl, &flag)) trace_mark(sy, phase, 2);
   }
   // Leave the pass: the last workgroup out resets the barrier and join counters.
   if (arrive_last(p.exit_cnt, p.G, &flag)) {
@@ -1245,55 +1172,73 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
   }
 }
 
+template <int DH>
+constexpr size_t dyn_lds_bytes() {
+  constexpr size_t attn = AttnGeom<DH>::BYTES;
+  constexpr size_t merge = 2 * kAttnMaxSplits * kMaxNodes * 4;
+  constexpr size_t a = kAStageBytes;
+  constexpr size_t m1 = attn > merge ? attn : merge;
+  return m1 > a ? m1 : a;
+}
+
 template <int MB, int DH>
 hipError_t launch_pass_mb(KParams& p, const TreeArgs& tree, hipStream_t st) {
+  static bool attr_set = false;  // per process; the attribute is per function
+  const void* fn = (const void*)pass_kernel<MB, DH>;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_lds_bytes<DH>());
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
   void* args[] = {(void*)&p, (void*)&tree};
-  return hipLaunchCooperativeKernel((const void*)pass_kernel<MB, DH>, dim3(p.G), dim3(kThreads), args,
-                                    0, st);
+  return hipLaunchCooperativeKernel(fn, dim3(p.G), dim3(kThreads), args, (unsigned)dyn_lds_bytes<DH>(), st);
 }
 
 template <int MB, int DH>
 int occupancy_mb() {
+  const void* fn = (const void*)pass_kernel<MB, DH>;
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_lds_bytes<DH>()) != hipSuccess)
+    return 0;
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, (const void*)pass_kernel<MB, DH>, kThreads,
-                                                   0) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, kThreads, dyn_lds_bytes<DH>()) != hipSuccess)
     return 0;
   return blocks;
 }
 
 }  // namespace
 
-hipError_t launch_pass(int mb, KParams& p, const TreeArgs& tree, hipStream_t st) {
+hipError_t launch_pass(int mb32, KParams& p, const TreeArgs& tree, hipStream_t st) {
 #define LLMCAD_PASS_CASE(M)                                                 \
   case M:                                                                   \
     return p.Dh == 128 ? launch_pass_mb<M, 128>(p, tree, st)                \
                        : launch_pass_mb<M, 64>(p, tree, st);
-  switch (mb) {
+  switch (mb32) {
     LLMCAD_PASS_CASE(1)
     LLMCAD_PASS_CASE(2)
-    LLMCAD_PASS_CASE(3)
     LLMCAD_PASS_CASE(4)
-    LLMCAD_PASS_CASE(8)
     default:
       return hipErrorInvalidValue;
   }
 #undef LLMCAD_PASS_CASE
 }
 
-int pass_occupancy(int mb, int dh) {
+int pass_occupancy(int mb32, int dh) {
 #define LLMCAD_OCC_CASE(M) \
   case M:                  \
     return dh == 128 ? occupancy_mb<M, 128>() : occupancy_mb<M, 64>();
-  switch (mb) {
+  switch (mb32) {
     LLMCAD_OCC_CASE(1)
     LLMCAD_OCC_CASE(2)
-    LLMCAD_OCC_CASE(3)
     LLMCAD_OCC_CASE(4)
-    LLMCAD_OCC_CASE(8)
     default:
       return 0;
   }
 #undef LLMCAD_OCC_CASE
+}
+
+size_t pass_lds_bytes(int mb32, int dh) {
+  (void)mb32;
+  return dh == 128 ? dyn_lds_bytes<128>() : dyn_lds_bytes<64>();
 }
 
 }  // namespace llmcad

@@ -103,13 +103,13 @@ def test_verify_matches_oracle(model, tree):
 
 def test_launch_shape_variants(model, monkeypatch):
     # One position split per head (every split spans several 128-key tiles),
-    # three splits, and two workgroups per CU (a different stream-K cut and
-    # main-block width) all meet the oracle bar.
+    # three splits, and smaller grids (other GEMM tilings: more K splits per
+    # column group, several tiles per workgroup) all meet the oracle bar.
     parent = TREES["b432_n41"]
     tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=7)
     _check_all(model, parent, tok, "default")
     for env in ({"LLMCAD_ATTN_SPLITS": "1"}, {"LLMCAD_ATTN_SPLITS": "3"},
-                {"LLMCAD_PASS_WGS_PER_CU": "2"}):
+                {"LLMCAD_PASS_GRID": "200"}, {"LLMCAD_PASS_GRID": "24"}):
         for k, v in env.items():
             monkeypatch.setenv(k, v)
         _check_all(model, parent, tok, str(env))
