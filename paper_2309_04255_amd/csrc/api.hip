@@ -202,6 +202,8 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   if (s.H * S > G) S = G / s.H;
   if (S < 1) S = 1;
   p.attn_splits = S;
+  p.group_cnt_all = (int*)(ws + W.counters);
+  p.n_group_cnt = W.n_group_counters;
   p.head_cnt = (int*)(ws + W.head_counters());
   p.lm_cnt = (int*)(ws + W.lm_cnt());
   p.exit_cnt = (int*)(ws + W.exit_cnt());
@@ -455,7 +457,7 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
     case 3: *offset = W.hs; *bytes = (size_t)W.Mp * s.Fp * 2; break;
     case 4: *offset = W.amax; *bytes = (size_t)W.Mp * 4; break;
     case 5: *offset = W.status(); *bytes = 4; break;
-    case 6: *offset = W.trace; *bytes = (size_t)8 * (2 + 5 * s.L) * 6 * 8; break;
+    case 6: *offset = W.trace; *bytes = (size_t)8 * (2 + 5 * s.L) * 8 * 8; break;
     case 7: *offset = W.xs; *bytes = (size_t)(2 * s.L + 1) * W.Mp * s.d * 4; break;
     case 8: *offset = W.ssqs; *bytes = (size_t)(2 * s.L + 1) * s.d_nb * W.Mp * 4; break;
     case 9: *offset = W.qs; *bytes = (size_t)s.L * W.Mp * s.d * 2; break;

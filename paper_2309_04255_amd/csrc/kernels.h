@@ -66,12 +66,14 @@ struct PassParams {
   float* attn_o;    // [H][S][Mp][Dh]
   float* attn_ml;   // [H][S][Mp][2]
   int attn_splits;
+  int* group_cnt_all;  // every step's group counters (cleared when the pass ends)
+  int n_group_cnt;
   int* head_cnt;
   int* lm_cnt;
   int* exit_cnt;
   int* status;
   int* bar;         // [kBarSlots][kBarStride]
-  float* lm_val;    // [v_nb][Mp]
+  float* lm_val;    // [LM argmax slots][Mp]
   int* lm_idx;
   int* amax;        // [Mp]
   // outputs
@@ -82,7 +84,7 @@ struct PassParams {
   int* next_token;
   // control
   int spin_limit;    // bound of every wait loop (polls)
-  long long* trace;  // diagnostics: [8][2 + 5L][6] phase timestamps, or null
+  long long* trace;  // diagnostics: [8][2 + 5L][8] phase timestamps, or null
 };
 
 hipError_t launch_pass(int mb32, const PassParams& p, const TreeArgs& tree, hipStream_t st);

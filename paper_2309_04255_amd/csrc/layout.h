@@ -192,12 +192,12 @@ struct WorkspaceLayout {
   size_t bar;          // int32 [kBarSlots][kBarStride] grid-barrier counters
   size_t scratch_out;  // int32 [128 + 2] path/len/next sink for prefill
   size_t tree;         // int32 tok[128] | parent[128] | depth[128] | pos[128] | uint32 anc[128][4]
-  size_t trace;        // int64 [8][2 + 5L][6]    phase timestamps (diagnostics)
+  size_t trace;        // int64 [8][2 + 5L][8]    phase timestamps (diagnostics)
   size_t zero;         // kZeroBytes of zeros (never written by a pass)
   size_t rope;         // fp32 [Mp][Dh/2][2]      cos, sin of every node's rotary angles
   size_t amax;         // int32 [Mp]              per-node greedy token
-  size_t lm_val;       // fp32 [v_nb][Mp]         argmax per LM-head column group
-  size_t lm_idx;       // int32 [v_nb][Mp]
+  size_t lm_val;       // fp32 [slots][Mp]        LM-head argmax per tile (or column group)
+  size_t lm_idx;       // int32 [slots][Mp]
   size_t xs;           // fp32 [2L+1][Mp][d]      residual stream versions
   size_t ssqs;         // fp32 [2L+1][d/32][Mp]   their per-n-block sums of squares
   size_t qs;           // bf16 [L][Mp][d]         queries after the rotary embedding
@@ -227,12 +227,13 @@ struct WorkspaceLayout {
     bar = take((size_t)kBarSlots * kBarStride * 4);
     scratch_out = take((128 + 2) * 4);
     tree = take(4 * 128 * 4 + 128 * 4 * 4);
-    trace = take((size_t)8 * (2 + 5 * s.L) * 6 * 8);
+    trace = take((size_t)8 * (2 + 5 * s.L) * 8 * 8);
     zero = take(kZeroBytes);
     rope = take((size_t)Mp * s.Dh * 4);
     amax = take((size_t)Mp * 4);
-    lm_val = take((size_t)s.v_nb * Mp * 4);
-    lm_idx = take((size_t)s.v_nb * Mp * 4);
+    const int lm_slots = plans.g[STEP_LM].tiles() > s.v_nb ? plans.g[STEP_LM].tiles() : s.v_nb;
+    lm_val = take((size_t)lm_slots * Mp * 4);
+    lm_idx = take((size_t)lm_slots * Mp * 4);
     xs = take((size_t)(2 * s.L + 1) * Mp * s.d * 4);
     ssqs = take((size_t)(2 * s.L + 1) * s.d_nb * Mp * 4);
     qs = take((size_t)s.L * Mp * s.d * 2);

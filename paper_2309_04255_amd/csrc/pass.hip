@@ -95,7 +95,7 @@ struct Sync {
   int* status;
   int limit;
   int* lds_flag;
-  long long* trace;  // [phase][6] timestamps of this workgroup, or null
+  long long* trace;  // [phase][8] timestamps of this workgroup, or null
 };
 
 __device__ __forceinline__ Sync make_sync(KParams& p, int* lds_flag) {
@@ -105,16 +105,17 @@ __device__ __forceinline__ Sync make_sync(KParams& p, int* lds_flag) {
   s.limit = p.spin_limit;
   s.lds_flag = lds_flag;
   s.trace = p.trace != nullptr && (int)blockIdx.x < kTraceWgs
-                ? p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 6
+                ? p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 8
                 : nullptr;
   return s;
 }
 
 // Diagnostics: wall-clock (100 MHz) marks per phase: 0 = barrier wait
 // entered, 1 = wait over, 2 = phase work done; GEMM phases also mark 3 =
-// activations staged, 4 = weight streaming done, 5 = epilogue done.
+// activations staged, 4 = weight streaming done, 5 = epilogue done, 6 =
+// group hand-off done, 7 = partials added (group's last workgroup).
 __device__ __forceinline__ void trace_mark(const Sync& s, int phase, int k) {
-  if (s.trace != nullptr && threadIdx.x == 0) stg(s.trace + phase * 6 + k, (long long)wall_clock64());
+  if (s.trace != nullptr && threadIdx.x == 0) stg(s.trace + phase * 8 + k, (long long)wall_clock64());
 }
 
 // End of a phase: this workgroup's stores have completed, then one
@@ -404,7 +405,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (wait_phase >= 0 && p.trace != nullptr && (int)blockIdx.x < kTraceWgs && threadIdx.x == 0)
-    stg(p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 6 + wait_phase * 6 + 3, (long long)wall_clock64());
+    stg(p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 8 + wait_phase * 8 + 3, (long long)wall_clock64());
 
   float rs[MB];
 #pragma unroll
@@ -494,15 +495,69 @@ __device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) 
   return exp2f(-(2.0f * (float)j / (float)Dh) * log2_theta);
 }
 
-// Epilogue of a complete group held in T (fp32 [cw][MB][64][16]): each
-// wave takes (n-block, row block) units in turn, one accumulator tile per
-// unit, and writes the step's outputs with device-coherent stores.
+// Epilogue.  A group's output is cw n-blocks x MB row blocks, one 32x32
+// accumulator tile ("unit") each, unit u = c MB + mb, held in T (fp32
+// [cw][MB][64 lanes][16], MFMA accumulator order).  A workgroup finishes
+// units [u_lo, u_hi): its waves take them in turn, kEpiBatch per wave at a
+// time, and write the step's outputs with device-coherent stores.  The
+// inputs a batch reads from memory (the residual stream, the rotary table)
+// are loaded first, all at once (EpiPre), so that a batch costs one round
+// trip; the first batch's are issued before the group's partials are read.
+constexpr int kEpiBatch = 2;
+
+template <int EPI>
+struct EpiPre {
+  static constexpr int U = (EPI == EPI_RESID || EPI == EPI_QKV) ? kEpiBatch : 1;
+  float a[U][16];                       // RESID: x_in; QKV: cos
+  float b[EPI == EPI_QKV ? U : 1][16];  // QKV: sin
+};
+
 template <int MB, int EPI>
-__device__ __forceinline__ void epilogue(KParams& p, const StepIo& io, const float* T, int nb0, int cw, int group,
-                                         GemmLds& gl) {
+__device__ __forceinline__ void epilogue_preload(KParams& p, const StepIo& io, int nb0, int u_lo, int u_hi, int ub,
+                                                 EpiPre<EPI>& pre) {
+  if constexpr (EPI == EPI_RESID || EPI == EPI_QKV) {
+    const int wave = wave_index(), lane = threadIdx.x & 63;
+    const int j = lane & 31;
+#pragma unroll
+    for (int uu = 0; uu < kEpiBatch; ++uu) {
+      const int unit = u_lo + wave + kWaves * (ub + uu);
+      if (unit >= u_hi) break;
+      const int c = unit / MB, mb = unit % MB;
+      const int nb = nb0 + c;
+      if constexpr (EPI == EPI_RESID) {
+        const int col = kNB * nb + j;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = 32 * mb + acc_row(i, lane);
+          pre.a[uu][i] = r < p.n ? ldg(io.x_in + (size_t)r * p.d + col) : 0.0f;
+        }
+      } else {
+        const int d = p.d, dh = p.Dh;
+        if (kNB * nb < 2 * d) {
+          const int t = ((kNB * nb) % d % dh) / kNB;
+          const int jj = 16 * t + (j & 15);
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int r = 32 * mb + acc_row(i, lane);
+            const float2 cs = r < p.n ? ldg((const float2*)p.rope + (size_t)r * (dh / 2) + jj) : make_float2(1.0f, 0.0f);
+            pre.a[uu][i] = cs.x;
+            pre.b[uu][i] = cs.y;
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int MB, int EPI>
+__device__ __forceinline__ void epilogue(KParams& p, const StepIo& io, const float* T, int nb0, int u_lo, int u_hi,
+                                         int ub, const EpiPre<EPI>& pre, GemmLds& gl) {
   const int wave = wave_index(), lane = threadIdx.x & 63;
   const int j = lane & 31;
-  for (int unit = wave; unit < cw * MB; unit += kWaves) {
+#pragma unroll
+  for (int uu = 0; uu < kEpiBatch; ++uu) {
+    const int unit = u_lo + wave + kWaves * (ub + uu);
+    if (unit >= u_hi) break;
     const int c = unit / MB, mb = unit % MB;
     const int nb = nb0 + c;
     float v[16];
@@ -531,8 +586,7 @@ __device__ __forceinline__ void epilogue(KParams& p, const StepIo& io, const flo
         for (int i = 0; i < 16; ++i) {
           const int r = 32 * mb + acc_row(i, lane);
           const float partner = __shfl_xor(v[i], 16, kWave);
-          const float2 cssn = r < p.n ? ldg((const float2*)p.rope + (size_t)r * (dh / 2) + jj) : make_float2(1.0f, 0.0f);
-          const float cs = cssn.x, sn = cssn.y;
+          const float cs = pre.a[uu][i], sn = pre.b[uu][i];
           const float outv = j < 16 ? v[i] * cs - partner * sn : v[i] * cs + partner * sn;
           const float nxt = __shfl_down(outv, 1, kWave);
           if (r < p.n && (j & 1) == 0) {
@@ -555,11 +609,8 @@ __device__ __forceinline__ void epilogue(KParams& p, const StepIo& io, const flo
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int r = 32 * mb + acc_row(i, lane);
-        float xn = 0.0f;
-        if (r < p.n) {
-          xn = ldg(io.x_in + (size_t)r * p.d + col) + v[i];
-          st_coherent(io.x_out + (size_t)r * p.d + col, xn);
-        }
+        const float xn = r < p.n ? pre.a[uu][i] + v[i] : 0.0f;
+        if (r < p.n) st_coherent(io.x_out + (size_t)r * p.d + col, xn);
         float s = xn * xn;  // sum of squares over the n-block's 32 columns
         s += __shfl_xor(s, 16, kWave);
         s += __shfl_xor(s, 8, kWave);
@@ -604,22 +655,29 @@ __device__ __forceinline__ void epilogue(KParams& p, const StepIo& io, const flo
       }
     }
   }
-  if constexpr (EPI == EPI_LOGITS) {
-    __syncthreads();
-    for (int r = threadIdx.x; r < 32 * MB; r += kThreads) {
-      float mv = -INFINITY;
-      int mi = 0x7fffffff;
-      for (int c = 0; c < cw; ++c) {
-        const float v = gl.red_v[r][c];
-        const int i = gl.red_i[r][c];
-        if (v > mv || (v == mv && i < mi)) {
-          mv = v;
-          mi = i;
-        }
+}
+
+// LM head: per row, the best (value, lowest column) over this workgroup's
+// units of the group, into argmax slot `slot` (-inf where it has none).
+template <int MB>
+__device__ __forceinline__ void logits_units_argmax(KParams& p, int cw, int u_lo, int u_hi, int slot, GemmLds& gl) {
+  __syncthreads();
+  for (int r = threadIdx.x; r < 32 * MB; r += kThreads) {
+    const int mb = r / 32;
+    float mv = -INFINITY;
+    int mi = 0x7fffffff;
+    for (int c = 0; c < cw; ++c) {
+      const int u = c * MB + mb;
+      if (u < u_lo || u >= u_hi) continue;
+      const float v = gl.red_v[r][c];
+      const int i = gl.red_i[r][c];
+      if (v > mv || (v == mv && i < mi)) {
+        mv = v;
+        mi = i;
       }
-      st_coherent(&p.lm_val[(size_t)group * p.Mp + r], mv);
-      st_coherent(&p.lm_idx[(size_t)group * p.Mp + r], mi);
     }
+    st_coherent(&p.lm_val[(size_t)slot * p.Mp + r], mv);
+    st_coherent(&p.lm_idx[(size_t)slot * p.Mp + r], mi);
   }
 }
 
@@ -691,6 +749,116 @@ __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl
   __syncthreads();
 }
 
+// The hand-off of one tile whose sum is in T.  With S > 1 the tile's
+// partial goes to memory; when the step has at most one tile per workgroup,
+// the S workgroups of the group wait for each other and each adds the S
+// partials of its own 1/S of the group's units (in slice order) and runs
+// their epilogue; otherwise (no waits inside a phase: a workgroup's later
+// tile could be waited for) the group's last workgroup does all of it.  A
+// function of its own so that its registers are allocated apart from the
+// streaming loops'.  False if a wait ran out.
+template <int MB, int EPI>
+__device__ __attribute__((noinline, not_tail_called)) bool finish_tile(KParams& pin, int step, int layer, int t,
+                                                                      int tr_phase, char* A, GemmLds& gl,
+                                                                      int* lds_flag) {
+  KParams& p = uniform_params(pin);
+  step = wave_uniform(step);
+  layer = wave_uniform(layer);
+  t = wave_uniform(t);
+  tr_phase = wave_uniform(tr_phase);
+  const Sync sy = make_sync(p, lds_flag);
+  const StepPlan& sp = p.step[step];
+  const int S = sp.S, tiles = sp.groups * sp.S;
+  const StepIo io = step_io(p, step, layer);
+  const int g = t / S, s = t % S;
+  const int nb0 = g * sp.cw + (g < sp.n_hi ? g : sp.n_hi);
+  const int cw = sp.cw + (g < sp.n_hi ? 1 : 0);
+  const int U = cw * MB;
+  const int tile_words = U * 1024;
+  float* T = reinterpret_cast<float*>(A);
+  int u_lo = 0, u_hi = U;
+  bool finish = true;
+  const bool shared = tiles <= p.G;
+  int* cnt = sp.group_cnt + g;
+  float* part_g = p.part + (size_t)(nb0 * S) * MB * 1024;
+  if (S > 1) {
+    float* mine = part_g + (size_t)s * tile_words;
+    for (int w = 2 * threadIdx.x; w < tile_words; w += 2 * kThreads) st_coherent2(mine + w, T[w], T[w + 1]);
+    if (shared) {
+      u_lo = s * U / S;
+      u_hi = (s + 1) * U / S;
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      if (threadIdx.x == 0) atomic_add_dev(cnt, 1);
+    } else {
+      finish = arrive_last(cnt, S, lds_flag);
+    }
+  }
+  EpiPre<EPI> pre;
+  if (finish) epilogue_preload<MB, EPI>(p, io, nb0, u_lo, u_hi, 0, pre);
+  if (S > 1) {
+    if (tr_phase >= 0) trace_mark(sy, tr_phase, 6);
+    // Group counters are cleared when the pass ends: within a pass a step's
+    // counter of a group is used once per layer.
+    if (shared && !wait_at_least(sy, cnt, S * (layer + 1))) return false;
+    if (finish) {
+      // T[units u_lo..u_hi) = sum of the S partials in slice order.  Loads
+      // go out in batches of 4 slices x 8 pairs per thread, so the sum costs
+      // about S / 4 round trips.
+      constexpr int B = 8;
+      const int p_lo = u_lo * 512, p_hi = u_hi * 512;  // float2 pairs
+      for (int base = p_lo + (int)threadIdx.x; base < p_hi; base += kThreads * B) {
+        float2 acc[B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) acc[j] = make_float2(0.0f, 0.0f);
+        for (int s0 = 0; s0 < S; s0 += 4) {
+          float2 v[4][B];
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+              const int idx = base + j * kThreads;
+              v[k][j] = (s0 + k < S && idx < p_hi)
+                            ? ld_coherent2(part_g + (size_t)(s0 + k) * tile_words + 2 * idx)
+                            : make_float2(0.0f, 0.0f);
+            }
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+              acc[j].x += v[k][j].x;
+              acc[j].y += v[k][j].y;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+          const int idx = base + j * kThreads;
+          if (idx < p_hi) {
+            T[2 * idx] = acc[j].x;
+            T[2 * idx + 1] = acc[j].y;
+          }
+        }
+      }
+      __syncthreads();
+      if (tr_phase >= 0) trace_mark(sy, tr_phase, 7);
+    }
+  }
+  if (finish) {
+    for (int ub = 0; u_lo + wave_index() + kWaves * ub < u_hi; ub += kEpiBatch) {
+      if (ub > 0) epilogue_preload<MB, EPI>(p, io, nb0, u_lo, u_hi, ub, pre);
+      epilogue<MB, EPI>(p, io, T, nb0, u_lo, u_hi, ub, pre, gl);
+    }
+    if constexpr (EPI == EPI_LOGITS) {
+      const int slot = shared ? t : g;
+      logits_units_argmax<MB>(p, cw, u_lo, u_hi, slot, gl);
+      if (arrive_last(p.lm_cnt, shared ? tiles : sp.groups, lds_flag)) finish_walk(p, shared ? tiles : sp.groups, gl);
+    }
+  }
+  __syncthreads();
+  return true;
+}
+
 // One GEMM phase: this workgroup's tiles, each followed by its share of the
 // group hand-off and, in the group's last workgroup, the epilogue.
 template <int MB, int EPI>
@@ -704,7 +872,6 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   const Sync sy = make_sync(p, lds_flag);
   const StepPlan& sp = p.step[step];
   const int S = sp.S, tiles = sp.groups * sp.S;
-  const StepIo io = step_io(p, step, layer);
   constexpr bool NORM = EPI != EPI_RESID;
   constexpr int CWM = kMaxCW / MB;
   // The barrier counts arrivals: it is exact only if every workgroup waits
@@ -724,64 +891,8 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
     if (!tile_dispatch<MB, NORM, CWM>(cw, p, step, layer, nb0, k0, k1, first ? phase : -1, A, gl, lds_flag))
       return false;
     if (first) trace_mark(sy, phase, 4);
+    if (!finish_tile<MB, EPI>(p, step, layer, t, first ? phase : -1, A, gl, lds_flag)) return false;
     first = false;
-    float* T = reinterpret_cast<float*>(A);
-    const int tile_words = cw * MB * 1024;
-    bool finish = true;
-    if (S > 1) {
-      // Store this slice's partial; the group's last workgroup adds all S.
-      float* part_g = p.part + (size_t)(nb0 * S) * MB * 1024;
-      float* mine = part_g + (size_t)s * tile_words;
-      for (int w = 2 * threadIdx.x; w < tile_words; w += 2 * kThreads) st_coherent2(mine + w, T[w], T[w + 1]);
-      finish = arrive_last(sp.group_cnt + g, S, lds_flag);
-      if (finish) {
-        // T = sum of the S partials in slice order.  Loads go out in batches
-        // of 4 slices x 8 pairs per thread, so a group costs about S / 4
-        // round trips.
-        constexpr int B = 8;
-        const int pairs = tile_words / 2;
-        for (int base = threadIdx.x; base < pairs; base += kThreads * B) {
-          float2 acc[B];
-#pragma unroll
-          for (int j = 0; j < B; ++j) acc[j] = make_float2(0.0f, 0.0f);
-          for (int s0 = 0; s0 < S; s0 += 4) {
-            float2 v[4][B];
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-#pragma unroll
-              for (int j = 0; j < B; ++j) {
-                const int idx = base + j * kThreads;
-                v[k][j] = (s0 + k < S && idx < pairs)
-                              ? ld_coherent2(part_g + (size_t)(s0 + k) * tile_words + 2 * idx)
-                              : make_float2(0.0f, 0.0f);
-              }
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-#pragma unroll
-              for (int j = 0; j < B; ++j) {
-                acc[j].x += v[k][j].x;
-                acc[j].y += v[k][j].y;
-              }
-          }
-#pragma unroll
-          for (int j = 0; j < B; ++j) {
-            const int idx = base + j * kThreads;
-            if (idx < pairs) {
-              T[2 * idx] = acc[j].x;
-              T[2 * idx + 1] = acc[j].y;
-            }
-          }
-        }
-        __syncthreads();
-      }
-    }
-    if (finish) {
-      epilogue<MB, EPI>(p, io, T, nb0, cw, g, gl);
-      if constexpr (EPI == EPI_LOGITS) {
-        if (arrive_last(p.lm_cnt, sp.groups, lds_flag)) finish_walk(p, sp.groups, gl);
-      }
-    }
-    __syncthreads();
   }
   trace_mark(sy, phase, 5);
   return true;
@@ -1169,6 +1280,7 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
   if (arrive_last(p.exit_cnt, p.G, &flag)) {
     if (threadIdx.x < kBarSlots) st_coherent(p.bar + threadIdx.x * kBarStride, 0);
     for (int h = threadIdx.x; h < p.H; h += kThreads) st_coherent(&p.head_cnt[h], 0);
+    for (int i = threadIdx.x; i < p.n_group_cnt; i += kThreads) st_coherent(p.group_cnt_all + i, 0);
   }
 }
 
