@@ -175,7 +175,9 @@ const char* llmcad_status_string(int status);
  * variable LLMCAD_TRACE is 1), 7 every residual stream version fp32
  * [2L+1][Mp][d], 8 their per-32-column sums of squares fp32 [2L+1][d/32][Mp],
  * 9 every layer's queries bf16 [L][Mp][d], 10 attention outputs bf16
- * [L][Mp][d], 11 SwiGLU products bf16 [L][Mp][Fp];
+ * [L][Mp][d], 11 SwiGLU products bf16 [L][Mp][Fp], 12 every residual
+ * stream version times the gain of the RMSNorm that reads it, bf16
+ * [2L+1][Mp][d] (the input of the QKV, gate/up and LM-head products);
  * Mp = max_n rounded up to 32, 64 or 128, Fp = F rounded up to 16.  Offsets describe a
  * pass over max_n nodes (call with max_n = that pass's n). */
 int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t which, size_t* offset,

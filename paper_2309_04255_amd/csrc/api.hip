@@ -186,6 +186,7 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.zero = ws + W.zero;
   p.rope = (float*)(ws + W.rope);
   p.x = (float*)(ws + W.xs);
+  p.xg = (bf16*)(ws + W.xgs);
   p.ssq = (float*)(ws + W.ssqs);
   p.q = (bf16*)(ws + W.qs);
   p.o = (bf16*)(ws + W.os);
@@ -463,6 +464,7 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
     case 9: *offset = W.qs; *bytes = (size_t)s.L * W.Mp * s.d * 2; break;
     case 10: *offset = W.os; *bytes = (size_t)s.L * W.Mp * s.d * 2; break;
     case 11: *offset = W.hs; *bytes = (size_t)s.L * W.Mp * s.Fp * 2; break;
+    case 12: *offset = W.xgs; *bytes = (size_t)(2 * s.L + 1) * W.Mp * s.d * 2; break;
     default: return LLMCAD_EARG;
   }
   return LLMCAD_OK;

@@ -58,6 +58,7 @@ struct PassParams {
   const char* zero; // kZeroBytes of zeros
   float* rope;      // [Mp][Dh/2][2] cos, sin of every node's rotary angles
   float* x;         // [2L+1][Mp][d]
+  bf16* xg;         // [2L+1][Mp][d] bf16(x * g), g the gain of the norm that reads x
   float* ssq;       // [2L+1][d/32][Mp]
   bf16* q;          // [L][Mp][d]   queries after the rotary embedding
   bf16* o;          // [L][Mp][d]

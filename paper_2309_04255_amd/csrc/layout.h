@@ -117,23 +117,20 @@ struct GemmPlan {
   int kt_max() const { return cdiv(ksteps, S); }
 };
 
-// Bytes of LDS a tile's activation slice takes: per k-step and 32-row block
-// 1 KiB of bf16 (or 2 KiB of fp32 plus the norm gains, 32 bytes per k-step
-// copied in whole KiB, when the RMSNorm is applied as the slice is read).
-inline int a_stage_bytes(int kt, int mb32, bool norm) {
-  return norm ? kt * mb32 * 2048 + cdiv(kt, 32) * 1024 : kt * mb32 * 1024;
-}
+// Bytes of LDS a tile's bf16 activation slice takes: 1 KiB per k-step and
+// 32-row block.
+inline int a_stage_bytes(int kt, int mb32) { return kt * mb32 * 1024; }
 
 // Chooses S and the column groups for G workgroups: every tile's activation
 // slice must fit kAStageBytes; among those, minimise the busiest workgroup's
 // weight bytes plus a share of its activation and partial-sum traffic.
-inline GemmPlan plan_gemm(int nblocks, int ksteps, int mb32, bool norm, int G) {
+inline GemmPlan plan_gemm(int nblocks, int ksteps, int mb32, int G) {
   GemmPlan best{nblocks, ksteps, 0, 0, 0, 0};
   double best_cost = 1e300;
   const int cw_cap = kMaxCW / mb32;
   for (int S = 1; S <= kMaxSplits && S <= ksteps; ++S) {
     const int kt = cdiv(ksteps, S);
-    if (a_stage_bytes(kt, mb32, norm) > kAStageBytes) continue;
+    if (a_stage_bytes(kt, mb32) > kAStageBytes) continue;
     int groups = G / S;
     if (groups < 1) groups = 1;
     if (groups > nblocks) groups = nblocks;
@@ -142,7 +139,7 @@ inline GemmPlan plan_gemm(int nblocks, int ksteps, int mb32, bool norm, int G) {
     const int cwm = cw + (n_hi > 0 ? 1 : 0);
     const int rounds = cdiv(groups * S, G);
     const double w_kb = (double)rounds * cwm * kt;
-    const double a_kb = (double)rounds * a_stage_bytes(kt, mb32, norm) / 1024.0;
+    const double a_kb = (double)rounds * a_stage_bytes(kt, mb32) / 1024.0;
     const double fix_kb = S > 1 ? (double)S * cwm * mb32 * 4.0 : 0.0;
     const double cost = w_kb + 0.5 * a_kb + 0.5 * fix_kb;
     if (cost < best_cost - 1e-9) {
@@ -156,11 +153,11 @@ inline GemmPlan plan_gemm(int nblocks, int ksteps, int mb32, bool norm, int G) {
 struct PassPlans {
   GemmPlan g[kSteps];
   PassPlans(const Shape& s, int mb32, int G) {
-    g[STEP_QKV] = plan_gemm(s.qkv_nb, s.ks_d, mb32, true, G);
-    g[STEP_O] = plan_gemm(s.d_nb, s.ks_d, mb32, false, G);
-    g[STEP_GATE_UP] = plan_gemm(s.gu_nb, s.ks_d, mb32, true, G);
-    g[STEP_DOWN] = plan_gemm(s.d_nb, s.ks_f, mb32, false, G);
-    g[STEP_LM] = plan_gemm(s.v_nb, s.ks_d, mb32, true, G);
+    g[STEP_QKV] = plan_gemm(s.qkv_nb, s.ks_d, mb32, G);
+    g[STEP_O] = plan_gemm(s.d_nb, s.ks_d, mb32, G);
+    g[STEP_GATE_UP] = plan_gemm(s.gu_nb, s.ks_d, mb32, G);
+    g[STEP_DOWN] = plan_gemm(s.d_nb, s.ks_f, mb32, G);
+    g[STEP_LM] = plan_gemm(s.v_nb, s.ks_d, mb32, G);
   }
   bool ok() const {
     for (int i = 0; i < kSteps; ++i)
@@ -199,6 +196,7 @@ struct WorkspaceLayout {
   size_t lm_val;       // fp32 [slots][Mp]        LM-head argmax per tile (or column group)
   size_t lm_idx;       // int32 [slots][Mp]
   size_t xs;           // fp32 [2L+1][Mp][d]      residual stream versions
+  size_t xgs;          // bf16 [2L+1][Mp][d]      bf16(x * g) of each version (g: its norm's gain)
   size_t ssqs;         // fp32 [2L+1][d/32][Mp]   their per-n-block sums of squares
   size_t qs;           // bf16 [L][Mp][d]         queries after the rotary embedding
   size_t os;           // bf16 [L][Mp][d]         attention output
@@ -235,6 +233,7 @@ struct WorkspaceLayout {
     lm_val = take((size_t)lm_slots * Mp * 4);
     lm_idx = take((size_t)lm_slots * Mp * 4);
     xs = take((size_t)(2 * s.L + 1) * Mp * s.d * 4);
+    xgs = take((size_t)(2 * s.L + 1) * Mp * s.d * 2);
     ssqs = take((size_t)(2 * s.L + 1) * s.d_nb * Mp * 4);
     qs = take((size_t)s.L * Mp * s.d * 2);
     os = take((size_t)s.L * Mp * s.d * 2);

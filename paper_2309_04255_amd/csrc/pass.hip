@@ -194,16 +194,18 @@ struct GemmLds {
   int walk_len;
 };
 
-// What one GEMM step reads and writes in a given layer.
+// What one GEMM step reads and writes in a given layer.  The activations
+// of every step are bf16 [Mp][lda]: the attention output, the SwiGLU
+// product, or, for the steps behind an RMSNorm, bf16(x * g) of the residual
+// version x with that norm's gain g; the norm's per-row scale
+// 1 / sqrt(mean(x^2) + eps) is then applied to the step's output rows.
 struct StepIo {
   const bf16x8* w;   // packed matrix
   int ks;            // k-steps per n-block (K / 16)
-  bool norm;         // activations: RMSNorm(x) with gain, else bf16 a
+  bool norm;         // rows of the output are scaled by the norm's rstd
   const bf16* a;     // [Mp][lda]
   int lda;
-  const float* x;    // [Mp][d]
-  const float* ssq;  // [d/32][Mp]
-  const bf16* gain;  // [d]
+  const float* ssq;  // norm: [d/32][Mp] sums of squares of the residual version
   // epilogue
   bf16* q;           // QKV: [Mp][d] queries after the rotary embedding
   bf16* kc;          // QKV: K cache of this layer [H][cap][Dh]
@@ -211,6 +213,8 @@ struct StepIo {
   const float* x_in; // RESID: [Mp][d]
   float* x_out;      // RESID: [Mp][d]
   float* ssq_out;    // RESID: [d/32][Mp]
+  bf16* xg_out;      // RESID: [Mp][d] bf16(x_out * g_next)
+  const bf16* g_next;  // RESID: gain of the norm that reads x_out
   bf16* h;           // SWIGLU: [Mp][Fp]
 };
 
@@ -224,9 +228,9 @@ __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
   switch (step) {
     case STEP_QKV:
       io.norm = true;
-      io.x = p.x + (size_t)(2 * l) * xsz;
+      io.a = p.xg + (size_t)(2 * l) * xsz;
+      io.lda = p.d;
       io.ssq = p.ssq + (size_t)(2 * l) * ssz;
-      io.gain = (const bf16*)(lw + p.o_attn_norm);
       io.q = p.q + (size_t)l * p.Mp * p.d;
       io.kc = p.k_cache + (size_t)l * p.H * p.cap * p.Dh;
       io.vc = p.v_cache + (size_t)l * p.H * p.cap * p.Dh;
@@ -238,12 +242,14 @@ __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
       io.x_in = p.x + (size_t)(2 * l) * xsz;
       io.x_out = p.x + (size_t)(2 * l + 1) * xsz;
       io.ssq_out = p.ssq + (size_t)(2 * l + 1) * ssz;
+      io.xg_out = p.xg + (size_t)(2 * l + 1) * xsz;
+      io.g_next = (const bf16*)(lw + p.o_ffn_norm);
       break;
     case STEP_GATE_UP:
       io.norm = true;
-      io.x = p.x + (size_t)(2 * l + 1) * xsz;
+      io.a = p.xg + (size_t)(2 * l + 1) * xsz;
+      io.lda = p.d;
       io.ssq = p.ssq + (size_t)(2 * l + 1) * ssz;
-      io.gain = (const bf16*)(lw + p.o_ffn_norm);
       io.h = p.h + (size_t)l * p.Mp * p.Fp;
       break;
     case STEP_DOWN:
@@ -253,54 +259,37 @@ __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
       io.x_in = p.x + (size_t)(2 * l + 1) * xsz;
       io.x_out = p.x + (size_t)(2 * l + 2) * xsz;
       io.ssq_out = p.ssq + (size_t)(2 * l + 2) * ssz;
+      io.xg_out = p.xg + (size_t)(2 * l + 2) * xsz;
+      io.g_next = l + 1 < p.L ? (const bf16*)(lw + p.layer_bytes + p.o_attn_norm)
+                              : (const bf16*)(p.packed + p.o_final_norm);
       break;
     default:  // STEP_LM
       io.norm = true;
-      io.x = p.x + (size_t)(2 * p.L) * xsz;
+      io.a = p.xg + (size_t)(2 * p.L) * xsz;
+      io.lda = p.d;
       io.ssq = p.ssq + (size_t)(2 * p.L) * ssz;
-      io.gain = (const bf16*)(p.packed + p.o_final_norm);
       break;
   }
   return io;
 }
 
 // Copies the tile's activation slice (k-steps [k0, k0 + kt), all Mp rows)
-// into LDS in MFMA A-operand lane order.  bf16: unit (kk, mb) = 1 KiB at
+// into LDS in MFMA A-operand lane order: unit (kk, mb) = 1 KiB at
 // (kk MB + mb) KiB, lane l's 16 bytes = row 32 mb + l % 32, inputs
-// 16 (k0 + kk) + 8 (l / 32) .. + 7.  Norm (fp32 x): unit ((kk MB + mb) 2 + h)
-// holds inputs + 4 h .. + 3 of the same lane; then the gains, 32 bytes per
-// k-step (16 per lane half).  Rows >= n read zeros.  Waves take units in
-// turn; the caller waits for the loads.
+// 16 (k0 + kk) + 8 (l / 32) .. + 7.  Rows >= n read zeros.  Waves take units
+// in turn; the caller waits for the loads.
 template <int MB>
 __device__ __forceinline__ void stage_activations(KParams& p, const StepIo& io, int k0, int kt, char* A) {
   const int wave = wave_index(), lane = threadIdx.x & 63;
   const int lrow = lane & 31, khalf = lane >> 5;
   const char* zero = p.zero + lane * 16;
-  if (!io.norm) {
-    const int units = kt * MB;
-    for (int u = wave; u < units; u += kWaves) {
-      const int kk = u / MB, mb = u % MB;
-      const int r = 32 * mb + lrow;
-      const void* src = r < p.n ? (const void*)(io.a + (size_t)r * io.lda + 16 * (k0 + kk) + 8 * khalf)
-                                : (const void*)zero;
-      dma16(src, A + (size_t)u * 1024);
-    }
-  } else {
-    const int units = kt * MB * 2;
-    for (int u = wave; u < units; u += kWaves) {
-      const int kk = u / (2 * MB), mb = (u / 2) % MB, hh = u & 1;
-      const int r = 32 * mb + lrow;
-      const void* src = r < p.n
-                            ? (const void*)(io.x + (size_t)r * p.d + 16 * (k0 + kk) + 8 * khalf + 4 * hh)
-                            : (const void*)zero;
-      dma16(src, A + (size_t)u * 1024);
-    }
-    char* G = A + (size_t)kt * MB * 2048;
-    for (int j = wave; j * 32 < kt; j += kWaves) {
-      const int kk = 32 * j + (lane >> 1);
-      const void* src = kk < kt ? (const void*)(io.gain + 16 * (k0 + kk) + 8 * (lane & 1)) : (const void*)zero;
-      dma16(src, G + (size_t)j * 1024);
-    }
+  const int units = kt * MB;
+  for (int u = wave; u < units; u += kWaves) {
+    const int kk = u / MB, mb = u % MB;
+    const int r = 32 * mb + lrow;
+    const void* src = r < p.n ? (const void*)(io.a + (size_t)r * io.lda + 16 * (k0 + kk) + 8 * khalf)
+                              : (const void*)zero;
+    dma16(src, A + (size_t)u * 1024);
   }
 }
 
@@ -362,7 +351,7 @@ constexpr int tile_depth() {
 // weights and leaves the tile's sum in LDS at T = A:
 // fp32 [CW][MB][64 lanes][16] (MFMA accumulator order).  False if a wait
 // ran out.
-template <int MB, int CW, bool NORM>
+template <int MB, int CW>
 __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams& pin, int step, int layer,
                                                                        int nb0, int k0, int k1,
                                                                        int wait_phase, char* A,
@@ -401,16 +390,11 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
     trace_mark(sy, wait_phase, 1);
   }
   stage_activations<MB>(p, io, k0, kt, A);
-  if constexpr (NORM) row_scales<MB>(p, io, gl);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (wait_phase >= 0 && p.trace != nullptr && (int)blockIdx.x < kTraceWgs && threadIdx.x == 0)
     stg(p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 8 + wait_phase * 8 + 3, (long long)wall_clock64());
 
-  float rs[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) rs[mb] = NORM ? gl.rstd[32 * mb + (lane & 31)] : 1.0f;
-  const char* G = A + (size_t)kt * MB * 2048;
   f32x16 acc[MB][CW];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -423,21 +407,8 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
       if (i + u < ns) {
         const int kk = wave + kWaves * (i + u);
         bf16x8 a[MB];
-        if constexpr (NORM) {
-          const bf16x8 g = *(const bf16x8*)(G + kk * 32 + (lane >> 5) * 16);
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb) {
-            const char* base = A + (size_t)(kk * MB + mb) * 2048 + lane * 16;
-            const float4 x0 = *(const float4*)base;
-            const float4 x1 = *(const float4*)(base + 1024);
-            const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-#pragma unroll
-            for (int e = 0; e < 8; ++e) a[mb][e] = f2bf(xs[e] * rs[mb] * bf2f(g[e]));
-          }
-        } else {
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb) a[mb] = *(const bf16x8*)(A + (size_t)(kk * MB + mb) * 1024 + lane * 16);
-        }
+        for (int mb = 0; mb < MB; ++mb) a[mb] = *(const bf16x8*)(A + (size_t)(kk * MB + mb) * 1024 + lane * 16);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -479,12 +450,12 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   return true;
 }
 
-template <int MB, bool NORM, int CW>
+template <int MB, int CW>
 __device__ __forceinline__ bool tile_dispatch(int cw, KParams& p, int step, int layer, int nb0, int k0,
                                               int k1, int wait_phase, char* A, GemmLds& gl, int* flag) {
   if constexpr (CW >= 1) {
-    if (cw == CW) return tile_compute<MB, CW, NORM>(p, step, layer, nb0, k0, k1, wait_phase, A, gl, flag);
-    return tile_dispatch<MB, NORM, CW - 1>(cw, p, step, layer, nb0, k0, k1, wait_phase, A, gl, flag);
+    if (cw == CW) return tile_compute<MB, CW>(p, step, layer, nb0, k0, k1, wait_phase, A, gl, flag);
+    return tile_dispatch<MB, CW - 1>(cw, p, step, layer, nb0, k0, k1, wait_phase, A, gl, flag);
   } else {
     return false;
   }
@@ -510,6 +481,7 @@ struct EpiPre {
   static constexpr int U = (EPI == EPI_RESID || EPI == EPI_QKV) ? kEpiBatch : 1;
   float a[U][16];                       // RESID: x_in; QKV: cos
   float b[EPI == EPI_QKV ? U : 1][16];  // QKV: sin
+  float g[EPI == EPI_RESID ? U : 1];    // RESID: gain of the next norm at this lane's column
 };
 
 template <int MB, int EPI>
@@ -526,6 +498,7 @@ __device__ __forceinline__ void epilogue_preload(KParams& p, const StepIo& io, i
       const int nb = nb0 + c;
       if constexpr (EPI == EPI_RESID) {
         const int col = kNB * nb + j;
+        pre.g[uu] = bf2f(ldg(io.g_next + col));
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int r = 32 * mb + acc_row(i, lane);
@@ -572,6 +545,10 @@ __device__ __forceinline__ void epilogue(KParams& p, const StepIo& io, const flo
         v[4 * q + 3] = f.w;
       }
     }
+    if constexpr (EPI != EPI_RESID) {  // the norm's per-row scale
+#pragma unroll
+      for (int i = 0; i < 16; ++i) v[i] *= gl.rstd[32 * mb + acc_row(i, lane)];
+    }
     if constexpr (EPI == EPI_QKV) {
       const int d = p.d, dh = p.Dh;
       const int col = kNB * nb + j;
@@ -611,6 +588,9 @@ __device__ __forceinline__ void epilogue(KParams& p, const StepIo& io, const flo
         const int r = 32 * mb + acc_row(i, lane);
         const float xn = r < p.n ? pre.a[uu][i] + v[i] : 0.0f;
         if (r < p.n) st_coherent(io.x_out + (size_t)r * p.d + col, xn);
+        const float xg = xn * pre.g[uu];
+        const float xg1 = __shfl_down(xg, 1, kWave);
+        if (r < p.n && (j & 1) == 0) st_coherent_bf2(io.xg_out + (size_t)r * p.d + col, xg, xg1);
         float s = xn * xn;  // sum of squares over the n-block's 32 columns
         s += __shfl_xor(s, 16, kWave);
         s += __shfl_xor(s, 8, kWave);
@@ -797,6 +777,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool finish_tile(KParams& 
   }
   EpiPre<EPI> pre;
   if (finish) epilogue_preload<MB, EPI>(p, io, nb0, u_lo, u_hi, 0, pre);
+  if constexpr (EPI != EPI_RESID) {
+    if (finish) row_scales<MB>(p, io, gl);
+  }
   if (S > 1) {
     if (tr_phase >= 0) trace_mark(sy, tr_phase, 6);
     // Group counters are cleared when the pass ends: within a pass a step's
@@ -872,7 +855,6 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   const Sync sy = make_sync(p, lds_flag);
   const StepPlan& sp = p.step[step];
   const int S = sp.S, tiles = sp.groups * sp.S;
-  constexpr bool NORM = EPI != EPI_RESID;
   constexpr int CWM = kMaxCW / MB;
   // The barrier counts arrivals: it is exact only if every workgroup waits
   // at every phase before it arrives again, tile or no tile.
@@ -888,7 +870,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
     const int nb0 = g * sp.cw + (g < sp.n_hi ? g : sp.n_hi);
     const int cw = sp.cw + (g < sp.n_hi ? 1 : 0);
     const int k0 = (int)((long)s * sp.ksteps / S), k1 = (int)((long)(s + 1) * sp.ksteps / S);
-    if (!tile_dispatch<MB, NORM, CWM>(cw, p, step, layer, nb0, k0, k1, first ? phase : -1, A, gl, lds_flag))
+    if (!tile_dispatch<MB, CWM>(cw, p, step, layer, nb0, k0, k1, first ? phase : -1, A, gl, lds_flag))
       return false;
     if (first) trace_mark(sy, phase, 4);
     if (!finish_tile<MB, EPI>(p, step, layer, t, first ? phase : -1, A, gl, lds_flag)) return false;
@@ -1220,9 +1202,13 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
       st_coherent2(p.rope + ((size_t)m * (p.Dh / 2) + jj) * 2, cs, sn);
     }
     const bf16* row = E + (size_t)tree.tok[m] * p.d;
+    const bf16* g0 = (const bf16*)(p.packed + p.layer0 + p.o_attn_norm);
     for (int c = threadIdx.x; c < p.d; c += kThreads) {
       const float v = bf2f(ldg(row + c));
       st_coherent(&p.x[(size_t)m * p.d + c], v);
+      const float xg = v * bf2f(ldg(g0 + c));
+      const float xg1 = __shfl_down(xg, 1, kWave);
+      if ((c & 1) == 0) st_coherent_bf2(p.xg + (size_t)m * p.d + c, xg, xg1);
       float s = v * v;
       s += __shfl_xor(s, 16, kWave);
       s += __shfl_xor(s, 8, kWave);
