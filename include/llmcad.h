@@ -171,7 +171,7 @@ const char* llmcad_status_string(int status);
  * must be cleared with llmcad_workspace_init before the next pass; 3 = the
  * kernel did not find its parameter block where it reads it, and did
  * nothing),
- * 6 phase timestamps int64 [8][2 + 5L][8] (written when the environment
+ * 6 phase timestamps int64 [8][3 + 5L][8] (written when the environment
  * variable LLMCAD_TRACE is 1), 7 every residual stream version fp32
  * [2L+1][Mp][d], 8 their per-32-column sums of squares fp32 [2L+1][d/32][Mp],
  * 9 every layer's queries bf16 [L][Mp][d], 10 attention outputs bf16

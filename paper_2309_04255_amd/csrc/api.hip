@@ -128,14 +128,12 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   const PackedLayout P(s);
   const int G = pass_grid();
   const WorkspaceLayout W(s, a.n, G);
-  const int MB = W.Mp / 32;
+  const int MB = W.Mp / 16;
   const int occ = pass_occupancy(MB, s.Dh);
   if (device_info().cus <= 0 || occ * device_info().cus < G) {
     g_last_error = hipErrorInvalidConfiguration;
     return LLMCAD_EHIP;
   }
-  const PassPlans plans(s, MB, G);
-  if (!plans.ok()) return LLMCAD_ESHAPE;
   char* ws = a.ws;
 
   PassParams p;
@@ -168,17 +166,11 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   const long long w_off[kSteps] = {(long long)P.w_qkv, (long long)P.w_o, (long long)P.w_gate_up,
                                    (long long)P.w_down, (long long)P.lm_head};
   for (int i = 0; i < kSteps; ++i) {
-    const GemmPlan& g = plans.g[i];
     StepPlan& sp = p.step[i];
-    sp.S = g.S;
-    sp.groups = g.groups;
-    sp.cw = g.cw;
-    sp.n_hi = g.n_hi;
-    sp.nblocks = g.nblocks;
-    sp.ksteps = g.ksteps;
+    sp.nblocks = step_blocks(s, i);
+    sp.ksteps = step_ksteps(s, i);
     sp.w_off = w_off[i];
     sp.layer_rel = i == STEP_LM ? 0 : 1;
-    sp.group_cnt = (int*)(ws + W.group_counters(i));
   }
   p.k_cache = (bf16*)a.k_cache;
   p.v_cache = (bf16*)a.v_cache;
@@ -188,10 +180,10 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.x = (float*)(ws + W.xs);
   p.xg = (bf16*)(ws + W.xgs);
   p.ssq = (float*)(ws + W.ssqs);
+  p.ssq_regs = W.Mp <= 32 && cdiv(s.d_nb, 1024 / W.Mp) <= 8 ? 1 : 0;
   p.q = (bf16*)(ws + W.qs);
   p.o = (bf16*)(ws + W.os);
   p.h = (bf16*)(ws + W.hs);
-  p.part = (float*)(ws + W.part);
   p.attn_o = (float*)(ws + W.attn_o);
   p.attn_ml = (float*)(ws + W.attn_ml);
   // Position splits per head: enough (head, split) units for the grid, at
@@ -203,8 +195,6 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   if (s.H * S > G) S = G / s.H;
   if (S < 1) S = 1;
   p.attn_splits = S;
-  p.group_cnt_all = (int*)(ws + W.counters);
-  p.n_group_cnt = W.n_group_counters;
   p.head_cnt = (int*)(ws + W.head_counters());
   p.lm_cnt = (int*)(ws + W.lm_cnt());
   p.exit_cnt = (int*)(ws + W.exit_cnt());
@@ -458,7 +448,7 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
     case 3: *offset = W.hs; *bytes = (size_t)W.Mp * s.Fp * 2; break;
     case 4: *offset = W.amax; *bytes = (size_t)W.Mp * 4; break;
     case 5: *offset = W.status(); *bytes = 4; break;
-    case 6: *offset = W.trace; *bytes = (size_t)8 * (2 + 5 * s.L) * 8 * 8; break;
+    case 6: *offset = W.trace; *bytes = (size_t)8 * pass_phases(s.L) * 8 * 8; break;
     case 7: *offset = W.xs; *bytes = (size_t)(2 * s.L + 1) * W.Mp * s.d * 4; break;
     case 8: *offset = W.ssqs; *bytes = (size_t)(2 * s.L + 1) * s.d_nb * W.Mp * 4; break;
     case 9: *offset = W.qs; *bytes = (size_t)s.L * W.Mp * s.d * 2; break;

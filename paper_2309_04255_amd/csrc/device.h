@@ -45,9 +45,11 @@ __device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_rea
 #if defined(__HIP_DEVICE_COMPILE__)
 #define LLMCAD_GLOBAL __attribute__((address_space(1)))
 #define LLMCAD_CONSTANT __attribute__((address_space(4)))
+#define LLMCAD_LDS __attribute__((address_space(3)))
 #else
 #define LLMCAD_GLOBAL
 #define LLMCAD_CONSTANT
+#define LLMCAD_LDS
 #endif
 template <class T>
 __device__ __forceinline__ T ldg(const T* p) {
@@ -56,6 +58,16 @@ __device__ __forceinline__ T ldg(const T* p) {
 template <class T>
 __device__ __forceinline__ void stg(T* p, const T& v) {
   *(LLMCAD_GLOBAL T*)p = v;
+}
+// LDS access through a pointer the compiler cannot trace to a __shared__
+// object (a generic access would be FLAT, counted with global loads).
+template <class T>
+__device__ __forceinline__ T lds_ld(const void* p) {
+  return *(const LLMCAD_LDS T*)p;
+}
+template <class T>
+__device__ __forceinline__ void lds_st(void* p, const T& v) {
+  *(LLMCAD_LDS T*)p = v;
 }
 
 __device__ __forceinline__ float bf2f(bf16 x) { return (float)x; }

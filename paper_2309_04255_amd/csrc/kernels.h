@@ -27,13 +27,11 @@ struct TreeArgs {
 // the parameters in place.
 constexpr int kPassMagic = 0x4c4d4342;
 
-// One GEMM step's tiling (see GemmPlan) and where its weights live.
+// One GEMM step's shape and where its weights live.
 struct StepPlan {
-  int S, groups, cw, n_hi;
-  int nblocks, ksteps;
-  long long w_off;     // packed matrix: offset from the packed image (globals) or the layer start
-  int layer_rel;       // 1 if w_off is relative to the layer's start
-  int* group_cnt;      // [nblocks] arrival counters of the groups
+  int nblocks, ksteps;  // 16-column blocks, 32-input k-steps
+  long long w_off;      // packed matrix: offset from the packed image (globals) or the layer start
+  int layer_rel;        // 1 if w_off is relative to the layer's start
 };
 
 // Must stay the first kernel argument of the pass kernel.
@@ -58,23 +56,22 @@ struct PassParams {
   const char* zero; // kZeroBytes of zeros
   float* rope;      // [Mp][Dh/2][2] cos, sin of every node's rotary angles
   float* x;         // [2L+1][Mp][d]
-  bf16* xg;         // [2L+1][Mp][d] bf16(x * g), g the gain of the norm that reads x
-  float* ssq;       // [2L+1][d/32][Mp]
+  bf16* xg;         // [2L+1] x fragment-order [Mp][d]: bf16(x * g), g the gain of the norm that reads x
+  float* ssq;       // [2L+1][d/16][Mp]
+  int ssq_regs;     // 1 if a norm step's tiles hold its sums of squares in registers
+                    // (Mp <= 32 and at most 8 blocks per chunk of d/16 / (1024 / Mp) blocks)
   bf16* q;          // [L][Mp][d]   queries after the rotary embedding
-  bf16* o;          // [L][Mp][d]
-  bf16* h;          // [L][Mp][Fp]
-  float* part;      // split-K partial tiles
+  bf16* o;          // [L] x fragment-order [Mp][d]
+  bf16* h;          // [L] x fragment-order [Mp][Fp]
   float* attn_o;    // [H][S][Mp][Dh]
   float* attn_ml;   // [H][S][Mp][2]
   int attn_splits;
-  int* group_cnt_all;  // every step's group counters (cleared when the pass ends)
-  int n_group_cnt;
   int* head_cnt;
   int* lm_cnt;
   int* exit_cnt;
   int* status;
   int* bar;         // [kBarSlots][kBarStride]
-  float* lm_val;    // [LM argmax slots][Mp]
+  float* lm_val;    // [G][Mp] LM-head argmax per workgroup
   int* lm_idx;
   int* amax;        // [Mp]
   // outputs
@@ -88,8 +85,10 @@ struct PassParams {
   long long* trace;  // diagnostics: [8][2 + 5L][8] phase timestamps, or null
 };
 
-hipError_t launch_pass(int mb32, const PassParams& p, const TreeArgs& tree, hipStream_t st);
-int pass_occupancy(int mb32, int dh);  // resident workgroups per CU (0 if unavailable)
-size_t pass_lds_bytes(int mb32, int dh);
+// mb16: 16-row blocks of the pass (Mp / 16: 1, 2, 4 or 8).
+hipError_t launch_pass(int mb16, const PassParams& p, const TreeArgs& tree, hipStream_t st);
+int pass_occupancy(int mb16, int dh);  // resident workgroups per CU (0 if unavailable)
+size_t pass_lds_bytes(int mb16, int dh);
+
 
 }  // namespace llmcad

@@ -1,25 +1,24 @@
 // One-time re-layout of plain W[out][in] matrices into MFMA-fragment order.
 //
-// Packed image of a matrix with `nblocks` 32-column n-blocks and `ksteps`
-// 16-wide k-steps: n-block-major, block (nb, s) is 1 KiB at
+// Packed image of a matrix with `nblocks` 16-column blocks and `ksteps`
+// 32-wide k-steps: block-major, block (nb, s) is 1 KiB at
 // ((nb * ksteps + s) * 1 KiB), and lane l's 16 bytes hold
-// W[col(32 nb + l % 32)][16 s + 8 (l / 32) + e], e = 0..7 — exactly the B
-// operand of one 32x32x16 MFMA.  A wave streams an n-block's weights with
-// one contiguous 1 KiB load per k-step, and consecutive k-steps are
-// consecutive KiBs.  Columns beyond the matrix and inputs beyond K are zero.
+// W[col(16 nb + l % 16)][32 s + 8 (l / 16) + e], e = 0..7 -- exactly the B
+// operand of one 16x16x32 MFMA.  A wave streams a block's weights with one
+// contiguous 1 KiB load per k-step, and consecutive k-steps are consecutive
+// KiBs.  Columns beyond the matrix and inputs beyond K are zero.
 //
 // Column orders:
 //  PACK_PLAIN     packed column c is output row c.
-//  PACK_GATE_UP   n-block i holds gate rows [16i, 16i+16) then up rows
-//                 [16i, 16i+16), so the SwiGLU product of 16 columns is
-//                 formed inside one n-block; F is padded to a multiple of 16
-//                 with zeros.
+//  PACK_GATE_UP   block i holds gate rows [8i, 8i+8) then up rows [8i, 8i+8),
+//                 so the SwiGLU product of 8 columns is formed inside one
+//                 block; F is padded to a multiple of 32 with zeros.
 //  PACK_QKV_ROPE  the fused [q; k; v] projection (N = 3d rows).  In the q and
-//                 k parts, n-block t of a head (Dh / 32 per head) holds that
-//                 head's dims [16t, 16t+16) then [16t + Dh/2, 16t + Dh/2 + 16):
-//                 the pairs the rotary embedding mixes (rotate-half pairing,
-//                 dim j with j + Dh/2) sit 16 columns apart inside one
-//                 n-block.  The v part is plain.
+//                 k parts, block t of a head (Dh / 16 per head) holds that
+//                 head's dims [8t, 8t+8) then [8t + Dh/2, 8t + Dh/2 + 8): the
+//                 pairs the rotary embedding mixes (rotate-half pairing, dim j
+//                 with j + Dh/2) sit 8 columns apart inside one block.  The v
+//                 part is plain.
 #include "device.h"
 #include "kernels.h"
 #include "layout.h"
@@ -33,13 +32,13 @@ __device__ __forceinline__ int packed_col_to_row(int c, int N, int kind, int aux
     if (c >= 2 * d) return c < N ? c : -1;
     const int part = c / d, cq = c % d, head = cq / dh, w = cq % dh;
     const int t = w / kNB, ci = w % kNB;
-    return part * d + head * dh + 16 * t + (ci % 16) + (ci < 16 ? 0 : dh / 2);
+    return part * d + head * dh + 8 * t + (ci % 8) + (ci < 8 ? 0 : dh / 2);
   }
   const int F = aux;
   const int nb = c / kNB, cc = c % kNB;
-  const int f = 16 * nb + (cc % 16);
+  const int f = 8 * nb + (cc % 8);
   if (f >= F) return -1;
-  return cc < 16 ? f : F + f;
+  return cc < 8 ? f : F + f;
 }
 
 __global__ void pack_kernel(const bf16* __restrict__ w, int N, int K, bf16x8* __restrict__ out,
@@ -50,8 +49,8 @@ __global__ void pack_kernel(const bf16* __restrict__ w, int N, int K, bf16x8* __
     const long blk = ch / 64;  // nb * ksteps + s
     const int s = (int)(blk % ksteps);
     const int nb = (int)(blk / ksteps);
-    const int row = packed_col_to_row(kNB * nb + lane % 32, N, kind, aux);
-    const int k0 = kStepK * s + 8 * (lane / 32);
+    const int row = packed_col_to_row(kNB * nb + lane % 16, N, kind, aux);
+    const int k0 = kStepK * s + 8 * (lane / 16);
     bf16x8 v;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {

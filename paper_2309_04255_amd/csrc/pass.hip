@@ -10,32 +10,35 @@
 // next tile before it waits at the barrier, and HBM keeps streaming
 // meanwhile.
 //
-// Phases: embed + tree prep; per layer QKV projection (RMSNorm applied to
-// the staged activations; rotary embedding and K/V cache write in the
-// epilogue) -> tree attention (ancestor mask) -> O projection (+residual) ->
-// gate/up (RMSNorm; SwiGLU epilogue) -> down projection (+residual); then
-// final RMSNorm + LM head + argmax, and the accept walk in the workgroup that
+// Phases: embed + tree prep; per layer QKV projection (RMSNorm scale,
+// rotary embedding and K/V cache write in the epilogue) -> tree attention
+// (ancestor mask) -> O projection (+residual) -> gate/up (RMSNorm scale;
+// SwiGLU epilogue) -> down projection (+residual); then the LM head (final
+// RMSNorm scale) + argmax, and the accept walk in the workgroup that
 // completes the argmax.
 //
 // GEMM phases (activations X [Mp rows x K], packed weights W [N x K]): the
-// host cuts every step into tiles (GemmPlan): a tile is a group of up to 16
-// consecutive 32-column n-blocks times a slice of the k-steps.  A tile's
-// activation slice is copied once into LDS with direct global->LDS loads, in
-// exactly the lane order of the 32x32x16 MFMA A operand, while the weights
-// stream from HBM through a register pipeline (non-temporal loads); the
-// activations are never re-read from L2 per n-block.  The four waves take
-// interleaved k-steps and their partial tiles are added in LDS in wave
-// order.  When a group's k-steps are split over S tiles, each tile stores its
-// partial sum and the workgroup that completes the group last adds the S
-// partials in slice order (bit-reproducible) and runs the epilogue.
+// 16-column blocks of a step are dealt out in contiguous runs, one run per
+// workgroup, and every block is computed over the full K by one workgroup,
+// so no partial sum ever leaves the CU: the epilogue follows the main loop
+// directly.  The four waves take interleaved 32-wide k-steps; per k-step a
+// wave loads one 1 KiB weight fragment per block (non-temporal: weights are
+// read once) and one 1 KiB activation fragment per 16-row block -- the
+// activations are stored in MFMA fragment order by the phase that produces
+// them, so that read is one contiguous 1 KiB load that every CU of an XCD
+// shares through L2.  Both streams run through one register pipeline.  The
+// waves' partial tiles meet in LDS and are added in wave order
+// (bit-reproducible).  Inputs of the epilogue that do not depend on the
+// tile (the residual stream, rotary table, norm gains, sums of squares) are
+// copied into LDS by direct global->LDS loads issued before the main loop.
 //
 // Coherence without cache maintenance: every buffer handed from one phase to
 // the next is written once per pass at its own address with device-coherent
 // stores and read after the barrier with ordinary loads, so no L2 can hold an
-// older copy; buffers reused within a pass (partials) are read with
-// device-coherent loads.  Barriers and per-head joins are counters polled
-// with bounded spins: a wait that exceeds its bound records an error status
-// and the workgroup leaves the pass, so no wave can hang.
+// older copy; buffers reused within a pass (attention partials) are read
+// with device-coherent loads.  Barriers and per-head joins are counters
+// polled with bounded spins: a wait that exceeds its bound records an error
+// status and the workgroup leaves the pass, so no wave can hang.
 #include <math.h>
 
 #include "device.h"
@@ -49,19 +52,8 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 constexpr int kTraceWgs = 8;  // workgroups that record phase timestamps
-
-// D = A(32x16) * B(16x32) + C on the matrix cores, bf16 inputs, fp32
-// accumulate.  Lane l holds A row l % 32 and B column l % 32, k-slots
-// 8 (l / 32) .. + 7 of both; D element i of lane l is row
-// 8 (i / 4) + 4 (l / 32) + i % 4, column l % 32.
-__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-__device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 
 // The launch parameters, read in place from the kernel-argument segment
 // (constant memory): loads through a wave-uniform address of it are scalar
@@ -81,11 +73,24 @@ __device__ __forceinline__ bf16x8 ldg_nt(const bf16x8* p) {
   return __builtin_nontemporal_load((const LLMCAD_GLOBAL bf16x8*)p);
 }
 
-// Direct global -> LDS copy of 16 bytes per lane: lane l's bytes land at
-// lds + 16 l.  `lds` must be the same in every lane.
-__device__ __forceinline__ void dma16(const void* src, char* lds) {
-  __builtin_amdgcn_global_load_lds((const LLMCAD_GLOBAL void*)src,
-                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+// The pointer as a value the compiler cannot see through: a load from a
+// pointer chosen by a condition stays one unconditional load (the compiler
+// would otherwise turn the choice into a branch around the load, and a load
+// that may or may not have been issued makes every later wait a full drain).
+template <class T>
+__device__ __forceinline__ const T* opaque(const T* p) {
+  asm volatile("" : "+v"(p));
+  return p;
+}
+
+// Element offset of (row, col) in a fragment-order bf16 [Mp][K] matrix with
+// MB 16-row blocks: block (col / 32, row / 16) is 1 KiB at
+// ((col / 32) MB + row / 16) KiB, and holds row 16 rb + l % 16, columns
+// 32 s + 8 (l / 16) + e at lane l, element e -- the A operand of one
+// 16x16x32 MFMA.
+__device__ __forceinline__ size_t frag_off(int row, int col, int MB) {
+  return ((size_t)((col >> 5) * MB + (row >> 4)) * 64 + (row & 15) + 16 * ((col >> 3) & 3)) * 8 +
+         (col & 7);
 }
 
 // ------------------------------------------------------------------ sync
@@ -105,15 +110,15 @@ __device__ __forceinline__ Sync make_sync(KParams& p, int* lds_flag) {
   s.limit = p.spin_limit;
   s.lds_flag = lds_flag;
   s.trace = p.trace != nullptr && (int)blockIdx.x < kTraceWgs
-                ? p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 8
+                ? p.trace + (size_t)blockIdx.x * pass_phases(p.L) * 8
                 : nullptr;
   return s;
 }
 
 // Diagnostics: wall-clock (100 MHz) marks per phase: 0 = barrier wait
 // entered, 1 = wait over, 2 = phase work done; GEMM phases also mark 3 =
-// activations staged, 4 = weight streaming done, 5 = epilogue done, 6 =
-// group hand-off done, 7 = partials added (group's last workgroup).
+// activation stream started, 4 = first tile's main loop done, 5 = all tiles
+// and epilogues done.
 __device__ __forceinline__ void trace_mark(const Sync& s, int phase, int k) {
   if (s.trace != nullptr && threadIdx.x == 0) stg(s.trace + phase * 8 + k, (long long)wall_clock64());
 }
@@ -182,10 +187,12 @@ __device__ __forceinline__ bool wait_at_least(const Sync& s, const int* c, int t
 // ------------------------------------------------------------------ GEMM
 
 struct GemmLds {
-  float rstd[kMaxNodes];          // RMSNorm scale per row of the current tile
-  float part_ss[256];             // their partial sums
-  float red_v[kMaxNodes][kMaxCW]; // LM head: argmax per (row, n-block)
-  int red_i[kMaxNodes][kMaxCW];
+  float rstd[kMaxNodes];        // RMSNorm scale per row
+  float part_ss[1024];          // its partial sums
+  float red_v[kMaxNodes][8];    // LM head: argmax per (row, block of the tile)
+  int red_i[kMaxNodes][8];
+  float best_v[kMaxNodes];      // LM head: argmax per row over this workgroup's blocks
+  int best_i[kMaxNodes];
   int reach[kMaxNodes];
   int amax[kMaxNodes];
   int tok[kMaxNodes];  // accept walk: the tree, staged from the workspace
@@ -194,28 +201,37 @@ struct GemmLds {
   int walk_len;
 };
 
-// What one GEMM step reads and writes in a given layer.  The activations
-// of every step are bf16 [Mp][lda]: the attention output, the SwiGLU
-// product, or, for the steps behind an RMSNorm, bf16(x * g) of the residual
-// version x with that norm's gain g; the norm's per-row scale
+// LDS of a GEMM phase (dynamic shared memory):
+//   [0, 64 KiB)        the waves' partial tiles, fp32 [4][cw][MB][64 lanes][4]
+//   [64, 88 KiB)       epilogue inputs: per (block, row block) 1 KiB of the
+//                      residual stream (fp32 [16 rows][16]) or of the rotary
+//                      table (fp32 [16 rows][8 pairs][2]); then per block
+//                      1 KiB holding its 16 norm gains (bf16, first 32 bytes)
+constexpr int kTwOff = 0;
+constexpr int kEpiOff = 64 * 1024;
+constexpr int kGemmLdsBytes = 88 * 1024;
+
+// What one GEMM step reads and writes in a given layer.  The activations of
+// every step are fragment-order bf16 [Mp][K]: the attention output, the
+// SwiGLU product, or, for the steps behind an RMSNorm, bf16(x * g) of the
+// residual version x with that norm's gain g; the norm's per-row scale
 // 1 / sqrt(mean(x^2) + eps) is then applied to the step's output rows.
 struct StepIo {
   const bf16x8* w;   // packed matrix
-  int ks;            // k-steps per n-block (K / 16)
+  int ks;            // k-steps (K / 32)
   bool norm;         // rows of the output are scaled by the norm's rstd
-  const bf16* a;     // [Mp][lda]
-  int lda;
-  const float* ssq;  // norm: [d/32][Mp] sums of squares of the residual version
+  const bf16x8* a;   // fragment-order activations
+  const float* ssq;  // norm: [d/16][Mp] sums of squares of the residual version
   // epilogue
   bf16* q;           // QKV: [Mp][d] queries after the rotary embedding
   bf16* kc;          // QKV: K cache of this layer [H][cap][Dh]
   bf16* vc;          // QKV: V cache of this layer [H][cap][Dh]
   const float* x_in; // RESID: [Mp][d]
   float* x_out;      // RESID: [Mp][d]
-  float* ssq_out;    // RESID: [d/32][Mp]
-  bf16* xg_out;      // RESID: [Mp][d] bf16(x_out * g_next)
+  float* ssq_out;    // RESID: [d/16][Mp]
+  bf16* xg_out;      // RESID: fragment-order bf16(x_out * g_next)
   const bf16* g_next;  // RESID: gain of the norm that reads x_out
-  bf16* h;           // SWIGLU: [Mp][Fp]
+  bf16* h;           // SWIGLU: fragment-order [Mp][Fp]
 };
 
 __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
@@ -228,8 +244,7 @@ __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
   switch (step) {
     case STEP_QKV:
       io.norm = true;
-      io.a = p.xg + (size_t)(2 * l) * xsz;
-      io.lda = p.d;
+      io.a = (const bf16x8*)(p.xg + (size_t)(2 * l) * xsz);
       io.ssq = p.ssq + (size_t)(2 * l) * ssz;
       io.q = p.q + (size_t)l * p.Mp * p.d;
       io.kc = p.k_cache + (size_t)l * p.H * p.cap * p.Dh;
@@ -237,8 +252,7 @@ __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
       break;
     case STEP_O:
       io.norm = false;
-      io.a = p.o + (size_t)l * p.Mp * p.d;
-      io.lda = p.d;
+      io.a = (const bf16x8*)(p.o + (size_t)l * xsz);
       io.x_in = p.x + (size_t)(2 * l) * xsz;
       io.x_out = p.x + (size_t)(2 * l + 1) * xsz;
       io.ssq_out = p.ssq + (size_t)(2 * l + 1) * ssz;
@@ -247,15 +261,13 @@ __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
       break;
     case STEP_GATE_UP:
       io.norm = true;
-      io.a = p.xg + (size_t)(2 * l + 1) * xsz;
-      io.lda = p.d;
+      io.a = (const bf16x8*)(p.xg + (size_t)(2 * l + 1) * xsz);
       io.ssq = p.ssq + (size_t)(2 * l + 1) * ssz;
       io.h = p.h + (size_t)l * p.Mp * p.Fp;
       break;
     case STEP_DOWN:
       io.norm = false;
-      io.a = p.h + (size_t)l * p.Mp * p.Fp;
-      io.lda = p.Fp;
+      io.a = (const bf16x8*)(p.h + (size_t)l * p.Mp * p.Fp);
       io.x_in = p.x + (size_t)(2 * l + 1) * xsz;
       io.x_out = p.x + (size_t)(2 * l + 2) * xsz;
       io.ssq_out = p.ssq + (size_t)(2 * l + 2) * ssz;
@@ -265,67 +277,255 @@ __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
       break;
     default:  // STEP_LM
       io.norm = true;
-      io.a = p.xg + (size_t)(2 * p.L) * xsz;
-      io.lda = p.d;
+      io.a = (const bf16x8*)(p.xg + (size_t)(2 * p.L) * xsz);
       io.ssq = p.ssq + (size_t)(2 * p.L) * ssz;
       break;
   }
   return io;
 }
 
-// Copies the tile's activation slice (k-steps [k0, k0 + kt), all Mp rows)
-// into LDS in MFMA A-operand lane order: unit (kk, mb) = 1 KiB at
-// (kk MB + mb) KiB, lane l's 16 bytes = row 32 mb + l % 32, inputs
-// 16 (k0 + kk) + 8 (l / 32) .. + 7.  Rows >= n read zeros.  Waves take units
-// in turn; the caller waits for the loads.
-template <int MB>
-__device__ __forceinline__ void stage_activations(KParams& p, const StepIo& io, int k0, int kt, char* A) {
+// What a tile's main loop reads, with every field assigned for every step
+// (branch-free selects: the compiler keeps this in registers).
+struct TileIn {
+  const bf16x8* w;     // packed matrix
+  const bf16x8* a;     // fragment-order activations
+  const float* ssq;    // norm steps: [d/16][Mp] sums of squares; else null
+  const float* x_in;   // residual steps: [Mp][d]; else null
+  const bf16* g_next;  // residual steps: gain of the next norm; else null
+  int ks;
+  bool norm, resid;
+};
+
+__device__ __forceinline__ TileIn tile_in(KParams& p, int step, int l) {
+  const size_t xsz = (size_t)p.Mp * p.d, ssz = (size_t)p.d_nb * p.Mp;
+  const char* lw = p.packed + p.layer0 + (long long)l * p.layer_bytes;
+  const StepPlan& sp = p.step[step];
+  TileIn t;
+  t.w = (const bf16x8*)((sp.layer_rel ? lw : p.packed) + sp.w_off);
+  t.ks = sp.ksteps;
+  t.resid = step == STEP_O || step == STEP_DOWN;
+  t.norm = !t.resid;
+  // x version read by a norm step: QKV 2l, GU 2l+1, LM 2L; residual input: O 2l, DOWN 2l+1
+  const int ver = step == STEP_LM ? 2 * p.L : (step == STEP_GATE_UP || step == STEP_DOWN) ? 2 * l + 1 : 2 * l;
+  const bf16* act = step == STEP_O ? p.o + (size_t)l * xsz
+                  : step == STEP_DOWN ? p.h + (size_t)l * p.Mp * p.Fp
+                                      : p.xg + (size_t)ver * xsz;
+  t.a = (const bf16x8*)act;
+  t.ssq = t.norm ? p.ssq + (size_t)ver * ssz : nullptr;
+  t.x_in = t.resid ? p.x + (size_t)ver * xsz : nullptr;
+  const bf16* g_o = (const bf16*)(lw + p.o_ffn_norm);
+  const bf16* g_d = l + 1 < p.L ? (const bf16*)(lw + p.layer_bytes + p.o_attn_norm)
+                                : (const bf16*)(p.packed + p.o_final_norm);
+  t.g_next = step == STEP_O ? g_o : step == STEP_DOWN ? g_d : nullptr;
+  return t;
+}
+
+// Weight (and activation) stages per wave: about 160 VGPRs.
+template <int MB, int C>
+constexpr int tile_depth() {
+  constexpr int d = 40 / (C + MB);
+  return d < 2 ? 2 : (d > 16 ? 16 : d);
+}
+
+// One tile: blocks [nb0, nb0 + C) of a step over all its k-steps.  Issues
+// the first weight stages, then (wait_phase >= 0) waits at the grid barrier
+// for the step's inputs, starts the activation stream and the epilogue
+// inputs, streams both through the MFMAs and leaves the waves' partial tiles
+// in LDS.  False if a wait ran out.
+template <int MB, int C>
+__device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams& pin, int step, int layer,
+                                                                       int nb0, int wait_phase, char* lds,
+                                                                       GemmLds& gl, int* lds_flag) {
+  KParams& p = uniform_params(pin);
+  step = wave_uniform(step);
+  layer = wave_uniform(layer);
+  nb0 = wave_uniform(nb0);
+  wait_phase = wave_uniform(wait_phase);
+  const TileIn io = tile_in(p, step, layer);
   const int wave = wave_index(), lane = threadIdx.x & 63;
-  const int lrow = lane & 31, khalf = lane >> 5;
-  const char* zero = p.zero + lane * 16;
-  const int units = kt * MB;
-  for (int u = wave; u < units; u += kWaves) {
-    const int kk = u / MB, mb = u % MB;
-    const int r = 32 * mb + lrow;
-    const void* src = r < p.n ? (const void*)(io.a + (size_t)r * io.lda + 16 * (k0 + kk) + 8 * khalf)
-                              : (const void*)zero;
-    dma16(src, A + (size_t)u * 1024);
+  const int ks = io.ks;
+  const int ns = wave_uniform(wave < ks ? (ks - wave + kWaves - 1) / kWaves : 0);
+  constexpr int D = tile_depth<MB, C>();
+  // this wave's k-steps: wave + 4 i
+  const bf16x8* wt = io.w + ((size_t)nb0 * ks + wave) * 64 + lane;
+  const size_t cstride = (size_t)ks * 64;
+  const bf16x8* at = io.a + (size_t)wave * MB * 64 + lane;
+  // Loads past the wave's last k-step read a line of zeros instead (the
+  // load is still issued, so that the compiler's count of loads in flight
+  // stays exact and every wait in the loop is for one stage only).  For the
+  // same reason every load of a tile is unconditional: inputs a step does
+  // not have are read from the zero line too.
+  const bf16x8* zero = (const bf16x8*)p.zero + lane;
+  const f32x4* zero4 = (const f32x4*)p.zero + lane;
+  bf16x8 bw[D][C];
+  bf16x8 ba[D][MB];
+  auto load_w = [&](int slot, int i) {
+    const bool live = i < ns;
+#pragma unroll
+    for (int c = 0; c < C; ++c) bw[slot][c] = ldg_nt(opaque(live ? wt + c * cstride + (size_t)(kWaves * i) * 64 : zero));
+  };
+  auto load_a = [&](int slot, int i) {
+    const bool live = i < ns;
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) ba[slot][rb] = ldg(opaque(live ? at + ((size_t)kWaves * i * MB + rb) * 64 : zero));
+  };
+
+  // Epilogue inputs that do not depend on this phase's barrier (the residual
+  // stream and rotary table were written two or more phases ago; gains are
+  // weights): per (block, row block) unit 16 B per lane, plus each block's
+  // gains.  Loaded first, parked in LDS once they land.
+  constexpr int KU = (C * MB + kWaves - 1) / kWaves;
+  constexpr int KG = (C + kWaves - 1) / kWaves;
+  const bool resid = io.resid;
+  f32x4 sx[KU], sg[KG];
+#pragma unroll
+  for (int k = 0; k < KU; ++k) {
+    const int u = wave + kWaves * k, c = u / MB, rb = u % MB;
+    const int col0 = kNB * (nb0 + c);
+    const f32x4* src = zero4;
+    if (u < C * MB) {
+      if (resid) {  // residual rows 16 rb + l / 4, columns col0 + 4 (l % 4) .. + 3
+        src = (const f32x4*)(io.x_in + (size_t)(16 * rb + (lane >> 2)) * p.d + col0 + 4 * (lane & 3));
+      } else if (step == STEP_QKV && col0 < 2 * p.d) {  // (cos, sin) of pairs 8 t + 2 (l % 4), + 1
+        const int t = (col0 % p.d % p.Dh) / kNB;
+        src = (const f32x4*)(p.rope + ((size_t)(16 * rb + (lane >> 2)) * (p.Dh / 2) + 8 * t + 2 * (lane & 3)) * 2);
+      }
+    }
+    sx[k] = ldg(opaque(src));
+  }
+#pragma unroll
+  for (int k = 0; k < KG; ++k) {
+    const int c = wave + kWaves * k;
+    sg[k] = ldg(opaque(resid && c < C ? (const f32x4*)(io.g_next + kNB * (nb0 + c) + 8 * (lane & 1)) : zero4));
+  }
+#pragma unroll
+  for (int u = 0; u < D; ++u) load_w(u, u);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int k = 0; k < KU; ++k) {
+    const int u = wave + kWaves * k;
+    if (u < C * MB) lds_st<f32x4>(lds + kEpiOff + (size_t)u * 1024 + lane * 16, sx[k]);
+  }
+#pragma unroll
+  for (int k = 0; k < KG; ++k) {
+    const int c = wave + kWaves * k;
+    if (c < C) lds_st<f32x4>(lds + kEpiOff + (size_t)(C * MB + c) * 1024 + lane * 16, sg[k]);
+  }
+  if (wait_phase >= 0) {
+    const Sync sy = make_sync(p, lds_flag);
+    trace_mark(sy, wait_phase, 0);
+    if (!grid_wait(sy, wait_phase, p.G)) return false;
+    trace_mark(sy, wait_phase, 1);
+  }
+  // A norm step's sums of squares (written by the previous phase), held in
+  // registers through the main loop: thread t takes rows 4 q .. 4 q + 3
+  // (q = t % (Mp / 4)) of the 16-column blocks of chunk t / (Mp / 4).
+  constexpr bool SSQR = MB <= 2;
+  constexpr int SSQN = SSQR ? 8 : 1;
+  f32x4 sr[SSQN];
+  if constexpr (SSQR) {
+    constexpr int QUADS = 4 * MB, CH = 256 / QUADS;
+    const int q = threadIdx.x % QUADS, ch = threadIdx.x / QUADS;
+    const int t0 = ch * p.d_nb / CH, t1 = (ch + 1) * p.d_nb / CH;
+    const bool on = io.norm && p.ssq_regs;
+#pragma unroll
+    for (int k = 0; k < SSQN; ++k)
+      sr[k] = ldg(opaque(on && t0 + k < t1 ? (const f32x4*)(io.ssq + (size_t)(t0 + k) * (16 * MB) + 4 * q) : zero4));
+  }
+#pragma unroll
+  for (int u = 0; u < D; ++u) load_a(u, u);
+  __builtin_amdgcn_sched_barrier(0);
+  if (wait_phase >= 0 && p.trace != nullptr && (int)blockIdx.x < kTraceWgs && threadIdx.x == 0)
+    stg(p.trace + (size_t)blockIdx.x * pass_phases(p.L) * 8 + wait_phase * 8 + 3, (long long)wall_clock64());
+
+  f32x4 acc[MB][C];
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < ns; i += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      __builtin_amdgcn_sched_barrier(0);
+      // (steps past the end multiply zero lines: no guard, so the loop is
+      // straight-line code and every wait covers one stage)
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+        for (int c = 0; c < C; ++c) acc[rb][c] = mfma16x16x32(ba[u][rb], bw[u][c], acc[rb][c]);
+      __builtin_amdgcn_sched_barrier(0);
+      load_w(u, i + u + D);
+      load_a(u, i + u + D);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (SSQR) {
+    if (io.norm && p.ssq_regs) {
+      constexpr int QUADS = 4 * MB;
+      const int q = threadIdx.x % QUADS, ch = threadIdx.x / QUADS;
+      f32x4 t = sr[0];
+#pragma unroll
+      for (int k = 1; k < SSQN; ++k) t += sr[k];
+      *(f32x4*)&gl.part_ss[ch * 16 * MB + 4 * q] = t;
+    }
+  }
+  // This wave's partial tile -> LDS; the epilogue adds the four in wave order.
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb)
+      lds_st<f32x4>(lds + kTwOff + ((size_t)((wave * C + c) * MB + rb) * 64 + lane) * 16, acc[rb][c]);
+  __syncthreads();
+  return true;
+}
+
+template <int MB, int C>
+__device__ __forceinline__ bool tile_dispatch(int cw, KParams& p, int step, int layer, int nb0, int wait_phase,
+                                              char* lds, GemmLds& gl, int* flag) {
+  if constexpr (C >= 1) {
+    if (cw == C) return tile_compute<MB, C>(p, step, layer, nb0, wait_phase, lds, gl, flag);
+    return tile_dispatch<MB, C - 1>(cw, p, step, layer, nb0, wait_phase, lds, gl, flag);
+  } else {
+    return false;
   }
 }
 
+// Rotary embedding frequency of dim pair (j, j + Dh/2): theta^(-2j/Dh).
+__device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) {
+  return exp2f(-(2.0f * (float)j / (float)Dh) * log2_theta);
+}
+
 // RMSNorm scales of rows [0, Mp): 1 / sqrt(mean of squares + eps) from the
-// per-n-block sums of squares the producing phase wrote (added in n-block
-// order); 0 for rows >= n.  Loads are issued here, the sums are formed by
-// finish_row_scales after the caller's wait.
+// per-16-column sums of squares the producing phase wrote, added in a fixed
+// order; 0 for rows >= n.  When the tile held them in registers its chunk
+// sums are in part_ss already.
 template <int MB>
-struct SsqLoads {
-  static constexpr int ROWS = 32 * MB, CHK = 256 / ROWS, PER = 16;
-  float v[PER];
-};
-template <int MB>
-__device__ __forceinline__ void row_scale_loads(KParams& p, const StepIo& io, SsqLoads<MB>& L, int pass) {
-  constexpr int ROWS = 32 * MB, CHK = 256 / ROWS, PER = SsqLoads<MB>::PER;
+__device__ __forceinline__ void row_scales(KParams& p, const StepIo& io, GemmLds& gl) {
+  constexpr int ROWS = 16 * MB;
+  if (MB <= 2 && p.ssq_regs) {
+    constexpr int CH = 256 / (4 * MB);
+    if (threadIdx.x < ROWS) {
+      float t = 0.0f;
+      for (int c = 0; c < CH; ++c) t += gl.part_ss[c * ROWS + threadIdx.x];
+      gl.rstd[threadIdx.x] = threadIdx.x < p.n ? 1.0f / sqrtf(t * p.inv_d + p.eps) : 0.0f;
+    }
+    __syncthreads();
+    return;
+  }
+  constexpr int CHK = 256 / ROWS;
   const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
   const int dn = p.d_nb;
   const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int t = t0 + pass * PER + i;
-    L.v[i] = (r < p.n && t < t1) ? ldg(io.ssq + (size_t)t * p.Mp + r) : 0.0f;
-  }
-}
-template <int MB>
-__device__ __forceinline__ void row_scales(KParams& p, const StepIo& io, GemmLds& gl) {
-  constexpr int ROWS = 32 * MB, CHK = 256 / ROWS, PER = SsqLoads<MB>::PER;
-  const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
-  const int dn = p.d_nb;
-  const int len = (ch + 1) * dn / CHK - ch * dn / CHK;
   float ss = 0.0f;
-  for (int pass = 0; pass * PER < len; ++pass) {
-    SsqLoads<MB> L;
-    row_scale_loads<MB>(p, io, L, pass);
+  if (r < p.n) {
+    constexpr int PER = 8;
+    for (int t = t0; t < t1; t += PER) {
+      float v[PER];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) ss += L.v[i];
+      for (int k = 0; k < PER; ++k) v[k] = t + k < t1 ? ldg(io.ssq + (size_t)(t + k) * ROWS + r) : 0.0f;
+#pragma unroll
+      for (int k = 0; k < PER; ++k) ss += v[k];
+    }
   }
   gl.part_ss[ch * ROWS + r] = ss;
   __syncthreads();
@@ -337,327 +537,109 @@ __device__ __forceinline__ void row_scales(KParams& p, const StepIo& io, GemmLds
   __syncthreads();
 }
 
-// Weight stages per wave: about 160 VGPRs, 2 to 16 k-steps; one stage for
-// the widest tiles, whose accumulators fill the AGPRs.
-template <int CW>
-constexpr int tile_depth() {
-  constexpr int d = 40 / CW;
-  return CW >= 12 ? 1 : (d < 2 ? 2 : (d > 16 ? 16 : d));
-}
-
-// One tile: n-blocks [nb0, nb0 + CW) x k-steps [k0, k1) of a step.  Issues
-// the first weight stages, then (wait_phase >= 0) waits at the grid barrier
-// for the step's inputs, stages the activations into LDS, streams the
-// weights and leaves the tile's sum in LDS at T = A:
-// fp32 [CW][MB][64 lanes][16] (MFMA accumulator order).  False if a wait
-// ran out.
-template <int MB, int CW>
-__device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams& pin, int step, int layer,
-                                                                       int nb0, int k0, int k1,
-                                                                       int wait_phase, char* A,
-                                                                       GemmLds& gl, int* lds_flag) {
-  KParams& p = uniform_params(pin);
-  step = wave_uniform(step);
-  layer = wave_uniform(layer);
-  nb0 = wave_uniform(nb0);
-  k0 = wave_uniform(k0);
-  k1 = wave_uniform(k1);
-  wait_phase = wave_uniform(wait_phase);
-  const StepIo io = step_io(p, step, layer);
-  const int wave = wave_index(), lane = threadIdx.x & 63;
-  const int kt = k1 - k0;
-  const int ns = wave_uniform(wave < kt ? (kt - wave + kWaves - 1) / kWaves : 0);
-  constexpr int D = tile_depth<CW>();
-  // this wave's k-steps: k0 + wave + 4 i
-  const bf16x8* wt = io.w + ((size_t)nb0 * io.ks + k0 + wave) * 64 + lane;
-  const size_t cstride = (size_t)io.ks * 64;
-  bf16x8 bw[D][CW];
-  auto load_stage = [&](int slot, int i) {
-#pragma unroll
-    for (int c = 0; c < CW; ++c) bw[slot][c] = ldg_nt(wt + c * cstride + (size_t)(kWaves * i) * 64);
-  };
-  if (ns > 0) {
-#pragma unroll
-    for (int u = 0; u < D; ++u) {
-      load_stage(u, u < ns ? u : ns - 1);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  }
-  if (wait_phase >= 0) {
-    const Sync sy = make_sync(p, lds_flag);
-    trace_mark(sy, wait_phase, 0);
-    if (!grid_wait(sy, wait_phase, p.G)) return false;
-    trace_mark(sy, wait_phase, 1);
-  }
-  stage_activations<MB>(p, io, k0, kt, A);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (wait_phase >= 0 && p.trace != nullptr && (int)blockIdx.x < kTraceWgs && threadIdx.x == 0)
-    stg(p.trace + (size_t)blockIdx.x * (2 + 5 * p.L) * 8 + wait_phase * 8 + 3, (long long)wall_clock64());
-
-  f32x16 acc[MB][CW];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int c = 0; c < CW; ++c) acc[mb][c] = f32x16{};
-  for (int i = 0; i < ns; i += D) {
-#pragma unroll
-    for (int u = 0; u < D; ++u) {
-      __builtin_amdgcn_sched_barrier(0);
-      if (i + u < ns) {
-        const int kk = wave + kWaves * (i + u);
-        bf16x8 a[MB];
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) a[mb] = *(const bf16x8*)(A + (size_t)(kk * MB + mb) * 1024 + lane * 16);
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-          for (int c = 0; c < CW; ++c) acc[mb][c] = mfma32(a[mb], bw[u][c], acc[mb][c]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      const int nx = i + u + D < ns ? i + u + D : ns - 1;
-      load_stage(u, nx);
-    }
-  }
-  __builtin_amdgcn_sched_barrier(0);
-  __syncthreads();  // every wave is done reading the activations
-  // Wave partials -> T (the activation region), added in wave order.
-  float* T = reinterpret_cast<float*>(A);
-  for (int w = 0; w < kWaves; ++w) {
-    if (wave == w) {
-#pragma unroll
-      for (int c = 0; c < CW; ++c)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          float4* dst = reinterpret_cast<float4*>(T + ((size_t)(c * MB + mb) * 64 + lane) * 16);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            float4 v = make_float4(acc[mb][c][4 * j], acc[mb][c][4 * j + 1], acc[mb][c][4 * j + 2],
-                                   acc[mb][c][4 * j + 3]);
-            if (w > 0) {
-              const float4 o = dst[j];
-              v.x += o.x;
-              v.y += o.y;
-              v.z += o.z;
-              v.w += o.w;
-            }
-            dst[j] = v;
-          }
-        }
-    }
-    __syncthreads();
-  }
-  return true;
-}
-
-template <int MB, int CW>
-__device__ __forceinline__ bool tile_dispatch(int cw, KParams& p, int step, int layer, int nb0, int k0,
-                                              int k1, int wait_phase, char* A, GemmLds& gl, int* flag) {
-  if constexpr (CW >= 1) {
-    if (cw == CW) return tile_compute<MB, CW>(p, step, layer, nb0, k0, k1, wait_phase, A, gl, flag);
-    return tile_dispatch<MB, CW - 1>(cw, p, step, layer, nb0, k0, k1, wait_phase, A, gl, flag);
-  } else {
-    return false;
-  }
-}
-
-// Rotary embedding frequency of dim pair (j, j + Dh/2): theta^(-2j/Dh).
-__device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) {
-  return exp2f(-(2.0f * (float)j / (float)Dh) * log2_theta);
-}
-
-// Epilogue.  A group's output is cw n-blocks x MB row blocks, one 32x32
-// accumulator tile ("unit") each, unit u = c MB + mb, held in T (fp32
-// [cw][MB][64 lanes][16], MFMA accumulator order).  A workgroup finishes
-// units [u_lo, u_hi): its waves take them in turn, kEpiBatch per wave at a
-// time, and write the step's outputs with device-coherent stores.  The
-// inputs a batch reads from memory (the residual stream, the rotary table)
-// are loaded first, all at once (EpiPre), so that a batch costs one round
-// trip; the first batch's are issued before the group's partials are read.
-constexpr int kEpiBatch = 2;
-
-template <int EPI>
-struct EpiPre {
-  static constexpr int U = (EPI == EPI_RESID || EPI == EPI_QKV) ? kEpiBatch : 1;
-  float a[U][16];                       // RESID: x_in; QKV: cos
-  float b[EPI == EPI_QKV ? U : 1][16];  // QKV: sin
-  float g[EPI == EPI_RESID ? U : 1];    // RESID: gain of the next norm at this lane's column
-};
-
+// Epilogue of one accumulator tile ("unit": block c of the tile x row block
+// rb, 16 x 16).  The unit's sum is the four waves' partials added in wave
+// order; lane l holds rows 16 rb + 4 (l / 16) + i, i < 4, column l % 16.
+// Outputs are written with device-coherent stores.
 template <int MB, int EPI>
-__device__ __forceinline__ void epilogue_preload(KParams& p, const StepIo& io, int nb0, int u_lo, int u_hi, int ub,
-                                                 EpiPre<EPI>& pre) {
-  if constexpr (EPI == EPI_RESID || EPI == EPI_QKV) {
-    const int wave = wave_index(), lane = threadIdx.x & 63;
-    const int j = lane & 31;
+__device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, const char* lds, int cw, int c, int rb,
+                                              int nb, GemmLds& gl) {
+  const int lane = threadIdx.x & 63, j = lane & 15, q4 = lane >> 4;
+  const int unit = c * MB + rb;
+  f32x4 s = lds_ld<f32x4>(lds + kTwOff + ((size_t)unit * 64 + lane) * 16);
 #pragma unroll
-    for (int uu = 0; uu < kEpiBatch; ++uu) {
-      const int unit = u_lo + wave + kWaves * (ub + uu);
-      if (unit >= u_hi) break;
-      const int c = unit / MB, mb = unit % MB;
-      const int nb = nb0 + c;
-      if constexpr (EPI == EPI_RESID) {
-        const int col = kNB * nb + j;
-        pre.g[uu] = bf2f(ldg(io.g_next + col));
+  for (int w = 1; w < kWaves; ++w) s += lds_ld<f32x4>(lds + kTwOff + ((size_t)(w * cw * MB + unit) * 64 + lane) * 16);
+  float v[4] = {s[0], s[1], s[2], s[3]};
+  const int rr0 = 4 * q4;  // first row of this lane inside the row block
+  if constexpr (EPI != EPI_RESID) {  // the norm's per-row scale
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int r = 32 * mb + acc_row(i, lane);
-          pre.a[uu][i] = r < p.n ? ldg(io.x_in + (size_t)r * p.d + col) : 0.0f;
-        }
-      } else {
-        const int d = p.d, dh = p.Dh;
-        if (kNB * nb < 2 * d) {
-          const int t = ((kNB * nb) % d % dh) / kNB;
-          const int jj = 16 * t + (j & 15);
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int r = 32 * mb + acc_row(i, lane);
-            const float2 cs = r < p.n ? ldg((const float2*)p.rope + (size_t)r * (dh / 2) + jj) : make_float2(1.0f, 0.0f);
-            pre.a[uu][i] = cs.x;
-            pre.b[uu][i] = cs.y;
-          }
-        }
-      }
-    }
+    for (int i = 0; i < 4; ++i) v[i] *= gl.rstd[16 * rb + rr0 + i];
   }
-}
-
-template <int MB, int EPI>
-__device__ __forceinline__ void epilogue(KParams& p, const StepIo& io, const float* T, int nb0, int u_lo, int u_hi,
-                                         int ub, const EpiPre<EPI>& pre, GemmLds& gl) {
-  const int wave = wave_index(), lane = threadIdx.x & 63;
-  const int j = lane & 31;
+  const char* epi = lds + kEpiOff;
+  const int col = kNB * nb + j;
+  if constexpr (EPI == EPI_QKV) {
+    const int d = p.d, dh = p.Dh;
+    if (kNB * nb < 2 * d) {
+      // q or k: this block holds dims [8t, 8t+8) (lanes j < 8) and their
+      // rotary partners + Dh/2 (lanes j >= 8) of one head.
+      const int part = (kNB * nb) / d, cq = (kNB * nb) % d, hh = cq / dh, t = (cq % dh) / kNB;
+      const int dim = 8 * t + (j & 7) + (j < 8 ? 0 : dh / 2);
+      bf16* base = part == 0 ? io.q + hh * dh : io.kc + (size_t)hh * p.cap * dh;
+      const char* csu = epi + (size_t)unit * 1024;
 #pragma unroll
-  for (int uu = 0; uu < kEpiBatch; ++uu) {
-    const int unit = u_lo + wave + kWaves * (ub + uu);
-    if (unit >= u_hi) break;
-    const int c = unit / MB, mb = unit % MB;
-    const int nb = nb0 + c;
-    float v[16];
-    {
-      const float4* src = reinterpret_cast<const float4*>(T + ((size_t)unit * 64 + lane) * 16);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 f = src[q];
-        v[4 * q] = f.x;
-        v[4 * q + 1] = f.y;
-        v[4 * q + 2] = f.z;
-        v[4 * q + 3] = f.w;
-      }
-    }
-    if constexpr (EPI != EPI_RESID) {  // the norm's per-row scale
-#pragma unroll
-      for (int i = 0; i < 16; ++i) v[i] *= gl.rstd[32 * mb + acc_row(i, lane)];
-    }
-    if constexpr (EPI == EPI_QKV) {
-      const int d = p.d, dh = p.Dh;
-      const int col = kNB * nb + j;
-      if (col < 2 * d) {
-        // q or k: this n-block holds dims [16t, 16t+16) (lanes j < 16) and
-        // their rotary partners + Dh/2 (lanes j >= 16) of one head.
-        const int part = col / d, cq = (kNB * nb) % d, hh = cq / dh, t = (cq % dh) / kNB;
-        const int jj = 16 * t + (j & 15);  // pair index < Dh/2
-        const int dim = jj + (j < 16 ? 0 : dh / 2);
-        bf16* base = part == 0 ? io.q + hh * dh : io.kc + (size_t)hh * p.cap * dh;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int r = 32 * mb + acc_row(i, lane);
-          const float partner = __shfl_xor(v[i], 16, kWave);
-          const float cs = pre.a[uu][i], sn = pre.b[uu][i];
-          const float outv = j < 16 ? v[i] * cs - partner * sn : v[i] * cs + partner * sn;
-          const float nxt = __shfl_down(outv, 1, kWave);
-          if (r < p.n && (j & 1) == 0) {
-            bf16* dst = part == 0 ? base + (size_t)r * d : base + (size_t)(p.prefix_len + r) * dh;
-            st_coherent_bf2(dst + dim, outv, nxt);
-          }
-        }
-      } else {
-        const int cv = col - 2 * d, hh = cv / dh, dim = cv % dh;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int r = 32 * mb + acc_row(i, lane);
-          const float nxt = __shfl_down(v[i], 1, kWave);
-          if (r < p.n && (j & 1) == 0)
-            st_coherent_bf2(io.vc + ((size_t)hh * p.cap + p.prefix_len + r) * dh + dim, v[i], nxt);
+      for (int i = 0; i < 4; ++i) {
+        const int rr = rr0 + i, r = 16 * rb + rr;
+        const float2 cs = lds_ld<float2>(csu + (size_t)(rr * 8 + (j & 7)) * 8);
+        const float partner = __shfl_xor(v[i], 8, kWave);
+        const float outv = j < 8 ? v[i] * cs.x - partner * cs.y : v[i] * cs.x + partner * cs.y;
+        const float nxt = __shfl_down(outv, 1, kWave);
+        if (r < p.n && (j & 1) == 0) {
+          bf16* dst = part == 0 ? base + (size_t)r * d : base + (size_t)(p.prefix_len + r) * dh;
+          st_coherent_bf2(dst + dim, outv, nxt);
         }
       }
-    } else if constexpr (EPI == EPI_RESID) {
-      const int col = kNB * nb + j;
+    } else {
+      const int cv = col - 2 * d, hh = cv / dh, dim = cv % dh;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int r = 32 * mb + acc_row(i, lane);
-        const float xn = r < p.n ? pre.a[uu][i] + v[i] : 0.0f;
-        if (r < p.n) st_coherent(io.x_out + (size_t)r * p.d + col, xn);
-        const float xg = xn * pre.g[uu];
-        const float xg1 = __shfl_down(xg, 1, kWave);
-        if (r < p.n && (j & 1) == 0) st_coherent_bf2(io.xg_out + (size_t)r * p.d + col, xg, xg1);
-        float s = xn * xn;  // sum of squares over the n-block's 32 columns
-        s += __shfl_xor(s, 16, kWave);
-        s += __shfl_xor(s, 8, kWave);
-        s += __shfl_xor(s, 4, kWave);
-        s += __shfl_xor(s, 2, kWave);
-        s += __shfl_xor(s, 1, kWave);
-        if (j == 0 && r < p.n) st_coherent(io.ssq_out + (size_t)nb * p.Mp + r, s);
-      }
-    } else if constexpr (EPI == EPI_SWIGLU) {
-      const int f = 16 * nb + (j & 15);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int r = 32 * mb + acc_row(i, lane);
-        const float up = __shfl_xor(v[i], 16, kWave);
-        const float hv = v[i] / (1.0f + expf(-v[i])) * up;
-        const float nxt = __shfl_down(hv, 1, kWave);
-        if (r < p.n && j < 16 && (j & 1) == 0) st_coherent_bf2(io.h + (size_t)r * p.Fp + f, hv, nxt);
-      }
-    } else {  // EPI_LOGITS
-      const int col = kNB * nb + j;
-      const bool vcol = col < p.V;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int r = 32 * mb + acc_row(i, lane);
-        const bool valid = vcol && r < p.n;
-        if (valid && p.logits != nullptr && r >= p.row_lo) stg(p.logits + (size_t)(r - p.row_lo) * p.V + col, v[i]);
-        float mv = valid ? v[i] : -INFINITY;
-        int mi = valid ? col : 0x7fffffff;
-#pragma unroll
-        for (int off = 16; off >= 1; off >>= 1) {  // argmax over the n-block's 32 columns
-          const float ov = __shfl_xor(mv, off, kWave);
-          const int oi = __shfl_xor(mi, off, kWave);
-          if (ov > mv || (ov == mv && oi < mi)) {
-            mv = ov;
-            mi = oi;
-          }
-        }
-        if (j == 0) {
-          gl.red_v[r][c] = mv;
-          gl.red_i[r][c] = mi;
-        }
+      for (int i = 0; i < 4; ++i) {
+        const int r = 16 * rb + rr0 + i;
+        const float nxt = __shfl_down(v[i], 1, kWave);
+        if (r < p.n && (j & 1) == 0)
+          st_coherent_bf2(io.vc + ((size_t)hh * p.cap + p.prefix_len + r) * dh + dim, v[i], nxt);
       }
     }
-  }
-}
-
-// LM head: per row, the best (value, lowest column) over this workgroup's
-// units of the group, into argmax slot `slot` (-inf where it has none).
-template <int MB>
-__device__ __forceinline__ void logits_units_argmax(KParams& p, int cw, int u_lo, int u_hi, int slot, GemmLds& gl) {
-  __syncthreads();
-  for (int r = threadIdx.x; r < 32 * MB; r += kThreads) {
-    const int mb = r / 32;
-    float mv = -INFINITY;
-    int mi = 0x7fffffff;
-    for (int c = 0; c < cw; ++c) {
-      const int u = c * MB + mb;
-      if (u < u_lo || u >= u_hi) continue;
-      const float v = gl.red_v[r][c];
-      const int i = gl.red_i[r][c];
-      if (v > mv || (v == mv && i < mi)) {
-        mv = v;
-        mi = i;
+  } else if constexpr (EPI == EPI_RESID) {
+    const char* xu = epi + (size_t)unit * 1024;
+    const float g = bf2f(lds_ld<bf16>(epi + (size_t)(cw * MB + c) * 1024 + 16 * (j >> 3) + 2 * (j & 7)));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = rr0 + i, r = 16 * rb + rr;
+      const float xn = r < p.n ? lds_ld<float>(xu + (size_t)(rr * 16 + j) * 4) + v[i] : 0.0f;
+      const float xn1 = __shfl_down(xn, 1, kWave);
+      if (r < p.n && (j & 1) == 0) st_coherent2(io.x_out + (size_t)r * p.d + col, xn, xn1);
+      const float xg = xn * g;
+      const float xg1 = __shfl_down(xg, 1, kWave);
+      if (r < p.n && (j & 1) == 0) st_coherent_bf2(io.xg_out + frag_off(r, col, MB), xg, xg1);
+      float sq = xn * xn;  // sum of squares over the block's 16 columns
+      sq += __shfl_xor(sq, 8, kWave);
+      sq += __shfl_xor(sq, 4, kWave);
+      sq += __shfl_xor(sq, 2, kWave);
+      sq += __shfl_xor(sq, 1, kWave);
+      if (j == 0 && r < p.n) st_coherent(io.ssq_out + (size_t)nb * p.Mp + r, sq);
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    const int f = 8 * nb + (j & 7);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * rb + rr0 + i;
+      const float up = __shfl_xor(v[i], 8, kWave);
+      const float hv = v[i] / (1.0f + expf(-v[i])) * up;
+      const float nxt = __shfl_down(hv, 1, kWave);
+      if (r < p.n && j < 8 && (j & 1) == 0) st_coherent_bf2(io.h + frag_off(r, f, MB), hv, nxt);
+    }
+  } else {  // EPI_LOGITS
+    const bool vcol = col < p.V;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * rb + rr0 + i;
+      const bool valid = vcol && r < p.n;
+      if (valid && p.logits != nullptr && r >= p.row_lo) stg(p.logits + (size_t)(r - p.row_lo) * p.V + col, v[i]);
+      float mv = valid ? v[i] : -INFINITY;
+      int mi = valid ? col : 0x7fffffff;
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) {  // argmax over the block's 16 columns
+        const float ov = __shfl_xor(mv, off, kWave);
+        const int oi = __shfl_xor(mi, off, kWave);
+        if (ov > mv || (ov == mv && oi < mi)) {
+          mv = ov;
+          mi = oi;
+        }
+      }
+      if (j == 0) {
+        gl.red_v[r][c] = mv;
+        gl.red_i[r][c] = mi;
       }
     }
-    st_coherent(&p.lm_val[(size_t)slot * p.Mp + r], mv);
-    st_coherent(&p.lm_idx[(size_t)slot * p.Mp + r], mi);
   }
 }
 
@@ -729,124 +711,52 @@ __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl
   __syncthreads();
 }
 
-// The hand-off of one tile whose sum is in T.  With S > 1 the tile's
-// partial goes to memory; when the step has at most one tile per workgroup,
-// the S workgroups of the group wait for each other and each adds the S
-// partials of its own 1/S of the group's units (in slice order) and runs
-// their epilogue; otherwise (no waits inside a phase: a workgroup's later
-// tile could be waited for) the group's last workgroup does all of it.  A
-// function of its own so that its registers are allocated apart from the
-// streaming loops'.  False if a wait ran out.
+// The epilogue of one tile (blocks [nb0, nb0 + cw)): the waves take its
+// units in turn.  The LM head also folds the tile's per-block argmax into
+// the workgroup's running argmax per row.  A function of its own so that its
+// registers are allocated apart from the streaming loop's.
 template <int MB, int EPI>
-__device__ __attribute__((noinline, not_tail_called)) bool finish_tile(KParams& pin, int step, int layer, int t,
-                                                                      int tr_phase, char* A, GemmLds& gl,
-                                                                      int* lds_flag) {
+__device__ __attribute__((noinline, not_tail_called)) void finish_tile(KParams& pin, int step, int layer, int nb0,
+                                                                      int cw, char* lds, GemmLds& gl) {
   KParams& p = uniform_params(pin);
   step = wave_uniform(step);
   layer = wave_uniform(layer);
-  t = wave_uniform(t);
-  tr_phase = wave_uniform(tr_phase);
-  const Sync sy = make_sync(p, lds_flag);
-  const StepPlan& sp = p.step[step];
-  const int S = sp.S, tiles = sp.groups * sp.S;
+  nb0 = wave_uniform(nb0);
+  cw = wave_uniform(cw);
   const StepIo io = step_io(p, step, layer);
-  const int g = t / S, s = t % S;
-  const int nb0 = g * sp.cw + (g < sp.n_hi ? g : sp.n_hi);
-  const int cw = sp.cw + (g < sp.n_hi ? 1 : 0);
-  const int U = cw * MB;
-  const int tile_words = U * 1024;
-  float* T = reinterpret_cast<float*>(A);
-  int u_lo = 0, u_hi = U;
-  bool finish = true;
-  const bool shared = tiles <= p.G;
-  int* cnt = sp.group_cnt + g;
-  float* part_g = p.part + (size_t)(nb0 * S) * MB * 1024;
-  if (S > 1) {
-    float* mine = part_g + (size_t)s * tile_words;
-    for (int w = 2 * threadIdx.x; w < tile_words; w += 2 * kThreads) st_coherent2(mine + w, T[w], T[w + 1]);
-    if (shared) {
-      u_lo = s * U / S;
-      u_hi = (s + 1) * U / S;
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      if (threadIdx.x == 0) atomic_add_dev(cnt, 1);
-    } else {
-      finish = arrive_last(cnt, S, lds_flag);
-    }
+  if constexpr (EPI != EPI_RESID) row_scales<MB>(p, io, gl);
+  const int units = cw * MB;
+  for (int u = wave_index(); u < units; u += kWaves) {
+    const int c = u / MB, rb = u % MB;
+    epilogue_unit<MB, EPI>(p, io, lds, cw, c, rb, nb0 + c, gl);
   }
-  EpiPre<EPI> pre;
-  if (finish) epilogue_preload<MB, EPI>(p, io, nb0, u_lo, u_hi, 0, pre);
-  if constexpr (EPI != EPI_RESID) {
-    if (finish) row_scales<MB>(p, io, gl);
-  }
-  if (S > 1) {
-    if (tr_phase >= 0) trace_mark(sy, tr_phase, 6);
-    // Group counters are cleared when the pass ends: within a pass a step's
-    // counter of a group is used once per layer.
-    if (shared && !wait_at_least(sy, cnt, S * (layer + 1))) return false;
-    if (finish) {
-      // T[units u_lo..u_hi) = sum of the S partials in slice order.  Loads
-      // go out in batches of 4 slices x 8 pairs per thread, so the sum costs
-      // about S / 4 round trips.
-      constexpr int B = 8;
-      const int p_lo = u_lo * 512, p_hi = u_hi * 512;  // float2 pairs
-      for (int base = p_lo + (int)threadIdx.x; base < p_hi; base += kThreads * B) {
-        float2 acc[B];
-#pragma unroll
-        for (int j = 0; j < B; ++j) acc[j] = make_float2(0.0f, 0.0f);
-        for (int s0 = 0; s0 < S; s0 += 4) {
-          float2 v[4][B];
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-#pragma unroll
-            for (int j = 0; j < B; ++j) {
-              const int idx = base + j * kThreads;
-              v[k][j] = (s0 + k < S && idx < p_hi)
-                            ? ld_coherent2(part_g + (size_t)(s0 + k) * tile_words + 2 * idx)
-                            : make_float2(0.0f, 0.0f);
-            }
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-#pragma unroll
-            for (int j = 0; j < B; ++j) {
-              acc[j].x += v[k][j].x;
-              acc[j].y += v[k][j].y;
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < B; ++j) {
-          const int idx = base + j * kThreads;
-          if (idx < p_hi) {
-            T[2 * idx] = acc[j].x;
-            T[2 * idx + 1] = acc[j].y;
-          }
+  if constexpr (EPI == EPI_LOGITS) {
+    __syncthreads();
+    for (int r = threadIdx.x; r < 16 * MB; r += kThreads) {
+      float mv = gl.best_v[r];
+      int mi = gl.best_i[r];
+      for (int c = 0; c < cw; ++c) {
+        const float v = gl.red_v[r][c];
+        const int i = gl.red_i[r][c];
+        if (v > mv || (v == mv && i < mi)) {
+          mv = v;
+          mi = i;
         }
       }
-      __syncthreads();
-      if (tr_phase >= 0) trace_mark(sy, tr_phase, 7);
-    }
-  }
-  if (finish) {
-    for (int ub = 0; u_lo + wave_index() + kWaves * ub < u_hi; ub += kEpiBatch) {
-      if (ub > 0) epilogue_preload<MB, EPI>(p, io, nb0, u_lo, u_hi, ub, pre);
-      epilogue<MB, EPI>(p, io, T, nb0, u_lo, u_hi, ub, pre, gl);
-    }
-    if constexpr (EPI == EPI_LOGITS) {
-      const int slot = shared ? t : g;
-      logits_units_argmax<MB>(p, cw, u_lo, u_hi, slot, gl);
-      if (arrive_last(p.lm_cnt, shared ? tiles : sp.groups, lds_flag)) finish_walk(p, shared ? tiles : sp.groups, gl);
+      gl.best_v[r] = mv;
+      gl.best_i[r] = mi;
     }
   }
   __syncthreads();
-  return true;
 }
 
-// One GEMM phase: this workgroup's tiles, each followed by its share of the
-// group hand-off and, in the group's last workgroup, the epilogue.
+// One GEMM phase: this workgroup's run of blocks, in tiles of at most
+// tile_max_blocks blocks over the full K, each followed by its epilogue.  The
+// LM head then publishes the workgroup's argmax per row, and the last
+// workgroup to do so runs the accept walk.
 template <int MB, int EPI>
 __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& pin, int step, int layer,
-                                                                     int phase, char* A, GemmLds& gl,
+                                                                     int phase, char* lds, GemmLds& gl,
                                                                      int* lds_flag) {
   KParams& p = uniform_params(pin);
   step = wave_uniform(step);
@@ -854,29 +764,39 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   phase = wave_uniform(phase);
   const Sync sy = make_sync(p, lds_flag);
   const StepPlan& sp = p.step[step];
-  const int S = sp.S, tiles = sp.groups * sp.S;
-  constexpr int CWM = kMaxCW / MB;
-  // The barrier counts arrivals: it is exact only if every workgroup waits
-  // at every phase before it arrives again, tile or no tile.
-  if ((int)blockIdx.x >= tiles) {
-    trace_mark(sy, phase, 0);
-    const bool ok = grid_wait(sy, phase, p.G);
-    trace_mark(sy, phase, 1);
-    return ok;
+  constexpr int CM = MB <= 2 ? 8 : 16 / MB;
+  const int nbk = sp.nblocks, G = p.G;
+  const int lo = wave_uniform((int)((long)blockIdx.x * nbk / G));
+  const int hi = wave_uniform((int)((long)(blockIdx.x + 1) * nbk / G));
+  if constexpr (EPI == EPI_LOGITS) {
+    for (int r = threadIdx.x; r < 16 * MB; r += kThreads) {
+      gl.best_v[r] = -INFINITY;
+      gl.best_i[r] = 0x7fffffff;
+    }
   }
-  bool first = true;
-  for (int t = blockIdx.x; t < tiles; t += p.G) {
-    const int g = t / S, s = t % S;
-    const int nb0 = g * sp.cw + (g < sp.n_hi ? g : sp.n_hi);
-    const int cw = sp.cw + (g < sp.n_hi ? 1 : 0);
-    const int k0 = (int)((long)s * sp.ksteps / S), k1 = (int)((long)(s + 1) * sp.ksteps / S);
-    if (!tile_dispatch<MB, CWM>(cw, p, step, layer, nb0, k0, k1, first ? phase : -1, A, gl, lds_flag))
-      return false;
+  if (lo >= hi) {
+    // The barrier counts arrivals: it is exact only if every workgroup waits
+    // at every phase before it arrives again, work or no work.
+    trace_mark(sy, phase, 0);
+    if (!grid_wait(sy, phase, G)) return false;
+    trace_mark(sy, phase, 1);
+  }
+  for (int b0 = lo; b0 < hi; b0 += CM) {
+    const int cw = hi - b0 < CM ? hi - b0 : CM;
+    const bool first = b0 == lo;
+    if (!tile_dispatch<MB, CM>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag)) return false;
     if (first) trace_mark(sy, phase, 4);
-    if (!finish_tile<MB, EPI>(p, step, layer, t, first ? phase : -1, A, gl, lds_flag)) return false;
-    first = false;
+    finish_tile<MB, EPI>(p, step, layer, b0, cw, lds, gl);
   }
   trace_mark(sy, phase, 5);
+  if constexpr (EPI == EPI_LOGITS) {
+    __syncthreads();
+    for (int r = threadIdx.x; r < 16 * MB; r += kThreads) {
+      st_coherent(&p.lm_val[(size_t)blockIdx.x * p.Mp + r], gl.best_v[r]);
+      st_coherent(&p.lm_idx[(size_t)blockIdx.x * p.Mp + r], gl.best_i[r]);
+    }
+    if (arrive_last(p.lm_cnt, G, lds_flag)) finish_walk(p, G, gl);
+  }
   return true;
 }
 
@@ -929,7 +849,7 @@ __device__ __forceinline__ void attn_stage(char* lds, const bf16* kc, const bf16
 // matrix cores, online softmax in the log2 domain, O^T += V^T P^T with P split
 // into two bf16 halves (P never leaves registers: the S result's lane layout
 // is the PV product's k-slot order).  Then the head's splits join and each
-// merges its share of the rows.
+// merges its share of the rows.  MB: 16-row blocks of the pass.
 template <int MB, int DH>
 __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& pin, int layer, int phase, char* lds,
                                                                      int* lds_flag) {
@@ -1153,7 +1073,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
         o0 += v.x * wgt[ss][i];
         o1 += v.y * wgt[ss][i];
       }
-      st_coherent_bf2(obase + (size_t)i * p.d + h * DH + dd, o0, o1);
+      st_coherent_bf2(obase + frag_off(i, h * DH + dd, MB), o0, o1);
     }
     __syncthreads();
   }
@@ -1164,8 +1084,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
 
 // Tree preparation (every node's depth, position prefix_len + depth, and
 // ancestor-or-self set: its row of the tree masking table) and the residual
-// stream's first version: the nodes' embedding rows, with the sums of
-// squares of every 32-column n-block.
+// stream's first version: the nodes' embedding rows, bf16(x * g) for the
+// first layer's norm, and the sums of squares of every 16 columns.
+template <int MB>
 __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, int* par_s) {
   const bf16* E = (const bf16*)(p.packed + p.o_embed);
   if (blockIdx.x == 0) {
@@ -1208,29 +1129,37 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
       st_coherent(&p.x[(size_t)m * p.d + c], v);
       const float xg = v * bf2f(ldg(g0 + c));
       const float xg1 = __shfl_down(xg, 1, kWave);
-      if ((c & 1) == 0) st_coherent_bf2(p.xg + (size_t)m * p.d + c, xg, xg1);
+      if ((c & 1) == 0) st_coherent_bf2(p.xg + frag_off(m, c, MB), xg, xg1);
       float s = v * v;
-      s += __shfl_xor(s, 16, kWave);
       s += __shfl_xor(s, 8, kWave);
       s += __shfl_xor(s, 4, kWave);
       s += __shfl_xor(s, 2, kWave);
       s += __shfl_xor(s, 1, kWave);
-      if ((lane & 31) == 0) st_coherent(&p.ssq[(size_t)(c / kNB) * p.Mp + m], s);
+      if ((lane & 15) == 0) st_coherent(&p.ssq[(size_t)(c / kNB) * p.Mp + m], s);
     }
   }
 }
 
 // ------------------------------------------------------------------ kernel
 
+template <int DH>
+constexpr size_t dyn_lds_bytes() {
+  constexpr size_t attn = AttnGeom<DH>::BYTES;
+  constexpr size_t merge = 2 * kAttnMaxSplits * kMaxNodes * 4;
+  constexpr size_t gemm = kGemmLdsBytes;
+  constexpr size_t m1 = attn > merge ? attn : merge;
+  return m1 > gemm ? m1 : gemm;
+}
+
 template <int MB, int DH>
 __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_arg, const TreeArgs tree) {
-  extern __shared__ __attribute__((aligned(16))) char lds_raw[];
+  extern __shared__ __attribute__((aligned(1024))) char lds_raw[];
   __shared__ GemmLds gl;
   __shared__ int par_s[128];
   __shared__ int flag;
   // The parameter block is the first kernel argument: read it in place.
   KParams& p = *(KParams*)__builtin_amdgcn_kernarg_segment_ptr();
-  if (p.magic != kPassMagic || p.G != p_arg.G || p.n != p_arg.n) {
+  if (p.magic != kPassMagic || p.G != p_arg.G || p.n != p_arg.n || p.Mp != 16 * MB) {
     if (threadIdx.x == 0 && blockIdx.x == 0) stg(p_arg.status, 3);
     return;  // (uniform over the grid: no workgroup reaches a barrier)
   }
@@ -1238,7 +1167,13 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
   int phase = 0;
   bool ok = true;
 
-  embed_phase(p, tree, par_s);
+  embed_phase<MB>(p, tree, par_s);
+  grid_arrive(sy, phase);
+  ++phase;
+  // The QKV phases load the rotary table before they wait at their barrier
+  // (it is written long before, except for the first layer's): one more
+  // barrier publishes it.
+  ok = grid_wait(sy, phase, p.G);
   grid_arrive(sy, phase);
   ++phase;
 
@@ -1246,7 +1181,7 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
     ok = gemm_phase<MB, EPI_QKV>(p, STEP_QKV, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
-    ok = attn_phase<2 * MB, DH>(p, l, phase, lds_raw, &flag);
+    ok = attn_phase<MB, DH>(p, l, phase, lds_raw, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
     ok = gemm_phase<MB, EPI_RESID>(p, STEP_O, l, phase, lds_raw, gl, &flag);
@@ -1259,24 +1194,14 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
     if (!ok) break;
     grid_arrive(sy, phase++);
   }
-  if (ok) {  // final norm + LM head + argmax + accept walk
+  if (ok) {  // LM head (final norm scale) + argmax + accept walk
     if (gemm_phase<MB, EPI_LOGITS>(p, STEP_LM, 0, phase, lds_raw, gl, &flag)) trace_mark(sy, phase, 2);
   }
   // Leave the pass: the last workgroup out resets the barrier and join counters.
   if (arrive_last(p.exit_cnt, p.G, &flag)) {
     if (threadIdx.x < kBarSlots) st_coherent(p.bar + threadIdx.x * kBarStride, 0);
     for (int h = threadIdx.x; h < p.H; h += kThreads) st_coherent(&p.head_cnt[h], 0);
-    for (int i = threadIdx.x; i < p.n_group_cnt; i += kThreads) st_coherent(p.group_cnt_all + i, 0);
   }
-}
-
-template <int DH>
-constexpr size_t dyn_lds_bytes() {
-  constexpr size_t attn = AttnGeom<DH>::BYTES;
-  constexpr size_t merge = 2 * kAttnMaxSplits * kMaxNodes * 4;
-  constexpr size_t a = kAStageBytes;
-  constexpr size_t m1 = attn > merge ? attn : merge;
-  return m1 > a ? m1 : a;
 }
 
 template <int MB, int DH>
@@ -1305,37 +1230,39 @@ int occupancy_mb() {
 
 }  // namespace
 
-hipError_t launch_pass(int mb32, KParams& p, const TreeArgs& tree, hipStream_t st) {
+hipError_t launch_pass(int mb16, KParams& p, const TreeArgs& tree, hipStream_t st) {
 #define LLMCAD_PASS_CASE(M)                                                 \
   case M:                                                                   \
     return p.Dh == 128 ? launch_pass_mb<M, 128>(p, tree, st)                \
                        : launch_pass_mb<M, 64>(p, tree, st);
-  switch (mb32) {
+  switch (mb16) {
     LLMCAD_PASS_CASE(1)
     LLMCAD_PASS_CASE(2)
     LLMCAD_PASS_CASE(4)
+    LLMCAD_PASS_CASE(8)
     default:
       return hipErrorInvalidValue;
   }
 #undef LLMCAD_PASS_CASE
 }
 
-int pass_occupancy(int mb32, int dh) {
+int pass_occupancy(int mb16, int dh) {
 #define LLMCAD_OCC_CASE(M) \
   case M:                  \
     return dh == 128 ? occupancy_mb<M, 128>() : occupancy_mb<M, 64>();
-  switch (mb32) {
+  switch (mb16) {
     LLMCAD_OCC_CASE(1)
     LLMCAD_OCC_CASE(2)
     LLMCAD_OCC_CASE(4)
+    LLMCAD_OCC_CASE(8)
     default:
       return 0;
   }
 #undef LLMCAD_OCC_CASE
 }
 
-size_t pass_lds_bytes(int mb32, int dh) {
-  (void)mb32;
+size_t pass_lds_bytes(int mb16, int dh) {
+  (void)mb16;
   return dh == 128 ? dyn_lds_bytes<128>() : dyn_lds_bytes<64>();
 }
 
