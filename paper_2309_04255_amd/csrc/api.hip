@@ -184,17 +184,16 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.q = (bf16*)(ws + W.qs);
   p.o = (bf16*)(ws + W.os);
   p.h = (bf16*)(ws + W.hs);
-  p.attn_o = (float*)(ws + W.attn_o);
-  p.attn_ml = (float*)(ws + W.attn_ml);
-  // Position splits per head: enough (head, split) units for the grid, at
-  // least 16 positions each.
-  const int T = a.prefix_len + a.n;
+  // Splits per head: enough (head, split) units for the grid; the prefix
+  // splits hold at least 16 positions each.
   int S = env_int("LLMCAD_ATTN_SPLITS", G / s.H);
   if (S > kAttnMaxSplits) S = kAttnMaxSplits;
-  if (S > cdiv(T, 16)) S = cdiv(T, 16);
+  if (S > 1 + cdiv(a.prefix_len, 16)) S = 1 + cdiv(a.prefix_len, 16);
   if (s.H * S > G) S = G / s.H;
   if (S < 1) S = 1;
   p.attn_splits = S;
+  p.attn_o = (float*)(ws + W.attn_o);
+  p.attn_ml = (float*)(ws + W.attn_ml);
   p.head_cnt = (int*)(ws + W.head_counters());
   p.lm_cnt = (int*)(ws + W.lm_cnt());
   p.exit_cnt = (int*)(ws + W.exit_cnt());

@@ -98,6 +98,16 @@ __device__ __forceinline__ void wave_argmax(float& v, int& idx) {
   }
 }
 
+// Workgroup barrier for LDS hand-offs only: waits for this wave's LDS
+// accesses, not for its global loads (__syncthreads also drains every global
+// load in flight, which would defeat a prefetch issued before it).
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt left alone
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 // Hand-off between workgroups of one launch without L2 maintenance.
 //
 // A full device-scope fence on this GPU writes back and invalidates the

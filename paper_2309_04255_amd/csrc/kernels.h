@@ -63,14 +63,14 @@ struct PassParams {
   bf16* q;          // [L][Mp][d]   queries after the rotary embedding
   bf16* o;          // [L] x fragment-order [Mp][d]
   bf16* h;          // [L] x fragment-order [Mp][Fp]
-  float* attn_o;    // [H][S][Mp][Dh]
-  float* attn_ml;   // [H][S][Mp][2]
-  int attn_splits;
-  int* head_cnt;
   int* lm_cnt;
   int* exit_cnt;
   int* status;
   int* bar;         // [kBarSlots][kBarStride]
+  float* attn_o;    // [H][S][Mp][Dh] per-split unnormalised outputs
+  float* attn_ml;   // [H][S][Mp][2]  per-split running max and sum
+  int attn_splits;  // S
+  int* head_cnt;    // [H] arrivals of the head's splits
   float* lm_val;    // [G][Mp] LM-head argmax per workgroup
   int* lm_idx;
   int* amax;        // [Mp]

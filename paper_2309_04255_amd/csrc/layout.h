@@ -152,7 +152,7 @@ struct WorkspaceLayout {
   size_t qs;           // bf16 [L][Mp][d]         queries after the rotary embedding
   size_t os;           // bf16 [L] x (Mp x d, fragment order)   attention output
   size_t hs;           // bf16 [L] x (Mp x Fp, fragment order)  SwiGLU product
-  size_t attn_o;       // fp32 [H][S][Mp][Dh]     per-split unnormalised outputs
+  size_t attn_o;       // fp32 [H][S][Mp][Dh]     per-split unnormalised attention outputs
   size_t attn_ml;      // fp32 [H][S][Mp][2]      per-split running max and sum
   size_t total;
   WorkspaceLayout(const Shape& s, int max_n, int G) {

@@ -164,26 +164,6 @@ __device__ __forceinline__ bool grid_wait(const Sync& s, int phase, int G) {
   return ok;
 }
 
-// Waits until *c >= target (one poller); false if the bounded spin ran out.
-__device__ __forceinline__ bool wait_at_least(const Sync& s, const int* c, int target) {
-  if (threadIdx.x == 0) {
-    int ok = 1, spins = 0;
-    while (ld_coherent(c) < target) {
-      __builtin_amdgcn_s_sleep(1);
-      if (++spins > s.limit) {
-        st_coherent(s.status, 1);
-        ok = 0;
-        break;
-      }
-    }
-    *s.lds_flag = ok;
-  }
-  __syncthreads();
-  const bool ok = *s.lds_flag != 0;
-  __syncthreads();
-  return ok;
-}
-
 // ------------------------------------------------------------------ GEMM
 
 struct GemmLds {
@@ -816,40 +796,78 @@ struct AttnGeom {
 // row-major, V transposed; other rows zero.  Every key comes from the cache:
 // the tree's keys and values were written to their slots, already rotated,
 // by the QKV phase.
+// K/V of key positions [p0, p0 + CH) ∩ [lo, hi) of one head, loaded into
+// registers (other positions zero): a thread's 16-byte items of K and V.
 template <int DH>
-__device__ __forceinline__ void attn_stage(char* lds, const bf16* kc, const bf16* vc, int p0, int lo,
-                                           int hi) {
-  using Gm = AttnGeom<DH>;
-  bf16* Ks = reinterpret_cast<bf16*>(lds);
-  bf16* Vt = reinterpret_cast<bf16*>(lds + Gm::KS_BYTES);
-  for (int idx = threadIdx.x; idx < Gm::CH * (DH / 8); idx += kThreads) {
+struct AttnChunkRegs {
+  static constexpr int IT = AttnGeom<DH>::CH * (DH / 8) / kThreads;
+  bf16x8 k[IT], v[IT];
+};
+
+template <int DH>
+__device__ __forceinline__ void attn_load(AttnChunkRegs<DH>& R, const bf16* kc, const bf16* vc, int p0, int lo,
+                                          int hi) {
+#pragma unroll
+  for (int k = 0; k < AttnChunkRegs<DH>::IT; ++k) {
+    const int idx = threadIdx.x + k * kThreads;
     const int j = idx / (DH / 8), dc = (idx % (DH / 8)) * 8;
     const int pos = p0 + j;
-    bf16x8 k0, v0;
     if (pos >= lo && pos < hi) {
-      k0 = ldg((const bf16x8*)(kc + (size_t)pos * DH + dc));
-      v0 = ldg((const bf16x8*)(vc + (size_t)pos * DH + dc));
+      R.k[k] = ldg((const bf16x8*)(kc + (size_t)pos * DH + dc));
+      R.v[k] = ldg((const bf16x8*)(vc + (size_t)pos * DH + dc));
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        k0[e] = (bf16)0.0f;
-        v0[e] = (bf16)0.0f;
+        R.k[k][e] = (bf16)0.0f;
+        R.v[k][e] = (bf16)0.0f;
       }
     }
-    *(bf16x8*)&Ks[j * Gm::KST + dc] = k0;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) Vt[(dc + e) * Gm::VST + j] = v0[e];
   }
 }
 
-// Tree attention phase: unit (head, split) per workgroup; split s of a head
-// covers positions [s T / S, (s + 1) T / S) rounded down to 16, T = prefix_len
-// + n.  Node i attends to the prefix and to the cache slots of its
+// Registers -> one LDS chunk buffer: K row-major, V transposed.
+template <int DH>
+__device__ __forceinline__ void attn_store(char* buf, const AttnChunkRegs<DH>& R) {
+  using Gm = AttnGeom<DH>;
+  char* Ks = buf;
+  char* Vt = buf + Gm::KS_BYTES;
+#pragma unroll
+  for (int k = 0; k < AttnChunkRegs<DH>::IT; ++k) {
+    const int idx = threadIdx.x + k * kThreads;
+    const int j = idx / (DH / 8), dc = (idx % (DH / 8)) * 8;
+    lds_st<bf16x8>(Ks + ((size_t)j * Gm::KST + dc) * 2, R.k[k]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) lds_st<bf16>(Vt + ((size_t)(dc + e) * Gm::VST + j) * 2, R.v[k][e]);
+  }
+}
+
+// Key positions of split s of S: with one split, all T = prefix_len + n
+// positions; otherwise the first S - 1 splits share the prefix (cut at
+// multiples of 16) and the last one takes the tree's own n positions.  The
+// prefix splits read only cache slots this pass does not write, so their
+// first LDS chunk can be staged before the phase's barrier; only the tree
+// split waits for the QKV phase's keys.
+__device__ __forceinline__ void attn_split_range(int s, int S, int P, int n, int& lo, int& hi) {
+  if (S == 1) {
+    lo = 0;
+    hi = P + n;
+  } else if (s == S - 1) {
+    lo = P;
+    hi = P + n;
+  } else {
+    lo = (s * P / (S - 1)) & ~15;
+    hi = s == S - 2 ? P : ((s + 1) * P / (S - 1)) & ~15;
+  }
+}
+
+// Tree attention phase: unit (head, split) per workgroup (split ranges
+// above).  Node i attends to the prefix and to the cache slots of its
 // ancestors-or-self (a 128-bit set per node).  Per unit: S^T = K q^T on the
-// matrix cores, online softmax in the log2 domain, O^T += V^T P^T with P split
-// into two bf16 halves (P never leaves registers: the S result's lane layout
-// is the PV product's k-slot order).  Then the head's splits join and each
-// merges its share of the rows.  MB: 16-row blocks of the pass.
+// matrix cores, online softmax in the log2 domain, O^T += V^T P^T with P
+// split into two bf16 halves (P never leaves registers: the S result's lane
+// layout is the PV product's k-slot order).  Each split stores its partial
+// result; the head's last split to arrive merges them all, in split order.
+// MB: 16-row blocks of the pass.
 template <int MB, int DH>
 __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& pin, int layer, int phase, char* lds,
                                                                      int* lds_flag) {
@@ -862,26 +880,28 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
   constexpr int RPW = MB > 4 ? 2 : 1;
   const int S = wave_uniform(p.attn_splits);
   const int units = wave_uniform(p.H) * S;
-  const int total = wave_uniform(p.prefix_len + p.n);
   const int wave = wave_index(), lane = threadIdx.x & 63, li = lane & 15, g = lane >> 4;
-  const int MBr = wave_uniform(p.Mp / 16);
   const size_t kv_layer = (size_t)p.H * p.cap * DH;
-  bf16* kcl = p.k_cache + (size_t)layer * kv_layer;
+  const bf16* kcl = p.k_cache + (size_t)layer * kv_layer;
   const bf16* vcl = p.v_cache + (size_t)layer * kv_layer;
   const bf16* qb = p.q + (size_t)layer * p.Mp * p.d;
-  bf16* Ks = reinterpret_cast<bf16*>(lds);
-  bf16* Vt = reinterpret_cast<bf16*>(lds + Gm::KS_BYTES);
+  bf16* obase = p.o + (size_t)layer * p.Mp * p.d;
+  const bf16* Ks = reinterpret_cast<const bf16*>(lds);
+  const bf16* Vt = reinterpret_cast<const bf16*>(lds + Gm::KS_BYTES);
 
-  // The first tile of the first unit is staged before the barrier when it
+  // The first chunk of the first unit is staged before the barrier when it
   // only holds prefix keys (which this pass does not write).
   int u = blockIdx.x;
   bool staged = false;
   if (u < units) {
     const int h = u / S, s = u % S;
-    const int lo = (s * total / S) & ~15, hi = s + 1 == S ? total : ((s + 1) * total / S) & ~15;
+    int lo, hi;
+    attn_split_range(s, S, p.prefix_len, p.n, lo, hi);
     const int hi0 = lo + CH < hi ? lo + CH : hi;
     if (lo < hi && hi0 <= p.prefix_len) {
-      attn_stage<DH>(lds, kcl + (size_t)h * p.cap * DH, vcl + (size_t)h * p.cap * DH, lo, lo, hi0);
+      AttnChunkRegs<DH> R;
+      attn_load<DH>(R, kcl + (size_t)h * p.cap * DH, vcl + (size_t)h * p.cap * DH, lo, lo, hi0);
+      attn_store<DH>(lds, R);
       staged = true;
     }
   }
@@ -891,8 +911,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
 
   for (; u < units; u += p.G) {
     const int h = u / S, s = u % S;
-    const int lo = (s * total / S) & ~15, hi = s + 1 == S ? total : ((s + 1) * total / S) & ~15;
-    bf16* kc = kcl + (size_t)h * p.cap * DH;
+    int lo, hi;
+    attn_split_range(s, S, p.prefix_len, p.n, lo, hi);
+    const bf16* kc = kcl + (size_t)h * p.cap * DH;
     const bf16* vc = vcl + (size_t)h * p.cap * DH;
     // Query fragments (B operand of S^T = K q^T): lane holds row 16 rb + li,
     // dims 32 ks + 8 g + e (queries were rotated by the QKV phase).
@@ -903,7 +924,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
       const int rb = wave + 4 * r;
-      const int row = 16 * (rb < MBr ? rb : 0) + li;
+      const int row = 16 * (rb < MB ? rb : 0) + li;
       const bf16* qrow = qb + (size_t)row * p.d + h * DH;
 #pragma unroll
       for (int ks = 0; ks < KSTEPS; ++ks) qf[r][ks] = ldg((const bf16x8*)(qrow + 32 * ks + 8 * g));
@@ -919,15 +940,17 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
     for (int p0 = lo; p0 < hi; p0 += CH) {
       const int hi_t = p0 + CH < hi ? p0 + CH : hi;
       if (!staged) {
-        __syncthreads();
-        attn_stage<DH>(lds, kc, vc, p0, p0, hi_t);
+        AttnChunkRegs<DH> R;
+        attn_load<DH>(R, kc, vc, p0, p0, hi_t);
+        lds_barrier();  // the previous chunk's readers are done
+        attn_store<DH>(lds, R);
       }
       staged = false;
-      __syncthreads();
+      lds_barrier();
 #pragma unroll
       for (int r = 0; r < RPW; ++r) {
         const int rb = wave + 4 * r;
-        if (rb >= MBr) continue;
+        if (rb >= MB) continue;
         for (int c0 = 0; c0 < CH && p0 + c0 < hi_t; c0 += 64) {  // 64 keys per softmax step
           f32x4 sc[4];
 #pragma unroll
@@ -935,7 +958,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
             sc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < KSTEPS; ++ks) {
-              const bf16x8 a = *(const bf16x8*)&Ks[(c0 + 16 * jb + li) * KST + 32 * ks + 8 * g];
+              const bf16x8 a = lds_ld<bf16x8>(&Ks[(c0 + 16 * jb + li) * KST + 32 * ks + 8 * g]);
               sc[jb] = mfma16x16x32(a, qf[r][ks], sc[jb]);
             }
           }
@@ -987,8 +1010,8 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
               const bf16* vrow = &Vt[(16 * db + li) * VST + c0 + 32 * t2 + 4 * g];
-              const bf16x4 lo4 = *(const bf16x4*)vrow;
-              const bf16x4 hi4 = *(const bf16x4*)(vrow + 16);
+              const bf16x4 lo4 = lds_ld<bf16x4>(vrow);
+              const bf16x4 hi4 = lds_ld<bf16x4>(vrow + 16);
               bf16x8 av;
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
@@ -1002,14 +1025,34 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
         }
       }
     }
-    // Per-split results, then join the head's splits and merge this split's
-    // share of the rows.
     const size_t head_base = (size_t)h * S * p.Mp;
+    if (S == 1) {  // the whole softmax is here: normalise and write the output
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+        const int rb = wave + 4 * r;
+        if (rb >= MB) continue;
+        const int row = 16 * rb + li;
+        const float inv = 1.0f / l_run[r];
+        if (row < p.n) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const int col = h * DH + 16 * db + 4 * g;
+            st_coherent_bf2(obase + frag_off(row, col, MB), oacc[r][db][0] * inv, oacc[r][db][1] * inv);
+            st_coherent_bf2(obase + frag_off(row, col + 2, MB), oacc[r][db][2] * inv, oacc[r][db][3] * inv);
+          }
+        }
+      }
+      trace_mark(sy, phase, 4);
+      trace_mark(sy, phase, 5);
+      lds_barrier();
+      continue;
+    }
+    // This split's partial result; the head's last split merges them all.
     const size_t split_base = head_base + (size_t)s * p.Mp;
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
       const int rb = wave + 4 * r;
-      if (rb >= MBr) continue;
+      if (rb >= MB) continue;
       const int row = 16 * rb + li;
       if (g == 0) st_coherent2(&p.attn_ml[(split_base + row) * 2], m_run[r], l_run[r]);
 #pragma unroll
@@ -1019,63 +1062,91 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
         st_coherent2(dst + 2, oacc[r][db][2], oacc[r][db][3]);
       }
     }
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (threadIdx.x == 0) atomic_add_dev(&p.head_cnt[h], 1);
     trace_mark(sy, phase, 4);
-    if (!wait_at_least(sy, &p.head_cnt[h], S * (layer + 1))) return false;
+    const bool last = arrive_last(&p.head_cnt[h], S, lds_flag);
     trace_mark(sy, phase, 5);
+    if (!last) continue;
 
-    const int r_lo = s * p.n / S, r_hi = (s + 1) * p.n / S;
-    const int nr = r_hi - r_lo;
+    // Merge: o = sum_s exp2(m_s - M) o_s / sum_s exp2(m_s - M) l_s.  The
+    // (m, l) pairs and the partial outputs of a batch of rows are all loaded
+    // before any is used, so a batch costs one round trip.
+    const int n = p.n;
     float (*wgt)[kMaxNodes] = reinterpret_cast<float (*)[kMaxNodes]>(lds);
     float (*lsum)[kMaxNodes] = wgt + kAttnMaxSplits;
-    for (int idx = threadIdx.x; idx < S * nr; idx += kThreads) {
-      const int ss = idx / nr, i = r_lo + idx % nr;
-      const float2 ml = ld_coherent2(&p.attn_ml[(head_base + (size_t)ss * p.Mp + i) * 2]);
-      wgt[ss][i] = ml.x;
-      lsum[ss][i] = ml.y;
+    constexpr int IB = 8, SB = 8;  // items x splits per thread per round trip
+    const int items = n * (DH / 2);
+    const bool one_rt = S <= SB && items <= IB * kThreads;
+    float2 pre[IB][SB];
+    if (one_rt) {  // issue the partial-output loads before the weights are known
+#pragma unroll
+      for (int k = 0; k < IB; ++k) {
+        const int idx = threadIdx.x + k * kThreads;
+        const int i = idx / (DH / 2), dd = 2 * (idx % (DH / 2));
+#pragma unroll
+        for (int j = 0; j < SB; ++j)
+          pre[k][j] = idx < items && j < S
+                          ? ld_coherent2(&p.attn_o[(head_base + (size_t)j * p.Mp + i) * DH + dd])
+                          : make_float2(0.0f, 0.0f);
+      }
     }
-    __syncthreads();
-    if (threadIdx.x < nr) {
-      const int i = r_lo + threadIdx.x;
+    for (int idx = threadIdx.x; idx < S * n; idx += kThreads) {
+      const int ss = idx / n, i = idx % n;
+      const float2 ml = ld_coherent2(&p.attn_ml[(head_base + (size_t)ss * p.Mp + i) * 2]);
+      lds_st<float>(&wgt[ss][i], ml.x);
+      lds_st<float>(&lsum[ss][i], ml.y);
+    }
+    lds_barrier();
+    if (threadIdx.x < n) {
+      const int i = threadIdx.x;
       float M = -INFINITY;
-      for (int ss = 0; ss < S; ++ss) M = fmaxf(M, wgt[ss][i]);
+      for (int ss = 0; ss < S; ++ss) M = fmaxf(M, lds_ld<float>(&wgt[ss][i]));
       float L = 0.0f;
       for (int ss = 0; ss < S; ++ss) {
-        const float w = exp2f(wgt[ss][i] - M);
-        wgt[ss][i] = w;
-        L += lsum[ss][i] * w;
+        const float w = exp2f(lds_ld<float>(&wgt[ss][i]) - M);
+        lds_st<float>(&wgt[ss][i], w);
+        L += lds_ld<float>(&lsum[ss][i]) * w;
       }
       const float inv = 1.0f / L;
-      for (int ss = 0; ss < S; ++ss) wgt[ss][i] *= inv;
+      for (int ss = 0; ss < S; ++ss) lds_st<float>(&wgt[ss][i], lds_ld<float>(&wgt[ss][i]) * inv);
     }
-    __syncthreads();
-    bf16* obase = p.o + (size_t)layer * p.Mp * p.d;
-    for (int idx = threadIdx.x; idx < nr * (DH / 2); idx += kThreads) {
-      const int i = r_lo + idx / (DH / 2), dd = 2 * (idx % (DH / 2));
-      float o0 = 0.0f, o1 = 0.0f;
-      int ss = 0;
-      for (; ss + 4 <= S; ss += 4) {
-        float2 v[4];
+    lds_barrier();
+    if (one_rt) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-          v[k] = ld_coherent2(&p.attn_o[(head_base + (size_t)(ss + k) * p.Mp + i) * DH + dd]);
+      for (int k = 0; k < IB; ++k) {
+        const int idx = threadIdx.x + k * kThreads;
+        if (idx < items) {
+          const int i = idx / (DH / 2), dd = 2 * (idx % (DH / 2));
+          float o0 = 0.0f, o1 = 0.0f;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          o0 += v[k].x * wgt[ss + k][i];
-          o1 += v[k].y * wgt[ss + k][i];
+          for (int j = 0; j < SB; ++j) {
+            const float w = j < S ? lds_ld<float>(&wgt[j][i]) : 0.0f;
+            o0 += pre[k][j].x * w;
+            o1 += pre[k][j].y * w;
+          }
+          st_coherent_bf2(obase + frag_off(i, h * DH + dd, MB), o0, o1);
         }
       }
-      for (; ss < S; ++ss) {
-        const float2 v = ld_coherent2(&p.attn_o[(head_base + (size_t)ss * p.Mp + i) * DH + dd]);
-        o0 += v.x * wgt[ss][i];
-        o1 += v.y * wgt[ss][i];
+    } else {
+      for (int idx = threadIdx.x; idx < items; idx += kThreads) {
+        const int i = idx / (DH / 2), dd = 2 * (idx % (DH / 2));
+        float o0 = 0.0f, o1 = 0.0f;
+        for (int s0 = 0; s0 < S; s0 += SB) {
+          float2 v[SB];
+#pragma unroll
+          for (int j = 0; j < SB; ++j)
+            v[j] = s0 + j < S ? ld_coherent2(&p.attn_o[(head_base + (size_t)(s0 + j) * p.Mp + i) * DH + dd])
+                              : make_float2(0.0f, 0.0f);
+#pragma unroll
+          for (int j = 0; j < SB; ++j) {
+            const float w = s0 + j < S ? lds_ld<float>(&wgt[s0 + j][i]) : 0.0f;
+            o0 += v[j].x * w;
+            o1 += v[j].y * w;
+          }
+        }
+        st_coherent_bf2(obase + frag_off(i, h * DH + dd, MB), o0, o1);
       }
-      st_coherent_bf2(obase + frag_off(i, h * DH + dd, MB), o0, o1);
     }
-    __syncthreads();
+    lds_barrier();
   }
   return true;
 }
@@ -1197,10 +1268,9 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
   if (ok) {  // LM head (final norm scale) + argmax + accept walk
     if (gemm_phase<MB, EPI_LOGITS>(p, STEP_LM, 0, phase, lds_raw, gl, &flag)) trace_mark(sy, phase, 2);
   }
-  // Leave the pass: the last workgroup out resets the barrier and join counters.
+  // Leave the pass: the last workgroup out resets the barrier counters.
   if (arrive_last(p.exit_cnt, p.G, &flag)) {
     if (threadIdx.x < kBarSlots) st_coherent(p.bar + threadIdx.x * kBarStride, 0);
-    for (int h = threadIdx.x; h < p.H; h += kThreads) st_coherent(&p.head_cnt[h], 0);
   }
 }
 
