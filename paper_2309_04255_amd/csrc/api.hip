@@ -184,14 +184,13 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.q = (bf16*)(ws + W.qs);
   p.o = (bf16*)(ws + W.os);
   p.h = (bf16*)(ws + W.hs);
-  // Splits per head: enough (head, split) units for the grid; the prefix
-  // splits hold at least 16 positions each.
-  int S = env_int("LLMCAD_ATTN_SPLITS", G / s.H);
-  if (S > kAttnMaxSplits) S = kAttnMaxSplits;
-  if (S > 1 + cdiv(a.prefix_len, 16)) S = 1 + cdiv(a.prefix_len, 16);
-  if (s.H * S > G) S = G / s.H;
-  if (S < 1) S = 1;
-  p.attn_splits = S;
+  // Key splits per (head, row block) of the attention: four (LLMCAD_ATTN_SPLITS
+  // asks for 1 to 4), at most one per prefix chunk, 1 without a prefix.
+  int KS = env_int("LLMCAD_ATTN_SPLITS", 4);
+  if (KS > kAttnMaxSplits) KS = kAttnMaxSplits;
+  if (KS > cdiv(a.prefix_len, kAttnChunk)) KS = cdiv(a.prefix_len, kAttnChunk);
+  if (KS < 1) KS = 1;
+  p.attn_splits = KS;
   p.attn_o = (float*)(ws + W.attn_o);
   p.attn_ml = (float*)(ws + W.attn_ml);
   p.head_cnt = (int*)(ws + W.head_counters());

@@ -67,10 +67,10 @@ struct PassParams {
   int* exit_cnt;
   int* status;
   int* bar;         // [kBarSlots][kBarStride]
-  float* attn_o;    // [H][S][Mp][Dh] per-split unnormalised outputs
-  float* attn_ml;   // [H][S][Mp][2]  per-split running max and sum
-  int attn_splits;  // S
-  int* head_cnt;    // [H] arrivals of the head's splits
+  float* attn_o;    // [H][MB][KS][16][Dh] key-split partial outputs (unnormalised)
+  float* attn_ml;   // [H][MB][KS][16][2]  their running max and sum
+  int attn_splits;  // KS, key splits per (head, row block): 1 to 4
+  int* head_cnt;    // [H][MB] arrivals of the key splits
   float* lm_val;    // [G][Mp] LM-head argmax per workgroup
   int* lm_idx;
   int* amax;        // [Mp]

@@ -17,7 +17,7 @@ constexpr int kStepK = 32;                     // inputs per k-step
 constexpr int kBlockBytes = kNB * kStepK * 2;  // 1 KiB
 constexpr int kMaxNodes = LLMCAD_MAX_NODES;
 constexpr int kAttnChunk = 128;     // key positions staged in LDS at once
-constexpr int kAttnMaxSplits = 32;  // position splits per head
+constexpr int kAttnMaxSplits = 4;   // key splits per (head, 16-row block)
 constexpr int kPassMaxGrid = 1024;  // workgroups of the pass
 constexpr int kBarSlots = 16;       // grid-barrier counters
 constexpr int kBarStride = 32;      // ints between barrier counters (128 bytes)
@@ -135,7 +135,7 @@ inline int step_ksteps(const Shape& s, int step) { return step == STEP_DOWN ? s.
 struct WorkspaceLayout {
   int Mp;
   int n_head_counters;
-  size_t counters;     // int32: heads [H] | lm | exit | status | spare
+  size_t counters;     // int32: (head, row block) [H][Mp/16] | lm | exit | status | spare
   size_t counters_bytes;
   size_t bar;          // int32 [kBarSlots][kBarStride] grid-barrier counters
   size_t scratch_out;  // int32 [128 + 2] path/len/next sink for prefill
@@ -152,8 +152,8 @@ struct WorkspaceLayout {
   size_t qs;           // bf16 [L][Mp][d]         queries after the rotary embedding
   size_t os;           // bf16 [L] x (Mp x d, fragment order)   attention output
   size_t hs;           // bf16 [L] x (Mp x Fp, fragment order)  SwiGLU product
-  size_t attn_o;       // fp32 [H][S][Mp][Dh]     per-split unnormalised attention outputs
-  size_t attn_ml;      // fp32 [H][S][Mp][2]      per-split running max and sum
+  size_t attn_o;       // fp32 [H][Mp/16][KS][16][Dh]  key-split partial attention outputs
+  size_t attn_ml;      // fp32 [H][Mp/16][KS][16][2]   their running max and sum
   size_t total;
   WorkspaceLayout(const Shape& s, int max_n, int G) {
     Mp = pass_rows(max_n);
@@ -163,7 +163,7 @@ struct WorkspaceLayout {
       o_ = align_up(o_ + bytes, 256);
       return at;
     };
-    n_head_counters = s.H;
+    n_head_counters = s.H * (Mp / 16);
     counters_bytes = (size_t)(n_head_counters + 4) * 4;
     counters = take(counters_bytes);
     bar = take((size_t)kBarSlots * kBarStride * 4);
@@ -181,8 +181,8 @@ struct WorkspaceLayout {
     qs = take((size_t)s.L * Mp * s.d * 2);
     os = take((size_t)s.L * Mp * s.d * 2);
     hs = take((size_t)s.L * Mp * s.Fp * 2);
-    attn_o = take((size_t)s.H * kAttnMaxSplits * Mp * s.Dh * 4);
-    attn_ml = take((size_t)s.H * kAttnMaxSplits * Mp * 2 * 4);
+    attn_o = take((size_t)s.H * Mp * kAttnMaxSplits * s.Dh * 4);
+    attn_ml = take((size_t)s.H * Mp * kAttnMaxSplits * 2 * 4);
     total = o_;
   }
   size_t head_counters() const { return counters; }

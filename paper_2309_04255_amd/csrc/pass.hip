@@ -158,9 +158,11 @@ __device__ __forceinline__ bool grid_wait(const Sync& s, int phase, int G) {
     }
     if (lane == 0) *s.lds_flag = ok;
   }
-  __syncthreads();
+  // (LDS-only barriers: the other waves may have weight loads in flight,
+  // which must not be drained here)
+  lds_barrier();
   const bool ok = *s.lds_flag != 0;
-  __syncthreads();
+  lds_barrier();
   return ok;
 }
 
@@ -181,15 +183,26 @@ struct GemmLds {
   int walk_len;
 };
 
-// LDS of a GEMM phase (dynamic shared memory):
-//   [0, 64 KiB)        the waves' partial tiles, fp32 [4][cw][MB][64 lanes][4]
-//   [64, 88 KiB)       epilogue inputs: per (block, row block) 1 KiB of the
-//                      residual stream (fp32 [16 rows][16]) or of the rotary
-//                      table (fp32 [16 rows][8 pairs][2]); then per block
-//                      1 KiB holding its 16 norm gains (bf16, first 32 bytes)
-constexpr int kTwOff = 0;
-constexpr int kEpiOff = 64 * 1024;
-constexpr int kGemmLdsBytes = 88 * 1024;
+// LDS of a GEMM tile of cw blocks (dynamic shared memory), in KiB:
+//   [0, 4 cw MB)                 the waves' partial tiles, fp32 [4][cw][MB][64 lanes][4]
+//   [4 cw MB, 5 cw MB + cw)      epilogue inputs: per (block, row block) 1 KiB
+//                                of the residual stream (fp32 [16 rows][16]) or
+//                                of the rotary table (fp32 [16 rows][8 pairs][2]);
+//                                then per block 1 KiB holding its 16 norm gains
+//                                (bf16, first 32 bytes)
+//   [5 cw MB + cw, 142)          the first weight stages of each wave, copied
+//                                before the phase's barrier
+constexpr int kGemmLdsBytes = 142 * 1024;
+__host__ __device__ constexpr int tw_off() { return 0; }
+__host__ __device__ constexpr int epi_off(int cw, int MB) { return 4 * cw * MB * 1024; }
+__host__ __device__ constexpr int wl_off(int cw, int MB) { return (5 * cw * MB + cw) * 1024; }
+
+// Direct global -> LDS copy of 16 bytes per lane: lane l's bytes land at
+// lds + 16 l.  `lds` must be the same in every lane.
+__device__ __forceinline__ void dma16(const void* src, char* lds) {
+  __builtin_amdgcn_global_load_lds((const LLMCAD_GLOBAL void*)src,
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
 
 // What one GEMM step reads and writes in a given layer.  The activations of
 // every step are fragment-order bf16 [Mp][K]: the attention output, the
@@ -339,8 +352,15 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   const f32x4* zero4 = (const f32x4*)p.zero + lane;
   bf16x8 bw[D][C];
   bf16x8 ba[D][MB];
-  auto load_w = [&](int slot, int i) {
-    const bool live = i < ns;
+  // The first P stages of the wave's weights are copied into LDS before the
+  // barrier (P a multiple of D, as many as fit); the register pipeline
+  // starts at stage P.
+  constexpr int WL_STAGES = (kGemmLdsBytes - wl_off(C, MB)) / (kWaves * C * 1024);
+  constexpr int PMAX = WL_STAGES / D * D;
+  const int P = wave_uniform(wait_phase >= 0 ? (ns / D * D < PMAX ? ns / D * D : PMAX) : 0);
+  char* wl = lds + wl_off(C, MB) + (size_t)wave * PMAX * C * 1024;
+  auto load_w = [&](int slot, int i, bool want) {  // stage i, or nothing (zero line)
+    const bool live = want && i < ns;
 #pragma unroll
     for (int c = 0; c < C; ++c) bw[slot][c] = ldg_nt(opaque(live ? wt + c * cstride + (size_t)(kWaves * i) * 64 : zero));
   };
@@ -354,48 +374,64 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   // stream and rotary table were written two or more phases ago; gains are
   // weights): per (block, row block) unit 16 B per lane, plus each block's
   // gains.  Loaded first, parked in LDS once they land.
-  constexpr int KU = (C * MB + kWaves - 1) / kWaves;
-  constexpr int KG = (C + kWaves - 1) / kWaves;
-  const bool resid = io.resid;
-  f32x4 sx[KU], sg[KG];
+  // Before the barrier, waves 1-3 start the weight stream: each its own
+  // register stages and LDS stages, wave 1 also wave 0's LDS stages.  Wave 0
+  // polls the barrier and issues no load before it has seen it (a poll
+  // waits for every older load of its wave).
+  const int ns0 = (ks + kWaves - 1) / kWaves;
+  const int P0 = wave_uniform(wait_phase >= 0 ? (ns0 / D * D < PMAX ? ns0 / D * D : PMAX) : 0);
+  if (wave != 0) {
+    if constexpr (PMAX > 0) {
+      for (int i = 0; i < P; ++i)
 #pragma unroll
-  for (int k = 0; k < KU; ++k) {
-    const int u = wave + kWaves * k, c = u / MB, rb = u % MB;
-    const int col0 = kNB * (nb0 + c);
-    const f32x4* src = zero4;
-    if (u < C * MB) {
+        for (int c = 0; c < C; ++c)
+          dma16(wt + c * cstride + (size_t)(kWaves * i) * 64, wl + (size_t)(i * C + c) * 1024);
+      if (wave == 1) {
+        const bf16x8* wt0 = wt - 64;
+        char* wl0 = lds + wl_off(C, MB);
+        for (int i = 0; i < P0; ++i)
+#pragma unroll
+          for (int c = 0; c < C; ++c)
+            dma16(wt0 + c * cstride + (size_t)(kWaves * i) * 64, wl0 + (size_t)(i * C + c) * 1024);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < D; ++u) load_w(u, P + u, true);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if (wait_phase >= 0) {
+    const Sync sy = make_sync(p, lds_flag);
+    trace_mark(sy, wait_phase, 0);
+    if (!grid_wait(sy, wait_phase, p.G)) return false;
+    trace_mark(sy, wait_phase, 1);
+  }
+  // Epilogue inputs (residual stream or rotary table, and the next norm's
+  // gains; written two or more phases ago), by wave 0: per (block, row
+  // block) unit 16 B per lane, then each block's gains.
+  if (wave == 0) {
+    constexpr int KU = C * MB;
+    const bool resid = io.resid;
+    f32x4 sx[KU], sg[C];
+#pragma unroll
+    for (int u = 0; u < KU; ++u) {
+      const int c = u / MB, rb = u % MB;
+      const int col0 = kNB * (nb0 + c);
+      const f32x4* src = zero4;
       if (resid) {  // residual rows 16 rb + l / 4, columns col0 + 4 (l % 4) .. + 3
         src = (const f32x4*)(io.x_in + (size_t)(16 * rb + (lane >> 2)) * p.d + col0 + 4 * (lane & 3));
       } else if (step == STEP_QKV && col0 < 2 * p.d) {  // (cos, sin) of pairs 8 t + 2 (l % 4), + 1
         const int t = (col0 % p.d % p.Dh) / kNB;
         src = (const f32x4*)(p.rope + ((size_t)(16 * rb + (lane >> 2)) * (p.Dh / 2) + 8 * t + 2 * (lane & 3)) * 2);
       }
+      sx[u] = ldg(opaque(src));
     }
-    sx[k] = ldg(opaque(src));
-  }
 #pragma unroll
-  for (int k = 0; k < KG; ++k) {
-    const int c = wave + kWaves * k;
-    sg[k] = ldg(opaque(resid && c < C ? (const f32x4*)(io.g_next + kNB * (nb0 + c) + 8 * (lane & 1)) : zero4));
-  }
+    for (int c = 0; c < C; ++c)
+      sg[c] = ldg(opaque(resid ? (const f32x4*)(io.g_next + kNB * (nb0 + c) + 8 * (lane & 1)) : zero4));
 #pragma unroll
-  for (int u = 0; u < D; ++u) load_w(u, u);
-  __builtin_amdgcn_sched_barrier(0);
+    for (int u = 0; u < KU; ++u) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)u * 1024 + lane * 16, sx[u]);
 #pragma unroll
-  for (int k = 0; k < KU; ++k) {
-    const int u = wave + kWaves * k;
-    if (u < C * MB) lds_st<f32x4>(lds + kEpiOff + (size_t)u * 1024 + lane * 16, sx[k]);
-  }
-#pragma unroll
-  for (int k = 0; k < KG; ++k) {
-    const int c = wave + kWaves * k;
-    if (c < C) lds_st<f32x4>(lds + kEpiOff + (size_t)(C * MB + c) * 1024 + lane * 16, sg[k]);
-  }
-  if (wait_phase >= 0) {
-    const Sync sy = make_sync(p, lds_flag);
-    trace_mark(sy, wait_phase, 0);
-    if (!grid_wait(sy, wait_phase, p.G)) return false;
-    trace_mark(sy, wait_phase, 1);
+    for (int c = 0; c < C; ++c) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)(C * MB + c) * 1024 + lane * 16, sg[c]);
   }
   // A norm step's sums of squares (written by the previous phase), held in
   // registers through the main loop: thread t takes rows 4 q .. 4 q + 3
@@ -414,6 +450,16 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   }
 #pragma unroll
   for (int u = 0; u < D; ++u) load_a(u, u);
+  // Every load so far has landed (the direct-to-LDS copies among them; from
+  // here on only register loads are in flight, so that the loop's waits can
+  // count them exactly), and wave 0's LDS stages, copied by wave 1, are
+  // visible to it.  Then wave 0's register stages.
+  __builtin_amdgcn_s_waitcnt(0);
+  lds_barrier();
+  if (wave == 0) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) load_w(u, P + u, true);
+  }
   __builtin_amdgcn_sched_barrier(0);
   if (wait_phase >= 0 && p.trace != nullptr && (int)blockIdx.x < kTraceWgs && threadIdx.x == 0)
     stg(p.trace + (size_t)blockIdx.x * pass_phases(p.L) * 8 + wait_phase * 8 + 3, (long long)wall_clock64());
@@ -423,18 +469,36 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
     for (int c = 0; c < C; ++c) acc[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int i = 0; i < ns; i += D) {
+  // Stages [0, P) from LDS (only activation loads in flight), then the
+  // register pipeline, whose first D stages came with the prologue.  (Steps
+  // past the end multiply zero lines: no guard, so the loops are
+  // straight-line code and every wait covers one stage.)
+  int i = 0;
+  for (; i < P; i += D) {
 #pragma unroll
     for (int u = 0; u < D; ++u) {
       __builtin_amdgcn_sched_barrier(0);
-      // (steps past the end multiply zero lines: no guard, so the loop is
-      // straight-line code and every wait covers one stage)
+      bf16x8 b[C];
+#pragma unroll
+      for (int c = 0; c < C; ++c) b[c] = lds_ld<bf16x8>(wl + (size_t)((i + u) * C + c) * 1024 + lane * 16);
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+        for (int c = 0; c < C; ++c) acc[rb][c] = mfma16x16x32(ba[u][rb], b[c], acc[rb][c]);
+      __builtin_amdgcn_sched_barrier(0);
+      load_a(u, i + u + D);
+    }
+  }
+  for (; i < ns; i += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
         for (int c = 0; c < C; ++c) acc[rb][c] = mfma16x16x32(ba[u][rb], bw[u][c], acc[rb][c]);
       __builtin_amdgcn_sched_barrier(0);
-      load_w(u, i + u + D);
+      load_w(u, i + u + D, true);
       load_a(u, i + u + D);
     }
   }
@@ -454,7 +518,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   for (int c = 0; c < C; ++c)
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb)
-      lds_st<f32x4>(lds + kTwOff + ((size_t)((wave * C + c) * MB + rb) * 64 + lane) * 16, acc[rb][c]);
+      lds_st<f32x4>(lds + tw_off() + ((size_t)((wave * C + c) * MB + rb) * 64 + lane) * 16, acc[rb][c]);
   __syncthreads();
   return true;
 }
@@ -526,16 +590,16 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
                                               int nb, GemmLds& gl) {
   const int lane = threadIdx.x & 63, j = lane & 15, q4 = lane >> 4;
   const int unit = c * MB + rb;
-  f32x4 s = lds_ld<f32x4>(lds + kTwOff + ((size_t)unit * 64 + lane) * 16);
+  f32x4 s = lds_ld<f32x4>(lds + tw_off() + ((size_t)unit * 64 + lane) * 16);
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) s += lds_ld<f32x4>(lds + kTwOff + ((size_t)(w * cw * MB + unit) * 64 + lane) * 16);
+  for (int w = 1; w < kWaves; ++w) s += lds_ld<f32x4>(lds + tw_off() + ((size_t)(w * cw * MB + unit) * 64 + lane) * 16);
   float v[4] = {s[0], s[1], s[2], s[3]};
   const int rr0 = 4 * q4;  // first row of this lane inside the row block
   if constexpr (EPI != EPI_RESID) {  // the norm's per-row scale
 #pragma unroll
     for (int i = 0; i < 4; ++i) v[i] *= gl.rstd[16 * rb + rr0 + i];
   }
-  const char* epi = lds + kEpiOff;
+  const char* epi = lds + epi_off(cw, MB);
   const int col = kNB * nb + j;
   if constexpr (EPI == EPI_QKV) {
     const int d = p.d, dh = p.Dh;
@@ -786,7 +850,7 @@ template <int DH>
 struct AttnGeom {
   static constexpr int CH = kAttnChunk;  // key positions per LDS tile
   static constexpr int KST = DH + 8;     // K row stride (bf16)
-  static constexpr int VST = CH + 8;     // V^T row stride (bf16)
+  static constexpr int VST = CH + 4;     // V^T row stride (bf16): 8 rows apart fall in 2 banks
   static constexpr int KS_BYTES = CH * KST * 2;
   static constexpr int VT_BYTES = DH * VST * 2;
   static constexpr int BYTES = KS_BYTES + VT_BYTES;
@@ -825,9 +889,11 @@ __device__ __forceinline__ void attn_load(AttnChunkRegs<DH>& R, const bf16* kc, 
   }
 }
 
-// Registers -> one LDS chunk buffer: K row-major, V transposed.
+// Registers -> one LDS chunk buffer: K row-major, V transposed; positions
+// [0, npos) of the chunk (the 64-key steps that read it must find finite
+// values: V enters the products even where the softmax weight is 0).
 template <int DH>
-__device__ __forceinline__ void attn_store(char* buf, const AttnChunkRegs<DH>& R) {
+__device__ __forceinline__ void attn_store(char* buf, const AttnChunkRegs<DH>& R, int npos = AttnGeom<DH>::CH) {
   using Gm = AttnGeom<DH>;
   char* Ks = buf;
   char* Vt = buf + Gm::KS_BYTES;
@@ -835,39 +901,29 @@ __device__ __forceinline__ void attn_store(char* buf, const AttnChunkRegs<DH>& R
   for (int k = 0; k < AttnChunkRegs<DH>::IT; ++k) {
     const int idx = threadIdx.x + k * kThreads;
     const int j = idx / (DH / 8), dc = (idx % (DH / 8)) * 8;
+    if (j >= npos) continue;
     lds_st<bf16x8>(Ks + ((size_t)j * Gm::KST + dc) * 2, R.k[k]);
 #pragma unroll
     for (int e = 0; e < 8; ++e) lds_st<bf16>(Vt + ((size_t)(dc + e) * Gm::VST + j) * 2, R.v[k][e]);
   }
 }
 
-// Key positions of split s of S: with one split, all T = prefix_len + n
-// positions; otherwise the first S - 1 splits share the prefix (cut at
-// multiples of 16) and the last one takes the tree's own n positions.  The
-// prefix splits read only cache slots this pass does not write, so their
-// first LDS chunk can be staged before the phase's barrier; only the tree
-// split waits for the QKV phase's keys.
-__device__ __forceinline__ void attn_split_range(int s, int S, int P, int n, int& lo, int& hi) {
-  if (S == 1) {
-    lo = 0;
-    hi = P + n;
-  } else if (s == S - 1) {
-    lo = P;
-    hi = P + n;
-  } else {
-    lo = (s * P / (S - 1)) & ~15;
-    hi = s == S - 2 ? P : ((s + 1) * P / (S - 1)) & ~15;
-  }
-}
-
-// Tree attention phase: unit (head, split) per workgroup (split ranges
-// above).  Node i attends to the prefix and to the cache slots of its
-// ancestors-or-self (a 128-bit set per node).  Per unit: S^T = K q^T on the
-// matrix cores, online softmax in the log2 domain, O^T += V^T P^T with P
-// split into two bf16 halves (P never leaves registers: the S result's lane
-// layout is the PV product's k-slot order).  Each split stores its partial
-// result; the head's last split to arrive merges them all, in split order.
-// MB: 16-row blocks of the pass.
+// Tree attention phase.  Unit (head, 16-row block, key split) per
+// workgroup; the KS key splits of a (head, row block) take contiguous runs
+// of the prefix's CH-position chunks, and the last one also the tree's own
+// positions.  Node i attends to the prefix and to the cache slots of its
+// ancestors-or-self (a 128-bit set per node).  A unit's keys go through LDS
+// two chunks at a time (a "pair": four 64-key steps, one per wave; the
+// waves' partial results are merged in LDS, in wave order).  Its first pair
+// of prefix chunks is staged before the phase's barrier (this pass does not
+// write the prefix), further prefix chunks are read once into L2 meanwhile,
+// and the tree's keys (written by the QKV phase) are loaded into registers as
+// soon as the barrier is passed.  Per step: S^T = K q^T on the matrix cores,
+// online softmax in the log2 domain, O^T += V^T P^T with P split into two
+// bf16 halves (P never leaves registers: the S result's lane layout is the
+// PV product's k-slot order).  With KS > 1 each split stores its partial
+// result and the last to arrive merges them, in split order.  MB: 16-row
+// blocks of the pass.
 template <int MB, int DH>
 __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& pin, int layer, int phase, char* lds,
                                                                      int* lds_flag) {
@@ -877,275 +933,257 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
   phase = wave_uniform(phase);
   using Gm = AttnGeom<DH>;
   constexpr int CH = Gm::CH, KSTEPS = DH / 32, DB = DH / 16, KST = Gm::KST, VST = Gm::VST;
-  constexpr int RPW = MB > 4 ? 2 : 1;
-  const int S = wave_uniform(p.attn_splits);
-  const int units = wave_uniform(p.H) * S;
+  const int KS = wave_uniform(p.attn_splits);
+  const int rbn = wave_uniform((p.n + 15) / 16);  // row blocks holding nodes
+  const int units = wave_uniform(p.H) * rbn * KS;
   const int wave = wave_index(), lane = threadIdx.x & 63, li = lane & 15, g = lane >> 4;
+  const int P = wave_uniform(p.prefix_len), n = wave_uniform(p.n);
+  const int npc = (P + CH - 1) / CH;  // prefix chunks; chunk npc is the tree's
   const size_t kv_layer = (size_t)p.H * p.cap * DH;
   const bf16* kcl = p.k_cache + (size_t)layer * kv_layer;
   const bf16* vcl = p.v_cache + (size_t)layer * kv_layer;
   const bf16* qb = p.q + (size_t)layer * p.Mp * p.d;
   bf16* obase = p.o + (size_t)layer * p.Mp * p.d;
-  const bf16* Ks = reinterpret_cast<const bf16*>(lds);
-  const bf16* Vt = reinterpret_cast<const bf16*>(lds + Gm::KS_BYTES);
+  char* buf[2] = {lds, lds + Gm::BYTES};
+  // chunk c: prefix positions [c CH, min((c + 1) CH, P)) for c < npc, the
+  // tree's [P, P + n) for c == npc
+  auto chunk_lo = [&](int c) { return c < npc ? c * CH : P; };
+  auto chunk_hi = [&](int c) { return c < npc ? ((c + 1) * CH < P ? (c + 1) * CH : P) : P + n; };
+  // the chunks of split ks: prefix chunks [c_lo, c_hi), then the tree's if ks is the last
+  auto split_chunks = [&](int ks, int& c_lo, int& c_hi, int& nch) {
+    c_lo = ks * npc / KS;
+    c_hi = (ks + 1) * npc / KS;
+    nch = c_hi - c_lo + (ks == KS - 1 ? 1 : 0);
+  };
+  auto list_chunk = [&](int c_lo, int c_hi, int j) { return c_lo + j < c_hi ? c_lo + j : npc; };
 
-  // The first chunk of the first unit is staged before the barrier when it
-  // only holds prefix keys (which this pass does not write).
   int u = blockIdx.x;
-  bool staged = false;
+  int staged = 0;  // list entries (bit j: entry j, j < 2) already in LDS
   if (u < units) {
-    const int h = u / S, s = u % S;
-    int lo, hi;
-    attn_split_range(s, S, p.prefix_len, p.n, lo, hi);
-    const int hi0 = lo + CH < hi ? lo + CH : hi;
-    if (lo < hi && hi0 <= p.prefix_len) {
-      AttnChunkRegs<DH> R;
-      attn_load<DH>(R, kcl + (size_t)h * p.cap * DH, vcl + (size_t)h * p.cap * DH, lo, lo, hi0);
-      attn_store<DH>(lds, R);
-      staged = true;
+    const int h = u / (rbn * KS), ks = u % KS;
+    const bf16* kc = kcl + (size_t)h * p.cap * DH;
+    const bf16* vc = vcl + (size_t)h * p.cap * DH;
+    int c_lo, c_hi, nch;
+    split_chunks(ks, c_lo, c_hi, nch);
+    AttnChunkRegs<DH> R;
+    for (int j = 0; j < 2 && c_lo + j < c_hi; ++j) {
+      const int c = c_lo + j;
+      attn_load<DH>(R, kc, vc, chunk_lo(c), chunk_lo(c), chunk_hi(c));
+      attn_store<DH>(buf[j], R);
+      staged |= 1 << j;
     }
+    // the rest of the split's prefix: read once so that it waits in L2
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    uint32_t sink = 0;
+    for (int c = c_lo + 2; c < c_hi; ++c) {
+      attn_load<DH>(R, kc, vc, chunk_lo(c), chunk_lo(c), chunk_hi(c));
+#pragma unroll
+      for (int k = 0; k < AttnChunkRegs<DH>::IT; ++k)
+        sink ^= __builtin_bit_cast(u32x4, R.k[k])[0] ^ __builtin_bit_cast(u32x4, R.v[k])[0];
+    }
+    // (a store the compiler cannot rule out keeps the reads; n >= 1 always)
+    if (p.n < 0) stg(p.lm_idx + blockIdx.x, (int)sink);
   }
   trace_mark(sy, phase, 0);
   if (!grid_wait(sy, phase, p.G)) return false;
   trace_mark(sy, phase, 1);
 
   for (; u < units; u += p.G) {
-    const int h = u / S, s = u % S;
-    int lo, hi;
-    attn_split_range(s, S, p.prefix_len, p.n, lo, hi);
+    const int h = u / (rbn * KS), rb = (u / KS) % rbn, ks = u % KS;
     const bf16* kc = kcl + (size_t)h * p.cap * DH;
     const bf16* vc = vcl + (size_t)h * p.cap * DH;
+    int c_lo, c_hi, nch;
+    split_chunks(ks, c_lo, c_hi, nch);
+    const bool has_tree = ks == KS - 1;
     // Query fragments (B operand of S^T = K q^T): lane holds row 16 rb + li,
     // dims 32 ks + 8 g + e (queries were rotated by the QKV phase).
-    bf16x8 qf[RPW][KSTEPS];
-    uint32_t anc[RPW][4];
-    float m_run[RPW], l_run[RPW];
-    f32x4 oacc[RPW][DB];
-#pragma unroll
-    for (int r = 0; r < RPW; ++r) {
-      const int rb = wave + 4 * r;
-      const int row = 16 * (rb < MB ? rb : 0) + li;
+    bf16x8 qf[KSTEPS];
+    uint32_t anc[4];
+    const int row = 16 * rb + li;
+    {
       const bf16* qrow = qb + (size_t)row * p.d + h * DH;
 #pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) qf[r][ks] = ldg((const bf16x8*)(qrow + 32 * ks + 8 * g));
+      for (int s2 = 0; s2 < KSTEPS; ++s2) qf[s2] = ldg((const bf16x8*)(qrow + 32 * s2 + 8 * g));
       const uint32_t* ap = (const uint32_t*)(p.tree + 512) + row * 4;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) anc[r][w] = ldg(ap + w);
-      m_run[r] = -INFINITY;
-      l_run[r] = 0.0f;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) oacc[r][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int w = 0; w < 4; ++w) anc[w] = ldg(ap + w);
     }
+    // the tree's keys (last split): loaded now, stored when their buffer is free
+    AttnChunkRegs<DH> RT;
+    attn_load<DH>(RT, kc, vc, P, P, has_tree ? P + n : P);
+    float m_run = -INFINITY, l_run = 0.0f;
+    f32x4 oacc[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) oacc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
     trace_mark(sy, phase, 3);
-    for (int p0 = lo; p0 < hi; p0 += CH) {
-      const int hi_t = p0 + CH < hi ? p0 + CH : hi;
-      if (!staged) {
-        AttnChunkRegs<DH> R;
-        attn_load<DH>(R, kc, vc, p0, p0, hi_t);
-        lds_barrier();  // the previous chunk's readers are done
-        attn_store<DH>(lds, R);
-      }
-      staged = false;
-      lds_barrier();
-#pragma unroll
-      for (int r = 0; r < RPW; ++r) {
-        const int rb = wave + 4 * r;
-        if (rb >= MB) continue;
-        for (int c0 = 0; c0 < CH && p0 + c0 < hi_t; c0 += 64) {  // 64 keys per softmax step
-          f32x4 sc[4];
-#pragma unroll
-          for (int jb = 0; jb < 4; ++jb) {
-            sc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < KSTEPS; ++ks) {
-              const bf16x8 a = lds_ld<bf16x8>(&Ks[(c0 + 16 * jb + li) * KST + 32 * ks + 8 * g]);
-              sc[jb] = mfma16x16x32(a, qf[r][ks], sc[jb]);
-            }
-          }
-          float mx = -INFINITY;
-#pragma unroll
-          for (int jb = 0; jb < 4; ++jb)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int pos = p0 + c0 + 16 * jb + 4 * g + e;
-              const int t = pos - p.prefix_len;
-              const bool vis = pos < hi_t && (pos < p.prefix_len ||
-                                              (t < p.n && ((anc[r][t >> 5] >> (t & 31)) & 1u)));
-              const float sv = vis ? sc[jb][e] * p.scale_log2 : -INFINITY;
-              sc[jb][e] = sv;
-              mx = fmaxf(mx, sv);
-            }
-          mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-          mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-          const float m_new = fmaxf(m_run[r], mx);
-          const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
-          const float alpha = exp2f(m_run[r] - m_use);
-          bf16 ph[4][4], pl[4][4];
-          float psum = 0.0f;
-#pragma unroll
-          for (int jb = 0; jb < 4; ++jb)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float pe = exp2f(sc[jb][e] - m_use);
-              ph[jb][e] = f2bf(pe);
-              pl[jb][e] = f2bf(pe - bf2f(ph[jb][e]));
-              psum += pe;
-            }
-          psum += __shfl_xor(psum, 16, kWave);
-          psum += __shfl_xor(psum, 32, kWave);
-          l_run[r] = l_run[r] * alpha + psum;
-          m_run[r] = m_new;
-#pragma unroll
-          for (int db = 0; db < DB; ++db) oacc[r][db] = oacc[r][db] * alpha;
-#pragma unroll
-          for (int t2 = 0; t2 < 2; ++t2) {
-            bf16x8 bph, bpl;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              bph[e] = ph[2 * t2][e];
-              bph[4 + e] = ph[2 * t2 + 1][e];
-              bpl[e] = pl[2 * t2][e];
-              bpl[4 + e] = pl[2 * t2 + 1][e];
-            }
-#pragma unroll
-            for (int db = 0; db < DB; ++db) {
-              const bf16* vrow = &Vt[(16 * db + li) * VST + c0 + 32 * t2 + 4 * g];
-              const bf16x4 lo4 = lds_ld<bf16x4>(vrow);
-              const bf16x4 hi4 = lds_ld<bf16x4>(vrow + 16);
-              bf16x8 av;
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                av[e] = lo4[e];
-                av[4 + e] = hi4[e];
-              }
-              oacc[r][db] = mfma16x16x32(av, bph, oacc[r][db]);
-              oacc[r][db] = mfma16x16x32(av, bpl, oacc[r][db]);
-            }
+    for (int j0 = 0; j0 < nch; j0 += 2) {  // a pair of list entries: buffers 0 and 1
+      const int have = j0 == 0 ? staged : 0;
+      const int need = (j0 + 1 < nch ? 3 : 1) & ~have;
+      if (need) {
+        lds_barrier();  // the previous pair's readers are done
+        for (int j = 0; j < 2; ++j) {
+          if (!((need >> j) & 1)) continue;
+          const int c = list_chunk(c_lo, c_hi, j0 + j);
+          if (c == npc) {
+            attn_store<DH>(buf[j], RT, (n + 63) & ~63);
+          } else {
+            AttnChunkRegs<DH> R;
+            attn_load<DH>(R, kc, vc, chunk_lo(c), chunk_lo(c), chunk_hi(c));
+            attn_store<DH>(buf[j], R);
           }
         }
       }
-    }
-    const size_t head_base = (size_t)h * S * p.Mp;
-    if (S == 1) {  // the whole softmax is here: normalise and write the output
+      lds_barrier();
+      // step w of the pair: entry j0 + w / 2, keys 64 (w % 2) .. + 63
+      const int jw = j0 + wave / 2;
+      const int c = list_chunk(c_lo, c_hi, jw < nch ? jw : 0);
+      const int p0 = chunk_lo(c), hi_t = jw < nch ? chunk_hi(c) : 0;
+      const int c0k = 64 * (wave & 1);
+      if (p0 + c0k < hi_t) {
+        const bf16* Ks = reinterpret_cast<const bf16*>(buf[wave / 2]);
+        const bf16* Vt = reinterpret_cast<const bf16*>(buf[wave / 2] + Gm::KS_BYTES);
+        f32x4 sc[4];
 #pragma unroll
-      for (int r = 0; r < RPW; ++r) {
-        const int rb = wave + 4 * r;
-        if (rb >= MB) continue;
-        const int row = 16 * rb + li;
-        const float inv = 1.0f / l_run[r];
-        if (row < p.n) {
+        for (int jb = 0; jb < 4; ++jb) {
+          sc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s2 = 0; s2 < KSTEPS; ++s2) {
+            const bf16x8 a = lds_ld<bf16x8>(&Ks[(c0k + 16 * jb + li) * KST + 32 * s2 + 8 * g]);
+            sc[jb] = mfma16x16x32(a, qf[s2], sc[jb]);
+          }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int pos = p0 + c0k + 16 * jb + 4 * g + e;
+            const int t = pos - P;
+            const bool vis = pos < hi_t && (pos < P || (t < n && ((anc[t >> 5] >> (t & 31)) & 1u)));
+            const float sv = vis ? sc[jb][e] * p.scale_log2 : -INFINITY;
+            sc[jb][e] = sv;
+            mx = fmaxf(mx, sv);
+          }
+        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        const float m_new = fmaxf(m_run, mx);
+        const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
+        const float alpha = exp2f(m_run - m_use);
+        bf16 ph[4][4], pl[4][4];
+        float psum = 0.0f;
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float pe = exp2f(sc[jb][e] - m_use);
+            ph[jb][e] = f2bf(pe);
+            pl[jb][e] = f2bf(pe - bf2f(ph[jb][e]));
+            psum += pe;
+          }
+        psum += __shfl_xor(psum, 16, kWave);
+        psum += __shfl_xor(psum, 32, kWave);
+        l_run = l_run * alpha + psum;
+        m_run = m_new;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) oacc[db] = oacc[db] * alpha;
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2) {
+          bf16x8 bph, bpl;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            bph[e] = ph[2 * t2][e];
+            bph[4 + e] = ph[2 * t2 + 1][e];
+            bpl[e] = pl[2 * t2][e];
+            bpl[4 + e] = pl[2 * t2 + 1][e];
+          }
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
-            const int col = h * DH + 16 * db + 4 * g;
-            st_coherent_bf2(obase + frag_off(row, col, MB), oacc[r][db][0] * inv, oacc[r][db][1] * inv);
-            st_coherent_bf2(obase + frag_off(row, col + 2, MB), oacc[r][db][2] * inv, oacc[r][db][3] * inv);
+            const bf16* vrow = &Vt[(16 * db + li) * VST + c0k + 32 * t2 + 4 * g];
+            const bf16x4 lo4 = lds_ld<bf16x4>(vrow);
+            const bf16x4 hi4 = lds_ld<bf16x4>(vrow + 16);
+            bf16x8 av;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              av[e] = lo4[e];
+              av[4 + e] = hi4[e];
+            }
+            oacc[db] = mfma16x16x32(av, bph, oacc[db]);
+            oacc[db] = mfma16x16x32(av, bpl, oacc[db]);
           }
         }
       }
-      trace_mark(sy, phase, 4);
-      trace_mark(sy, phase, 5);
-      lds_barrier();
-      continue;
     }
-    // This split's partial result; the head's last split merges them all.
-    const size_t split_base = head_base + (size_t)s * p.Mp;
-#pragma unroll
-    for (int r = 0; r < RPW; ++r) {
-      const int rb = wave + 4 * r;
-      if (rb >= MB) continue;
-      const int row = 16 * rb + li;
-      if (g == 0) st_coherent2(&p.attn_ml[(split_base + row) * 2], m_run[r], l_run[r]);
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        float* dst = &p.attn_o[(split_base + row) * DH + 16 * db + 4 * g];
-        st_coherent2(dst, oacc[r][db][0], oacc[r][db][1]);
-        st_coherent2(dst + 2, oacc[r][db][2], oacc[r][db][3]);
-      }
-    }
+    staged = 0;
     trace_mark(sy, phase, 4);
-    const bool last = arrive_last(&p.head_cnt[h], S, lds_flag);
-    trace_mark(sy, phase, 5);
-    if (!last) continue;
-
-    // Merge: o = sum_s exp2(m_s - M) o_s / sum_s exp2(m_s - M) l_s.  The
-    // (m, l) pairs and the partial outputs of a batch of rows are all loaded
-    // before any is used, so a batch costs one round trip.
-    const int n = p.n;
-    float (*wgt)[kMaxNodes] = reinterpret_cast<float (*)[kMaxNodes]>(lds);
-    float (*lsum)[kMaxNodes] = wgt + kAttnMaxSplits;
-    constexpr int IB = 8, SB = 8;  // items x splits per thread per round trip
-    const int items = n * (DH / 2);
-    const bool one_rt = S <= SB && items <= IB * kThreads;
-    float2 pre[IB][SB];
-    if (one_rt) {  // issue the partial-output loads before the weights are known
-#pragma unroll
-      for (int k = 0; k < IB; ++k) {
-        const int idx = threadIdx.x + k * kThreads;
-        const int i = idx / (DH / 2), dd = 2 * (idx % (DH / 2));
-#pragma unroll
-        for (int j = 0; j < SB; ++j)
-          pre[k][j] = idx < items && j < S
-                          ? ld_coherent2(&p.attn_o[(head_base + (size_t)j * p.Mp + i) * DH + dd])
-                          : make_float2(0.0f, 0.0f);
-      }
-    }
-    for (int idx = threadIdx.x; idx < S * n; idx += kThreads) {
-      const int ss = idx / n, i = idx % n;
-      const float2 ml = ld_coherent2(&p.attn_ml[(head_base + (size_t)ss * p.Mp + i) * 2]);
-      lds_st<float>(&wgt[ss][i], ml.x);
-      lds_st<float>(&lsum[ss][i], ml.y);
-    }
+    // The four waves' partial results -> LDS (the chunk buffers are free),
+    // merged in wave order: o = sum_w exp2(m_w - M) o_w / sum_w exp2(m_w - M) l_w
+    // (unnormalised when the key splits still have to be merged).
     lds_barrier();
-    if (threadIdx.x < n) {
-      const int i = threadIdx.x;
+    float* mlm = reinterpret_cast<float*>(lds);  // [4][16][2]
+    float* om = mlm + kWaves * 16 * 2;          // [4][16][DH]
+    if (g == 0) {
+      lds_st<float>(&mlm[(wave * 16 + li) * 2], m_run);
+      lds_st<float>(&mlm[(wave * 16 + li) * 2 + 1], l_run);
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db) lds_st<f32x4>(&om[(size_t)(wave * 16 + li) * DH + 16 * db + 4 * g], oacc[db]);
+    lds_barrier();
+    const size_t rbi = (size_t)h * MB + rb;  // (head, row block) slot
+    for (int it = threadIdx.x; it < 16 * (DH / 2); it += kThreads) {
+      const int i = it / (DH / 2), dd = 2 * (it % (DH / 2));
       float M = -INFINITY;
-      for (int ss = 0; ss < S; ++ss) M = fmaxf(M, lds_ld<float>(&wgt[ss][i]));
-      float L = 0.0f;
-      for (int ss = 0; ss < S; ++ss) {
-        const float w = exp2f(lds_ld<float>(&wgt[ss][i]) - M);
-        lds_st<float>(&wgt[ss][i], w);
-        L += lds_ld<float>(&lsum[ss][i]) * w;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) M = fmaxf(M, lds_ld<float>(&mlm[(w * 16 + i) * 2]));
+      float L = 0.0f, o0 = 0.0f, o1 = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float m = lds_ld<float>(&mlm[(w * 16 + i) * 2]);
+        const float wt = m == -INFINITY ? 0.0f : exp2f(m - M);
+        L += lds_ld<float>(&mlm[(w * 16 + i) * 2 + 1]) * wt;
+        const float2 ov = lds_ld<float2>(&om[(size_t)(w * 16 + i) * DH + dd]);
+        o0 += ov.x * wt;
+        o1 += ov.y * wt;
       }
-      const float inv = 1.0f / L;
-      for (int ss = 0; ss < S; ++ss) lds_st<float>(&wgt[ss][i], lds_ld<float>(&wgt[ss][i]) * inv);
-    }
-    lds_barrier();
-    if (one_rt) {
-#pragma unroll
-      for (int k = 0; k < IB; ++k) {
-        const int idx = threadIdx.x + k * kThreads;
-        if (idx < items) {
-          const int i = idx / (DH / 2), dd = 2 * (idx % (DH / 2));
-          float o0 = 0.0f, o1 = 0.0f;
-#pragma unroll
-          for (int j = 0; j < SB; ++j) {
-            const float w = j < S ? lds_ld<float>(&wgt[j][i]) : 0.0f;
-            o0 += pre[k][j].x * w;
-            o1 += pre[k][j].y * w;
-          }
-          st_coherent_bf2(obase + frag_off(i, h * DH + dd, MB), o0, o1);
-        }
-      }
-    } else {
-      for (int idx = threadIdx.x; idx < items; idx += kThreads) {
-        const int i = idx / (DH / 2), dd = 2 * (idx % (DH / 2));
-        float o0 = 0.0f, o1 = 0.0f;
-        for (int s0 = 0; s0 < S; s0 += SB) {
-          float2 v[SB];
-#pragma unroll
-          for (int j = 0; j < SB; ++j)
-            v[j] = s0 + j < S ? ld_coherent2(&p.attn_o[(head_base + (size_t)(s0 + j) * p.Mp + i) * DH + dd])
-                              : make_float2(0.0f, 0.0f);
-#pragma unroll
-          for (int j = 0; j < SB; ++j) {
-            const float w = s0 + j < S ? lds_ld<float>(&wgt[s0 + j][i]) : 0.0f;
-            o0 += v[j].x * w;
-            o1 += v[j].y * w;
-          }
-        }
-        st_coherent_bf2(obase + frag_off(i, h * DH + dd, MB), o0, o1);
+      if (KS == 1) {
+        const int r = 16 * rb + i;
+        const float inv = 1.0f / L;
+        if (r < n) st_coherent_bf2(obase + frag_off(r, h * DH + dd, MB), o0 * inv, o1 * inv);
+      } else {
+        const size_t sl = rbi * KS + ks;  // this split's partial slot
+        st_coherent2(&p.attn_o[(sl * 16 + i) * DH + dd], o0, o1);
+        if (dd == 0) st_coherent2(&p.attn_ml[(sl * 16 + i) * 2], M, L);
       }
     }
+    if (KS > 1 && arrive_last(&p.head_cnt[rbi], KS, lds_flag)) {
+      // Merge the key splits, in split order; every load of a row issued
+      // before any is used.
+      for (int it = threadIdx.x; it < 16 * (DH / 2); it += kThreads) {
+        const int i = it / (DH / 2), dd = 2 * (it % (DH / 2));
+        const int r = 16 * rb + i;
+        constexpr int SB = 4;  // (KS <= 4)
+        float2 ml[SB], ov[SB];
+#pragma unroll
+        for (int s2 = 0; s2 < SB; ++s2) {
+          const size_t sl = rbi * KS + s2;
+          ml[s2] = s2 < KS ? ld_coherent2(&p.attn_ml[(sl * 16 + i) * 2]) : make_float2(-INFINITY, 0.0f);
+          ov[s2] = s2 < KS ? ld_coherent2(&p.attn_o[(sl * 16 + i) * DH + dd]) : make_float2(0.0f, 0.0f);
+        }
+        float M = -INFINITY;
+#pragma unroll
+        for (int s2 = 0; s2 < SB; ++s2) M = fmaxf(M, ml[s2].x);
+        float L = 0.0f, o0 = 0.0f, o1 = 0.0f;
+#pragma unroll
+        for (int s2 = 0; s2 < SB; ++s2) {
+          const float wt = ml[s2].x == -INFINITY ? 0.0f : exp2f(ml[s2].x - M);
+          L += ml[s2].y * wt;
+          o0 += ov[s2].x * wt;
+          o1 += ov[s2].y * wt;
+        }
+        const float inv = 1.0f / L;
+        if (r < n) st_coherent_bf2(obase + frag_off(r, h * DH + dd, MB), o0 * inv, o1 * inv);
+      }
+    }
+    trace_mark(sy, phase, 5);
     lds_barrier();
   }
   return true;
@@ -1215,11 +1253,9 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
 
 template <int DH>
 constexpr size_t dyn_lds_bytes() {
-  constexpr size_t attn = AttnGeom<DH>::BYTES;
-  constexpr size_t merge = 2 * kAttnMaxSplits * kMaxNodes * 4;
-  constexpr size_t gemm = kGemmLdsBytes;
-  constexpr size_t m1 = attn > merge ? attn : merge;
-  return m1 > gemm ? m1 : gemm;
+  constexpr size_t attn = 2 * AttnGeom<DH>::BYTES;  // two chunk buffers
+  constexpr size_t gemm = kGemmLdsBytes;              // (all LDS but the static part)
+  return attn > gemm ? attn : gemm;
 }
 
 template <int MB, int DH>

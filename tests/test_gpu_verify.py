@@ -102,21 +102,56 @@ def test_verify_matches_oracle(model, tree):
 
 
 def test_launch_shape_variants(model, monkeypatch):
-    # One attention split per head (its softmax spans several 128-key
-    # chunks), three splits, and smaller grids (each workgroup then takes
-    # longer runs of column blocks, cut into several tiles, and with 3
-    # workgroups the attention units take several rounds) meet the oracle
-    # bar too.
+    # One and four key splits in the attention, and smaller grids (each
+    # workgroup then takes longer runs of column blocks, cut into several
+    # tiles, and with 3 workgroups the attention units take several rounds)
+    # meet the oracle bar too.
     parent = TREES["b432_n41"]
     tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=7)
     _check_all(model, parent, tok, "default")
-    for env in ({"LLMCAD_ATTN_SPLITS": "1"}, {"LLMCAD_ATTN_SPLITS": "3"},
+    for env in ({"LLMCAD_ATTN_SPLITS": "1"}, {"LLMCAD_ATTN_SPLITS": "4"},
                 {"LLMCAD_PASS_GRID": "200"}, {"LLMCAD_PASS_GRID": "24"}, {"LLMCAD_PASS_GRID": "3"}):
         for k, v in env.items():
             monkeypatch.setenv(k, v)
         _check_all(model, parent, tok, str(env))
         for k in env:
             monkeypatch.delenv(k)
+
+
+@pytest.mark.parametrize("splits", ["default", "1", "2", "3", "4"])
+def test_long_prefix_key_splits(model, monkeypatch, splits):
+    # A 600-position prefix (four full 128-key chunks and a ragged fifth):
+    # the attention's key splits (1 to 4 per head and row block, merged in
+    # split order) all meet the oracle bar.  The prefix K/V are seeded random
+    # bf16 values written straight into the cache and handed to the oracle.
+    PL = 600
+    shape, binding = model.shape, model.binding
+    sess = binding.Session(shape, capacity=PL + 160, max_n=128)
+    binding.workspace_init(sess.cfg, 128, sess.workspace)
+    sess.load_weights(model.gen)
+    rng = np.random.default_rng(0x10AD)
+    dims = (shape.n_layers, PL, shape.n_heads, shape.head_dim)
+    pk = oracle.bf16_round(rng.standard_normal(dims) * 0.7)
+    pv = oracle.bf16_round(rng.standard_normal(dims) * 0.7)
+    sess.k_cache[:, :, :PL] = torch.from_numpy(pk.transpose(0, 2, 1, 3).astype(np.float32)).to(torch.bfloat16).cuda()
+    sess.v_cache[:, :, :PL] = torch.from_numpy(pv.transpose(0, 2, 1, 3).astype(np.float32)).to(torch.bfloat16).cuda()
+    if splits != "default":
+        monkeypatch.setenv("LLMCAD_ATTN_SPLITS", splits)
+    parent = TREES["b432_n41"]
+    n = len(parent)
+    tok = workloads.draw_tokens(n, shape.vocab, seed=23)
+    sess.verify_tree(PL, tok, parent)
+    logits, path, acc, nxt = sess.results(n)
+    logits = logits.numpy()
+    ref, _, _ = oracle.tree_forward(model.ow, pk, pv, tok, parent, rounding=True)
+    what = f"{shape.name}/P{PL}/splits={splits}"
+    err, rel = parity.check_logits(logits, ref, what)
+    off, _ = binding.workspace_region(sess.cfg, n, 4)
+    amax = sess.workspace[off:off + 4 * n].view(torch.int32).cpu().numpy()
+    np.testing.assert_array_equal(amax, np.argmax(logits, axis=1))
+    parity.check_argmax(amax, ref, what)
+    parity.check_walk(parent, tok, amax, path, acc, nxt, ref, what)
+    print(f"[{what}] max_abs={err:.2e} rel={rel:.2e}", flush=True)
 
 
 def test_pass_status_ok(model):
