@@ -70,6 +70,51 @@ def load_traffic(workload):
     return t.get("bytes_per_launch")
 
 
+def write_traffic(fetch_csv, write_csv, workload, copy_mib):
+    """From two rocprofv3 --pmc runs of `bench.py --calibration-copy-mib N`
+    (one collecting FETCH_SIZE, one WRITE_SIZE; per dispatch, in KiB), the
+    pass kernel's HBM bytes per launch.  Calibration: the N MiB fill that
+    precedes the copy writes a known size (write factor), and the copy's
+    chunks read as much as they write (read factor).  Writes TRAFFIC_FILE
+    tagged with the kernel sources' hash."""
+    import csv
+
+    def per_kernel(path):
+        vals = {}
+        with open(path, newline="") as f:
+            for row in csv.DictReader(f):
+                vals.setdefault(row["Kernel_Name"], []).append(float(row["Counter_Value"]))
+        return vals
+
+    fetch, write = per_kernel(fetch_csv), per_kernel(write_csv)
+    copy = "__amd_rocclr_copyBuffer"
+    fill = [k for k in write if "FillFunctor<float>" in k]
+    if copy not in fetch or copy not in write or not fill:
+        raise SystemExit(f"calibration kernels not found: {sorted(write)}")
+    fill_kib = max(write[fill[0]])
+    write_factor = copy_mib * 1024.0 / fill_kib
+    chunk_fetch = statistics.median(v for v in fetch[copy] if v > 4096)
+    chunk_write = statistics.median(v for v in write[copy] if v > 4096)
+    read_factor = chunk_write * write_factor / chunk_fetch
+    # (the prefill's passes run another instance of the pass kernel, for
+    # 128-row chunks; the verification passes are the most frequent one)
+    passk = max((k for k in fetch if "pass_kernel" in k), key=lambda k: len(fetch[k]))
+    f_kib, w_kib = statistics.mean(fetch[passk]), statistics.mean(write[passk])
+    out = {
+        "workload": workload, "kernel_sources_sha256_16": source_hash(), "kernel": passk[:90],
+        "launches": len(fetch[passk]), "fetch_kib_mean": round(f_kib), "write_kib_mean": round(w_kib),
+        "calibration": {"fill_mib": copy_mib, "fill_write_kib": fill_kib, "write_factor": round(write_factor, 4),
+                        "copy_chunk_fetch_kib": chunk_fetch, "copy_chunk_write_kib": chunk_write,
+                        "read_factor": round(read_factor, 4)},
+        "read_bytes": round(f_kib * 1024 * read_factor), "write_bytes": round(w_kib * 1024 * write_factor),
+    }
+    out["bytes_per_launch"] = out["read_bytes"] + out["write_bytes"]
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out, indent=1))
+
+
 def cpu_baseline(shape, P, n, seed):
     """Time the CPU oracle on a bounded sample: tree_forward with 1 and 2 of the
     model's layers (+ embedding and LM head); one pass = t1 + (L-1)(t2 - t1)."""
@@ -137,7 +182,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama7b_p512_n31")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibration-copy-mib", type=int, default=0,
+                    help="(profiling) first copy this many MiB three times: the counter calibration")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the traffic file from two rocprofv3 --pmc counter CSVs and exit")
     args = ap.parse_args()
+    if args.write_traffic:
+        write_traffic(args.write_traffic[0], args.write_traffic[1], args.workload,
+                      args.calibration_copy_mib or 1024)
+        return
     if args.gpus != 1:
         print("bench.py measures a single GPU: this build has no multi-GPU path "
               "(run with --gpus 1).", file=sys.stderr)
@@ -176,6 +229,14 @@ def main():
     def one_pass():
         binding.verify_tree(sess.cfg, sess.packed, sess.k_cache, sess.v_cache, P, tok, parent,
                             sess.logits, sess.path, sess.accept_len, sess.next_token, sess.workspace)
+
+    if args.calibration_copy_mib > 0:
+        src = torch.ones(args.calibration_copy_mib << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         one_pass()

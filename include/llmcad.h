@@ -36,7 +36,7 @@
  *                 w_gate_up [2F][d] (rows gate, then up), w_down [d][F]
  *  - Packed weights: an opaque device image of llmcad_packed_bytes() bytes
  *    written by llmcad_pack_globals / llmcad_pack_layer (MFMA-fragment order:
- *    1 KiB contiguous per 32 output columns x 16 inputs, consecutive inputs
+ *    1 KiB contiguous per 16 output columns x 32 inputs, consecutive inputs
  *    consecutive).  The globals sit
  *    first, then layer 0, 1, ...; an image packed for L layers also serves a
  *    configuration with fewer layers.
@@ -162,10 +162,13 @@ int llmcad_prefill(const llmcad_config* cfg, const void* packed, void* k_cache, 
 const char* llmcad_status_string(int status);
 
 /* Byte offset and size of a named intermediate buffer inside a workspace
- * sized for max_n (for diagnostics): 0 final residual stream fp32 [Mp][d],
- * 1 layer 0's queries after the rotary embedding bf16 [Mp][d], 2 layer
- * 0's attention output bf16 [Mp][d], 3 layer 0's SwiGLU product bf16
- * [Mp][Fp], 4 per-node greedy token int32 [Mp],
+ * sized for max_n (for diagnostics).  "Fragment order" stores a bf16 [Mp][K]
+ * matrix as 1 KiB blocks, block (k-step s, row block b) at (s Mp/16 + b) KiB,
+ * its 16-byte lane l holding row 16 b + l % 16, columns 32 s + 8 (l / 16) ..
+ * + 7.  0 final residual stream fp32 [Mp][d], 1 layer 0's queries after the
+ * rotary embedding bf16 [Mp][d], 2 layer 0's attention output bf16 [Mp][d]
+ * in fragment order, 3 layer 0's SwiGLU product bf16 [Mp][Fp] in fragment
+ * order, 4 per-node greedy token int32 [Mp],
  * 5 pass status int32 (0 = ok; 1 = a grid wait of the single-launch pass ran
  * out of its bounded spin: the pass's outputs are invalid, and the workspace
  * must be cleared with llmcad_workspace_init before the next pass; 3 = the
@@ -173,12 +176,13 @@ const char* llmcad_status_string(int status);
  * nothing),
  * 6 phase timestamps int64 [8][3 + 5L][8] (written when the environment
  * variable LLMCAD_TRACE is 1), 7 every residual stream version fp32
- * [2L+1][Mp][d], 8 their per-32-column sums of squares fp32 [2L+1][d/32][Mp],
+ * [2L+1][Mp][d], 8 their per-16-column sums of squares fp32 [2L+1][d/16][Mp],
  * 9 every layer's queries bf16 [L][Mp][d], 10 attention outputs bf16
- * [L][Mp][d], 11 SwiGLU products bf16 [L][Mp][Fp], 12 every residual
- * stream version times the gain of the RMSNorm that reads it, bf16
- * [2L+1][Mp][d] (the input of the QKV, gate/up and LM-head products);
- * Mp = max_n rounded up to 32, 64 or 128, Fp = F rounded up to 16.  Offsets describe a
+ * [L] x [Mp][d] in fragment order, 11 SwiGLU products bf16 [L] x [Mp][Fp]
+ * in fragment order, 12 every residual stream version times the gain of the
+ * RMSNorm that reads it, bf16 [2L+1] x [Mp][d] in fragment order (the input
+ * of the QKV, gate/up and LM-head products);
+ * Mp = max_n rounded up to 16, 32, 64 or 128, Fp = F rounded up to 32.  Offsets describe a
  * pass over max_n nodes (call with max_n = that pass's n). */
 int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t which, size_t* offset,
                             size_t* bytes);
