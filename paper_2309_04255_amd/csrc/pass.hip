@@ -338,7 +338,13 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   const int wave = wave_index(), lane = threadIdx.x & 63;
   const int ks = io.ks;
   const int ns = wave_uniform(wave < ks ? (ks - wave + kWaves - 1) / kWaves : 0);
-  constexpr int D = tile_depth<MB, C>();
+  // Pipeline depth: about 160 VGPRs of stages, but no deeper than the LDS
+  // stages that fit, so that wide tiles still get some (the LDS phase
+  // advances D stages at a time); at C >= 5 a few stages of C KiB are plenty
+  // in flight.
+  constexpr int WL_STAGES = (kGemmLdsBytes - wl_off(C, MB)) / (kWaves * C * 1024);
+  constexpr int D0 = tile_depth<MB, C>();
+  constexpr int D = WL_STAGES >= 2 && WL_STAGES < D0 ? WL_STAGES : D0;
   // this wave's k-steps: wave + 4 i
   const bf16x8* wt = io.w + ((size_t)nb0 * ks + wave) * 64 + lane;
   const size_t cstride = (size_t)ks * 64;
@@ -355,7 +361,6 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   // The first P stages of the wave's weights are copied into LDS before the
   // barrier (P a multiple of D, as many as fit); the register pipeline
   // starts at stage P.
-  constexpr int WL_STAGES = (kGemmLdsBytes - wl_off(C, MB)) / (kWaves * C * 1024);
   constexpr int PMAX = WL_STAGES / D * D;
   const int P = wave_uniform(wait_phase >= 0 ? (ns / D * D < PMAX ? ns / D * D : PMAX) : 0);
   char* wl = lds + wl_off(C, MB) + (size_t)wave * PMAX * C * 1024;
