@@ -174,16 +174,19 @@ const char* llmcad_status_string(int status);
  * must be cleared with llmcad_workspace_init before the next pass; 3 = the
  * kernel did not find its parameter block where it reads it, and did
  * nothing),
- * 6 phase timestamps int64 [8][3 + 5L][8] (written when the environment
+ * 6 phase timestamps int64 [G][3 + 5L][8], G the pass's workgroups (written when the environment
  * variable LLMCAD_TRACE is 1), 7 every residual stream version fp32
  * [2L+1][Mp][d], 8 their per-16-column sums of squares fp32 [2L+1][d/16][Mp],
  * 9 every layer's queries bf16 [L][Mp][d], 10 attention outputs bf16
  * [L] x [Mp][d] in fragment order, 11 SwiGLU products bf16 [L] x [Mp][Fp]
  * in fragment order, 12 every residual stream version times the gain of the
  * RMSNorm that reads it, bf16 [2L+1] x [Mp][d] in fragment order (the input
- * of the QKV, gate/up and LM-head products);
+ * of the QKV, gate/up and LM-head products), 13 the line of zeros that the
+ * kernels read in place of absent inputs (cleared by llmcad_workspace_init);
  * Mp = max_n rounded up to 16, 32, 64 or 128, Fp = F rounded up to 32.  Offsets describe a
- * pass over max_n nodes (call with max_n = that pass's n). */
+ * pass over max_n nodes (call with max_n = that pass's n); those of regions 5
+ * and 13, which hold state from one pass to the next, depend on neither the
+ * node count nor the pass's grid. */
 int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t which, size_t* offset,
                             size_t* bytes);
 

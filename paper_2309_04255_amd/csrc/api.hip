@@ -207,6 +207,7 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.accept_len = a.accept_len;
   p.next_token = a.next_token;
   p.spin_limit = env_int("LLMCAD_SPIN_LIMIT", 4000000);
+  p.wl_cap = env_int("LLMCAD_WL_STAGES", 1 << 20);  // (diagnostics: a smaller pre-barrier copy)
   p.trace = env_int("LLMCAD_TRACE", 0) ? (long long*)(ws + W.trace) : nullptr;
   TimedLaunch tl(LLMCAD_KERNEL_PASS, a.st);
   HIP_TRY(launch_pass(MB, p, tree, a.st));
@@ -446,13 +447,14 @@ int llmcad_workspace_region(const llmcad_config* cfg, int32_t max_n, int32_t whi
     case 3: *offset = W.hs; *bytes = (size_t)W.Mp * s.Fp * 2; break;
     case 4: *offset = W.amax; *bytes = (size_t)W.Mp * 4; break;
     case 5: *offset = W.status(); *bytes = 4; break;
-    case 6: *offset = W.trace; *bytes = (size_t)8 * pass_phases(s.L) * 8 * 8; break;
+    case 6: *offset = W.trace; *bytes = (size_t)pass_grid() * pass_phases(s.L) * 8 * 8; break;
     case 7: *offset = W.xs; *bytes = (size_t)(2 * s.L + 1) * W.Mp * s.d * 4; break;
     case 8: *offset = W.ssqs; *bytes = (size_t)(2 * s.L + 1) * s.d_nb * W.Mp * 4; break;
     case 9: *offset = W.qs; *bytes = (size_t)s.L * W.Mp * s.d * 2; break;
     case 10: *offset = W.os; *bytes = (size_t)s.L * W.Mp * s.d * 2; break;
     case 11: *offset = W.hs; *bytes = (size_t)s.L * W.Mp * s.Fp * 2; break;
     case 12: *offset = W.xgs; *bytes = (size_t)(2 * s.L + 1) * W.Mp * s.d * 2; break;
+    case 13: *offset = W.zero; *bytes = kZeroBytes; break;
     default: return LLMCAD_EARG;
   }
   return LLMCAD_OK;

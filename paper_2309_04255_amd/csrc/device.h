@@ -149,6 +149,16 @@ __device__ __forceinline__ int atomic_add_dev(int* p, int v) {
   return __hip_atomic_fetch_add((LLMCAD_GLOBAL int*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Counts this workgroup's arrival on `counter` once its stores above have
+// completed (the waiting side uses join_wait).  Must be called by all
+// threads of the workgroup.
+__device__ __forceinline__ void arrive_count(int* counter) {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) atomic_add_dev(counter, 1);
+}
+
 // Counts this workgroup's arrival on `counter`; returns true (to every
 // thread) in the last of `expected` arriving workgroups, which also resets
 // the counter.  The caller's cross-workgroup data must have been written

@@ -82,7 +82,8 @@ struct PassParams {
   int* next_token;
   // control
   int spin_limit;    // bound of every wait loop (polls)
-  long long* trace;  // diagnostics: [8][2 + 5L][8] phase timestamps, or null
+  int wl_cap;        // weight stages per wave copied to LDS before a barrier, at most
+  long long* trace;  // diagnostics: [G][3 + 5L][8] phase timestamps, or null
 };
 
 // mb16: 16-row blocks of the pass (Mp / 16: 1, 2, 4 or 8).

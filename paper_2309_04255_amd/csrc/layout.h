@@ -135,13 +135,12 @@ inline int step_ksteps(const Shape& s, int step) { return step == STEP_DOWN ? s.
 struct WorkspaceLayout {
   int Mp;
   int n_head_counters;
-  size_t counters;     // int32: (head, row block) [H][Mp/16] | lm | exit | status | spare
+  size_t counters;     // int32: (head, row block) [H][8] | lm | exit | status
   size_t counters_bytes;
   size_t bar;          // int32 [kBarSlots][kBarStride] grid-barrier counters
+  size_t zero;         // kZeroBytes of zeros (never written by a pass)
   size_t scratch_out;  // int32 [128 + 2] path/len/next sink for prefill
   size_t tree;         // int32 tok[128] | parent[128] | depth[128] | pos[128] | uint32 anc[128][4]
-  size_t trace;        // int64 [8][3 + 5L][8]    phase timestamps (diagnostics)
-  size_t zero;         // kZeroBytes of zeros (never written by a pass)
   size_t rope;         // fp32 [Mp][Dh/2][2]      cos, sin of every node's rotary angles
   size_t amax;         // int32 [Mp]              per-node greedy token
   size_t lm_val;       // fp32 [G][Mp]            LM-head argmax per workgroup
@@ -154,6 +153,7 @@ struct WorkspaceLayout {
   size_t hs;           // bf16 [L] x (Mp x Fp, fragment order)  SwiGLU product
   size_t attn_o;       // fp32 [H][Mp/16][KS][16][Dh]  key-split partial attention outputs
   size_t attn_ml;      // fp32 [H][Mp/16][KS][16][2]   their running max and sum
+  size_t trace;        // int64 [G][3 + 5L][8]    phase timestamps (diagnostics)
   size_t total;
   WorkspaceLayout(const Shape& s, int max_n, int G) {
     Mp = pass_rows(max_n);
@@ -163,14 +163,17 @@ struct WorkspaceLayout {
       o_ = align_up(o_ + bytes, 256);
       return at;
     };
-    n_head_counters = s.H * (Mp / 16);
+    // The regions that hold state from one pass to the next (counters, the
+    // barrier, the zero line) come first, sized for the largest pass, so
+    // that their offsets do not depend on the pass's node count or grid:
+    // llmcad_workspace_init clears them once for every later pass.
+    n_head_counters = s.H * (kMaxNodes / 16);
     counters_bytes = (size_t)(n_head_counters + 4) * 4;
     counters = take(counters_bytes);
     bar = take((size_t)kBarSlots * kBarStride * 4);
+    zero = take(kZeroBytes);
     scratch_out = take((128 + 2) * 4);
     tree = take(4 * 128 * 4 + 128 * 4 * 4);
-    trace = take((size_t)8 * pass_phases(s.L) * 8 * 8);
-    zero = take(kZeroBytes);
     rope = take((size_t)Mp * s.Dh * 4);
     amax = take((size_t)Mp * 4);
     lm_val = take((size_t)G * Mp * 4);
@@ -183,6 +186,7 @@ struct WorkspaceLayout {
     hs = take((size_t)s.L * Mp * s.Fp * 2);
     attn_o = take((size_t)s.H * Mp * kAttnMaxSplits * s.Dh * 4);
     attn_ml = take((size_t)s.H * Mp * kAttnMaxSplits * 2 * 4);
+    trace = take((size_t)G * pass_phases(s.L) * 8 * 8);
     total = o_;
   }
   size_t head_counters() const { return counters; }

@@ -53,7 +53,6 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
-constexpr int kTraceWgs = 8;  // workgroups that record phase timestamps
 
 // The launch parameters, read in place from the kernel-argument segment
 // (constant memory): loads through a wave-uniform address of it are scalar
@@ -109,9 +108,7 @@ __device__ __forceinline__ Sync make_sync(KParams& p, int* lds_flag) {
   s.status = p.status;
   s.limit = p.spin_limit;
   s.lds_flag = lds_flag;
-  s.trace = p.trace != nullptr && (int)blockIdx.x < kTraceWgs
-                ? p.trace + (size_t)blockIdx.x * pass_phases(p.L) * 8
-                : nullptr;
+  s.trace = p.trace != nullptr ? p.trace + (size_t)blockIdx.x * pass_phases(p.L) * 8 : nullptr;
   return s;
 }
 
@@ -134,32 +131,65 @@ __device__ __forceinline__ void grid_arrive(const Sync& s, int phase) {
   if (threadIdx.x == 0) atomic_add_dev(s.bar + (blockIdx.x % kBarSlots) * kBarStride, 1);
 }
 
-// Waits until all G workgroups have arrived `phase` times; one wave polls all
-// counters.  False (to all threads) if the bounded spin ran out.  The total
-// is exact only because every workgroup waits at every phase before it
-// arrives again: no workgroup can then be more than one arrival ahead.
+// Polled by one wave: returns 1 once all G workgroups have arrived `phase`
+// times (every lane reads one counter), 0 if the bounded spin ran out (the
+// pass status is then set).  The total is exact only because every
+// workgroup waits at every phase before it arrives again: no workgroup can
+// then be more than one arrival ahead.
+__device__ __forceinline__ int poll_grid(const Sync& s, int phase, int G) {
+  const int lane = threadIdx.x & 63;
+  const int slots = G < kBarSlots ? G : kBarSlots;
+  const int per = G / kBarSlots + (lane < G % kBarSlots ? 1 : 0);
+  const int want = lane < slots ? phase * (G < kBarSlots ? 1 : per) : 0;
+  const int* slot = s.bar + (lane < slots ? lane : 0) * kBarStride;
+  int spins = 0;
+  while (true) {
+    const int v = lane < slots ? ld_coherent(slot) : 0;
+    if (__all(v >= want)) return 1;
+    __builtin_amdgcn_s_sleep(1);
+    if (++spins > s.limit) {
+      if (lane == 0) st_coherent(s.status, 1);
+      return 0;
+    }
+  }
+}
+
+// Waits until all G workgroups have arrived `phase` times; wave 0 polls.
+// False (to all threads) if the bounded spin ran out.
 __device__ __forceinline__ bool grid_wait(const Sync& s, int phase, int G) {
   if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    const int slots = G < kBarSlots ? G : kBarSlots;
-    const int per = G / kBarSlots + (lane < G % kBarSlots ? 1 : 0);
-    const int want = lane < slots ? phase * (G < kBarSlots ? 1 : per) : 0;
-    const int* slot = s.bar + (lane < slots ? lane : 0) * kBarStride;
+    const int ok = poll_grid(s, phase, G);
+    if (threadIdx.x == 0) *s.lds_flag = ok;
+  }
+  // (LDS-only barriers: the other waves may have weight loads in flight,
+  // which must not be drained here)
+  lds_barrier();
+  const bool ok = *s.lds_flag != 0;
+  lds_barrier();
+  return ok;
+}
+
+// Waits until `counter` has counted `expected` arrivals (arrive_count),
+// then resets it for its next use; one wave polls.  False (to all threads)
+// if the bounded spin ran out.
+__device__ __forceinline__ bool join_wait(const Sync& s, int* counter, int expected) {
+  if (threadIdx.x < 64) {
     int ok = 1, spins = 0;
     while (true) {
-      const int v = lane < slots ? ld_coherent(slot) : 0;
-      if (__all(v >= want)) break;
+      const int v = ld_coherent(counter);
+      if (__all(v >= expected)) break;
       __builtin_amdgcn_s_sleep(1);
       if (++spins > s.limit) {
-        if (lane == 0) st_coherent(s.status, 1);
+        if (threadIdx.x == 0) st_coherent(s.status, 1);
         ok = 0;
         break;
       }
     }
-    if (lane == 0) *s.lds_flag = ok;
+    if (threadIdx.x == 0) {
+      if (ok) st_coherent(counter, 0);
+      *s.lds_flag = ok;
+    }
   }
-  // (LDS-only barriers: the other waves may have weight loads in flight,
-  // which must not be drained here)
   lds_barrier();
   const bool ok = *s.lds_flag != 0;
   lds_barrier();
@@ -313,7 +343,9 @@ __device__ __forceinline__ TileIn tile_in(KParams& p, int step, int l) {
   return t;
 }
 
-// Weight (and activation) stages per wave: about 160 VGPRs.
+// Weight (and activation) stages per wave: about 160 VGPRs.  (Deeper
+// pipelines gain nothing: a wave counts at most 63 loads in flight, and
+// they leave fewer stages to the LDS copy.)
 template <int MB, int C>
 constexpr int tile_depth() {
   constexpr int d = 40 / (C + MB);
@@ -362,7 +394,8 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   // barrier (P a multiple of D, as many as fit); the register pipeline
   // starts at stage P.
   constexpr int PMAX = WL_STAGES / D * D;
-  const int P = wave_uniform(wait_phase >= 0 ? (ns / D * D < PMAX ? ns / D * D : PMAX) : 0);
+  const int pcap = wave_uniform(p.wl_cap < PMAX ? p.wl_cap / D * D : PMAX);
+  const int P = wave_uniform(wait_phase >= 0 ? (ns / D * D < pcap ? ns / D * D : pcap) : 0);
   char* wl = lds + wl_off(C, MB) + (size_t)wave * PMAX * C * 1024;
   auto load_w = [&](int slot, int i, bool want) {  // stage i, or nothing (zero line)
     const bool live = want && i < ns;
@@ -384,7 +417,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   // polls the barrier and issues no load before it has seen it (a poll
   // waits for every older load of its wave).
   const int ns0 = (ks + kWaves - 1) / kWaves;
-  const int P0 = wave_uniform(wait_phase >= 0 ? (ns0 / D * D < PMAX ? ns0 / D * D : PMAX) : 0);
+  const int P0 = wave_uniform(wait_phase >= 0 ? (ns0 / D * D < pcap ? ns0 / D * D : pcap) : 0);
   if (wave != 0) {
     if constexpr (PMAX > 0) {
       for (int i = 0; i < P; ++i)
@@ -466,7 +499,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
     for (int u = 0; u < D; ++u) load_w(u, P + u, true);
   }
   __builtin_amdgcn_sched_barrier(0);
-  if (wait_phase >= 0 && p.trace != nullptr && (int)blockIdx.x < kTraceWgs && threadIdx.x == 0)
+  if (wait_phase >= 0 && p.trace != nullptr && threadIdx.x == 0)
     stg(p.trace + (size_t)blockIdx.x * pass_phases(p.L) * 8 + wait_phase * 8 + 3, (long long)wall_clock64());
 
   f32x4 acc[MB][C];
@@ -926,9 +959,9 @@ __device__ __forceinline__ void attn_store(char* buf, const AttnChunkRegs<DH>& R
 // soon as the barrier is passed.  Per step: S^T = K q^T on the matrix cores,
 // online softmax in the log2 domain, O^T += V^T P^T with P split into two
 // bf16 halves (P never leaves registers: the S result's lane layout is the
-// PV product's k-slot order).  With KS > 1 each split stores its partial
-// result and the last to arrive merges them, in split order.  MB: 16-row
-// blocks of the pass.
+// PV product's k-slot order).  With KS > 1 the prefix-only splits store
+// their partial results and the tree's split, which has the most work,
+// merges them with its own, in split order.  MB: 16-row blocks of the pass.
 template <int MB, int DH>
 __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& pin, int layer, int phase, char* lds,
                                                                      int* lds_flag) {
@@ -1134,7 +1167,14 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
     for (int db = 0; db < DB; ++db) lds_st<f32x4>(&om[(size_t)(wave * 16 + li) * DH + 16 * db + 4 * g], oacc[db]);
     lds_barrier();
     const size_t rbi = (size_t)h * MB + rb;  // (head, row block) slot
-    for (int it = threadIdx.x; it < 16 * (DH / 2); it += kThreads) {
+    // This thread's items of the unit's result: row it / (Dh/2), columns
+    // dd, dd + 1 (it = thread + k * threads).
+    constexpr int NIT = 16 * (DH / 2) / kThreads;
+    static_assert(NIT * kThreads == 16 * (DH / 2), "items per thread");
+    float uM[NIT], uL[NIT], u0[NIT], u1[NIT];
+#pragma unroll
+    for (int k = 0; k < NIT; ++k) {
+      const int it = threadIdx.x + k * kThreads;
       const int i = it / (DH / 2), dd = 2 * (it % (DH / 2));
       float M = -INFINITY;
 #pragma unroll
@@ -1149,41 +1189,73 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
         o0 += ov.x * wt;
         o1 += ov.y * wt;
       }
-      if (KS == 1) {
-        const int r = 16 * rb + i;
-        const float inv = 1.0f / L;
-        if (r < n) st_coherent_bf2(obase + frag_off(r, h * DH + dd, MB), o0 * inv, o1 * inv);
-      } else {
-        const size_t sl = rbi * KS + ks;  // this split's partial slot
-        st_coherent2(&p.attn_o[(sl * 16 + i) * DH + dd], o0, o1);
-        if (dd == 0) st_coherent2(&p.attn_ml[(sl * 16 + i) * 2], M, L);
-      }
+      uM[k] = M;
+      uL[k] = L;
+      u0[k] = o0;
+      u1[k] = o1;
     }
-    if (KS > 1 && arrive_last(&p.head_cnt[rbi], KS, lds_flag)) {
-      // Merge the key splits, in split order; every load of a row issued
-      // before any is used.
-      for (int it = threadIdx.x; it < 16 * (DH / 2); it += kThreads) {
+    if (KS > 1 && !has_tree) {
+      // A prefix split: its partial result, for the tree's split to merge.
+#pragma unroll
+      for (int k = 0; k < NIT; ++k) {
+        const int it = threadIdx.x + k * kThreads;
+        const int i = it / (DH / 2), dd = 2 * (it % (DH / 2));
+        const size_t sl = rbi * KS + ks;
+        st_coherent2(&p.attn_o[(sl * 16 + i) * DH + dd], u0[k], u1[k]);
+        if (dd == 0) st_coherent2(&p.attn_ml[(sl * 16 + i) * 2], uM[k], uL[k]);
+      }
+      arrive_count(&p.head_cnt[rbi]);
+    } else {
+      // The tree's split (the last of the key splits, and the one with the
+      // most work) merges: it waits for the other splits' partials, loads
+      // them all before using any, and adds them in split order, its own
+      // last.  (Units are taken in increasing order and a merge waits only
+      // for lower-numbered units, so every wait ends.)
+      constexpr int SO = kAttnMaxSplits - 1;
+      static_assert(SO >= 1, "key splits");
+      float2 ml[NIT][SO], ov[NIT][SO];
+      if (KS > 1) {
+        if (!join_wait(sy, &p.head_cnt[rbi], KS - 1)) return false;
+#pragma unroll
+        for (int k = 0; k < NIT; ++k) {
+          const int it = threadIdx.x + k * kThreads;
+          const int i = it / (DH / 2), dd = 2 * (it % (DH / 2));
+#pragma unroll
+          for (int s2 = 0; s2 < SO; ++s2) {
+            const size_t sl = rbi * KS + (s2 < KS - 1 ? s2 : 0);
+            ml[k][s2] = s2 < KS - 1 ? ld_coherent2(&p.attn_ml[(sl * 16 + i) * 2]) : make_float2(-INFINITY, 0.0f);
+            ov[k][s2] = s2 < KS - 1 ? ld_coherent2(&p.attn_o[(sl * 16 + i) * DH + dd]) : make_float2(0.0f, 0.0f);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < NIT; ++k)
+#pragma unroll
+          for (int s2 = 0; s2 < SO; ++s2) {
+            ml[k][s2] = make_float2(-INFINITY, 0.0f);
+            ov[k][s2] = make_float2(0.0f, 0.0f);
+          }
+      }
+#pragma unroll
+      for (int k = 0; k < NIT; ++k) {
+        const int it = threadIdx.x + k * kThreads;
         const int i = it / (DH / 2), dd = 2 * (it % (DH / 2));
         const int r = 16 * rb + i;
-        constexpr int SB = 4;  // (KS <= 4)
-        float2 ml[SB], ov[SB];
+        float M = uM[k];
 #pragma unroll
-        for (int s2 = 0; s2 < SB; ++s2) {
-          const size_t sl = rbi * KS + s2;
-          ml[s2] = s2 < KS ? ld_coherent2(&p.attn_ml[(sl * 16 + i) * 2]) : make_float2(-INFINITY, 0.0f);
-          ov[s2] = s2 < KS ? ld_coherent2(&p.attn_o[(sl * 16 + i) * DH + dd]) : make_float2(0.0f, 0.0f);
-        }
-        float M = -INFINITY;
-#pragma unroll
-        for (int s2 = 0; s2 < SB; ++s2) M = fmaxf(M, ml[s2].x);
+        for (int s2 = 0; s2 < SO; ++s2) M = fmaxf(M, ml[k][s2].x);
         float L = 0.0f, o0 = 0.0f, o1 = 0.0f;
 #pragma unroll
-        for (int s2 = 0; s2 < SB; ++s2) {
-          const float wt = ml[s2].x == -INFINITY ? 0.0f : exp2f(ml[s2].x - M);
-          L += ml[s2].y * wt;
-          o0 += ov[s2].x * wt;
-          o1 += ov[s2].y * wt;
+        for (int s2 = 0; s2 < SO; ++s2) {
+          const float wt = ml[k][s2].x == -INFINITY ? 0.0f : exp2f(ml[k][s2].x - M);
+          L += ml[k][s2].y * wt;
+          o0 += ov[k][s2].x * wt;
+          o1 += ov[k][s2].y * wt;
         }
+        const float wt = uM[k] == -INFINITY ? 0.0f : exp2f(uM[k] - M);
+        L += uL[k] * wt;
+        o0 += u0[k] * wt;
+        o1 += u1[k] * wt;
         const float inv = 1.0f / L;
         if (r < n) st_coherent_bf2(obase + frag_off(r, h * DH + dd, MB), o0 * inv, o1 * inv);
       }

@@ -64,6 +64,29 @@ def test_sizes(binding):
     assert size == 32 * s.d_model * 4 and off + size <= binding.workspace_bytes(cfg, 31)
 
 
+def test_state_regions_fixed(binding, monkeypatch):
+    # The regions that hold state between passes (counters with the pass
+    # status, and the zero line the kernels read for absent inputs) sit at
+    # offsets that depend on neither the pass's node count nor its grid, so
+    # that one llmcad_workspace_init serves passes of every size.
+    cfg = binding.make_config(workloads.MODELS["llama7b"])
+    seen = {5: set(), 13: set()}
+    for grid in (None, "3", "24", "200"):
+        if grid is None:
+            monkeypatch.delenv("LLMCAD_PASS_GRID", raising=False)
+        else:
+            monkeypatch.setenv("LLMCAD_PASS_GRID", grid)
+        for n in (1, 16, 17, 31, 64, 100, 128):
+            for which in seen:
+                off, size = binding.workspace_region(cfg, n, which)
+                seen[which].add((off, size))
+                assert off + size <= binding.workspace_bytes(cfg, n)
+    assert len(seen[5]) == 1 and len(seen[13]) == 1, seen
+    (zoff, zsize), = seen[13]
+    (soff, _), = seen[5]
+    assert zsize >= 4096 and not (zoff <= soff < zoff + zsize)
+
+
 def _call_verify(binding, cfg, tok, par, prefix_len=10, cap=64, ws_bytes=1 << 30, packed=16):
     lib = binding.lib()
     tok = np.ascontiguousarray(tok, dtype=np.int32)
