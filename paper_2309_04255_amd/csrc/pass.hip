@@ -343,13 +343,18 @@ __device__ __forceinline__ TileIn tile_in(KParams& p, int step, int l) {
   return t;
 }
 
-// Weight (and activation) stages per wave: about 160 VGPRs.  (Deeper
-// pipelines gain nothing: a wave counts at most 63 loads in flight, and
-// they leave fewer stages to the LDS copy.)
+// Register stages per wave: at most ~160 VGPRs of them, and few -- 8 for
+// one-block tiles, 4 for wider ones.  The bytes in flight across a barrier
+// come mostly from the stages copied to LDS before it; a deeper register
+// pipeline only lengthens the queues in the memory system (on the 7B
+// workload 8 and 4 stages beat the 13, 8 and 5 that fill ~160 VGPRs by
+// 3%), and a depth that divides the LDS stages lets the copy use them all.
 template <int MB, int C>
 constexpr int tile_depth() {
-  constexpr int d = 40 / (C + MB);
-  return d < 2 ? 2 : (d > 16 ? 16 : d);
+  constexpr int regs = 40 / (C + MB);
+  constexpr int cap = C == 1 ? 8 : 4;
+  constexpr int d = regs < cap ? regs : cap;
+  return d < 2 ? 2 : d;
 }
 
 // One tile: blocks [nb0, nb0 + C) of a step over all its k-steps.  Issues
@@ -370,10 +375,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   const int wave = wave_index(), lane = threadIdx.x & 63;
   const int ks = io.ks;
   const int ns = wave_uniform(wave < ks ? (ks - wave + kWaves - 1) / kWaves : 0);
-  // Pipeline depth: about 160 VGPRs of stages, but no deeper than the LDS
-  // stages that fit, so that wide tiles still get some (the LDS phase
-  // advances D stages at a time); at C >= 5 a few stages of C KiB are plenty
-  // in flight.
+  // Pipeline depth (tile_depth), but no deeper than the LDS stages that
+  // fit, so that wide tiles still get some (the LDS phase advances D stages
+  // at a time).
   constexpr int WL_STAGES = (kGemmLdsBytes - wl_off(C, MB)) / (kWaves * C * 1024);
   constexpr int D0 = tile_depth<MB, C>();
   constexpr int D = WL_STAGES >= 2 && WL_STAGES < D0 ? WL_STAGES : D0;
