@@ -531,7 +531,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
       load_a(u, i + u + D);
     }
   }
-  for (; i < ns; i += D) {
+  for (; i + D < ns; i += D) {
 #pragma unroll
     for (int u = 0; u < D; ++u) {
       __builtin_amdgcn_sched_barrier(0);
@@ -542,6 +542,18 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
       __builtin_amdgcn_sched_barrier(0);
       load_w(u, i + u + D, true);
       load_a(u, i + u + D);
+    }
+  }
+  // the last round: nothing left to load (no zero-line loads for the
+  // barrier at the end of the tile to wait for)
+  if (i < ns) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+        for (int c = 0; c < C; ++c) acc[rb][c] = mfma16x16x32(ba[u][rb], bw[u][c], acc[rb][c]);
     }
   }
   __builtin_amdgcn_sched_barrier(0);
