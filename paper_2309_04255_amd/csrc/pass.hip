@@ -115,7 +115,9 @@ __device__ __forceinline__ Sync make_sync(KParams& p, int* lds_flag) {
 // Diagnostics: wall-clock (100 MHz) marks per phase: 0 = barrier wait
 // entered, 1 = wait over, 2 = phase work done; GEMM phases also mark 3 =
 // activation stream started, 4 = first tile's main loop done, 5 = all tiles
-// and epilogues done.
+// and epilogues done; the attention marks 3 = loads issued, 4 = keys done,
+// 5 = result stored, and in a merging split 6 = the other splits' arrivals
+// seen, 7 = their partials loaded.
 __device__ __forceinline__ void trace_mark(const Sync& s, int phase, int k) {
   if (s.trace != nullptr && threadIdx.x == 0) stg(s.trace + phase * 8 + k, (long long)wall_clock64());
 }
@@ -1232,6 +1234,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
       float2 ml[NIT][SO], ov[NIT][SO];
       if (KS > 1) {
         if (!join_wait(sy, &p.head_cnt[rbi], KS - 1)) return false;
+        trace_mark(sy, phase, 6);
 #pragma unroll
         for (int k = 0; k < NIT; ++k) {
           const int it = threadIdx.x + k * kThreads;
@@ -1274,6 +1277,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
         o1 += u1[k] * wt;
         const float inv = 1.0f / L;
         if (r < n) st_coherent_bf2(obase + frag_off(r, h * DH + dd, MB), o0 * inv, o1 * inv);
+        if (k == 0) trace_mark(sy, phase, 7);
       }
     }
     trace_mark(sy, phase, 5);
