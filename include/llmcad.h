@@ -174,7 +174,7 @@ const char* llmcad_status_string(int status);
  * must be cleared with llmcad_workspace_init before the next pass; 3 = the
  * kernel did not find its parameter block where it reads it, and did
  * nothing),
- * 6 phase timestamps int64 [G][3 + 5L][8], G the pass's workgroups (written when the environment
+ * 6 phase timestamps int64 [G][4 + 5L][8], G the pass's workgroups (written when the environment
  * variable LLMCAD_TRACE is 1), 7 every residual stream version fp32
  * [2L+1][Mp][d], 8 their per-16-column sums of squares fp32 [2L+1][d/16][Mp],
  * 9 every layer's queries bf16 [L][Mp][d], 10 attention outputs bf16

@@ -32,6 +32,8 @@ from .model import (  # noqa: F401
     causal_forward,
     prefill_kv,
     tree_forward,
+    tree_layer,
+    logits_from_stream,
     verify_tree,
 )
 from .walk import accept_walk, branch_sequences, correct_sequences  # noqa: F401

@@ -165,13 +165,20 @@ def _qkv(cfg, w, x, pos, R):
     return q, k, v
 
 
-def _after_attention(cfg, w, x, o, R):
+def _attn_residual(cfg, w, x, o, R):
     n = x.shape[0]
     o = R(o.reshape(n, cfg.d_model))
-    x = x + o @ w["wo"].T
+    return x + o @ w["wo"].T
+
+
+def _ffn_residual(cfg, w, x, R):
     xn = R(rmsnorm(x, w["ffn_norm"], cfg.rms_eps))
     hidden = R(silu(xn @ w["wg"].T) * (xn @ w["wu"].T))
     return x + hidden @ w["wd"].T
+
+
+def _after_attention(cfg, w, x, o, R):
+    return _ffn_residual(cfg, w, _attn_residual(cfg, w, x, o, R), R)
 
 
 def _logits(weights, x, R):
@@ -245,25 +252,47 @@ def tree_forward(weights: OracleWeights, prefix_k, prefix_v, tree_tokens, parent
     cfg = weights.cfg
     R = _rnd(rounding)
     tree_tokens = np.asarray(tree_tokens, dtype=np.int64)
-    parent = np.asarray(parent, dtype=np.int64)
-    n = len(tree_tokens)
-    P = prefix_k.shape[1]
-    pos = P + _depths(parent)
-    branch = [ancestors_and_self(parent, i) for i in range(n)]
     x = weights.tok_embed[tree_tokens].copy()
     ks, vs = [], []
     for l in range(cfg.n_layers):
-        w = weights.layer(l)
-        q, k, v = _qkv(cfg, w, x, pos, R)
-        o = np.empty_like(q)
-        for i in range(n):
-            keys = np.concatenate([prefix_k[l], k[branch[i]]], axis=0)
-            vals = np.concatenate([prefix_v[l], v[branch[i]]], axis=0)
-            o[i] = attend(q[i], keys, vals)
-        x = _after_attention(cfg, w, x, o, R)
+        _, x, k, v = tree_layer(weights, l, x, prefix_k[l], prefix_v[l], parent, rounding)
         ks.append(k)
         vs.append(v)
     return _logits(weights, x, R), np.stack(ks), np.stack(vs)
+
+
+def tree_layer(weights: OracleWeights, l, x, prefix_k_l, prefix_v_l, parent, rounding=True):
+    """Decoder layer l of the masked pass (§3.2).
+
+    x [n, d] is the layer's input residual stream; prefix_k_l/prefix_v_l
+    [P, H, Dh] are that layer's prefix keys/values.  Node i sits at position
+    P + depth(i) and attends to the P prefix positions and to its branch
+    (ancestors, root first, then itself).  Returns (the residual stream after
+    the attention block, after the whole layer, tree k [n, H, Dh], tree v
+    [n, H, Dh]).
+    """
+    cfg = weights.cfg
+    R = _rnd(rounding)
+    parent = np.asarray(parent, dtype=np.int64)
+    n = len(parent)
+    P = prefix_k_l.shape[0]
+    pos = P + _depths(parent)
+    w = weights.layer(l)
+    x = np.asarray(x, dtype=np.float64)
+    q, k, v = _qkv(cfg, w, x, pos, R)
+    o = np.empty_like(q)
+    for i in range(n):
+        branch = ancestors_and_self(parent, i)
+        keys = np.concatenate([prefix_k_l, k[branch]], axis=0)
+        vals = np.concatenate([prefix_v_l, v[branch]], axis=0)
+        o[i] = attend(q[i], keys, vals)
+    x_mid = _attn_residual(cfg, w, x, o, R)
+    return x_mid, _ffn_residual(cfg, w, x_mid, R), k, v
+
+
+def logits_from_stream(weights: OracleWeights, x, rounding=True):
+    """Final RMSNorm and LM head of a residual stream x [n, d] -> logits [n, V]."""
+    return _logits(weights, np.asarray(x, dtype=np.float64), _rnd(rounding))
 
 
 def verify_tree(weights: OracleWeights, prefix_k, prefix_v, tree_tokens, parent, rounding=True):

@@ -179,6 +179,7 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.rope = (float*)(ws + W.rope);
   p.x = (float*)(ws + W.xs);
   p.xg = (bf16*)(ws + W.xgs);
+  p.xnf = (bf16*)(ws + W.xnf);
   p.ssq = (float*)(ws + W.ssqs);
   p.ssq_regs = W.Mp <= 32 && cdiv(s.d_nb, 1024 / W.Mp) <= 8 ? 1 : 0;
   p.q = (bf16*)(ws + W.qs);

@@ -57,6 +57,7 @@ struct PassParams {
   float* rope;      // [Mp][Dh/2][2] cos, sin of every node's rotary angles
   float* x;         // [2L+1][Mp][d]
   bf16* xg;         // [2L+1] x fragment-order [Mp][d]: bf16(x * g), g the gain of the norm that reads x
+  bf16* xnf;        // fragment-order [Mp][d]: the final norm's output bf16(x rstd g), the LM head's input
   float* ssq;       // [2L+1][d/16][Mp]
   int ssq_regs;     // 1 if a norm step's tiles hold its sums of squares in registers
                     // (Mp <= 32 and at most 8 blocks per chunk of d/16 / (1024 / Mp) blocks)
@@ -83,7 +84,7 @@ struct PassParams {
   // control
   int spin_limit;    // bound of every wait loop (polls)
   int wl_cap;        // weight stages per wave copied to LDS before a barrier, at most
-  long long* trace;  // diagnostics: [G][3 + 5L][8] phase timestamps, or null
+  long long* trace;  // diagnostics: [G][4 + 5L][8] phase timestamps, or null
 };
 
 // mb16: 16-row blocks of the pass (Mp / 16: 1, 2, 4 or 8).

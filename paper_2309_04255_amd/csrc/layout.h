@@ -24,11 +24,11 @@ constexpr int kBarStride = 32;      // ints between barrier counters (128 bytes)
 constexpr int kZeroBytes = 4096;    // zeros (padding reads)
 
 // Phases of a pass: tree prep + embedding, a barrier that publishes the
-// rotary table, five per layer, and the LM head.
+// rotary table, five per layer, the final norm, and the LM head.
 #if defined(__HIPCC__)
 __host__ __device__
 #endif
-inline int pass_phases(int L) { return 3 + 5 * L; }
+inline int pass_phases(int L) { return 4 + 5 * L; }
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 inline int round_up(int x, int a) { return (x + a - 1) / a * a; }
@@ -147,13 +147,14 @@ struct WorkspaceLayout {
   size_t lm_idx;       // int32 [G][Mp]
   size_t xs;           // fp32 [2L+1][Mp][d]      residual stream versions
   size_t xgs;          // bf16 [2L+1] x (Mp x d, fragment order)  bf16(x * g) (g: its norm's gain)
+  size_t xnf;          // bf16 Mp x d, fragment order   the final norm's output bf16(x rstd g)
   size_t ssqs;         // fp32 [2L+1][d/16][Mp]   their per-16-column sums of squares
   size_t qs;           // bf16 [L][Mp][d]         queries after the rotary embedding
   size_t os;           // bf16 [L] x (Mp x d, fragment order)   attention output
   size_t hs;           // bf16 [L] x (Mp x Fp, fragment order)  SwiGLU product
   size_t attn_o;       // fp32 [H][Mp/16][KS][16][Dh]  key-split partial attention outputs
   size_t attn_ml;      // fp32 [H][Mp/16][KS][16][2]   their running max and sum
-  size_t trace;        // int64 [G][3 + 5L][8]    phase timestamps (diagnostics)
+  size_t trace;        // int64 [G][4 + 5L][8]    phase timestamps (diagnostics)
   size_t total;
   WorkspaceLayout(const Shape& s, int max_n, int G) {
     Mp = pass_rows(max_n);
@@ -180,6 +181,7 @@ struct WorkspaceLayout {
     lm_idx = take((size_t)G * Mp * 4);
     xs = take((size_t)(2 * s.L + 1) * Mp * s.d * 4);
     xgs = take((size_t)(2 * s.L + 1) * Mp * s.d * 2);
+    xnf = take((size_t)Mp * s.d * 2);
     ssqs = take((size_t)(2 * s.L + 1) * s.d_nb * Mp * 4);
     qs = take((size_t)s.L * Mp * s.d * 2);
     os = take((size_t)s.L * Mp * s.d * 2);

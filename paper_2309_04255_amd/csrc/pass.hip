@@ -13,9 +13,9 @@
 // Phases: embed + tree prep; per layer QKV projection (RMSNorm scale,
 // rotary embedding and K/V cache write in the epilogue) -> tree attention
 // (ancestor mask) -> O projection (+residual) -> gate/up (RMSNorm scale;
-// SwiGLU epilogue) -> down projection (+residual); then the LM head (final
-// RMSNorm scale) + argmax, and the accept walk in the workgroup that
-// completes the argmax.
+// SwiGLU epilogue) -> down projection (+residual); then the final RMSNorm,
+// the LM head + argmax, and the accept walk in the workgroup that completes
+// the argmax.
 //
 // GEMM phases (activations X [Mp rows x K], packed weights W [N x K]): the
 // 16-column blocks of a step are dealt out in contiguous runs, one run per
@@ -300,10 +300,9 @@ __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
       io.g_next = l + 1 < p.L ? (const bf16*)(lw + p.layer_bytes + p.o_attn_norm)
                               : (const bf16*)(p.packed + p.o_final_norm);
       break;
-    default:  // STEP_LM
-      io.norm = true;
-      io.a = (const bf16x8*)(p.xg + (size_t)(2 * p.L) * xsz);
-      io.ssq = p.ssq + (size_t)(2 * p.L) * ssz;
+    default:  // STEP_LM: its input is the final norm's output, already scaled
+      io.norm = false;
+      io.a = (const bf16x8*)p.xnf;
       break;
   }
   return io;
@@ -329,11 +328,12 @@ __device__ __forceinline__ TileIn tile_in(KParams& p, int step, int l) {
   t.w = (const bf16x8*)((sp.layer_rel ? lw : p.packed) + sp.w_off);
   t.ks = sp.ksteps;
   t.resid = step == STEP_O || step == STEP_DOWN;
-  t.norm = !t.resid;
+  t.norm = step == STEP_QKV || step == STEP_GATE_UP;
   // x version read by a norm step: QKV 2l, GU 2l+1, LM 2L; residual input: O 2l, DOWN 2l+1
   const int ver = step == STEP_LM ? 2 * p.L : (step == STEP_GATE_UP || step == STEP_DOWN) ? 2 * l + 1 : 2 * l;
   const bf16* act = step == STEP_O ? p.o + (size_t)l * xsz
                   : step == STEP_DOWN ? p.h + (size_t)l * p.Mp * p.Fp
+                  : step == STEP_LM ? p.xnf
                                       : p.xg + (size_t)ver * xsz;
   t.a = (const bf16x8*)act;
   t.ssq = t.norm ? p.ssq + (size_t)ver * ssz : nullptr;
@@ -599,6 +599,36 @@ __device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) 
 // per-16-column sums of squares the producing phase wrote, added in a fixed
 // order; 0 for rows >= n.  When the tile held them in registers its chunk
 // sums are in part_ss already.
+// RMSNorm scales of rows [0, Mp) into gl.rstd from a version's sums of
+// squares ssq [d/16][Mp] (added in a fixed order); 0 for rows >= n.
+template <int MB>
+__device__ __forceinline__ void row_rstd(KParams& p, const float* ssq, GemmLds& gl) {
+  constexpr int ROWS = 16 * MB;
+  constexpr int CHK = 256 / ROWS;
+  const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
+  const int dn = p.d_nb;
+  const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
+  float ss = 0.0f;
+  if (r < p.n) {
+    constexpr int PER = 8;
+    for (int t = t0; t < t1; t += PER) {
+      float v[PER];
+#pragma unroll
+      for (int k = 0; k < PER; ++k) v[k] = t + k < t1 ? ldg(ssq + (size_t)(t + k) * ROWS + r) : 0.0f;
+#pragma unroll
+      for (int k = 0; k < PER; ++k) ss += v[k];
+    }
+  }
+  gl.part_ss[ch * ROWS + r] = ss;
+  __syncthreads();
+  if (threadIdx.x < ROWS) {
+    float t = 0.0f;
+    for (int c = 0; c < CHK; ++c) t += gl.part_ss[c * ROWS + threadIdx.x];
+    gl.rstd[threadIdx.x] = threadIdx.x < p.n ? 1.0f / sqrtf(t * p.inv_d + p.eps) : 0.0f;
+  }
+  __syncthreads();
+}
+
 template <int MB>
 __device__ __forceinline__ void row_scales(KParams& p, const StepIo& io, GemmLds& gl) {
   constexpr int ROWS = 16 * MB;
@@ -612,29 +642,7 @@ __device__ __forceinline__ void row_scales(KParams& p, const StepIo& io, GemmLds
     __syncthreads();
     return;
   }
-  constexpr int CHK = 256 / ROWS;
-  const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
-  const int dn = p.d_nb;
-  const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
-  float ss = 0.0f;
-  if (r < p.n) {
-    constexpr int PER = 8;
-    for (int t = t0; t < t1; t += PER) {
-      float v[PER];
-#pragma unroll
-      for (int k = 0; k < PER; ++k) v[k] = t + k < t1 ? ldg(io.ssq + (size_t)(t + k) * ROWS + r) : 0.0f;
-#pragma unroll
-      for (int k = 0; k < PER; ++k) ss += v[k];
-    }
-  }
-  gl.part_ss[ch * ROWS + r] = ss;
-  __syncthreads();
-  if (threadIdx.x < ROWS) {
-    float t = 0.0f;
-    for (int c = 0; c < CHK; ++c) t += gl.part_ss[c * ROWS + threadIdx.x];
-    gl.rstd[threadIdx.x] = threadIdx.x < p.n ? 1.0f / sqrtf(t * p.inv_d + p.eps) : 0.0f;
-  }
-  __syncthreads();
+  row_rstd<MB>(p, io.ssq, gl);
 }
 
 // Epilogue of one accumulator tile ("unit": block c of the tile x row block
@@ -651,7 +659,7 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
   for (int w = 1; w < kWaves; ++w) s += lds_ld<f32x4>(lds + tw_off() + ((size_t)(w * cw * MB + unit) * 64 + lane) * 16);
   float v[4] = {s[0], s[1], s[2], s[3]};
   const int rr0 = 4 * q4;  // first row of this lane inside the row block
-  if constexpr (EPI != EPI_RESID) {  // the norm's per-row scale
+  if constexpr (EPI == EPI_QKV || EPI == EPI_SWIGLU) {  // the norm's per-row scale
 #pragma unroll
     for (int i = 0; i < 4; ++i) v[i] *= gl.rstd[16 * rb + rr0 + i];
   }
@@ -824,7 +832,7 @@ __device__ __attribute__((noinline, not_tail_called)) void finish_tile(KParams& 
   nb0 = wave_uniform(nb0);
   cw = wave_uniform(cw);
   const StepIo io = step_io(p, step, layer);
-  if constexpr (EPI != EPI_RESID) row_scales<MB>(p, io, gl);
+  if constexpr (EPI == EPI_QKV || EPI == EPI_SWIGLU) row_scales<MB>(p, io, gl);
   const int units = cw * MB;
   for (int u = wave_index(); u < units; u += kWaves) {
     const int c = u / MB, rb = u % MB;
@@ -1355,6 +1363,42 @@ constexpr size_t dyn_lds_bytes() {
   return attn > gemm ? attn : gemm;
 }
 
+// ------------------------------------------------------------------ final norm
+
+// The final RMSNorm, rounded where the model rounds it: xnf = bf16(x rstd g)
+// of the last residual version, in fragment order, the LM head's input.  (A
+// layer's norms round bf16(x g) instead and scale the product's rows, which
+// needs no phase of its own; for the logits one phase per pass keeps the
+// model's rounding point.)  Workgroup w takes the 16-column blocks
+// [w d/16 / G, (w + 1) d/16 / G).
+template <int MB>
+__device__ __attribute__((noinline, not_tail_called)) bool final_norm_phase(KParams& pin, int phase, GemmLds& gl,
+                                                                           int* lds_flag) {
+  KParams& p = uniform_params(pin);
+  phase = wave_uniform(phase);
+  const Sync sy = make_sync(p, lds_flag);
+  trace_mark(sy, phase, 0);
+  if (!grid_wait(sy, phase, p.G)) return false;
+  trace_mark(sy, phase, 1);
+  constexpr int ROWS = 16 * MB;
+  row_rstd<MB>(p, p.ssq + (size_t)(2 * p.L) * p.d_nb * p.Mp, gl);
+  const float* x = p.x + (size_t)(2 * p.L) * p.Mp * p.d;
+  const bf16* g = (const bf16*)(p.packed + p.o_final_norm);
+  const int lo = wave_uniform((int)((long)blockIdx.x * p.d_nb / p.G));
+  const int hi = wave_uniform((int)((long)(blockIdx.x + 1) * p.d_nb / p.G));
+  for (int e = threadIdx.x; e < (hi - lo) * ROWS * (kNB / 2); e += kThreads) {
+    const int pr = e % (kNB / 2), r = (e / (kNB / 2)) % ROWS, b = lo + e / ((kNB / 2) * ROWS);
+    const int c = kNB * b + 2 * pr;
+    if (r < p.n) {
+      const float2 xv = ldg((const float2*)(x + (size_t)r * p.d + c));
+      const float s = gl.rstd[r];
+      st_coherent_bf2(p.xnf + frag_off(r, c, MB), xv.x * s * bf2f(g[c]), xv.y * s * bf2f(g[c + 1]));
+    }
+  }
+  trace_mark(sy, phase, 5);
+  return true;
+}
+
 template <int MB, int DH>
 __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_arg, const TreeArgs tree) {
   extern __shared__ __attribute__((aligned(1024))) char lds_raw[];
@@ -1398,7 +1442,9 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
     if (!ok) break;
     grid_arrive(sy, phase++);
   }
-  if (ok) {  // LM head (final norm scale) + argmax + accept walk
+  if (ok) ok = final_norm_phase<MB>(p, phase, gl, &flag);
+  if (ok) {  // LM head + argmax + accept walk
+    grid_arrive(sy, phase++);
     if (gemm_phase<MB, EPI_LOGITS>(p, STEP_LM, 0, phase, lds_raw, gl, &flag)) trace_mark(sy, phase, 2);
   }
   // Leave the pass: the last workgroup out resets the barrier counters.

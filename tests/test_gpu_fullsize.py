@@ -1,0 +1,147 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+bench times (all workgroups, default key splits).
+
+A whole oracle pass at these sizes (7B to 30B, 32 to 60 layers) takes too long
+on the host, so the comparison is layer-sampled.  The pass keeps every version
+of its residual stream (workspace region 7: the input of every layer, the
+stream after its attention block, and after the layer).  For a few sampled
+layers the oracle recomputes the layer from the GPU's own input version and the
+GPU's own prefix K/V (written by its prefill), and the test compares what each
+of the layer's two blocks adds to the stream, and the tree's K/V cache slots.  The LM head is recomputed from
+the GPU's last version and compared over all n x V logits; the argmax and the
+accept walk are checked as in the small-model tests.  The embedding rows are
+compared exactly.
+
+Bars: logits as everywhere (max abs 2e-2, relative L2 1e-2); a block's
+contribution or a K/V slice: max |gpu - oracle| <= 2e-2 max |oracle| and
+relative L2 <= 1e-2, the logits bar taken relative to the tensor's scale (both
+sides accumulate in fp32 or better; the difference comes from the bf16
+rounding points of the layer's products, each ~2^-9 relative).
+"""
+
+import gc
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from tests import parity
+from tests.util import oracle_config, to_np
+
+pytestmark = pytest.mark.gpu
+
+# (workload, sampled layers): the bench's workload with three layers, the
+# other parity workloads with their first and last layer
+CASES = [
+    ("llama7b_p512_n31", (0, 15, 31)),
+    ("llama7b_p2048_n41", (0, 31)),
+    ("llama13b_p1024_n41", (0, 39)),
+    ("llama30b_p1024_n1", (0, 59)),
+    ("llama30b_p1024_n32", (59,)),
+    ("llama30b_p1024_n128", (0, 59)),
+]
+_MODEL = {}
+
+
+def _log(msg):
+    print(f"[fullsize {time.strftime('%H:%M:%S')}] {msg}", flush=True)
+
+
+def _model(name):
+    """One model resident at a time: packed weights on the GPU, a session whose
+    cache holds the largest prefix of the model's workloads, the generator, and
+    the oracle's weights (LM head; sampled layers as they are first used)."""
+    if name in _MODEL:
+        return _MODEL[name]
+    _MODEL.clear()
+    gc.collect()  # (the previous model's session, generator and oracle copies)
+    torch.cuda.empty_cache()
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2309_04255_amd import binding
+
+    shape = workloads.MODELS[name]
+    cap = max(workloads.get_workload(w).prefix_len for w, _ in CASES
+              if workloads.get_workload(w).model == name) + 128
+    _log(f"{name}: packing weights on the GPU")
+    sess = binding.Session(shape, capacity=cap, max_n=128)
+    binding.workspace_init(sess.cfg, 128, sess.workspace)
+    # The oracle's weights come from the same seeded generator run by torch on
+    # the GPU (its values equal the CPU run's, which another test checks):
+    # generating a 30B layer on the host takes tens of seconds.
+    gen = workloads.make_weights(shape, "cuda")
+    sess.load_weights(gen)
+    torch.cuda.synchronize()
+    _log(f"{name}: oracle LM head")
+    ow = oracle.OracleWeights(oracle_config(shape), np.zeros((1, shape.d_model)), to_np(gen.final_norm()),
+                              to_np(gen.lm_head()), lambda l: {k: to_np(v) for k, v in gen.layer(l).items()})
+    _MODEL[name] = (shape, sess, gen, ow, binding)
+    return _MODEL[name]
+
+
+def gen_device(gen):
+    return gen.final_norm().device
+
+
+def _check_tensor(gpu, ref, what):
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert np.all(np.isfinite(gpu)), f"{what}: non-finite"
+    scale = np.abs(ref).max()
+    err = np.abs(gpu - ref).max()
+    rel = np.linalg.norm(gpu - ref) / np.linalg.norm(ref)
+    assert err <= parity.ABS_TOL * scale, f"{what}: max abs error {err:.3e} > {parity.ABS_TOL} x {scale:.3e}"
+    assert rel <= parity.REL_TOL, f"{what}: relative L2 error {rel:.3e} > {parity.REL_TOL}"
+    return err / scale, rel
+
+
+@pytest.mark.parametrize("wl_name,layers", CASES, ids=[c[0] for c in CASES])
+def test_full_size_layer_sampled(wl_name, layers):
+    wl = workloads.get_workload(wl_name)
+    shape, sess, gen, ow, binding = _model(wl.model)
+    P, L, d, H, Dh = wl.prefix_len, shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim
+    parent, tok = workloads.make_tree(wl.tree, shape.vocab, wl.seed)
+    n = len(parent)
+    _log(f"{wl_name}: prefill of {P} tokens, then the verification pass (n={n})")
+    sess.prefill(workloads.draw_tokens(P, shape.vocab, seed=wl.seed), 0)
+    sess.verify_tree(P, tok, parent)
+    logits, path, acc, nxt = sess.results(n)
+    logits = logits.numpy().astype(np.float64)
+    off, size = binding.workspace_region(sess.cfg, n, 7)
+    mp = size // ((2 * L + 1) * d * 4)
+    xs = sess.workspace[off:off + size].view(torch.float32).view(2 * L + 1, mp, d)[:, :n]
+    off4, _ = binding.workspace_region(sess.cfg, n, 4)
+    amax = sess.workspace[off4:off4 + 4 * n].view(torch.int32).cpu().numpy()
+    torch.cuda.synchronize()
+
+    # embedding rows: exact
+    emb = to_np(gen.tok_embed()[torch.as_tensor(np.asarray(tok, dtype=np.int64), device=gen_device(gen))])
+    np.testing.assert_array_equal(to_np(xs[0]), emb)
+
+    for l in layers:
+        t0 = time.time()
+        pk = sess.k_cache[l, :, :P].float().cpu().numpy().astype(np.float64).transpose(1, 0, 2)
+        pv = sess.v_cache[l, :, :P].float().cpu().numpy().astype(np.float64).transpose(1, 0, 2)
+        x_in = to_np(xs[2 * l])
+        g_mid, g_out = to_np(xs[2 * l + 1]), to_np(xs[2 * l + 2])
+        x_mid, x_out, k, v = oracle.tree_layer(ow, l, x_in, pk, pv, parent)
+        # each block's contribution to the stream (the stream itself is
+        # dominated by the input, which both sides share)
+        a1 = _check_tensor(g_mid - x_in, x_mid - x_in, f"{wl_name} layer {l} attention block")
+        a2 = _check_tensor(g_out - g_mid, x_out - x_mid, f"{wl_name} layer {l} feed-forward block")
+        gk = sess.k_cache[l, :, P:P + n].float().cpu().numpy().transpose(1, 0, 2)
+        gv = sess.v_cache[l, :, P:P + n].float().cpu().numpy().transpose(1, 0, 2)
+        a3 = _check_tensor(gk, k, f"{wl_name} layer {l} tree K")
+        a4 = _check_tensor(gv, v, f"{wl_name} layer {l} tree V")
+        _log(f"{wl_name} layer {l}: rel max/L2 mid {a1[0]:.1e}/{a1[1]:.1e} out {a2[0]:.1e}/{a2[1]:.1e} "
+             f"K {a3[0]:.1e} V {a4[0]:.1e} ({time.time() - t0:.1f} s)")
+
+    ref = oracle.logits_from_stream(ow, to_np(xs[2 * L]))
+    err, rel = parity.check_logits(logits, ref, f"{wl_name} logits")
+    np.testing.assert_array_equal(amax, np.argmax(logits, axis=1))
+    parity.check_argmax(amax, ref, wl_name)
+    parity.check_walk(parent, tok, amax, path, acc, nxt, ref, wl_name)
+    _log(f"{wl_name}: logits max abs {err:.2e} rel {rel:.2e}; path {list(path)} next {nxt}")

@@ -65,10 +65,10 @@ def test_rope_sign_error_is_caught(setup, monkeypatch):
 
 
 def test_missing_residual_is_caught(setup, monkeypatch):
-    real = om._after_attention
+    real = om._ffn_residual
 
-    def no_ffn_residual(cfg, w, x, o, R):
-        y = real(cfg, w, x, o, R)
-        return y - x  # drops the residual stream
-    monkeypatch.setattr(om, "_after_attention", no_ffn_residual)
+    def no_ffn_residual(cfg, w, x, R):
+        y = real(cfg, w, x, R)
+        return y - x  # drops the residual stream around the feed-forward block
+    monkeypatch.setattr(om, "_ffn_residual", no_ffn_residual)
     assert _err(setup) > 1e-3
