@@ -1336,20 +1336,39 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
       sincosf((float)(p.prefix_len + dep) * rope_inv_freq(jj, p.Dh, p.log2_theta), &sn, &cs);
       st_coherent2(p.rope + ((size_t)m * (p.Dh / 2) + jj) * 2, cs, sn);
     }
-    const bf16* row = E + (size_t)tree.tok[m] * p.d;
-    const bf16* g0 = (const bf16*)(p.packed + p.layer0 + p.o_attn_norm);
-    for (int c = threadIdx.x; c < p.d; c += kThreads) {
-      const float v = bf2f(ldg(row + c));
-      st_coherent(&p.x[(size_t)m * p.d + c], v);
-      const float xg = v * bf2f(ldg(g0 + c));
+  }
+  // The stream's first version, dealt out over every workgroup by element
+  // (node m, column c) in row-major order -- 16 consecutive lanes hold one
+  // 16-column block of one row -- with each thread's loads all issued before
+  // its stores.
+  const bf16* g0 = (const bf16*)(p.packed + p.layer0 + p.o_attn_norm);
+  const int total = p.n * p.d, stride = p.G * kThreads;
+  constexpr int PER = 4;
+  for (int base = blockIdx.x * kThreads; base < total; base += PER * stride) {
+    float v[PER], g[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int e = base + k * stride + threadIdx.x;
+      const int m = e < total ? e / p.d : 0, c = e < total ? e % p.d : 0;
+      v[k] = e < total ? bf2f(ldg(E + (size_t)tree.tok[m] * p.d + c)) : 0.0f;
+      g[k] = e < total ? bf2f(ldg(g0 + c)) : 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int e = base + k * stride + threadIdx.x;
+      const int m = e / p.d, c = e % p.d;
+      const float xg = v[k] * g[k];
       const float xg1 = __shfl_down(xg, 1, kWave);
-      if ((c & 1) == 0) st_coherent_bf2(p.xg + frag_off(m, c, MB), xg, xg1);
-      float s = v * v;
-      s += __shfl_xor(s, 8, kWave);
-      s += __shfl_xor(s, 4, kWave);
-      s += __shfl_xor(s, 2, kWave);
-      s += __shfl_xor(s, 1, kWave);
-      if ((lane & 15) == 0) st_coherent(&p.ssq[(size_t)(c / kNB) * p.Mp + m], s);
+      float sq = v[k] * v[k];  // sum of squares over the 16-column block
+      sq += __shfl_xor(sq, 8, kWave);
+      sq += __shfl_xor(sq, 4, kWave);
+      sq += __shfl_xor(sq, 2, kWave);
+      sq += __shfl_xor(sq, 1, kWave);
+      if (e < total) {
+        st_coherent(&p.x[(size_t)m * p.d + c], v[k]);
+        if ((c & 1) == 0) st_coherent_bf2(p.xg + frag_off(m, c, MB), xg, xg1);
+        if ((lane & 15) == 0) st_coherent(&p.ssq[(size_t)(c / kNB) * p.Mp + m], sq);
+      }
     }
   }
 }
