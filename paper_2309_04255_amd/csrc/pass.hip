@@ -610,7 +610,7 @@ __device__ __forceinline__ void row_rstd(KParams& p, const float* ssq, GemmLds& 
   const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
   float ss = 0.0f;
   if (r < p.n) {
-    constexpr int PER = 8;
+    constexpr int PER = 32;  // (d/16 per chunk at d = 4096 and 32 rows: one round)
     for (int t = t0; t < t1; t += PER) {
       float v[PER];
 #pragma unroll
@@ -757,29 +757,45 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
 // node (lowest index among equally deep ones).
 __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl) {
   const int wave = wave_index(), lane = threadIdx.x & 63;
-  for (int r = wave; r < p.n; r += kWaves) {
-    float mv = -INFINITY;
-    int mi = 0x7fffffff;
-    for (int t0 = 0; t0 < entries; t0 += 4 * 64) {
-      float v[4];
-      int ix[4];
+  constexpr int RB = 4;  // rows per wave whose partials are loaded together
+  for (int r0 = wave; r0 < p.n; r0 += kWaves * RB) {
+    float mv[RB];
+    int mi[RB];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int t = t0 + 64 * u + lane;
-        v[u] = t < entries ? ld_coherent(&p.lm_val[(size_t)t * p.Mp + r]) : -INFINITY;
-        ix[u] = t < entries ? ld_coherent(&p.lm_idx[(size_t)t * p.Mp + r]) : 0x7fffffff;
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (v[u] > mv || (v[u] == mv && ix[u] < mi)) {
-          mv = v[u];
-          mi = ix[u];
-        }
+    for (int k = 0; k < RB; ++k) {
+      mv[k] = -INFINITY;
+      mi[k] = 0x7fffffff;
     }
-    wave_argmax(mv, mi);
-    if (lane == 0) {
-      stg(p.amax + r, mi);
-      gl.amax[r] = mi;
+    for (int t0 = 0; t0 < entries; t0 += 4 * 64) {
+      float v[RB][4];
+      int ix[RB][4];
+#pragma unroll
+      for (int k = 0; k < RB; ++k)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int t = t0 + 64 * u + lane, r = r0 + kWaves * k;
+          const bool on = t < entries && r < p.n;
+          v[k][u] = on ? ld_coherent(&p.lm_val[(size_t)t * p.Mp + r]) : -INFINITY;
+          ix[k][u] = on ? ld_coherent(&p.lm_idx[(size_t)t * p.Mp + r]) : 0x7fffffff;
+        }
+#pragma unroll
+      for (int k = 0; k < RB; ++k)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (v[k][u] > mv[k] || (v[k][u] == mv[k] && ix[k][u] < mi[k])) {
+            mv[k] = v[k][u];
+            mi[k] = ix[k][u];
+          }
+    }
+#pragma unroll
+    for (int k = 0; k < RB; ++k) {
+      const int r = r0 + kWaves * k;
+      if (r >= p.n) break;
+      wave_argmax(mv[k], mi[k]);
+      if (lane == 0) {
+        stg(p.amax + r, mi[k]);
+        gl.amax[r] = mi[k];
+      }
     }
   }
   for (int i = threadIdx.x; i < p.n; i += kThreads) {
