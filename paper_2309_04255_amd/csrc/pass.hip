@@ -92,6 +92,17 @@ __device__ __forceinline__ size_t frag_off(int row, int col, int MB) {
          (col & 7);
 }
 
+// Workgroups are dispatched to the GPU's 8 XCDs round-robin (workgroup w
+// runs on XCD w % 8).  Phases deal out their work by this virtual index,
+// which runs XCD by XCD: each XCD gets a contiguous, equal share, so shares
+// that differ by a block spread evenly over the XCDs (dealt by w itself,
+// every 8th workgroup would take the larger share, all on the same XCDs).
+constexpr int kXcds = 8;
+__device__ __forceinline__ int virtual_wg(int G) {
+  const int w = blockIdx.x;
+  return G % kXcds == 0 ? (w % kXcds) * (G / kXcds) + w / kXcds : w;
+}
+
 // ------------------------------------------------------------------ sync
 
 struct Sync {
@@ -890,8 +901,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   const StepPlan& sp = p.step[step];
   constexpr int CM = MB <= 2 ? 8 : 16 / MB;
   const int nbk = sp.nblocks, G = p.G;
-  const int lo = wave_uniform((int)((long)blockIdx.x * nbk / G));
-  const int hi = wave_uniform((int)((long)(blockIdx.x + 1) * nbk / G));
+  const int vw = virtual_wg(G);
+  const int lo = wave_uniform((int)((long)vw * nbk / G));
+  const int hi = wave_uniform((int)((long)(vw + 1) * nbk / G));
   if constexpr (EPI == EPI_LOGITS) {
     for (int r = threadIdx.x; r < 16 * MB; r += kThreads) {
       gl.best_v[r] = -INFINITY;
@@ -1037,7 +1049,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
   };
   auto list_chunk = [&](int c_lo, int c_hi, int j) { return c_lo + j < c_hi ? c_lo + j : npc; };
 
-  int u = blockIdx.x;
+  int u = virtual_wg(p.G);
   int staged = 0;  // list entries (bit j: entry j, j < 2) already in LDS
   if (u < units) {
     const int h = u / (rbn * KS), ks = u % KS;
@@ -1419,8 +1431,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool final_norm_phase(KPar
   row_rstd<MB>(p, p.ssq + (size_t)(2 * p.L) * p.d_nb * p.Mp, gl);
   const float* x = p.x + (size_t)(2 * p.L) * p.Mp * p.d;
   const bf16* g = (const bf16*)(p.packed + p.o_final_norm);
-  const int lo = wave_uniform((int)((long)blockIdx.x * p.d_nb / p.G));
-  const int hi = wave_uniform((int)((long)(blockIdx.x + 1) * p.d_nb / p.G));
+  const int vw = virtual_wg(p.G);
+  const int lo = wave_uniform((int)((long)vw * p.d_nb / p.G));
+  const int hi = wave_uniform((int)((long)(vw + 1) * p.d_nb / p.G));
   for (int e = threadIdx.x; e < (hi - lo) * ROWS * (kNB / 2); e += kThreads) {
     const int pr = e % (kNB / 2), r = (e / (kNB / 2)) % ROWS, b = lo + e / ((kNB / 2) * ROWS);
     const int c = kNB * b + 2 * pr;
