@@ -247,75 +247,40 @@ __device__ __forceinline__ void dma16(const void* src, char* lds) {
                                    (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
-// What one GEMM step reads and writes in a given layer.  The activations of
-// every step are fragment-order bf16 [Mp][K]: the attention output, the
-// SwiGLU product, or, for the steps behind an RMSNorm, bf16(x * g) of the
-// residual version x with that norm's gain g; the norm's per-row scale
-// 1 / sqrt(mean(x^2) + eps) is then applied to the step's output rows.
+// Where the epilogue of one GEMM step writes in a given layer, and the sums
+// of squares of the residual version a norm step reads.  Every field is
+// assigned for every step by branch-free selects: built behind a switch on
+// the (run-time) step, the structure would live in scratch memory, and each
+// output store would first wait for a scratch reload queued behind the
+// previous store.
 struct StepIo {
-  const bf16x8* w;   // packed matrix
-  int ks;            // k-steps (K / 32)
-  bool norm;         // rows of the output are scaled by the norm's rstd
-  const bf16x8* a;   // fragment-order activations
-  const float* ssq;  // norm: [d/16][Mp] sums of squares of the residual version
-  // epilogue
+  const float* ssq;  // norm steps: [d/16][Mp] sums of squares of the residual version
   bf16* q;           // QKV: [Mp][d] queries after the rotary embedding
   bf16* kc;          // QKV: K cache of this layer [H][cap][Dh]
   bf16* vc;          // QKV: V cache of this layer [H][cap][Dh]
-  const float* x_in; // RESID: [Mp][d]
   float* x_out;      // RESID: [Mp][d]
   float* ssq_out;    // RESID: [d/16][Mp]
   bf16* xg_out;      // RESID: fragment-order bf16(x_out * g_next)
-  const bf16* g_next;  // RESID: gain of the norm that reads x_out
   bf16* h;           // SWIGLU: fragment-order [Mp][Fp]
 };
 
+template <int EPI>
 __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
   const size_t xsz = (size_t)p.Mp * p.d, ssz = (size_t)p.d_nb * p.Mp;
-  const char* lw = p.packed + p.layer0 + (long long)l * p.layer_bytes;
-  const StepPlan& sp = p.step[step];
-  StepIo io{};
-  io.w = (const bf16x8*)((sp.layer_rel ? lw : p.packed) + sp.w_off);
-  io.ks = sp.ksteps;
-  switch (step) {
-    case STEP_QKV:
-      io.norm = true;
-      io.a = (const bf16x8*)(p.xg + (size_t)(2 * l) * xsz);
-      io.ssq = p.ssq + (size_t)(2 * l) * ssz;
-      io.q = p.q + (size_t)l * p.Mp * p.d;
-      io.kc = p.k_cache + (size_t)l * p.H * p.cap * p.Dh;
-      io.vc = p.v_cache + (size_t)l * p.H * p.cap * p.Dh;
-      break;
-    case STEP_O:
-      io.norm = false;
-      io.a = (const bf16x8*)(p.o + (size_t)l * xsz);
-      io.x_in = p.x + (size_t)(2 * l) * xsz;
-      io.x_out = p.x + (size_t)(2 * l + 1) * xsz;
-      io.ssq_out = p.ssq + (size_t)(2 * l + 1) * ssz;
-      io.xg_out = p.xg + (size_t)(2 * l + 1) * xsz;
-      io.g_next = (const bf16*)(lw + p.o_ffn_norm);
-      break;
-    case STEP_GATE_UP:
-      io.norm = true;
-      io.a = (const bf16x8*)(p.xg + (size_t)(2 * l + 1) * xsz);
-      io.ssq = p.ssq + (size_t)(2 * l + 1) * ssz;
-      io.h = p.h + (size_t)l * p.Mp * p.Fp;
-      break;
-    case STEP_DOWN:
-      io.norm = false;
-      io.a = (const bf16x8*)(p.h + (size_t)l * p.Mp * p.Fp);
-      io.x_in = p.x + (size_t)(2 * l + 1) * xsz;
-      io.x_out = p.x + (size_t)(2 * l + 2) * xsz;
-      io.ssq_out = p.ssq + (size_t)(2 * l + 2) * ssz;
-      io.xg_out = p.xg + (size_t)(2 * l + 2) * xsz;
-      io.g_next = l + 1 < p.L ? (const bf16*)(lw + p.layer_bytes + p.o_attn_norm)
-                              : (const bf16*)(p.packed + p.o_final_norm);
-      break;
-    default:  // STEP_LM: its input is the final norm's output, already scaled
-      io.norm = false;
-      io.a = (const bf16x8*)p.xnf;
-      break;
-  }
+  const size_t kv = (size_t)l * p.H * p.cap * p.Dh;
+  // residual version read by a norm step (QKV 2l, gate/up 2l+1) or written
+  // by a residual step (O 2l+1, down 2l+2)
+  const int ver_in = EPI == EPI_SWIGLU ? 2 * l + 1 : 2 * l;
+  const int ver_out = step == STEP_DOWN ? 2 * l + 2 : 2 * l + 1;
+  StepIo io;
+  io.ssq = p.ssq + (size_t)ver_in * ssz;
+  io.q = p.q + (size_t)l * xsz;
+  io.kc = p.k_cache + kv;
+  io.vc = p.v_cache + kv;
+  io.x_out = p.x + (size_t)ver_out * xsz;
+  io.ssq_out = p.ssq + (size_t)ver_out * ssz;
+  io.xg_out = p.xg + (size_t)ver_out * xsz;
+  io.h = p.h + (size_t)l * p.Mp * p.Fp;
   return io;
 }
 
@@ -858,7 +823,7 @@ __device__ __attribute__((noinline, not_tail_called)) void finish_tile(KParams& 
   layer = wave_uniform(layer);
   nb0 = wave_uniform(nb0);
   cw = wave_uniform(cw);
-  const StepIo io = step_io(p, step, layer);
+  const StepIo io = step_io<EPI>(p, step, layer);
   if constexpr (EPI == EPI_QKV || EPI == EPI_SWIGLU) row_scales<MB>(p, io, gl);
   const int units = cw * MB;
   for (int u = wave_index(); u < units; u += kWaves) {
