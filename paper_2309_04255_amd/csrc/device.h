@@ -98,6 +98,49 @@ __device__ __forceinline__ void wave_argmax(float& v, int& idx) {
   }
 }
 
+// Lane moves inside each row of 16 lanes, on the vector ALU (DPP), for the
+// epilogues' reductions and neighbour exchanges: a __shfl is a ds_bpermute,
+// an LDS round trip, and a chain of dependent ones serialises.
+constexpr int kDppQuadXor1 = 0xB1;       // quad_perm [1,0,3,2]: reads lane ^ 1
+constexpr int kDppQuadXor2 = 0x4E;       // quad_perm [2,3,0,1]: reads lane ^ 2
+constexpr int kDppRowShl1 = 0x101;       // row_shl:1: lane i of a row reads lane i + 1 (lane 15 gets 0)
+constexpr int kDppRowRor8 = 0x128;       // row_ror:8: reads lane (i + 8) mod 16, i.e. lane ^ 8
+constexpr int kDppRowMirror = 0x140;     // reads lane 15 - i of the row
+constexpr int kDppRowHalfMirror = 0x141; // reads lane 7 - i of the half row
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
+}
+// Sum over the 16 lanes of each row (quads first, then half rows, then the
+// row); every lane gets the same bits (each step adds a pair in both orders).
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f<kDppQuadXor1>(v);
+  v += dpp_f<kDppQuadXor2>(v);
+  v += dpp_f<kDppRowHalfMirror>(v);
+  v += dpp_f<kDppRowMirror>(v);
+  return v;
+}
+// Max with the lowest index among equal values, over the 16 lanes of each row.
+template <int CTRL>
+__device__ __forceinline__ void argmax_step(float& v, int& idx) {
+  const float ov = dpp_f<CTRL>(v);
+  const int oi = dpp_i<CTRL>(idx);
+  if (ov > v || (ov == v && oi < idx)) {
+    v = ov;
+    idx = oi;
+  }
+}
+__device__ __forceinline__ void row16_argmax(float& v, int& idx) {
+  argmax_step<kDppQuadXor1>(v, idx);
+  argmax_step<kDppQuadXor2>(v, idx);
+  argmax_step<kDppRowHalfMirror>(v, idx);
+  argmax_step<kDppRowMirror>(v, idx);
+}
+
 // Workgroup barrier for LDS hand-offs only: waits for this wave's LDS
 // accesses, not for its global loads (__syncthreads also drains every global
 // load in flight, which would defeat a prefetch issued before it).

@@ -72,7 +72,7 @@ struct PassParams {
   float* attn_ml;   // [H][MB][KS][16][2]  their running max and sum
   int attn_splits;  // KS, key splits per (head, row block): 1 to 4
   int* head_cnt;    // [H][MB] arrivals of the key splits
-  float* lm_val;    // [G][Mp] LM-head argmax per workgroup
+  float* lm_val;    // [Mp][G] LM-head argmax per row and workgroup
   int* lm_idx;
   int* amax;        // [Mp]
   // outputs

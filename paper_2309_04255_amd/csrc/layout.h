@@ -143,8 +143,8 @@ struct WorkspaceLayout {
   size_t tree;         // int32 tok[128] | parent[128] | depth[128] | pos[128] | uint32 anc[128][4]
   size_t rope;         // fp32 [Mp][Dh/2][2]      cos, sin of every node's rotary angles
   size_t amax;         // int32 [Mp]              per-node greedy token
-  size_t lm_val;       // fp32 [G][Mp]            LM-head argmax per workgroup
-  size_t lm_idx;       // int32 [G][Mp]
+  size_t lm_val;       // fp32 [Mp][G]            LM-head argmax per row and workgroup
+  size_t lm_idx;       // int32 [Mp][G]
   size_t xs;           // fp32 [2L+1][Mp][d]      residual stream versions
   size_t xgs;          // bf16 [2L+1] x (Mp x d, fragment order)  bf16(x * g) (g: its norm's gain)
   size_t xnf;          // bf16 Mp x d, fragment order   the final norm's output bf16(x rstd g)

@@ -654,9 +654,9 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
       for (int i = 0; i < 4; ++i) {
         const int rr = rr0 + i, r = 16 * rb + rr;
         const float2 cs = lds_ld<float2>(csu + (size_t)(rr * 8 + (j & 7)) * 8);
-        const float partner = __shfl_xor(v[i], 8, kWave);
+        const float partner = dpp_f<kDppRowRor8>(v[i]);
         const float outv = j < 8 ? v[i] * cs.x - partner * cs.y : v[i] * cs.x + partner * cs.y;
-        const float nxt = __shfl_down(outv, 1, kWave);
+        const float nxt = dpp_f<kDppRowShl1>(outv);
         if (r < p.n && (j & 1) == 0) {
           bf16* dst = part == 0 ? base + (size_t)r * d : base + (size_t)(p.prefix_len + r) * dh;
           st_coherent_bf2(dst + dim, outv, nxt);
@@ -667,7 +667,7 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 16 * rb + rr0 + i;
-        const float nxt = __shfl_down(v[i], 1, kWave);
+        const float nxt = dpp_f<kDppRowShl1>(v[i]);
         if (r < p.n && (j & 1) == 0)
           st_coherent_bf2(io.vc + ((size_t)hh * p.cap + p.prefix_len + r) * dh + dim, v[i], nxt);
       }
@@ -679,16 +679,12 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
     for (int i = 0; i < 4; ++i) {
       const int rr = rr0 + i, r = 16 * rb + rr;
       const float xn = r < p.n ? lds_ld<float>(xu + (size_t)(rr * 16 + j) * 4) + v[i] : 0.0f;
-      const float xn1 = __shfl_down(xn, 1, kWave);
+      const float xn1 = dpp_f<kDppRowShl1>(xn);
       if (r < p.n && (j & 1) == 0) st_coherent2(io.x_out + (size_t)r * p.d + col, xn, xn1);
       const float xg = xn * g;
-      const float xg1 = __shfl_down(xg, 1, kWave);
+      const float xg1 = dpp_f<kDppRowShl1>(xg);
       if (r < p.n && (j & 1) == 0) st_coherent_bf2(io.xg_out + frag_off(r, col, MB), xg, xg1);
-      float sq = xn * xn;  // sum of squares over the block's 16 columns
-      sq += __shfl_xor(sq, 8, kWave);
-      sq += __shfl_xor(sq, 4, kWave);
-      sq += __shfl_xor(sq, 2, kWave);
-      sq += __shfl_xor(sq, 1, kWave);
+      const float sq = row16_sum(xn * xn);  // sum of squares over the block's 16 columns
       if (j == 0 && r < p.n) st_coherent(io.ssq_out + (size_t)nb * p.Mp + r, sq);
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
@@ -696,9 +692,9 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = 16 * rb + rr0 + i;
-      const float up = __shfl_xor(v[i], 8, kWave);
+      const float up = dpp_f<kDppRowRor8>(v[i]);
       const float hv = v[i] / (1.0f + expf(-v[i])) * up;
-      const float nxt = __shfl_down(hv, 1, kWave);
+      const float nxt = dpp_f<kDppRowShl1>(hv);
       if (r < p.n && j < 8 && (j & 1) == 0) st_coherent_bf2(io.h + frag_off(r, f, MB), hv, nxt);
     }
   } else {  // EPI_LOGITS
@@ -710,15 +706,7 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
       if (valid && p.logits != nullptr && r >= p.row_lo) stg(p.logits + (size_t)(r - p.row_lo) * p.V + col, v[i]);
       float mv = valid ? v[i] : -INFINITY;
       int mi = valid ? col : 0x7fffffff;
-#pragma unroll
-      for (int off = 8; off >= 1; off >>= 1) {  // argmax over the block's 16 columns
-        const float ov = __shfl_xor(mv, off, kWave);
-        const int oi = __shfl_xor(mi, off, kWave);
-        if (ov > mv || (ov == mv && oi < mi)) {
-          mv = ov;
-          mi = oi;
-        }
-      }
+      row16_argmax(mv, mi);  // argmax over the block's 16 columns
       if (j == 0) {
         gl.red_v[r][c] = mv;
         gl.red_i[r][c] = mi;
@@ -751,8 +739,8 @@ __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl
         for (int u = 0; u < 4; ++u) {
           const int t = t0 + 64 * u + lane, r = r0 + kWaves * k;
           const bool on = t < entries && r < p.n;
-          v[k][u] = on ? ld_coherent(&p.lm_val[(size_t)t * p.Mp + r]) : -INFINITY;
-          ix[k][u] = on ? ld_coherent(&p.lm_idx[(size_t)t * p.Mp + r]) : 0x7fffffff;
+          v[k][u] = on ? ld_coherent(&p.lm_val[(size_t)r * p.G + t]) : -INFINITY;
+          ix[k][u] = on ? ld_coherent(&p.lm_idx[(size_t)r * p.G + t]) : 0x7fffffff;
         }
 #pragma unroll
       for (int k = 0; k < RB; ++k)
@@ -893,8 +881,8 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   if constexpr (EPI == EPI_LOGITS) {
     __syncthreads();
     for (int r = threadIdx.x; r < 16 * MB; r += kThreads) {
-      st_coherent(&p.lm_val[(size_t)blockIdx.x * p.Mp + r], gl.best_v[r]);
-      st_coherent(&p.lm_idx[(size_t)blockIdx.x * p.Mp + r], gl.best_i[r]);
+      st_coherent(&p.lm_val[(size_t)r * G + blockIdx.x], gl.best_v[r]);
+      st_coherent(&p.lm_idx[(size_t)r * G + blockIdx.x], gl.best_i[r]);
     }
     if (arrive_last(p.lm_cnt, G, lds_flag)) finish_walk(p, G, gl);
   }
@@ -1351,12 +1339,8 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
       const int e = base + k * stride + threadIdx.x;
       const int m = e / p.d, c = e % p.d;
       const float xg = v[k] * g[k];
-      const float xg1 = __shfl_down(xg, 1, kWave);
-      float sq = v[k] * v[k];  // sum of squares over the 16-column block
-      sq += __shfl_xor(sq, 8, kWave);
-      sq += __shfl_xor(sq, 4, kWave);
-      sq += __shfl_xor(sq, 2, kWave);
-      sq += __shfl_xor(sq, 1, kWave);
+      const float xg1 = dpp_f<kDppRowShl1>(xg);
+      const float sq = row16_sum(v[k] * v[k]);  // sum of squares over the 16-column block
       if (e < total) {
         st_coherent(&p.x[(size_t)m * p.d + c], v[k]);
         if ((c & 1) == 0) st_coherent_bf2(p.xg + frag_off(m, c, MB), xg, xg1);
