@@ -14,6 +14,9 @@ Contents
   walk.py   greedy acceptance: branch correct sequences, the correct token
             tree and its depth-first longest path (§3.2 "Depth-first verified
             sequence searching")
+  decode.py greedy decoding, plainly and by the generate-and-verify loop
+            with rollback of the token tree to its verified sequence (§3.1,
+            §3.2 "Token tree verification and rectification")
 
 Every function is pinned by tests/test_oracle_*.py against something other
 than itself: brute force, an independent library implementation
@@ -37,3 +40,4 @@ from .model import (  # noqa: F401
     verify_tree,
 )
 from .walk import accept_walk, branch_sequences, correct_sequences  # noqa: F401
+from .decode import commit_path, greedy_decode, speculative_decode  # noqa: F401

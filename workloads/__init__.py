@@ -22,4 +22,5 @@ from .trees import (  # noqa: F401
     draw_tokens,
     make_tree,
     plant_path,
+    draft_tree,
 )

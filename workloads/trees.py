@@ -101,3 +101,13 @@ def plant_path(parent, tree_tokens, leaf: int, continuation, vocab: int):
             if sib != node and tok[sib] == c_k:
                 tok[sib] = (c_k + 1) % vocab
     return tok
+
+
+def draft_tree(parent, root_token: int, continuation, K: int, leaf: int, vocab: int, seed: int):
+    """Draft tokens for a tree of the given shape: the root carries root_token,
+    every other node a uniform draw, and the root->leaf branch has the first K
+    tokens of `continuation` (the target's greedy tokens after the root,
+    supplied by the caller) planted, then a wrong token (plant_path)."""
+    tok = draw_tokens(len(parent), vocab, seed, stream=2)
+    tok[0] = root_token
+    return plant_path(parent, tok, leaf, list(continuation)[: K + 1], vocab)
