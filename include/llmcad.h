@@ -158,6 +158,33 @@ int llmcad_prefill(const llmcad_config* cfg, const void* packed, void* k_cache, 
                    int32_t capacity, const int32_t* tokens, int32_t n_tokens, int32_t start_pos,
                    float* last_logits, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Rollback to the verified sequence after a verification pass (§3.2 "Token
+ * tree verification and rectification": the tree is rolled back to the
+ * verified sequence, which becomes the new input; §3.1: generation then
+ * continues from the target's token after it).
+ *
+ * path and accept_len are device buffers holding llmcad_verify_tree's outputs
+ * for a tree of n nodes verified at prefix_len (they are read on the stream,
+ * after that pass).  For every layer and head, the keys and values of cache
+ * slot prefix_len + path[k] move to slot prefix_len + k, k = 1..accept_len
+ * (path[0] = 0, the root, is in place).  The cache then holds the accepted
+ * sequence -- the prefix, the root and the accepted draft tokens, each at the
+ * position it was verified at -- in slots [0, prefix_len + accept_len + 1):
+ * the next pass uses prefix_len' = prefix_len + accept_len + 1 with the
+ * returned next token as its root.  Slots past that are left as they are.
+ * Asynchronous on `stream`; allocates nothing.
+ *
+ * Errors (checked on the host, nothing enqueued): LLMCAD_EARG for a NULL
+ * pointer, LLMCAD_ETREE unless 1 <= n <= 128, LLMCAD_ECAPACITY unless
+ * 0 <= prefix_len and prefix_len + n <= capacity.  Device-side values
+ * outside what a pass over n nodes writes (accept_len not in [0, n), an entry
+ * path[k] not in [k, n)) move nothing for the affected rows.
+ */
+int llmcad_commit_path(const llmcad_config* cfg, void* k_cache, void* v_cache, int32_t capacity,
+                       int32_t prefix_len, const int32_t* path, const int32_t* accept_len, int32_t n,
+                       void* stream);
+
 /* Static text for a status code. */
 const char* llmcad_status_string(int status);
 

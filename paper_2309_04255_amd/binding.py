@@ -32,6 +32,7 @@ SYMBOLS = (
     "llmcad_workspace_init",
     "llmcad_verify_tree",
     "llmcad_prefill",
+    "llmcad_commit_path",
     "llmcad_status_string",
     "llmcad_workspace_region",
     "llmcad_timing_enable",
@@ -84,6 +85,7 @@ def _load():
         "llmcad_verify_tree": (ctypes.c_int, [CFG, P, P, P, I32, I32, I32P, I32P, I32, P, P, P, P,
                                               P, SZ, P]),
         "llmcad_prefill": (ctypes.c_int, [CFG, P, P, P, I32, I32P, I32, I32, P, P, SZ, P]),
+        "llmcad_commit_path": (ctypes.c_int, [CFG, P, P, I32, I32, P, P, I32, P]),
         "llmcad_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "llmcad_workspace_region": (ctypes.c_int, [CFG, I32, I32, ctypes.POINTER(SZ),
                                                    ctypes.POINTER(SZ)]),
@@ -199,6 +201,18 @@ def prefill(cfg, packed, k_cache, v_cache, tokens, start_pos: int, last_logits, 
     return rc
 
 
+def commit_path(cfg, k_cache, v_cache, prefix_len: int, path, accept_len, n: int, stream=None,
+                raise_on_error=True) -> int:
+    """Rollback to the verified sequence: path/accept_len are the device outputs of the
+    verification pass over n nodes at prefix_len (see llmcad_commit_path)."""
+    cap = k_cache.shape[-2]
+    rc = _lib.llmcad_commit_path(ctypes.byref(cfg), _ptr(k_cache), _ptr(v_cache), int(cap), int(prefix_len),
+                                 _ptr(path), _ptr(accept_len), int(n), _stream(stream))
+    if raise_on_error:
+        _check(rc, "llmcad_commit_path")
+    return rc
+
+
 def workspace_region(cfg, n: int, which: int):
     off, size = ctypes.c_size_t(), ctypes.c_size_t()
     _check(_lib.llmcad_workspace_region(ctypes.byref(cfg), int(n), int(which), ctypes.byref(off),
@@ -262,6 +276,10 @@ class Session:
                     parent, self.logits if want_logits else None, self.path, self.accept_len,
                     self.next_token, self.workspace)
         return n
+
+    def commit(self, prefix_len, n):
+        """Roll the cache back to the verified sequence of the last verify_tree over n nodes."""
+        commit_path(self.cfg, self.k_cache, self.v_cache, prefix_len, self.path, self.accept_len, n)
 
     def results(self, n):
         """Synchronise and return (logits [n, V] fp32 cpu, path list, accept_len, next_token)."""

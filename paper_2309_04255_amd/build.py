@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libllmcad.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "pass.hip", "pack.hip"]
+SOURCES = ["api.hip", "pass.hip", "pack.hip", "commit.hip"]
 
 
 def hipcc() -> str:

@@ -328,6 +328,20 @@ int llmcad_verify_tree(const llmcad_config* cfg, const void* packed, void* k_cac
   return run_pass(a, tree);
 }
 
+int llmcad_commit_path(const llmcad_config* cfg, void* k_cache, void* v_cache, int32_t capacity,
+                       int32_t prefix_len, const int32_t* path, const int32_t* accept_len, int32_t n,
+                       void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!k_cache || !v_cache || !path || !accept_len) return LLMCAD_EARG;
+  if (n < 1 || n > kMaxNodes) return LLMCAD_ETREE;
+  if (capacity < 1 || prefix_len < 0 || (long)prefix_len + n > capacity) return LLMCAD_ECAPACITY;
+  if (n == 1) return LLMCAD_OK;  // only the root, already in place
+  HIP_TRY(launch_commit(k_cache, v_cache, cfg->n_layers * cfg->n_heads, capacity, prefix_len, path, accept_len, n,
+                        cfg->head_dim, (hipStream_t)stream));
+  return LLMCAD_OK;
+}
+
 int llmcad_prefill(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
                    int32_t capacity, const int32_t* tokens, int32_t n_tokens, int32_t start_pos,
                    float* last_logits, void* workspace, size_t workspace_bytes, void* stream) {

@@ -17,6 +17,13 @@ enum PackKind { PACK_PLAIN = 0, PACK_GATE_UP = 1, PACK_QKV_ROPE = 2 };
 hipError_t launch_pack(const void* w, int N, int K, void* out, int nblocks, int ksteps, int kind,
                        int aux, hipStream_t st);
 
+// ---- rollback to the verified sequence (commit.hip): for each of the
+// layers_heads (layer, head) row sets of the cache, slot prefix_len + path[k]
+// -> prefix_len + k for k = 1..*accept_len (path and accept_len in device
+// memory; n = the pass's node count bounds both).  LDS: 2 n dh bf16.
+hipError_t launch_commit(void* k_cache, void* v_cache, int layers_heads, int cap, int prefix_len, const int* path,
+                         const int* accept_len, int n, int dh, hipStream_t st);
+
 // ---- the verification pass as one persistent launch (pass.hip)
 struct TreeArgs {
   int32_t tok[128];

@@ -135,3 +135,18 @@ def test_prefill_validation(binding):
     rc = lib.llmcad_prefill(ctypes.byref(cfg), fake, fake, fake, 64, toks.ctypes.data_as(I32P), 3, 0,
                             None, fake, 100, None)
     assert rc == binding.EWORKSPACE
+
+
+def test_commit_validation(binding):
+    # Host-side checks of the rollback entry point; none of these calls
+    # enqueues anything (n = 1 leaves the root in place and returns at once).
+    cfg = binding.make_config(workloads.MODELS["tiny"])
+    lib = binding.lib()
+    fake = ctypes.c_void_p(256)
+    assert lib.llmcad_commit_path(ctypes.byref(cfg), None, fake, 64, 10, fake, fake, 4, None) == binding.EARG
+    assert lib.llmcad_commit_path(ctypes.byref(cfg), fake, fake, 64, 10, None, fake, 4, None) == binding.EARG
+    assert lib.llmcad_commit_path(ctypes.byref(cfg), fake, fake, 64, 10, fake, fake, 0, None) == binding.ETREE
+    assert lib.llmcad_commit_path(ctypes.byref(cfg), fake, fake, 64, 10, fake, fake, 129, None) == binding.ETREE
+    assert lib.llmcad_commit_path(ctypes.byref(cfg), fake, fake, 64, 61, fake, fake, 4, None) == binding.ECAPACITY
+    assert lib.llmcad_commit_path(ctypes.byref(cfg), fake, fake, 64, -1, fake, fake, 4, None) == binding.ECAPACITY
+    assert lib.llmcad_commit_path(ctypes.byref(cfg), fake, fake, 64, 10, fake, fake, 1, None) == binding.OK
