@@ -175,6 +175,81 @@ def cpu_baseline(shape, P, n, seed):
     }
 
 
+def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
+    """The generate-and-verify loop (verify, roll back, continue) on the bench
+    workload's tree.  Before each iteration the target's own greedy
+    continuation from the loop's current context is taken from one-node
+    passes (plain greedy decoding, untimed), and `planted` of its tokens are
+    planted along one deepest branch of the tree, the other nodes uniform.
+    Timed per iteration: the verification pass, the rollback kernel and the
+    read-back of accept_len / next token that the host needs for the next
+    tree.  Also times the rollback kernel alone."""
+    import numpy as np
+    import torch
+
+    import workloads
+
+    n = len(parent)
+    leaf = n - 1
+
+    def greedy_from(plen, root, k):
+        out = []
+        for t in range(k):
+            sess.verify_tree(plen + t, np.array([root]), np.array([-1]), want_logits=False)
+            root = int(sess.next_token.item())
+            out.append(root)
+        return out
+
+    plen, root = P, int(tok[0])
+    accs, t_loop, made = [], 0.0, 0
+    last = None
+    for it in range(iterations + 1):  # the first iteration warms up
+        cont = greedy_from(plen, root, planted + 1)
+        ptok = workloads.draft_tree(parent, root, cont, planted, leaf, shape.vocab, seed=it)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        sess.verify_tree(plen, ptok, parent, want_logits=False)
+        sess.commit(plen, n)
+        acc = int(sess.accept_len.item())
+        nxt = int(sess.next_token.item())
+        dt = time.perf_counter() - t
+        if it > 0:
+            t_loop += dt
+            made += acc + 1
+            accs.append(acc)
+        last = (plen, [int(x) for x in sess.path[: acc + 1].cpu()])
+        plen, root = plen + acc + 1, nxt
+    # rollback kernel alone: the last tree's accepted rows, moved again
+    # (the same rows, the same bytes)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 50
+    e0.record(stream)
+    for _ in range(reps):
+        sess.commit(last[0], n)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    commit_us = e0.elapsed_time(e1) * 1e3 / reps
+    moved = sum(1 for k, i in enumerate(last[1]) if i != k)
+    commit_bytes = 2 * 2 * moved * shape.n_layers * shape.n_heads * shape.head_dim * 2  # K+V, read+write
+    log(f"decode loop: {made} tokens in {iterations} passes, {t_loop * 1e3:.1f} ms; rollback {commit_us:.1f} us "
+        f"for {moved} rows per layer and head")
+    return {
+        "tokens_per_s": round(made / t_loop, 1),
+        "passes": iterations,
+        "tokens_per_pass": round(made / iterations, 3),
+        "ms_per_iteration": round(t_loop * 1e3 / iterations, 4),
+        "accept_lens": accs,
+        "draft": (f"{n}-node tree of the workload; {planted} tokens of the target's own greedy continuation "
+                  f"(one-node passes from the loop's context, untimed) planted along one depth-{planted} "
+                  f"branch, the other nodes uniform"),
+        "iteration": "verify pass + rollback kernel + read back accept_len / next token (host sync)",
+        "commit_us": round(commit_us, 2),
+        "commit_rows_moved": moved,
+        "commit_bytes": commit_bytes,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -182,6 +257,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama7b_p512_n31")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode-loop", action="store_true",
+                    help="skip the generate-and-verify loop measurement")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="(profiling) first copy this many MiB three times: the counter calibration")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -281,6 +358,8 @@ def main():
         sess.accept_len.cpu()
         lat.append(time.perf_counter() - t)
 
+    decode = None if args.no_decode_loop else decode_loop(sess, shape, P, parent, tok)
+
     frac = B / (elapsed / args.steps) / HBM_PEAK
     traffic = load_traffic(wl.name)
     out = {
@@ -320,6 +399,8 @@ def main():
             "mean_launch_us": round(k_ms * 1e3, 2),
         },
     }
+    if decode is not None:
+        out["decode_loop"] = decode
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (bounded sample)")
         out["cpu_baseline"] = cpu_baseline(shape, P, n, wl.seed)
