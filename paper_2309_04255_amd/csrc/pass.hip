@@ -390,16 +390,45 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
     for (int rb = 0; rb < MB; ++rb) ba[slot][rb] = ldg(opaque(live ? at + ((size_t)kWaves * i * MB + rb) * 64 : zero));
   };
 
-  // Epilogue inputs that do not depend on this phase's barrier (the residual
-  // stream and rotary table were written two or more phases ago; gains are
-  // weights): per (block, row block) unit 16 B per lane, plus each block's
-  // gains.  Loaded first, parked in LDS once they land.
   // Before the barrier, waves 1-3 start the weight stream: each its own
-  // register stages and LDS stages, wave 1 also wave 0's LDS stages.  Wave 0
+  // LDS stages (wave 1 also wave 0's), then its register stages.  Wave 0
   // polls the barrier and issues no load before it has seen it (a poll
   // waits for every older load of its wave).
   const int ns0 = (ks + kWaves - 1) / kWaves;
   const int P0 = wave_uniform(wait_phase >= 0 ? (ns0 / D * D < pcap ? ns0 / D * D : pcap) : 0);
+  // Epilogue inputs (residual stream or rotary table, and the next norm's
+  // gains; written two or more phases ago, so they need no barrier), by the
+  // last wave before the barrier: per (block, row block) unit 16 B per lane,
+  // then each block's gains, parked in LDS once they land -- before that
+  // wave's weight stages, so that the wait is for them alone (a wait behind
+  // a direct-to-LDS loop is a full drain).  After the barrier only the
+  // activations are then on the critical path.
+  constexpr int KU = C * MB;
+  constexpr int kEpiWave = kWaves - 1;
+  f32x4 sx[KU], sg[C];
+  if (wave == kEpiWave) {
+    const bool resid = io.resid;
+#pragma unroll
+    for (int u = 0; u < KU; ++u) {
+      const int c = u / MB, rb = u % MB;
+      const int col0 = kNB * (nb0 + c);
+      const f32x4* src = zero4;
+      if (resid) {  // residual rows 16 rb + l / 4, columns col0 + 4 (l % 4) .. + 3
+        src = (const f32x4*)(io.x_in + (size_t)(16 * rb + (lane >> 2)) * p.d + col0 + 4 * (lane & 3));
+      } else if (step == STEP_QKV && col0 < 2 * p.d) {  // (cos, sin) of pairs 8 t + 2 (l % 4), + 1
+        const int t = (col0 % p.d % p.Dh) / kNB;
+        src = (const f32x4*)(p.rope + ((size_t)(16 * rb + (lane >> 2)) * (p.Dh / 2) + 8 * t + 2 * (lane & 3)) * 2);
+      }
+      sx[u] = ldg(opaque(src));
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+      sg[c] = ldg(opaque(resid ? (const f32x4*)(io.g_next + kNB * (nb0 + c) + 8 * (lane & 1)) : zero4));
+#pragma unroll
+    for (int u = 0; u < KU; ++u) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)u * 1024 + lane * 16, sx[u]);
+#pragma unroll
+    for (int c = 0; c < C; ++c) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)(C * MB + c) * 1024 + lane * 16, sg[c]);
+  }
   if (wave != 0) {
     if constexpr (PMAX > 0) {
       for (int i = 0; i < P; ++i)
@@ -424,34 +453,6 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
     trace_mark(sy, wait_phase, 0);
     if (!grid_wait(sy, wait_phase, p.G)) return false;
     trace_mark(sy, wait_phase, 1);
-  }
-  // Epilogue inputs (residual stream or rotary table, and the next norm's
-  // gains; written two or more phases ago), by wave 0: per (block, row
-  // block) unit 16 B per lane, then each block's gains.
-  if (wave == 0) {
-    constexpr int KU = C * MB;
-    const bool resid = io.resid;
-    f32x4 sx[KU], sg[C];
-#pragma unroll
-    for (int u = 0; u < KU; ++u) {
-      const int c = u / MB, rb = u % MB;
-      const int col0 = kNB * (nb0 + c);
-      const f32x4* src = zero4;
-      if (resid) {  // residual rows 16 rb + l / 4, columns col0 + 4 (l % 4) .. + 3
-        src = (const f32x4*)(io.x_in + (size_t)(16 * rb + (lane >> 2)) * p.d + col0 + 4 * (lane & 3));
-      } else if (step == STEP_QKV && col0 < 2 * p.d) {  // (cos, sin) of pairs 8 t + 2 (l % 4), + 1
-        const int t = (col0 % p.d % p.Dh) / kNB;
-        src = (const f32x4*)(p.rope + ((size_t)(16 * rb + (lane >> 2)) * (p.Dh / 2) + 8 * t + 2 * (lane & 3)) * 2);
-      }
-      sx[u] = ldg(opaque(src));
-    }
-#pragma unroll
-    for (int c = 0; c < C; ++c)
-      sg[c] = ldg(opaque(resid ? (const f32x4*)(io.g_next + kNB * (nb0 + c) + 8 * (lane & 1)) : zero4));
-#pragma unroll
-    for (int u = 0; u < KU; ++u) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)u * 1024 + lane * 16, sx[u]);
-#pragma unroll
-    for (int c = 0; c < C; ++c) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)(C * MB + c) * 1024 + lane * 16, sg[c]);
   }
   // A norm step's sums of squares (written by the previous phase), held in
   // registers through the main loop: thread t takes rows 4 q .. 4 q + 3
