@@ -126,7 +126,8 @@ __device__ __forceinline__ Sync make_sync(KParams& p, int* lds_flag) {
 // Diagnostics: wall-clock (100 MHz) marks per phase: 0 = barrier wait
 // entered, 1 = wait over, 2 = phase work done; GEMM phases also mark 3 =
 // activation stream started, 4 = first tile's main loop done, 5 = all tiles
-// and epilogues done; the attention marks 3 = loads issued, 4 = keys done,
+// and epilogues done (in the LM head's walking workgroup 6 = walk started,
+// 7 = walk done); the attention marks 3 = loads issued, 4 = keys done,
 // 5 = result stored, and in a merging split 6 = the other splits' arrivals
 // seen, 7 = their partials loaded.
 __device__ __forceinline__ void trace_mark(const Sync& s, int phase, int k) {
@@ -218,7 +219,8 @@ struct GemmLds {
   int red_i[kMaxNodes][8];
   float best_v[kMaxNodes];      // LM head: argmax per row over this workgroup's blocks
   int best_i[kMaxNodes];
-  int reach[kMaxNodes];
+  int reach[kMaxNodes];         // accept walk: reachability of each node,
+  int jump[kMaxNodes];          // its pointer-jumping ancestor, then the path by depth
   int amax[kMaxNodes];
   int tok[kMaxNodes];  // accept walk: the tree, staged from the workspace
   int par[kMaxNodes];
@@ -720,10 +722,23 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
 // (§3.2): node i is reachable when its parent is and its draft token equals
 // the target's token after the parent; the result is the deepest reachable
 // node (lowest index among equally deep ones).
+//
+// One workgroup, so every dependent step is paid once per pass: the tree and
+// all of a wave's argmax partials are loaded in one round trip, the rows'
+// reductions are interleaved, and reachability is found by pointer jumping
+// (ceil(log2 n) rounds over all nodes at once) instead of a serial walk.
+// (LDS hand-offs only: lds_barrier, which leaves the global stores in flight.)
 __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl) {
   const int wave = wave_index(), lane = threadIdx.x & 63;
-  constexpr int RB = 4;  // rows per wave whose partials are loaded together
-  for (int r0 = wave; r0 < p.n; r0 += kWaves * RB) {
+  const int n = p.n;
+  // the tree (written by the first phase): one node per thread (n <= 128)
+  const int me = threadIdx.x;
+  const bool mine = me < n;
+  const int t_tok = ldg(p.tree + (mine ? me : 0));
+  const int t_par = ldg(p.tree + 128 + (mine ? me : 0));
+  const int t_dep = ldg(p.tree + 256 + (mine ? me : 0));
+  constexpr int RB = 8;  // rows per wave whose partials are loaded together
+  for (int r0 = wave; r0 < n; r0 += kWaves * RB) {
     float mv[RB];
     int mi[RB];
 #pragma unroll
@@ -739,7 +754,7 @@ __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int t = t0 + 64 * u + lane, r = r0 + kWaves * k;
-          const bool on = t < entries && r < p.n;
+          const bool on = t < entries && r < n;
           v[k][u] = on ? ld_coherent(&p.lm_val[(size_t)r * p.G + t]) : -INFINITY;
           ix[k][u] = on ? ld_coherent(&p.lm_idx[(size_t)r * p.G + t]) : 0x7fffffff;
         }
@@ -752,52 +767,80 @@ __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl
             mi[k] = ix[k][u];
           }
     }
+    // across the wave: rows of 16 lanes on DPP, then lanes 16 and 32 apart
+#pragma unroll
+    for (int k = 0; k < RB; ++k) row16_argmax(mv[k], mi[k]);
+#pragma unroll
+    for (int off = 16; off <= 32; off *= 2) {
+#pragma unroll
+      for (int k = 0; k < RB; ++k) {
+        const float ov = __shfl_xor(mv[k], off, kWave);
+        const int oi = __shfl_xor(mi[k], off, kWave);
+        if (ov > mv[k] || (ov == mv[k] && oi < mi[k])) {
+          mv[k] = ov;
+          mi[k] = oi;
+        }
+      }
+    }
 #pragma unroll
     for (int k = 0; k < RB; ++k) {
       const int r = r0 + kWaves * k;
-      if (r >= p.n) break;
-      wave_argmax(mv[k], mi[k]);
-      if (lane == 0) {
+      if (lane == 0 && r < n) {
         stg(p.amax + r, mi[k]);
         gl.amax[r] = mi[k];
       }
     }
   }
-  for (int i = threadIdx.x; i < p.n; i += kThreads) {
-    gl.tok[i] = ldg(p.tree + i);
-    gl.par[i] = ldg(p.tree + 128 + i);
-    gl.dep[i] = ldg(p.tree + 256 + i);
+  if (mine) {
+    gl.tok[me] = t_tok;
+    gl.par[me] = t_par;
+    gl.dep[me] = t_dep;
   }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const int* tok = gl.tok;
-    const int* par = gl.par;
-    const int* dep = gl.dep;
-    int best = 0, best_depth = 0;
-    gl.reach[0] = 1;
-    for (int i = 1; i < p.n; ++i) {
-      const int pr = par[i];
-      const int ok = gl.reach[pr] && (tok[i] == gl.amax[pr]);
-      gl.reach[i] = ok;
-      if (ok && dep[i] > best_depth) {
-        best = i;
-        best_depth = dep[i];
-      }
+  lds_barrier();
+  // reach[i]: AND of ok over node i and its ancestors below jump[i], where
+  // ok(i) = (token of i == greedy token after its parent), ok(root) = 1;
+  // each round doubles the span (jump[i] <- jump[jump[i]]) until every
+  // jump[] is the root, whose reach is 1.
+  if (mine) {
+    gl.reach[me] = me == 0 ? 1 : (t_tok == gl.amax[t_par > 0 ? t_par : 0] ? 1 : 0);
+    gl.jump[me] = me == 0 ? 0 : t_par;
+  }
+  lds_barrier();
+  for (int span = 1; span < n; span *= 2) {
+    int rv = 0, jv = 0;
+    if (mine) {
+      const int j = gl.jump[me];
+      rv = gl.reach[me] & gl.reach[j];
+      jv = gl.jump[j];
     }
-    for (int i = best; i >= 0; i = par[i]) gl.reach[dep[i]] = -1 - i;  // path by depth, encoded
-    gl.walk_len = best_depth;
-    stg(p.accept_len, best_depth);
-    stg(p.next_token, gl.amax[best]);
+    lds_barrier();
+    if (mine) {
+      gl.reach[me] = rv;
+      gl.jump[me] = jv;
+    }
+    lds_barrier();
   }
-  __syncthreads();
+  // deepest reachable node, lowest index first: max of (depth, 127 - i)
+  if (wave == 0) {
+    int key = -1;
+    for (int i = lane; i < n; i += 64)
+      if (gl.reach[i]) key = max(key, (gl.dep[i] << 8) | (127 - i));
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) key = max(key, __shfl_xor(key, off, kWave));
+    if (lane == 0) {
+      const int best = 127 - (key & 255), best_depth = key >> 8;
+      for (int i = best; i >= 0; i = gl.par[i]) gl.jump[gl.dep[i]] = i;  // the path, by depth
+      gl.walk_len = best_depth;
+      stg(p.accept_len, best_depth);
+      stg(p.next_token, gl.amax[best]);
+    }
+  }
+  lds_barrier();
   {
     const int best_depth = gl.walk_len;
-    for (int k = threadIdx.x; k < p.n; k += kThreads) {
-      const int v = gl.reach[k];
-      stg(p.path + k, (k <= best_depth && v < 0) ? -1 - v : -1);
-    }
+    for (int k = threadIdx.x; k < n; k += kThreads) stg(p.path + k, k <= best_depth ? gl.jump[k] : -1);
   }
-  __syncthreads();
+  lds_barrier();
 }
 
 // The epilogue of one tile (blocks [nb0, nb0 + cw)): the waves take its
@@ -885,7 +928,11 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
       st_coherent(&p.lm_val[(size_t)r * G + blockIdx.x], gl.best_v[r]);
       st_coherent(&p.lm_idx[(size_t)r * G + blockIdx.x], gl.best_i[r]);
     }
-    if (arrive_last(p.lm_cnt, G, lds_flag)) finish_walk(p, G, gl);
+    if (arrive_last(p.lm_cnt, G, lds_flag)) {
+      trace_mark(sy, phase, 6);
+      finish_walk(p, G, gl);
+      trace_mark(sy, phase, 7);
+    }
   }
   return true;
 }
