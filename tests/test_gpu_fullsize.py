@@ -10,7 +10,8 @@ GPU's own prefix K/V (written by its prefill), and the test compares what each
 of the layer's two blocks adds to the stream, and the tree's K/V cache slots.  The LM head is recomputed from
 the GPU's last version and compared over all n x V logits; the argmax and the
 accept walk are checked as in the small-model tests.  The embedding rows are
-compared exactly.
+compared exactly.  At the bench's workload the rollback after a pass is
+checked too (bit-exact row moves).
 
 Bars: logits as everywhere (max abs 2e-2, relative L2 1e-2); a block's
 contribution or a K/V slice: max |gpu - oracle| <= 2e-2 max |oracle| and
@@ -96,6 +97,50 @@ def _check_tensor(gpu, ref, what):
     assert err <= parity.ABS_TOL * scale, f"{what}: max abs error {err:.3e} > {parity.ABS_TOL} x {scale:.3e}"
     assert rel <= parity.REL_TOL, f"{what}: relative L2 error {rel:.3e} > {parity.REL_TOL}"
     return err / scale, rel
+
+
+def test_full_size_rollback():
+    # The bench's workload: a tree with 4 tokens of the target's own greedy
+    # continuation planted along its last branch (the continuation from
+    # one-node passes on the GPU, i.e. plain greedy decoding), verified, then
+    # rolled back.  Every layer and head's accepted rows must move bit-exact,
+    # the prefix and the other slots stay as they were.  The tree pass and the
+    # one-node passes batch the tokens differently (logits within a few 1e-2
+    # of each other), so only steps whose top-2 gap clears 0.2 must be accepted.
+    wl = workloads.get_workload("llama7b_p512_n31")
+    shape, sess, gen, ow, binding = _model(wl.model)
+    P = wl.prefix_len
+    parent, tok = workloads.make_tree(wl.tree, shape.vocab, wl.seed)
+    n = len(parent)
+    sess.prefill(workloads.draw_tokens(P, shape.vocab, seed=wl.seed), 0)
+    cont, gaps, r = [], [], int(tok[0])
+    for t in range(5):
+        sess.verify_tree(P + t, np.array([r]), np.array([-1]), want_logits=True)
+        lg, _, _, nxt = sess.results(1)
+        top = np.sort(lg.numpy()[0])[-2:]
+        gaps.append(float(top[1] - top[0]))
+        cont.append(nxt)
+        r = nxt
+    K, leaf = 4, n - 1
+    ptok = workloads.draft_tree(parent, int(tok[0]), cont, K, leaf, shape.vocab, seed=1)
+    sess.verify_tree(P, ptok, parent, want_logits=False)
+    torch.cuda.synchronize()
+    acc = int(sess.accept_len.item())
+    path = [int(x) for x in sess.path[: acc + 1].cpu()]
+    sure = 0
+    while sure < K and gaps[sure] > 0.2:
+        sure += 1
+    assert acc >= sure, (acc, gaps)
+    k0, v0 = sess.k_cache[:, :, :P + n].clone(), sess.v_cache[:, :, :P + n].clone()
+    sess.commit(P, n)
+    torch.cuda.synchronize()
+    for k in range(n):
+        src = path[k] if k <= acc else k
+        assert torch.equal(sess.k_cache[:, :, P + k], k0[:, :, P + src]), k
+        assert torch.equal(sess.v_cache[:, :, P + k], v0[:, :, P + src]), k
+    assert torch.equal(sess.k_cache[:, :, :P], k0[:, :, :P])
+    assert torch.equal(sess.v_cache[:, :, :P], v0[:, :, :P])
+    _log(f"rollback: path {path}, gaps {np.round(gaps, 3).tolist()}")
 
 
 @pytest.mark.parametrize("wl_name,layers", CASES, ids=[c[0] for c in CASES])
