@@ -159,6 +159,31 @@ int llmcad_prefill(const llmcad_config* cfg, const void* packed, void* k_cache, 
                    float* last_logits, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * One step of the tree decoder (§3.2 "Token tree generation", tree decoder):
+ * the forward of nodes [first, n) of a token tree whose nodes [0, first)
+ * were computed by earlier calls on the same cache, prefix_len and tree.
+ *
+ * The tree arrays are as for llmcad_verify_tree (host, all n nodes; node i
+ * at position prefix_len + depth(i)).  Each computed node attends to the
+ * prefix and to its ancestors and itself -- the masking table of the tree
+ * decoder -- reading the earlier nodes' keys/values from their cache slots
+ * prefix_len + i, and its own K/V are written to slot prefix_len + i.
+ * logits: device fp32 [n - first][V], row r = the model's logits after node
+ * first + r (NULL: not stored).  With first = 0 this is the forward part of
+ * a verification pass; no argmax, path or next token is produced.  A draft
+ * model grows its tree with calls of one new node each (first = n - 1).
+ * Asynchronous on `stream`; allocates nothing.
+ *
+ * Errors (checked on the host, nothing enqueued): as llmcad_verify_tree, and
+ * LLMCAD_ETREE unless 0 <= first < n; the workspace must hold a pass over
+ * n - first rows (llmcad_workspace_bytes with max_n >= n - first).
+ */
+int llmcad_extend_tree(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                       int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens, const int32_t* parent,
+                       int32_t n, int32_t first, float* logits, void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+/*
  * Rollback to the verified sequence after a verification pass (§3.2 "Token
  * tree verification and rectification": the tree is rolled back to the
  * verified sequence, which becomes the new input; §3.1: generation then

@@ -33,6 +33,7 @@ SYMBOLS = (
     "llmcad_verify_tree",
     "llmcad_prefill",
     "llmcad_commit_path",
+    "llmcad_extend_tree",
     "llmcad_status_string",
     "llmcad_workspace_region",
     "llmcad_timing_enable",
@@ -86,6 +87,7 @@ def _load():
                                               P, SZ, P]),
         "llmcad_prefill": (ctypes.c_int, [CFG, P, P, P, I32, I32P, I32, I32, P, P, SZ, P]),
         "llmcad_commit_path": (ctypes.c_int, [CFG, P, P, I32, I32, P, P, I32, P]),
+        "llmcad_extend_tree": (ctypes.c_int, [CFG, P, P, P, I32, I32, I32P, I32P, I32, I32, P, P, SZ, P]),
         "llmcad_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "llmcad_workspace_region": (ctypes.c_int, [CFG, I32, I32, ctypes.POINTER(SZ),
                                                    ctypes.POINTER(SZ)]),
@@ -201,6 +203,23 @@ def prefill(cfg, packed, k_cache, v_cache, tokens, start_pos: int, last_logits, 
     return rc
 
 
+def extend_tree(cfg, packed, k_cache, v_cache, prefix_len: int, tree_tokens, parent, first: int, logits,
+                workspace, stream=None, raise_on_error=True) -> int:
+    """Tree-decoder step: the forward of nodes [first, n) of the tree (see llmcad_extend_tree)."""
+    tok, tok_p = _i32(tree_tokens)
+    par, par_p = _i32(parent)
+    if len(par) != len(tok):
+        raise ValueError("tree_tokens and parent differ in length")
+    cap = k_cache.shape[-2]
+    rc = _lib.llmcad_extend_tree(
+        ctypes.byref(cfg), _ptr(packed), _ptr(k_cache), _ptr(v_cache), int(cap), int(prefix_len), tok_p, par_p,
+        int(len(tok)), int(first), _ptr(logits), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _stream(stream))
+    if raise_on_error:
+        _check(rc, "llmcad_extend_tree")
+    return rc
+
+
 def commit_path(cfg, k_cache, v_cache, prefix_len: int, path, accept_len, n: int, stream=None,
                 raise_on_error=True) -> int:
     """Rollback to the verified sequence: path/accept_len are the device outputs of the
@@ -276,6 +295,13 @@ class Session:
                     parent, self.logits if want_logits else None, self.path, self.accept_len,
                     self.next_token, self.workspace)
         return n
+
+    def extend(self, prefix_len, tree_tokens, parent, first):
+        """Forward of nodes [first, n) of the tree; returns their logits [n - first, V] (device)."""
+        n = len(tree_tokens)
+        extend_tree(self.cfg, self.packed, self.k_cache, self.v_cache, prefix_len, tree_tokens, parent, first,
+                    self.logits, self.workspace)
+        return self.logits[: n - first]
 
     def commit(self, prefix_len, n):
         """Roll the cache back to the verified sequence of the last verify_tree over n nodes."""

@@ -86,7 +86,9 @@ struct Pass {
   char* v_cache;
   int cap;
   int prefix_len;
-  int n;
+  int n;       // rows: nodes [m0, m0 + n) of a tree of nt nodes
+  int m0 = 0;
+  int nt = 0;  // (0: n)
   float* logits;
   int row_lo;
   int* path;
@@ -151,6 +153,8 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.log2_theta = (float)log2((double)a.cfg->rope_theta);
   p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.Dh));
   p.n = a.n;
+  p.m0 = a.m0;
+  p.nt = a.nt > 0 ? a.nt : a.n;
   p.Mp = W.Mp;
   p.prefix_len = a.prefix_len;
   p.cap = a.cap;
@@ -323,6 +327,50 @@ int llmcad_verify_tree(const llmcad_config* cfg, const void* packed, void* k_cac
   a.path = path;
   a.accept_len = accept_len;
   a.next_token = next_token;
+  a.ws = (char*)workspace;
+  a.st = (hipStream_t)stream;
+  return run_pass(a, tree);
+}
+
+int llmcad_extend_tree(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                       int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens, const int32_t* parent,
+                       int32_t n, int32_t first, float* logits, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!packed || !k_cache || !v_cache || !tree_tokens || !parent || !workspace) return LLMCAD_EARG;
+  if (n < 1 || n > kMaxNodes || first < 0 || first >= n) return LLMCAD_ETREE;
+  if (parent[0] != -1) return LLMCAD_ETREE;
+  for (int i = 0; i < n; ++i) {
+    if (tree_tokens[i] < 0 || tree_tokens[i] >= cfg->vocab) return LLMCAD_ETREE;
+    if (i > 0 && (parent[i] < 0 || parent[i] >= i)) return LLMCAD_ETREE;
+  }
+  if (capacity < 1 || prefix_len < 0 || (long)prefix_len + n > capacity) return LLMCAD_ECAPACITY;
+  const Shape s(*cfg);
+  const int G = pass_grid();
+  if (workspace_bytes < WorkspaceLayout(s, n - first, G).total) return LLMCAD_EWORKSPACE;
+  TreeArgs tree;
+  memset(&tree, 0, sizeof(tree));
+  for (int i = 0; i < n; ++i) {
+    tree.tok[i] = tree_tokens[i];
+    tree.parent[i] = parent[i];
+  }
+  int* sink = (int*)((char*)workspace + WorkspaceLayout(s, 1, G).scratch_out);  // (no walk is run)
+  Pass a;
+  a.cfg = cfg;
+  a.packed = (const char*)packed;
+  a.k_cache = (char*)k_cache;
+  a.v_cache = (char*)v_cache;
+  a.cap = capacity;
+  a.prefix_len = prefix_len;
+  a.n = n - first;
+  a.m0 = first;
+  a.nt = n;
+  a.logits = logits;
+  a.row_lo = 0;
+  a.path = sink;
+  a.accept_len = sink + 128;
+  a.next_token = sink + 129;
   a.ws = (char*)workspace;
   a.st = (hipStream_t)stream;
   return run_pass(a, tree);

@@ -47,8 +47,11 @@ struct PassParams {
   // model
   int L, d, H, Dh, F, Fp, V;
   float eps, inv_d, log2_theta, scale_log2;
-  // pass
+  // pass: rows n = nodes [m0, nt) of a tree of nt nodes (m0 = 0: all of it);
+  // nodes [0, m0) were computed by earlier passes, their K/V are in slots
+  // prefix_len + i
   int n, Mp, prefix_len, cap, G;
+  int m0, nt;
   // packed weights
   const char* packed;
   long long o_embed, o_final_norm, layer0, layer_bytes;

@@ -661,7 +661,7 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
         const float outv = j < 8 ? v[i] * cs.x - partner * cs.y : v[i] * cs.x + partner * cs.y;
         const float nxt = dpp_f<kDppRowShl1>(outv);
         if (r < p.n && (j & 1) == 0) {
-          bf16* dst = part == 0 ? base + (size_t)r * d : base + (size_t)(p.prefix_len + r) * dh;
+          bf16* dst = part == 0 ? base + (size_t)r * d : base + (size_t)(p.prefix_len + p.m0 + r) * dh;
           st_coherent_bf2(dst + dim, outv, nxt);
         }
       }
@@ -672,7 +672,7 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
         const int r = 16 * rb + rr0 + i;
         const float nxt = dpp_f<kDppRowShl1>(v[i]);
         if (r < p.n && (j & 1) == 0)
-          st_coherent_bf2(io.vc + ((size_t)hh * p.cap + p.prefix_len + r) * dh + dim, v[i], nxt);
+          st_coherent_bf2(io.vc + ((size_t)hh * p.cap + p.prefix_len + p.m0 + r) * dh + dim, v[i], nxt);
       }
     }
   } else if constexpr (EPI == EPI_RESID) {
@@ -928,7 +928,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
       st_coherent(&p.lm_val[(size_t)r * G + blockIdx.x], gl.best_v[r]);
       st_coherent(&p.lm_idx[(size_t)r * G + blockIdx.x], gl.best_i[r]);
     }
-    if (arrive_last(p.lm_cnt, G, lds_flag)) {
+    if (arrive_last(p.lm_cnt, G, lds_flag) && p.m0 == 0) {
       trace_mark(sy, phase, 6);
       finish_walk(p, G, gl);
       trace_mark(sy, phase, 7);
@@ -1031,6 +1031,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
   const int units = wave_uniform(p.H) * rbn * KS;
   const int wave = wave_index(), lane = threadIdx.x & 63, li = lane & 15, g = lane >> 4;
   const int P = wave_uniform(p.prefix_len), n = wave_uniform(p.n);
+  const int nt = wave_uniform(p.nt), m0 = wave_uniform(p.m0);  // the tree's nodes; node of row 0
   const int npc = (P + CH - 1) / CH;  // prefix chunks; chunk npc is the tree's
   const size_t kv_layer = (size_t)p.H * p.cap * DH;
   const bf16* kcl = p.k_cache + (size_t)layer * kv_layer;
@@ -1039,9 +1040,10 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
   bf16* obase = p.o + (size_t)layer * p.Mp * p.d;
   char* buf[2] = {lds, lds + Gm::BYTES};
   // chunk c: prefix positions [c CH, min((c + 1) CH, P)) for c < npc, the
-  // tree's [P, P + n) for c == npc
+  // tree's [P, P + nt) for c == npc (all its nodes: those computed before
+  // this pass are in their cache slots already)
   auto chunk_lo = [&](int c) { return c < npc ? c * CH : P; };
-  auto chunk_hi = [&](int c) { return c < npc ? ((c + 1) * CH < P ? (c + 1) * CH : P) : P + n; };
+  auto chunk_hi = [&](int c) { return c < npc ? ((c + 1) * CH < P ? (c + 1) * CH : P) : P + nt; };
   // the chunks of split ks: prefix chunks [c_lo, c_hi), then the tree's if ks is the last
   auto split_chunks = [&](int ks, int& c_lo, int& c_hi, int& nch) {
     c_lo = ks * npc / KS;
@@ -1097,13 +1099,14 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
       const bf16* qrow = qb + (size_t)row * p.d + h * DH;
 #pragma unroll
       for (int s2 = 0; s2 < KSTEPS; ++s2) qf[s2] = ldg((const bf16x8*)(qrow + 32 * s2 + 8 * g));
-      const uint32_t* ap = (const uint32_t*)(p.tree + 512) + row * 4;
+      const int node = m0 + row < kMaxNodes ? m0 + row : kMaxNodes - 1;  // (rows past n: any node)
+      const uint32_t* ap = (const uint32_t*)(p.tree + 512) + node * 4;
 #pragma unroll
       for (int w = 0; w < 4; ++w) anc[w] = ldg(ap + w);
     }
     // the tree's keys (last split): loaded now, stored when their buffer is free
     AttnChunkRegs<DH> RT;
-    attn_load<DH>(RT, kc, vc, P, P, has_tree ? P + n : P);
+    attn_load<DH>(RT, kc, vc, P, P, has_tree ? P + nt : P);
     float m_run = -INFINITY, l_run = 0.0f;
     f32x4 oacc[DB];
 #pragma unroll
@@ -1118,7 +1121,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
           if (!((need >> j) & 1)) continue;
           const int c = list_chunk(c_lo, c_hi, j0 + j);
           if (c == npc) {
-            attn_store<DH>(buf[j], RT, (n + 63) & ~63);
+            attn_store<DH>(buf[j], RT, (nt + 63) & ~63);
           } else {
             AttnChunkRegs<DH> R;
             attn_load<DH>(R, kc, vc, chunk_lo(c), chunk_lo(c), chunk_hi(c));
@@ -1152,7 +1155,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
           for (int e = 0; e < 4; ++e) {
             const int pos = p0 + c0k + 16 * jb + 4 * g + e;
             const int t = pos - P;
-            const bool vis = pos < hi_t && (pos < P || (t < n && ((anc[t >> 5] >> (t & 31)) & 1u)));
+            const bool vis = pos < hi_t && (pos < P || (t < nt && ((anc[t >> 5] >> (t & 31)) & 1u)));
             const float sv = vis ? sc[jb][e] * p.scale_log2 : -INFINITY;
             sc[jb][e] = sv;
             mx = fmaxf(mx, sv);
@@ -1333,20 +1336,20 @@ template <int MB>
 __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, int* par_s) {
   const bf16* E = (const bf16*)(p.packed + p.o_embed);
   if (blockIdx.x == 0) {
-    if (threadIdx.x < 128) par_s[threadIdx.x] = threadIdx.x < p.n ? tree.parent[threadIdx.x] : -1;
+    if (threadIdx.x < 128) par_s[threadIdx.x] = threadIdx.x < p.nt ? tree.parent[threadIdx.x] : -1;
     __syncthreads();
     if (threadIdx.x < 128) {
       const int i = threadIdx.x;
       int dep = 0;
       uint32_t a[4] = {0u, 0u, 0u, 0u};
-      if (i < p.n) {
+      if (i < p.nt) {
         for (int j = i; j >= 0; j = par_s[j]) {
           a[j >> 5] |= 1u << (j & 31);
           ++dep;
         }
         --dep;
       }
-      st_coherent(&p.tree[i], i < p.n ? tree.tok[i] : 0);
+      st_coherent(&p.tree[i], i < p.nt ? tree.tok[i] : 0);
       st_coherent(&p.tree[128 + i], par_s[i]);
       st_coherent(&p.tree[256 + i], dep);
       st_coherent(&p.tree[384 + i], p.prefix_len + dep);
@@ -1356,10 +1359,11 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
   }
   const int lane = threadIdx.x & 63;
   for (int m = blockIdx.x; m < p.n; m += p.G) {
-    // rotary table row m: (cos, sin) of pos(m) * theta^(-2j/Dh), j < Dh/2
+    // rotary table row m (node m0 + m): (cos, sin) of its position times
+    // theta^(-2j/Dh), j < Dh/2
     if (threadIdx.x < p.Dh / 2) {
       int dep = 0;
-      for (int j = tree.parent[m]; j >= 0; j = tree.parent[j]) ++dep;
+      for (int j = tree.parent[p.m0 + m]; j >= 0; j = tree.parent[j]) ++dep;
       const int jj = threadIdx.x;
       float sn, cs;
       sincosf((float)(p.prefix_len + dep) * rope_inv_freq(jj, p.Dh, p.log2_theta), &sn, &cs);
@@ -1379,7 +1383,7 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
     for (int k = 0; k < PER; ++k) {
       const int e = base + k * stride + threadIdx.x;
       const int m = e < total ? e / p.d : 0, c = e < total ? e % p.d : 0;
-      v[k] = e < total ? bf2f(ldg(E + (size_t)tree.tok[m] * p.d + c)) : 0.0f;
+      v[k] = e < total ? bf2f(ldg(E + (size_t)tree.tok[p.m0 + m] * p.d + c)) : 0.0f;
       g[k] = e < total ? bf2f(ldg(g0 + c)) : 0.0f;
     }
 #pragma unroll

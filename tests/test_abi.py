@@ -150,3 +150,25 @@ def test_commit_validation(binding):
     assert lib.llmcad_commit_path(ctypes.byref(cfg), fake, fake, 64, 61, fake, fake, 4, None) == binding.ECAPACITY
     assert lib.llmcad_commit_path(ctypes.byref(cfg), fake, fake, 64, -1, fake, fake, 4, None) == binding.ECAPACITY
     assert lib.llmcad_commit_path(ctypes.byref(cfg), fake, fake, 64, 10, fake, fake, 1, None) == binding.OK
+
+
+def test_extend_validation(binding):
+    # Host-side checks of the tree-decoder step; nothing is enqueued.
+    cfg = binding.make_config(workloads.MODELS["tiny"])
+    lib = binding.lib()
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    fake = ctypes.c_void_p(256)
+    tok = np.array([1, 2, 3], dtype=np.int32)
+    par = np.array([-1, 0, 1], dtype=np.int32)
+
+    def call(first, n=3, prefix_len=10, cap=64, t=tok, p=par, ws=1 << 30):
+        return lib.llmcad_extend_tree(ctypes.byref(cfg), fake, fake, fake, cap, prefix_len,
+                                      t.ctypes.data_as(I32P), p.ctypes.data_as(I32P), n, first, None, fake, ws,
+                                      None)
+
+    assert call(3) == binding.ETREE             # first must be < n
+    assert call(-1) == binding.ETREE
+    assert call(1, p=np.array([-1, 0, 2], dtype=np.int32)) == binding.ETREE
+    assert call(1, t=np.array([1, 2, cfg.vocab], dtype=np.int32)) == binding.ETREE
+    assert call(1, prefix_len=62) == binding.ECAPACITY
+    assert call(1, ws=100) == binding.EWORKSPACE
