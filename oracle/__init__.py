@@ -17,6 +17,9 @@ Contents
   decode.py greedy decoding, plainly and by the generate-and-verify loop
             with rollback of the token tree to its verified sequence (§3.1,
             §3.2 "Token tree verification and rectification")
+  draft.py  draft-side tree generation: the tree decoder, the 30% branch
+            threshold and the confidence-based branch pacer (§3.1, §3.2
+            "Token tree generation", Eq. 1)
 
 Every function is pinned by tests/test_oracle_*.py against something other
 than itself: brute force, an independent library implementation
@@ -41,3 +44,4 @@ from .model import (  # noqa: F401
 )
 from .walk import accept_walk, branch_sequences, correct_sequences  # noqa: F401
 from .decode import commit_path, greedy_decode, speculative_decode  # noqa: F401
+from .draft import generate_tree  # noqa: F401

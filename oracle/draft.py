@@ -1,0 +1,90 @@
+"""Draft-side token-tree generation: the tree decoder and the branch pacer.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+The draft model grows a token tree rooted at the last accepted token (§3.1
+"Simplified workflow"; §3.2 "Token tree generation"):
+- Tree decoder: one node is fed per iteration; it attends to the prefix and to
+  its own branch only (the masking table), so branches do not affect each
+  other.  Feeding node x gives the draft's distribution over x's successor.
+- Candidates: the most likely successor always extends x's branch; every
+  other token whose probability exceeds the threshold (30% in the paper)
+  starts a branch of its own.  A candidate is a draft token with a known
+  value; it becomes a fed node when its branch is chosen to grow.
+- Branch pacer (Eq. 1): with M the number of iterations of the whole tree,
+  branch x (ending at candidate x) holding T_x draft tokens with cumulative
+  confidence C_x (the product of its tokens' probabilities), its deficit is
+  f(x) = M C_x / sum_i C_i - T_x.  Under max-min fairness the branch with the
+  largest deficit grows next (ties: the candidate created first).
+
+Node numbering is the feeding order (a node is fed after its parent).  The
+tree handed to the target holds the fed nodes and, after them, the pending
+candidates as leaves.  Each iteration's forward is `tree_forward` over the
+fed nodes (the last row is the new node's), which is the pinned one-pass form.
+"""
+
+import numpy as np
+
+from .model import tree_forward
+
+
+def _softmax64(row):
+    z = np.asarray(row, dtype=np.float64)
+    e = np.exp(z - z.max())
+    return e / e.sum()
+
+
+def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold=0.3, rounding=True,
+                  forward=None):
+    """Grow a draft tree with `iterations` fed nodes after the root.
+
+    prefix_k/prefix_v: the draft model's prefix keys/values [L, P, H, Dh].
+    forward(tokens, parent) -> the draft's logits row of the last node, by
+    default the last row of tree_forward.  Returns (tree_tokens, parent, info)
+    where info lists per fed node its token, parent and confidence.
+    """
+    if forward is None:
+        def forward(tokens, parent):
+            logits, _, _ = tree_forward(weights, prefix_k, prefix_v, tokens, parent, rounding)
+            return logits[-1]
+
+    tokens, parent, conf = [int(root_token)], [-1], [1.0]   # fed nodes
+    pending = []  # candidates: (token, fed parent, probability, cumulative confidence, depth)
+
+    def expand(node):
+        prob = _softmax64(forward(np.asarray(tokens), np.asarray(parent)))
+        order = np.argsort(-prob, kind="stable")  # most likely first, lowest index among ties
+        best = int(order[0])
+        cum = float(np.prod([conf[i] for i in _branch(parent, node)]))
+        depth = len(_branch(parent, node)) + 1  # draft tokens of the candidate's branch
+        pending.append((best, node, float(prob[best]), cum * float(prob[best]), depth))
+        for t in order[1:]:
+            if prob[t] <= threshold:
+                break
+            pending.append((int(t), node, float(prob[t]), cum * float(prob[t]), depth))
+
+    expand(0)
+    M = iterations
+    for _ in range(iterations):
+        total = sum(c for _, _, _, c, _ in pending)
+        deficits = [M * c / total - d for _, _, _, c, d in pending]
+        k = int(np.argmax(deficits))  # first maximum: the earliest candidate
+        tok, par, p, _, _ = pending.pop(k)
+        tokens.append(tok)
+        parent.append(par)
+        conf.append(p)
+        expand(len(tokens) - 1)
+    # the tree for verification: the fed nodes, then the pending candidates as leaves
+    all_tokens = tokens + [t for t, _, _, _, _ in pending]
+    all_parent = parent + [q for _, q, _, _, _ in pending]
+    info = {"fed": len(tokens), "conf": conf, "pending": [(t, q, p) for t, q, p, _, _ in pending]}
+    return np.asarray(all_tokens, dtype=np.int64), np.asarray(all_parent, dtype=np.int64), info
+
+
+def _branch(parent, node):
+    """Draft nodes of node's branch (root excluded), root side first."""
+    out = []
+    while node > 0:
+        out.append(node)
+        node = int(parent[node])
+    return out[::-1]
