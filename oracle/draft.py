@@ -41,7 +41,9 @@ def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold
     prefix_k/prefix_v: the draft model's prefix keys/values [L, P, H, Dh].
     forward(tokens, parent) -> the draft's logits row of the last node, by
     default the last row of tree_forward.  Returns (tree_tokens, parent, info)
-    where info lists per fed node its token, parent and confidence.
+    where info holds the number of fed nodes, each fed node's probability, the
+    pending candidates and, per iteration, the pacer's margin (largest deficit
+    minus the runner-up).
     """
     if forward is None:
         def forward(tokens, parent):
@@ -65,10 +67,13 @@ def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold
 
     expand(0)
     M = iterations
+    gaps = []  # per iteration: largest deficit minus the runner-up (inf with one candidate)
     for _ in range(iterations):
         total = sum(c for _, _, _, c, _ in pending)
         deficits = [M * c / total - d for _, _, _, c, d in pending]
         k = int(np.argmax(deficits))  # first maximum: the earliest candidate
+        rest = deficits[:k] + deficits[k + 1:]
+        gaps.append(deficits[k] - max(rest) if rest else np.inf)
         tok, par, p, _, _ = pending.pop(k)
         tokens.append(tok)
         parent.append(par)
@@ -77,7 +82,8 @@ def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold
     # the tree for verification: the fed nodes, then the pending candidates as leaves
     all_tokens = tokens + [t for t, _, _, _, _ in pending]
     all_parent = parent + [q for _, q, _, _, _ in pending]
-    info = {"fed": len(tokens), "conf": conf, "pending": [(t, q, p) for t, q, p, _, _ in pending]}
+    info = {"fed": len(tokens), "conf": conf, "pending": [(t, q, p) for t, q, p, _, _ in pending],
+            "deficit_gaps": gaps}
     return np.asarray(all_tokens, dtype=np.int64), np.asarray(all_parent, dtype=np.int64), info
 
 

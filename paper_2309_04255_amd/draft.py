@@ -1,0 +1,82 @@
+"""Draft-side token-tree generation on the GPU (§3.1, §3.2 "Token tree generation").
+
+A draft model (any model the library runs, in its own Session, its cache
+holding the accepted prefix) grows a token tree rooted at the last accepted
+token:
+- tree decoder: each iteration feeds one node through llmcad_extend_tree
+  (the new node's forward against the prefix and its own branch, the earlier
+  nodes' keys/values read from the cache), and its logits row comes back;
+- candidates: the most likely successor of the fed node always extends its
+  branch, and every other token with probability above `threshold` (30% in
+  the paper) starts a branch;
+- branch pacer (Eq. 1, max-min fairness): with M the iteration budget and a
+  candidate's branch holding T tokens of cumulative confidence C (product of
+  their probabilities), the candidate with the largest M C / sum(C) - T is fed
+  next (the earliest created among equal ones).
+
+Host control: the probabilities of one row (float64 softmax of the returned
+logits) and the pacer's choice are computed on the host between steps, which
+need the host anyway (the next node depends on them).  Nodes are numbered in
+feeding order; the returned tree lists the fed nodes, then the candidates not
+yet fed as leaves.
+"""
+
+import numpy as np
+
+
+class _Tree:
+    def __init__(self, root):
+        self.tok = [int(root)]
+        self.par = [-1]
+        self.cum = [1.0]    # cumulative confidence of the node's branch
+        self.depth = [0]    # draft tokens of the node's branch
+        self.cand = []      # [token, fed parent, probability] in creation order
+
+    def add_candidates(self, node, prob, threshold):
+        # most likely first (lowest index among equal probabilities)
+        order = np.argsort(-prob, kind="stable")
+        take = 1 + int(np.count_nonzero(prob[order[1:]] > threshold))
+        for t in order[:take]:
+            self.cand.append([int(t), node, float(prob[t])])
+
+    def pick(self, budget):
+        conf = np.array([self.cum[q] * p for _, q, p in self.cand])
+        length = np.array([self.depth[q] + 1 for _, q, _ in self.cand])
+        deficit = budget * conf / conf.sum() - length
+        return int(np.argmax(deficit))
+
+    def feed(self, k):
+        t, q, p = self.cand.pop(k)
+        self.tok.append(t)
+        self.par.append(q)
+        self.cum.append(self.cum[q] * p)
+        self.depth.append(self.depth[q] + 1)
+        return len(self.tok) - 1
+
+
+def _probs(logits_row):
+    z = logits_row.astype(np.float64)
+    z = np.exp(z - z.max())
+    return z / z.sum()
+
+
+def generate_tree(sess, prefix_len: int, root_token: int, iterations: int, threshold: float = 0.3):
+    """Grow a draft tree with `iterations` fed nodes after the root, on the
+    draft model in `sess`.  Returns (tree_tokens, parent, info): the tree for
+    verification (fed nodes, then the pending candidates), and info with the
+    number of fed nodes, each fed node's probability and the fed nodes'
+    logits rows ("fed", "conf", "logits")."""
+    tree = _Tree(root_token)
+    rows = []
+    node = 0
+    for it in range(iterations + 1):
+        row = sess.extend(prefix_len, np.asarray(tree.tok), np.asarray(tree.par), node)[0]
+        rows.append(row.float().cpu().numpy())
+        tree.add_candidates(node, _probs(rows[-1]), threshold)
+        if it == iterations:
+            break
+        node = tree.feed(tree.pick(iterations))
+    tok = np.asarray(tree.tok + [c[0] for c in tree.cand], dtype=np.int32)
+    par = np.asarray(tree.par + [c[1] for c in tree.cand], dtype=np.int32)
+    conf = [1.0] + [tree.cum[i] / tree.cum[tree.par[i]] for i in range(1, len(tree.tok))]
+    return tok, par, {"fed": len(tree.tok), "conf": conf, "logits": np.stack(rows)}
