@@ -234,6 +234,7 @@ def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
     commit_bytes = 2 * 2 * moved * shape.n_layers * shape.n_heads * shape.head_dim * 2  # K+V, read+write
     log(f"decode loop: {made} tokens in {iterations} passes, {t_loop * 1e3:.1f} ms; rollback {commit_us:.1f} us "
         f"for {moved} rows per layer and head")
+    draft_tree = draft_generation(sess, plen, root, iterations)
     return {
         "tokens_per_s": round(made / t_loop, 1),
         "passes": iterations,
@@ -247,6 +248,45 @@ def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
         "commit_us": round(commit_us, 2),
         "commit_rows_moved": moved,
         "commit_bytes": commit_bytes,
+        "draft_tree": draft_tree,
+    }
+
+
+def draft_generation(sess, plen, root, iterations, threshold=0.3):
+    """Draft-side tree generation with this model as the draft (in the
+    paper's LLaMA2 pair the 7B model drafts for the 13B): `iterations` fed
+    nodes after the root, one tree-decoder step each, the logits row read back
+    and the branch pacer run on the host between steps.  Also times one
+    tree-decoder step alone (the step's launch on the stream, no read-back)."""
+    import numpy as np
+    import torch
+
+    from paper_2309_04255_amd import draft
+
+    draft.generate_tree(sess, plen, root, iterations, threshold)  # warm-up
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    tok, par, info = draft.generate_tree(sess, plen, root, iterations, threshold)
+    dt = time.perf_counter() - t
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    ftok, fpar = np.asarray(tok[:info["fed"]]), np.asarray(par[:info["fed"]])
+    e0.record(stream)
+    for _ in range(reps):
+        sess.extend(plen, ftok, fpar, len(ftok) - 1)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    step_us = e0.elapsed_time(e1) * 1e3 / reps
+    log(f"draft tree: {iterations} steps in {dt * 1e3:.1f} ms, {len(tok)} nodes; one step {step_us:.1f} us")
+    return {
+        "iterations": iterations,
+        "threshold": threshold,
+        "nodes": len(tok),
+        "ms": round(dt * 1e3, 3),
+        "step_us": round(step_us, 2),
+        "what": ("one tree-decoder step per fed node (this model as the draft), logits row read back and "
+                 "threshold + branch pacer on the host; step_us: one step's kernel time at the last fed node"),
     }
 
 

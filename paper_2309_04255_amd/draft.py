@@ -33,11 +33,14 @@ class _Tree:
         self.cand = []      # [token, fed parent, probability] in creation order
 
     def add_candidates(self, node, prob, threshold):
-        # most likely first (lowest index among equal probabilities)
-        order = np.argsort(-prob, kind="stable")
-        take = 1 + int(np.count_nonzero(prob[order[1:]] > threshold))
-        for t in order[:take]:
-            self.cand.append([int(t), node, float(prob[t])])
+        # the most likely token (lowest index among equal maxima), then every
+        # other token above the threshold, most likely first (ties: lower index)
+        best = int(np.argmax(prob))
+        over = np.flatnonzero(prob > threshold)
+        over = over[over != best]
+        over = over[np.argsort(-prob[over], kind="stable")]
+        for t in [best] + [int(x) for x in over]:
+            self.cand.append([t, node, float(prob[t])])
 
     def pick(self, budget):
         conf = np.array([self.cum[q] * p for _, q, p in self.cand])

@@ -1,0 +1,70 @@
+"""The GPU draft driver's host policy (branch threshold, §3.1; branch pacer,
+§3.2 Eq. 1) against the oracle's generator, on the CPU: a stand-in session
+serves logits rows from a table, so both sides see the same probabilities and
+must make the same integer decisions (which candidates, in which order, which
+branch grows)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2309_04255_amd import draft
+
+
+class TableSession:
+    """Answers a tree-decoder step for the node `first` with the row forward(tokens, parent)."""
+
+    def __init__(self, forward):
+        self.forward = forward
+        self.calls = 0
+
+    def extend(self, prefix_len, tree_tokens, parent, first):
+        assert first == len(tree_tokens) - 1  # one new node per step
+        self.calls += 1
+        row = self.forward(np.asarray(tree_tokens), np.asarray(parent))
+        return torch.from_numpy(np.asarray(row, dtype=np.float32)[None, :])
+
+
+def _random_forward(vocab, seed, peak):
+    """Successor logits keyed by the fed token's branch: a few large logits so
+    that several tokens land near the threshold, plus exact ties."""
+
+    def forward(tokens, parent):
+        key = hash((seed, tuple(int(t) for t in tokens), tuple(int(q) for q in parent))) & 0xFFFFFFFF
+        g = np.random.default_rng(key)
+        row = g.normal(0, 1, vocab)
+        hot = g.choice(vocab, 4, replace=False)
+        row[hot] += peak * g.random(4)
+        row[hot[1]] = row[hot[2]]  # an exact tie among the likely tokens
+        return row.astype(np.float32)
+
+    return forward
+
+
+def test_hand_worked_example():
+    table = {0: {1: .60, 2: .35}, 1: {3: .50, 4: .45}, 2: {5: .90}}
+
+    def forward(tokens, parent):
+        p = dict(table.get(int(tokens[-1]), {6: .95}))
+        rest = (1.0 - sum(p.values())) / (8 - len(p))
+        return np.log(np.array([p.get(t, rest) for t in range(8)]))
+
+    tok, par, info = draft.generate_tree(TableSession(forward), 0, 0, 3, threshold=0.3)
+    assert tok.tolist() == [0, 1, 2, 5, 3, 4, 6]
+    assert par.tolist() == [-1, 0, 0, 2, 1, 1, 3]
+    assert info["fed"] == 4
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("threshold", [0.3, 0.1, 0.02])
+def test_matches_oracle_generator(seed, threshold):
+    forward = _random_forward(64, seed, peak=9.0)
+    sess = TableSession(forward)
+    tok, par, info = draft.generate_tree(sess, 0, 5, 10, threshold=threshold)
+    otok, opar, oinfo = oracle.generate_tree(None, None, None, 5, 10, threshold=threshold,
+                                             forward=lambda t, p: forward(t, p).astype(np.float64))
+    np.testing.assert_array_equal(tok, otok)
+    np.testing.assert_array_equal(par, opar)
+    np.testing.assert_allclose(info["conf"], oinfo["conf"], rtol=1e-12)
+    assert sess.calls == 11
