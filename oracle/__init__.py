@@ -19,7 +19,9 @@ Contents
             §3.2 "Token tree verification and rectification")
   draft.py  draft-side tree generation: the tree decoder, the 30% branch
             threshold and the confidence-based branch pacer (§3.1, §3.2
-            "Token tree generation", Eq. 1)
+            "Token tree generation", Eq. 1), with the fallback stop
+  fallback.py  self-adaptive fallback: tree-cumulative confidence and the
+            threshold update of Eq. 3 (§3.3)
 
 Every function is pinned by tests/test_oracle_*.py against something other
 than itself: brute force, an independent library implementation
@@ -45,3 +47,4 @@ from .model import (  # noqa: F401
 from .walk import accept_walk, branch_sequences, correct_sequences  # noqa: F401
 from .decode import commit_path, greedy_decode, speculative_decode  # noqa: F401
 from .draft import generate_tree  # noqa: F401
+from .fallback import DEFAULT_ALPHA, tree_confidence, update_alpha, most_matching_branch  # noqa: F401

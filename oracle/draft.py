@@ -35,7 +35,7 @@ def _softmax64(row):
 
 
 def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold=0.3, rounding=True,
-                  forward=None):
+                  forward=None, alpha=None):
     """Grow a draft tree with `iterations` fed nodes after the root.
 
     prefix_k/prefix_v: the draft model's prefix keys/values [L, P, H, Dh].
@@ -44,6 +44,12 @@ def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold
     where info holds the number of fed nodes, each fed node's probability, the
     pending candidates and, per iteration, the pacer's margin (largest deficit
     minus the runner-up).
+
+    alpha: the self-adaptive fallback threshold (§3.3); when given, growth
+    stops after the first draft step whose tree-cumulative confidence T_c
+    (the largest cumulative confidence of a pending candidate) is below it,
+    and `iterations` is only the cap (the pacer's M).  info["t_c"] lists T_c
+    after each step (the root's expansion first).
     """
     if forward is None:
         def forward(tokens, parent):
@@ -65,10 +71,18 @@ def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold
                 break
             pending.append((int(t), node, float(prob[t]), cum * float(prob[t]), depth))
 
+    def fall_back():
+        t_cs.append(max(c for _, _, _, c, _ in pending))
+        return alpha is not None and t_cs[-1] < alpha
+
+    t_cs = []
     expand(0)
+    stop = fall_back()
     M = iterations
     gaps = []  # per iteration: largest deficit minus the runner-up (inf with one candidate)
     for _ in range(iterations):
+        if stop:
+            break
         total = sum(c for _, _, _, c, _ in pending)
         deficits = [M * c / total - d for _, _, _, c, d in pending]
         k = int(np.argmax(deficits))  # first maximum: the earliest candidate
@@ -79,11 +93,12 @@ def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold
         parent.append(par)
         conf.append(p)
         expand(len(tokens) - 1)
+        stop = fall_back()
     # the tree for verification: the fed nodes, then the pending candidates as leaves
     all_tokens = tokens + [t for t, _, _, _, _ in pending]
     all_parent = parent + [q for _, q, _, _, _ in pending]
     info = {"fed": len(tokens), "conf": conf, "pending": [(t, q, p) for t, q, p, _, _ in pending],
-            "deficit_gaps": gaps}
+            "deficit_gaps": gaps, "t_c": t_cs}
     return np.asarray(all_tokens, dtype=np.int64), np.asarray(all_parent, dtype=np.int64), info
 
 
