@@ -14,6 +14,11 @@ token:
   their probabilities), the candidate with the largest M C / sum(C) - T is fed
   next (the earliest created among equal ones).
 
+Self-adaptive fallback (§3.3): with a threshold alpha, growth stops after
+the first step whose tree-cumulative confidence T_c (the largest cumulative
+confidence of a pending candidate) is below alpha, and the target verifies;
+`Fallback` updates alpha after each verification (Eq. 3).
+
 Host control: the probabilities of one row (float64 softmax of the returned
 logits) and the pacer's choice are computed on the host between steps, which
 need the host anyway (the next node depends on them).  Nodes are numbered in
@@ -63,23 +68,55 @@ def _probs(logits_row):
     return z / z.sum()
 
 
-def generate_tree(sess, prefix_len: int, root_token: int, iterations: int, threshold: float = 0.3):
-    """Grow a draft tree with `iterations` fed nodes after the root, on the
-    draft model in `sess`.  Returns (tree_tokens, parent, info): the tree for
+def generate_tree(sess, prefix_len: int, root_token: int, iterations: int, threshold: float = 0.3,
+                  alpha: float | None = None):
+    """Grow a draft tree with `iterations` fed nodes after the root (at most,
+    when `alpha` is given: see the module docstring), on the draft model in
+    `sess`.  Returns (tree_tokens, parent, info): the tree for
     verification (fed nodes, then the pending candidates), and info with the
-    number of fed nodes, each fed node's probability and the fed nodes'
-    logits rows ("fed", "conf", "logits")."""
+    number of fed nodes, each fed node's probability, the fed nodes' logits
+    rows and T_c after each step ("fed", "conf", "logits", "t_c")."""
     tree = _Tree(root_token)
-    rows = []
+    rows, t_c = [], []
     node = 0
     for it in range(iterations + 1):
         row = sess.extend(prefix_len, np.asarray(tree.tok), np.asarray(tree.par), node)[0]
         rows.append(row.float().cpu().numpy())
         tree.add_candidates(node, _probs(rows[-1]), threshold)
-        if it == iterations:
+        t_c.append(max(tree.cum[q] * p for _, q, p in tree.cand))
+        if it == iterations or (alpha is not None and t_c[-1] < alpha):
             break
         node = tree.feed(tree.pick(iterations))
     tok = np.asarray(tree.tok + [c[0] for c in tree.cand], dtype=np.int32)
     par = np.asarray(tree.par + [c[1] for c in tree.cand], dtype=np.int32)
     conf = [1.0] + [tree.cum[i] / tree.cum[tree.par[i]] for i in range(1, len(tree.tok))]
-    return tok, par, {"fed": len(tree.tok), "conf": conf, "logits": np.stack(rows)}
+    return tok, par, {"fed": len(tree.tok), "conf": conf, "logits": np.stack(rows), "t_c": t_c}
+
+
+class Fallback:
+    """The self-adaptive threshold alpha of §3.3 (default 0.01)."""
+
+    def __init__(self, alpha: float = 0.01):
+        self.alpha = alpha
+
+    def update(self, parent, path, t_c: float) -> float:
+        """Eq. 3 after a verification of the tree `parent` that accepted the
+        nodes `path` (root first).  The most matching branch is the deepest
+        root-to-leaf branch through the last accepted node; its draft tokens
+        are N_all, the accepted ones N_correct."""
+        parent = np.asarray(parent)
+        n = len(parent)
+        depth = np.zeros(n, dtype=np.int64)
+        under = np.zeros(n, dtype=bool)
+        under[path[-1]] = True
+        for i in range(1, n):
+            depth[i] = depth[parent[i]] + 1
+            under[i] |= under[parent[i]]
+        n_all = int(depth[under].max())
+        n_correct = len(path) - 1
+        if n_all > 0:
+            if n_correct == n_all:
+                self.alpha *= 0.5
+            else:
+                self.alpha /= t_c ** ((n_all - n_correct) / n_all)
+        return self.alpha

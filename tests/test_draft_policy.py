@@ -68,3 +68,34 @@ def test_matches_oracle_generator(seed, threshold):
     np.testing.assert_array_equal(par, opar)
     np.testing.assert_allclose(info["conf"], oinfo["conf"], rtol=1e-12)
     assert sess.calls == 11
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("alpha", [0.5, 0.05, 0.005])
+def test_fallback_stop_matches_oracle(seed, alpha):
+    forward = _random_forward(64, seed, peak=6.0)
+    tok, par, info = draft.generate_tree(TableSession(forward), 0, 5, 12, threshold=0.1, alpha=alpha)
+    otok, opar, oinfo = oracle.generate_tree(None, None, None, 5, 12, threshold=0.1, alpha=alpha,
+                                             forward=lambda t, p: forward(t, p).astype(np.float64))
+    np.testing.assert_array_equal(tok, otok)
+    np.testing.assert_array_equal(par, opar)
+    np.testing.assert_allclose(info["t_c"], oinfo["t_c"], rtol=1e-12)
+
+
+def test_fallback_update_matches_oracle():
+    rng = np.random.default_rng(7)
+    fb, alpha = draft.Fallback(), oracle.DEFAULT_ALPHA
+    assert fb.alpha == alpha
+    for _ in range(200):
+        n = int(rng.integers(2, 20))
+        parent = [-1] + [int(rng.integers(0, i)) for i in range(1, n)]
+        path = [0]
+        while True:  # an accepted path: a random descent that may stop anywhere
+            kids = [i for i in range(n) if parent[i] == path[-1]]
+            if not kids or rng.random() < 0.3:
+                break
+            path.append(int(rng.choice(kids)))
+        t_c = float(rng.uniform(0.01, 1.0))
+        n_all, n_correct = oracle.most_matching_branch(parent, path)
+        alpha = oracle.update_alpha(alpha, n_correct, n_all, t_c)
+        assert fb.update(parent, path, t_c) == pytest.approx(alpha, rel=1e-12)

@@ -30,8 +30,8 @@ pytestmark = pytest.mark.gpu
 
 DRAFT = workloads.ModelShape("draft_tiny", 2, 256, 4, 64, 688, 1024, weight_std=0.3, seed=0x5EEDD001)
 P = 24
-# threshold, prefix seed, iterations
-CASES = [(0.3, 51, 12), (0.15, 40, 12), (0.15, 45, 16)]
+# threshold, prefix seed, iterations, fallback threshold alpha (§3.3) or None
+CASES = [(0.3, 51, 12, None), (0.15, 40, 12, None), (0.15, 45, 16, None), (0.15, 45, 16, 0.03)]
 
 
 @pytest.fixture(scope="module")
@@ -52,19 +52,23 @@ def _softmax(rows):
     return z / z.sum(axis=-1, keepdims=True)
 
 
-@pytest.mark.parametrize("threshold,seed,iterations", CASES)
-def test_draft_tree_matches_oracle(draft_model, threshold, seed, iterations):
+@pytest.mark.parametrize("threshold,seed,iterations,alpha", CASES)
+def test_draft_tree_matches_oracle(draft_model, threshold, seed, iterations, alpha):
     from paper_2309_04255_amd import draft
 
     sess, ow = draft_model
     prefix = workloads.draw_tokens(P, DRAFT.vocab, seed=seed)
     root = int(workloads.draw_tokens(1, DRAFT.vocab, seed=seed, stream=9)[0])
-    what = f"thr={threshold} seed={seed} it={iterations}"
+    what = f"thr={threshold} seed={seed} it={iterations} alpha={alpha}"
     print(f"\n[draft] {what}", flush=True)
     sess.prefill(prefix, 0)
-    tok, par, info = draft.generate_tree(sess, P, root, iterations, threshold)
+    tok, par, info = draft.generate_tree(sess, P, root, iterations, threshold, alpha=alpha)
     fed = info["fed"]
-    assert fed == iterations + 1 and len(tok) > fed
+    assert len(tok) > fed
+    if alpha is None:
+        assert fed == iterations + 1
+    else:  # stopped by the fallback before the cap
+        assert fed < iterations + 1 and info["t_c"][-1] < alpha <= min(info["t_c"][:-1])
     assert np.any(np.bincount(par[1:], minlength=len(par)) >= 2), "no branching"
     gpu_rows = info["logits"]
 
@@ -87,7 +91,8 @@ def test_draft_tree_matches_oracle(draft_model, threshold, seed, iterations):
         np.testing.assert_array_equal(parent, par[:len(parent)])
         return gpu_rows[len(tokens) - 1]
 
-    otok, opar, oinfo = oracle.generate_tree(None, None, None, root, iterations, threshold, forward=replay)
+    otok, opar, oinfo = oracle.generate_tree(None, None, None, root, iterations, threshold, forward=replay,
+                                             alpha=alpha)
     np.testing.assert_array_equal(otok, tok)
     np.testing.assert_array_equal(opar, par)
     np.testing.assert_allclose(oinfo["conf"], info["conf"], rtol=1e-12)
