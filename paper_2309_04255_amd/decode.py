@@ -35,3 +35,45 @@ def speculative_decode(sess, prefix_len: int, first_token: int, steps: int, draf
         prefix_len += acc + 1
         root = nxt
     return np.asarray(out[:steps], dtype=np.int64), log, prefix_len
+
+
+def draft_decode(target, drafter, prefix_len: int, first_token: int, steps: int, iterations: int = 8,
+                 threshold: float = 0.3, fallback=None):
+    """The generate-and-verify loop with a draft model (§3.1, §3.2, §3.3).
+
+    `target` and `drafter` are Sessions whose caches hold the same prefix of
+    length prefix_len.  Each iteration the drafter grows a tree from the
+    current token (draft.generate_tree, stopped by the fallback threshold
+    alpha or at `iterations` fed nodes), the target verifies it and rolls its
+    cache back to the verified sequence, the drafter's cache is rolled back
+    with the same accepted path, and alpha is updated (Eq. 3).  An accepted
+    node that the drafter never fed (a pending candidate, always the last
+    one of the path) gets its keys/values from one tree-decoder step.
+    Returns (tokens, per-iteration log, final prefix length)."""
+    import numpy as np
+
+    from . import binding, draft
+
+    fb = fallback if fallback is not None else draft.Fallback()
+    out, log, root = [], [], int(first_token)
+    while len(out) < steps:
+        alpha = fb.alpha
+        tok, par, info = draft.generate_tree(drafter, prefix_len, root, iterations, threshold, alpha=alpha)
+        n = len(tok)
+        target.verify_tree(prefix_len, tok, par, want_logits=False)
+        target.commit(prefix_len, n)
+        binding.commit_path(drafter.cfg, drafter.k_cache, drafter.v_cache, prefix_len, target.path,
+                            target.accept_len, n)
+        acc = int(target.accept_len.item())  # (synchronises: the next tree depends on it)
+        path = [int(x) for x in target.path[: acc + 1].cpu()]
+        nxt = int(target.next_token.item())
+        if path[-1] >= info["fed"]:
+            chain = np.asarray([tok[i] for i in path])
+            drafter.extend(prefix_len, chain, np.arange(-1, acc), acc)
+        fb.update(par, path, info["t_c"][-1])
+        out += [int(tok[i]) for i in path[1:]] + [nxt]
+        log.append({"accept_len": acc, "nodes": n, "fed": info["fed"], "alpha": alpha,
+                    "t_c": info["t_c"][-1], "prefix_len": prefix_len})
+        prefix_len += acc + 1
+        root = nxt
+    return out[:steps], log, prefix_len

@@ -140,3 +140,42 @@ def test_loop_with_one_node_trees_is_greedy_decoding(model):
                                               lambda root, produced: (np.array([root]), np.array([-1])))
     assert _compare_with_greedy(m, out, "one-node") == 8
     assert all(r["accept_len"] == 0 for r in log)
+
+
+@pytest.mark.parametrize("drafter_kind,threshold,alpha", [("self", 0.3, 1e-4), ("self", 0.03, 1e-3),
+                                                          ("other", 0.03, 0.01)])
+def test_draft_model_loop_is_greedy(model, drafter_kind, threshold, alpha):
+    # The full loop with a draft model (§3.1-§3.3): the drafter grows each tree
+    # (threshold, branch pacer, fallback), the target verifies and both caches
+    # roll back.  "self" drafts with the target's own weights (most drafts are
+    # accepted, and the last accepted node is often a candidate the drafter
+    # never fed); "other" with a different random model (almost nothing is
+    # accepted).  Either way the output is the target's greedy decoding, and
+    # the drafter's cache holds the accepted sequence's keys/values.
+    m = model
+    from paper_2309_04255_amd import draft
+
+    shape = m.shape if drafter_kind == "self" else workloads.ModelShape(
+        m.shape.name + "_draft", m.shape.n_layers, m.shape.d_model, m.shape.n_heads, m.shape.head_dim,
+        m.shape.d_ffn, m.shape.vocab, seed=m.shape.seed ^ 0xD0)
+    drafter = m.binding.Session(shape, capacity=P + 200, max_n=128)
+    m.binding.workspace_init(drafter.cfg, 128, drafter.workspace)
+    drafter.load_weights(workloads.make_weights(shape, "cuda", gain_jitter=0.1))
+    _reset(m)
+    drafter.prefill(m.prefix, 0)
+    what = f"{m.shape.name}/draft-{drafter_kind}/thr={threshold}/alpha={alpha}"
+    print(f"[{what}]", flush=True)
+    out, log, plen = m.decode.draft_decode(m.sess, drafter, P, m.first, STEPS, iterations=6,
+                                           threshold=threshold, fallback=draft.Fallback(alpha))
+    agree = _compare_with_greedy(m, out, what)
+    accs = [e["accept_len"] for e in log]
+    print(f"[{what}] {len(log)} passes, accept lengths {accs}, nodes {[e['nodes'] for e in log]}, "
+          f"agree {agree}/{len(out)}", flush=True)
+    if drafter_kind == "self":
+        assert sum(accs) >= len(accs), accs   # self-drafting accepts on average at least one token per pass
+    # the drafter's cache rows [P, plen) hold the accepted sequence's keys/values, as the target's do
+    for a, b in ((drafter.k_cache, m.sess.k_cache), (drafter.v_cache, m.sess.v_cache)):
+        if drafter_kind == "self":
+            ga = a[:, :, P:plen].float()
+            gb = b[:, :, P:plen].float()
+            assert (ga - gb).abs().max().item() <= 2e-2 * gb.abs().max().item()
