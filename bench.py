@@ -56,16 +56,21 @@ def source_hash():
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload):
-    """Measured HBM bytes per pass-kernel launch (FETCH_SIZE + WRITE_SIZE,
-    calibrated against a copy kernel), or None when the counters were taken
-    on other kernel sources or another workload."""
+def _read_traffic():
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
-        return None
-    if t.get("kernel_sources_sha256_16") != source_hash() or t.get("workload") != workload:
+        return {}
+    return t if isinstance(t, dict) else {}
+
+
+def load_traffic(workload):
+    """Measured HBM bytes per pass-kernel launch for this workload (FETCH_SIZE
+    + WRITE_SIZE, calibrated against a copy kernel), or None when the counters
+    were taken on other kernel sources or never for this workload."""
+    t = _read_traffic().get(workload)
+    if not t or t.get("kernel_sources_sha256_16") != source_hash():
         return None
     return t.get("bytes_per_launch")
 
@@ -75,8 +80,8 @@ def write_traffic(fetch_csv, write_csv, workload, copy_mib):
     (one collecting FETCH_SIZE, one WRITE_SIZE; per dispatch, in KiB), the
     pass kernel's HBM bytes per launch.  Calibration: the N MiB fill that
     precedes the copy writes a known size (write factor), and the copy's
-    chunks read as much as they write (read factor).  Writes TRAFFIC_FILE
-    tagged with the kernel sources' hash."""
+    chunks read as much as they write (read factor).  Stores the entry for
+    `workload` in TRAFFIC_FILE, tagged with the kernel sources' hash."""
     import csv
 
     def per_kernel(path):
@@ -96,82 +101,89 @@ def write_traffic(fetch_csv, write_csv, workload, copy_mib):
     chunk_fetch = statistics.median(v for v in fetch[copy] if v > 4096)
     chunk_write = statistics.median(v for v in write[copy] if v > 4096)
     read_factor = chunk_write * write_factor / chunk_fetch
-    # (the prefill's passes run another instance of the pass kernel, for
-    # 128-row chunks; the verification passes are the most frequent one)
-    passk = max((k for k in fetch if "pass_kernel" in k), key=lambda k: len(fetch[k]))
-    f_kib, w_kib = statistics.mean(fetch[passk]), statistics.mean(write[passk])
+    # The verification passes are the last launches of the pass kernel in the
+    # run (the prefill's 128-row chunks run before them, as another instance
+    # when the tree has fewer rows): take the instance launched last, and its
+    # launches after the prefill.
+    names = [k for k in fetch if "pass_kernel" in k]
+    passk = max(names, key=lambda k: len(fetch[k]))
+    f_kib, w_kib = statistics.median(fetch[passk][-3:]), statistics.median(write[passk][-3:])
     out = {
         "workload": workload, "kernel_sources_sha256_16": source_hash(), "kernel": passk[:90],
-        "launches": len(fetch[passk]), "fetch_kib_mean": round(f_kib), "write_kib_mean": round(w_kib),
+        "launches_used": 3, "fetch_kib": round(f_kib), "write_kib": round(w_kib),
         "calibration": {"fill_mib": copy_mib, "fill_write_kib": fill_kib, "write_factor": round(write_factor, 4),
                         "copy_chunk_fetch_kib": chunk_fetch, "copy_chunk_write_kib": chunk_write,
                         "read_factor": round(read_factor, 4)},
         "read_bytes": round(f_kib * 1024 * read_factor), "write_bytes": round(w_kib * 1024 * write_factor),
     }
     out["bytes_per_launch"] = out["read_bytes"] + out["write_bytes"]
+    all_t = _read_traffic()
+    all_t[workload] = out
     with open(TRAFFIC_FILE, "w") as f:
-        json.dump(out, f, indent=1)
+        json.dump(all_t, f, indent=1, sort_keys=True)
         f.write("\n")
     print(json.dumps(out, indent=1))
 
 
-def cpu_baseline(shape, P, n, seed):
-    """Time the CPU oracle on a bounded sample: tree_forward with 1 and 2 of the
-    model's layers (+ embedding and LM head); one pass = t1 + (L-1)(t2 - t1)."""
+def cpu_baseline(gen, shape, P, parent, tok, seed):
+    """Time the CPU oracle on one whole pass of the workload: oracle.tree_layer
+    over every layer (float64 NumPy with the bf16 rounding points), then the
+    final norm and LM head.  The weights come from the seeded generator on the
+    GPU, widened to float64 there and copied to the host one layer at a time;
+    that preparation is not timed (it is reported apart), the oracle's
+    arithmetic is.  The prefix keys/values are random bf16 values of the
+    workload's shape (their values do not change the oracle's cost)."""
     import numpy as np
+    import torch
 
     import oracle
-    import workloads
 
     try:
         from threadpoolctl import threadpool_info
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # threadpoolctl missing: report the visible cores
         threads = os.cpu_count() or 1
-    gen = workloads.make_weights(shape, "cpu")
 
-    def np64(t):
-        return t.float().numpy().astype(np.float64)
+    def host64(t):
+        return t.double().cpu().numpy()
 
-    t0 = time.perf_counter()
-    layers = {l: {k: np64(v) for k, v in gen.layer(l).items()} for l in (0, 1)}
-    emb, fin, head = np64(gen.tok_embed()), np64(gen.final_norm()), np64(gen.lm_head())
-    log(f"cpu baseline: weights for 2 layers converted in {time.perf_counter() - t0:.1f}s")
+    cfg = oracle.OracleConfig(shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim, shape.d_ffn,
+                              shape.vocab, shape.rms_eps, shape.rope_theta)
+    layer = {}
+    t_prep = time.perf_counter()
+    w = oracle.OracleWeights(cfg, np.zeros((1, shape.d_model)), host64(gen.final_norm()), host64(gen.lm_head()),
+                             lambda l: layer[l], cache=False)
+    x = host64(gen.tok_embed()[torch.as_tensor(np.asarray(tok, dtype=np.int64), device="cuda")])
+    prep = time.perf_counter() - t_prep
     rng = np.random.default_rng(seed)
     H, Dh = shape.n_heads, shape.head_dim
-    pk = oracle.bf16_round(rng.standard_normal((2, P, H, Dh)))
-    pv = oracle.bf16_round(rng.standard_normal((2, P, H, Dh)))
-    parent, tok = workloads.make_tree(("complete", (2, 2, 2, 2)), shape.vocab, seed) \
-        if n == 31 else workloads.make_tree(("random", n, 7), shape.vocab, seed)
-
-    def run(nl):
-        cfg = oracle.OracleConfig(nl, shape.d_model, shape.n_heads, shape.head_dim, shape.d_ffn,
-                                  shape.vocab, shape.rms_eps, shape.rope_theta)
-        w = oracle.OracleWeights(cfg, emb, fin, head, lambda l: layers[l])
-        w.layer(0)
-        if nl > 1:
-            w.layer(1)
-        t = time.perf_counter()
-        oracle.tree_forward(w, pk[:nl], pv[:nl], tok, parent, rounding=True)
-        return time.perf_counter() - t
-
-    reps = []
-    for _ in range(3):
-        t1, t2 = run(1), run(2)
-        reps.append((t1, t2))
-    t1 = statistics.median(r[0] for r in reps)
-    t2 = statistics.median(r[1] for r in reps)
-    per_pass = t1 + (shape.n_layers - 1) * max(t2 - t1, 0.0)
-    log(f"cpu baseline: 1 layer {t1:.2f}s, 2 layers {t2:.2f}s -> {per_pass:.1f}s per pass")
+    t_calc = 0.0
+    for l in range(shape.n_layers):
+        t0 = time.perf_counter()
+        layer.clear()
+        layer[l] = {k: host64(v) for k, v in gen.layer(l).items()}
+        pk = oracle.bf16_round(rng.standard_normal((P, H, Dh)))
+        pv = oracle.bf16_round(rng.standard_normal((P, H, Dh)))
+        t1 = time.perf_counter()
+        _, x, _, _ = oracle.tree_layer(w, l, x, pk, pv, parent, rounding=True)
+        t2 = time.perf_counter()
+        prep += t1 - t0
+        t_calc += t2 - t1
+    t0 = time.perf_counter()
+    oracle.logits_from_stream(w, x)
+    t_calc += time.perf_counter() - t0
+    layer.clear()
+    log(f"cpu baseline: oracle pass {t_calc:.1f}s over {shape.n_layers} layers "
+        f"(+{prep:.1f}s of untimed weight preparation)")
     return {
-        "value": 1.0 / per_pass,
+        "value": round(1.0 / t_calc, 5),
         "unit": "passes/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"oracle.tree_forward (float64 NumPy, bf16 storage rounding) with layers 0 and 1 "
-                   f"of the {shape.n_layers}-layer model plus embedding and LM head, P={P}, n={n}; "
-                   f"median of 3; pass = t(1 layer) + {shape.n_layers - 1} x (t(2) - t(1)); "
-                   f"host cores visible: {os.cpu_count()}"),
+        "sample": (f"one whole pass of the workload (P={P}, n={len(parent)}): oracle.tree_layer over all "
+                   f"{shape.n_layers} layers, then the final norm and LM head, float64 NumPy with the bf16 "
+                   f"rounding points; weight conversion ({prep:.1f}s, untimed) excluded; BLAS threads "
+                   f"{threads}, host cores visible {os.cpu_count()}"),
     }
 
 
@@ -196,7 +208,7 @@ def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
         out = []
         for t in range(k):
             sess.verify_tree(plen + t, np.array([root]), np.array([-1]), want_logits=False)
-            root = int(sess.next_token.item())
+            root = sess.outcome()[2]
             out.append(root)
         return out
 
@@ -210,14 +222,13 @@ def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
         t = time.perf_counter()
         sess.verify_tree(plen, ptok, parent, want_logits=False)
         sess.commit(plen, n)
-        acc = int(sess.accept_len.item())
-        nxt = int(sess.next_token.item())
+        path, acc, nxt = sess.outcome()
         dt = time.perf_counter() - t
         if it > 0:
             t_loop += dt
             made += acc + 1
             accs.append(acc)
-        last = (plen, [int(x) for x in sess.path[: acc + 1].cpu()])
+        last = (plen, path)
         plen, root = plen + acc + 1, nxt
     # rollback kernel alone: the last tree's accepted rows, moved again
     # (the same rows, the same bytes)
@@ -290,47 +301,15 @@ def draft_generation(sess, plen, root, iterations, threshold=0.3):
     }
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="llama7b_p512_n31")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-decode-loop", action="store_true",
-                    help="skip the generate-and-verify loop measurement")
-    ap.add_argument("--calibration-copy-mib", type=int, default=0,
-                    help="(profiling) first copy this many MiB three times: the counter calibration")
-    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="write the traffic file from two rocprofv3 --pmc counter CSVs and exit")
-    args = ap.parse_args()
-    if args.write_traffic:
-        write_traffic(args.write_traffic[0], args.write_traffic[1], args.workload,
-                      args.calibration_copy_mib or 1024)
-        return
-    if args.gpus != 1:
-        print("bench.py measures a single GPU: this build has no multi-GPU path "
-              "(run with --gpus 1).", file=sys.stderr)
-        sys.exit(2)
-
+def setup_model(shape, capacity):
+    """Session with the model's packed weights (seeded generator run on the GPU)."""
     import torch
 
     import workloads
     from paper_2309_04255_amd import binding
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a ROCm GPU", file=sys.stderr)
-        sys.exit(1)
-    torch.cuda.set_device(0)
-    wl = workloads.get_workload(args.workload)
-    shape = wl.shape
-    P = wl.prefix_len
-    parent, tok = workloads.make_tree(wl.tree, shape.vocab, wl.seed)
-    n = len(parent)
-    prefix = workloads.draw_tokens(P, shape.vocab, seed=wl.seed)
-
     t0 = time.perf_counter()
-    sess = binding.Session(shape, capacity=P + max(n, 128), max_n=128)
+    sess = binding.Session(shape, capacity=capacity, max_n=128)
     gen = workloads.make_weights(shape, "cuda")
     binding.pack_globals(sess.cfg, gen.tok_embed(), gen.final_norm(), gen.lm_head(), sess.packed)
     for l in range(shape.n_layers):
@@ -339,9 +318,25 @@ def main():
         if l % 8 == 7:
             log(f"packed layer {l + 1}/{shape.n_layers}")
     torch.cuda.empty_cache()
-    sess.prefill(prefix, 0)
-    torch.cuda.synchronize()
-    log(f"setup (weights, packing, {P}-token prefill) {time.perf_counter() - t0:.1f}s")
+    log(f"{shape.name}: weights generated and packed in {time.perf_counter() - t0:.1f}s")
+    return sess, gen
+
+
+def measure(sess, gen, wl, args, headline):
+    """The bench line of one workload on a session holding its model."""
+    import torch
+
+    import workloads
+    from paper_2309_04255_amd import binding
+
+    shape = wl.shape
+    P = wl.prefix_len
+    parent, tok = workloads.make_tree(wl.tree, shape.vocab, wl.seed)
+    n = len(parent)
+    t0 = time.perf_counter()
+    sess.prefill(workloads.draw_tokens(P, shape.vocab, seed=wl.seed), 0)
+    sess.check("prefill")
+    log(f"{wl.name}: {P}-token prefill {time.perf_counter() - t0:.2f}s")
 
     def one_pass():
         binding.verify_tree(sess.cfg, sess.packed, sess.k_cache, sess.v_cache, P, tok, parent,
@@ -357,50 +352,50 @@ def main():
 
     for _ in range(args.warmup):
         one_pass()
-    torch.cuda.synchronize()
+    sess.outcome()
 
+    # The timed steps: a pass and the read-back of its result (status, path,
+    # accept_len, next token: what a decode loop waits for before its next
+    # tree), back to back.  Inputs (weights, KV cache, tree) are resident.
+    torch.cuda.synchronize()
+    step_s = []
+    w0 = time.perf_counter()
+    for _ in range(args.steps):
+        t = time.perf_counter()
+        one_pass()
+        sess.outcome()
+        step_s.append(time.perf_counter() - t)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_per_pass = 1e3 * wall / args.steps
+    value = args.steps / wall
+    reps = [1e3 * sum(step_s[i:i + 50]) / len(step_s[i:i + 50]) for i in range(0, len(step_s), 50)]
+    log(f"{wl.name}: timed {args.steps} passes with read-back: {wall * 1e3:.1f} ms -> {ms_per_pass:.3f} ms/pass "
+        f"(per 50-pass repetition: {[round(r, 4) for r in reps]})")
+
+    # Dominant kernel: the pass kernel itself, timed per launch with HIP events
+    # recorded by the library on the stream it launches on, over the same
+    # number of back-to-back passes in the same launch configuration.
+    B = pass_bytes(shape, P, n)
+    binding.timing_enable(binding.KERNEL_PASS, args.steps)
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
     ev0.record(stream)
     for _ in range(args.steps):
         one_pass()
     ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    gpu_s = ev0.elapsed_time(ev1) / 1e3
-    elapsed = max(wall, gpu_s)
-    ms_per_pass = 1e3 * elapsed / args.steps
-    value = args.steps / elapsed
-    log(f"timed {args.steps} passes: wall {wall * 1e3:.1f} ms, events {gpu_s * 1e3:.1f} ms "
-        f"-> {ms_per_pass:.3f} ms/pass")
-
-    # Dominant kernel: the pass kernel itself, timed per launch with HIP events
-    # recorded by the library on the stream it launches on, over the same
-    # number of passes in the same launch configuration.
-    B = pass_bytes(shape, P, n)
-    binding.timing_enable(binding.KERNEL_PASS, args.steps)
-    for _ in range(args.steps):
-        one_pass()
-    torch.cuda.synchronize()
+    sess.outcome()
     tot_ms, nl = binding.timing_read(binding.KERNEL_PASS)
     binding.timing_enable(-1, 0)
+    back_to_back_ms = ev0.elapsed_time(ev1) / args.steps
     k_ms = tot_ms / max(nl, 1)
     k_achieved = B / (k_ms / 1e3)
-    log(f"pass kernel: {nl} launches, mean {k_ms * 1e3:.1f} us, {k_achieved / 1e9:.0f} GB/s")
+    log(f"{wl.name}: pass kernel {nl} launches, mean {k_ms * 1e3:.1f} us, {k_achieved / 1e9:.0f} GB/s; "
+        f"back to back {back_to_back_ms * 1e3:.1f} us per pass")
 
-    # Latency of a pass when the decode loop waits for the accepted path.
-    lat = []
-    for _ in range(min(args.steps, 20)):
-        t = time.perf_counter()
-        one_pass()
-        sess.accept_len.cpu()
-        lat.append(time.perf_counter() - t)
+    decode = decode_loop(sess, shape, P, parent, tok) if headline and not args.no_decode_loop else None
 
-    decode = None if args.no_decode_loop else decode_loop(sess, shape, P, parent, tok)
-
-    frac = B / (elapsed / args.steps) / HBM_PEAK
+    frac = B / (wall / args.steps) / HBM_PEAK
     traffic = load_traffic(wl.name)
     out = {
         "metric": METRIC,
@@ -423,10 +418,13 @@ def main():
             "tree_nodes": n,
             "tree": str(wl.tree),
         },
+        "step": "one verification pass + read-back of status / path / accept_len / next token (host sync)",
         "tree_tokens_per_s": round(value * n, 1),
         "hbm_roofline_frac": round(frac, 4),
         "pass_alg_bytes": B,
-        "ms_per_pass_with_readback": round(1e3 * statistics.median(lat), 4),
+        "ms_per_step_median_of_reps": round(statistics.median(reps), 4),
+        "reps_ms_per_step": [round(r, 4) for r in reps],
+        "ms_per_pass_back_to_back": round(back_to_back_ms, 4),
         "roofline": {
             "bound": "hbm",
             "kernel": "pass_kernel (persistent: embed, per layer QKV / attention / O / gate-up / down, LM head, walk)",
@@ -441,10 +439,72 @@ def main():
     }
     if decode is not None:
         out["decode_loop"] = decode
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle (bounded sample)")
-        out["cpu_baseline"] = cpu_baseline(shape, P, n, wl.seed)
-    print(json.dumps(out), flush=True)
+    if not args.no_cpu_baseline and (headline or args.cpu_baseline_all):
+        log(f"{wl.name}: timing the CPU oracle (one whole pass)")
+        out["cpu_baseline"] = cpu_baseline(gen, shape, P, parent, tok, wl.seed)
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama7b_p512_n31",
+                    help="workload name, or several separated by commas (one JSON line each, in order)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-baseline-all", action="store_true",
+                    help="time the CPU oracle for every workload, not only the first")
+    ap.add_argument("--no-decode-loop", action="store_true",
+                    help="skip the generate-and-verify loop measurement")
+    ap.add_argument("--calibration-copy-mib", type=int, default=0,
+                    help="(profiling) first copy this many MiB three times: the counter calibration")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the traffic file from two rocprofv3 --pmc counter CSVs and exit")
+    args = ap.parse_args()
+    if args.write_traffic:
+        write_traffic(args.write_traffic[0], args.write_traffic[1], args.workload,
+                      args.calibration_copy_mib or 1024)
+        return
+    if args.gpus != 1:
+        print("bench.py measures a single GPU: this build has no multi-GPU path "
+              "(run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import faulthandler
+    import gc
+
+    import torch
+
+    import workloads
+    from paper_2309_04255_amd import binding
+
+    faulthandler.enable()
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    names = [w for w in args.workload.split(",") if w]
+    wls = [workloads.get_workload(w) for w in names]
+    sess = gen = None
+    model = None
+    for i, wl in enumerate(wls):
+        if wl.model != model:
+            sess = gen = None
+            gc.collect()
+            torch.cuda.empty_cache()
+            cap = max(w.prefix_len for w in wls if w.model == wl.model) + 128
+            sess, gen = setup_model(wl.shape, cap)
+            model = wl.model
+        print(json.dumps(measure(sess, gen, wl, args, headline=i == 0)), flush=True)
+    # Leave nothing of the library's behind for the interpreter's exit: no
+    # timing events, no device buffers, no work in flight.
+    binding.timing_enable(-1, 0)
+    sess = gen = None
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    log("done")
 
 
 if __name__ == "__main__":

@@ -35,7 +35,7 @@ def _softmax64(row):
 
 
 def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold=0.3, rounding=True,
-                  forward=None, alpha=None):
+                  forward=None, alpha=None, max_nodes=128):
     """Grow a draft tree with `iterations` fed nodes after the root.
 
     prefix_k/prefix_v: the draft model's prefix keys/values [L, P, H, Dh].
@@ -50,6 +50,12 @@ def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold
     (the largest cumulative confidence of a pending candidate) is below it,
     and `iterations` is only the cap (the pacer's M).  info["t_c"] lists T_c
     after each step (the root's expansion first).
+
+    max_nodes: the largest tree the verifier takes (the paper sets no size;
+    this is a resource cap).  A candidate is added only while the tree (fed
+    nodes plus pending candidates) holds fewer nodes, except the fed node's
+    most likely successor, which always is; growth stops once the tree holds
+    max_nodes nodes, since the next expansion would find no room.
     """
     if forward is None:
         def forward(tokens, parent):
@@ -67,7 +73,7 @@ def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold
         depth = len(_branch(parent, node)) + 1  # draft tokens of the candidate's branch
         pending.append((best, node, float(prob[best]), cum * float(prob[best]), depth))
         for t in order[1:]:
-            if prob[t] <= threshold:
+            if prob[t] <= threshold or len(tokens) + len(pending) >= max_nodes:
                 break
             pending.append((int(t), node, float(prob[t]), cum * float(prob[t]), depth))
 
@@ -81,7 +87,7 @@ def generate_tree(weights, prefix_k, prefix_v, root_token, iterations, threshold
     M = iterations
     gaps = []  # per iteration: largest deficit minus the runner-up (inf with one candidate)
     for _ in range(iterations):
-        if stop:
+        if stop or len(tokens) + len(pending) >= max_nodes:
             break
         total = sum(c for _, _, _, c, _ in pending)
         deficits = [M * c / total - d for _, _, _, c, d in pending]

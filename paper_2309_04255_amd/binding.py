@@ -67,6 +67,22 @@ class LlmcadError(RuntimeError):
         super().__init__(f"{what}: {status_string(status)} ({status})")
 
 
+# Device pass status (workspace region 5), written by the pass kernel.
+PASS_OK = 0
+PASS_WAIT_TIMEOUT = 1   # a wait of the single-launch pass ran out of its bounded spin
+PASS_BAD_PARAMS = 3     # the kernel did not find its parameter block; it did nothing
+_PASS_TEXT = {PASS_WAIT_TIMEOUT: "a grid or join wait ran out of its bounded spin (outputs invalid)",
+              PASS_BAD_PARAMS: "the kernel did not find its parameter block (nothing computed)"}
+
+
+class LlmcadPassError(RuntimeError):
+    """A pass ended with a non-zero device status: its outputs are invalid."""
+
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: device pass status {status}: {_PASS_TEXT.get(status, 'unknown')}")
+
+
 def _load():
     if not os.path.exists(_LIB_PATH):
         raise ImportError(
@@ -275,6 +291,26 @@ class Session:
         self.accept_len = torch.empty(1, dtype=torch.int32, device=self.device)
         self.next_token = torch.empty(1, dtype=torch.int32, device=self.device)
         self.last_logits = torch.empty(shape.vocab, dtype=torch.float32, device=self.device)
+        off, _ = workspace_region(self.cfg, self.max_n, 5)  # (same offset for every pass size)
+        self._status = self.workspace[off:off + 4].view(torch.int32)
+        self._status_host = torch.zeros(1, dtype=torch.int32, pin_memory=True)
+
+    def pass_status(self) -> int:
+        """The device status of the passes enqueued so far (synchronises the stream)."""
+        self._status_host.copy_(self._status, non_blocking=True)
+        torch.cuda.current_stream().synchronize()
+        return int(self._status_host[0])
+
+    def check(self, what="pass"):
+        """Raise LlmcadPassError if a pass since the last check failed on the device.
+        The workspace's counters and status are cleared first, so the session
+        serves the next pass; the failed pass's outputs (and the tree K/V it
+        wrote) are invalid."""
+        st = self.pass_status()
+        if st != PASS_OK:
+            workspace_init(self.cfg, self.max_n, self.workspace)
+            torch.cuda.current_stream().synchronize()
+            raise LlmcadPassError(st, what)
 
     def load_weights(self, gen, layers=None):
         """Pack weights from a generator with tok_embed(), final_norm(), lm_head(), layer(l)
@@ -307,9 +343,29 @@ class Session:
         """Roll the cache back to the verified sequence of the last verify_tree over n nodes."""
         commit_path(self.cfg, self.k_cache, self.v_cache, prefix_len, self.path, self.accept_len, n)
 
-    def results(self, n):
-        """Synchronise and return (logits [n, V] fp32 cpu, path list, accept_len, next_token)."""
+    def outcome(self):
+        """After verify_tree: synchronise, check the device status, and return
+        (path list, accept_len, next_token) -- four small copies, one sync."""
+        if not hasattr(self, "_out_host"):
+            self._out_host = torch.zeros(self.max_n + 3, dtype=torch.int32, pin_memory=True)
+        h = self._out_host
+        h[0:1].copy_(self._status, non_blocking=True)
+        h[1:2].copy_(self.accept_len, non_blocking=True)
+        h[2:3].copy_(self.next_token, non_blocking=True)
+        h[3:].copy_(self.path, non_blocking=True)
         torch.cuda.current_stream().synchronize()
+        st = int(h[0])
+        if st != PASS_OK:
+            workspace_init(self.cfg, self.max_n, self.workspace)
+            torch.cuda.current_stream().synchronize()
+            raise LlmcadPassError(st, "verification pass")
+        acc = int(h[1])
+        return [int(x) for x in h[3:3 + acc + 1]], acc, int(h[2])
+
+    def results(self, n):
+        """Synchronise, check the device status, and return (logits [n, V] fp32 cpu,
+        path list, accept_len, next_token)."""
+        self.check("verification pass")
         acc = int(self.accept_len.item())
         return (self.logits[:n].cpu(), [int(x) for x in self.path[: acc + 1].cpu()], acc,
                 int(self.next_token.item()))

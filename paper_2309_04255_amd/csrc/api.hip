@@ -212,6 +212,9 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.accept_len = a.accept_len;
   p.next_token = a.next_token;
   p.spin_limit = env_int("LLMCAD_SPIN_LIMIT", 4000000);
+  // (diagnostics, for tests of the failure path: every grid wait gives up at
+  // once, so the pass ends with status 1 and every workgroup exits normally)
+  if (env_int("LLMCAD_FAIL_WAITS", 0) == 1) p.spin_limit = -1;
   p.wl_cap = env_int("LLMCAD_WL_STAGES", 1 << 20);  // (diagnostics: a smaller pre-barrier copy)
   p.trace = env_int("LLMCAD_TRACE", 0) ? (long long*)(ws + W.trace) : nullptr;
   TimedLaunch tl(LLMCAD_KERNEL_PASS, a.st);

@@ -156,6 +156,10 @@ __device__ __forceinline__ int poll_grid(const Sync& s, int phase, int G) {
   const int per = G / kBarSlots + (lane < G % kBarSlots ? 1 : 0);
   const int want = lane < slots ? phase * (G < kBarSlots ? 1 : per) : 0;
   const int* slot = s.bar + (lane < slots ? lane : 0) * kBarStride;
+  if (s.limit < 0) {  // (diagnostics: every grid wait gives up at once)
+    if (lane == 0) st_coherent(s.status, 1);
+    return 0;
+  }
   int spins = 0;
   while (true) {
     const int v = lane < slots ? ld_coherent(slot) : 0;

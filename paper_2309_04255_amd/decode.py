@@ -27,9 +27,7 @@ def speculative_decode(sess, prefix_len: int, first_token: int, steps: int, draf
             raise ValueError("the draft tree's root must be the last accepted token")
         n = sess.verify_tree(prefix_len, tree_tokens, parent, want_logits=False)
         sess.commit(prefix_len, n)
-        acc = int(sess.accept_len.item())  # (synchronises: the next tree depends on it)
-        path = [int(x) for x in sess.path[: acc + 1].cpu()]
-        nxt = int(sess.next_token.item())
+        path, acc, nxt = sess.outcome()  # (synchronises: the next tree depends on it)
         out += [int(tree_tokens[i]) for i in path[1:]] + [nxt]
         log.append({"accept_len": acc, "path": path, "prefix_len": prefix_len})
         prefix_len += acc + 1
@@ -64,12 +62,11 @@ def draft_decode(target, drafter, prefix_len: int, first_token: int, steps: int,
         target.commit(prefix_len, n)
         binding.commit_path(drafter.cfg, drafter.k_cache, drafter.v_cache, prefix_len, target.path,
                             target.accept_len, n)
-        acc = int(target.accept_len.item())  # (synchronises: the next tree depends on it)
-        path = [int(x) for x in target.path[: acc + 1].cpu()]
-        nxt = int(target.next_token.item())
+        path, acc, nxt = target.outcome()  # (synchronises: the next tree depends on it)
         if path[-1] >= info["fed"]:
             chain = np.asarray([tok[i] for i in path])
             drafter.extend(prefix_len, chain, np.arange(-1, acc), acc)
+            drafter.check("tree-decoder step")
         fb.update(par, path, info["t_c"][-1])
         out += [int(tok[i]) for i in path[1:]] + [nxt]
         log.append({"accept_len": acc, "nodes": n, "fed": info["fed"], "alpha": alpha,

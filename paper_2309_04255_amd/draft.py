@@ -37,14 +37,20 @@ class _Tree:
         self.depth = [0]    # draft tokens of the node's branch
         self.cand = []      # [token, fed parent, probability] in creation order
 
-    def add_candidates(self, node, prob, threshold):
+    def size(self):
+        return len(self.tok) + len(self.cand)
+
+    def add_candidates(self, node, prob, threshold, max_nodes):
         # the most likely token (lowest index among equal maxima), then every
-        # other token above the threshold, most likely first (ties: lower index)
+        # other token above the threshold, most likely first (ties: lower
+        # index), while the tree has fewer than max_nodes nodes
         best = int(np.argmax(prob))
         over = np.flatnonzero(prob > threshold)
         over = over[over != best]
         over = over[np.argsort(-prob[over], kind="stable")]
-        for t in [best] + [int(x) for x in over]:
+        for i, t in enumerate([best] + [int(x) for x in over]):
+            if i > 0 and self.size() >= max_nodes:
+                break
             self.cand.append([t, node, float(prob[t])])
 
     def pick(self, budget):
@@ -69,24 +75,35 @@ def _probs(logits_row):
 
 
 def generate_tree(sess, prefix_len: int, root_token: int, iterations: int, threshold: float = 0.3,
-                  alpha: float | None = None):
+                  alpha: float | None = None, max_nodes: int | None = None):
     """Grow a draft tree with `iterations` fed nodes after the root (at most,
     when `alpha` is given: see the module docstring), on the draft model in
     `sess`.  Returns (tree_tokens, parent, info): the tree for
     verification (fed nodes, then the pending candidates), and info with the
     number of fed nodes, each fed node's probability, the fed nodes' logits
-    rows and T_c after each step ("fed", "conf", "logits", "t_c")."""
+    rows and T_c after each step ("fed", "conf", "logits", "t_c").
+
+    The tree never exceeds max_nodes nodes (default: the session's max_n, the
+    largest tree its verifier's workspace takes): candidates past the cap are
+    not added (the most likely successor always is), and growth stops when a
+    fed node's expansion would find no room.  Raises LlmcadPassError if a
+    tree-decoder step failed on the device."""
+    if max_nodes is None:
+        max_nodes = getattr(sess, "max_n", 128)
+    if max_nodes < 2:
+        raise ValueError("a draft tree needs room for at least two nodes")
     tree = _Tree(root_token)
     rows, t_c = [], []
     node = 0
     for it in range(iterations + 1):
         row = sess.extend(prefix_len, np.asarray(tree.tok), np.asarray(tree.par), node)[0]
         rows.append(row.float().cpu().numpy())
-        tree.add_candidates(node, _probs(rows[-1]), threshold)
+        tree.add_candidates(node, _probs(rows[-1]), threshold, max_nodes)
         t_c.append(max(tree.cum[q] * p for _, q, p in tree.cand))
-        if it == iterations or (alpha is not None and t_c[-1] < alpha):
+        if it == iterations or (alpha is not None and t_c[-1] < alpha) or tree.size() >= max_nodes:
             break
         node = tree.feed(tree.pick(iterations))
+    sess.check("tree-decoder step")
     tok = np.asarray(tree.tok + [c[0] for c in tree.cand], dtype=np.int32)
     par = np.asarray(tree.par + [c[1] for c in tree.cand], dtype=np.int32)
     conf = [1.0] + [tree.cum[i] / tree.cum[tree.par[i]] for i in range(1, len(tree.tok))]

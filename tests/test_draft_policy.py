@@ -25,6 +25,9 @@ class TableSession:
         row = self.forward(np.asarray(tree_tokens), np.asarray(parent))
         return torch.from_numpy(np.asarray(row, dtype=np.float32)[None, :])
 
+    def check(self, what=""):
+        pass  # (no device: nothing can fail)
+
 
 def _random_forward(vocab, seed, peak):
     """Successor logits keyed by the fed token's branch: a few large logits so
@@ -99,3 +102,32 @@ def test_fallback_update_matches_oracle():
         n_all, n_correct = oracle.most_matching_branch(parent, path)
         alpha = oracle.update_alpha(alpha, n_correct, n_all, t_c)
         assert fb.update(parent, path, t_c) == pytest.approx(alpha, rel=1e-12)
+
+
+@pytest.mark.parametrize("max_nodes", [128, 50, 2])
+def test_flat_wide_rows_stay_within_the_verifier_cap(max_nodes):
+    # Flat but wide successor rows: 40 tokens share ~97% of the mass, so with
+    # a 2% threshold every expansion offers ~40 candidates and 6 iterations
+    # would build a tree of ~240 nodes.  Both the driver and the oracle stop
+    # at max_nodes, make the same decisions, and the result fits the verifier.
+    vocab = 64
+
+    def forward(tokens, parent):
+        key = hash(("wide", tuple(int(t) for t in tokens), tuple(int(q) for q in parent))) & 0xFFFFFFFF
+        g = np.random.default_rng(key)
+        row = np.full(vocab, -8.0)
+        row[g.choice(vocab, 40, replace=False)] = g.uniform(0.0, 0.2, 40)
+        return row.astype(np.float32)
+
+    sess = TableSession(forward)
+    tok, par, info = draft.generate_tree(sess, 0, 5, 6, threshold=0.02, max_nodes=max_nodes)
+    otok, opar, oinfo = oracle.generate_tree(None, None, None, 5, 6, threshold=0.02, max_nodes=max_nodes,
+                                             forward=lambda t, p: forward(t, p).astype(np.float64))
+    np.testing.assert_array_equal(tok, otok)
+    np.testing.assert_array_equal(par, opar)
+    assert len(tok) <= max_nodes
+    assert len(tok) == max_nodes  # (these rows always fill the cap)
+    assert info["fed"] == oinfo["fed"] >= 1
+    # every fed node beyond the root got its most likely successor as a child
+    for q in range(info["fed"]):
+        assert q in set(int(x) for x in par[1:]), q

@@ -90,8 +90,10 @@ def test_commit_moves_path_rows(model):
     torch.cuda.synchronize()
     acc = int(s.accept_len.item())
     path = [int(x) for x in s.path[: acc + 1].cpu()]
-    if np.all(m.gaps[:2] > parity.GAP):
-        assert acc == 2 and path == [0, 2, 6], path  # planted along root -> 2 -> 6 -> 14
+    # (the fixture's seed gives the first greedy steps top-2 gaps above 1e-2 on
+    # both models, so the planted acceptance is always asserted)
+    assert np.all(m.gaps[:2] > parity.GAP), m.gaps[:2]
+    assert acc == 2 and path == [0, 2, 6], path  # planted along root -> 2 -> 6 -> 14
     for k in range(n):
         src = path[k] if k <= acc else k
         assert torch.equal(s.k_cache[:, :, P + k], k0[:, :, P + src]), k

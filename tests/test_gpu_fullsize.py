@@ -1,23 +1,32 @@
 """GPU parity at the workloads' full sizes, in the launch configuration the
 bench times (all workgroups, default key splits).
 
-A whole oracle pass at these sizes (7B to 30B, 32 to 60 layers) takes too long
-on the host, so the comparison is layer-sampled.  The pass keeps every version
-of its residual stream (workspace region 7: the input of every layer, the
-stream after its attention block, and after the layer).  For a few sampled
-layers the oracle recomputes the layer from the GPU's own input version and the
-GPU's own prefix K/V (written by its prefill), and the test compares what each
-of the layer's two blocks adds to the stream, and the tree's K/V cache slots.  The LM head is recomputed from
-the GPU's last version and compared over all n x V logits; the argmax and the
-accept walk are checked as in the small-model tests.  The embedding rows are
-compared exactly.  At the bench's workload the rollback after a pass is
-checked too (bit-exact row moves).
+End to end: for every full-size workload (7B with P = 512, n = 31, the bench's
+workload; 7B with P = 2048, n = 41; 13B with P = 1024, n = 41; 30B with
+P = 1024, n = 1, 8, 32, 128) the oracle runs the whole masked pass over all L
+layers from the nodes' embedding rows -- its own residual stream, never the
+GPU's -- and its logits are compared with the GPU's over all n x V entries,
+then the argmax and the accept walk (§3.2: one pass gives every node the
+result of examining its branch sequentially).  The only GPU-made inputs of
+that chain are the prefix keys/values, read from the GPU cache: the GPU
+prefill wrote them, and prefill is an entry point of its own (its logits are
+checked against the oracle's causal forward on the small models).
+
+Per layer: the pass keeps every version of its residual stream (workspace
+region 7).  At every layer of the bench's workload, and at the first and
+last layer of the others, the oracle also recomputes the layer from the GPU's
+own input version, and the test compares what each of the layer's two blocks
+adds to the stream and the tree's K/V cache slots: a fault inside one layer
+shows there even when the end-to-end logits stay inside their bar.
+
+Weights: the seeded generator runs in torch on the GPU (its values equal the
+CPU run's bit for bit, which test_gpu_verify checks); each layer is widened
+to float64 on the GPU (exact) and copied into reused pinned host buffers, one
+layer at a time, so the float64 oracle runs the 30B shape without holding it.
 
 Bars: logits as everywhere (max abs 2e-2, relative L2 1e-2); a block's
 contribution or a K/V slice: max |gpu - oracle| <= 2e-2 max |oracle| and
-relative L2 <= 1e-2, the logits bar taken relative to the tensor's scale (both
-sides accumulate in fp32 or better; the difference comes from the bf16
-rounding points of the layer's products, each ~2^-9 relative).
+relative L2 <= 1e-2 (the logits bar taken relative to the tensor's scale).
 """
 
 import gc
@@ -30,18 +39,18 @@ import torch
 import oracle
 import workloads
 from tests import parity
-from tests.util import oracle_config, to_np
+from tests.util import oracle_config
 
 pytestmark = pytest.mark.gpu
 
-# (workload, sampled layers): the bench's workload with three layers, the
-# other parity workloads with their first and last layer
+# (workload, layers recomputed from the GPU's own input stream; None = all)
 CASES = [
-    ("llama7b_p512_n31", (0, 15, 31)),
+    ("llama7b_p512_n31", None),
     ("llama7b_p2048_n41", (0, 31)),
     ("llama13b_p1024_n41", (0, 39)),
     ("llama30b_p1024_n1", (0, 59)),
-    ("llama30b_p1024_n32", (59,)),
+    ("llama30b_p1024_n8", (0, 59)),
+    ("llama30b_p1024_n32", (0, 59)),
     ("llama30b_p1024_n128", (0, 59)),
 ]
 _MODEL = {}
@@ -51,10 +60,40 @@ def _log(msg):
     print(f"[fullsize {time.strftime('%H:%M:%S')}] {msg}", flush=True)
 
 
+class HostLayers:
+    """One layer of the GPU-generated weights at a time as float64 NumPy
+    arrays, in pinned host buffers reused from layer to layer."""
+
+    def __init__(self, gen):
+        self.gen = gen
+        self.l = None
+        self.bufs = {}
+        self.arrays = {}
+
+    def _host(self, name, t):
+        t = t.double()
+        buf = self.bufs.get(name)
+        if buf is None or buf.shape != t.shape:
+            buf = torch.empty(t.shape, dtype=torch.float64, pin_memory=True)
+            self.bufs[name] = buf
+        buf.copy_(t)
+        return buf.numpy()
+
+    def __call__(self, l):
+        if self.l != l:
+            self.arrays = {k: self._host(k, v) for k, v in self.gen.layer(l).items()}
+            self.l = l
+        return self.arrays
+
+
+def _np64(t):
+    return t.double().cpu().numpy()
+
+
 def _model(name):
     """One model resident at a time: packed weights on the GPU, a session whose
-    cache holds the largest prefix of the model's workloads, the generator, and
-    the oracle's weights (LM head; sampled layers as they are first used)."""
+    cache holds the largest prefix of the model's workloads, the generator and
+    the oracle's weights (globals resident, layers one at a time)."""
     if name in _MODEL:
         return _MODEL[name]
     _MODEL.clear()
@@ -70,21 +109,13 @@ def _model(name):
     _log(f"{name}: packing weights on the GPU")
     sess = binding.Session(shape, capacity=cap, max_n=128)
     binding.workspace_init(sess.cfg, 128, sess.workspace)
-    # The oracle's weights come from the same seeded generator run by torch on
-    # the GPU (its values equal the CPU run's, which another test checks):
-    # generating a 30B layer on the host takes tens of seconds.
     gen = workloads.make_weights(shape, "cuda")
     sess.load_weights(gen)
     torch.cuda.synchronize()
-    _log(f"{name}: oracle LM head")
-    ow = oracle.OracleWeights(oracle_config(shape), np.zeros((1, shape.d_model)), to_np(gen.final_norm()),
-                              to_np(gen.lm_head()), lambda l: {k: to_np(v) for k, v in gen.layer(l).items()})
+    ow = oracle.OracleWeights(oracle_config(shape), np.zeros((1, shape.d_model)), _np64(gen.final_norm()),
+                              _np64(gen.lm_head()), HostLayers(gen), cache=False)
     _MODEL[name] = (shape, sess, gen, ow, binding)
     return _MODEL[name]
-
-
-def gen_device(gen):
-    return gen.final_norm().device
 
 
 def _check_tensor(gpu, ref, what):
@@ -124,9 +155,7 @@ def test_full_size_rollback():
     K, leaf = 4, n - 1
     ptok = workloads.draft_tree(parent, int(tok[0]), cont, K, leaf, shape.vocab, seed=1)
     sess.verify_tree(P, ptok, parent, want_logits=False)
-    torch.cuda.synchronize()
-    acc = int(sess.accept_len.item())
-    path = [int(x) for x in sess.path[: acc + 1].cpu()]
+    path, acc, _ = sess.outcome()
     sure = 0
     while sure < K and gaps[sure] > 0.2:
         sure += 1
@@ -143,11 +172,11 @@ def test_full_size_rollback():
     _log(f"rollback: path {path}, gaps {np.round(gaps, 3).tolist()}")
 
 
-@pytest.mark.parametrize("wl_name,layers", CASES, ids=[c[0] for c in CASES])
-def test_full_size_layer_sampled(wl_name, layers):
+@pytest.mark.parametrize("wl_name,isolated", CASES, ids=[c[0] for c in CASES])
+def test_full_size_end_to_end(wl_name, isolated):
     wl = workloads.get_workload(wl_name)
     shape, sess, gen, ow, binding = _model(wl.model)
-    P, L, d, H, Dh = wl.prefix_len, shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim
+    P, L, d = wl.prefix_len, shape.n_layers, shape.d_model
     parent, tok = workloads.make_tree(wl.tree, shape.vocab, wl.seed)
     n = len(parent)
     _log(f"{wl_name}: prefill of {P} tokens, then the verification pass (n={n})")
@@ -162,31 +191,44 @@ def test_full_size_layer_sampled(wl_name, layers):
     amax = sess.workspace[off4:off4 + 4 * n].view(torch.int32).cpu().numpy()
     torch.cuda.synchronize()
 
-    # embedding rows: exact
-    emb = to_np(gen.tok_embed()[torch.as_tensor(np.asarray(tok, dtype=np.int64), device=gen_device(gen))])
-    np.testing.assert_array_equal(to_np(xs[0]), emb)
+    # the nodes' embedding rows: the oracle's first stream, and exact on the GPU
+    x = _np64(gen.tok_embed()[torch.as_tensor(np.asarray(tok, dtype=np.int64), device=xs.device)])
+    np.testing.assert_array_equal(_np64(xs[0]), x)
 
-    for l in layers:
-        t0 = time.time()
-        pk = sess.k_cache[l, :, :P].float().cpu().numpy().astype(np.float64).transpose(1, 0, 2)
-        pv = sess.v_cache[l, :, :P].float().cpu().numpy().astype(np.float64).transpose(1, 0, 2)
-        x_in = to_np(xs[2 * l])
-        g_mid, g_out = to_np(xs[2 * l + 1]), to_np(xs[2 * l + 2])
-        x_mid, x_out, k, v = oracle.tree_layer(ow, l, x_in, pk, pv, parent)
-        # each block's contribution to the stream (the stream itself is
-        # dominated by the input, which both sides share)
-        a1 = _check_tensor(g_mid - x_in, x_mid - x_in, f"{wl_name} layer {l} attention block")
-        a2 = _check_tensor(g_out - g_mid, x_out - x_mid, f"{wl_name} layer {l} feed-forward block")
-        gk = sess.k_cache[l, :, P:P + n].float().cpu().numpy().transpose(1, 0, 2)
-        gv = sess.v_cache[l, :, P:P + n].float().cpu().numpy().transpose(1, 0, 2)
-        a3 = _check_tensor(gk, k, f"{wl_name} layer {l} tree K")
-        a4 = _check_tensor(gv, v, f"{wl_name} layer {l} tree V")
-        _log(f"{wl_name} layer {l}: rel max/L2 mid {a1[0]:.1e}/{a1[1]:.1e} out {a2[0]:.1e}/{a2[1]:.1e} "
-             f"K {a3[0]:.1e} V {a4[0]:.1e} ({time.time() - t0:.1f} s)")
+    layers = range(L) if isolated is None else isolated
+    t_start = time.time()
+    for l in range(L):
+        pk = _np64(sess.k_cache[l, :, :P]).transpose(1, 0, 2)
+        pv = _np64(sess.v_cache[l, :, :P]).transpose(1, 0, 2)
+        # the oracle's own chain: layer l from its own stream
+        _, x, _, _ = oracle.tree_layer(ow, l, x, pk, pv, parent)
+        if l in layers:
+            # layer l from the GPU's own input version: each block's
+            # contribution (the stream itself is dominated by the input, which
+            # both sides share) and the tree's K/V slots
+            x_in = _np64(xs[2 * l])
+            g_mid, g_out = _np64(xs[2 * l + 1]), _np64(xs[2 * l + 2])
+            x_mid, x_out, k, v = oracle.tree_layer(ow, l, x_in, pk, pv, parent)
+            a1 = _check_tensor(g_mid - x_in, x_mid - x_in, f"{wl_name} layer {l} attention block")
+            a2 = _check_tensor(g_out - g_mid, x_out - x_mid, f"{wl_name} layer {l} feed-forward block")
+            a3 = _check_tensor(_np64(sess.k_cache[l, :, P:P + n]).transpose(1, 0, 2), k,
+                               f"{wl_name} layer {l} tree K")
+            a4 = _check_tensor(_np64(sess.v_cache[l, :, P:P + n]).transpose(1, 0, 2), v,
+                               f"{wl_name} layer {l} tree V")
+            if l % 8 == 0 or l == L - 1 or isolated is not None:
+                _log(f"{wl_name} layer {l}: rel max/L2 attention {a1[0]:.1e}/{a1[1]:.1e} "
+                     f"ffn {a2[0]:.1e}/{a2[1]:.1e} K {a3[0]:.1e} V {a4[0]:.1e}")
+        if l % 8 == 7 or l == L - 1:
+            g = _np64(xs[2 * l + 2])
+            drift = np.linalg.norm(g - x) / np.linalg.norm(x)
+            _log(f"{wl_name}: {l + 1}/{L} layers ({time.time() - t_start:.0f} s); "
+                 f"GPU stream vs the oracle's own: relative L2 {drift:.2e}")
 
-    ref = oracle.logits_from_stream(ow, to_np(xs[2 * L]))
-    err, rel = parity.check_logits(logits, ref, f"{wl_name} logits")
+    ref = oracle.logits_from_stream(ow, x)
+    err, rel = parity.check_logits(logits, ref, f"{wl_name} logits (end to end)")
     np.testing.assert_array_equal(amax, np.argmax(logits, axis=1))
-    parity.check_argmax(amax, ref, wl_name)
-    parity.check_walk(parent, tok, amax, path, acc, nxt, ref, wl_name)
-    _log(f"{wl_name}: logits max abs {err:.2e} rel {rel:.2e}; path {list(path)} next {nxt}")
+    sure = parity.check_argmax(amax, ref, wl_name)
+    confident = parity.check_walk(parent, tok, amax, path, acc, nxt, ref, wl_name)
+    _log(f"{wl_name}: end-to-end logits max abs {err:.2e} rel {rel:.2e}; argmax equal at {sure}/{n} "
+         f"confident rows; walk {'equal' if confident else 'valid (a read node is within 1e-2)'}: "
+         f"path {list(path)} next {nxt}")
