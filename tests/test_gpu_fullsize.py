@@ -4,13 +4,17 @@ bench times (all workgroups, default key splits).
 End to end: for every full-size workload (7B with P = 512, n = 31, the bench's
 workload; 7B with P = 2048, n = 41; 13B with P = 1024, n = 41; 30B with
 P = 1024, n = 1, 8, 32, 128) the oracle runs the whole masked pass over all L
-layers from the nodes' embedding rows -- its own residual stream, never the
-GPU's -- and its logits are compared with the GPU's over all n x V entries,
-then the argmax and the accept walk (§3.2: one pass gives every node the
-result of examining its branch sequentially).  The only GPU-made inputs of
-that chain are the prefix keys/values, read from the GPU cache: the GPU
-prefill wrote them, and prefill is an entry point of its own (its logits are
-checked against the oracle's causal forward on the small models).
+layers from the nodes' embedding rows -- its own residual streams, never the
+GPU's -- once with the bf16 rounding points and once exactly (float64, no
+activation rounding), and the GPU's logits are compared over all n x V
+entries with the exact forward, under a bar derived from the oracle's own
+bf16 error (see E2E_FACTOR), then the argmax and the accept walk (§3.2: one
+pass gives every node the result of examining its branch sequentially).  The
+only GPU-made inputs of those chains are the prefix keys/values, read from
+the GPU cache: the GPU prefill wrote them, and prefill is an entry point of
+its own (its logits are checked against the oracle's causal forward on the
+small models).  The final norm and LM head are checked at the stated bar
+over all n x V logits, from the GPU's own final stream.
 
 Per layer: the pass keeps every version of its residual stream (workspace
 region 7).  At every layer of the bench's workload, and at the first and
@@ -43,15 +47,21 @@ from tests.util import oracle_config
 
 pytestmark = pytest.mark.gpu
 
-# (workload, layers recomputed from the GPU's own input stream; None = all)
+# (workload, layers recomputed from the GPU's own input stream (None = all),
+#  nodes the oracle's end-to-end chains cover (None = all)).  A node's result
+#  depends only on its ancestors, and parent[i] < i, so the first m nodes of a
+#  tree form a tree of their own whose results are the big tree's rows [0, m):
+#  at 30B with n = 128 the two float64 chains cover the first 32 nodes (the
+#  GPU pass still runs all 128; its other rows are checked per layer and at
+#  the LM head).
 CASES = [
-    ("llama7b_p512_n31", None),
-    ("llama7b_p2048_n41", (0, 31)),
-    ("llama13b_p1024_n41", (0, 39)),
-    ("llama30b_p1024_n1", (0, 59)),
-    ("llama30b_p1024_n8", (0, 59)),
-    ("llama30b_p1024_n32", (0, 59)),
-    ("llama30b_p1024_n128", (0, 59)),
+    ("llama7b_p512_n31", None, None),
+    ("llama7b_p2048_n41", (0, 31), None),
+    ("llama13b_p1024_n41", (0, 39), None),
+    ("llama30b_p1024_n1", (0, 59), None),
+    ("llama30b_p1024_n8", (0, 59), None),
+    ("llama30b_p1024_n32", (0, 59), None),
+    ("llama30b_p1024_n128", (0, 59), 32),
 ]
 _MODEL = {}
 
@@ -104,7 +114,7 @@ def _model(name):
     from paper_2309_04255_amd import binding
 
     shape = workloads.MODELS[name]
-    cap = max(workloads.get_workload(w).prefix_len for w, _ in CASES
+    cap = max(workloads.get_workload(w).prefix_len for w, _, _ in CASES
               if workloads.get_workload(w).model == name) + 128
     _log(f"{name}: packing weights on the GPU")
     sess = binding.Session(shape, capacity=cap, max_n=128)
@@ -172,8 +182,29 @@ def test_full_size_rollback():
     _log(f"rollback: path {path}, gaps {np.round(gaps, 3).tolist()}")
 
 
-@pytest.mark.parametrize("wl_name,isolated", CASES, ids=[c[0] for c in CASES])
-def test_full_size_end_to_end(wl_name, isolated):
+# End to end, a bf16 pass cannot be held to the per-pass logits bar: every
+# bf16 rounding of an activation (norm outputs, q/k/v, attention output,
+# SwiGLU product) moves the value by up to half an ulp (2^-9 relative), and
+# over 32 to 60 layers these perturbations add up in the residual stream like
+# a random walk (relative drift ~ sqrt(L)).  Measured at the 7B workload:
+# the oracle's own bf16 mode and the same oracle rounding the norm output at
+# another point (bf16(x g), then the row's rstd after the product) differ by
+# 0.25 max-abs in the logits, while each layer alone agrees within 5e-3.  So
+# the end-to-end comparison is against the exact forward (the oracle without
+# any activation rounding, float64 on the bf16 weights and the bf16 prefix
+# K/V), and the bar is derived from the oracle itself: the GPU's distance to
+# the exact forward may exceed the oracle's own bf16 distance by at most half
+# (E2E_FACTOR).  The stated bar applies where it can: to every layer on its
+# own, and to the final norm + LM head over all n x V logits.
+E2E_FACTOR = 1.5
+
+
+def _dist(a, b):
+    return float(np.abs(a - b).max()), float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+
+@pytest.mark.parametrize("wl_name,isolated,chain_nodes", CASES, ids=[c[0] for c in CASES])
+def test_full_size_end_to_end(wl_name, isolated, chain_nodes):
     wl = workloads.get_workload(wl_name)
     shape, sess, gen, ow, binding = _model(wl.model)
     P, L, d = wl.prefix_len, shape.n_layers, shape.d_model
@@ -190,18 +221,23 @@ def test_full_size_end_to_end(wl_name, isolated):
     off4, _ = binding.workspace_region(sess.cfg, n, 4)
     amax = sess.workspace[off4:off4 + 4 * n].view(torch.int32).cpu().numpy()
     torch.cuda.synchronize()
+    np.testing.assert_array_equal(amax, np.argmax(logits, axis=1))
 
     # the nodes' embedding rows: the oracle's first stream, and exact on the GPU
-    x = _np64(gen.tok_embed()[torch.as_tensor(np.asarray(tok, dtype=np.int64), device=xs.device)])
-    np.testing.assert_array_equal(_np64(xs[0]), x)
+    emb = _np64(gen.tok_embed()[torch.as_tensor(np.asarray(tok, dtype=np.int64), device=xs.device)])
+    np.testing.assert_array_equal(_np64(xs[0]), emb)
 
     layers = range(L) if isolated is None else isolated
+    m = n if chain_nodes is None else chain_nodes
+    x_ref, x_exact = emb[:m].copy(), emb[:m].copy()
     t_start = time.time()
     for l in range(L):
         pk = _np64(sess.k_cache[l, :, :P]).transpose(1, 0, 2)
         pv = _np64(sess.v_cache[l, :, :P]).transpose(1, 0, 2)
-        # the oracle's own chain: layer l from its own stream
-        _, x, _, _ = oracle.tree_layer(ow, l, x, pk, pv, parent)
+        # the oracle's own chains from the embedding: with the bf16 rounding
+        # points, and exact
+        _, x_ref, _, _ = oracle.tree_layer(ow, l, x_ref, pk, pv, parent[:m], rounding=True)
+        _, x_exact, _, _ = oracle.tree_layer(ow, l, x_exact, pk, pv, parent[:m], rounding=False)
         if l in layers:
             # layer l from the GPU's own input version: each block's
             # contribution (the stream itself is dominated by the input, which
@@ -219,16 +255,37 @@ def test_full_size_end_to_end(wl_name, isolated):
                 _log(f"{wl_name} layer {l}: rel max/L2 attention {a1[0]:.1e}/{a1[1]:.1e} "
                      f"ffn {a2[0]:.1e}/{a2[1]:.1e} K {a3[0]:.1e} V {a4[0]:.1e}")
         if l % 8 == 7 or l == L - 1:
-            g = _np64(xs[2 * l + 2])
-            drift = np.linalg.norm(g - x) / np.linalg.norm(x)
-            _log(f"{wl_name}: {l + 1}/{L} layers ({time.time() - t_start:.0f} s); "
-                 f"GPU stream vs the oracle's own: relative L2 {drift:.2e}")
+            _log(f"{wl_name}: {l + 1}/{L} layers ({time.time() - t_start:.0f} s); relative L2 to the exact "
+                 f"stream: GPU {_dist(_np64(xs[2 * l + 2])[:m], x_exact)[1]:.2e}, oracle bf16 "
+                 f"{_dist(x_ref, x_exact)[1]:.2e}")
 
-    ref = oracle.logits_from_stream(ow, x)
-    err, rel = parity.check_logits(logits, ref, f"{wl_name} logits (end to end)")
-    np.testing.assert_array_equal(amax, np.argmax(logits, axis=1))
-    sure = parity.check_argmax(amax, ref, wl_name)
-    confident = parity.check_walk(parent, tok, amax, path, acc, nxt, ref, wl_name)
-    _log(f"{wl_name}: end-to-end logits max abs {err:.2e} rel {rel:.2e}; argmax equal at {sure}/{n} "
-         f"confident rows; walk {'equal' if confident else 'valid (a read node is within 1e-2)'}: "
-         f"path {list(path)} next {nxt}")
+    # final norm + LM head at the stated bar, from the GPU's own final stream
+    head = oracle.logits_from_stream(ow, _np64(xs[2 * L]))
+    e_head = parity.check_logits(logits, head, f"{wl_name} LM head from the GPU's final stream")
+    # end to end against the exact forward, bar derived from the oracle's own bf16 error
+    exact = oracle.logits_from_stream(ow, x_exact, rounding=False)
+    ref = oracle.logits_from_stream(ow, x_ref)
+    e_gpu, e_ref = _dist(logits[:m], exact), _dist(ref, exact)
+    _log(f"{wl_name}: end to end vs the exact forward: GPU max abs {e_gpu[0]:.3e} rel L2 {e_gpu[1]:.3e}; "
+         f"oracle bf16 max abs {e_ref[0]:.3e} rel L2 {e_ref[1]:.3e}; LM head alone max abs {e_head[0]:.2e}")
+    assert e_gpu[0] <= E2E_FACTOR * e_ref[0], (e_gpu, e_ref)
+    assert e_gpu[1] <= E2E_FACTOR * e_ref[1], (e_gpu, e_ref)
+    # argmax and walk: exact wherever the exact forward's top-2 gap exceeds
+    # twice the GPU's largest end-to-end deviation (there no deviation of that
+    # size can reorder the top two)
+    gap = parity.top2_gap(exact)
+    margin = 2.0 * e_gpu[0]
+    sure = gap > margin
+    bad = np.nonzero(sure & (amax[:m] != np.argmax(exact, axis=1)))[0]
+    assert len(bad) == 0, f"{wl_name}: argmax differs from the exact forward at rows {bad.tolist()}"
+    # the walk: bit-exact on the GPU's own argmax; equal to the exact
+    # forward's walk when every node that walk reads is confident
+    wpath, wnext, _ = oracle.accept_walk(parent, tok, amax)
+    assert list(path) == wpath and nxt == wnext, (path, wpath, nxt, wnext)
+    if m == n:
+        reach = parity.reachable(parent, tok, np.argmax(exact, axis=1))
+        if np.all(sure[reach]):
+            epath, enext, _ = oracle.accept_walk(parent, tok, np.argmax(exact, axis=1))
+            assert list(path) == epath and nxt == enext, (path, epath, nxt, enext)
+    _log(f"{wl_name}: argmax equal to the exact forward's at all {int(sure.sum())}/{m} rows with gap > "
+         f"{margin:.3f}; path {list(path)} next {nxt}")
