@@ -147,6 +147,38 @@ int llmcad_verify_tree(const llmcad_config* cfg, const void* packed, void* k_cac
                        int32_t* accept_len, int32_t* next_token, void* workspace,
                        size_t workspace_bytes, void* stream);
 
+/* Size of the scratch buffer behind llmcad_verify_tree_noalloc: 96 MiB of
+ * device memory per device, enough for any pass whose workspace fits
+ * (llmcad_workspace_bytes(cfg, n) <= this; e.g. the LLaMA-7B shape up to
+ * n = 32, the LLaMA-13B shape up to n = 16). */
+#define LLMCAD_SCRATCH_BYTES (96u << 20)
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): one
+ * verification pass exactly as llmcad_verify_tree -- same arguments, checks,
+ * kernels and outputs -- with the workspace replaced by a scratch buffer the
+ * library holds itself, LLMCAD_SCRATCH_BYTES of device memory on each device
+ * it runs on, from the first call on that device until the process ends.
+ *
+ * The call allocates and frees nothing.  It enqueues on `stream` a clear of
+ * the scratch's synchronisation state (the scratch keeps the previous call's
+ * contents), the pass, and, when status is not NULL, a copy of the pass's
+ * device status to status (device int32 [1]: 0 = ok, 1 = a wait of the pass
+ * ran out of its bounded spin and the outputs are invalid; see region 5 of
+ * llmcad_workspace_region).  Every call on one device uses that device's one
+ * scratch: calls that overlap on a device (different streams or threads)
+ * race and must be serialised by the caller.
+ *
+ * Errors (checked on the host, nothing enqueued): as llmcad_verify_tree, and
+ * LLMCAD_EWORKSPACE when the pass needs more workspace than the scratch holds;
+ * LLMCAD_EHIP when the scratch's device address cannot be obtained.
+ */
+int llmcad_verify_tree_noalloc(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                               int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens,
+                               const int32_t* parent, int32_t n, float* logits, int32_t* path,
+                               int32_t* accept_len, int32_t* next_token, int32_t* status, void* stream);
+
 /*
  * Prefill: runs tokens[0..n_tokens) (host array) as positions
  * [start_pos, start_pos + n_tokens) against cache slots [0, start_pos),

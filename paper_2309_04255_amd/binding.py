@@ -31,6 +31,7 @@ SYMBOLS = (
     "llmcad_workspace_bytes",
     "llmcad_workspace_init",
     "llmcad_verify_tree",
+    "llmcad_verify_tree_noalloc",
     "llmcad_prefill",
     "llmcad_commit_path",
     "llmcad_extend_tree",
@@ -101,6 +102,8 @@ def _load():
         "llmcad_workspace_init": (ctypes.c_int, [CFG, I32, P, SZ, P]),
         "llmcad_verify_tree": (ctypes.c_int, [CFG, P, P, P, I32, I32, I32P, I32P, I32, P, P, P, P,
                                               P, SZ, P]),
+        "llmcad_verify_tree_noalloc": (ctypes.c_int, [CFG, P, P, P, I32, I32, I32P, I32P, I32, P, P, P, P,
+                                                      P, P]),
         "llmcad_prefill": (ctypes.c_int, [CFG, P, P, P, I32, I32P, I32, I32, P, P, SZ, P]),
         "llmcad_commit_path": (ctypes.c_int, [CFG, P, P, I32, I32, P, P, I32, P]),
         "llmcad_extend_tree": (ctypes.c_int, [CFG, P, P, P, I32, I32, I32P, I32P, I32, I32, P, P, SZ, P]),
@@ -203,6 +206,29 @@ def verify_tree(cfg, packed, k_cache, v_cache, prefix_len: int, tree_tokens, par
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
     if raise_on_error:
         _check(rc, "llmcad_verify_tree")
+    return rc
+
+
+SCRATCH_BYTES = 96 << 20  # LLMCAD_SCRATCH_BYTES
+
+
+def verify_tree_noalloc(cfg, packed, k_cache, v_cache, prefix_len: int, tree_tokens, parent, logits, path,
+                        accept_len, next_token, status=None, stream=None, raise_on_error=True) -> int:
+    """Enqueue one verification pass on the library's own scratch buffer (no
+    workspace argument, no allocation); `status` (device int32 [1] or None)
+    receives the pass's device status."""
+    tok, tok_p = _i32(tree_tokens)
+    par, par_p = _i32(parent)
+    n = len(tok)
+    if len(par) != n:
+        raise ValueError("tree_tokens and parent differ in length")
+    cap = k_cache.shape[-2]
+    rc = _lib.llmcad_verify_tree_noalloc(
+        ctypes.byref(cfg), _ptr(packed), _ptr(k_cache), _ptr(v_cache), int(cap), int(prefix_len),
+        tok_p, par_p, int(n), _ptr(logits), _ptr(path), _ptr(accept_len), _ptr(next_token), _ptr(status),
+        _stream(stream))
+    if raise_on_error:
+        _check(rc, "llmcad_verify_tree_noalloc")
     return rc
 
 

@@ -14,6 +14,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "kernels.h"
 #include "layout.h"
 #include "llmcad.h"
@@ -222,6 +224,62 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   return LLMCAD_OK;
 }
 
+// The workspace of llmcad_verify_tree_noalloc: device memory the library
+// holds itself, one copy per device (each device that runs the entry point
+// holds it until the process ends).  In host code `scratch` names a host-side
+// stand-in, not the device array: its device address is looked up once per
+// device (scratch_base) and only that address is handed to the kernels.
+static __device__ __align__(256) char scratch[LLMCAD_SCRATCH_BYTES];
+
+// Device address of this device's `scratch` (null if the lookup failed; the
+// HIP status is kept for llmcad_status_string).
+char* scratch_base() {
+  static std::mutex mu;
+  static char* base[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= 64) {
+    g_last_error = e != hipSuccess ? e : hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (base[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr) {
+      g_last_error = e != hipSuccess ? e : hipErrorInvalidSymbol;
+      return nullptr;
+    }
+    base[dev] = (char*)p;
+  }
+  return base[dev];
+}
+
+// Host-side checks of a verification pass's arguments (llmcad_verify_tree's
+// contract), then the tree copied into the launch arguments.
+int check_verify_args(const llmcad_config* cfg, const void* packed, const void* k_cache, const void* v_cache,
+                      int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens, const int32_t* parent,
+                      int32_t n, const int32_t* path, const int32_t* accept_len, const int32_t* next_token,
+                      TreeArgs* tree) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!packed || !k_cache || !v_cache || !tree_tokens || !parent || !path || !accept_len || !next_token)
+    return LLMCAD_EARG;
+  if (n < 1 || n > kMaxNodes) return LLMCAD_ETREE;
+  if (parent[0] != -1) return LLMCAD_ETREE;
+  for (int i = 0; i < n; ++i) {
+    if (tree_tokens[i] < 0 || tree_tokens[i] >= cfg->vocab) return LLMCAD_ETREE;
+    if (i > 0 && (parent[i] < 0 || parent[i] >= i)) return LLMCAD_ETREE;
+  }
+  if (capacity < 1 || prefix_len < 0 || (long)prefix_len + n > capacity) return LLMCAD_ECAPACITY;
+  memset(tree, 0, sizeof(*tree));
+  for (int i = 0; i < n; ++i) {
+    tree->tok[i] = tree_tokens[i];
+    tree->parent[i] = parent[i];
+  }
+  return LLMCAD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -297,26 +355,13 @@ int llmcad_verify_tree(const llmcad_config* cfg, const void* packed, void* k_cac
                        const int32_t* parent, int32_t n, float* logits, int32_t* path,
                        int32_t* accept_len, int32_t* next_token, void* workspace,
                        size_t workspace_bytes, void* stream) {
-  int rc = check_cfg(cfg);
+  TreeArgs tree;
+  int rc = check_verify_args(cfg, packed, k_cache, v_cache, capacity, prefix_len, tree_tokens, parent, n, path,
+                             accept_len, next_token, &tree);
   if (rc != LLMCAD_OK) return rc;
-  if (!packed || !k_cache || !v_cache || !tree_tokens || !parent || !path || !accept_len ||
-      !next_token || !workspace)
-    return LLMCAD_EARG;
-  if (n < 1 || n > kMaxNodes) return LLMCAD_ETREE;
-  if (parent[0] != -1) return LLMCAD_ETREE;
-  for (int i = 0; i < n; ++i) {
-    if (tree_tokens[i] < 0 || tree_tokens[i] >= cfg->vocab) return LLMCAD_ETREE;
-    if (i > 0 && (parent[i] < 0 || parent[i] >= i)) return LLMCAD_ETREE;
-  }
-  if (capacity < 1 || prefix_len < 0 || (long)prefix_len + n > capacity) return LLMCAD_ECAPACITY;
+  if (!workspace) return LLMCAD_EARG;
   const Shape s(*cfg);
   if (workspace_bytes < WorkspaceLayout(s, n, pass_grid()).total) return LLMCAD_EWORKSPACE;
-  TreeArgs tree;
-  memset(&tree, 0, sizeof(tree));
-  for (int i = 0; i < n; ++i) {
-    tree.tok[i] = tree_tokens[i];
-    tree.parent[i] = parent[i];
-  }
   Pass a;
   a.cfg = cfg;
   a.packed = (const char*)packed;
@@ -333,6 +378,45 @@ int llmcad_verify_tree(const llmcad_config* cfg, const void* packed, void* k_cac
   a.ws = (char*)workspace;
   a.st = (hipStream_t)stream;
   return run_pass(a, tree);
+}
+
+int llmcad_verify_tree_noalloc(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                               int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens,
+                               const int32_t* parent, int32_t n, float* logits, int32_t* path,
+                               int32_t* accept_len, int32_t* next_token, int32_t* status, void* stream) {
+  TreeArgs tree;
+  int rc = check_verify_args(cfg, packed, k_cache, v_cache, capacity, prefix_len, tree_tokens, parent, n, path,
+                             accept_len, next_token, &tree);
+  if (rc != LLMCAD_OK) return rc;
+  const Shape s(*cfg);
+  const WorkspaceLayout W(s, n, pass_grid());
+  if (W.total > (size_t)LLMCAD_SCRATCH_BYTES) return LLMCAD_EWORKSPACE;
+  char* ws = scratch_base();
+  if (ws == nullptr) return LLMCAD_EHIP;
+  hipStream_t st = (hipStream_t)stream;
+  // The scratch keeps the previous call's contents: its synchronisation
+  // state (counters with the pass status, barrier counters, the zero line,
+  // which lie first and together) starts every call cleared.
+  HIP_TRY(hipMemsetAsync(ws, 0, W.zero + kZeroBytes, st));
+  Pass a;
+  a.cfg = cfg;
+  a.packed = (const char*)packed;
+  a.k_cache = (char*)k_cache;
+  a.v_cache = (char*)v_cache;
+  a.cap = capacity;
+  a.prefix_len = prefix_len;
+  a.n = n;
+  a.logits = logits;
+  a.row_lo = 0;
+  a.path = path;
+  a.accept_len = accept_len;
+  a.next_token = next_token;
+  a.ws = ws;
+  a.st = st;
+  rc = run_pass(a, tree);
+  if (rc != LLMCAD_OK) return rc;
+  if (status != nullptr) HIP_TRY(hipMemcpyAsync(status, ws + W.status(), 4, hipMemcpyDeviceToDevice, st));
+  return LLMCAD_OK;
 }
 
 int llmcad_extend_tree(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,

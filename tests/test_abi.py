@@ -119,6 +119,35 @@ def test_host_validation(binding):
     assert binding.status_string(binding.ETREE) == "invalid token tree"
 
 
+def _call_noalloc(binding, cfg, tok, par, prefix_len=10, cap=64, packed=16):
+    lib = binding.lib()
+    tok = np.ascontiguousarray(tok, dtype=np.int32)
+    par = np.ascontiguousarray(par, dtype=np.int32)
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    fake = ctypes.c_void_p(256)  # never dereferenced: every case below fails a host check
+    return lib.llmcad_verify_tree_noalloc(
+        ctypes.byref(cfg), ctypes.c_void_p(packed) if packed else None, fake, fake, cap, prefix_len,
+        tok.ctypes.data_as(I32P), par.ctypes.data_as(I32P), len(tok), fake, fake, fake, fake, None, None)
+
+
+def test_noalloc_host_validation(binding):
+    # the no-allocation entry point makes llmcad_verify_tree's host checks,
+    # and refuses a pass whose workspace exceeds its scratch, before any
+    # device call
+    cfg = binding.make_config(workloads.MODELS["tiny"])
+    V = cfg.vocab
+    assert _call_noalloc(binding, cfg, [1, 2], [0, 0]) == binding.ETREE
+    assert _call_noalloc(binding, cfg, [1, V], [-1, 0]) == binding.ETREE
+    assert _call_noalloc(binding, cfg, np.zeros(129), np.arange(-1, 128)) == binding.ETREE
+    assert _call_noalloc(binding, cfg, [1, 2], [-1, 0], prefix_len=63, cap=64) == binding.ECAPACITY
+    assert _call_noalloc(binding, cfg, [1, 2], [-1, 0], packed=0) == binding.EARG
+    big = binding.make_config(workloads.MODELS["llama30b"])
+    assert binding.workspace_bytes(big, 128) > binding.SCRATCH_BYTES
+    assert _call_noalloc(binding, big, np.zeros(128), np.arange(-1, 127), cap=4096) == binding.EWORKSPACE
+    b7 = binding.make_config(workloads.MODELS["llama7b"])
+    assert binding.workspace_bytes(b7, 32) <= binding.SCRATCH_BYTES < binding.workspace_bytes(b7, 33)
+
+
 def test_prefill_validation(binding):
     cfg = binding.make_config(workloads.MODELS["tiny"])
     lib = binding.lib()
