@@ -40,7 +40,11 @@
  *    consecutive).  The globals sit
  *    first, then layer 0, 1, ...; an image packed for L layers also serves a
  *    configuration with fewer layers.
- *  - KV cache: k_cache and v_cache are bf16 [L][H][capacity][Dh] each.  Slot p
+ *  - KV cache: k_cache is bf16 [L][H][capacity][Dh] and v_cache is bf16
+ *    [L][H][Dh][capacity] (V transposed per head: a slot is one entry of each
+ *    of the head's Dh rows, so that both operands of the attention's products
+ *    load from the cache in matrix-core fragment order).  capacity must be a
+ *    multiple of 64 (so that every V row starts on a 128-byte line).  Slot p
  *    holds position p of the accepted sequence for p < prefix_len.
  */
 #ifndef LLMCAD_H
@@ -58,7 +62,8 @@ extern "C" {
 #define LLMCAD_EARG (-1)       /* NULL pointer, bad config value, bad layer index   */
 #define LLMCAD_ETREE (-2)      /* n < 1 or n > max, parent[0] != -1, parent[i] not
                                   in [0, i), token outside [0, V)                    */
-#define LLMCAD_ECAPACITY (-3)  /* prefix_len < 0 or prefix_len + n > capacity       */
+#define LLMCAD_ECAPACITY (-3)  /* prefix_len < 0, prefix_len + n > capacity, or
+                                  capacity not a positive multiple of 64             */
 #define LLMCAD_ESHAPE (-4)     /* unsupported shape (see llmcad_check_config)       */
 #define LLMCAD_EHIP (-5)       /* a HIP launch or runtime call failed               */
 #define LLMCAD_EWORKSPACE (-6) /* workspace or packed image smaller than required   */

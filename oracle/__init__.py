@@ -22,6 +22,8 @@ Contents
             "Token tree generation", Eq. 1), with the fallback stop
   fallback.py  self-adaptive fallback: tree-cumulative confidence and the
             threshold update of Eq. 3 (§3.3)
+  quant.py  group-wise 4-bit weights (the INT4 targets of §4.1): the
+            dequantisation w = s (q - 8)
 
 Every function is pinned by tests/test_oracle_*.py against something other
 than itself: brute force, an independent library implementation
@@ -48,3 +50,4 @@ from .walk import accept_walk, branch_sequences, correct_sequences  # noqa: F401
 from .decode import commit_path, greedy_decode, speculative_decode  # noqa: F401
 from .draft import generate_tree  # noqa: F401
 from .fallback import DEFAULT_ALPHA, tree_confidence, update_alpha, most_matching_branch  # noqa: F401
+from .quant import dequantize, unpack_codes  # noqa: F401

@@ -305,11 +305,15 @@ class Session:
         self.shape = shape
         self.device = torch.device(device)
         self.max_n = int(max_n)
-        self.capacity = int(capacity)
+        self.capacity = (int(capacity) + 63) // 64 * 64  # (the library takes multiples of 64)
+        cap = self.capacity
         L, H, Dh = shape.n_layers, shape.n_heads, shape.head_dim
         self.packed = torch.empty(packed_bytes(self.cfg), dtype=torch.uint8, device=self.device)
-        self.k_cache = torch.zeros((L, H, capacity, Dh), dtype=torch.bfloat16, device=self.device)
-        self.v_cache = torch.zeros((L, H, capacity, Dh), dtype=torch.bfloat16, device=self.device)
+        # K [L][H][cap][Dh]; V transposed per head [L][H][Dh][cap].  v_rows is
+        # a [L][H][cap][Dh] view of the V cache (slot-major, like k_cache).
+        self.k_cache = torch.zeros((L, H, cap, Dh), dtype=torch.bfloat16, device=self.device)
+        self.v_cache = torch.zeros((L, H, Dh, cap), dtype=torch.bfloat16, device=self.device)
+        self.v_rows = self.v_cache.transpose(2, 3)
         self.workspace = torch.zeros(workspace_bytes(self.cfg, self.max_n), dtype=torch.uint8,
                                      device=self.device)
         self.logits = torch.empty((self.max_n, shape.vocab), dtype=torch.float32, device=self.device)

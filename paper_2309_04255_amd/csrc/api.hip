@@ -191,11 +191,15 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.q = (bf16*)(ws + W.qs);
   p.o = (bf16*)(ws + W.os);
   p.h = (bf16*)(ws + W.hs);
-  // Key splits per (head, row block) of the attention: four (LLMCAD_ATTN_SPLITS
-  // asks for 1 to 4), at most one per prefix chunk, 1 without a prefix.
-  int KS = env_int("LLMCAD_ATTN_SPLITS", 4);
+  // Key splits per (head, row block) of the attention: about four 32-key
+  // steps of the prefix per split (one per wave), at most four splits
+  // (LLMCAD_ATTN_SPLITS, diagnostics, asks for 1 to 4).  A workgroup pulls its
+  // keys and values at the rate one CU's memory path gives, so a head's keys
+  // are spread over several; the splits' merge costs a hand-off through memory.
+  const int prefix_steps = cdiv(a.prefix_len, 32);
+  int KS = env_int("LLMCAD_ATTN_SPLITS", cdiv(prefix_steps, 4));
   if (KS > kAttnMaxSplits) KS = kAttnMaxSplits;
-  if (KS > cdiv(a.prefix_len, kAttnChunk)) KS = cdiv(a.prefix_len, kAttnChunk);
+  if (KS > prefix_steps) KS = prefix_steps;
   if (KS < 1) KS = 1;
   p.attn_splits = KS;
   p.attn_o = (float*)(ws + W.attn_o);
@@ -218,6 +222,8 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   // once, so the pass ends with status 1 and every workgroup exits normally)
   if (env_int("LLMCAD_FAIL_WAITS", 0) == 1) p.spin_limit = -1;
   p.wl_cap = env_int("LLMCAD_WL_STAGES", 1 << 20);  // (diagnostics: a smaller pre-barrier copy)
+  // (diagnostics: LLMCAD_ATTN_PREFETCH=2 fetches every attention step after the barrier)
+  p.attn_prefetch = env_int("LLMCAD_ATTN_PREFETCH", 1) == 2 ? 0 : 1;
   p.trace = env_int("LLMCAD_TRACE", 0) ? (long long*)(ws + W.trace) : nullptr;
   TimedLaunch tl(LLMCAD_KERNEL_PASS, a.st);
   HIP_TRY(launch_pass(MB, p, tree, a.st));
@@ -271,7 +277,8 @@ int check_verify_args(const llmcad_config* cfg, const void* packed, const void* 
     if (tree_tokens[i] < 0 || tree_tokens[i] >= cfg->vocab) return LLMCAD_ETREE;
     if (i > 0 && (parent[i] < 0 || parent[i] >= i)) return LLMCAD_ETREE;
   }
-  if (capacity < 1 || prefix_len < 0 || (long)prefix_len + n > capacity) return LLMCAD_ECAPACITY;
+  if (capacity < 64 || capacity % 64 != 0 || prefix_len < 0 || (long)prefix_len + n > capacity)
+    return LLMCAD_ECAPACITY;
   memset(tree, 0, sizeof(*tree));
   for (int i = 0; i < n; ++i) {
     tree->tok[i] = tree_tokens[i];
@@ -432,7 +439,8 @@ int llmcad_extend_tree(const llmcad_config* cfg, const void* packed, void* k_cac
     if (tree_tokens[i] < 0 || tree_tokens[i] >= cfg->vocab) return LLMCAD_ETREE;
     if (i > 0 && (parent[i] < 0 || parent[i] >= i)) return LLMCAD_ETREE;
   }
-  if (capacity < 1 || prefix_len < 0 || (long)prefix_len + n > capacity) return LLMCAD_ECAPACITY;
+  if (capacity < 64 || capacity % 64 != 0 || prefix_len < 0 || (long)prefix_len + n > capacity)
+    return LLMCAD_ECAPACITY;
   const Shape s(*cfg);
   const int G = pass_grid();
   if (workspace_bytes < WorkspaceLayout(s, n - first, G).total) return LLMCAD_EWORKSPACE;
@@ -470,7 +478,8 @@ int llmcad_commit_path(const llmcad_config* cfg, void* k_cache, void* v_cache, i
   if (rc != LLMCAD_OK) return rc;
   if (!k_cache || !v_cache || !path || !accept_len) return LLMCAD_EARG;
   if (n < 1 || n > kMaxNodes) return LLMCAD_ETREE;
-  if (capacity < 1 || prefix_len < 0 || (long)prefix_len + n > capacity) return LLMCAD_ECAPACITY;
+  if (capacity < 64 || capacity % 64 != 0 || prefix_len < 0 || (long)prefix_len + n > capacity)
+    return LLMCAD_ECAPACITY;
   if (n == 1) return LLMCAD_OK;  // only the root, already in place
   HIP_TRY(launch_commit(k_cache, v_cache, cfg->n_layers * cfg->n_heads, capacity, prefix_len, path, accept_len, n,
                         cfg->head_dim, (hipStream_t)stream));
@@ -486,7 +495,8 @@ int llmcad_prefill(const llmcad_config* cfg, const void* packed, void* k_cache, 
   if (n_tokens < 1) return LLMCAD_ETREE;
   for (int i = 0; i < n_tokens; ++i)
     if (tokens[i] < 0 || tokens[i] >= cfg->vocab) return LLMCAD_ETREE;
-  if (capacity < 1 || start_pos < 0 || (long)start_pos + n_tokens > capacity) return LLMCAD_ECAPACITY;
+  if (capacity < 64 || capacity % 64 != 0 || start_pos < 0 || (long)start_pos + n_tokens > capacity)
+    return LLMCAD_ECAPACITY;
   const Shape s(*cfg);
   // Largest chain the workspace holds.
   int chunk = 0;

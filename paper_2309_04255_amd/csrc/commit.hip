@@ -2,7 +2,8 @@
 // rectification": the tree is rolled back to its verified sequence, which
 // becomes the input of the next generation step).
 //
-// The pass wrote node i's keys and values to cache slot prefix_len + i, at
+// The pass wrote node i's keys and values to cache slot prefix_len + i (K
+// row-major per head, V transposed per head), at
 // the position the node keeps if accepted (prefix_len + its depth).  The
 // accepted nodes are path[0] = 0 (the root), path[1..len], one per depth, so
 // committing them is a move of slot prefix_len + path[k] to prefix_len + k for
@@ -19,28 +20,38 @@ namespace {
 __global__ __launch_bounds__(256) void commit_kernel(bf16* __restrict__ k_cache, bf16* __restrict__ v_cache,
                                                      int cap, int prefix_len, const int* __restrict__ path,
                                                      const int* __restrict__ accept_len, int n, int dh) {
-  extern __shared__ bf16x8 rows[];  // [2][len + 1][dh / 8]: K rows, then V rows
+  // LDS: the K rows [len + 1][dh / 8] (16-byte pieces), then the V entries
+  // [dh][len + 1] (the V cache is transposed per head: a slot is one entry of
+  // each of the head's dh rows)
+  extern __shared__ bf16x8 rows[];
   const int len = ldg(accept_len);
   if (len < 1 || len >= n) return;  // nothing moves (or not the output of a pass over n nodes)
-  const int cpr = dh / 8;            // 16-byte chunks per row
-  const int items = (len + 1) * cpr;
-  const size_t base = (size_t)blockIdx.x * cap * dh;  // this (layer, head)'s rows
-  for (int e = threadIdx.x; e < items; e += blockDim.x) {
-    const int k = e / cpr, c = e % cpr;
+  const int cpr = dh / 8;            // 16-byte pieces per K row
+  const int kitems = (len + 1) * cpr, vitems = (len + 1) * dh;
+  bf16* vents = (bf16*)(rows + kitems);
+  const size_t base = (size_t)blockIdx.x * cap * dh;  // this (layer, head)'s K rows, and its V^T rows
+  auto source = [&](int k) {
     const int src = ldg(path + k);
-    const bool ok = src >= k && src < n;
-    const size_t at = base + (size_t)(prefix_len + (ok ? src : k)) * dh + 8 * c;
-    rows[e] = ldg((const bf16x8*)(k_cache + at));
-    rows[items + e] = ldg((const bf16x8*)(v_cache + at));
+    return src >= k && src < n ? src : k;  // (an invalid entry reads its own slot: left alone)
+  };
+  for (int e = threadIdx.x; e < kitems; e += blockDim.x) {
+    const int k = e / cpr, c = e % cpr;
+    rows[e] = ldg((const bf16x8*)(k_cache + base + (size_t)(prefix_len + source(k)) * dh + 8 * c));
+  }
+  for (int e = threadIdx.x; e < vitems; e += blockDim.x) {
+    const int dim = e / (len + 1), k = e % (len + 1);
+    vents[e] = ldg(v_cache + base + (size_t)dim * cap + prefix_len + source(k));
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < items; e += blockDim.x) {
+  for (int e = threadIdx.x; e < kitems; e += blockDim.x) {
     const int k = e / cpr, c = e % cpr;
-    const int src = ldg(path + k);
-    if (src == k || src < k || src >= n) continue;  // in place already (or an invalid entry: left alone)
-    const size_t at = base + (size_t)(prefix_len + k) * dh + 8 * c;
-    stg((bf16x8*)(k_cache + at), rows[e]);
-    stg((bf16x8*)(v_cache + at), rows[items + e]);
+    if (source(k) == k) continue;  // in place already
+    stg((bf16x8*)(k_cache + base + (size_t)(prefix_len + k) * dh + 8 * c), rows[e]);
+  }
+  for (int e = threadIdx.x; e < vitems; e += blockDim.x) {
+    const int dim = e / (len + 1), k = e % (len + 1);
+    if (source(k) == k) continue;
+    stg(v_cache + base + (size_t)dim * cap + prefix_len + k, vents[e]);
   }
 }
 

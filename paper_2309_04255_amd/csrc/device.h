@@ -176,6 +176,10 @@ __device__ __forceinline__ void st_coherent_bf2(bf16* p, float a, float b) {  //
   __hip_atomic_store((LLMCAD_GLOBAL uint32_t*)p, lo | (hi << 16), __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ void st_coherent_bf(bf16* p, float a) {  // p 2-byte aligned
+  __hip_atomic_store((LLMCAD_GLOBAL uint16_t*)p, __builtin_bit_cast(uint16_t, f2bf(a)), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ float ld_coherent(const float* p) {
   return __hip_atomic_load((const LLMCAD_GLOBAL float*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -190,16 +194,6 @@ __device__ __forceinline__ float2 ld_coherent2(const float* p) {  // p 8-byte al
 // Device-scope counter updates.
 __device__ __forceinline__ int atomic_add_dev(int* p, int v) {
   return __hip_atomic_fetch_add((LLMCAD_GLOBAL int*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Counts this workgroup's arrival on `counter` once its stores above have
-// completed (the waiting side uses join_wait).  Must be called by all
-// threads of the workgroup.
-__device__ __forceinline__ void arrive_count(int* counter) {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) atomic_add_dev(counter, 1);
 }
 
 // Counts this workgroup's arrival on `counter`; returns true (to every

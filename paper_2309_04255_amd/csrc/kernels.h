@@ -58,7 +58,7 @@ struct PassParams {
   long long o_attn_norm, o_ffn_norm;
   int d_nb;
   StepPlan step[kSteps];
-  // KV cache [L][H][cap][Dh]
+  // KV cache: K [L][H][cap][Dh], V transposed per head [L][H][Dh][cap]
   bf16* k_cache;
   bf16* v_cache;
   // workspace
@@ -80,7 +80,7 @@ struct PassParams {
   int* bar;         // [kBarSlots][kBarStride]
   float* attn_o;    // [H][MB][KS][16][Dh] key-split partial outputs (unnormalised)
   float* attn_ml;   // [H][MB][KS][16][2]  their running max and sum
-  int attn_splits;  // KS, key splits per (head, row block): 1 to 4
+  int attn_splits;  // KS, key splits per (head, row block): 1 to 4 (the split's 32-key steps contiguous)
   int* head_cnt;    // [H][MB] arrivals of the key splits
   float* lm_val;    // [Mp][G] LM-head argmax per row and workgroup
   int* lm_idx;
@@ -94,6 +94,7 @@ struct PassParams {
   // control
   int spin_limit;    // bound of every wait loop (polls)
   int wl_cap;        // weight stages per wave copied to LDS before a barrier, at most
+  int attn_prefetch; // 1: the attention fetches its prefix steps before its barrier (0: all after)
   long long* trace;  // diagnostics: [G][4 + 5L][8] phase timestamps, or null
 };
 

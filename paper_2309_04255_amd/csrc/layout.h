@@ -16,7 +16,6 @@ constexpr int kNB = 16;                        // output columns per block
 constexpr int kStepK = 32;                     // inputs per k-step
 constexpr int kBlockBytes = kNB * kStepK * 2;  // 1 KiB
 constexpr int kMaxNodes = LLMCAD_MAX_NODES;
-constexpr int kAttnChunk = 128;     // key positions staged in LDS at once
 constexpr int kAttnMaxSplits = 4;   // key splits per (head, 16-row block)
 constexpr int kPassMaxGrid = 1024;  // workgroups of the pass
 constexpr int kBarSlots = 16;       // grid-barrier counters

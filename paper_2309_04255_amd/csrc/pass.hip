@@ -187,33 +187,6 @@ __device__ __forceinline__ bool grid_wait(const Sync& s, int phase, int G) {
   return ok;
 }
 
-// Waits until `counter` has counted `expected` arrivals (arrive_count),
-// then resets it for its next use; one wave polls.  False (to all threads)
-// if the bounded spin ran out.
-__device__ __forceinline__ bool join_wait(const Sync& s, int* counter, int expected) {
-  if (threadIdx.x < 64) {
-    int ok = 1, spins = 0;
-    while (true) {
-      const int v = ld_coherent(counter);
-      if (__all(v >= expected)) break;
-      __builtin_amdgcn_s_sleep(1);
-      if (++spins > s.limit) {
-        if (threadIdx.x == 0) st_coherent(s.status, 1);
-        ok = 0;
-        break;
-      }
-    }
-    if (threadIdx.x == 0) {
-      if (ok) st_coherent(counter, 0);
-      *s.lds_flag = ok;
-    }
-  }
-  lds_barrier();
-  const bool ok = *s.lds_flag != 0;
-  lds_barrier();
-  return ok;
-}
-
 // ------------------------------------------------------------------ GEMM
 
 struct GemmLds {
@@ -263,7 +236,7 @@ struct StepIo {
   const float* ssq;  // norm steps: [d/16][Mp] sums of squares of the residual version
   bf16* q;           // QKV: [Mp][d] queries after the rotary embedding
   bf16* kc;          // QKV: K cache of this layer [H][cap][Dh]
-  bf16* vc;          // QKV: V cache of this layer [H][cap][Dh]
+  bf16* vc;          // QKV: V cache of this layer, transposed per head [H][Dh][cap]
   float* x_out;      // RESID: [Mp][d]
   float* ssq_out;    // RESID: [d/16][Mp]
   bf16* xg_out;      // RESID: fragment-order bf16(x_out * g_next)
@@ -670,13 +643,14 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
         }
       }
     } else {
+      // v: the cache holds V transposed per head ([Dh][cap]); this lane's
+      // four rows are four consecutive slots of one dim
       const int cv = col - 2 * d, hh = cv / dh, dim = cv % dh;
+      bf16* vrow = io.vc + ((size_t)hh * dh + dim) * p.cap + p.prefix_len + p.m0;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 16 * rb + rr0 + i;
-        const float nxt = dpp_f<kDppRowShl1>(v[i]);
-        if (r < p.n && (j & 1) == 0)
-          st_coherent_bf2(io.vc + ((size_t)hh * p.cap + p.prefix_len + p.m0 + r) * dh + dim, v[i], nxt);
+        if (r < p.n) st_coherent_bf(vrow + r, v[i]);
       }
     }
   } else if constexpr (EPI == EPI_RESID) {
@@ -943,84 +917,162 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
 
 // ------------------------------------------------------------------ attention
 
+// The cache holds K row-major per head ([cap][DH]) and V transposed per head
+// ([DH][cap]), so that both operands of the attention's matrix products load
+// straight from memory in MFMA fragment order, 16 bytes per lane, with no
+// staging or transposition in between:
+//  - K is the A operand of S^T = K q^T (16 keys x 32 dims per MFMA).  Key
+//    block b of a 32-key step at key0 puts key key0 + 8 (r / 4) + 4 b + r % 4
+//    in its row r, so that lane (li, g) of the result holds the scores of keys
+//    key0 + 8 g + 4 b + i (i < 4) for query row li;
+//  - V^T is the A operand of O^T = V^T P^T (16 dims x 32 keys): lane (li, g)
+//    holds dim 16 db + li for keys key0 + 8 g .. + 7 -- exactly the keys whose
+//    scores it holds, so the probabilities go from the S result into the PV
+//    product's B operand without leaving the lane.
 template <int DH>
-struct AttnGeom {
-  static constexpr int CH = kAttnChunk;  // key positions per LDS tile
-  static constexpr int KST = DH + 8;     // K row stride (bf16)
-  static constexpr int VST = CH + 4;     // V^T row stride (bf16): 8 rows apart fall in 2 banks
-  static constexpr int KS_BYTES = CH * KST * 2;
-  static constexpr int VT_BYTES = DH * VST * 2;
-  static constexpr int BYTES = KS_BYTES + VT_BYTES;
+struct AttnStep {
+  static constexpr int NS = DH / 32;         // 32-dim k-steps of S^T
+  static constexpr int NB = DH / 16;         // 16-dim blocks of O^T
+  static constexpr int LOADS = 2 * NS + NB;  // 16-byte loads per lane (1 KiB per wave each)
+  bf16x8 f[LOADS];                           // K block b, k-step s at b NS + s; V^T block db at 2 NS + db
 };
 
-// Stage key positions [p0, p0 + CH) ∩ [lo, hi) of one head into LDS: K
-// row-major, V transposed; other rows zero.  Every key comes from the cache:
-// the tree's keys and values were written to their slots, already rotated,
-// by the QKV phase.
-// K/V of key positions [p0, p0 + CH) ∩ [lo, hi) of one head, loaded into
-// registers (other positions zero): a thread's 16-byte items of K and V.
+// Steps of a unit fetched before the phase's barrier.  Wave 0 polls the
+// barrier and issues no load before it has seen it (a poll waits for every
+// older load of its wave), so its first W0 steps are copied straight to LDS
+// by wave 1; wave 1 holds its first two steps in registers; waves 2 and 3
+// hold two in registers and the next W23 in LDS.  The LDS slots (one step
+// each) are laid out wave 0's, then wave 2's, then wave 3's.
 template <int DH>
-struct AttnChunkRegs {
-  static constexpr int IT = AttnGeom<DH>::CH * (DH / 8) / kThreads;
-  bf16x8 k[IT], v[IT];
+struct AttnPrefetch {
+  static constexpr int REG = 2;
+  static constexpr int STEP_BYTES = AttnStep<DH>::LOADS * 1024;  // one wave's step
+  static constexpr int SLOTS0 = kGemmLdsBytes / STEP_BYTES;
+  static constexpr int SLOTS = SLOTS0 < 16 ? SLOTS0 : 16;
+  static constexpr int W0 = SLOTS / 2 < 6 ? SLOTS / 2 : 6;
+  static constexpr int W23 = (SLOTS - W0) / 2;
+  static constexpr int STEPS = W0 + REG + 2 * (REG + W23);  // per unit
+  // steps in registers and in LDS of wave w, and the first LDS slot of its share
+  __device__ static int reg(int w) { return w == 0 ? 0 : REG; }
+  __device__ static int lds(int w) { return w == 0 ? W0 : w == 1 ? 0 : W23; }
+  __device__ static int slot0(int w) { return w == 0 ? 0 : w == 2 ? W0 : W0 + W23; }
 };
 
+// Source of load e of the 32-key step at key0 for this lane (the zero line
+// for keys at or past lim).  kc: the head's K [cap][DH]; vt: its V^T [DH][cap]
+// (cap a multiple of 8, so a lane's 8 keys never cross a row of V^T).
 template <int DH>
-__device__ __forceinline__ void attn_load(AttnChunkRegs<DH>& R, const bf16* kc, const bf16* vc, int p0, int lo,
-                                          int hi) {
+__device__ __forceinline__ const bf16x8* attn_src(const bf16* kc, const bf16* vt, int cap, int key0, int lim,
+                                                  const bf16x8* zero, int e) {
+  const int lane = threadIdx.x & 63, li = lane & 15, g = lane >> 4;
+  constexpr int NS = AttnStep<DH>::NS;
+  if (e < 2 * NS) {
+    const int b = e / NS, s = e % NS;
+    const int key = key0 + 8 * (li >> 2) + 4 * b + (li & 3);
+    return opaque(key < lim ? (const bf16x8*)(kc + (size_t)key * DH + 32 * s + 8 * g) : zero);
+  }
+  const int kv = key0 + 8 * g;
+  return opaque(kv < lim ? (const bf16x8*)(vt + (size_t)(16 * (e - 2 * NS) + li) * cap + kv) : zero);
+}
+
+template <int DH>
+__device__ __forceinline__ void attn_load(AttnStep<DH>& R, const bf16* kc, const bf16* vt, int cap, int key0, int lim,
+                                          const bf16x8* zero) {
 #pragma unroll
-  for (int k = 0; k < AttnChunkRegs<DH>::IT; ++k) {
-    const int idx = threadIdx.x + k * kThreads;
-    const int j = idx / (DH / 8), dc = (idx % (DH / 8)) * 8;
-    const int pos = p0 + j;
-    if (pos >= lo && pos < hi) {
-      R.k[k] = ldg((const bf16x8*)(kc + (size_t)pos * DH + dc));
-      R.v[k] = ldg((const bf16x8*)(vc + (size_t)pos * DH + dc));
-    } else {
+  for (int e = 0; e < AttnStep<DH>::LOADS; ++e) R.f[e] = ldg(attn_src<DH>(kc, vt, cap, key0, lim, zero, e));
+}
+
+// The step's loads copied straight to LDS: load e lands at buf + e KiB (lane
+// l's 16 bytes at + 16 l).
+template <int DH>
+__device__ __forceinline__ void attn_copy(char* buf, const bf16* kc, const bf16* vt, int cap, int key0, int lim,
+                                          const bf16x8* zero) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        R.k[k][e] = (bf16)0.0f;
-        R.v[k][e] = (bf16)0.0f;
-      }
+  for (int e = 0; e < AttnStep<DH>::LOADS; ++e) dma16(attn_src<DH>(kc, vt, cap, key0, lim, zero, e), buf + e * 1024);
+}
+
+template <int DH>
+__device__ __forceinline__ void attn_from_lds(AttnStep<DH>& R, const char* buf) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int e = 0; e < AttnStep<DH>::LOADS; ++e) R.f[e] = lds_ld<bf16x8>(buf + e * 1024 + lane * 16);
+}
+
+// One 32-key step for the 16 query rows of a unit: S^T on the matrix cores,
+// the mask (the prefix, then the tree's slots of the row's ancestors-or-self;
+// keys at or past lim are not visible), the online softmax in the log2 domain,
+// and O^T += V^T P^T with P split into two bf16 halves (hi + lo, ~16
+// significant bits).  V entries of keys at or past lim inside a loaded piece
+// are zeroed: the cache there may hold anything, and 0 x NaN is NaN.
+template <int DH>
+__device__ __forceinline__ void attn_compute(const AttnStep<DH>& R, const bf16x8 (&qf)[DH / 32],
+                                             const uint32_t (&anc)[4], int key0, int P, int lim, float scale_log2,
+                                             float& m_run, float& l_run, f32x4 (&oacc)[DH / 16]) {
+  constexpr int NS = AttnStep<DH>::NS, NB = AttnStep<DH>::NB;
+  const int lane = threadIdx.x & 63, g = lane >> 4;
+  f32x4 sc[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    sc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NS; ++s) sc[b] = mfma16x16x32(R.f[b * NS + s], qf[s], sc[b]);
+  }
+  float sv[8];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int pos = key0 + 8 * g + e;
+    const int t = pos - P < 0 ? 0 : pos - P;  // (tree slot; any in-range index for prefix keys)
+    const bool vis = pos < lim && (pos < P || ((anc[(t >> 5) & 3] >> (t & 31)) & 1u));
+    sv[e] = vis ? sc[e >> 2][e & 3] * scale_log2 : -INFINITY;
+    mx = fmaxf(mx, sv[e]);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+  const float m_new = fmaxf(m_run, mx);
+  const float m_use = m_new == -INFINITY ? 0.0f : m_new;
+  const float alpha = exp2f(m_run - m_use);
+  bf16x8 ph, pl;
+  float psum = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float pe = exp2f(sv[e] - m_use);
+    ph[e] = f2bf(pe);
+    pl[e] = f2bf(pe - bf2f(ph[e]));
+    psum += pe;
+  }
+  psum += __shfl_xor(psum, 16, kWave);
+  psum += __shfl_xor(psum, 32, kWave);
+  l_run = l_run * alpha + psum;
+  m_run = m_new;
+  const bool edge = key0 + 32 > lim;  // (wave-uniform)
+  const int valid = lim - (key0 + 8 * g);
+#pragma unroll
+  for (int db = 0; db < NB; ++db) {
+    bf16x8 a = R.f[2 * NS + db];
+    if (edge) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a[e] = e < valid ? a[e] : (bf16)0.0f;
     }
+    oacc[db] = oacc[db] * alpha;
+    oacc[db] = mfma16x16x32(a, ph, oacc[db]);
+    oacc[db] = mfma16x16x32(a, pl, oacc[db]);
   }
 }
 
-// Registers -> one LDS chunk buffer: K row-major, V transposed; positions
-// [0, npos) of the chunk (the 64-key steps that read it must find finite
-// values: V enters the products even where the softmax weight is 0).
-template <int DH>
-__device__ __forceinline__ void attn_store(char* buf, const AttnChunkRegs<DH>& R, int npos = AttnGeom<DH>::CH) {
-  using Gm = AttnGeom<DH>;
-  char* Ks = buf;
-  char* Vt = buf + Gm::KS_BYTES;
-#pragma unroll
-  for (int k = 0; k < AttnChunkRegs<DH>::IT; ++k) {
-    const int idx = threadIdx.x + k * kThreads;
-    const int j = idx / (DH / 8), dc = (idx % (DH / 8)) * 8;
-    if (j >= npos) continue;
-    lds_st<bf16x8>(Ks + ((size_t)j * Gm::KST + dc) * 2, R.k[k]);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) lds_st<bf16>(Vt + ((size_t)(dc + e) * Gm::VST + j) * 2, R.v[k][e]);
-  }
-}
-
-// Tree attention phase.  Unit (head, 16-row block, key split) per
-// workgroup; the KS key splits of a (head, row block) take contiguous runs
-// of the prefix's CH-position chunks, and the last one also the tree's own
-// positions.  Node i attends to the prefix and to the cache slots of its
-// ancestors-or-self (a 128-bit set per node).  A unit's keys go through LDS
-// two chunks at a time (a "pair": four 64-key steps, one per wave; the
-// waves' partial results are merged in LDS, in wave order).  Its first pair
-// of prefix chunks is staged before the phase's barrier (this pass does not
-// write the prefix), further prefix chunks are read once into L2 meanwhile,
-// and the tree's keys (written by the QKV phase) are loaded into registers as
-// soon as the barrier is passed.  Per step: S^T = K q^T on the matrix cores,
-// online softmax in the log2 domain, O^T += V^T P^T with P split into two
-// bf16 halves (P never leaves registers: the S result's lane layout is the
-// PV product's k-slot order).  With KS > 1 the prefix-only splits store
-// their partial results and the tree's split, which has the most work,
-// merges them with its own, in split order.  MB: 16-row blocks of the pass.
+// Tree attention phase.  Unit (head, 16-row block, key split) per workgroup;
+// the KS splits of a (head, row block) take contiguous runs of the key range's
+// 32-key steps (the prefix, then the tree's n_t slots), the last one ending
+// with the tree.  Node i attends to the prefix and to the cache slots of its
+// ancestors-or-self (a 128-bit set per node).  The four waves take a unit's
+// steps in turn; the steps that hold prefix keys only (this pass does not
+// write the prefix) are fetched before the phase's barrier, a wave's first
+// two into registers and the next into its share of the LDS, so after the
+// barrier only the queries and the tree's keys (written by the QKV phase) are
+// waited for.  The waves' partial results are merged in LDS, in wave order;
+// with KS > 1 the prefix-only splits store their partial results and the
+// tree's split merges them with its own, in split order.  MB: 16-row blocks
+// of the pass.
 template <int MB, int DH>
 __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& pin, int layer, int phase, char* lds,
                                                                      int* lds_flag) {
@@ -1028,74 +1080,108 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
   const Sync sy = make_sync(p, lds_flag);
   layer = wave_uniform(layer);
   phase = wave_uniform(phase);
-  using Gm = AttnGeom<DH>;
-  constexpr int CH = Gm::CH, KSTEPS = DH / 32, DB = DH / 16, KST = Gm::KST, VST = Gm::VST;
+  using PF = AttnPrefetch<DH>;
+  constexpr int KSTEPS = DH / 32, DB = DH / 16;
   const int KS = wave_uniform(p.attn_splits);
   const int rbn = wave_uniform((p.n + 15) / 16);  // row blocks holding nodes
   const int units = wave_uniform(p.H) * rbn * KS;
   const int wave = wave_index(), lane = threadIdx.x & 63, li = lane & 15, g = lane >> 4;
   const int P = wave_uniform(p.prefix_len), n = wave_uniform(p.n);
   const int nt = wave_uniform(p.nt), m0 = wave_uniform(p.m0);  // the tree's nodes; node of row 0
-  const int npc = (P + CH - 1) / CH;  // prefix chunks; chunk npc is the tree's
-  const size_t kv_layer = (size_t)p.H * p.cap * DH;
+  const int cap = wave_uniform(p.cap);
+  const int limit = P + nt;                 // keys: prefix [0, P), then the tree's slots [P, P + nt)
+  const int nsteps = (limit + 31) / 32;     // 32-key steps of the key range
+  const size_t kv_layer = (size_t)p.H * cap * DH;
   const bf16* kcl = p.k_cache + (size_t)layer * kv_layer;
-  const bf16* vcl = p.v_cache + (size_t)layer * kv_layer;
+  const bf16* vtl = p.v_cache + (size_t)layer * kv_layer;
   const bf16* qb = p.q + (size_t)layer * p.Mp * p.d;
   bf16* obase = p.o + (size_t)layer * p.Mp * p.d;
-  char* buf[2] = {lds, lds + Gm::BYTES};
-  // chunk c: prefix positions [c CH, min((c + 1) CH, P)) for c < npc, the
-  // tree's [P, P + nt) for c == npc (all its nodes: those computed before
-  // this pass are in their cache slots already)
-  auto chunk_lo = [&](int c) { return c < npc ? c * CH : P; };
-  auto chunk_hi = [&](int c) { return c < npc ? ((c + 1) * CH < P ? (c + 1) * CH : P) : P + nt; };
-  // the chunks of split ks: prefix chunks [c_lo, c_hi), then the tree's if ks is the last
-  auto split_chunks = [&](int ks, int& c_lo, int& c_hi, int& nch) {
-    c_lo = ks * npc / KS;
-    c_hi = (ks + 1) * npc / KS;
-    nch = c_hi - c_lo + (ks == KS - 1 ? 1 : 0);
+  const bf16x8* zero = (const bf16x8*)p.zero + lane;
+  // step range [s_lo, s_hi) of split ks; keys of the split end at lim
+  auto split_steps = [&](int ks, int& s_lo, int& s_hi, int& lim) {
+    s_lo = ks * nsteps / KS;
+    s_hi = (ks + 1) * nsteps / KS;
+    lim = 32 * s_hi < limit ? 32 * s_hi : limit;
   };
-  auto list_chunk = [&](int c_lo, int c_hi, int j) { return c_lo + j < c_hi ? c_lo + j : npc; };
+  // A step can be fetched before the barrier when no cache line it touches
+  // holds a tree slot: the QKV phase writes the tree's slots (with stores that
+  // go to memory), and a line read into this XCD's L2 before then would stay
+  // stale.  K rows are whole lines per key; a V^T row holds 64 slots per
+  // 128-byte line (rows start on lines: the capacity is a multiple of 64), so
+  // the step must end at or before the last 64-slot boundary of the prefix.
+  const int P_lines = P & ~63;
+  auto early = [&](int j) { return 32 * j + 32 <= P_lines; };
 
-  int u = virtual_wg(p.G);
-  int staged = 0;  // list entries (bit j: entry j, j < 2) already in LDS
-  if (u < units) {
-    const int h = u / (rbn * KS), ks = u % KS;
-    const bf16* kc = kcl + (size_t)h * p.cap * DH;
-    const bf16* vc = vcl + (size_t)h * p.cap * DH;
-    int c_lo, c_hi, nch;
-    split_chunks(ks, c_lo, c_hi, nch);
-    AttnChunkRegs<DH> R;
-    for (int j = 0; j < 2 && c_lo + j < c_hi; ++j) {
-      const int c = c_lo + j;
-      attn_load<DH>(R, kc, vc, chunk_lo(c), chunk_lo(c), chunk_hi(c));
-      attn_store<DH>(buf[j], R);
-      staged |= 1 << j;
+  // Attention units are dealt out so that each head's units (its row blocks
+  // and key splits, which read the same keys and values) sit together on one
+  // XCD and consecutive heads on consecutive XCDs: workgroup w (on XCD w % 8)
+  // takes, in round k, the unit of head (q / R) 8 + w % 8 numbered q % R
+  // within the head, q = (w + k G) / 8, R = units per head.  (With a grid
+  // that is not a multiple of 8, unit i = w + k G.)  Within a head the units
+  // keep their order, so a merging split's partners come earlier or in the
+  // same round and every wait ends.
+  const int R = rbn * KS;
+  const int G = wave_uniform(p.G);
+  const bool by_xcd = G % kXcds == 0;
+  auto unit_of = [&](int i) {  // unit of slot i, or -1 (no unit), or -2 (past the last)
+    if (!by_xcd) return i < units ? i : -2;
+    const int q = i / kXcds, h = (q / R) * kXcds + i % kXcds;
+    if ((q / R) * kXcds >= p.H) return -2;
+    return h < p.H ? h * R + q % R : -1;
+  };
+
+  AttnStep<DH> A, B;
+  const int wg = blockIdx.x;
+  const bool prefetch = p.attn_prefetch != 0;
+  {
+    const int u = prefetch ? unit_of(wg) : -1;
+    if (u >= 0) {
+      const int h = u / R, ks = u % KS;
+      const bf16* kc = kcl + (size_t)h * cap * DH;
+      const bf16* vt = vtl + (size_t)h * cap * DH;
+      int s_lo, s_hi, lim;
+      split_steps(ks, s_lo, s_hi, lim);
+      const int j0 = s_lo + wave;
+      if (wave == 1) {  // wave 0's first steps, into its LDS slots
+        for (int i = 0; i < PF::W0; ++i) {
+          const int j = s_lo + 4 * i;
+          if (j < s_hi && early(j)) attn_copy<DH>(lds + (size_t)i * PF::STEP_BYTES, kc, vt, cap, 32 * j, lim, zero);
+        }
+      }
+      if (wave != 0) {
+        if (j0 < s_hi && early(j0)) attn_load<DH>(A, kc, vt, cap, 32 * j0, lim, zero);
+        if (j0 + 4 < s_hi && early(j0 + 4)) attn_load<DH>(B, kc, vt, cap, 32 * (j0 + 4), lim, zero);
+        for (int i = PF::REG; i < PF::REG + PF::lds(wave); ++i) {
+          const int j = j0 + 4 * i;
+          if (j < s_hi && early(j))
+            attn_copy<DH>(lds + (size_t)(PF::slot0(wave) + i - PF::REG) * PF::STEP_BYTES, kc, vt, cap, 32 * j, lim,
+                          zero);
+        }
+      }
     }
-    // the rest of the split's prefix: read once so that it waits in L2
-    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-    uint32_t sink = 0;
-    for (int c = c_lo + 2; c < c_hi; ++c) {
-      attn_load<DH>(R, kc, vc, chunk_lo(c), chunk_lo(c), chunk_hi(c));
-#pragma unroll
-      for (int k = 0; k < AttnChunkRegs<DH>::IT; ++k)
-        sink ^= __builtin_bit_cast(u32x4, R.k[k])[0] ^ __builtin_bit_cast(u32x4, R.v[k])[0];
-    }
-    // (a store the compiler cannot rule out keeps the reads; n >= 1 always)
-    if (p.n < 0) stg(p.lm_idx + blockIdx.x, (int)sink);
   }
   trace_mark(sy, phase, 0);
   if (!grid_wait(sy, phase, p.G)) return false;
   trace_mark(sy, phase, 1);
+  // The prefetched steps have landed (each wave's own loads and copies), and
+  // wave 1's copies for wave 0 are visible to it.
+  __builtin_amdgcn_s_waitcnt(0);
+  lds_barrier();
 
-  for (; u < units; u += p.G) {
-    const int h = u / (rbn * KS), rb = (u / KS) % rbn, ks = u % KS;
-    const bf16* kc = kcl + (size_t)h * p.cap * DH;
-    const bf16* vc = vcl + (size_t)h * p.cap * DH;
-    int c_lo, c_hi, nch;
-    split_chunks(ks, c_lo, c_hi, nch);
-    const bool has_tree = ks == KS - 1;
+  for (int i_slot = wg, round = 0;; i_slot += G, ++round) {
+    const int u = unit_of(i_slot);
+    if (u == -2) break;
+    if (u < 0) continue;
+    const bool first_unit = round == 0 && prefetch;
+    const int h = u / R, rb = (u / KS) % rbn, ks = u % KS;
+    const bf16* kc = kcl + (size_t)h * cap * DH;
+    const bf16* vt = vtl + (size_t)h * cap * DH;
+    int s_lo, s_hi, lim;
+    split_steps(ks, s_lo, s_hi, lim);
+    const int j0 = s_lo + wave;
+    const int cnt = j0 < s_hi ? (s_hi - j0 + 3) / 4 : 0;  // this wave's steps: j0 + 4 i, i < cnt
     // Query fragments (B operand of S^T = K q^T): lane holds row 16 rb + li,
-    // dims 32 ks + 8 g + e (queries were rotated by the QKV phase).
+    // dims 32 s + 8 g + e (queries were rotated by the QKV phase).
     bf16x8 qf[KSTEPS];
     uint32_t anc[4];
     const int row = 16 * rb + li;
@@ -1108,114 +1194,33 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
 #pragma unroll
       for (int w = 0; w < 4; ++w) anc[w] = ldg(ap + w);
     }
-    // the tree's keys (last split): loaded now, stored when their buffer is free
-    AttnChunkRegs<DH> RT;
-    attn_load<DH>(RT, kc, vc, P, P, has_tree ? P + nt : P);
+    // Where step i of this wave is: in a register buffer (fetched before the
+    // barrier), in an LDS slot (copied before the barrier), or still in memory.
+    const int nreg = first_unit ? PF::reg(wave) : 0, nlds = first_unit ? PF::lds(wave) : 0;
+    auto fetch = [&](AttnStep<DH>& R_, int i) {
+      const int j = j0 + 4 * i;
+      if (i >= nreg && i < nreg + nlds && i < cnt && early(j))
+        attn_from_lds<DH>(R_, lds + (size_t)(PF::slot0(wave) + i - nreg) * PF::STEP_BYTES);
+      else
+        attn_load<DH>(R_, kc, vt, cap, 32 * j, lim, zero);
+    };
+    if (!(nreg > 0 && cnt > 0 && early(j0))) fetch(A, 0);
+    if (!(nreg > 1 && cnt > 1 && early(j0 + 4))) fetch(B, 1);
+    trace_mark(sy, phase, 3);
     float m_run = -INFINITY, l_run = 0.0f;
     f32x4 oacc[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-    trace_mark(sy, phase, 3);
-    for (int j0 = 0; j0 < nch; j0 += 2) {  // a pair of list entries: buffers 0 and 1
-      const int have = j0 == 0 ? staged : 0;
-      const int need = (j0 + 1 < nch ? 3 : 1) & ~have;
-      if (need) {
-        lds_barrier();  // the previous pair's readers are done
-        for (int j = 0; j < 2; ++j) {
-          if (!((need >> j) & 1)) continue;
-          const int c = list_chunk(c_lo, c_hi, j0 + j);
-          if (c == npc) {
-            attn_store<DH>(buf[j], RT, (nt + 63) & ~63);
-          } else {
-            AttnChunkRegs<DH> R;
-            attn_load<DH>(R, kc, vc, chunk_lo(c), chunk_lo(c), chunk_hi(c));
-            attn_store<DH>(buf[j], R);
-          }
-        }
-      }
-      lds_barrier();
-      // step w of the pair: entry j0 + w / 2, keys 64 (w % 2) .. + 63
-      const int jw = j0 + wave / 2;
-      const int c = list_chunk(c_lo, c_hi, jw < nch ? jw : 0);
-      const int p0 = chunk_lo(c), hi_t = jw < nch ? chunk_hi(c) : 0;
-      const int c0k = 64 * (wave & 1);
-      if (p0 + c0k < hi_t) {
-        const bf16* Ks = reinterpret_cast<const bf16*>(buf[wave / 2]);
-        const bf16* Vt = reinterpret_cast<const bf16*>(buf[wave / 2] + Gm::KS_BYTES);
-        f32x4 sc[4];
-#pragma unroll
-        for (int jb = 0; jb < 4; ++jb) {
-          sc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int s2 = 0; s2 < KSTEPS; ++s2) {
-            const bf16x8 a = lds_ld<bf16x8>(&Ks[(c0k + 16 * jb + li) * KST + 32 * s2 + 8 * g]);
-            sc[jb] = mfma16x16x32(a, qf[s2], sc[jb]);
-          }
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int jb = 0; jb < 4; ++jb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int pos = p0 + c0k + 16 * jb + 4 * g + e;
-            const int t = pos - P;
-            const bool vis = pos < hi_t && (pos < P || (t < nt && ((anc[t >> 5] >> (t & 31)) & 1u)));
-            const float sv = vis ? sc[jb][e] * p.scale_log2 : -INFINITY;
-            sc[jb][e] = sv;
-            mx = fmaxf(mx, sv);
-          }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
-        const float alpha = exp2f(m_run - m_use);
-        bf16 ph[4][4], pl[4][4];
-        float psum = 0.0f;
-#pragma unroll
-        for (int jb = 0; jb < 4; ++jb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float pe = exp2f(sc[jb][e] - m_use);
-            ph[jb][e] = f2bf(pe);
-            pl[jb][e] = f2bf(pe - bf2f(ph[jb][e]));
-            psum += pe;
-          }
-        psum += __shfl_xor(psum, 16, kWave);
-        psum += __shfl_xor(psum, 32, kWave);
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) oacc[db] = oacc[db] * alpha;
-#pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2) {
-          bf16x8 bph, bpl;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            bph[e] = ph[2 * t2][e];
-            bph[4 + e] = ph[2 * t2 + 1][e];
-            bpl[e] = pl[2 * t2][e];
-            bpl[4 + e] = pl[2 * t2 + 1][e];
-          }
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const bf16* vrow = &Vt[(16 * db + li) * VST + c0k + 32 * t2 + 4 * g];
-            const bf16x4 lo4 = lds_ld<bf16x4>(vrow);
-            const bf16x4 hi4 = lds_ld<bf16x4>(vrow + 16);
-            bf16x8 av;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              av[e] = lo4[e];
-              av[4 + e] = hi4[e];
-            }
-            oacc[db] = mfma16x16x32(av, bph, oacc[db]);
-            oacc[db] = mfma16x16x32(av, bpl, oacc[db]);
-          }
-        }
-      }
+    // step i + 2 refills the buffer step i leaves
+    for (int i = 0; i < cnt; i += 2) {
+      attn_compute<DH>(A, qf, anc, 32 * (j0 + 4 * i), P, lim, p.scale_log2, m_run, l_run, oacc);
+      if (i + 2 < cnt) fetch(A, i + 2);
+      if (i + 1 >= cnt) break;
+      attn_compute<DH>(B, qf, anc, 32 * (j0 + 4 * (i + 1)), P, lim, p.scale_log2, m_run, l_run, oacc);
+      if (i + 3 < cnt) fetch(B, i + 3);
     }
-    staged = 0;
     trace_mark(sy, phase, 4);
-    // The four waves' partial results -> LDS (the chunk buffers are free),
+    // The four waves' partial results -> LDS (the prefetch slots are spent),
     // merged in wave order: o = sum_w exp2(m_w - M) o_w / sum_w exp2(m_w - M) l_w
     // (unnormalised when the key splits still have to be merged).
     lds_barrier();
@@ -1256,8 +1261,12 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
       u0[k] = o0;
       u1[k] = o1;
     }
-    if (KS > 1 && !has_tree) {
-      // A prefix split: its partial result, for the tree's split to merge.
+    // With key splits, every split stores its partial result and counts its
+    // arrival on the (head, row block) counter; the last to arrive merges all
+    // of them (no split waits for another), in split order whichever split
+    // that is, so the result is bit-reproducible.
+    bool merge = true;
+    if (KS > 1) {
 #pragma unroll
       for (int k = 0; k < NIT; ++k) {
         const int it = threadIdx.x + k * kThreads;
@@ -1266,45 +1275,32 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
         st_coherent2(&p.attn_o[(sl * 16 + i) * DH + dd], u0[k], u1[k]);
         if (dd == 0) st_coherent2(&p.attn_ml[(sl * 16 + i) * 2], uM[k], uL[k]);
       }
-      arrive_count(&p.head_cnt[rbi]);
-    } else {
-      // The tree's split (the last of the key splits, and the one with the
-      // most work) merges: it waits for the other splits' partials, loads
-      // them all before using any, and adds them in split order, its own
-      // last.  (Units are taken in increasing order and a merge waits only
-      // for lower-numbered units, so every wait ends.)
-      constexpr int SO = kAttnMaxSplits - 1;
-      static_assert(SO >= 1, "key splits");
+      merge = arrive_last(&p.head_cnt[rbi], KS, lds_flag);
+      if (merge) trace_mark(sy, phase, 6);
+    }
+    if (merge) {
+      constexpr int SO = kAttnMaxSplits;
       float2 ml[NIT][SO], ov[NIT][SO];
-      if (KS > 1) {
-        if (!join_wait(sy, &p.head_cnt[rbi], KS - 1)) return false;
-        trace_mark(sy, phase, 6);
 #pragma unroll
-        for (int k = 0; k < NIT; ++k) {
-          const int it = threadIdx.x + k * kThreads;
-          const int i = it / (DH / 2), dd = 2 * (it % (DH / 2));
+      for (int k = 0; k < NIT; ++k) {
+        const int it = threadIdx.x + k * kThreads;
+        const int i = it / (DH / 2), dd = 2 * (it % (DH / 2));
 #pragma unroll
-          for (int s2 = 0; s2 < SO; ++s2) {
-            const size_t sl = rbi * KS + (s2 < KS - 1 ? s2 : 0);
-            ml[k][s2] = s2 < KS - 1 ? ld_coherent2(&p.attn_ml[(sl * 16 + i) * 2]) : make_float2(-INFINITY, 0.0f);
-            ov[k][s2] = s2 < KS - 1 ? ld_coherent2(&p.attn_o[(sl * 16 + i) * DH + dd]) : make_float2(0.0f, 0.0f);
-          }
+        for (int s2 = 0; s2 < SO; ++s2) {
+          const bool other = s2 < KS && s2 != ks;
+          const size_t sl = rbi * KS + (other ? s2 : 0);
+          ml[k][s2] = other ? ld_coherent2(&p.attn_ml[(sl * 16 + i) * 2])
+                            : (s2 == ks ? make_float2(uM[k], uL[k]) : make_float2(-INFINITY, 0.0f));
+          ov[k][s2] = other ? ld_coherent2(&p.attn_o[(sl * 16 + i) * DH + dd])
+                            : (s2 == ks ? make_float2(u0[k], u1[k]) : make_float2(0.0f, 0.0f));
         }
-      } else {
-#pragma unroll
-        for (int k = 0; k < NIT; ++k)
-#pragma unroll
-          for (int s2 = 0; s2 < SO; ++s2) {
-            ml[k][s2] = make_float2(-INFINITY, 0.0f);
-            ov[k][s2] = make_float2(0.0f, 0.0f);
-          }
       }
 #pragma unroll
       for (int k = 0; k < NIT; ++k) {
         const int it = threadIdx.x + k * kThreads;
         const int i = it / (DH / 2), dd = 2 * (it % (DH / 2));
         const int r = 16 * rb + i;
-        float M = uM[k];
+        float M = -INFINITY;
 #pragma unroll
         for (int s2 = 0; s2 < SO; ++s2) M = fmaxf(M, ml[k][s2].x);
         float L = 0.0f, o0 = 0.0f, o1 = 0.0f;
@@ -1315,10 +1311,6 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
           o0 += ov[k][s2].x * wt;
           o1 += ov[k][s2].y * wt;
         }
-        const float wt = uM[k] == -INFINITY ? 0.0f : exp2f(uM[k] - M);
-        L += uL[k] * wt;
-        o0 += u0[k] * wt;
-        o1 += u1[k] * wt;
         const float inv = 1.0f / L;
         if (r < n) st_coherent_bf2(obase + frag_off(r, h * DH + dd, MB), o0 * inv, o1 * inv);
         if (k == 0) trace_mark(sy, phase, 7);
@@ -1408,11 +1400,16 @@ __device__ __forceinline__ void embed_phase(KParams& p, const TreeArgs& tree, in
 
 // ------------------------------------------------------------------ kernel
 
+// Dynamic LDS: the GEMM tiles' region (all LDS but the static part), which
+// the attention reuses for its prefetched steps and its merge.
 template <int DH>
 constexpr size_t dyn_lds_bytes() {
-  constexpr size_t attn = 2 * AttnGeom<DH>::BYTES;  // two chunk buffers
-  constexpr size_t gemm = kGemmLdsBytes;              // (all LDS but the static part)
-  return attn > gemm ? attn : gemm;
+  static_assert(AttnPrefetch<DH>::W0 >= 1 && AttnPrefetch<DH>::W23 >= 1 &&
+                    (size_t)(AttnPrefetch<DH>::W0 + 2 * AttnPrefetch<DH>::W23) * AttnPrefetch<DH>::STEP_BYTES <=
+                        kGemmLdsBytes,
+                "attention prefetch slots");
+  static_assert((size_t)kWaves * 16 * (DH + 2) * 4 <= kGemmLdsBytes, "attention merge");
+  return kGemmLdsBytes;
 }
 
 // ------------------------------------------------------------------ final norm

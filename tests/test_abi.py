@@ -110,6 +110,7 @@ def test_host_validation(binding):
     assert _call_verify(binding, cfg, np.zeros(129), np.arange(-1, 128)) == binding.ETREE
     assert _call_verify(binding, cfg, [1, 2], [-1, 0], prefix_len=63, cap=64) == binding.ECAPACITY
     assert _call_verify(binding, cfg, [1, 2], [-1, 0], prefix_len=-1) == binding.ECAPACITY
+    assert _call_verify(binding, cfg, [1, 2], [-1, 0], cap=96) == binding.ECAPACITY  # (not a multiple of 64)
     assert _call_verify(binding, cfg, [1, 2], [-1, 0], ws_bytes=1000) == binding.EWORKSPACE
     assert _call_verify(binding, cfg, [1, 2], [-1, 0], packed=0) == binding.EARG
     bad = binding.make_config(workloads.MODELS["tiny"])

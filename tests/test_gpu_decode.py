@@ -85,7 +85,7 @@ def test_commit_moves_path_rows(model):
     tok = workloads.draft_tree(BINARY, m.first, m.greedy, 2, 14, m.shape.vocab, seed=7)
     s.verify_tree(P, tok, BINARY, want_logits=False)
     torch.cuda.synchronize()
-    k0, v0 = s.k_cache[:, :, :P + n].clone(), s.v_cache[:, :, :P + n].clone()
+    k0, v0 = s.k_cache[:, :, :P + n].clone(), s.v_rows[:, :, :P + n].clone()
     s.commit(P, n)
     torch.cuda.synchronize()
     acc = int(s.accept_len.item())
@@ -97,14 +97,14 @@ def test_commit_moves_path_rows(model):
     for k in range(n):
         src = path[k] if k <= acc else k
         assert torch.equal(s.k_cache[:, :, P + k], k0[:, :, P + src]), k
-        assert torch.equal(s.v_cache[:, :, P + k], v0[:, :, P + src]), k
+        assert torch.equal(s.v_rows[:, :, P + k], v0[:, :, P + src]), k
     assert torch.equal(s.k_cache[:, :, :P], k0[:, :, :P])
-    assert torch.equal(s.v_cache[:, :, :P], v0[:, :, :P])
+    assert torch.equal(s.v_rows[:, :, :P], v0[:, :, :P])
     # the cache now holds the accepted sequence's causal keys/values
     seq = np.concatenate([m.prefix, [m.first], m.greedy[:acc]])
     rk, rv = oracle.prefill_kv(m.ow, seq, rounding=True)
     gk = s.k_cache[:, :, P:P + acc + 1].float().cpu().numpy().transpose(0, 2, 1, 3)
-    gv = s.v_cache[:, :, P:P + acc + 1].float().cpu().numpy().transpose(0, 2, 1, 3)
+    gv = s.v_rows[:, :, P:P + acc + 1].float().cpu().numpy().transpose(0, 2, 1, 3)
     for g, r in ((gk, rk[:, P:]), (gv, rv[:, P:])):
         assert np.abs(g - r).max() <= 2e-2 * np.abs(r).max()
 
@@ -176,7 +176,7 @@ def test_draft_model_loop_is_greedy(model, drafter_kind, threshold, alpha):
     if drafter_kind == "self":
         assert sum(accs) >= len(accs), accs   # self-drafting accepts on average at least one token per pass
     # the drafter's cache rows [P, plen) hold the accepted sequence's keys/values, as the target's do
-    for a, b in ((drafter.k_cache, m.sess.k_cache), (drafter.v_cache, m.sess.v_cache)):
+    for a, b in ((drafter.k_cache, m.sess.k_cache), (drafter.v_rows, m.sess.v_rows)):
         if drafter_kind == "self":
             ga = a[:, :, P:plen].float()
             gb = b[:, :, P:plen].float()

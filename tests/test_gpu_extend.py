@@ -77,7 +77,7 @@ def test_grown_tree_matches_one_pass(model, tree, cuts):
     err, rel = parity.check_logits(logits, ref, what)
     parity.check_argmax(np.argmax(logits, axis=1), ref, what)
     gk = m.sess.k_cache[:, :, P:P + n].float().cpu().numpy().transpose(0, 2, 1, 3)
-    gv = m.sess.v_cache[:, :, P:P + n].float().cpu().numpy().transpose(0, 2, 1, 3)
+    gv = m.sess.v_rows[:, :, P:P + n].float().cpu().numpy().transpose(0, 2, 1, 3)
     for g, r in ((gk, rk), (gv, rv)):
         assert np.abs(g - r).max() <= 2e-2 * np.abs(r).max()
     print(f"[{what}] {len(steps)} steps, max_abs={err:.2e} rel={rel:.2e}", flush=True)

@@ -170,15 +170,15 @@ def test_full_size_rollback():
     while sure < K and gaps[sure] > 0.2:
         sure += 1
     assert acc >= sure, (acc, gaps)
-    k0, v0 = sess.k_cache[:, :, :P + n].clone(), sess.v_cache[:, :, :P + n].clone()
+    k0, v0 = sess.k_cache[:, :, :P + n].clone(), sess.v_rows[:, :, :P + n].clone()
     sess.commit(P, n)
     torch.cuda.synchronize()
     for k in range(n):
         src = path[k] if k <= acc else k
         assert torch.equal(sess.k_cache[:, :, P + k], k0[:, :, P + src]), k
-        assert torch.equal(sess.v_cache[:, :, P + k], v0[:, :, P + src]), k
+        assert torch.equal(sess.v_rows[:, :, P + k], v0[:, :, P + src]), k
     assert torch.equal(sess.k_cache[:, :, :P], k0[:, :, :P])
-    assert torch.equal(sess.v_cache[:, :, :P], v0[:, :, :P])
+    assert torch.equal(sess.v_rows[:, :, :P], v0[:, :, :P])
     _log(f"rollback: path {path}, gaps {np.round(gaps, 3).tolist()}")
 
 
@@ -233,7 +233,7 @@ def test_full_size_end_to_end(wl_name, isolated, chain_nodes):
     t_start = time.time()
     for l in range(L):
         pk = _np64(sess.k_cache[l, :, :P]).transpose(1, 0, 2)
-        pv = _np64(sess.v_cache[l, :, :P]).transpose(1, 0, 2)
+        pv = _np64(sess.v_rows[l, :, :P]).transpose(1, 0, 2)
         # the oracle's own chains from the embedding: with the bf16 rounding
         # points, and exact
         _, x_ref, _, _ = oracle.tree_layer(ow, l, x_ref, pk, pv, parent[:m], rounding=True)
@@ -249,7 +249,7 @@ def test_full_size_end_to_end(wl_name, isolated, chain_nodes):
             a2 = _check_tensor(g_out - g_mid, x_out - x_mid, f"{wl_name} layer {l} feed-forward block")
             a3 = _check_tensor(_np64(sess.k_cache[l, :, P:P + n]).transpose(1, 0, 2), k,
                                f"{wl_name} layer {l} tree K")
-            a4 = _check_tensor(_np64(sess.v_cache[l, :, P:P + n]).transpose(1, 0, 2), v,
+            a4 = _check_tensor(_np64(sess.v_rows[l, :, P:P + n]).transpose(1, 0, 2), v,
                                f"{wl_name} layer {l} tree V")
             if l % 8 == 0 or l == L - 1 or isolated is not None:
                 _log(f"{wl_name} layer {l}: rel max/L2 attention {a1[0]:.1e}/{a1[1]:.1e} "

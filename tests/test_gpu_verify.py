@@ -104,8 +104,9 @@ def test_verify_matches_oracle(model, tree):
 def test_launch_shape_variants(model, monkeypatch):
     # One and four key splits in the attention, and smaller grids (each
     # workgroup then takes longer runs of column blocks, cut into several
-    # tiles, and with 3 workgroups the attention units take several rounds)
-    # meet the oracle bar too.
+    # tiles, and with 24 or 3 workgroups the attention units take several
+    # rounds, the later ones with nothing fetched before the barrier) meet
+    # the oracle bar too.
     parent = TREES["b432_n41"]
     tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=7)
     _check_all(model, parent, tok, "default")
@@ -118,13 +119,9 @@ def test_launch_shape_variants(model, monkeypatch):
             monkeypatch.delenv(k)
 
 
-@pytest.mark.parametrize("splits", ["default", "1", "2", "3", "4"])
-def test_long_prefix_key_splits(model, monkeypatch, splits):
-    # A 600-position prefix (four full 128-key chunks and a ragged fifth):
-    # the attention's key splits (1 to 4 per head and row block, merged in
-    # split order) all meet the oracle bar.  The prefix K/V are seeded random
-    # bf16 values written straight into the cache and handed to the oracle.
-    PL = 600
+def _long_prefix_session(model, PL):
+    """A session whose cache holds PL seeded random bf16 prefix keys/values
+    (written straight into the cache) and the oracle's copies of them."""
     shape, binding = model.shape, model.binding
     sess = binding.Session(shape, capacity=PL + 160, max_n=128)
     binding.workspace_init(sess.cfg, 128, sess.workspace)
@@ -134,7 +131,43 @@ def test_long_prefix_key_splits(model, monkeypatch, splits):
     pk = oracle.bf16_round(rng.standard_normal(dims) * 0.7)
     pv = oracle.bf16_round(rng.standard_normal(dims) * 0.7)
     sess.k_cache[:, :, :PL] = torch.from_numpy(pk.transpose(0, 2, 1, 3).astype(np.float32)).to(torch.bfloat16).cuda()
-    sess.v_cache[:, :, :PL] = torch.from_numpy(pv.transpose(0, 2, 1, 3).astype(np.float32)).to(torch.bfloat16).cuda()
+    sess.v_rows[:, :, :PL] = torch.from_numpy(pv.transpose(0, 2, 1, 3).astype(np.float32)).to(torch.bfloat16).cuda()
+    return sess, pk, pv
+
+
+@pytest.mark.parametrize("PL", [P, 600])
+def test_attention_prefetch_is_exact(model, monkeypatch, PL):
+    # The attention fetches the prefix part of its keys/values before its
+    # phase's barrier (registers, and copies to LDS made for one wave by
+    # another); fetched after the barrier instead, every output bit must be
+    # the same.  Two prefix lengths: a few steps, and several per wave.
+    sess = model.sess if PL == P else _long_prefix_session(model, PL)[0]
+    parent = TREES["b432_n41"]
+    n = len(parent)
+    tok = workloads.draw_tokens(n, model.shape.vocab, seed=19)
+    runs = []
+    for mode in ("1", "2"):
+        monkeypatch.setenv("LLMCAD_ATTN_PREFETCH", mode)
+        sess.verify_tree(PL, tok, parent)
+        logits, path, acc, nxt = sess.results(n)
+        runs.append((logits.numpy(), path, acc, nxt))
+    np.testing.assert_array_equal(runs[0][0], runs[1][0])
+    assert runs[0][1:] == runs[1][1:]
+
+
+@pytest.mark.parametrize("PL,splits", [(600, "default"), (600, "1"), (600, "2"), (600, "3"), (600, "4"),
+                                       (2100, "default"), (2100, "1")])
+def test_long_prefix_key_splits(model, monkeypatch, PL, splits):
+    # Long prefixes (600 and 2100 positions; neither a multiple of the
+    # attention's 32-key step, so one step holds prefix and tree keys): the
+    # attention's key splits (1 to 4 per head and row block, merged in split
+    # order) all meet the oracle bar, whether a split's prefix steps were all
+    # fetched before the phase's barrier or (one split over a 2100-position
+    # prefix) most of them stream in afterwards.  The prefix K/V are seeded
+    # random bf16 values written straight into the cache and handed to the
+    # oracle.
+    shape, binding = model.shape, model.binding
+    sess, pk, pv = _long_prefix_session(model, PL)
     if splits != "default":
         monkeypatch.setenv("LLMCAD_ATTN_SPLITS", splits)
     parent = TREES["b432_n41"]
@@ -165,13 +198,13 @@ def test_pass_status_ok(model):
 def test_deterministic_and_prefix_untouched(model):
     parent = TREES["random_n77"]
     tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=5)
-    before = model.sess.k_cache[:, :, :P].clone(), model.sess.v_cache[:, :, :P].clone()
+    before = model.sess.k_cache[:, :, :P].clone(), model.sess.v_rows[:, :, :P].clone()
     a = _run(model, parent, tok)
     b = _run(model, parent, tok)
     np.testing.assert_array_equal(a[0], b[0])
     assert a[1:4] == b[1:4]
     assert torch.equal(model.sess.k_cache[:, :, :P], before[0])
-    assert torch.equal(model.sess.v_cache[:, :, :P], before[1])
+    assert torch.equal(model.sess.v_rows[:, :, :P], before[1])
 
 
 def test_tree_kv_written_to_node_slots(model):
@@ -182,7 +215,7 @@ def test_tree_kv_written_to_node_slots(model):
     _, tk, tv = oracle.tree_forward(model.ow, model.ok, model.ov, tok, parent, rounding=True)
     # cache [L][H][cap][Dh] vs oracle [L][n][H][Dh]
     gk = model.sess.k_cache[:, :, P:P + n].float().cpu().numpy().transpose(0, 2, 1, 3)
-    gv = model.sess.v_cache[:, :, P:P + n].float().cpu().numpy().transpose(0, 2, 1, 3)
+    gv = model.sess.v_rows[:, :, P:P + n].float().cpu().numpy().transpose(0, 2, 1, 3)
     for g, r in ((gk, tk), (gv, tv)):
         scale = np.abs(r).max()
         assert np.abs(g - r).max() <= 2e-2 * scale
@@ -191,18 +224,18 @@ def test_tree_kv_written_to_node_slots(model):
 def test_isolated_prefix_kv(model):
     # Upload the oracle's bf16 prefix K/V instead of the GPU prefill's.
     s = model.sess
-    saved = s.k_cache[:, :, :P].clone(), s.v_cache[:, :, :P].clone()
+    saved = s.k_cache[:, :, :P].clone(), s.v_rows[:, :, :P].clone()
     try:
         s.k_cache[:, :, :P] = torch.from_numpy(model.ok.transpose(0, 2, 1, 3).astype(np.float32)).to(
             torch.bfloat16).cuda()
-        s.v_cache[:, :, :P] = torch.from_numpy(model.ov.transpose(0, 2, 1, 3).astype(np.float32)).to(
+        s.v_rows[:, :, :P] = torch.from_numpy(model.ov.transpose(0, 2, 1, 3).astype(np.float32)).to(
             torch.bfloat16).cuda()
         parent = TREES["binary_d4_n31"]
         tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=13)
         _check_all(model, parent, tok, "isolated")
     finally:
         s.k_cache[:, :, :P] = saved[0]
-        s.v_cache[:, :, :P] = saved[1]
+        s.v_rows[:, :, :P] = saved[1]
 
 
 def test_prefill_last_logits(model):
