@@ -196,8 +196,14 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   // (LLMCAD_ATTN_SPLITS, diagnostics, asks for 1 to 4).  A workgroup pulls its
   // keys and values at the rate one CU's memory path gives, so a head's keys
   // are spread over several; the splits' merge costs a hand-off through memory.
+  // Fewer splits when the (head, row block) pairs alone fill the grid: each
+  // split of a pair re-reads the keys and values the pair's other row blocks
+  // read too, and another round of units costs more than a longer unit.
   const int prefix_steps = cdiv(a.prefix_len, 32);
-  int KS = env_int("LLMCAD_ATTN_SPLITS", cdiv(prefix_steps, 4));
+  const int pairs = s.H * cdiv(a.n, 16);
+  int KS = cdiv(prefix_steps, 4);
+  if (KS > G / pairs) KS = G / pairs;
+  KS = env_int("LLMCAD_ATTN_SPLITS", KS);
   if (KS > kAttnMaxSplits) KS = kAttnMaxSplits;
   if (KS > prefix_steps) KS = prefix_steps;
   if (KS < 1) KS = 1;

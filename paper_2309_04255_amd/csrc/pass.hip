@@ -52,6 +52,23 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 
+// Tuning constants of the GEMM phases (the defaults were measured best on the
+// LLaMA-7B workload; -D overrides them for sweeps): the VGPRs (in units of 4)
+// a tile's register pipeline may hold, its depth for one-block and for wider
+// tiles, and the widest tile (in 16-column blocks) at 128 rows.
+#ifndef LLMCAD_STAGE_REGS
+#define LLMCAD_STAGE_REGS 40
+#endif
+#ifndef LLMCAD_DEPTH_ONE
+#define LLMCAD_DEPTH_ONE 8
+#endif
+#ifndef LLMCAD_DEPTH_WIDE
+#define LLMCAD_DEPTH_WIDE 4
+#endif
+#ifndef LLMCAD_TILE_BLOCKS_MB8
+#define LLMCAD_TILE_BLOCKS_MB8 3
+#endif
+
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 
 // The launch parameters, read in place from the kernel-argument segment
@@ -308,8 +325,8 @@ __device__ __forceinline__ TileIn tile_in(KParams& p, int step, int l) {
 // 3%), and a depth that divides the LDS stages lets the copy use them all.
 template <int MB, int C>
 constexpr int tile_depth() {
-  constexpr int regs = 40 / (C + MB);
-  constexpr int cap = C == 1 ? 8 : 4;
+  constexpr int regs = LLMCAD_STAGE_REGS / (C + MB);
+  constexpr int cap = C == 1 ? LLMCAD_DEPTH_ONE : LLMCAD_DEPTH_WIDE;
   constexpr int d = regs < cap ? regs : cap;
   return d < 2 ? 2 : d;
 }
@@ -559,23 +576,22 @@ __device__ __forceinline__ float rope_inv_freq(int j, int Dh, float log2_theta) 
 // squares ssq [d/16][Mp] (added in a fixed order); 0 for rows >= n.
 template <int MB>
 __device__ __forceinline__ void row_rstd(KParams& p, const float* ssq, GemmLds& gl) {
-  constexpr int ROWS = 16 * MB;
-  constexpr int CHK = 256 / ROWS;
-  const int r = threadIdx.x % ROWS, ch = threadIdx.x / ROWS;
+  // thread t: rows 4 q .. 4 q + 3 (q = t % (ROWS / 4)) of the 16-column blocks
+  // of chunk t / (ROWS / 4); 16-byte loads, a batch of them in flight at once
+  constexpr int ROWS = 16 * MB, QUADS = ROWS / 4, CHK = kThreads / QUADS, BATCH = 16;
+  const int q = threadIdx.x % QUADS, ch = threadIdx.x / QUADS;
   const int dn = p.d_nb;
   const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
-  float ss = 0.0f;
-  if (r < p.n) {
-    constexpr int PER = 32;  // (d/16 per chunk at d = 4096 and 32 rows: one round)
-    for (int t = t0; t < t1; t += PER) {
-      float v[PER];
+  f32x4 ss = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int t = t0; t < t1; t += BATCH) {
+    f32x4 v[BATCH];
 #pragma unroll
-      for (int k = 0; k < PER; ++k) v[k] = t + k < t1 ? ldg(ssq + (size_t)(t + k) * ROWS + r) : 0.0f;
+    for (int k = 0; k < BATCH; ++k)
+      v[k] = t + k < t1 ? ldg((const f32x4*)(ssq + (size_t)(t + k) * ROWS + 4 * q)) : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int k = 0; k < PER; ++k) ss += v[k];
-    }
+    for (int k = 0; k < BATCH; ++k) ss += v[k];
   }
-  gl.part_ss[ch * ROWS + r] = ss;
+  *(f32x4*)&gl.part_ss[ch * ROWS + 4 * q] = ss;
   __syncthreads();
   if (threadIdx.x < ROWS) {
     float t = 0.0f;
@@ -874,7 +890,8 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   phase = wave_uniform(phase);
   const Sync sy = make_sync(p, lds_flag);
   const StepPlan& sp = p.step[step];
-  constexpr int CM = MB <= 2 ? 8 : 16 / MB;
+  constexpr int CM = MB <= 2 ? 8 : MB == 4 ? 4 : LLMCAD_TILE_BLOCKS_MB8;
+  static_assert(wl_off(CM, MB) <= kGemmLdsBytes, "a tile's partial sums and epilogue inputs fit the LDS");
   const int nbk = sp.nblocks, G = p.G;
   const int vw = virtual_wg(G);
   const int lo = wave_uniform((int)((long)vw * nbk / G));

@@ -65,6 +65,9 @@ WORKLOADS = {
     "tiny_p32_n15": Workload("tiny_p32_n15", "tiny", 32, ("complete", (2, 2, 2))),
     "llama7b_p512_n31": Workload("llama7b_p512_n31", "llama7b", 512, ("complete", (2, 2, 2, 2))),
     "llama7b_p2048_n41": Workload("llama7b_p2048_n41", "llama7b", 2048, ("complete", (4, 3, 2))),
+    # (the 128-row pass at the 7B shape: the widest tree a pass takes, and the
+    # prefill's chunk size)
+    "llama7b_p512_n128": Workload("llama7b_p512_n128", "llama7b", 512, ("random", 128, 7)),
     "llama13b_p1024_n41": Workload("llama13b_p1024_n41", "llama13b", 1024, ("complete", (4, 3, 2))),
     "llama30b_p1024_n1": Workload("llama30b_p1024_n1", "llama30b", 1024, ("random", 1, 7)),
     "llama30b_p1024_n8": Workload("llama30b_p1024_n8", "llama30b", 1024, ("random", 8, 7)),
