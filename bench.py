@@ -41,11 +41,12 @@ def log(msg):
 
 
 def pass_bytes(shape, P, n):
-    """Algorithmic HBM bytes of one pass: every weight byte once (embedding: n
-    rows), prefix K+V read once, tree K/V written, embedding rows, fp32 logits."""
-    L, d, F, V = shape.n_layers, shape.d_model, shape.d_ffn, shape.vocab
-    weights = 2 * (L * (4 * d * d + 3 * d * F + 2 * d) + V * d + d)
-    return weights + 4 * L * P * d + 4 * L * n * d + 2 * n * d + 4 * n * V
+    """Algorithmic HBM bytes of one pass: every weight byte once (layer
+    matrices as stored: bf16, or 4-bit codes plus a bf16 scale per 128
+    inputs; norm gains, LM head), prefix K+V read once, tree K/V written,
+    the nodes' embedding rows, fp32 logits."""
+    L, d, V = shape.n_layers, shape.d_model, shape.vocab
+    return shape.weight_bytes() + 4 * L * P * d + 4 * L * n * d + 2 * n * d + 4 * n * V
 
 
 def source_hash():
@@ -145,6 +146,9 @@ def cpu_baseline(gen, shape, P, parent, tok, seed):
         threads = os.cpu_count() or 1
 
     def host64(t):
+        if isinstance(t, tuple):  # a 4-bit matrix: the oracle's dequantisation on the host
+            codes, scales = t
+            return oracle.dequantize(oracle.unpack_codes(codes.cpu().numpy()), host64(scales), 128)
         return t.double().cpu().numpy()
 
     cfg = oracle.OracleConfig(shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim, shape.d_ffn,
@@ -312,8 +316,9 @@ def setup_model(shape, capacity):
     sess = binding.Session(shape, capacity=capacity, max_n=128)
     gen = workloads.make_weights(shape, "cuda")
     binding.pack_globals(sess.cfg, gen.tok_embed(), gen.final_norm(), gen.lm_head(), sess.packed)
+    pack = binding.pack_layer_q4 if sess.cfg.weight_bits == 4 else binding.pack_layer
     for l in range(shape.n_layers):
-        binding.pack_layer(sess.cfg, l, gen.layer(l), sess.packed)
+        pack(sess.cfg, l, gen.layer(l), sess.packed)
         torch.cuda.synchronize()
         if l % 8 == 7:
             log(f"packed layer {l + 1}/{shape.n_layers}")
@@ -397,6 +402,8 @@ def measure(sess, gen, wl, args, headline):
 
     frac = B / (wall / args.steps) / HBM_PEAK
     traffic = load_traffic(wl.name)
+    q4 = ("4-bit codes, one bf16 scale per 128 inputs (GPTQ-style symmetric groups); bf16 MFMA on the codes"
+          if getattr(shape, "weight_bits", 16) == 4 else None)
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -409,11 +416,15 @@ def measure(sess, gen, wl, args, headline):
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic: random-init bf16 weights (counter-hash Irwin-Hall, std 0.02), uniform tokens",
+        "data": ("synthetic: random-init bf16 weights (counter-hash Irwin-Hall, std 0.02), uniform tokens"
+                 if q4 is None else
+                 "synthetic: random-init 4-bit layer weights (uniform codes, bf16 group scales, spread 0.02), "
+                 "bf16 embedding / LM head, uniform tokens"),
         "config": {
             "workload": wl.name,
             "shape": f"L{shape.n_layers} d{shape.d_model} H{shape.n_heads}x{shape.head_dim} "
                      f"F{shape.d_ffn} V{shape.vocab}",
+            "weights": "bf16" if q4 is None else q4,
             "prefix_len": P,
             "tree_nodes": n,
             "tree": str(wl.tree),

@@ -81,6 +81,10 @@ typedef struct llmcad_config {
   int32_t vocab;     /* V                                            */
   float rms_eps;     /* RMSNorm epsilon                              */
   float rope_theta;  /* rotary base: pair j rotates at theta^(-2j/Dh) */
+  int32_t weight_bits; /* layer matrices: 16 (or 0) = bf16; 4 = group-quantised
+                          4-bit codes (see llmcad_pack_layer_q4; d and d_ffn
+                          multiples of 128).  Embedding, LM head and norm gains
+                          are bf16 either way.                                */
 } llmcad_config;
 
 typedef struct llmcad_layer_weights {
@@ -93,7 +97,9 @@ typedef struct llmcad_layer_weights {
 } llmcad_layer_weights;
 
 /* Checks a configuration: LLMCAD_OK, LLMCAD_EARG (non-positive sizes, bad
- * eps/theta) or LLMCAD_ESHAPE (head_dim not 64/128, d != H*Dh, d % 64 != 0). */
+ * eps/theta, weight_bits not 0/16/4) or LLMCAD_ESHAPE (head_dim not 64/128,
+ * d != H*Dh, d % 64 != 0; with weight_bits 4, d or d_ffn not a multiple of
+ * 128). */
 int llmcad_check_config(const llmcad_config* cfg);
 
 /* Bytes of the packed weight image for cfg (0 if cfg is invalid). */
@@ -105,9 +111,41 @@ size_t llmcad_packed_bytes(const llmcad_config* cfg);
 int llmcad_pack_globals(const llmcad_config* cfg, const void* tok_embed, const void* final_norm,
                         const void* lm_head, void* packed, size_t packed_bytes, void* stream);
 
-/* Re-lays one layer's weights (layer in [0, L)) into the packed image. */
+/* Re-lays one layer's weights (layer in [0, L)) into the packed image
+ * (bf16 configurations; LLMCAD_EARG for weight_bits 4). */
 int llmcad_pack_layer(const llmcad_config* cfg, int32_t layer, const llmcad_layer_weights* src,
                       void* packed, size_t packed_bytes, void* stream);
+
+/*
+ * 4-bit weights (the paper's phone targets are 4-bit models quantised with
+ * AutoGPTQ, §4.1 "Models and datasets"; GPTQ's symmetric group-wise form):
+ * a matrix W[out][in] is given as codes q[out][in] in [0, 16), two per byte
+ * (input 2j in the low nibble of byte j: uint8 [out][in / 2]), and bf16
+ * scales s[out][in / 128]; the weight it stands for is
+ *     w[o][i] = s[o][i / 128] * (q[o][i] - 8).
+ * The pass multiplies the codes on the matrix cores and applies each group's
+ * scales to its partial sums (in fp32): the dequantised matrix is never
+ * formed, and only the codes and scales cross HBM.
+ */
+typedef struct llmcad_q4_matrix {
+  const void* codes;  /* device uint8 [out][in / 2] */
+  const void* scales; /* device bf16 [out][in / 128] */
+} llmcad_q4_matrix;
+
+typedef struct llmcad_q4_layer_weights {
+  const void* attn_norm;     /* device bf16 [d]          */
+  llmcad_q4_matrix w_qkv;    /* [3d][d] (rows q, k, v)    */
+  llmcad_q4_matrix w_o;      /* [d][d]                    */
+  const void* ffn_norm;      /* device bf16 [d]          */
+  llmcad_q4_matrix w_gate_up;/* [2F][d] (rows gate, up)   */
+  llmcad_q4_matrix w_down;   /* [d][F]                    */
+} llmcad_q4_layer_weights;
+
+/* Re-lays one layer's 4-bit weights (weight_bits 4 configurations only, else
+ * LLMCAD_EARG) into the packed image; the globals are packed with
+ * llmcad_pack_globals as for bf16 models. */
+int llmcad_pack_layer_q4(const llmcad_config* cfg, int32_t layer, const llmcad_q4_layer_weights* src,
+                         void* packed, size_t packed_bytes, void* stream);
 
 /* Bytes of workspace for passes of up to max_n nodes (max_n in [1, 128]) on
  * the current device (the split of the work, and so the size, depends on its

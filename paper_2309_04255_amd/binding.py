@@ -28,6 +28,7 @@ SYMBOLS = (
     "llmcad_packed_bytes",
     "llmcad_pack_globals",
     "llmcad_pack_layer",
+    "llmcad_pack_layer_q4",
     "llmcad_workspace_bytes",
     "llmcad_workspace_init",
     "llmcad_verify_tree",
@@ -54,12 +55,25 @@ class LlmcadConfig(ctypes.Structure):
         ("vocab", ctypes.c_int32),
         ("rms_eps", ctypes.c_float),
         ("rope_theta", ctypes.c_float),
+        ("weight_bits", ctypes.c_int32),
     ]
 
 
 class LlmcadLayerWeights(ctypes.Structure):
     _fields_ = [(name, ctypes.c_void_p) for name in
                 ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")]
+
+
+class LlmcadQ4Matrix(ctypes.Structure):
+    _fields_ = [("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
+
+
+class LlmcadQ4LayerWeights(ctypes.Structure):
+    _fields_ = [("attn_norm", ctypes.c_void_p), ("w_qkv", LlmcadQ4Matrix), ("w_o", LlmcadQ4Matrix),
+                ("ffn_norm", ctypes.c_void_p), ("w_gate_up", LlmcadQ4Matrix), ("w_down", LlmcadQ4Matrix)]
+
+
+Q4_GROUP = 128  # inputs per scale group of a 4-bit matrix
 
 
 class LlmcadError(RuntimeError):
@@ -98,6 +112,7 @@ def _load():
         "llmcad_packed_bytes": (SZ, [CFG]),
         "llmcad_pack_globals": (ctypes.c_int, [CFG, P, P, P, P, SZ, P]),
         "llmcad_pack_layer": (ctypes.c_int, [CFG, I32, ctypes.POINTER(LlmcadLayerWeights), P, SZ, P]),
+        "llmcad_pack_layer_q4": (ctypes.c_int, [CFG, I32, ctypes.POINTER(LlmcadQ4LayerWeights), P, SZ, P]),
         "llmcad_workspace_bytes": (SZ, [CFG, I32]),
         "llmcad_workspace_init": (ctypes.c_int, [CFG, I32, P, SZ, P]),
         "llmcad_verify_tree": (ctypes.c_int, [CFG, P, P, P, I32, I32, I32P, I32P, I32, P, P, P, P,
@@ -132,9 +147,11 @@ def status_string(status: int) -> str:
 
 
 def make_config(shape) -> LlmcadConfig:
-    """From any object with n_layers, d_model, n_heads, head_dim, d_ffn, vocab, rms_eps, rope_theta."""
+    """From any object with n_layers, d_model, n_heads, head_dim, d_ffn, vocab, rms_eps, rope_theta
+    (and optionally weight_bits: 16, the default, or 4)."""
     return LlmcadConfig(shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim, shape.d_ffn,
-                        shape.vocab, float(shape.rms_eps), float(shape.rope_theta))
+                        shape.vocab, float(shape.rms_eps), float(shape.rope_theta),
+                        int(getattr(shape, "weight_bits", 16)))
 
 
 def _ptr(t):
@@ -183,6 +200,20 @@ def pack_layer(cfg, layer: int, w: dict, packed, stream=None):
     _check(_lib.llmcad_pack_layer(ctypes.byref(cfg), int(layer), ctypes.byref(src), _ptr(packed),
                                   packed.numel() * packed.element_size(), _stream(stream)),
            "llmcad_pack_layer")
+
+
+def pack_layer_q4(cfg, layer: int, w: dict, packed, stream=None):
+    """w: attn_norm, ffn_norm (bf16 [d]) and, per matrix m in w_qkv, w_o, w_gate_up,
+    w_down, a pair (codes uint8 [out][in/2], scales bf16 [out][in/128]) on the device."""
+    def mat(k):
+        codes, scales = w[k]
+        return LlmcadQ4Matrix(codes.data_ptr(), scales.data_ptr())
+
+    src = LlmcadQ4LayerWeights(w["attn_norm"].data_ptr(), mat("w_qkv"), mat("w_o"), w["ffn_norm"].data_ptr(),
+                               mat("w_gate_up"), mat("w_down"))
+    _check(_lib.llmcad_pack_layer_q4(ctypes.byref(cfg), int(layer), ctypes.byref(src), _ptr(packed),
+                                     packed.numel() * packed.element_size(), _stream(stream)),
+           "llmcad_pack_layer_q4")
 
 
 def workspace_init(cfg, max_n: int, workspace, stream=None):
@@ -344,10 +375,12 @@ class Session:
 
     def load_weights(self, gen, layers=None):
         """Pack weights from a generator with tok_embed(), final_norm(), lm_head(), layer(l)
-        returning plain-layout bf16 tensors on this device."""
+        returning plain-layout tensors on this device (bf16 matrices, or for a
+        4-bit model (codes, scales) pairs as pack_layer_q4 takes them)."""
         pack_globals(self.cfg, gen.tok_embed(), gen.final_norm(), gen.lm_head(), self.packed)
+        q4 = self.cfg.weight_bits == 4
         for l in range(self.shape.n_layers) if layers is None else layers:
-            pack_layer(self.cfg, l, gen.layer(l), self.packed)
+            (pack_layer_q4 if q4 else pack_layer)(self.cfg, l, gen.layer(l), self.packed)
             torch.cuda.current_stream().synchronize()  # let the plain layer be freed
 
     def prefill(self, tokens, start_pos=0, want_logits=False):

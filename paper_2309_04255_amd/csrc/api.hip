@@ -42,6 +42,8 @@ int check_cfg(const llmcad_config* c) {
   if (c->d_model % 64 != 0) return LLMCAD_ESHAPE;
   if (c->n_layers > 4096 || c->d_model > 65536 || c->d_ffn > (1 << 20) || c->vocab > (1 << 24))
     return LLMCAD_ESHAPE;
+  if (c->weight_bits != 0 && c->weight_bits != 16 && c->weight_bits != 4) return LLMCAD_EARG;
+  if (c->weight_bits == 4 && (c->d_model % kQ4Group != 0 || c->d_ffn % kQ4Group != 0)) return LLMCAD_ESHAPE;
   return LLMCAD_OK;
 }
 
@@ -174,9 +176,12 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   for (int i = 0; i < kSteps; ++i) {
     StepPlan& sp = p.step[i];
     sp.nblocks = step_blocks(s, i);
-    sp.ksteps = step_ksteps(s, i);
-    sp.w_off = w_off[i];
     sp.layer_rel = i == STEP_LM ? 0 : 1;
+    sp.q4 = s.q4 && i != STEP_LM ? 1 : 0;
+    // bf16: k-steps of 32 inputs; 4-bit: scale groups of 128 inputs
+    sp.ksteps = sp.q4 ? step_groups(s, i) : step_ksteps(s, i);
+    sp.w_off = w_off[i];
+    sp.s_off = sp.q4 ? w_off[i] + (long long)q4_codes_bytes(sp.nblocks, sp.ksteps) : 0;
   }
   p.k_cache = (bf16*)a.k_cache;
   p.v_cache = (bf16*)a.v_cache;
@@ -324,7 +329,7 @@ int llmcad_pack_layer(const llmcad_config* cfg, int32_t layer, const llmcad_laye
                       void* packed, size_t packed_bytes, void* stream) {
   int rc = check_cfg(cfg);
   if (rc != LLMCAD_OK) return rc;
-  if (!src || !packed || layer < 0 || layer >= cfg->n_layers) return LLMCAD_EARG;
+  if (!src || !packed || layer < 0 || layer >= cfg->n_layers || cfg->weight_bits == 4) return LLMCAD_EARG;
   if (!src->attn_norm || !src->w_qkv || !src->w_o || !src->ffn_norm || !src->w_gate_up ||
       !src->w_down)
     return LLMCAD_EARG;
@@ -341,6 +346,40 @@ int llmcad_pack_layer(const llmcad_config* cfg, int32_t layer, const llmcad_laye
   HIP_TRY(launch_pack(src->w_gate_up, 2 * s.F, s.d, out + P.w_gate_up, s.gu_nb, s.ks_d, PACK_GATE_UP,
                       s.F, st));
   HIP_TRY(launch_pack(src->w_down, s.d, s.F, out + P.w_down, s.d_nb, s.ks_f, PACK_PLAIN, s.F, st));
+  return LLMCAD_OK;
+}
+
+int llmcad_pack_layer_q4(const llmcad_config* cfg, int32_t layer, const llmcad_q4_layer_weights* src,
+                         void* packed, size_t packed_bytes, void* stream) {
+  int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!src || !packed || layer < 0 || layer >= cfg->n_layers || cfg->weight_bits != 4) return LLMCAD_EARG;
+  const llmcad_q4_matrix* m[4] = {&src->w_qkv, &src->w_o, &src->w_gate_up, &src->w_down};
+  if (!src->attn_norm || !src->ffn_norm) return LLMCAD_EARG;
+  for (int i = 0; i < 4; ++i)
+    if (!m[i]->codes || !m[i]->scales) return LLMCAD_EARG;
+  const Shape s(*cfg);
+  const PackedLayout P(s);
+  if (packed_bytes < P.total) return LLMCAD_EWORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  char* out = (char*)packed + P.layer(layer);
+  HIP_TRY(hipMemcpyAsync(out + P.attn_norm, src->attn_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(out + P.ffn_norm, src->ffn_norm, (size_t)s.d * 2, hipMemcpyDeviceToDevice, st));
+  // (N rows, K inputs, blocks, groups, column order, its parameter, offset)
+  struct Mat {
+    int N, K, nb, gs, kind, aux;
+    size_t off;
+  } mats[4] = {
+      {3 * s.d, s.d, s.qkv_nb, s.gs_d, PACK_QKV_ROPE, s.Dh, P.w_qkv},
+      {s.d, s.d, s.d_nb, s.gs_d, PACK_PLAIN, s.F, P.w_o},
+      {2 * s.F, s.d, s.gu_nb, s.gs_d, PACK_GATE_UP, s.F, P.w_gate_up},
+      {s.d, s.F, s.d_nb, s.gs_f, PACK_PLAIN, s.F, P.w_down},
+  };
+  for (int i = 0; i < 4; ++i) {
+    const Mat& q = mats[i];
+    HIP_TRY(launch_pack_q4(m[i]->codes, m[i]->scales, q.N, q.K, out + q.off, out + q.off + q4_codes_bytes(q.nb, q.gs),
+                           q.nb, q.gs, q.kind, q.aux, st));
+  }
   return LLMCAD_OK;
 }
 

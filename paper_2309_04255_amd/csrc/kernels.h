@@ -16,6 +16,10 @@ namespace llmcad {
 enum PackKind { PACK_PLAIN = 0, PACK_GATE_UP = 1, PACK_QKV_ROPE = 2 };
 hipError_t launch_pack(const void* w, int N, int K, void* out, int nblocks, int ksteps, int kind,
                        int aux, hipStream_t st);
+// 4-bit matrix: codes uint8 [N][K/2] and bf16 scales [N][K/128] -> packed
+// codes [nblocks][groups] x 1 KiB and packed scales [nblocks][groups][16].
+hipError_t launch_pack_q4(const void* codes, const void* scales, int N, int K, void* out_codes, void* out_scales,
+                          int nblocks, int groups, int kind, int aux, hipStream_t st);
 
 // ---- rollback to the verified sequence (commit.hip): for each of the
 // layers_heads (layer, head) row sets of the cache, slot prefix_len + path[k]
@@ -36,9 +40,11 @@ constexpr int kPassMagic = 0x4c4d4342;
 
 // One GEMM step's shape and where its weights live.
 struct StepPlan {
-  int nblocks, ksteps;  // 16-column blocks, 32-input k-steps
-  long long w_off;      // packed matrix: offset from the packed image (globals) or the layer start
+  int nblocks, ksteps;  // 16-column blocks; 32-input k-steps (4-bit: 128-input scale groups)
+  long long w_off;      // packed matrix (4-bit: its codes): offset from the packed image (globals) or the layer start
+  long long s_off;      // 4-bit: the packed scales, offset as w_off
   int layer_rel;        // 1 if w_off is relative to the layer's start
+  int q4;               // 1: 4-bit codes with group scales
 };
 
 // Must stay the first kernel argument of the pass kernel.

@@ -15,6 +15,12 @@ namespace llmcad {
 constexpr int kNB = 16;                        // output columns per block
 constexpr int kStepK = 32;                     // inputs per k-step
 constexpr int kBlockBytes = kNB * kStepK * 2;  // 1 KiB
+// Group-quantised 4-bit weights: one scale per output column and group of
+// kQ4Group inputs; a packed group of one 16-column block is 1 KiB of codes
+// (16 columns x 128 inputs x 4 bits) plus its 16 bf16 scales.
+constexpr int kQ4Group = 128;
+constexpr int kQ4BlockBytes = kNB * kQ4Group / 2;  // 1 KiB
+constexpr int kQ4ScaleBytes = kNB * 2;
 constexpr int kMaxNodes = LLMCAD_MAX_NODES;
 constexpr int kAttnMaxSplits = 4;   // key splits per (head, 16-row block)
 constexpr int kPassMaxGrid = 1024;  // workgroups of the pass
@@ -46,15 +52,20 @@ inline int tile_max_blocks(int mb16) { return mb16 <= 2 ? 8 : 16 / mb16; }
 
 struct Shape {
   int L, d, H, Dh, F, V;
+  bool q4;     // layer matrices group-quantised to 4 bits (embedding, LM head and norms bf16)
   int Fp;      // F rounded up to 32 (SwiGLU width as stored; K of the down projection)
   int qkv_nb;  // column blocks of the QKV projection (3d / 16)
   int d_nb;    // column blocks of the O and down projections (d / 16)
   int gu_nb;   // column blocks of gate/up: each holds 8 gate and the matching 8 up columns (Fp / 8)
   int v_nb;    // column blocks of the LM head (V / 16 rounded up)
   int ks_d, ks_f;  // k-steps over d and over Fp
+  int gs_d, gs_f;  // 4-bit weights: scale groups over d and over Fp
   explicit Shape(const llmcad_config& c)
-      : L(c.n_layers), d(c.d_model), H(c.n_heads), Dh(c.head_dim), F(c.d_ffn), V(c.vocab) {
+      : L(c.n_layers), d(c.d_model), H(c.n_heads), Dh(c.head_dim), F(c.d_ffn), V(c.vocab),
+        q4(c.weight_bits == 4) {
     Fp = round_up(F, kStepK);
+    gs_d = d / kQ4Group;
+    gs_f = Fp / kQ4Group;
     qkv_nb = 3 * d / kNB;
     d_nb = d / kNB;
     gu_nb = Fp / 8;
@@ -66,6 +77,11 @@ struct Shape {
 
 inline size_t packed_matrix_bytes(int nblocks, int ksteps) {
   return (size_t)nblocks * (size_t)ksteps * kBlockBytes;
+}
+// A 4-bit matrix: codes [nblocks][groups] x 1 KiB, then scales [nblocks][groups][16] bf16.
+inline size_t q4_codes_bytes(int nblocks, int groups) { return (size_t)nblocks * groups * kQ4BlockBytes; }
+inline size_t q4_matrix_bytes(int nblocks, int groups) {
+  return q4_codes_bytes(nblocks, groups) + (size_t)nblocks * groups * kQ4ScaleBytes;
 }
 
 // Byte offsets inside the packed image.
@@ -84,19 +100,21 @@ struct PackedLayout {
     lm_head = o;
     o = align_up(o + packed_matrix_bytes(s.v_nb, s.ks_d), 4096);
     globals_end = o;
+    // a layer matrix of nb blocks over K = 32 ks inputs, bf16 or 4-bit
+    auto mat = [&](int nb, int ks, int gs) { return s.q4 ? q4_matrix_bytes(nb, gs) : packed_matrix_bytes(nb, ks); };
     size_t p = 0;
     attn_norm = p;
     p = align_up(p + (size_t)s.d * 2, 4096);
     w_qkv = p;
-    p = align_up(p + packed_matrix_bytes(s.qkv_nb, s.ks_d), 4096);
+    p = align_up(p + mat(s.qkv_nb, s.ks_d, s.gs_d), 4096);
     w_o = p;
-    p = align_up(p + packed_matrix_bytes(s.d_nb, s.ks_d), 4096);
+    p = align_up(p + mat(s.d_nb, s.ks_d, s.gs_d), 4096);
     ffn_norm = p;
     p = align_up(p + (size_t)s.d * 2, 4096);
     w_gate_up = p;
-    p = align_up(p + packed_matrix_bytes(s.gu_nb, s.ks_d), 4096);
+    p = align_up(p + mat(s.gu_nb, s.ks_d, s.gs_d), 4096);
     w_down = p;
-    p = align_up(p + packed_matrix_bytes(s.d_nb, s.ks_f), 4096);
+    p = align_up(p + mat(s.d_nb, s.ks_f, s.gs_f), 4096);
     layer_bytes = p;
     total = globals_end + (size_t)s.L * layer_bytes;
   }
@@ -119,6 +137,8 @@ inline int step_blocks(const Shape& s, int step) {
   }
 }
 inline int step_ksteps(const Shape& s, int step) { return step == STEP_DOWN ? s.ks_f : s.ks_d; }
+// 4-bit layer steps: scale groups over K (the LM head stays bf16)
+inline int step_groups(const Shape& s, int step) { return step == STEP_DOWN ? s.gs_f : s.gs_d; }
 
 // Byte offsets inside a workspace sized for passes of up to max_n nodes on
 // a device with G workgroups (row count Mp = pass_rows(max_n)).  Buffers

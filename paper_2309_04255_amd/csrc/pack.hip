@@ -61,6 +61,51 @@ __global__ void pack_kernel(const bf16* __restrict__ w, int N, int K, bf16x8* __
   }
 }
 
+// 4-bit matrices.  Packed codes: block-major, (block nb, group g) is 1 KiB
+// at ((nb * groups + g) KiB); lane l's 16 bytes hold column col(16 nb + l % 16)
+// for the group's four 32-input k-steps t, one dword each, inputs
+// 128 g + 32 t + 8 (l / 16) + e, e = 0..7: code e = 2 p sits in bits
+// [4 p, 4 p + 4), code e = 2 p + 1 in bits [16 + 4 p, 20 + 4 p), so that
+// (dword >> 4 p) & 0x000F000F, ORed with the bf16 pattern of 128, is the pair
+// (128 + q_2p, 128 + q_2p+1) as two bf16 values.  Packed scales: (nb, g) holds
+// 16 bf16, column order as the codes.  Absent columns get code 8 and scale 0.
+__global__ void pack_q4_kernel(const uint8_t* __restrict__ codes, const bf16* __restrict__ scales, int N, int K,
+                               uint32_t* __restrict__ out_codes, bf16* __restrict__ out_scales, long total_lanes,
+                               int groups, int kind, int aux) {
+  for (long ch = blockIdx.x * (long)blockDim.x + threadIdx.x; ch < total_lanes;
+       ch += (long)gridDim.x * blockDim.x) {
+    const int lane = (int)(ch % 64);
+    const long blk = ch / 64;  // nb * groups + g
+    const int g = (int)(blk % groups);
+    const int nb = (int)(blk / groups);
+    const int row = packed_col_to_row(kNB * nb + lane % 16, N, kind, aux);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      uint32_t word = 0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int k = kQ4Group * g + kStepK * t + 8 * (lane / 16) + e;
+        uint32_t q = 8;
+        if (row >= 0 && k < K) q = (codes[(long)row * (K / 2) + k / 2] >> (4 * (k & 1))) & 0xF;
+        word |= q << ((e & 1) ? 16 + 4 * (e / 2) : 4 * (e / 2));
+      }
+      out_codes[ch * 4 + t] = word;
+    }
+    if (lane < kNB) out_scales[blk * kNB + lane] = row >= 0 ? scales[(long)row * (K / kQ4Group) + g] : (bf16)0.0f;
+  }
+}
+
+hipError_t launch_pack_q4(const void* codes, const void* scales, int N, int K, void* out_codes, void* out_scales,
+                          int nblocks, int groups, int kind, int aux, hipStream_t st) {
+  const long total = (long)nblocks * groups * 64;
+  long blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  pack_q4_kernel<<<dim3((unsigned)blocks), dim3(256), 0, st>>>((const uint8_t*)codes, (const bf16*)scales, N, K,
+                                                                (uint32_t*)out_codes, (bf16*)out_scales, total,
+                                                                groups, kind, aux);
+  return hipGetLastError();
+}
+
 hipError_t launch_pack(const void* w, int N, int K, void* out, int nblocks, int ksteps, int kind,
                        int aux, hipStream_t st) {
   const long total = (long)nblocks * ksteps * 64;

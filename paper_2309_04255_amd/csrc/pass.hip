@@ -283,7 +283,8 @@ __device__ __forceinline__ StepIo step_io(KParams& p, int step, int l) {
 // What a tile's main loop reads, with every field assigned for every step
 // (branch-free selects: the compiler keeps this in registers).
 struct TileIn {
-  const bf16x8* w;     // packed matrix
+  const bf16x8* w;     // packed matrix (4-bit: its codes)
+  const uint16_t* sc;  // 4-bit: its packed scales (bf16 bits)
   const bf16x8* a;     // fragment-order activations
   const float* ssq;    // norm steps: [d/16][Mp] sums of squares; else null
   const float* x_in;   // residual steps: [Mp][d]; else null
@@ -298,6 +299,7 @@ __device__ __forceinline__ TileIn tile_in(KParams& p, int step, int l) {
   const StepPlan& sp = p.step[step];
   TileIn t;
   t.w = (const bf16x8*)((sp.layer_rel ? lw : p.packed) + sp.w_off);
+  t.sc = (const uint16_t*)((sp.layer_rel ? lw : p.packed) + sp.s_off);
   t.ks = sp.ksteps;
   t.resid = step == STEP_O || step == STEP_DOWN;
   t.norm = step == STEP_QKV || step == STEP_GATE_UP;
@@ -550,6 +552,219 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
       lds_st<f32x4>(lds + tw_off() + ((size_t)((wave * C + c) * MB + rb) * 64 + lane) * 16, acc[rb][c]);
   __syncthreads();
   return true;
+}
+
+// ---- 4-bit weights
+
+// The B operand of one k-step from its dword of packed codes (see pack.hip):
+// the bf16 values 128 + q_e, formed by placing each code in the low mantissa
+// bits of 128 (exact: 128 + q < 256 has 8 significant bits).
+__device__ __forceinline__ bf16x8 q4_operand(uint32_t w) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 v;
+#pragma unroll
+  for (int p2 = 0; p2 < 4; ++p2) v[p2] = ((w >> (4 * p2)) & 0x000F000Fu) | 0x43004300u;
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// 4-bit tile: blocks [nb0, nb0 + C) of a layer step over all its scale
+// groups (128 inputs, four k-steps each), waves taking interleaved groups.
+// Per group the codes enter the matrix cores as 128 + q, and a product with
+// a constant operand of 136 = 128 + 8 gives 136 times the group's sum of
+// activations per row; their difference is sum_k (q_k - 8) a_k exactly as
+// fp32 sums, and the column's scale multiplies it into the accumulator --
+// w = s (q - 8) is never formed.  Structure as tile_compute (weight stages
+// before the barrier, epilogue inputs parked in LDS by the last wave, partial
+// tiles to LDS at the end), with register stages only.
+template <int MB, int C>
+__device__ __attribute__((noinline, not_tail_called)) bool tile_compute_q4(KParams& pin, int step, int layer,
+                                                                          int nb0, int wait_phase, char* lds,
+                                                                          GemmLds& gl, int* lds_flag) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  KParams& p = uniform_params(pin);
+  step = wave_uniform(step);
+  layer = wave_uniform(layer);
+  nb0 = wave_uniform(nb0);
+  wait_phase = wave_uniform(wait_phase);
+  const TileIn io = tile_in(p, step, layer);
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  const int gs = io.ks;  // scale groups
+  const int ns = wave_uniform(wave < gs ? (gs - wave + kWaves - 1) / kWaves : 0);
+  constexpr int D = 2;
+  // this wave's groups: wave + 4 i
+  const u32x4* wt = (const u32x4*)io.w + ((size_t)nb0 * gs + wave) * 64 + lane;
+  const size_t cstride = (size_t)gs * 64;
+  const uint16_t* st = io.sc + ((size_t)nb0 * gs + wave) * kNB + (lane & 15);
+  const size_t sstride = (size_t)gs * kNB;
+  const bf16x8* at = io.a + (size_t)wave * 4 * MB * 64 + lane;
+  const u32x4* zero_w = (const u32x4*)p.zero + lane;
+  const uint16_t* zero_s = (const uint16_t*)p.zero;
+  const bf16x8* zero = (const bf16x8*)p.zero + lane;
+  const f32x4* zero4 = (const f32x4*)p.zero + lane;
+  u32x4 bw[D][C];
+  uint32_t bs[D][C];
+  bf16x8 ba[D][4][MB];
+  auto load_w = [&](int slot, int i) {  // group i of this wave, or the zero line past the last
+    const bool live = i < ns;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      bw[slot][c] = __builtin_nontemporal_load(
+          (const LLMCAD_GLOBAL u32x4*)opaque(live ? wt + c * cstride + (size_t)(kWaves * i) * 64 : zero_w));
+      bs[slot][c] = ldg(opaque(live ? st + c * sstride + (size_t)(kWaves * i) * kNB : zero_s));
+    }
+  };
+  auto load_a = [&](int slot, int i) {
+    const bool live = i < ns;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb)
+        ba[slot][t][rb] = ldg(opaque(live ? at + ((size_t)kWaves * 4 * i * MB + t * MB + rb) * 64 : zero));
+  };
+  // Epilogue inputs, by the last wave before the barrier (as tile_compute).
+  constexpr int KU = C * MB;
+  constexpr int kEpiWave = kWaves - 1;
+  if (wave == kEpiWave) {
+    f32x4 sx[KU], sg[C];
+    const bool resid = io.resid;
+#pragma unroll
+    for (int u = 0; u < KU; ++u) {
+      const int c = u / MB, rb = u % MB;
+      const int col0 = kNB * (nb0 + c);
+      const f32x4* src = zero4;
+      if (resid) {
+        src = (const f32x4*)(io.x_in + (size_t)(16 * rb + (lane >> 2)) * p.d + col0 + 4 * (lane & 3));
+      } else if (step == STEP_QKV && col0 < 2 * p.d) {
+        const int t = (col0 % p.d % p.Dh) / kNB;
+        src = (const f32x4*)(p.rope + ((size_t)(16 * rb + (lane >> 2)) * (p.Dh / 2) + 8 * t + 2 * (lane & 3)) * 2);
+      }
+      sx[u] = ldg(opaque(src));
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+      sg[c] = ldg(opaque(resid ? (const f32x4*)(io.g_next + kNB * (nb0 + c) + 8 * (lane & 1)) : zero4));
+#pragma unroll
+    for (int u = 0; u < KU; ++u) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)u * 1024 + lane * 16, sx[u]);
+#pragma unroll
+    for (int c = 0; c < C; ++c) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)(C * MB + c) * 1024 + lane * 16, sg[c]);
+  }
+  if (wave != 0) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) load_w(u, u);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if (wait_phase >= 0) {
+    const Sync sy = make_sync(p, lds_flag);
+    trace_mark(sy, wait_phase, 0);
+    if (!grid_wait(sy, wait_phase, p.G)) return false;
+    trace_mark(sy, wait_phase, 1);
+  }
+  constexpr bool SSQR = MB <= 2;
+  constexpr int SSQN = SSQR ? 8 : 1;
+  f32x4 sr[SSQN];
+  if constexpr (SSQR) {
+    constexpr int QUADS = 4 * MB, CH = 256 / QUADS;
+    const int q = threadIdx.x % QUADS, ch = threadIdx.x / QUADS;
+    const int t0 = ch * p.d_nb / CH, t1 = (ch + 1) * p.d_nb / CH;
+    const bool on = io.norm && p.ssq_regs;
+#pragma unroll
+    for (int k = 0; k < SSQN; ++k)
+      sr[k] = ldg(opaque(on && t0 + k < t1 ? (const f32x4*)(io.ssq + (size_t)(t0 + k) * (16 * MB) + 4 * q) : zero4));
+  }
+#pragma unroll
+  for (int u = 0; u < D; ++u) load_a(u, u);
+  __builtin_amdgcn_s_waitcnt(0);
+  lds_barrier();
+  if (wave == 0) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) load_w(u, u);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if (wait_phase >= 0 && p.trace != nullptr && threadIdx.x == 0)
+    stg(p.trace + (size_t)blockIdx.x * pass_phases(p.L) * 8 + wait_phase * 8 + 3, (long long)wall_clock64());
+
+  f32x4 acc[MB][C];
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 c136;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) c136[e] = (bf16)136.0f;
+  auto group = [&](int u) {  // the group in stage u, into acc
+    f32x4 tmp[MB][C], corr[MB];
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) {
+      corr[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < C; ++c) tmp[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      bf16x8 b[C];
+#pragma unroll
+      for (int c = 0; c < C; ++c) b[c] = q4_operand(bw[u][c][t]);
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) tmp[rb][c] = mfma16x16x32(ba[u][t][rb], b[c], tmp[rb][c]);
+        corr[rb] = mfma16x16x32(ba[u][t][rb], c136, corr[rb]);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const float sc = __uint_as_float((bs[u][c] & 0xFFFFu) << 16);  // the column's bf16 scale
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) acc[rb][c] += sc * (tmp[rb][c] - corr[rb]);
+    }
+  };
+  int i = 0;
+  for (; i + D < ns; i += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      __builtin_amdgcn_sched_barrier(0);
+      group(u);
+      __builtin_amdgcn_sched_barrier(0);
+      load_w(u, i + u + D);
+      load_a(u, i + u + D);
+    }
+  }
+  if (i < ns) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      __builtin_amdgcn_sched_barrier(0);
+      group(u);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (SSQR) {
+    if (io.norm && p.ssq_regs) {
+      constexpr int QUADS = 4 * MB;
+      const int q = threadIdx.x % QUADS, ch = threadIdx.x / QUADS;
+      f32x4 t = sr[0];
+#pragma unroll
+      for (int k = 1; k < SSQN; ++k) t += sr[k];
+      *(f32x4*)&gl.part_ss[ch * 16 * MB + 4 * q] = t;
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb)
+      lds_st<f32x4>(lds + tw_off() + ((size_t)((wave * C + c) * MB + rb) * 64 + lane) * 16, acc[rb][c]);
+  __syncthreads();
+  return true;
+}
+
+template <int MB, int C>
+__device__ __forceinline__ bool tile_dispatch_q4(int cw, KParams& p, int step, int layer, int nb0, int wait_phase,
+                                                 char* lds, GemmLds& gl, int* flag) {
+  if constexpr (C >= 1) {
+    if (cw == C) return tile_compute_q4<MB, C>(p, step, layer, nb0, wait_phase, lds, gl, flag);
+    return tile_dispatch_q4<MB, C - 1>(cw, p, step, layer, nb0, wait_phase, lds, gl, flag);
+  } else {
+    return false;
+  }
 }
 
 template <int MB, int C>
@@ -892,6 +1107,10 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   const StepPlan& sp = p.step[step];
   constexpr int CM = MB <= 2 ? 8 : MB == 4 ? 4 : LLMCAD_TILE_BLOCKS_MB8;
   static_assert(wl_off(CM, MB) <= kGemmLdsBytes, "a tile's partial sums and epilogue inputs fit the LDS");
+  // 4-bit tiles hold a second set of accumulators (each group's partial sums)
+  constexpr int CMQ = MB <= 2 ? 6 : MB == 4 ? 2 : 1;
+  const bool q4 = wave_uniform(sp.q4) != 0;
+  const int cm = q4 ? CMQ : CM;
   const int nbk = sp.nblocks, G = p.G;
   const int vw = virtual_wg(G);
   const int lo = wave_uniform((int)((long)vw * nbk / G));
@@ -909,10 +1128,12 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
     if (!grid_wait(sy, phase, G)) return false;
     trace_mark(sy, phase, 1);
   }
-  for (int b0 = lo; b0 < hi; b0 += CM) {
-    const int cw = hi - b0 < CM ? hi - b0 : CM;
+  for (int b0 = lo; b0 < hi; b0 += cm) {
+    const int cw = hi - b0 < cm ? hi - b0 : cm;
     const bool first = b0 == lo;
-    if (!tile_dispatch<MB, CM>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag)) return false;
+    const bool ok = q4 ? tile_dispatch_q4<MB, CMQ>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag)
+                       : tile_dispatch<MB, CM>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag);
+    if (!ok) return false;
     if (first) trace_mark(sy, phase, 4);
     finish_tile<MB, EPI>(p, step, layer, b0, cw, lds, gl);
   }

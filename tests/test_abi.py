@@ -51,6 +51,58 @@ def test_config_checks(binding):
     assert binding.lib().llmcad_check_config(None) == binding.EARG
 
 
+def test_q4_config_checks(binding):
+    s = workloads.MODELS["llama7b_q4"]
+    cfg = binding.make_config(s)
+    assert cfg.weight_bits == 4 and binding.check_config(cfg) == binding.OK
+    for bits, want in ((0, binding.OK), (16, binding.OK), (8, binding.EARG), (-4, binding.EARG)):
+        c = binding.make_config(s)
+        c.weight_bits = bits
+        assert binding.check_config(c) == want, bits
+    # the scale groups need d and F in multiples of 128
+    c = binding.make_config(s)
+    c.d_ffn = 11000
+    assert binding.check_config(c) == binding.ESHAPE
+    c.weight_bits = 16
+    assert binding.check_config(c) == binding.OK
+    c = binding.make_config(workloads.MODELS["tiny"])  # d = 256, F = 688
+    c.weight_bits = 4
+    assert binding.check_config(c) == binding.ESHAPE
+
+
+def test_q4_sizes(binding):
+    # the packed image holds codes (half a byte per weight) and one bf16
+    # scale per 16 columns and group of 128 inputs, padded to whole blocks;
+    # the globals are bf16 as in the bf16 models (weight_bytes counts what a
+    # pass reads, so the embedding table is added here)
+    s = workloads.MODELS["llama7b_q4"]
+    pb = binding.packed_bytes(binding.make_config(s))
+    held = s.weight_bytes() + 2 * s.vocab * s.d_model
+    assert held <= pb <= held * 1.002
+    b16 = binding.packed_bytes(binding.make_config(workloads.MODELS["llama7b"]))
+    assert pb < 0.3 * b16
+
+
+def test_q4_pack_validation(binding):
+    lib = binding.lib()
+    fake = ctypes.c_void_p(0x1000)
+    q = binding.LlmcadQ4Matrix(fake.value, fake.value)
+    src = binding.LlmcadQ4LayerWeights(fake.value, q, q, fake.value, q, q)
+    cfg = binding.make_config(workloads.MODELS["q4small"])
+    pb = binding.packed_bytes(cfg)
+    # a bf16 configuration does not take 4-bit layers, nor a 4-bit one bf16 layers
+    c16 = binding.make_config(workloads.MODELS["q4small"])
+    c16.weight_bits = 16
+    assert lib.llmcad_pack_layer_q4(ctypes.byref(c16), 0, ctypes.byref(src), fake, pb, None) == binding.EARG
+    plain = binding.LlmcadLayerWeights(*([fake.value] * 6))
+    assert lib.llmcad_pack_layer(ctypes.byref(cfg), 0, ctypes.byref(plain), fake, pb, None) == binding.EARG
+    assert lib.llmcad_pack_layer_q4(ctypes.byref(cfg), 2, ctypes.byref(src), fake, pb, None) == binding.EARG
+    assert lib.llmcad_pack_layer_q4(ctypes.byref(cfg), 0, None, fake, pb, None) == binding.EARG
+    missing = binding.LlmcadQ4LayerWeights(fake.value, q, binding.LlmcadQ4Matrix(fake.value, None), fake.value, q, q)
+    assert lib.llmcad_pack_layer_q4(ctypes.byref(cfg), 0, ctypes.byref(missing), fake, pb, None) == binding.EARG
+    assert lib.llmcad_pack_layer_q4(ctypes.byref(cfg), 0, ctypes.byref(src), fake, pb - 1, None) == binding.EWORKSPACE
+
+
 def test_sizes(binding):
     s = workloads.MODELS["llama7b"]
     cfg = binding.make_config(s)

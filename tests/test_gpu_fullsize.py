@@ -2,7 +2,7 @@
 bench times (all workgroups, default key splits).
 
 End to end: for every full-size workload (7B with P = 512, n = 31, the bench's
-workload; 7B with P = 2048, n = 41; 13B with P = 1024, n = 41; 30B with
+workload, with bf16 and with 4-bit weights; 7B with P = 2048, n = 41; 13B with P = 1024, n = 41; 30B with
 P = 1024, n = 1, 8, 32, 128) the oracle runs the whole masked pass over all L
 layers from the nodes' embedding rows -- its own residual streams, never the
 GPU's -- once with the bf16 rounding points and once exactly (float64, no
@@ -27,6 +27,8 @@ Weights: the seeded generator runs in torch on the GPU (its values equal the
 CPU run's bit for bit, which test_gpu_verify checks); each layer is widened
 to float64 on the GPU (exact) and copied into reused pinned host buffers, one
 layer at a time, so the float64 oracle runs the 30B shape without holding it.
+A 4-bit layer's codes and scales go to the host as they are, and the
+oracle's dequantisation makes its float64 matrices there.
 
 Bars: logits as everywhere (max abs 2e-2, relative L2 1e-2); a block's
 contribution or a K/V slice: max |gpu - oracle| <= 2e-2 max |oracle| and
@@ -56,6 +58,7 @@ pytestmark = pytest.mark.gpu
 #  the LM head).
 CASES = [
     ("llama7b_p512_n31", None, None),
+    ("llama7b_q4_p512_n31", None, None),
     ("llama7b_p2048_n41", (0, 31), None),
     ("llama13b_p1024_n41", (0, 39), None),
     ("llama30b_p1024_n1", (0, 59), None),
@@ -89,9 +92,16 @@ class HostLayers:
         buf.copy_(t)
         return buf.numpy()
 
+    def _dequant(self, pair):
+        # a 4-bit matrix: its codes and scales to the host, and the oracle's
+        # dequantisation there
+        codes, scales = pair
+        return oracle.dequantize(oracle.unpack_codes(codes.cpu().numpy()), _np64(scales), 128)
+
     def __call__(self, l):
         if self.l != l:
-            self.arrays = {k: self._host(k, v) for k, v in self.gen.layer(l).items()}
+            self.arrays = {k: self._dequant(v) if isinstance(v, tuple) else self._host(k, v)
+                           for k, v in self.gen.layer(l).items()}
             self.l = l
         return self.arrays
 

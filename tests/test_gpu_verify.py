@@ -1,8 +1,10 @@
 """GPU parity of the HIP verification pass against the oracle (through the C ABI).
 
-Models: the tiny 2-layer shape (head_dim 64, F = 688 not a multiple of 32) and a
+Models: the tiny 2-layer shape (head_dim 64, F = 688 not a multiple of 32), a
 small head_dim-128 shape with ragged F and V (V = 1998 leaves a partial
-16-column block of the LM head).  Norm gains are jittered so that the gain path is exercised.
+16-column block of the LM head), and a small 4-bit model (group-quantised
+layer matrices, 4 to 11 scale groups per row; the oracle runs on the weights
+the codes and scales stand for).  Norm gains are jittered so that the gain path is exercised.
 Trees span one to eight 16-row blocks with ragged tails (n = 1 ... 128), and
 the prefix (100) is not a multiple of the 64-position attention chunk.
 """
@@ -25,6 +27,7 @@ P = 100
 SHAPES = {
     "tiny": workloads.MODELS["tiny"],
     "small128": workloads.ModelShape("small128", 2, 512, 4, 128, 1000, 1998, seed=0x5EED0128),
+    "q4small": workloads.MODELS["q4small"],
 }
 TREES = {
     "single": workloads.chain_tree(1),
@@ -91,7 +94,9 @@ def test_weights_identical_on_cpu_and_gpu(model):
     cpu = workloads.make_weights(model.shape, "cpu", gain_jitter=0.1).layer(1)
     gpu = model.gen.layer(1)
     for k in cpu:
-        assert torch.equal(cpu[k], gpu[k].cpu()), k
+        pairs = zip(cpu[k], gpu[k]) if isinstance(cpu[k], tuple) else [(cpu[k], gpu[k])]
+        for c, g in pairs:
+            assert torch.equal(c, g.cpu()), k
 
 
 @pytest.mark.parametrize("tree", list(TREES))

@@ -17,11 +17,19 @@ def to_np(t):
     return t.float().cpu().numpy().astype(np.float64)
 
 
+def host_matrix(v):
+    """float64 host copy of a plain weight, or the matrix a 4-bit (codes, scales) pair stands for."""
+    if isinstance(v, tuple):
+        codes, scales = v
+        return oracle.dequantize(oracle.unpack_codes(codes.cpu().numpy()), to_np(scales), 128)
+    return to_np(v)
+
+
 def oracle_weights(shape, gain_jitter=0.0, cache=True) -> oracle.OracleWeights:
     gen = workloads.make_weights(shape, "cpu", gain_jitter)
 
     def layer_fn(l):
-        return {k: to_np(v) for k, v in gen.layer(l).items()}
+        return {k: host_matrix(v) for k, v in gen.layer(l).items()}
 
     return oracle.OracleWeights(oracle_config(shape), to_np(gen.tok_embed()),
                                 to_np(gen.final_norm()), to_np(gen.lm_head()), layer_fn, cache=cache)

@@ -24,10 +24,20 @@ class ModelShape:
     rope_theta: float = 10000.0
     weight_std: float = 0.02
     seed: int = 0
+    weight_bits: int = 16  # layer matrices: 16 = bf16, 4 = 4-bit codes with a bf16 scale per 128 inputs
 
     def params(self) -> int:
         d, f, v, l = self.d_model, self.d_ffn, self.vocab, self.n_layers
         return l * (4 * d * d + 3 * d * f + 2 * d) + 2 * v * d + d
+
+    def weight_bytes(self) -> int:
+        """Bytes of every weight a pass reads once: the layer matrices (bf16,
+        or 4-bit codes plus one bf16 scale per 128 inputs), the norm gains and
+        the LM head; the embedding contributes only its gathered rows."""
+        d, f, v, l = self.d_model, self.d_ffn, self.vocab, self.n_layers
+        mats = 4 * d * d + 3 * d * f
+        per_mat = 2 * mats if self.weight_bits == 16 else mats // 2 + 2 * (mats // 128)
+        return l * (per_mat + 2 * 2 * d) + 2 * v * d + 2 * d
 
 
 MODELS = {
@@ -35,6 +45,11 @@ MODELS = {
     "llama7b": ModelShape("llama7b", 32, 4096, 32, 128, 11008, 32000, seed=0x5EED0007),
     "llama13b": ModelShape("llama13b", 40, 5120, 40, 128, 13824, 32000, seed=0x5EED0013),
     "llama30b": ModelShape("llama30b", 60, 6656, 52, 128, 17920, 32000, seed=0x5EED0030),
+    # 4-bit weight-only targets (the paper's phone models are INT4, §4.1).  The
+    # small one has a ragged vocabulary (not a multiple of 16) and more than
+    # one scale group per matrix row everywhere.
+    "q4small": ModelShape("q4small", 2, 512, 4, 128, 1408, 1998, seed=0x5EED0104, weight_bits=4),
+    "llama7b_q4": ModelShape("llama7b_q4", 32, 4096, 32, 128, 11008, 32000, seed=0x5EED0074, weight_bits=4),
 }
 
 
@@ -69,6 +84,8 @@ WORKLOADS = {
     # prefill's chunk size)
     "llama7b_p512_n128": Workload("llama7b_p512_n128", "llama7b", 512, ("random", 128, 7)),
     "llama13b_p1024_n41": Workload("llama13b_p1024_n41", "llama13b", 1024, ("complete", (4, 3, 2))),
+    "q4small_p96_n15": Workload("q4small_p96_n15", "q4small", 96, ("complete", (2, 2, 2))),
+    "llama7b_q4_p512_n31": Workload("llama7b_q4_p512_n31", "llama7b_q4", 512, ("complete", (2, 2, 2, 2))),
     "llama30b_p1024_n1": Workload("llama30b_p1024_n1", "llama30b", 1024, ("random", 1, 7)),
     "llama30b_p1024_n8": Workload("llama30b_p1024_n8", "llama30b", 1024, ("random", 8, 7)),
     "llama30b_p1024_n32": Workload("llama30b_p1024_n32", "llama30b", 1024, ("random", 32, 7)),

@@ -13,6 +13,16 @@ Plain (unpacked) layouts, all row-major with W[out][in]:
   tok_embed [V][d], lm_head [V][d], final_norm [d]
   per layer: attn_norm [d], w_qkv [3d][d] (rows: q, k, v), w_o [d][d],
              ffn_norm [d], w_gate_up [2F][d] (rows: gate, up), w_down [d][F]
+
+4-bit models (weight_bits 4) give each layer matrix as a pair (codes, scales):
+codes uint8 [out][in / 2] (input 2j in the low nibble of byte j); each code is
+8 + trunc((a - b) / 2) for two independent uniform nibbles a, b, a symmetric
+bell over [1, 15] centred on the zero point 8 (GPTQ's symmetric codes of
+near-normal weights have that shape; uniform codes would give every weight a
+mean of -s / 2); scales bf16 [out][in / 128], each uniform in [0.75, 1.25)
+times weight_std / 3.067, the RMS of (code - 8), so that the weights the pairs
+stand for have about the bf16 models' spread.  The embedding, LM head and norm
+gains stay bf16.
 """
 
 import math
@@ -35,6 +45,9 @@ KIND = {
 }
 
 _IH4_STD = math.sqrt(4.0 * (65536.0 * 65536.0 - 1.0) / 12.0)
+_Q4_GROUP = 128
+_Q4_CODE_STD = math.sqrt(2408.0 / 256.0)  # RMS of trunc((a - b) / 2) over uniform nibbles a, b
+_SCALE_TAG = 0x40  # added to a matrix's kind for its scales' stream
 _CHUNK = 1 << 24
 
 
@@ -60,6 +73,44 @@ def gen_tensor(shape: ModelShape, kind: str, layer: int, dims: tuple, device="cp
         numel *= x
     std = shape.weight_std if std is None else std
     return _draw(numel, key, std, device).view(*dims)
+
+
+def _draw_codes(nbytes: int, key: tuple, device) -> torch.Tensor:
+    out = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    for start in range(0, nbytes, _CHUNK):
+        stop = min(nbytes, start + _CHUNK)
+        e = torch.arange(start, stop, dtype=torch.int64, device=device)
+        h = hash_uniform16(e, key)
+
+        def code(shift):  # 8 + trunc((a - b) / 2) from the nibbles at bits shift and shift + 4
+            a, b = (h >> shift) & 0xF, (h >> (shift + 4)) & 0xF
+            return 8 + torch.div(a - b, 2, rounding_mode="trunc")
+
+        out[start:stop] = (code(0) | (code(8) << 4)).to(torch.uint8)
+    return out
+
+
+def _draw_scales(numel: int, key: tuple, std: float, device) -> torch.Tensor:
+    out = torch.empty(numel, dtype=torch.bfloat16, device=device)
+    for start in range(0, numel, _CHUNK):
+        stop = min(numel, start + _CHUNK)
+        e = torch.arange(start, stop, dtype=torch.int64, device=device)
+        u = (hash_uniform16(e, key) & 0xFFFF).to(torch.float32) * (1.0 / 65536.0)
+        out[start:stop] = ((0.75 + 0.5 * u) * (std / _Q4_CODE_STD)).to(torch.bfloat16)
+    return out
+
+
+def gen_q4_matrix(shape: ModelShape, kind: str, layer: int, dims: tuple, device="cpu") -> tuple:
+    """(codes uint8 [out][in / 2], scales bf16 [out][in / 128]) of one 4-bit matrix."""
+    n_out, n_in = dims
+    if n_in % _Q4_GROUP != 0:
+        raise ValueError(f"4-bit matrices need inputs in multiples of {_Q4_GROUP}, got {n_in}")
+    tag = (KIND[kind] << 16) | (layer & 0xFFFF)
+    codes = _draw_codes(n_out * n_in // 2, tensor_key(shape.seed, tag), device).view(n_out, n_in // 2)
+    stag = ((KIND[kind] + _SCALE_TAG) << 16) | (layer & 0xFFFF)
+    scales = _draw_scales(n_out * (n_in // _Q4_GROUP), tensor_key(shape.seed, stag), shape.weight_std,
+                          device).view(n_out, n_in // _Q4_GROUP)
+    return codes, scales
 
 
 class ModelWeights:
@@ -91,6 +142,15 @@ class ModelWeights:
     def layer(self, l: int) -> dict:
         s = self.shape
         d, f = s.d_model, s.d_ffn
+        if s.weight_bits == 4:
+            return {
+                "attn_norm": self._gain("attn_norm", l),
+                "w_qkv": gen_q4_matrix(s, "w_qkv", l, (3 * d, d), self.device),
+                "w_o": gen_q4_matrix(s, "w_o", l, (d, d), self.device),
+                "ffn_norm": self._gain("ffn_norm", l),
+                "w_gate_up": gen_q4_matrix(s, "w_gate_up", l, (2 * f, d), self.device),
+                "w_down": gen_q4_matrix(s, "w_down", l, (d, f), self.device),
+            }
         return {
             "attn_norm": self._gain("attn_norm", l),
             "w_qkv": gen_tensor(s, "w_qkv", l, (3 * d, d), self.device),
