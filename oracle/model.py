@@ -141,11 +141,13 @@ def attend(q, k, v):
     q [H, Dh]; k, v [T, H, Dh] -> [H, Dh].  Scores scaled by 1/sqrt(Dh).
     """
     dh = q.shape[-1]
-    s = np.einsum("hd,thd->ht", q, k) / np.sqrt(dh)
+    # per head h: s_h = k_h q_h / sqrt(Dh) over the T keys, then p_h^T v_h
+    # (products batched over the heads)
+    s = np.matmul(k.transpose(1, 0, 2), q[:, :, None])[:, :, 0] / np.sqrt(dh)
     s = s - s.max(axis=1, keepdims=True)
     p = np.exp(s)
     p = p / p.sum(axis=1, keepdims=True)
-    return np.einsum("ht,thd->hd", p, v)
+    return np.matmul(p[:, None, :], v.transpose(1, 0, 2))[:, 0, :]
 
 
 def _rnd(rounding):
