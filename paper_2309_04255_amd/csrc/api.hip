@@ -182,6 +182,27 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
     sp.ksteps = sp.q4 ? step_groups(s, i) : step_ksteps(s, i);
     sp.w_off = w_off[i];
     sp.s_off = sp.q4 ? w_off[i] + (long long)q4_codes_bytes(sp.nblocks, sp.ksteps) : 0;
+    sp.split = 1;
+  }
+  // Split-K for the projections with one column block per workgroup (O and
+  // down: d/16 blocks): groups of S workgroups share a group's blocks, each
+  // over 1/S of the k-steps, so each reads 1/S of the activations per block
+  // of weights; the partial tiles meet in memory and each workgroup finishes
+  // 1/S of the group's blocks.  It pays where the activations outweigh the
+  // weights by far: the down projection (K = F) of passes of 64 or more rows,
+  // in pairs (measured at the LLaMA-7B shape: -3.5% per pass at 41 and 128
+  // rows; at 32 rows, and for O, the hand-off costs more than it saves).
+  // (LLMCAD_SPLIT_O / LLMCAD_SPLIT_DOWN, diagnostics, ask for 1, 2 or 4.)
+  {
+    const int want[2] = {env_int("LLMCAD_SPLIT_O", 1), env_int("LLMCAD_SPLIT_DOWN", W.Mp >= 64 ? 2 : 1)};
+    const int steps[2] = {STEP_O, STEP_DOWN};
+    for (int j = 0; j < 2; ++j) {
+      StepPlan& sp = p.step[steps[j]];
+      const int S = want[j];
+      if ((S == 2 || S == 4) && !sp.q4 && G % S == 0 && sp.nblocks >= G / S &&
+          (size_t)G * cdiv(sp.nblocks, G / S) <= W.part_slots)
+        sp.split = S;
+    }
   }
   p.k_cache = (bf16*)a.k_cache;
   p.v_cache = (bf16*)a.v_cache;
@@ -216,6 +237,8 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.attn_o = (float*)(ws + W.attn_o);
   p.attn_ml = (float*)(ws + W.attn_ml);
   p.head_cnt = (int*)(ws + W.head_counters());
+  p.part = (float*)(ws + W.part);
+  p.grp_cnt = (int*)(ws + W.group_counters());
   p.lm_cnt = (int*)(ws + W.lm_cnt());
   p.exit_cnt = (int*)(ws + W.exit_cnt());
   p.status = (int*)(ws + W.status());

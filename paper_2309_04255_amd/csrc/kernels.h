@@ -45,6 +45,7 @@ struct StepPlan {
   long long s_off;      // 4-bit: the packed scales, offset as w_off
   int layer_rel;        // 1 if w_off is relative to the layer's start
   int q4;               // 1: 4-bit codes with group scales
+  int split;            // split-K: workgroups sharing each group of column blocks (1: none; 2 or 4)
 };
 
 // Must stay the first kernel argument of the pass kernel.
@@ -88,6 +89,9 @@ struct PassParams {
   float* attn_ml;   // [H][MB][KS][16][2]  their running max and sum
   int attn_splits;  // KS, key splits per (head, row block): 1 to 4 (the split's 32-key steps contiguous)
   int* head_cnt;    // [H][MB] arrivals of the key splits
+  float* part;      // split-K partial tiles: per workgroup w, [cdiv(blocks, G/S)][MB] x 1 KiB
+                    // (fp32 [64 lanes][4]) from slot w cdiv(blocks, G/S)
+  int* grp_cnt;     // [O, down][kPassMaxGrid / 2] arrivals of the workgroups of each split-K group
   float* lm_val;    // [Mp][G] LM-head argmax per row and workgroup
   int* lm_idx;
   int* amax;        // [Mp]

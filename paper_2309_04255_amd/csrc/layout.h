@@ -23,6 +23,7 @@ constexpr int kQ4BlockBytes = kNB * kQ4Group / 2;  // 1 KiB
 constexpr int kQ4ScaleBytes = kNB * 2;
 constexpr int kMaxNodes = LLMCAD_MAX_NODES;
 constexpr int kAttnMaxSplits = 4;   // key splits per (head, 16-row block)
+constexpr int kMaxSplitK = 4;       // workgroups sharing the k-steps of a group of column blocks
 constexpr int kPassMaxGrid = 1024;  // workgroups of the pass
 constexpr int kBarSlots = 16;       // grid-barrier counters
 constexpr int kBarStride = 32;      // ints between barrier counters (128 bytes)
@@ -154,7 +155,9 @@ inline int step_groups(const Shape& s, int step) { return step == STEP_DOWN ? s.
 struct WorkspaceLayout {
   int Mp;
   int n_head_counters;
-  size_t counters;     // int32: (head, row block) [H][8] | lm | exit | status
+  int n_group_counters;
+  size_t part_slots;   // 1 KiB x Mp/16 partial tiles the split-K region holds
+  size_t counters;     // int32: (head, row block) [H][8] | lm | exit | status | split-K groups
   size_t counters_bytes;
   size_t bar;          // int32 [kBarSlots][kBarStride] grid-barrier counters
   size_t zero;         // kZeroBytes of zeros (never written by a pass)
@@ -173,6 +176,7 @@ struct WorkspaceLayout {
   size_t hs;           // bf16 [L] x (Mp x Fp, fragment order)  SwiGLU product
   size_t attn_o;       // fp32 [H][Mp/16][KS][16][Dh]  key-split partial attention outputs
   size_t attn_ml;      // fp32 [H][Mp/16][KS][16][2]   their running max and sum
+  size_t part;         // fp32 [part_slots][Mp/16][64][4]  split-K partial tiles
   size_t trace;        // int64 [G][4 + 5L][8]    phase timestamps (diagnostics)
   size_t total;
   WorkspaceLayout(const Shape& s, int max_n, int G) {
@@ -188,7 +192,8 @@ struct WorkspaceLayout {
     // that their offsets do not depend on the pass's node count or grid:
     // llmcad_workspace_init clears them once for every later pass.
     n_head_counters = s.H * (kMaxNodes / 16);
-    counters_bytes = (size_t)(n_head_counters + 4) * 4;
+    n_group_counters = kPassMaxGrid;  // [O, down][up to G / 2 groups]
+    counters_bytes = (size_t)(n_head_counters + 4 + n_group_counters) * 4;
     counters = take(counters_bytes);
     bar = take((size_t)kBarSlots * kBarStride * 4);
     zero = take(kZeroBytes);
@@ -207,6 +212,12 @@ struct WorkspaceLayout {
     hs = take((size_t)s.L * Mp * s.Fp * 2);
     attn_o = take((size_t)s.H * Mp * kAttnMaxSplits * s.Dh * 4);
     attn_ml = take((size_t)s.H * Mp * kAttnMaxSplits * 2 * 4);
+    // split-K steps (O, down: d/16 column blocks; passes of 32 or more
+    // rows) in groups of S <= kMaxSplitK workgroups: each workgroup keeps a
+    // partial tile of every block of its group, G cdiv(d/16, G/S) <=
+    // S d/16 + G of them
+    part_slots = Mp >= 32 ? (size_t)kMaxSplitK * s.d_nb + G : 0;
+    part = take(part_slots * (Mp / 16) * 1024);
     trace = take((size_t)G * pass_phases(s.L) * 8 * 8);
     total = o_;
   }
@@ -214,6 +225,7 @@ struct WorkspaceLayout {
   size_t lm_cnt() const { return head_counters() + (size_t)n_head_counters * 4; }
   size_t exit_cnt() const { return lm_cnt() + 4; }
   size_t status() const { return lm_cnt() + 8; }
+  size_t group_counters() const { return lm_cnt() + 16; }
 };
 
 }  // namespace llmcad

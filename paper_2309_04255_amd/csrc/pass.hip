@@ -66,7 +66,7 @@ constexpr int kThreads = 64 * kWaves;
 #define LLMCAD_DEPTH_WIDE 4
 #endif
 #ifndef LLMCAD_TILE_BLOCKS_MB8
-#define LLMCAD_TILE_BLOCKS_MB8 3
+#define LLMCAD_TILE_BLOCKS_MB8 4
 #endif
 
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
@@ -222,19 +222,26 @@ struct GemmLds {
   int walk_len;
 };
 
-// LDS of a GEMM tile of cw blocks (dynamic shared memory), in KiB:
-//   [0, 4 cw MB)                 the waves' partial tiles, fp32 [4][cw][MB][64 lanes][4]
-//   [4 cw MB, 5 cw MB + cw)      epilogue inputs: per (block, row block) 1 KiB
+// LDS of a GEMM tile of cw blocks (dynamic shared memory), in KiB, with
+// SL partial-tile slots:
+//   [0, SL cw MB)                the partial tiles, fp32 [SL][cw][MB][64 lanes][4]:
+//                                the four waves' (SL = 4), or two sums of
+//                                two waves' (SL = 2, when four slots and the
+//                                epilogue inputs would not fit), or a split-K
+//                                group's partial sums (SL = S)
+//   [SL cw MB, (SL+1) cw MB + cw)  epilogue inputs: per (block, row block) 1 KiB
 //                                of the residual stream (fp32 [16 rows][16]) or
 //                                of the rotary table (fp32 [16 rows][8 pairs][2]);
 //                                then per block 1 KiB holding its 16 norm gains
 //                                (bf16, first 32 bytes)
-//   [5 cw MB + cw, 142)          the first weight stages of each wave, copied
+//   [(SL+1) cw MB + cw, 142)     the first weight stages of each wave, copied
 //                                before the phase's barrier
 constexpr int kGemmLdsBytes = 142 * 1024;
 __host__ __device__ constexpr int tw_off() { return 0; }
-__host__ __device__ constexpr int epi_off(int cw, int MB) { return 4 * cw * MB * 1024; }
-__host__ __device__ constexpr int wl_off(int cw, int MB) { return (5 * cw * MB + cw) * 1024; }
+__host__ __device__ constexpr int epi_off(int cw, int MB, int SL) { return SL * cw * MB * 1024; }
+__host__ __device__ constexpr int wl_off(int cw, int MB, int SL) { return ((SL + 1) * cw * MB + cw) * 1024; }
+// partial-tile slots of a tile: four, or two when four do not fit
+__host__ __device__ constexpr int tile_slots(int cw, int MB) { return wl_off(cw, MB, 4) <= kGemmLdsBytes ? 4 : 2; }
 
 // Direct global -> LDS copy of 16 bytes per lane: lane l's bytes land at
 // lds + 16 l.  `lds` must be the same in every lane.
@@ -341,26 +348,31 @@ constexpr int tile_depth() {
 template <int MB, int C>
 __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams& pin, int step, int layer,
                                                                        int nb0, int wait_phase, char* lds,
-                                                                       GemmLds& gl, int* lds_flag) {
+                                                                       GemmLds& gl, int* lds_flag, int k0,
+                                                                       int kn, int epi_in) {
   KParams& p = uniform_params(pin);
   step = wave_uniform(step);
   layer = wave_uniform(layer);
   nb0 = wave_uniform(nb0);
   wait_phase = wave_uniform(wait_phase);
+  k0 = wave_uniform(k0);
+  epi_in = wave_uniform(epi_in);
   const TileIn io = tile_in(p, step, layer);
   const int wave = wave_index(), lane = threadIdx.x & 63;
-  const int ks = io.ks;
+  // k-steps [k0, k0 + kn) of the step's io.ks (a split-K slice; all of them otherwise)
+  const int ks = wave_uniform(kn);
   const int ns = wave_uniform(wave < ks ? (ks - wave + kWaves - 1) / kWaves : 0);
   // Pipeline depth (tile_depth), but no deeper than the LDS stages that
   // fit, so that wide tiles still get some (the LDS phase advances D stages
   // at a time).
-  constexpr int WL_STAGES = (kGemmLdsBytes - wl_off(C, MB)) / (kWaves * C * 1024);
+  constexpr int SL = tile_slots(C, MB);
+  constexpr int WL_STAGES = (kGemmLdsBytes - wl_off(C, MB, SL)) / (kWaves * C * 1024);
   constexpr int D0 = tile_depth<MB, C>();
   constexpr int D = WL_STAGES >= 2 && WL_STAGES < D0 ? WL_STAGES : D0;
-  // this wave's k-steps: wave + 4 i
-  const bf16x8* wt = io.w + ((size_t)nb0 * ks + wave) * 64 + lane;
-  const size_t cstride = (size_t)ks * 64;
-  const bf16x8* at = io.a + (size_t)wave * MB * 64 + lane;
+  // this wave's k-steps: k0 + wave + 4 i
+  const bf16x8* wt = io.w + ((size_t)nb0 * io.ks + k0 + wave) * 64 + lane;
+  const size_t cstride = (size_t)io.ks * 64;
+  const bf16x8* at = io.a + (size_t)(k0 + wave) * MB * 64 + lane;
   // Loads past the wave's last k-step read a line of zeros instead (the
   // load is still issued, so that the compiler's count of loads in flight
   // stays exact and every wait in the loop is for one stage only).  For the
@@ -376,7 +388,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   constexpr int PMAX = WL_STAGES / D * D;
   const int pcap = wave_uniform(p.wl_cap < PMAX ? p.wl_cap / D * D : PMAX);
   const int P = wave_uniform(wait_phase >= 0 ? (ns / D * D < pcap ? ns / D * D : pcap) : 0);
-  char* wl = lds + wl_off(C, MB) + (size_t)wave * PMAX * C * 1024;
+  char* wl = lds + wl_off(C, MB, SL) + (size_t)wave * PMAX * C * 1024;
   auto load_w = [&](int slot, int i, bool want) {  // stage i, or nothing (zero line)
     const bool live = want && i < ns;
 #pragma unroll
@@ -404,7 +416,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   constexpr int KU = C * MB;
   constexpr int kEpiWave = kWaves - 1;
   f32x4 sx[KU], sg[C];
-  if (wave == kEpiWave) {
+  if (wave == kEpiWave && epi_in) {
     const bool resid = io.resid;
 #pragma unroll
     for (int u = 0; u < KU; ++u) {
@@ -423,9 +435,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
     for (int c = 0; c < C; ++c)
       sg[c] = ldg(opaque(resid ? (const f32x4*)(io.g_next + kNB * (nb0 + c) + 8 * (lane & 1)) : zero4));
 #pragma unroll
-    for (int u = 0; u < KU; ++u) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)u * 1024 + lane * 16, sx[u]);
+    for (int u = 0; u < KU; ++u) lds_st<f32x4>(lds + epi_off(C, MB, SL) + (size_t)u * 1024 + lane * 16, sx[u]);
 #pragma unroll
-    for (int c = 0; c < C; ++c) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)(C * MB + c) * 1024 + lane * 16, sg[c]);
+    for (int c = 0; c < C; ++c) lds_st<f32x4>(lds + epi_off(C, MB, SL) + (size_t)(C * MB + c) * 1024 + lane * 16, sg[c]);
   }
   if (wave != 0) {
     if constexpr (PMAX > 0) {
@@ -435,7 +447,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
           dma16(wt + c * cstride + (size_t)(kWaves * i) * 64, wl + (size_t)(i * C + c) * 1024);
       if (wave == 1) {
         const bf16x8* wt0 = wt - 64;
-        char* wl0 = lds + wl_off(C, MB);
+        char* wl0 = lds + wl_off(C, MB, SL);
         for (int i = 0; i < P0; ++i)
 #pragma unroll
           for (int c = 0; c < C; ++c)
@@ -544,12 +556,34 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
       *(f32x4*)&gl.part_ss[ch * 16 * MB + 4 * q] = t;
     }
   }
-  // This wave's partial tile -> LDS; the epilogue adds the four in wave order.
+  // This wave's partial tile -> LDS; the epilogue adds the four in wave
+  // order.  With two slots, waves 2 and 3 hand theirs to waves 0 and 1
+  // first, and the epilogue adds (w0 + w2) + (w1 + w3).
+  if constexpr (SL == 2) {
+    if (wave >= 2) {
 #pragma unroll
-  for (int c = 0; c < C; ++c)
+      for (int c = 0; c < C; ++c)
 #pragma unroll
-    for (int rb = 0; rb < MB; ++rb)
-      lds_st<f32x4>(lds + tw_off() + ((size_t)((wave * C + c) * MB + rb) * 64 + lane) * 16, acc[rb][c]);
+        for (int rb = 0; rb < MB; ++rb)
+          lds_st<f32x4>(lds + tw_off() + ((size_t)(((wave - 2) * C + c) * MB + rb) * 64 + lane) * 16, acc[rb][c]);
+    }
+    __syncthreads();
+    if (wave < 2) {
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int rb = 0; rb < MB; ++rb) {
+          char* at2 = lds + tw_off() + ((size_t)((wave * C + c) * MB + rb) * 64 + lane) * 16;
+          lds_st<f32x4>(at2, acc[rb][c] + lds_ld<f32x4>(at2));
+        }
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb)
+        lds_st<f32x4>(lds + tw_off() + ((size_t)((wave * C + c) * MB + rb) * 64 + lane) * 16, acc[rb][c]);
+  }
   __syncthreads();
   return true;
 }
@@ -644,9 +678,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute_q4(KPara
     for (int c = 0; c < C; ++c)
       sg[c] = ldg(opaque(resid ? (const f32x4*)(io.g_next + kNB * (nb0 + c) + 8 * (lane & 1)) : zero4));
 #pragma unroll
-    for (int u = 0; u < KU; ++u) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)u * 1024 + lane * 16, sx[u]);
+    for (int u = 0; u < KU; ++u) lds_st<f32x4>(lds + epi_off(C, MB, 4) + (size_t)u * 1024 + lane * 16, sx[u]);
 #pragma unroll
-    for (int c = 0; c < C; ++c) lds_st<f32x4>(lds + epi_off(C, MB) + (size_t)(C * MB + c) * 1024 + lane * 16, sg[c]);
+    for (int c = 0; c < C; ++c) lds_st<f32x4>(lds + epi_off(C, MB, 4) + (size_t)(C * MB + c) * 1024 + lane * 16, sg[c]);
   }
   if (wave != 0) {
 #pragma unroll
@@ -769,10 +803,10 @@ __device__ __forceinline__ bool tile_dispatch_q4(int cw, KParams& p, int step, i
 
 template <int MB, int C>
 __device__ __forceinline__ bool tile_dispatch(int cw, KParams& p, int step, int layer, int nb0, int wait_phase,
-                                              char* lds, GemmLds& gl, int* flag) {
+                                              char* lds, GemmLds& gl, int* flag, int k0, int kn, int epi_in) {
   if constexpr (C >= 1) {
-    if (cw == C) return tile_compute<MB, C>(p, step, layer, nb0, wait_phase, lds, gl, flag);
-    return tile_dispatch<MB, C - 1>(cw, p, step, layer, nb0, wait_phase, lds, gl, flag);
+    if (cw == C) return tile_compute<MB, C>(p, step, layer, nb0, wait_phase, lds, gl, flag, k0, kn, epi_in);
+    return tile_dispatch<MB, C - 1>(cw, p, step, layer, nb0, wait_phase, lds, gl, flag, k0, kn, epi_in);
   } else {
     return false;
   }
@@ -833,24 +867,27 @@ __device__ __forceinline__ void row_scales(KParams& p, const StepIo& io, GemmLds
 }
 
 // Epilogue of one accumulator tile ("unit": block c of the tile x row block
-// rb, 16 x 16).  The unit's sum is the four waves' partials added in wave
-// order; lane l holds rows 16 rb + 4 (l / 16) + i, i < 4, column l % 16.
+// rb, 16 x 16).  The unit's sum is the nsum partial tiles in LDS added in
+// order (the four waves' partials, or a split-K group's partial sums in
+// slice order); lane l holds rows 16 rb + 4 (l / 16) + i, i < 4, column
+// l % 16.
 // Outputs are written with device-coherent stores.
 template <int MB, int EPI>
 __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, const char* lds, int cw, int c, int rb,
-                                              int nb, GemmLds& gl) {
+                                              int nb, GemmLds& gl, int nsum) {
   const int lane = threadIdx.x & 63, j = lane & 15, q4 = lane >> 4;
   const int unit = c * MB + rb;
   f32x4 s = lds_ld<f32x4>(lds + tw_off() + ((size_t)unit * 64 + lane) * 16);
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) s += lds_ld<f32x4>(lds + tw_off() + ((size_t)(w * cw * MB + unit) * 64 + lane) * 16);
+  for (int w = 1; w < kWaves; ++w)
+    if (w < nsum) s += lds_ld<f32x4>(lds + tw_off() + ((size_t)(w * cw * MB + unit) * 64 + lane) * 16);
   float v[4] = {s[0], s[1], s[2], s[3]};
   const int rr0 = 4 * q4;  // first row of this lane inside the row block
   if constexpr (EPI == EPI_QKV || EPI == EPI_SWIGLU) {  // the norm's per-row scale
 #pragma unroll
     for (int i = 0; i < 4; ++i) v[i] *= gl.rstd[16 * rb + rr0 + i];
   }
-  const char* epi = lds + epi_off(cw, MB);
+  const char* epi = lds + epi_off(cw, MB, nsum);
   const int col = kNB * nb + j;
   if constexpr (EPI == EPI_QKV) {
     const int d = p.d, dh = p.Dh;
@@ -1058,18 +1095,19 @@ __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl
 // registers are allocated apart from the streaming loop's.
 template <int MB, int EPI>
 __device__ __attribute__((noinline, not_tail_called)) void finish_tile(KParams& pin, int step, int layer, int nb0,
-                                                                      int cw, char* lds, GemmLds& gl) {
+                                                                      int cw, char* lds, GemmLds& gl, int nsum) {
   KParams& p = uniform_params(pin);
   step = wave_uniform(step);
   layer = wave_uniform(layer);
   nb0 = wave_uniform(nb0);
   cw = wave_uniform(cw);
+  nsum = wave_uniform(nsum);
   const StepIo io = step_io<EPI>(p, step, layer);
   if constexpr (EPI == EPI_QKV || EPI == EPI_SWIGLU) row_scales<MB>(p, io, gl);
   const int units = cw * MB;
   for (int u = wave_index(); u < units; u += kWaves) {
     const int c = u / MB, rb = u % MB;
-    epilogue_unit<MB, EPI>(p, io, lds, cw, c, rb, nb0 + c, gl);
+    epilogue_unit<MB, EPI>(p, io, lds, cw, c, rb, nb0 + c, gl, nsum);
   }
   if constexpr (EPI == EPI_LOGITS) {
     __syncthreads();
@@ -1091,6 +1129,147 @@ __device__ __attribute__((noinline, not_tail_called)) void finish_tile(KParams& 
   __syncthreads();
 }
 
+// ---- split-K (projections with one column block per workgroup at 64 or
+// more rows: every workgroup would read the whole activation matrix per
+// block of weights)
+//
+// Groups of S consecutive workgroups (virtual index) share a group of column
+// blocks; workgroup s of a group computes every block of the group over the
+// k-steps [s ks/S, (s+1) ks/S), so it reads 1/S of the activations for the
+// same weight bytes.  Each stores its partial tiles (its waves' partials
+// added in wave order), counts its arrival on the group's counter, and then
+// finishes 1/S of the group's blocks: it waits for the group, adds the S
+// partial tiles of each of its units in slice order (bit-reproducible) and
+// runs the step's epilogue.
+
+// The tile's partial sums (its partial tiles in LDS, added in slot order)
+// to dst: unit u = c MB + rb of the tile at dst + u KiB, lane l's 16 bytes
+// at + 16 l.  Device-coherent stores: the region is reused by every split
+// phase of the pass.
+template <int MB>
+__device__ __forceinline__ void split_store(const char* lds, int cw, float* dst) {
+  const int lane = threadIdx.x & 63;
+  const int nsl = tile_slots(cw, MB);
+  for (int u = wave_index(); u < cw * MB; u += kWaves) {
+    f32x4 s = lds_ld<f32x4>(lds + tw_off() + ((size_t)u * 64 + lane) * 16);
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w)
+      if (w < nsl) s += lds_ld<f32x4>(lds + tw_off() + ((size_t)(w * cw * MB + u) * 64 + lane) * 16);
+    float* q = dst + ((size_t)u * 64 + lane) * 4;
+    st_coherent2(q, s[0], s[1]);
+    st_coherent2(q + 2, s[2], s[3]);
+  }
+}
+
+// Waits (wave 0 polls) until the counter reaches `want`; false (to all
+// threads) if the bounded spin ran out (the pass status is then set).
+__device__ __forceinline__ bool counter_wait(const Sync& s, const int* cnt, int want) {
+  if (threadIdx.x < 64) {
+    int ok = 1;
+    if (s.limit < 0) {
+      ok = 0;
+    } else {
+      int spins = 0;
+      while (ld_coherent(cnt) < want) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++spins > s.limit) {
+          ok = 0;
+          break;
+        }
+      }
+    }
+    if (!ok && threadIdx.x == 0) st_coherent(s.status, 1);
+    if (threadIdx.x == 0) *s.lds_flag = ok;
+  }
+  lds_barrier();
+  const bool ok = *s.lds_flag != 0;
+  lds_barrier();
+  return ok;
+}
+
+// One split-K phase of a residual step (O or down).  Each group counts its
+// arrivals on a counter of its own step, S per layer (the step's S is fixed
+// for the pass), so the counter reaches S (layer + 1) exactly when the group
+// has arrived in this layer.
+template <int MB, int EPI>
+__device__ __attribute__((noinline, not_tail_called)) bool split_phase(KParams& pin, int step, int layer,
+                                                                      int phase, char* lds, GemmLds& gl,
+                                                                      int* lds_flag) {
+  KParams& p = uniform_params(pin);
+  step = wave_uniform(step);
+  layer = wave_uniform(layer);
+  phase = wave_uniform(phase);
+  const Sync sy = make_sync(p, lds_flag);
+  const StepPlan& sp = p.step[step];
+  constexpr int CM = MB <= 2 ? 8 : MB == 4 ? 4 : LLMCAD_TILE_BLOCKS_MB8;
+  const int S = wave_uniform(sp.split), G = p.G, NG = G / S;
+  const int nbk = sp.nblocks, ks = sp.ksteps;
+  const int vw = virtual_wg(G);
+  const int g = vw / S, sl = vw % S;
+  const int glo = wave_uniform((int)((long)g * nbk / NG));
+  const int ghi = wave_uniform((int)((long)(g + 1) * nbk / NG));
+  const int bstride = (nbk + NG - 1) / NG;  // partial-tile slots per workgroup, in blocks
+  const int k0 = sl * ks / S, k1 = (sl + 1) * ks / S;
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  constexpr int U = MB * 256;  // floats of one block's partial tiles
+  int* cnt = p.grp_cnt + (step == STEP_DOWN ? kPassMaxGrid / 2 : 0) + g;
+  if (glo >= ghi) {  // (no blocks: the host splits only steps with a block per group)
+    trace_mark(sy, phase, 0);
+    if (!grid_wait(sy, phase, G)) return false;
+    trace_mark(sy, phase, 1);
+    return true;
+  }
+  float* mine = p.part + (size_t)vw * bstride * U;
+  for (int b0 = glo; b0 < ghi; b0 += CM) {
+    const int cw = ghi - b0 < CM ? ghi - b0 : CM;
+    const bool first = b0 == glo;
+    if (!tile_dispatch<MB, CM>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag, k0, k1 - k0, 0))
+      return false;
+    if (first) trace_mark(sy, phase, 4);
+    split_store<MB>(lds, cw, mine + (size_t)(b0 - glo) * U);
+    __syncthreads();  // (the next tile and the finish reuse the LDS)
+  }
+  // This workgroup's partial tiles have completed; count its arrival.
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) atomic_add_dev(cnt, 1);
+  const int B = ghi - glo;
+  const int olo = glo + sl * B / S, ohi = glo + (sl + 1) * B / S;  // the blocks it finishes
+  if (olo >= ohi) {
+    trace_mark(sy, phase, 5);
+    return true;
+  }
+  const TileIn io = tile_in(p, step, layer);
+  for (int c0 = olo; c0 < ohi; c0 += CM) {
+    const int cw = wave_uniform(ohi - c0 < CM ? ohi - c0 : CM);
+    char* epi = lds + epi_off(cw, MB, S);
+    // epilogue inputs (written two or more phases ago): the residual rows of
+    // each unit and the next norm's gains, straight to LDS, before the wait
+    if (wave == kWaves - 1) {
+      for (int u = 0; u < cw * MB; ++u) {
+        const int c = u / MB, rb = u % MB;
+        dma16(io.x_in + (size_t)(16 * rb + (lane >> 2)) * p.d + kNB * (c0 + c) + 4 * (lane & 3),
+              epi + (size_t)u * 1024);
+      }
+      for (int c = 0; c < cw; ++c) dma16(io.g_next + kNB * (c0 + c) + 8 * (lane & 1), epi + (size_t)(cw * MB + c) * 1024);
+    }
+    if (c0 == olo && !counter_wait(sy, cnt, S * (layer + 1))) return false;
+    // the group's S partial tiles of each unit -> LDS slots [t][c][rb]
+    for (int it = wave; it < S * cw * MB; it += kWaves) {
+      const int t = it / (cw * MB), u = it % (cw * MB);
+      const float* src = p.part + ((size_t)(g * S + t) * bstride + (c0 - glo)) * U + ((size_t)u * 64 + lane) * 4;
+      const float2 a = ld_coherent2(src), b = ld_coherent2(src + 2);
+      lds_st<f32x4>(lds + tw_off() + ((size_t)(t * cw * MB + u) * 64 + lane) * 16, f32x4{a.x, a.y, b.x, b.y});
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    finish_tile<MB, EPI>(p, step, layer, c0, cw, lds, gl, S);
+  }
+  trace_mark(sy, phase, 5);
+  return true;
+}
+
 // One GEMM phase: this workgroup's run of blocks, in tiles of at most
 // tile_max_blocks blocks over the full K, each followed by its epilogue.  The
 // LM head then publishes the workgroup's argmax per row, and the last
@@ -1106,7 +1285,8 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   const Sync sy = make_sync(p, lds_flag);
   const StepPlan& sp = p.step[step];
   constexpr int CM = MB <= 2 ? 8 : MB == 4 ? 4 : LLMCAD_TILE_BLOCKS_MB8;
-  static_assert(wl_off(CM, MB) <= kGemmLdsBytes, "a tile's partial sums and epilogue inputs fit the LDS");
+  static_assert(wl_off(CM, MB, tile_slots(CM, MB)) <= kGemmLdsBytes,
+                "a tile's partial sums and epilogue inputs fit the LDS");
   // 4-bit tiles hold a second set of accumulators (each group's partial sums)
   constexpr int CMQ = MB <= 2 ? 6 : MB == 4 ? 2 : 1;
   const bool q4 = wave_uniform(sp.q4) != 0;
@@ -1132,10 +1312,11 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
     const int cw = hi - b0 < cm ? hi - b0 : cm;
     const bool first = b0 == lo;
     const bool ok = q4 ? tile_dispatch_q4<MB, CMQ>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag)
-                       : tile_dispatch<MB, CM>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag);
+                       : tile_dispatch<MB, CM>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag, 0,
+                                               sp.ksteps, 1);
     if (!ok) return false;
     if (first) trace_mark(sy, phase, 4);
-    finish_tile<MB, EPI>(p, step, layer, b0, cw, lds, gl);
+    finish_tile<MB, EPI>(p, step, layer, b0, cw, lds, gl, q4 ? 4 : tile_slots(cw, MB));
   }
   trace_mark(sy, phase, 5);
   if constexpr (EPI == EPI_LOGITS) {
@@ -1720,13 +1901,16 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
     ok = attn_phase<MB, DH>(p, l, phase, lds_raw, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
-    ok = gemm_phase<MB, EPI_RESID>(p, STEP_O, l, phase, lds_raw, gl, &flag);
+    ok = p.step[STEP_O].split > 1 ? split_phase<MB, EPI_RESID>(p, STEP_O, l, phase, lds_raw, gl, &flag)
+                                  : gemm_phase<MB, EPI_RESID>(p, STEP_O, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
     ok = gemm_phase<MB, EPI_SWIGLU>(p, STEP_GATE_UP, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
-    ok = gemm_phase<MB, EPI_RESID>(p, STEP_DOWN, l, phase, lds_raw, gl, &flag);
+    ok = p.step[STEP_DOWN].split > 1
+             ? split_phase<MB, EPI_RESID>(p, STEP_DOWN, l, phase, lds_raw, gl, &flag)
+             : gemm_phase<MB, EPI_RESID>(p, STEP_DOWN, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
   }
@@ -1735,9 +1919,15 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
     grid_arrive(sy, phase++);
     if (gemm_phase<MB, EPI_LOGITS>(p, STEP_LM, 0, phase, lds_raw, gl, &flag)) trace_mark(sy, phase, 2);
   }
-  // Leave the pass: the last workgroup out resets the barrier counters.
+  // Leave the pass: the last workgroup out resets the barrier and split-K
+  // group counters.
   if (arrive_last(p.exit_cnt, p.G, &flag)) {
     if (threadIdx.x < kBarSlots) st_coherent(p.bar + threadIdx.x * kBarStride, 0);
+    if (p.step[STEP_O].split > 1 || p.step[STEP_DOWN].split > 1)
+      for (int i = threadIdx.x; i < p.G / 2; i += kThreads) {
+        st_coherent(p.grp_cnt + i, 0);
+        st_coherent(p.grp_cnt + kPassMaxGrid / 2 + i, 0);
+      }
   }
 }
 

@@ -124,6 +124,34 @@ def test_launch_shape_variants(model, monkeypatch):
             monkeypatch.delenv(k)
 
 
+@pytest.mark.parametrize("tree", ["binary_d4_n31", "b432_n41", "random_n77", "random_n128"])
+def test_split_k_variants(model, monkeypatch, tree):
+    # Split-K for the O and down projections (passes of 32 or more rows):
+    # groups of 2 or 4 workgroups share a group of column blocks, each over
+    # a slice of the k-steps, and add their partial tiles in slice order.
+    # The small models' d/16 blocks need a grid of at most 4 d/16 workgroups
+    # for a block per group: 64 and 24 workgroups (with 24 and S = 4 some
+    # workgroups of a group finish no block).  Each variant meets the oracle
+    # bar, and (bf16 models) its logits differ from the unsplit pass's
+    # somewhere (another order of fp32 additions): the split path ran.
+    parent = TREES[tree]
+    tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=11)
+    for grid, s_o, s_down in ((64, 4, 4), (64, 2, 4), (24, 4, 2), (24, 2, 4)):
+        monkeypatch.setenv("LLMCAD_PASS_GRID", str(grid))
+        monkeypatch.setenv("LLMCAD_SPLIT_O", "1")
+        monkeypatch.setenv("LLMCAD_SPLIT_DOWN", "1")
+        base = _check_all(model, parent, tok, f"grid {grid} unsplit")
+        monkeypatch.setenv("LLMCAD_SPLIT_O", str(s_o))
+        monkeypatch.setenv("LLMCAD_SPLIT_DOWN", str(s_down))
+        split = _check_all(model, parent, tok, f"grid {grid} split O {s_o} down {s_down}")
+        if model.shape.weight_bits == 16:
+            assert not np.array_equal(base, split), "the split-K path did not run"
+        again = _run(model, parent, tok)[0]
+        np.testing.assert_array_equal(split, again)  # bit-reproducible
+        for k in ("LLMCAD_PASS_GRID", "LLMCAD_SPLIT_O", "LLMCAD_SPLIT_DOWN"):
+            monkeypatch.delenv(k)
+
+
 def _long_prefix_session(model, PL):
     """A session whose cache holds PL seeded random bf16 prefix keys/values
     (written straight into the cache) and the oracle's copies of them."""
