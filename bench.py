@@ -126,14 +126,17 @@ def write_traffic(fetch_csv, write_csv, workload, copy_mib):
     print(json.dumps(out, indent=1))
 
 
-def cpu_baseline(gen, shape, P, parent, tok, seed):
-    """Time the CPU oracle on one whole pass of the workload: oracle.tree_layer
-    over every layer (float64 NumPy with the bf16 rounding points), then the
-    final norm and LM head.  The weights come from the seeded generator on the
-    GPU, widened to float64 there and copied to the host one layer at a time;
-    that preparation is not timed (it is reported apart), the oracle's
-    arithmetic is.  The prefix keys/values are random bf16 values of the
-    workload's shape (their values do not change the oracle's cost)."""
+def cpu_baseline(gen, shape, P, parent, tok, seed, budget_s=20.0):
+    """Time the CPU oracle on a pass of the workload: oracle.tree_layer layer
+    by layer (float64 NumPy with the bf16 rounding points), then the final
+    norm and LM head.  Layers are timed until `budget_s` seconds of oracle
+    arithmetic have been spent (every layer when the whole pass fits, as at
+    the LLaMA-7B shape); the per-layer mean is then scaled to all layers.
+    The weights come from the seeded generator on the GPU, widened to
+    float64 there and copied to the host one layer at a time; that
+    preparation is not timed (it is reported apart), the oracle's arithmetic
+    is.  The prefix keys/values are random bf16 values of the workload's
+    shape (their values do not change the oracle's cost)."""
     import numpy as np
     import torch
 
@@ -161,7 +164,7 @@ def cpu_baseline(gen, shape, P, parent, tok, seed):
     prep = time.perf_counter() - t_prep
     rng = np.random.default_rng(seed)
     H, Dh = shape.n_heads, shape.head_dim
-    t_calc = 0.0
+    t_layers, done = 0.0, 0
     for l in range(shape.n_layers):
         t0 = time.perf_counter()
         layer.clear()
@@ -172,22 +175,30 @@ def cpu_baseline(gen, shape, P, parent, tok, seed):
         _, x, _, _ = oracle.tree_layer(w, l, x, pk, pv, parent, rounding=True)
         t2 = time.perf_counter()
         prep += t1 - t0
-        t_calc += t2 - t1
+        t_layers += t2 - t1
+        done += 1
+        if t_layers >= budget_s:
+            break
     t0 = time.perf_counter()
     oracle.logits_from_stream(w, x)
-    t_calc += time.perf_counter() - t0
+    t_head = time.perf_counter() - t0
     layer.clear()
-    log(f"cpu baseline: oracle pass {t_calc:.1f}s over {shape.n_layers} layers "
-        f"(+{prep:.1f}s of untimed weight preparation)")
+    t_calc = t_layers * shape.n_layers / done + t_head
+    log(f"cpu baseline: oracle {t_layers:.1f}s over {done}/{shape.n_layers} layers + {t_head:.1f}s head "
+        f"-> {t_calc:.1f}s per pass (+{prep:.1f}s of untimed weight preparation)")
+    whole = done == shape.n_layers
     return {
-        "value": round(1.0 / t_calc, 5),
+        "value": round(1.0 / t_calc, 6),
         "unit": "passes/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"one whole pass of the workload (P={P}, n={len(parent)}): oracle.tree_layer over all "
-                   f"{shape.n_layers} layers, then the final norm and LM head, float64 NumPy with the bf16 "
-                   f"rounding points; weight conversion ({prep:.1f}s, untimed) excluded; BLAS threads "
-                   f"{threads}, host cores visible {os.cpu_count()}"),
+        "sample": ((f"one whole pass of the workload (P={P}, n={len(parent)}): oracle.tree_layer over all "
+                    f"{shape.n_layers} layers" if whole else
+                    f"a pass of the workload (P={P}, n={len(parent)}) with oracle.tree_layer timed on its first "
+                    f"{done} of {shape.n_layers} layers ({t_layers:.1f}s) and the mean scaled to all layers") +
+                   f", then the final norm and LM head, float64 NumPy with the bf16 rounding points; weight "
+                   f"conversion ({prep:.1f}s, untimed) excluded; BLAS threads {threads}, host cores visible "
+                   f"{os.cpu_count()}"),
     }
 
 
@@ -270,13 +281,15 @@ def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
 def draft_generation(sess, plen, root, iterations, threshold=0.3):
     """Draft-side tree generation with this model as the draft (in the
     paper's LLaMA2 pair the 7B model drafts for the 13B): `iterations` fed
-    nodes after the root, one tree-decoder step each, the logits row read back
-    and the branch pacer run on the host between steps.  Also times one
-    tree-decoder step alone (the step's launch on the stream, no read-back)."""
+    nodes after the root, one tree-decoder step each (with the candidate
+    summary: the argmax and the tokens above the threshold come back, not the
+    logits row), the branch pacer run on the host between steps.  Also times
+    one step alone (the step's launch on the stream, no read-back); the
+    difference per step is the host's share (read-back, pacer, launch)."""
     import numpy as np
     import torch
 
-    from paper_2309_04255_amd import draft
+    from paper_2309_04255_amd import binding, draft
 
     draft.generate_tree(sess, plen, root, iterations, threshold)  # warm-up
     torch.cuda.synchronize()
@@ -287,21 +300,119 @@ def draft_generation(sess, plen, root, iterations, threshold=0.3):
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     reps = 20
     ftok, fpar = np.asarray(tok[:info["fed"]]), np.asarray(par[:info["fed"]])
+    cand = torch.zeros((1, binding.CAND_WORDS), dtype=torch.int32, device="cuda")
     e0.record(stream)
     for _ in range(reps):
-        sess.extend(plen, ftok, fpar, len(ftok) - 1)
+        binding.extend_tree_candidates(sess.cfg, sess.packed, sess.k_cache, sess.v_cache, plen, ftok, fpar,
+                                       len(ftok) - 1, threshold, sess.logits, cand, sess.workspace)
     e1.record(stream)
     torch.cuda.synchronize()
     step_us = e0.elapsed_time(e1) * 1e3 / reps
-    log(f"draft tree: {iterations} steps in {dt * 1e3:.1f} ms, {len(tok)} nodes; one step {step_us:.1f} us")
+    steps = info["fed"]
+    host_us = (dt * 1e6 - steps * step_us) / steps
+    log(f"draft tree: {steps} steps in {dt * 1e3:.1f} ms, {len(tok)} nodes; one step {step_us:.1f} us on the "
+        f"device, {host_us:.1f} us of host per step")
     return {
         "iterations": iterations,
         "threshold": threshold,
         "nodes": len(tok),
         "ms": round(dt * 1e3, 3),
         "step_us": round(step_us, 2),
-        "what": ("one tree-decoder step per fed node (this model as the draft), logits row read back and "
-                 "threshold + branch pacer on the host; step_us: one step's kernel time at the last fed node"),
+        "host_us_per_step": round(host_us, 1),
+        "what": ("one tree-decoder step per fed node (this model as the draft), its candidate summary read back "
+                 "and the branch pacer on the host; step_us: one step's kernel time at the last fed node; "
+                 "host_us_per_step: the rest of each step (read-back, pacer, launch)"),
+    }
+
+
+def concurrent_draft(sess, shape, P, parent, tok, draft_model, reps=20):
+    """The speculative pipeline's overlap on one GPU (§3.4 runs draft
+    generation while the target verifies): a draft model's tree-decoder steps
+    issued on a second stream (default priority) while the target's
+    verification passes run on the first.  Every pass is one cooperative
+    launch with one workgroup per CU.  Times `reps` pairs (one verification
+    pass of the workload, one draft step: node 12 of a 12-node chain at the
+    same prefix length) issued one after the other on one stream, on two
+    streams with the whole grid each, and on two streams with the grid split
+    (the target's passes on 3/4 of the CUs, the draft's on 1/4); each alone
+    for reference.  Both sessions' pass status is checked after every mode."""
+    import numpy as np
+    import torch
+
+    import workloads
+    from paper_2309_04255_amd import binding
+
+    dshape = workloads.MODELS[draft_model]
+    dsess = binding.Session(dshape, capacity=P + 128, max_n=32)
+    dgen = workloads.make_weights(dshape, "cuda")
+    dsess.load_weights(dgen)
+    del dgen
+    dsess.prefill(workloads.draw_tokens(P, dshape.vocab, seed=7), 0)
+    dsess.check("draft prefill")
+    dtok = np.asarray(workloads.draw_tokens(12, dshape.vocab, seed=8))
+    dpar = np.arange(-1, 11)
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    G = torch.cuda.get_device_properties(0).multi_processor_count
+    grids = {"target": None, "draft": None}
+
+    def with_grid(g):
+        if g is None:
+            os.environ.pop("LLMCAD_PASS_GRID", None)
+        else:
+            os.environ["LLMCAD_PASS_GRID"] = str(g)
+
+    def verify(stream):
+        with_grid(grids["target"])
+        binding.verify_tree(sess.cfg, sess.packed, sess.k_cache, sess.v_cache, P, tok, parent, sess.logits,
+                            sess.path, sess.accept_len, sess.next_token, sess.workspace, stream=stream)
+
+    def step(stream):
+        with_grid(grids["draft"])
+        binding.extend_tree(dsess.cfg, dsess.packed, dsess.k_cache, dsess.v_cache, P, dtok, dpar, len(dtok) - 1,
+                            dsess.logits, dsess.workspace, stream=stream)
+
+    def run(mode):
+        grids["target"], grids["draft"] = (3 * G // 4, G // 4) if mode == "split" else (None, None)
+        for _ in range(2):  # warm-up
+            verify(main)
+            step(side if mode in ("concurrent", "split") else main)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(reps):
+            if mode != "draft":
+                verify(main)
+            if mode != "target":
+                step(side if mode in ("concurrent", "split") else main)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t) / reps * 1e3
+        with_grid(None)
+        sess.check(f"verification pass ({mode})")
+        dsess.check(f"draft step ({mode})")
+        return round(ms, 4)
+
+    saved_spin = os.environ.get("LLMCAD_SPIN_LIMIT")
+    os.environ["LLMCAD_SPIN_LIMIT"] = "400000"  # a pass that cannot gather its grid gives up quickly
+    out = {}
+    try:
+        for m in ("target", "draft", "serial", "concurrent", "split"):
+            try:
+                out[m] = run(m)
+            except binding.LlmcadPassError as e:  # (the workspace was re-initialised by the check)
+                torch.cuda.synchronize()
+                out[m] = f"failed: {e}"
+    finally:
+        if saved_spin is None:
+            os.environ.pop("LLMCAD_SPIN_LIMIT", None)
+        else:
+            os.environ["LLMCAD_SPIN_LIMIT"] = saved_spin
+        with_grid(None)
+    log(f"concurrent draft ({draft_model}): {out}")
+    return {
+        "draft_model": draft_model,
+        "ms_per_pair": out,
+        "what": ("ms per (31-node verification pass of the target, one tree-decoder step of the draft): "
+                 "target / draft alone, both on one stream (serial), on two streams with the whole grid each "
+                 "(concurrent), on two streams with the CUs split 3/4 target, 1/4 draft (split)"),
     }
 
 
@@ -459,7 +570,7 @@ def measure(sess, gen, wl, args, headline):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--steps", type=int, default=250)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama7b_p512_n31",
                     help="workload name, or several separated by commas (one JSON line each, in order)")
@@ -470,6 +581,8 @@ def main():
                     help="skip the generate-and-verify loop measurement")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="(profiling) first copy this many MiB three times: the counter calibration")
+    ap.add_argument("--concurrent-draft", metavar="DRAFT_MODEL", default=None,
+                    help="also time draft steps of DRAFT_MODEL on a second stream beside the first workload's passes")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the traffic file from two rocprofv3 --pmc counter CSVs and exit")
     args = ap.parse_args()
@@ -507,7 +620,12 @@ def main():
             cap = max(w.prefix_len for w in wls if w.model == wl.model) + 128
             sess, gen = setup_model(wl.shape, cap)
             model = wl.model
-        print(json.dumps(measure(sess, gen, wl, args, headline=i == 0)), flush=True)
+        line = measure(sess, gen, wl, args, headline=i == 0)
+        if i == 0 and args.concurrent_draft:
+            parent, tok = workloads.make_tree(wl.tree, wl.shape.vocab, wl.seed)
+            line["concurrent_draft"] = concurrent_draft(sess, wl.shape, wl.prefix_len, parent, tok,
+                                                        args.concurrent_draft)
+        print(json.dumps(line), flush=True)
     # Leave nothing of the library's behind for the interpreter's exit: no
     # timing events, no device buffers, no work in flight.
     binding.timing_enable(-1, 0)

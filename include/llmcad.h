@@ -259,6 +259,45 @@ int llmcad_extend_tree(const llmcad_config* cfg, const void* packed, void* k_cac
                        void* stream);
 
 /*
+ * A computed row's next-token distribution, summarised on the device for
+ * draft-tree growth (§3.1: the most likely token always extends the branch,
+ * and any other token whose probability exceeds the branch threshold starts a
+ * new branch; §3.2 Eq. 1: the branch pacer weighs candidates by their
+ * cumulative confidence).  Probabilities are the softmax of the row's fp32
+ * logits, exp(logit - max_logit) / sum_exp, in fp32.
+ */
+#define LLMCAD_CAND_MAX 64
+typedef struct {
+  int32_t count;     /* entries in tok/prob (1 .. LLMCAD_CAND_MAX); -1: more tokens than
+                        LLMCAD_CAND_MAX - 1 exceed the threshold (read the logits row instead) */
+  int32_t argmax;    /* the most likely token (lowest index among equal maxima) */
+  float max_logit;   /* the row's largest logit */
+  float sum_exp;     /* sum over the vocabulary of exp(logit - max_logit), fp32 */
+  int32_t tok[LLMCAD_CAND_MAX];  /* tok[0] = argmax, then every other token with probability >
+                                    threshold, by probability, higher first (ties: lower token first) */
+  float prob[LLMCAD_CAND_MAX];   /* their probabilities */
+} llmcad_candidates;
+
+/*
+ * A tree-decoder step (as llmcad_extend_tree) that also summarises each
+ * computed row's distribution: cand (device, [n - first] records, caller
+ * owned) receives, for row r (node first + r), the argmax, the softmax
+ * normaliser and every token whose probability exceeds `threshold`, so a
+ * draft driver reads back a few hundred bytes per fed node instead of the
+ * whole logits row.  logits (device fp32 [n - first][V]) is required: the
+ * summary is taken from the stored row.  The workgroup that completes the
+ * LM head's argmax builds the summaries at the end of the pass, in the same
+ * launch.  Asynchronous on `stream`; allocates nothing.
+ *
+ * Errors (checked on the host, nothing enqueued): as llmcad_extend_tree;
+ * LLMCAD_EARG if logits or cand is NULL or threshold is not in (0, 1).
+ */
+int llmcad_extend_tree_candidates(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                                  int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens,
+                                  const int32_t* parent, int32_t n, int32_t first, float threshold, float* logits,
+                                  llmcad_candidates* cand, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Rollback to the verified sequence after a verification pass (§3.2 "Token
  * tree verification and rectification": the tree is rolled back to the
  * verified sequence, which becomes the new input; §3.1: generation then

@@ -36,6 +36,7 @@ SYMBOLS = (
     "llmcad_prefill",
     "llmcad_commit_path",
     "llmcad_extend_tree",
+    "llmcad_extend_tree_candidates",
     "llmcad_status_string",
     "llmcad_workspace_region",
     "llmcad_timing_enable",
@@ -122,6 +123,8 @@ def _load():
         "llmcad_prefill": (ctypes.c_int, [CFG, P, P, P, I32, I32P, I32, I32, P, P, SZ, P]),
         "llmcad_commit_path": (ctypes.c_int, [CFG, P, P, I32, I32, P, P, I32, P]),
         "llmcad_extend_tree": (ctypes.c_int, [CFG, P, P, P, I32, I32, I32P, I32P, I32, I32, P, P, SZ, P]),
+        "llmcad_extend_tree_candidates": (ctypes.c_int, [CFG, P, P, P, I32, I32, I32P, I32P, I32, I32, ctypes.c_float,
+                                                         P, P, P, SZ, P]),
         "llmcad_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "llmcad_workspace_region": (ctypes.c_int, [CFG, I32, I32, ctypes.POINTER(SZ),
                                                    ctypes.POINTER(SZ)]),
@@ -293,6 +296,41 @@ def extend_tree(cfg, packed, k_cache, v_cache, prefix_len: int, tree_tokens, par
     return rc
 
 
+CAND_MAX = 64  # LLMCAD_CAND_MAX
+CAND_WORDS = 4 + 2 * CAND_MAX  # int32 words of one llmcad_candidates record
+
+
+def extend_tree_candidates(cfg, packed, k_cache, v_cache, prefix_len: int, tree_tokens, parent, first: int,
+                           threshold: float, logits, cand, workspace, stream=None, raise_on_error=True) -> int:
+    """Tree-decoder step with candidate summaries (see llmcad_extend_tree_candidates):
+    cand is a device int32 tensor of at least (n - first) x CAND_WORDS words."""
+    tok, tok_p = _i32(tree_tokens)
+    par, par_p = _i32(parent)
+    if len(par) != len(tok):
+        raise ValueError("tree_tokens and parent differ in length")
+    if cand.dtype != torch.int32 or cand.numel() < (len(tok) - first) * CAND_WORDS:
+        raise ValueError("cand must be an int32 device tensor of (n - first) records")
+    cap = k_cache.shape[-2]
+    rc = _lib.llmcad_extend_tree_candidates(
+        ctypes.byref(cfg), _ptr(packed), _ptr(k_cache), _ptr(v_cache), int(cap), int(prefix_len), tok_p, par_p,
+        int(len(tok)), int(first), float(threshold), _ptr(logits), _ptr(cand), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream))
+    if raise_on_error:
+        _check(rc, "llmcad_extend_tree_candidates")
+    return rc
+
+
+def parse_candidates(words):
+    """One llmcad_candidates record (int32 numpy array of CAND_WORDS words) ->
+    dict(count, argmax, max_logit, sum_exp, tok (list), prob (list))."""
+    w = np.asarray(words, dtype=np.int32)
+    f = w.view(np.float32)
+    count = int(w[0])
+    k = max(count, 0)
+    return {"count": count, "argmax": int(w[1]), "max_logit": float(f[2]), "sum_exp": float(f[3]),
+            "tok": [int(x) for x in w[4:4 + k]], "prob": [float(x) for x in f[4 + CAND_MAX:4 + CAND_MAX + k]]}
+
+
 def commit_path(cfg, k_cache, v_cache, prefix_len: int, path, accept_len, n: int, stream=None,
                 raise_on_error=True) -> int:
     """Rollback to the verified sequence: path/accept_len are the device outputs of the
@@ -401,6 +439,20 @@ class Session:
         extend_tree(self.cfg, self.packed, self.k_cache, self.v_cache, prefix_len, tree_tokens, parent, first,
                     self.logits, self.workspace)
         return self.logits[: n - first]
+
+    def extend_candidates(self, prefix_len, tree_tokens, parent, first, threshold):
+        """Forward of nodes [first, n) with candidate summaries; returns one parsed
+        record per computed row (synchronises; checks the device status)."""
+        rows = len(tree_tokens) - first
+        if not hasattr(self, "_cand"):
+            self._cand = torch.zeros((self.max_n, CAND_WORDS), dtype=torch.int32, device=self.device)
+            self._cand_host = torch.zeros((self.max_n, CAND_WORDS), dtype=torch.int32, pin_memory=True)
+        extend_tree_candidates(self.cfg, self.packed, self.k_cache, self.v_cache, prefix_len, tree_tokens, parent,
+                               first, threshold, self.logits, self._cand, self.workspace)
+        h = self._cand_host
+        h[:rows].copy_(self._cand[:rows], non_blocking=True)
+        self.check("tree-decoder step")
+        return [parse_candidates(h[i].numpy()) for i in range(rows)]
 
     def commit(self, prefix_len, n):
         """Roll the cache back to the verified sequence of the last verify_tree over n nodes."""

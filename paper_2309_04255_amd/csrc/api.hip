@@ -100,6 +100,8 @@ struct Pass {
   int* next_token;
   char* ws;
   hipStream_t st;
+  llmcad_candidates* cand = nullptr;  // candidate summaries of the computed rows, or null
+  float cand_thr = 0.0f;
 };
 
 // Device facts for the pass, looked up once per device.
@@ -245,6 +247,9 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   p.bar = (int*)(ws + W.bar);
   p.lm_val = (float*)(ws + W.lm_val);
   p.lm_idx = (int*)(ws + W.lm_idx);
+  p.lm_sum = (float*)(ws + W.lm_sum);
+  p.cand = a.cand;
+  p.cand_thr = a.cand_thr;
   p.amax = (int*)(ws + W.amax);
   p.logits = a.logits;
   p.row_lo = a.row_lo;
@@ -494,10 +499,17 @@ int llmcad_verify_tree_noalloc(const llmcad_config* cfg, const void* packed, voi
   return LLMCAD_OK;
 }
 
-int llmcad_extend_tree(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
-                       int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens, const int32_t* parent,
-                       int32_t n, int32_t first, float* logits, void* workspace, size_t workspace_bytes,
-                       void* stream) {
+}  // extern "C"
+
+namespace {
+
+static_assert(sizeof(llmcad_candidates) == (4 + 2 * LLMCAD_CAND_MAX) * 4, "candidate record layout");
+
+// llmcad_extend_tree, and with `cand` its candidate-summary variant.
+int extend_tree(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache, int32_t capacity,
+                int32_t prefix_len, const int32_t* tree_tokens, const int32_t* parent, int32_t n, int32_t first,
+                float* logits, llmcad_candidates* cand, float threshold, void* workspace, size_t workspace_bytes,
+                void* stream) {
   int rc = check_cfg(cfg);
   if (rc != LLMCAD_OK) return rc;
   if (!packed || !k_cache || !v_cache || !tree_tokens || !parent || !workspace) return LLMCAD_EARG;
@@ -536,7 +548,32 @@ int llmcad_extend_tree(const llmcad_config* cfg, const void* packed, void* k_cac
   a.next_token = sink + 129;
   a.ws = (char*)workspace;
   a.st = (hipStream_t)stream;
+  a.cand = cand;
+  a.cand_thr = threshold;
   return run_pass(a, tree);
+}
+
+}  // namespace
+
+extern "C" {
+
+int llmcad_extend_tree(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                       int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens, const int32_t* parent,
+                       int32_t n, int32_t first, float* logits, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  return extend_tree(cfg, packed, k_cache, v_cache, capacity, prefix_len, tree_tokens, parent, n, first, logits,
+                     nullptr, 0.0f, workspace, workspace_bytes, stream);
+}
+
+int llmcad_extend_tree_candidates(const llmcad_config* cfg, const void* packed, void* k_cache, void* v_cache,
+                                  int32_t capacity, int32_t prefix_len, const int32_t* tree_tokens,
+                                  const int32_t* parent, int32_t n, int32_t first, float threshold, float* logits,
+                                  llmcad_candidates* cand, void* workspace, size_t workspace_bytes, void* stream) {
+  const int rc = check_cfg(cfg);
+  if (rc != LLMCAD_OK) return rc;
+  if (!logits || !cand || !(threshold > 0.0f && threshold < 1.0f)) return LLMCAD_EARG;
+  return extend_tree(cfg, packed, k_cache, v_cache, capacity, prefix_len, tree_tokens, parent, n, first, logits,
+                     cand, threshold, workspace, workspace_bytes, stream);
 }
 
 int llmcad_commit_path(const llmcad_config* cfg, void* k_cache, void* v_cache, int32_t capacity,

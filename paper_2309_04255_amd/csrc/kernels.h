@@ -94,6 +94,11 @@ struct PassParams {
   int* grp_cnt;     // [O, down][kPassMaxGrid / 2] arrivals of the workgroups of each split-K group
   float* lm_val;    // [Mp][G] LM-head argmax per row and workgroup
   int* lm_idx;
+  float* lm_sum;    // [Mp][G] sum of exp(logit - the workgroup's max) over its columns (with cand)
+  // candidate summaries (llmcad_extend_tree_candidates): per computed row the
+  // argmax, softmax normaliser and every token above cand_thr, or null
+  llmcad_candidates* cand;
+  float cand_thr;
   int* amax;        // [Mp]
   // outputs
   float* logits;    // rows [row_lo, n) x V, or null

@@ -167,6 +167,7 @@ struct WorkspaceLayout {
   size_t amax;         // int32 [Mp]              per-node greedy token
   size_t lm_val;       // fp32 [Mp][G]            LM-head argmax per row and workgroup
   size_t lm_idx;       // int32 [Mp][G]
+  size_t lm_sum;       // fp32 [Mp][G]            its softmax normaliser (candidate summaries)
   size_t xs;           // fp32 [2L+1][Mp][d]      residual stream versions
   size_t xgs;          // bf16 [2L+1] x (Mp x d, fragment order)  bf16(x * g) (g: its norm's gain)
   size_t xnf;          // bf16 Mp x d, fragment order   the final norm's output bf16(x rstd g)
@@ -203,6 +204,7 @@ struct WorkspaceLayout {
     amax = take((size_t)Mp * 4);
     lm_val = take((size_t)G * Mp * 4);
     lm_idx = take((size_t)G * Mp * 4);
+    lm_sum = take((size_t)G * Mp * 4);
     xs = take((size_t)(2 * s.L + 1) * Mp * s.d * 4);
     xgs = take((size_t)(2 * s.L + 1) * Mp * s.d * 2);
     xnf = take((size_t)Mp * s.d * 2);

@@ -207,8 +207,16 @@ __device__ __forceinline__ bool grid_wait(const Sync& s, int phase, int G) {
 // ------------------------------------------------------------------ GEMM
 
 struct GemmLds {
-  float rstd[kMaxNodes];        // RMSNorm scale per row
-  float part_ss[1024];          // its partial sums
+  // (the LM head needs no RMSNorm scales: it reuses their room for its
+  // softmax normalisers)
+  union {
+    float rstd[kMaxNodes];      // RMSNorm scale per row
+    float best_s[kMaxNodes];    // LM head: sum of exp(logit - best_v) per row over this workgroup's blocks
+  };
+  union {
+    float part_ss[1024];        // its partial sums
+    float red_s[kMaxNodes][8];  // LM head: sum of exp(logit - red_v) per (row, block of the tile)
+  };
   float red_v[kMaxNodes][8];    // LM head: argmax per (row, block of the tile)
   int red_i[kMaxNodes][8];
   float best_v[kMaxNodes];      // LM head: argmax per row over this workgroup's blocks
@@ -948,17 +956,29 @@ __device__ __forceinline__ void epilogue_unit(KParams& p, const StepIo& io, cons
     }
   } else {  // EPI_LOGITS
     const bool vcol = col < p.V;
+    // (with candidate summaries the end of the pass reads the stored rows
+    // back: device-coherent stores)
+    const bool summ = p.cand != nullptr;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = 16 * rb + rr0 + i;
       const bool valid = vcol && r < p.n;
-      if (valid && p.logits != nullptr && r >= p.row_lo) stg(p.logits + (size_t)(r - p.row_lo) * p.V + col, v[i]);
+      if (valid && p.logits != nullptr && r >= p.row_lo) {
+        float* dst = p.logits + (size_t)(r - p.row_lo) * p.V + col;
+        if (summ)
+          st_coherent(dst, v[i]);
+        else
+          stg(dst, v[i]);
+      }
       float mv = valid ? v[i] : -INFINITY;
       int mi = valid ? col : 0x7fffffff;
       row16_argmax(mv, mi);  // argmax over the block's 16 columns
+      // the block's sum of exp(logit - its max), for the softmax normaliser
+      const float se = summ ? row16_sum(valid ? expf(v[i] - mv) : 0.0f) : 0.0f;
       if (j == 0) {
         gl.red_v[r][c] = mv;
         gl.red_i[r][c] = mi;
+        gl.red_s[r][c] = se;
       }
     }
   }
@@ -1089,6 +1109,89 @@ __device__ __forceinline__ void finish_walk(KParams& p, int entries, GemmLds& gl
   lds_barrier();
 }
 
+// (max, normaliser, argmax) of a set of logits merged with another set's:
+// the normalisers are sums of exp(logit - own max), rescaled to the larger
+// maximum; the argmax keeps the lowest index among equal maxima.
+__device__ __forceinline__ void softmax_merge(float& m, float& s, int& ix, float om, float os, int oi) {
+  const float mn = fmaxf(m, om);
+  s = (m == -INFINITY ? 0.0f : s * expf(m - mn)) + (om == -INFINITY ? 0.0f : os * expf(om - mn));
+  if (om > m || (om == m && oi < ix)) ix = oi;
+  m = mn;
+}
+
+// Candidate summaries of the computed rows (llmcad_extend_tree_candidates),
+// by the workgroup that completes the LM head's argmax, at the end of the
+// pass: per row, the workgroups' (max, argmax, normaliser) partials are
+// merged (one wave, in a fixed order), the stored logits row is scanned once
+// for every token whose probability exp(logit - max) / normaliser exceeds
+// the threshold, and the argmax and those tokens are written sorted by
+// probability, higher first (ties: lower token first).  `lds`: the GEMM
+// tiles' region, free once the phase's tiles are done.
+__device__ __attribute__((noinline, not_tail_called)) void finish_candidates(KParams& pin, int entries, char* lds) {
+  KParams& p = uniform_params(pin);
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  float* sm = (float*)lds;       // the row's max and normaliser
+  int* si = (int*)(lds + 64);    // its argmax and the candidate count
+  int* ctok = (int*)(lds + 1024);
+  float* cprob = (float*)(lds + 1024 + 4 * LLMCAD_CAND_MAX);
+  const int G = p.G, V = p.V;
+  for (int r = p.row_lo; r < p.n; ++r) {
+    if (wave == 0) {
+      float m = -INFINITY, s = 0.0f;
+      int ix = 0x7fffffff;
+      for (int t = lane; t < entries; t += 64)
+        softmax_merge(m, s, ix, ld_coherent(&p.lm_val[(size_t)r * G + t]), ld_coherent(&p.lm_sum[(size_t)r * G + t]),
+                      ld_coherent(&p.lm_idx[(size_t)r * G + t]));
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        const float om = __shfl_xor(m, off, kWave), os = __shfl_xor(s, off, kWave);
+        const int oi = __shfl_xor(ix, off, kWave);
+        softmax_merge(m, s, ix, om, os, oi);
+      }
+      if (lane == 0) {
+        sm[0] = m;
+        sm[1] = s;
+        si[0] = ix;
+        si[1] = 0;
+      }
+    }
+    __syncthreads();
+    const float M = sm[0], S = sm[1], thr = p.cand_thr;
+    const int amax = si[0];
+    const float* row = p.logits + (size_t)(r - p.row_lo) * V;
+    for (int v = threadIdx.x; v < V; v += kThreads) {
+      const float pr = expf(ld_coherent(row + v) - M) / S;
+      if (pr > thr || v == amax) {
+        const int k = atomicAdd(&si[1], 1);
+        if (k < LLMCAD_CAND_MAX) {
+          ctok[k] = v;
+          cprob[k] = pr;
+        }
+      }
+    }
+    __syncthreads();
+    const int cnt = si[1];
+    llmcad_candidates* rec = p.cand + (r - p.row_lo);
+    if (wave == 0) {
+      if (cnt <= LLMCAD_CAND_MAX && lane < cnt) {
+        const float mine = cprob[lane];
+        const int mt = ctok[lane];
+        int rank = 0;
+        for (int j = 0; j < cnt; ++j) rank += (cprob[j] > mine || (cprob[j] == mine && ctok[j] < mt)) ? 1 : 0;
+        stg(&rec->tok[rank], mt);
+        stg(&rec->prob[rank], mine);
+      }
+      if (lane == 0) {
+        stg(&rec->count, cnt <= LLMCAD_CAND_MAX ? cnt : -1);
+        stg(&rec->argmax, amax);
+        stg(&rec->max_logit, M);
+        stg(&rec->sum_exp, S);
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // The epilogue of one tile (blocks [nb0, nb0 + cw)): the waves take its
 // units in turn.  The LM head also folds the tile's per-block argmax into
 // the workgroup's running argmax per row.  A function of its own so that its
@@ -1111,12 +1214,18 @@ __device__ __attribute__((noinline, not_tail_called)) void finish_tile(KParams& 
   }
   if constexpr (EPI == EPI_LOGITS) {
     __syncthreads();
+    const bool summ = p.cand != nullptr;
     for (int r = threadIdx.x; r < 16 * MB; r += kThreads) {
       float mv = gl.best_v[r];
       int mi = gl.best_i[r];
+      float ms = gl.best_s[r];
       for (int c = 0; c < cw; ++c) {
         const float v = gl.red_v[r][c];
         const int i = gl.red_i[r][c];
+        if (summ) {  // the normalisers, relative to the larger of the two maxima
+          const float mn = fmaxf(mv, v);
+          ms = (mv == -INFINITY ? 0.0f : ms * expf(mv - mn)) + (v == -INFINITY ? 0.0f : gl.red_s[r][c] * expf(v - mn));
+        }
         if (v > mv || (v == mv && i < mi)) {
           mv = v;
           mi = i;
@@ -1124,6 +1233,7 @@ __device__ __attribute__((noinline, not_tail_called)) void finish_tile(KParams& 
       }
       gl.best_v[r] = mv;
       gl.best_i[r] = mi;
+      gl.best_s[r] = ms;
     }
   }
   __syncthreads();
@@ -1299,6 +1409,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
     for (int r = threadIdx.x; r < 16 * MB; r += kThreads) {
       gl.best_v[r] = -INFINITY;
       gl.best_i[r] = 0x7fffffff;
+      gl.best_s[r] = 0.0f;
     }
   }
   if (lo >= hi) {
@@ -1324,11 +1435,15 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
     for (int r = threadIdx.x; r < 16 * MB; r += kThreads) {
       st_coherent(&p.lm_val[(size_t)r * G + blockIdx.x], gl.best_v[r]);
       st_coherent(&p.lm_idx[(size_t)r * G + blockIdx.x], gl.best_i[r]);
+      if (p.cand != nullptr) st_coherent(&p.lm_sum[(size_t)r * G + blockIdx.x], gl.best_s[r]);
     }
-    if (arrive_last(p.lm_cnt, G, lds_flag) && p.m0 == 0) {
-      trace_mark(sy, phase, 6);
-      finish_walk(p, G, gl);
-      trace_mark(sy, phase, 7);
+    if (arrive_last(p.lm_cnt, G, lds_flag)) {
+      if (p.m0 == 0) {
+        trace_mark(sy, phase, 6);
+        finish_walk(p, G, gl);
+        trace_mark(sy, phase, 7);
+      }
+      if (p.cand != nullptr) finish_candidates(p, G, lds);
     }
   }
   return true;

@@ -19,11 +19,16 @@ the first step whose tree-cumulative confidence T_c (the largest cumulative
 confidence of a pending candidate) is below alpha, and the target verifies;
 `Fallback` updates alpha after each verification (Eq. 3).
 
-Host control: the probabilities of one row (float64 softmax of the returned
-logits) and the pacer's choice are computed on the host between steps, which
-need the host anyway (the next node depends on them).  Nodes are numbered in
-feeding order; the returned tree lists the fed nodes, then the candidates not
-yet fed as leaves.
+Each step is one llmcad_extend_tree_candidates call: the library returns the
+fed node's candidates -- its most likely token and every token whose
+probability exceeds the threshold, with their probabilities (the softmax of
+the node's logits, computed on the GPU in the same launch) -- so the host
+reads back one small record per step, not the logits row.  Only when more
+tokens exceed the threshold than a record holds (thresholds below 1/63) does
+the driver read the row and take the float64 softmax itself.  The pacer's
+choice is made on the host between steps (the next node depends on it).
+Nodes are numbered in feeding order; the returned tree lists the fed nodes,
+then the candidates not yet fed as leaves.
 """
 
 import numpy as np
@@ -40,18 +45,14 @@ class _Tree:
     def size(self):
         return len(self.tok) + len(self.cand)
 
-    def add_candidates(self, node, prob, threshold, max_nodes):
-        # the most likely token (lowest index among equal maxima), then every
-        # other token above the threshold, most likely first (ties: lower
-        # index), while the tree has fewer than max_nodes nodes
-        best = int(np.argmax(prob))
-        over = np.flatnonzero(prob > threshold)
-        over = over[over != best]
-        over = over[np.argsort(-prob[over], kind="stable")]
-        for i, t in enumerate([best] + [int(x) for x in over]):
+    def add_candidates(self, node, toks, probs, max_nodes):
+        # toks/probs: the most likely token (lowest index among equal maxima),
+        # then every other token above the threshold, most likely first (ties:
+        # lower index); added while the tree has fewer than max_nodes nodes
+        for i, (t, pr) in enumerate(zip(toks, probs)):
             if i > 0 and self.size() >= max_nodes:
                 break
-            self.cand.append([t, node, float(prob[t])])
+            self.cand.append([int(t), node, float(pr)])
 
     def pick(self, budget):
         conf = np.array([self.cum[q] * p for _, q, p in self.cand])
@@ -74,14 +75,28 @@ def _probs(logits_row):
     return z / z.sum()
 
 
+def candidates_from_row(logits_row, threshold):
+    """(tokens, probabilities) of a logits row on the host: the argmax, then
+    every other token whose float64 softmax probability exceeds the
+    threshold, most likely first (ties: lower index)."""
+    prob = _probs(logits_row)
+    best = int(np.argmax(prob))
+    over = np.flatnonzero(prob > threshold)
+    over = over[over != best]
+    over = over[np.argsort(-prob[over], kind="stable")]
+    toks = [best] + [int(x) for x in over]
+    return toks, [float(prob[t]) for t in toks]
+
+
 def generate_tree(sess, prefix_len: int, root_token: int, iterations: int, threshold: float = 0.3,
-                  alpha: float | None = None, max_nodes: int | None = None):
+                  alpha: float | None = None, max_nodes: int | None = None, keep_rows: bool = False):
     """Grow a draft tree with `iterations` fed nodes after the root (at most,
     when `alpha` is given: see the module docstring), on the draft model in
     `sess`.  Returns (tree_tokens, parent, info): the tree for
     verification (fed nodes, then the pending candidates), and info with the
-    number of fed nodes, each fed node's probability, the fed nodes' logits
-    rows and T_c after each step ("fed", "conf", "logits", "t_c").
+    number of fed nodes, each fed node's probability, T_c after each step,
+    every fed node's candidates (tokens, probabilities) and, with keep_rows,
+    the fed nodes' logits rows ("fed", "conf", "t_c", "cands", "logits").
 
     The tree never exceeds max_nodes nodes (default: the session's max_n, the
     largest tree its verifier's workspace takes): candidates past the cap are
@@ -93,12 +108,18 @@ def generate_tree(sess, prefix_len: int, root_token: int, iterations: int, thres
     if max_nodes < 2:
         raise ValueError("a draft tree needs room for at least two nodes")
     tree = _Tree(root_token)
-    rows, t_c = [], []
+    rows, t_c, cands = [], [], []
     node = 0
     for it in range(iterations + 1):
-        row = sess.extend(prefix_len, np.asarray(tree.tok), np.asarray(tree.par), node)[0]
-        rows.append(row.float().cpu().numpy())
-        tree.add_candidates(node, _probs(rows[-1]), threshold, max_nodes)
+        rec = sess.extend_candidates(prefix_len, np.asarray(tree.tok), np.asarray(tree.par), node, threshold)[0]
+        if keep_rows or rec["count"] < 1:
+            rows.append(sess.logits[0].float().cpu().numpy())
+        if rec["count"] >= 1:
+            toks, probs = rec["tok"], rec["prob"]
+        else:  # (more tokens above the threshold than a record holds)
+            toks, probs = candidates_from_row(rows[-1], threshold)
+        cands.append((toks, probs))
+        tree.add_candidates(node, toks, probs, max_nodes)
         t_c.append(max(tree.cum[q] * p for _, q, p in tree.cand))
         if it == iterations or (alpha is not None and t_c[-1] < alpha) or tree.size() >= max_nodes:
             break
@@ -107,7 +128,8 @@ def generate_tree(sess, prefix_len: int, root_token: int, iterations: int, thres
     tok = np.asarray(tree.tok + [c[0] for c in tree.cand], dtype=np.int32)
     par = np.asarray(tree.par + [c[1] for c in tree.cand], dtype=np.int32)
     conf = [1.0] + [tree.cum[i] / tree.cum[tree.par[i]] for i in range(1, len(tree.tok))]
-    return tok, par, {"fed": len(tree.tok), "conf": conf, "logits": np.stack(rows), "t_c": t_c}
+    return tok, par, {"fed": len(tree.tok), "conf": conf, "t_c": t_c, "cands": cands,
+                      "logits": np.stack(rows) if keep_rows else None}
 
 
 class Fallback:

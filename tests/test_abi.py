@@ -254,3 +254,37 @@ def test_extend_validation(binding):
     assert call(1, t=np.array([1, 2, cfg.vocab], dtype=np.int32)) == binding.ETREE
     assert call(1, prefix_len=62) == binding.ECAPACITY
     assert call(1, ws=100) == binding.EWORKSPACE
+
+
+def test_extend_candidates_validation(binding):
+    # Host-side checks of the tree-decoder step with candidate summaries:
+    # logits and the record buffer are required, the threshold lies in (0, 1),
+    # and the tree checks of llmcad_extend_tree apply; nothing is enqueued.
+    cfg = binding.make_config(workloads.MODELS["tiny"])
+    lib = binding.lib()
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    fake = ctypes.c_void_p(256)
+    tok = np.array([1, 2, 3], dtype=np.int32)
+    par = np.array([-1, 0, 1], dtype=np.int32)
+
+    def call(first=2, thr=0.3, logits=fake, cand=fake, t=tok, p=par, ws=1 << 30):
+        return lib.llmcad_extend_tree_candidates(ctypes.byref(cfg), fake, fake, fake, 64, 10,
+                                                 t.ctypes.data_as(I32P), p.ctypes.data_as(I32P), 3, first,
+                                                 ctypes.c_float(thr), logits, cand, fake, ws, None)
+
+    assert call(logits=None) == binding.EARG
+    assert call(cand=None) == binding.EARG
+    for thr in (0.0, 1.0, -0.5, float("nan")):
+        assert call(thr=thr) == binding.EARG, thr
+    assert call(first=3) == binding.ETREE
+    assert call(p=np.array([-1, 0, 2], dtype=np.int32)) == binding.ETREE
+    assert call(ws=100) == binding.EWORKSPACE
+    # the record layout the binding parses: 4 header words, then CAND_MAX tokens and probabilities
+    assert binding.CAND_WORDS == 4 + 2 * binding.CAND_MAX == 132
+    w = np.zeros(binding.CAND_WORDS, dtype=np.int32)
+    w[0], w[1] = 2, 7
+    w[2:4] = np.array([3.5, 1.25], dtype=np.float32).view(np.int32)
+    w[4:6] = [7, 9]
+    w[4 + binding.CAND_MAX:6 + binding.CAND_MAX] = np.array([0.5, 0.25], dtype=np.float32).view(np.int32)
+    rec = binding.parse_candidates(w)
+    assert rec == {"count": 2, "argmax": 7, "max_logit": 3.5, "sum_exp": 1.25, "tok": [7, 9], "prob": [0.5, 0.25]}

@@ -1,8 +1,10 @@
 """The GPU draft driver's host policy (branch threshold, §3.1; branch pacer,
 §3.2 Eq. 1) against the oracle's generator, on the CPU: a stand-in session
-serves logits rows from a table, so both sides see the same probabilities and
-must make the same integer decisions (which candidates, in which order, which
-branch grows)."""
+serves logits rows from a table -- and, for the candidates entry point, the
+record the library builds from such a row (the argmax and every token above
+the threshold, by probability) -- so both sides see the same probabilities
+and must make the same integer decisions (which candidates, in which order,
+which branch grows)."""
 
 import numpy as np
 import pytest
@@ -12,18 +14,39 @@ import oracle
 from paper_2309_04255_amd import draft
 
 
+CAND_MAX = 64  # entries of one candidate record (llmcad_candidates)
+
+
 class TableSession:
-    """Answers a tree-decoder step for the node `first` with the row forward(tokens, parent)."""
+    """Answers a tree-decoder step for the node `first` with the row
+    forward(tokens, parent): as logits (extend), or as the candidate record
+    of that row (extend_candidates; float64 softmax, the argmax first, then
+    the tokens above the threshold by probability, ties to the lower token;
+    count -1 when more than CAND_MAX - 1 exceed it)."""
 
     def __init__(self, forward):
         self.forward = forward
         self.calls = 0
+        self.logits = None
 
     def extend(self, prefix_len, tree_tokens, parent, first):
         assert first == len(tree_tokens) - 1  # one new node per step
         self.calls += 1
         row = self.forward(np.asarray(tree_tokens), np.asarray(parent))
-        return torch.from_numpy(np.asarray(row, dtype=np.float32)[None, :])
+        self.logits = torch.from_numpy(np.asarray(row, dtype=np.float32)[None, :])
+        return self.logits
+
+    def extend_candidates(self, prefix_len, tree_tokens, parent, first, threshold):
+        row = self.extend(prefix_len, tree_tokens, parent, first)[0].numpy().astype(np.float64)
+        e = np.exp(row - row.max())
+        prob = e / e.sum()
+        best = int(np.flatnonzero(row == row.max())[0])
+        others = sorted((v for v in range(len(row)) if prob[v] > threshold and v != best),
+                        key=lambda v: (-prob[v], v))
+        toks = [best] + others
+        if len(toks) > CAND_MAX:
+            return [{"count": -1, "argmax": best, "tok": [], "prob": []}]
+        return [{"count": len(toks), "argmax": best, "tok": toks, "prob": [float(prob[v]) for v in toks]}]
 
     def check(self, what=""):
         pass  # (no device: nothing can fail)
@@ -131,3 +154,25 @@ def test_flat_wide_rows_stay_within_the_verifier_cap(max_nodes):
     # every fed node beyond the root got its most likely successor as a child
     for q in range(info["fed"]):
         assert q in set(int(x) for x in par[1:]), q
+
+
+def test_record_overflow_reads_the_row():
+    # More tokens above the threshold than a candidate record holds: the
+    # driver takes the logits row and its own float64 softmax, and still makes
+    # the oracle's decisions.
+    vocab = 256
+
+    def forward(tokens, parent):
+        key = hash(("many", tuple(int(t) for t in tokens), tuple(int(q) for q in parent))) & 0xFFFFFFFF
+        g = np.random.default_rng(key)
+        row = np.full(vocab, -9.0)
+        row[g.choice(vocab, 120, replace=False)] = g.uniform(0.0, 0.1, 120)
+        return row.astype(np.float32)
+
+    sess = TableSession(forward)
+    tok, par, info = draft.generate_tree(sess, 0, 5, 2, threshold=0.005, max_nodes=128)
+    otok, opar, oinfo = oracle.generate_tree(None, None, None, 5, 2, threshold=0.005, max_nodes=128,
+                                             forward=lambda t, p: forward(t, p).astype(np.float64))
+    assert len(info["cands"][0][0]) > CAND_MAX  # the fallback ran
+    np.testing.assert_array_equal(tok, otok)
+    np.testing.assert_array_equal(par, opar)

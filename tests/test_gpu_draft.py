@@ -5,8 +5,15 @@ pacer, Eq. 1).
 Per case:
 1. forward: the logits row the GPU returned for every fed node matches the
    oracle's one-pass masked forward over the fed nodes;
-2. policy: the oracle's generator, handed the GPU's own rows, builds the
-   GPU's tree exactly (same probabilities in, integer decisions out).
+2. candidates: each fed node's record from the library (its argmax and every
+   token above the threshold, with fp32 softmax probabilities computed in the
+   same launch) is the float64 softmax of the GPU's own row: the same argmax,
+   the same tokens above the threshold (tokens within 1e-5 of it may fall
+   either way), probabilities within 1e-5 relative, most likely first;
+3. policy: the oracle's generator, handed the GPU's candidate probabilities
+   (as a row whose softmax gives them back: their logarithms, the remaining
+   mass spread evenly over the other tokens), builds the GPU's tree exactly
+   (same probabilities in, integer decisions out).
 
 The draft model is a small random LLaMA-shaped decoder whose weight scale
 (std 0.3) gives next-token distributions like a trained draft's (top-1
@@ -62,7 +69,7 @@ def test_draft_tree_matches_oracle(draft_model, threshold, seed, iterations, alp
     what = f"thr={threshold} seed={seed} it={iterations} alpha={alpha}"
     print(f"\n[draft] {what}", flush=True)
     sess.prefill(prefix, 0)
-    tok, par, info = draft.generate_tree(sess, P, root, iterations, threshold, alpha=alpha)
+    tok, par, info = draft.generate_tree(sess, P, root, iterations, threshold, alpha=alpha, keep_rows=True)
     fed = info["fed"]
     assert len(tok) > fed
     if alpha is None:
@@ -85,11 +92,27 @@ def test_draft_tree_matches_oracle(draft_model, threshold, seed, iterations, alp
           f"(rounding spread {spread:.2e} / {spread_rel:.2e})", flush=True)
     assert err <= 2 * spread and rel <= 2 * spread_rel, (what, err, spread, rel, spread_rel)
 
-    # 2. the oracle's policy on the GPU's rows builds the GPU's tree
+    # 2. the library's candidates are the float64 softmax of the GPU's rows
+    for q in range(fed):
+        toks, probs = info["cands"][q]
+        p64 = _softmax(gpu_rows[q])
+        assert toks[0] == int(np.argmax(gpu_rows[q])), (what, q)
+        np.testing.assert_allclose(probs, p64[toks], rtol=1e-5)
+        assert all(a >= b for a, b in zip(probs, probs[1:])), (what, q, probs)
+        near = np.abs(p64 - threshold) <= 1e-5 * threshold
+        want = set(np.flatnonzero((p64 > threshold) & ~near).tolist()) - {toks[0]}
+        got = set(toks[1:])
+        assert want <= got and got <= want | set(np.flatnonzero(near).tolist()), (what, q, want, got)
+
+    # 3. the oracle's policy on the GPU's candidate probabilities builds the GPU's tree
     def replay(tokens, parent):
         np.testing.assert_array_equal(tokens, tok[:len(tokens)])
         np.testing.assert_array_equal(parent, par[:len(parent)])
-        return gpu_rows[len(tokens) - 1]
+        toks, probs = info["cands"][len(tokens) - 1]
+        rest = (1.0 - sum(probs)) / (DRAFT.vocab - len(toks))
+        row = np.full(DRAFT.vocab, np.log(max(rest, 1e-300)))
+        row[toks] = np.log(probs)
+        return row
 
     otok, opar, oinfo = oracle.generate_tree(None, None, None, root, iterations, threshold, forward=replay,
                                              alpha=alpha)

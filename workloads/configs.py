@@ -45,6 +45,9 @@ MODELS = {
     "llama7b": ModelShape("llama7b", 32, 4096, 32, 128, 11008, 32000, seed=0x5EED0007),
     "llama13b": ModelShape("llama13b", 40, 5120, 40, 128, 13824, 32000, seed=0x5EED0013),
     "llama30b": ModelShape("llama30b", 60, 6656, 52, 128, 17920, 32000, seed=0x5EED0030),
+    # a ~1B draft model for the 7B-class targets (TinyLlama's depth and widths,
+    # as many K/V heads as query heads)
+    "draft1b": ModelShape("draft1b", 22, 2048, 16, 128, 5632, 32000, seed=0x5EED0001B),
     # 4-bit weight-only targets (the paper's phone models are INT4, §4.1).  The
     # small one has a ragged vocabulary (not a multiple of 16) and more than
     # one scale group per matrix row everywhere.
