@@ -55,7 +55,7 @@ constexpr int kThreads = 64 * kWaves;
 // Tuning constants of the GEMM phases (the defaults were measured best on the
 // LLaMA-7B workload; -D overrides them for sweeps): the VGPRs (in units of 4)
 // a tile's register pipeline may hold, its depth for one-block and for wider
-// tiles, and the widest tile (in 16-column blocks) at 128 rows.
+// tiles, and the widest tile (in 16-column blocks) at 128 and at 64 rows.
 #ifndef LLMCAD_STAGE_REGS
 #define LLMCAD_STAGE_REGS 40
 #endif
@@ -67,6 +67,9 @@ constexpr int kThreads = 64 * kWaves;
 #endif
 #ifndef LLMCAD_TILE_BLOCKS_MB8
 #define LLMCAD_TILE_BLOCKS_MB8 4
+#endif
+#ifndef LLMCAD_TILE_BLOCKS_MB4
+#define LLMCAD_TILE_BLOCKS_MB4 6
 #endif
 
 enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
@@ -248,8 +251,10 @@ constexpr int kGemmLdsBytes = 142 * 1024;
 __host__ __device__ constexpr int tw_off() { return 0; }
 __host__ __device__ constexpr int epi_off(int cw, int MB, int SL) { return SL * cw * MB * 1024; }
 __host__ __device__ constexpr int wl_off(int cw, int MB, int SL) { return ((SL + 1) * cw * MB + cw) * 1024; }
-// partial-tile slots of a tile: four, or two when four do not fit
-__host__ __device__ constexpr int tile_slots(int cw, int MB) { return wl_off(cw, MB, 4) <= kGemmLdsBytes ? 4 : 2; }
+// partial-tile slots of a tile: four, or two (or one) when four (two) do not fit
+__host__ __device__ constexpr int tile_slots(int cw, int MB) {
+  return wl_off(cw, MB, 4) <= kGemmLdsBytes ? 4 : wl_off(cw, MB, 2) <= kGemmLdsBytes ? 2 : 1;
+}
 
 // Direct global -> LDS copy of 16 bytes per lane: lane l's bytes land at
 // lds + 16 l.  `lds` must be the same in every lane.
@@ -566,8 +571,23 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   }
   // This wave's partial tile -> LDS; the epilogue adds the four in wave
   // order.  With two slots, waves 2 and 3 hand theirs to waves 0 and 1
-  // first, and the epilogue adds (w0 + w2) + (w1 + w3).
-  if constexpr (SL == 2) {
+  // first, and the epilogue adds (w0 + w2) + (w1 + w3); with one, the waves
+  // add theirs into it in turn: ((w3 + w2) + w1) + w0.
+  if constexpr (SL == 1) {
+#pragma unroll 1
+    for (int w = kWaves - 1; w >= 0; --w) {
+      if (wave == w) {
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+#pragma unroll
+          for (int rb = 0; rb < MB; ++rb) {
+            char* at1 = lds + tw_off() + ((size_t)(c * MB + rb) * 64 + lane) * 16;
+            lds_st<f32x4>(at1, w == kWaves - 1 ? acc[rb][c] : lds_ld<f32x4>(at1) + acc[rb][c]);
+          }
+      }
+      __syncthreads();
+    }
+  } else if constexpr (SL == 2) {
     if (wave >= 2) {
 #pragma unroll
       for (int c = 0; c < C; ++c)
@@ -1311,7 +1331,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool split_phase(KParams& 
   phase = wave_uniform(phase);
   const Sync sy = make_sync(p, lds_flag);
   const StepPlan& sp = p.step[step];
-  constexpr int CM = MB <= 2 ? 8 : MB == 4 ? 4 : LLMCAD_TILE_BLOCKS_MB8;
+  constexpr int CM = MB <= 2 ? 8 : MB == 4 ? LLMCAD_TILE_BLOCKS_MB4 : LLMCAD_TILE_BLOCKS_MB8;
   const int S = wave_uniform(sp.split), G = p.G, NG = G / S;
   const int nbk = sp.nblocks, ks = sp.ksteps;
   const int vw = virtual_wg(G);
@@ -1394,7 +1414,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   phase = wave_uniform(phase);
   const Sync sy = make_sync(p, lds_flag);
   const StepPlan& sp = p.step[step];
-  constexpr int CM = MB <= 2 ? 8 : MB == 4 ? 4 : LLMCAD_TILE_BLOCKS_MB8;
+  constexpr int CM = MB <= 2 ? 8 : MB == 4 ? LLMCAD_TILE_BLOCKS_MB4 : LLMCAD_TILE_BLOCKS_MB8;
   static_assert(wl_off(CM, MB, tile_slots(CM, MB)) <= kGemmLdsBytes,
                 "a tile's partial sums and epilogue inputs fit the LDS");
   // 4-bit tiles hold a second set of accumulators (each group's partial sums)
