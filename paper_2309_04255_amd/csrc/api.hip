@@ -260,7 +260,14 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   // (diagnostics, for tests of the failure path: every grid wait gives up at
   // once, so the pass ends with status 1 and every workgroup exits normally)
   if (env_int("LLMCAD_FAIL_WAITS", 0) == 1) p.spin_limit = -1;
-  p.wl_cap = env_int("LLMCAD_WL_STAGES", 1 << 20);  // (diagnostics: a smaller pre-barrier copy)
+  // (diagnostics: a smaller pre-barrier copy, for every step or for one:
+  // LLMCAD_WL_STAGES_QKV / _O / _GU / _DOWN / _LM)
+  {
+    const int all = env_int("LLMCAD_WL_STAGES", 1 << 20);
+    const char* names[kSteps] = {"LLMCAD_WL_STAGES_QKV", "LLMCAD_WL_STAGES_O", "LLMCAD_WL_STAGES_GU",
+                                 "LLMCAD_WL_STAGES_DOWN", "LLMCAD_WL_STAGES_LM"};
+    for (int i = 0; i < kSteps; ++i) p.step[i].wl_cap = env_int(names[i], all);
+  }
   // (diagnostics: LLMCAD_ATTN_PREFETCH=2 fetches every attention step after the barrier)
   p.attn_prefetch = env_int("LLMCAD_ATTN_PREFETCH", 1) == 2 ? 0 : 1;
   p.trace = env_int("LLMCAD_TRACE", 0) ? (long long*)(ws + W.trace) : nullptr;

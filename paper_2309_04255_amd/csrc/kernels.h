@@ -46,6 +46,7 @@ struct StepPlan {
   int layer_rel;        // 1 if w_off is relative to the layer's start
   int q4;               // 1: 4-bit codes with group scales
   int split;            // split-K: workgroups sharing each group of column blocks (1: none; 2 or 4)
+  int wl_cap;           // weight stages per wave copied to LDS before the step's barrier, at most
 };
 
 // Must stay the first kernel argument of the pass kernel.
@@ -108,7 +109,6 @@ struct PassParams {
   int* next_token;
   // control
   int spin_limit;    // bound of every wait loop (polls)
-  int wl_cap;        // weight stages per wave copied to LDS before a barrier, at most
   int attn_prefetch; // 1: the attention fetches its prefix steps before its barrier (0: all after)
   long long* trace;  // diagnostics: [G][4 + 5L][8] phase timestamps, or null
 };

@@ -399,7 +399,8 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   // barrier (P a multiple of D, as many as fit); the register pipeline
   // starts at stage P.
   constexpr int PMAX = WL_STAGES / D * D;
-  const int pcap = wave_uniform(p.wl_cap < PMAX ? p.wl_cap / D * D : PMAX);
+  const int wcap = wave_uniform(p.step[step].wl_cap);
+  const int pcap = wave_uniform(wcap < PMAX ? wcap / D * D : PMAX);
   const int P = wave_uniform(wait_phase >= 0 ? (ns / D * D < pcap ? ns / D * D : pcap) : 0);
   char* wl = lds + wl_off(C, MB, SL) + (size_t)wave * PMAX * C * 1024;
   auto load_w = [&](int slot, int i, bool want) {  // stage i, or nothing (zero line)
