@@ -93,3 +93,59 @@ def test_extend_from_zero_is_the_verification_forward(model):
     m.sess.verify_tree(P, tok, parent)
     ver = m.sess.logits[:n].float().cpu().numpy()
     np.testing.assert_array_equal(ext, ver)
+
+
+def _softmax64(row):
+    z = np.asarray(row, dtype=np.float64)
+    z = np.exp(z - z.max())
+    return z / z.sum()
+
+
+@pytest.mark.parametrize("first,threshold", [(0, 0.01), (5, 0.002), (0, 0.3)])
+def test_candidate_records_every_row(model, first, threshold):
+    # llmcad_extend_tree_candidates over several rows at once (a binary tree of
+    # 15 nodes, all of it or its nodes 5..14): each row's record is the float64
+    # softmax of the logits row the same call stored -- the argmax first, then
+    # every other token above the threshold (tokens within 1e-5 relative of it
+    # may fall either way), higher probability first, probabilities within
+    # 1e-5 relative -- and the row's max and normaliser.  The logits equal the
+    # plain tree-decoder step's bit for bit.
+    from paper_2309_04255_amd import binding
+
+    parent = workloads.complete_tree((2, 2, 2))
+    tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=77, stream=3)
+    n = len(parent)
+    plain = model.sess.extend(P, tok, parent, first).float().cpu().numpy()
+    recs = model.sess.extend_candidates(P, tok, parent, first, threshold)
+    rows = model.sess.logits[:n - first].float().cpu().numpy()
+    np.testing.assert_array_equal(rows, plain)
+    assert len(recs) == n - first
+    for r, rec in enumerate(recs):
+        p64 = _softmax64(rows[r])
+        assert rec["argmax"] == int(np.argmax(rows[r]))
+        assert rec["max_logit"] == float(rows[r].max())
+        np.testing.assert_allclose(rec["sum_exp"], np.exp(rows[r].astype(np.float64) - rows[r].max()).sum(),
+                                   rtol=1e-5)
+        assert 1 <= rec["count"] <= binding.CAND_MAX, rec["count"]
+        toks, probs = rec["tok"], rec["prob"]
+        assert toks[0] == rec["argmax"]
+        np.testing.assert_allclose(probs, p64[toks], rtol=1e-5)
+        assert all(a > b or (a == b and s < t) for a, b, s, t in zip(probs, probs[1:], toks, toks[1:]))
+        near = np.abs(p64 - threshold) <= 1e-5 * threshold
+        want = set(np.flatnonzero((p64 > threshold) & ~near).tolist()) - {toks[0]}
+        assert want <= set(toks[1:]) <= want | set(np.flatnonzero(near).tolist()), (r, want, toks)
+
+
+def test_candidate_records_overflow(model):
+    # A threshold below 1/64 on these near-uniform rows puts far more than 63
+    # tokens above it: every record says so (count -1) and still carries the
+    # argmax, the max and the normaliser, so a driver can fall back to the row.
+    parent = workloads.complete_tree((2, 2))
+    tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=78, stream=3)
+    recs = model.sess.extend_candidates(P, tok, parent, 0, 1e-4)
+    rows = model.sess.logits[:len(parent)].float().cpu().numpy()
+    for r, rec in enumerate(recs):
+        assert np.count_nonzero(_softmax64(rows[r]) > 1e-4) > 64
+        assert rec["count"] == -1 and rec["tok"] == [] and rec["prob"] == []
+        assert rec["argmax"] == int(np.argmax(rows[r]))
+        assert rec["max_logit"] == float(rows[r].max())
