@@ -270,6 +270,8 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
   }
   // (diagnostics: LLMCAD_ATTN_PREFETCH=2 fetches every attention step after the barrier)
   p.attn_prefetch = env_int("LLMCAD_ATTN_PREFETCH", 1) == 2 ? 0 : 1;
+  // (diagnostics: LLMCAD_ROW_TILES=2 turns the row-split tiles off)
+  p.row_tiles = env_int("LLMCAD_ROW_TILES", 1) == 2 ? 0 : 1;
   p.trace = env_int("LLMCAD_TRACE", 0) ? (long long*)(ws + W.trace) : nullptr;
   TimedLaunch tl(LLMCAD_KERNEL_PASS, a.st);
   HIP_TRY(launch_pass(MB, p, tree, a.st));

@@ -110,6 +110,7 @@ struct PassParams {
   // control
   int spin_limit;    // bound of every wait loop (polls)
   int attn_prefetch; // 1: the attention fetches its prefix steps before its barrier (0: all after)
+  int row_tiles;     // 1: GEMM phases of passes of 64+ rows take row-split tiles (waves split rows)
   long long* trace;  // diagnostics: [G][4 + 5L][8] phase timestamps, or null
 };
 

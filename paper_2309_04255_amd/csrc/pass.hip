@@ -617,6 +617,145 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute(KParams&
   return true;
 }
 
+// ---- row-split tiles (passes of 64 or more rows)
+//
+// A K-split tile keeps every wave's accumulators for all MB row blocks, which
+// caps it at a few blocks at 64 and 128 rows, so a workgroup with more blocks
+// than that reads the whole activation matrix once per tile.  Here the waves
+// split the rows instead: wave w owns row blocks [w MB/4, (w + 1) MB/4) of
+// every k-step of the tile's C blocks, so a tile takes up to 8 blocks and its
+// workgroup reads the activations once.  Per k-step wave w loads the weight
+// fragments of blocks w, w + 4 (a quarter of the tile) and its own row
+// blocks' activation fragments through its register pipeline, writes its
+// weight fragments to one of two LDS buffers, and after the workgroup's
+// barrier reads all C of them from there.  No partial sums cross waves: each
+// wave writes its rows' tiles to the one partial-tile slot.
+template <int MB, int C>
+__device__ __attribute__((noinline, not_tail_called)) bool tile_compute_rows(KParams& pin, int step, int layer,
+                                                                            int nb0, int wait_phase, char* lds,
+                                                                            int* lds_flag) {
+  KParams& p = uniform_params(pin);
+  step = wave_uniform(step);
+  layer = wave_uniform(layer);
+  nb0 = wave_uniform(nb0);
+  wait_phase = wave_uniform(wait_phase);
+  const TileIn io = tile_in(p, step, layer);
+  const int wave = wave_index(), lane = threadIdx.x & 63;
+  constexpr int RB = MB / kWaves;              // row blocks per wave
+  constexpr int NW = (C + kWaves - 1) / kWaves;  // weight fragments per wave per k-step
+  static_assert(RB >= 1 && RB * kWaves == MB, "row-split tiles need 4 or 8 row blocks");
+  constexpr int DR = LLMCAD_STAGE_REGS / (NW + RB);
+  constexpr int D = DR < 2 ? 2 : DR > 8 ? 8 : DR;
+  const int ks = wave_uniform(io.ks);
+  const size_t cstride = (size_t)ks * 64;
+  const bf16x8* at = io.a + (size_t)(wave * RB) * 64 + lane;
+  const bf16x8* zero = (const bf16x8*)p.zero + lane;
+  const f32x4* zero4 = (const f32x4*)p.zero + lane;
+  bf16x8 bw[D][NW];
+  bf16x8 ba[D][RB];
+  // this wave's weight fragments: blocks wave + 4 j (j < NW) of the tile
+  auto load_w = [&](int slot, int i) {  // k-step i, or the zero line past the last
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      const int c = wave + kWaves * j;
+      const bool live = i < ks && c < C;
+      bw[slot][j] = ldg_nt(opaque(live ? io.w + ((size_t)(nb0 + c) * ks + i) * 64 + lane : zero));
+    }
+  };
+  auto load_a = [&](int slot, int i) {
+    const bool live = i < ks;
+#pragma unroll
+    for (int r = 0; r < RB; ++r) ba[slot][r] = ldg(opaque(live ? at + ((size_t)i * MB + r) * 64 : zero));
+  };
+  char* wbuf = lds;  // two buffers of C KiB: k-step i's fragments in buffer i % 2, block c at c KiB
+#pragma unroll
+  for (int u = 0; u < D; ++u) load_w(u, u);
+  __builtin_amdgcn_sched_barrier(0);
+  if (wait_phase >= 0) {
+    const Sync sy = make_sync(p, lds_flag);
+    trace_mark(sy, wait_phase, 0);
+    if (!grid_wait(sy, wait_phase, p.G)) return false;
+    trace_mark(sy, wait_phase, 1);
+  }
+#pragma unroll
+  for (int u = 0; u < D; ++u) load_a(u, u);
+  __builtin_amdgcn_sched_barrier(0);
+  if (wait_phase >= 0 && p.trace != nullptr && threadIdx.x == 0)
+    stg(p.trace + (size_t)blockIdx.x * pass_phases(p.L) * 8 + wait_phase * 8 + 3, (long long)wall_clock64());
+  f32x4 acc[RB][C];
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[r][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // one k-step from register stage u: share the weights, multiply, refill
+  auto kstep = [&](int i, int u, bool refill) {
+    char* buf = wbuf + (size_t)(i & 1) * C * 1024;
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      const int c = wave + kWaves * j;
+      if (c < C) lds_st<bf16x8>(buf + (size_t)c * 1024 + lane * 16, bw[u][j]);
+    }
+    lds_barrier();  // (the other buffer's readers are past the previous barrier)
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const bf16x8 b = lds_ld<bf16x8>(buf + (size_t)c * 1024 + lane * 16);
+#pragma unroll
+      for (int r = 0; r < RB; ++r) acc[r][c] = mfma16x16x32(ba[u][r], b, acc[r][c]);
+    }
+    if (refill) {
+      load_w(u, i + D);
+      load_a(u, i + D);
+    }
+  };
+  int i = 0;
+  for (; i + D < ks; i += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) kstep(i + u, u, true);
+  }
+#pragma unroll
+  for (int u = 0; u < D; ++u)
+    if (i + u < ks) kstep(i + u, u, false);
+  lds_barrier();  // (every wave is done with the weight buffers)
+  // this wave's rows -> the one slot: unit (block c, row block rb) at (c MB + rb) KiB
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+      lds_st<f32x4>(lds + tw_off() + ((size_t)(c * MB + wave * RB + r) * 64 + lane) * 16, acc[r][c]);
+  // epilogue inputs (written two or more phases ago): per (block, row block)
+  // the residual rows or the rotary table, then each block's gains
+  char* epi = lds + epi_off(C, MB, 1);
+  const bool resid = io.resid;
+  for (int u = wave; u < C * MB; u += kWaves) {
+    const int c = u / MB, rb = u % MB;
+    const int col0 = kNB * (nb0 + c);
+    const f32x4* src = zero4;
+    if (resid) {
+      src = (const f32x4*)(io.x_in + (size_t)(16 * rb + (lane >> 2)) * p.d + col0 + 4 * (lane & 3));
+    } else if (step == STEP_QKV && col0 < 2 * p.d) {
+      const int t = (col0 % p.d % p.Dh) / kNB;
+      src = (const f32x4*)(p.rope + ((size_t)(16 * rb + (lane >> 2)) * (p.Dh / 2) + 8 * t + 2 * (lane & 3)) * 2);
+    }
+    lds_st<f32x4>(epi + (size_t)u * 1024 + lane * 16, ldg(opaque(src)));
+  }
+  for (int c = wave; c < C; c += kWaves)
+    lds_st<f32x4>(epi + (size_t)(C * MB + c) * 1024 + lane * 16,
+                  ldg(opaque(resid ? (const f32x4*)(io.g_next + kNB * (nb0 + c) + 8 * (lane & 1)) : zero4)));
+  __syncthreads();
+  return true;
+}
+
+template <int MB, int C>
+__device__ __forceinline__ bool tile_dispatch_rows(int cw, KParams& p, int step, int layer, int nb0,
+                                                   int wait_phase, char* lds, int* flag) {
+  if constexpr (C >= 1) {
+    if (cw == C) return tile_compute_rows<MB, C>(p, step, layer, nb0, wait_phase, lds, flag);
+    return tile_dispatch_rows<MB, C - 1>(cw, p, step, layer, nb0, wait_phase, lds, flag);
+  } else {
+    return false;
+  }
+}
+
 // ---- 4-bit weights
 
 // The B operand of one k-step from its dword of packed codes (see pack.hip):
@@ -1420,12 +1559,19 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
                 "a tile's partial sums and epilogue inputs fit the LDS");
   // 4-bit tiles hold a second set of accumulators (each group's partial sums)
   constexpr int CMQ = MB <= 2 ? 6 : MB == 4 ? 2 : 1;
+  // Row-split tiles (up to 8 blocks) for a workgroup of a pass of 64+ rows
+  // whose blocks do not fit one K-split tile: it then reads the activations
+  // once instead of once per tile (where one K-split tile holds them all,
+  // that tile is faster: no barrier per k-step).
+  constexpr int CMR = 8;
+  static_assert(MB < 4 || wl_off(CMR, MB, 1) <= kGemmLdsBytes, "a row-split tile fits the LDS");
   const bool q4 = wave_uniform(sp.q4) != 0;
-  const int cm = q4 ? CMQ : CM;
   const int nbk = sp.nblocks, G = p.G;
   const int vw = virtual_wg(G);
   const int lo = wave_uniform((int)((long)vw * nbk / G));
   const int hi = wave_uniform((int)((long)(vw + 1) * nbk / G));
+  const bool rows = MB >= 4 && !q4 && wave_uniform(p.row_tiles) != 0 && hi - lo > CM;
+  const int cm = q4 ? CMQ : rows ? CMR : CM;
   if constexpr (EPI == EPI_LOGITS) {
     for (int r = threadIdx.x; r < 16 * MB; r += kThreads) {
       gl.best_v[r] = -INFINITY;
@@ -1443,12 +1589,20 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   for (int b0 = lo; b0 < hi; b0 += cm) {
     const int cw = hi - b0 < cm ? hi - b0 : cm;
     const bool first = b0 == lo;
-    const bool ok = q4 ? tile_dispatch_q4<MB, CMQ>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag)
-                       : tile_dispatch<MB, CM>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag, 0,
-                                               sp.ksteps, 1);
+    bool ok;
+    if constexpr (MB >= 4) {
+      ok = q4     ? tile_dispatch_q4<MB, CMQ>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag)
+           : rows ? tile_dispatch_rows<MB, CMR>(cw, p, step, layer, b0, first ? phase : -1, lds, lds_flag)
+                  : tile_dispatch<MB, CM>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag, 0,
+                                          sp.ksteps, 1);
+    } else {
+      ok = q4 ? tile_dispatch_q4<MB, CMQ>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag)
+              : tile_dispatch<MB, CM>(cw, p, step, layer, b0, first ? phase : -1, lds, gl, lds_flag, 0,
+                                      sp.ksteps, 1);
+    }
     if (!ok) return false;
     if (first) trace_mark(sy, phase, 4);
-    finish_tile<MB, EPI>(p, step, layer, b0, cw, lds, gl, q4 ? 4 : tile_slots(cw, MB));
+    finish_tile<MB, EPI>(p, step, layer, b0, cw, lds, gl, q4 ? 4 : rows ? 1 : tile_slots(cw, MB));
   }
   trace_mark(sy, phase, 5);
   if constexpr (EPI == EPI_LOGITS) {

@@ -152,6 +152,30 @@ def test_split_k_variants(model, monkeypatch, tree):
             monkeypatch.delenv(k)
 
 
+@pytest.mark.parametrize("tree", ["b432_n41", "random_n77", "random_n128"])
+def test_row_split_tiles(model, monkeypatch, tree):
+    # Row-split tiles (passes of 64+ rows, workgroups with more blocks than a
+    # K-split tile holds: the waves split the rows and share each k-step's
+    # weight fragments through LDS).  The small models' phases give a
+    # workgroup that many blocks on small grids (on 3 workgroups every step
+    # does; on 24 some).  With them on (the default) and off, the pass meets
+    # the oracle bar and repeats bit for bit; on 3 workgroups the results
+    # differ somewhere (another order of fp32 additions: the path ran, bf16
+    # models).
+    parent = TREES[tree]
+    tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=13)
+    for grid in (24, 3):
+        monkeypatch.setenv("LLMCAD_PASS_GRID", str(grid))
+        monkeypatch.setenv("LLMCAD_ROW_TILES", "2")
+        base = _check_all(model, parent, tok, f"grid {grid} K-split tiles")
+        monkeypatch.delenv("LLMCAD_ROW_TILES")
+        rows = _check_all(model, parent, tok, f"grid {grid} row-split tiles")
+        if model.shape.weight_bits == 16 and grid == 3:
+            assert not np.array_equal(base, rows), "the row-split path did not run"
+        np.testing.assert_array_equal(rows, _run(model, parent, tok)[0])
+        monkeypatch.delenv("LLMCAD_PASS_GRID")
+
+
 def _long_prefix_session(model, PL):
     """A session whose cache holds PL seeded random bf16 prefix keys/values
     (written straight into the cache) and the oracle's copies of them."""
