@@ -668,14 +668,22 @@ __device__ __attribute__((noinline, not_tail_called)) bool tile_compute_rows(KPa
     for (int r = 0; r < RB; ++r) ba[slot][r] = ldg(opaque(live ? at + ((size_t)i * MB + r) * 64 : zero));
   };
   char* wbuf = lds;  // two buffers of C KiB: k-step i's fragments in buffer i % 2, block c at c KiB
+  // Waves 1-3 start their weight stages before the barrier; wave 0 polls it
+  // with no load in flight (a poll waits for every older load of its wave).
+  if (wave != 0) {
 #pragma unroll
-  for (int u = 0; u < D; ++u) load_w(u, u);
+    for (int u = 0; u < D; ++u) load_w(u, u);
+  }
   __builtin_amdgcn_sched_barrier(0);
   if (wait_phase >= 0) {
     const Sync sy = make_sync(p, lds_flag);
     trace_mark(sy, wait_phase, 0);
     if (!grid_wait(sy, wait_phase, p.G)) return false;
     trace_mark(sy, wait_phase, 1);
+  }
+  if (wave == 0) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) load_w(u, u);
   }
 #pragma unroll
   for (int u = 0; u < D; ++u) load_a(u, u);
