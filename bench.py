@@ -102,12 +102,20 @@ def write_traffic(fetch_csv, write_csv, workload, copy_mib):
     chunk_fetch = statistics.median(v for v in fetch[copy] if v > 4096)
     chunk_write = statistics.median(v for v in write[copy] if v > 4096)
     read_factor = chunk_write * write_factor / chunk_fetch
-    # The verification passes are the last launches of the pass kernel in the
-    # run (the prefill's 128-row chunks run before them, as another instance
-    # when the tree has fewer rows): take the instance launched last, and its
-    # launches after the prefill.
-    names = [k for k in fetch if "pass_kernel" in k]
-    passk = max(names, key=lambda k: len(fetch[k]))
+    # The verification passes are the last launches of the pass kernel's
+    # instance for the workload's row count (pass_kernel<16-row blocks, head
+    # dim>; the prefill's 128-row chunks run before them, as another instance
+    # when the tree has fewer rows): take that instance's last launches.
+    import workloads
+
+    wl = workloads.get_workload(workload)
+    n = len(workloads.make_tree(wl.tree, wl.shape.vocab, wl.seed)[0])
+    mb = -(-n // 16)
+    mb = 1 if mb <= 1 else 2 if mb <= 2 else 4 if mb <= 4 else 8
+    names = [k for k in fetch if f"pass_kernel<{mb}, {wl.shape.head_dim}>" in k]
+    if len(names) != 1:
+        raise SystemExit(f"pass kernel instance for {workload} not found: {sorted(fetch)}")
+    passk = names[0]
     f_kib, w_kib = statistics.median(fetch[passk][-3:]), statistics.median(write[passk][-3:])
     out = {
         "workload": workload, "kernel_sources_sha256_16": source_hash(), "kernel": passk[:90],
