@@ -1003,7 +1003,8 @@ template <int MB>
 __device__ __forceinline__ void row_rstd(KParams& p, const float* ssq, GemmLds& gl) {
   // thread t: rows 4 q .. 4 q + 3 (q = t % (ROWS / 4)) of the 16-column blocks
   // of chunk t / (ROWS / 4); 16-byte loads, a batch of them in flight at once
-  constexpr int ROWS = 16 * MB, QUADS = ROWS / 4, CHK = kThreads / QUADS, BATCH = 16;
+  // (a chunk's 4096 columns in one batch at 128 rows)
+  constexpr int ROWS = 16 * MB, QUADS = ROWS / 4, CHK = kThreads / QUADS, BATCH = MB >= 8 ? 32 : 16;
   const int q = threadIdx.x % QUADS, ch = threadIdx.x / QUADS;
   const int dn = p.d_nb;
   const int t0 = ch * dn / CHK, t1 = (ch + 1) * dn / CHK;
