@@ -1815,10 +1815,13 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
   const bf16* qb = p.q + (size_t)layer * p.Mp * p.d;
   bf16* obase = p.o + (size_t)layer * p.Mp * p.d;
   const bf16x8* zero = (const bf16x8*)p.zero + lane;
-  // step range [s_lo, s_hi) of split ks; keys of the split end at lim
+  // step range [s_lo, s_hi) of split ks; keys of the split end at lim.  When
+  // the steps do not divide evenly the first splits take the extra ones: the
+  // last split holds the tree's keys, whose step is only read after the
+  // barrier, and is the one the merge most often waits for.
   auto split_steps = [&](int ks, int& s_lo, int& s_hi, int& lim) {
-    s_lo = ks * nsteps / KS;
-    s_hi = (ks + 1) * nsteps / KS;
+    s_lo = (ks * nsteps + KS - 1) / KS;
+    s_hi = ((ks + 1) * nsteps + KS - 1) / KS;
     lim = 32 * s_hi < limit ? 32 * s_hi : limit;
   };
   // A step can be fetched before the barrier when no cache line it touches
