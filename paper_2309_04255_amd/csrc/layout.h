@@ -47,10 +47,6 @@ inline int pass_rows(int n) {
   return 16 * (mb <= 1 ? 1 : mb <= 2 ? 2 : mb <= 4 ? 4 : 8);
 }
 
-// Column blocks one tile holds at a given count of 16-row blocks: the tile's
-// accumulators (16 per (row block, column block) pair, 4 per lane) stay at 64.
-inline int tile_max_blocks(int mb16) { return mb16 <= 2 ? 8 : 16 / mb16; }
-
 struct Shape {
   int L, d, H, Dh, F, V;
   bool q4;     // layer matrices group-quantised to 4 bits (embedding, LM head and norms bf16)
@@ -127,7 +123,7 @@ enum Step { STEP_QKV = 0, STEP_O = 1, STEP_GATE_UP = 2, STEP_DOWN = 3, STEP_LM =
 
 // Column blocks of each step.  A step's blocks are dealt out in contiguous
 // runs: workgroup w of G takes blocks [w nb / G, (w + 1) nb / G), over the
-// full K, in tiles of at most tile_max_blocks blocks.
+// full K, in tiles of a few blocks each.
 inline int step_blocks(const Shape& s, int step) {
   switch (step) {
     case STEP_QKV: return s.qkv_nb;

@@ -20,17 +20,22 @@
 // GEMM phases (activations X [Mp rows x K], packed weights W [N x K]): the
 // 16-column blocks of a step are dealt out in contiguous runs, one run per
 // workgroup, and every block is computed over the full K by one workgroup,
-// so no partial sum ever leaves the CU: the epilogue follows the main loop
-// directly.  The four waves take interleaved 32-wide k-steps; per k-step a
-// wave loads one 1 KiB weight fragment per block (non-temporal: weights are
-// read once) and one 1 KiB activation fragment per 16-row block -- the
-// activations are stored in MFMA fragment order by the phase that produces
-// them, so that read is one contiguous 1 KiB load that every CU of an XCD
-// shares through L2.  Both streams run through one register pipeline.  The
-// waves' partial tiles meet in LDS and are added in wave order
-// (bit-reproducible).  Inputs of the epilogue that do not depend on the
-// tile (the residual stream, rotary table, norm gains, sums of squares) are
-// copied into LDS by direct global->LDS loads issued before the main loop.
+// so no partial sum leaves the CU and the epilogue follows the main loop
+// directly (except the split-K projections of 64+ row passes, below).  The
+// four waves take interleaved 32-wide k-steps; per k-step a wave loads one
+// 1 KiB weight fragment per block (non-temporal: weights are read once) and
+// one 1 KiB activation fragment per 16-row block -- the activations are
+// stored in MFMA fragment order by the phase that produces them, so that
+// read is one contiguous 1 KiB load that every CU of an XCD shares through
+// L2.  The first weight stages go to LDS by direct global->LDS loads before
+// the barrier; after it, both streams run through one register pipeline.
+// The waves' partial tiles meet in LDS and are added in wave order
+// (bit-reproducible).  Inputs of the epilogue that do not depend on the tile
+// (the residual stream, rotary table, norm gains) are parked in LDS before
+// the barrier.  Passes of 64+ rows add row-split tiles (the waves split the
+// rows and share each weight fragment through LDS) and split-K groups for
+// the projections with one block per workgroup; 4-bit weights have tiles of
+// their own (codes dequantised on the matrix cores).
 //
 // Coherence without cache maintenance: every buffer handed from one phase to
 // the next is written once per pass at its own address with device-coherent
@@ -1549,10 +1554,12 @@ __device__ __attribute__((noinline, not_tail_called)) bool split_phase(KParams& 
   return true;
 }
 
-// One GEMM phase: this workgroup's run of blocks, in tiles of at most
-// tile_max_blocks blocks over the full K, each followed by its epilogue.  The
-// LM head then publishes the workgroup's argmax per row, and the last
-// workgroup to do so runs the accept walk.
+// One GEMM phase: this workgroup's run of blocks, in tiles over the full K
+// (K-split tiles of up to 8, 6 or 4 blocks at 32, 64 or 128 rows; row-split
+// tiles of up to 8 where a run exceeds one K-split tile at 64+ rows; 4-bit
+// tiles of up to 6, 2 or 1), each followed by its epilogue.  The LM head then
+// publishes the workgroup's argmax per row, and the last workgroup to do so
+// runs the accept walk.
 template <int MB, int EPI>
 __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& pin, int step, int layer,
                                                                      int phase, char* lds, GemmLds& gl,
