@@ -124,6 +124,35 @@ __device__ __forceinline__ float row16_sum(float v) {
   v += dpp_f<kDppRowMirror>(v);
   return v;
 }
+// Across rows: the values of lanes l and l ^ 16 (l ^ 32) of the wave, from
+// one gfx950 permlane swap of the value with itself (lane l gets both of its
+// pair, in an order that depends on l), on the vector ALU.
+__device__ __forceinline__ void pair_xor16(float v, float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ void pair_xor32(float v, float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+// Max / sum over lanes l, l ^ 16, l ^ 32, l ^ 48 (a column of the wave's four
+// rows), xor 16 first: the same bits as v op shfl_xor(v, 16), then 32.
+__device__ __forceinline__ float col4_max(float v) {
+  float a, b;
+  pair_xor16(v, a, b);
+  v = fmaxf(a, b);
+  pair_xor32(v, a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float col4_sum(float v) {
+  float a, b;
+  pair_xor16(v, a, b);
+  v = a + b;
+  pair_xor32(v, a, b);
+  return a + b;
+}
 // Max with the lowest index among equal values, over the 16 lanes of each row.
 template <int CTRL>
 __device__ __forceinline__ void argmax_step(float& v, int& idx) {

@@ -1742,34 +1742,54 @@ __device__ __forceinline__ void attn_compute(const AttnStep<DH>& R, const bf16x8
 #pragma unroll
     for (int s = 0; s < NS; ++s) sc[b] = mfma16x16x32(R.f[b * NS + s], qf[s], sc[b]);
   }
+  // With one wave per SIMD a step costs what its instructions cost to issue:
+  // a step of prefix keys only (most of them) skips the mask, and the others
+  // take it branch-free (bitwise, not short-circuit).
   float sv[8];
   float mx = -INFINITY;
+  if (key0 + 32 <= P && key0 + 32 <= lim) {  // (wave-uniform)
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int pos = key0 + 8 * g + e;
-    const int t = pos - P < 0 ? 0 : pos - P;  // (tree slot; any in-range index for prefix keys)
-    const bool vis = pos < lim && (pos < P || ((anc[(t >> 5) & 3] >> (t & 31)) & 1u));
-    sv[e] = vis ? sc[e >> 2][e & 3] * scale_log2 : -INFINITY;
-    mx = fmaxf(mx, sv[e]);
+    for (int e = 0; e < 8; ++e) {
+      sv[e] = sc[e >> 2][e & 3] * scale_log2;
+      mx = fmaxf(mx, sv[e]);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int pos = key0 + 8 * g + e;
+      const int t = pos - P < 0 ? 0 : pos - P;  // (tree slot; any in-range index for prefix keys)
+      const uint32_t w = anc[(t >> 5) & 3];
+      const uint32_t vis = (uint32_t)(pos < lim) & ((uint32_t)(pos < P) | ((w >> (t & 31)) & 1u));
+      sv[e] = vis != 0u ? sc[e >> 2][e & 3] * scale_log2 : -INFINITY;
+      mx = fmaxf(mx, sv[e]);
+    }
   }
-  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+  mx = col4_max(mx);
   const float m_new = fmaxf(m_run, mx);
   const float m_use = m_new == -INFINITY ? 0.0f : m_new;
-  const float alpha = exp2f(m_run - m_use);
+  // (exponentials: the bare instruction; arguments are <= 0, and results
+  // below the normal range count as 0 here)
+  const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
   bf16x8 ph, pl;
   float psum = 0.0f;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const float pe = exp2f(sv[e] - m_use);
+    const float pe = __builtin_amdgcn_exp2f(sv[e] - m_use);
     ph[e] = f2bf(pe);
     pl[e] = f2bf(pe - bf2f(ph[e]));
     psum += pe;
   }
-  psum += __shfl_xor(psum, 16, kWave);
-  psum += __shfl_xor(psum, 32, kWave);
+  psum = col4_sum(psum);
+  // The running output is rescaled only when some lane needs it: a lane whose
+  // maximum did not move (alpha 1) or that has accumulated nothing yet (its
+  // output is 0) is unchanged by it, so skipping is exact.
+  const bool rescale = !__all(alpha == 1.0f || l_run == 0.0f);  // (wave-uniform)
   l_run = l_run * alpha + psum;
   m_run = m_new;
+  if (rescale) {
+#pragma unroll
+    for (int db = 0; db < NB; ++db) oacc[db] = oacc[db] * alpha;
+  }
   const bool edge = key0 + 32 > lim;  // (wave-uniform)
   const int valid = lim - (key0 + 8 * g);
 #pragma unroll
@@ -1779,7 +1799,6 @@ __device__ __forceinline__ void attn_compute(const AttnStep<DH>& R, const bf16x8
 #pragma unroll
       for (int e = 0; e < 8; ++e) a[e] = e < valid ? a[e] : (bf16)0.0f;
     }
-    oacc[db] = oacc[db] * alpha;
     oacc[db] = mfma16x16x32(a, ph, oacc[db]);
     oacc[db] = mfma16x16x32(a, pl, oacc[db]);
   }
@@ -1978,7 +1997,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
         const float m = lds_ld<float>(&mlm[(w * 16 + i) * 2]);
-        const float wt = m == -INFINITY ? 0.0f : exp2f(m - M);
+        const float wt = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m - M);
         L += lds_ld<float>(&mlm[(w * 16 + i) * 2 + 1]) * wt;
         const float2 ov = lds_ld<float2>(&om[(size_t)(w * 16 + i) * DH + dd]);
         o0 += ov.x * wt;
@@ -2034,7 +2053,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool attn_phase(KParams& p
         float L = 0.0f, o0 = 0.0f, o1 = 0.0f;
 #pragma unroll
         for (int s2 = 0; s2 < SO; ++s2) {
-          const float wt = ml[k][s2].x == -INFINITY ? 0.0f : exp2f(ml[k][s2].x - M);
+          const float wt = ml[k][s2].x == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(ml[k][s2].x - M);
           L += ml[k][s2].y * wt;
           o0 += ov[k][s2].x * wt;
           o1 += ov[k][s2].y * wt;
