@@ -214,8 +214,9 @@ def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
     """The generate-and-verify loop (verify, roll back, continue) on the bench
     workload's tree.  Before each iteration the target's own greedy
     continuation from the loop's current context is taken from one-node
-    passes (plain greedy decoding, untimed), and `planted` of its tokens are
-    planted along one deepest branch of the tree, the other nodes uniform.
+    passes (plain greedy decoding, checked against the tree pass's argmax;
+    untimed), and `planted` of its tokens are planted along one deepest
+    branch of the tree, the other nodes uniform.
     Timed per iteration: the verification pass, the rollback kernel and the
     read-back of accept_len / next token that the host needs for the next
     tree.  Also times the rollback kernel alone."""
@@ -226,6 +227,13 @@ def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
 
     n = len(parent)
     leaf = n - 1
+    chain = []  # the planted branch, root .. leaf
+    i = leaf
+    while i != -1:
+        chain.append(i)
+        i = int(parent[i])
+    chain = chain[::-1]
+    depth = min(planted, len(chain) - 1)
 
     def greedy_from(plen, root, k):
         out = []
@@ -235,12 +243,28 @@ def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
             out.append(root)
         return out
 
+    def plant(plen, root, it):
+        # One-node passes and the tree pass add their partial sums in
+        # different orders, so at near-ties (common with random weights)
+        # their greedy tokens can differ: check the planted tokens against the
+        # tree pass's own argmax and fix the first that differs, until none do.
+        cont = greedy_from(plen, root, planted + 1)
+        for _ in range(depth + 1):
+            ptok = workloads.draft_tree(parent, root, cont, planted, leaf, shape.vocab, seed=it)
+            sess.verify_tree(plen, ptok, parent, want_logits=True)
+            sess.outcome()
+            amax = sess.logits[:n].argmax(dim=1).cpu().numpy()
+            bad = [d for d in range(depth) if int(amax[chain[d]]) != int(cont[d])]
+            if not bad:
+                break
+            cont[bad[0]] = int(amax[chain[bad[0]]])
+        return ptok
+
     plen, root = P, int(tok[0])
     accs, t_loop, made = [], 0.0, 0
     last = None
     for it in range(iterations + 1):  # the first iteration warms up
-        cont = greedy_from(plen, root, planted + 1)
-        ptok = workloads.draft_tree(parent, root, cont, planted, leaf, shape.vocab, seed=it)
+        ptok = plant(plen, root, it)
         torch.cuda.synchronize()
         t = time.perf_counter()
         sess.verify_tree(plen, ptok, parent, want_logits=False)
@@ -276,8 +300,8 @@ def decode_loop(sess, shape, P, parent, tok, iterations=12, planted=4):
         "ms_per_iteration": round(t_loop * 1e3 / iterations, 4),
         "accept_lens": accs,
         "draft": (f"{n}-node tree of the workload; {planted} tokens of the target's own greedy continuation "
-                  f"(one-node passes from the loop's context, untimed) planted along one depth-{planted} "
-                  f"branch, the other nodes uniform"),
+                  f"(one-node passes from the loop's context, checked against the tree pass's own argmax; "
+                  f"untimed) planted along one depth-{planted} branch, the other nodes uniform"),
         "iteration": "verify pass + rollback kernel + read back accept_len / next token (host sync)",
         "commit_us": round(commit_us, 2),
         "commit_rows_moved": moved,
