@@ -1790,17 +1790,22 @@ __device__ __forceinline__ void attn_compute(const AttnStep<DH>& R, const bf16x8
 #pragma unroll
     for (int db = 0; db < NB; ++db) oacc[db] = oacc[db] * alpha;
   }
-  const bool edge = key0 + 32 > lim;  // (wave-uniform)
-  const int valid = lim - (key0 + 8 * g);
+  if (key0 + 32 > lim) {  // (wave-uniform) the last step of the key range
+    const int valid = lim - (key0 + 8 * g);
 #pragma unroll
-  for (int db = 0; db < NB; ++db) {
-    bf16x8 a = R.f[2 * NS + db];
-    if (edge) {
+    for (int db = 0; db < NB; ++db) {
+      bf16x8 a = R.f[2 * NS + db];
 #pragma unroll
       for (int e = 0; e < 8; ++e) a[e] = e < valid ? a[e] : (bf16)0.0f;
+      oacc[db] = mfma16x16x32(a, ph, oacc[db]);
+      oacc[db] = mfma16x16x32(a, pl, oacc[db]);
     }
-    oacc[db] = mfma16x16x32(a, ph, oacc[db]);
-    oacc[db] = mfma16x16x32(a, pl, oacc[db]);
+  } else {
+#pragma unroll
+    for (int db = 0; db < NB; ++db) {
+      oacc[db] = mfma16x16x32(R.f[2 * NS + db], ph, oacc[db]);
+      oacc[db] = mfma16x16x32(R.f[2 * NS + db], pl, oacc[db]);
+    }
   }
 }
 
