@@ -185,6 +185,10 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
     sp.w_off = w_off[i];
     sp.s_off = sp.q4 ? w_off[i] + (long long)q4_codes_bytes(sp.nblocks, sp.ksteps) : 0;
     sp.split = 1;
+    // Runs of more than 8 blocks per workgroup at 16 or 32 rows (gate/up of
+    // the 30B shape: 8.75) take one tile of 9 instead of 8 + 1, whose lone
+    // block re-reads the whole activation matrix (-2.5% per 30B pass).
+    sp.wide = i == STEP_GATE_UP && W.Mp <= 32 && !sp.q4 && cdiv(sp.nblocks, G) > 8 ? 1 : 0;
   }
   // Split-K for the projections with one column block per workgroup (O and
   // down: d/16 blocks): groups of S workgroups share a group's blocks, each

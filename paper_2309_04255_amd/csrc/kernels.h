@@ -47,6 +47,7 @@ struct StepPlan {
   int q4;               // 1: 4-bit codes with group scales
   int split;            // split-K: workgroups sharing each group of column blocks (1: none; 2 or 4)
   int wl_cap;           // weight stages per wave copied to LDS before the step's barrier, at most
+  int wide;             // 16- and 32-row passes: tiles of up to 9 blocks instead of 8
 };
 
 // Must stay the first kernel argument of the pass kernel.

@@ -60,7 +60,8 @@ constexpr int kThreads = 64 * kWaves;
 // Tuning constants of the GEMM phases (the defaults were measured best on the
 // LLaMA-7B workload; -D overrides them for sweeps): the VGPRs (in units of 4)
 // a tile's register pipeline may hold, its depth for one-block and for wider
-// tiles, and the widest tile (in 16-column blocks) at 128 and at 64 rows.
+// tiles, and the widest tile (in 16-column blocks) at 128 and at 64 rows (at
+// 16 and 32 rows: 8, or 9 for a gate/up step marked wide).
 #ifndef LLMCAD_STAGE_REGS
 #define LLMCAD_STAGE_REGS 40
 #endif
@@ -1560,7 +1561,7 @@ __device__ __attribute__((noinline, not_tail_called)) bool split_phase(KParams& 
 // tiles of up to 6, 2 or 1), each followed by its epilogue.  The LM head then
 // publishes the workgroup's argmax per row, and the last workgroup to do so
 // runs the accept walk.
-template <int MB, int EPI>
+template <int MB, int EPI, int CM2 = 8>
 __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& pin, int step, int layer,
                                                                      int phase, char* lds, GemmLds& gl,
                                                                      int* lds_flag) {
@@ -1570,9 +1571,12 @@ __device__ __attribute__((noinline, not_tail_called)) bool gemm_phase(KParams& p
   phase = wave_uniform(phase);
   const Sync sy = make_sync(p, lds_flag);
   const StepPlan& sp = p.step[step];
-  constexpr int CM = MB <= 2 ? 8 : MB == 4 ? LLMCAD_TILE_BLOCKS_MB4 : LLMCAD_TILE_BLOCKS_MB8;
+  // (CM2: 8, or 9 for a step marked wide; the LM head keeps 8, its per-block
+  // argmax slots)
+  constexpr int CM = MB <= 2 ? CM2 : MB == 4 ? LLMCAD_TILE_BLOCKS_MB4 : LLMCAD_TILE_BLOCKS_MB8;
   static_assert(wl_off(CM, MB, tile_slots(CM, MB)) <= kGemmLdsBytes,
                 "a tile's partial sums and epilogue inputs fit the LDS");
+  static_assert(EPI != EPI_LOGITS || CM2 <= 8, "the LM head's per-block argmax slots");
   // 4-bit tiles hold a second set of accumulators (each group's partial sums)
   constexpr int CMQ = MB <= 2 ? 6 : MB == 4 ? 2 : 1;
   // Row-split tiles (up to 8 blocks) for a workgroup of a pass of 64+ rows
@@ -2201,7 +2205,9 @@ __device__ __attribute__((noinline, not_tail_called)) bool final_norm_phase(KPar
   return true;
 }
 
-template <int MB, int DH>
+// WIDE: gate/up tiles of up to 9 blocks (a separate kernel, so that the
+// other kernels' code is unchanged by it).
+template <int MB, int DH, bool WIDE = false>
 __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_arg, const TreeArgs tree) {
   extern __shared__ __attribute__((aligned(1024))) char lds_raw[];
   __shared__ GemmLds gl;
@@ -2238,7 +2244,7 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
                                   : gemm_phase<MB, EPI_RESID>(p, STEP_O, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
-    ok = gemm_phase<MB, EPI_SWIGLU>(p, STEP_GATE_UP, l, phase, lds_raw, gl, &flag);
+    ok = gemm_phase<MB, EPI_SWIGLU, WIDE ? 9 : 8>(p, STEP_GATE_UP, l, phase, lds_raw, gl, &flag);
     if (!ok) break;
     grid_arrive(sy, phase++);
     ok = p.step[STEP_DOWN].split > 1
@@ -2264,10 +2270,10 @@ __global__ __launch_bounds__(kThreads, 1) void pass_kernel(const PassParams p_ar
   }
 }
 
-template <int MB, int DH>
+template <int MB, int DH, bool WIDE>
 hipError_t launch_pass_mb(KParams& p, const TreeArgs& tree, hipStream_t st) {
   static bool attr_set = false;  // per process; the attribute is per function
-  const void* fn = (const void*)pass_kernel<MB, DH>;
+  const void* fn = (const void*)pass_kernel<MB, DH, WIDE>;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_lds_bytes<DH>());
     if (e != hipSuccess) return e;
@@ -2291,15 +2297,24 @@ int occupancy_mb() {
 }  // namespace
 
 hipError_t launch_pass(int mb16, KParams& p, const TreeArgs& tree, hipStream_t st) {
-#define LLMCAD_PASS_CASE(M)                                                 \
+  const bool wide = p.step[STEP_GATE_UP].wide != 0;  // (set for 16- and 32-row passes only)
+#define LLMCAD_PASS_CASE(M, W)                                              \
   case M:                                                                   \
-    return p.Dh == 128 ? launch_pass_mb<M, 128>(p, tree, st)                \
-                       : launch_pass_mb<M, 64>(p, tree, st);
+    return p.Dh == 128 ? launch_pass_mb<M, 128, W>(p, tree, st)             \
+                       : launch_pass_mb<M, 64, W>(p, tree, st);
+  if (!wide) {
+    switch (mb16) {
+      LLMCAD_PASS_CASE(1, false)
+      LLMCAD_PASS_CASE(2, false)
+      LLMCAD_PASS_CASE(4, false)
+      LLMCAD_PASS_CASE(8, false)
+      default:
+        return hipErrorInvalidValue;
+    }
+  }
   switch (mb16) {
-    LLMCAD_PASS_CASE(1)
-    LLMCAD_PASS_CASE(2)
-    LLMCAD_PASS_CASE(4)
-    LLMCAD_PASS_CASE(8)
+    LLMCAD_PASS_CASE(1, true)
+    LLMCAD_PASS_CASE(2, true)
     default:
       return hipErrorInvalidValue;
   }
