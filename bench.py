@@ -21,6 +21,7 @@ Progress goes to stderr.
 import argparse
 import hashlib
 import json
+import re
 import os
 import statistics
 import sys
@@ -104,15 +105,17 @@ def write_traffic(fetch_csv, write_csv, workload, copy_mib):
     read_factor = chunk_write * write_factor / chunk_fetch
     # The verification passes are the last launches of the pass kernel's
     # instance for the workload's row count (pass_kernel<16-row blocks, head
-    # dim>; the prefill's 128-row chunks run before them, as another instance
-    # when the tree has fewer rows): take that instance's last launches.
+    # dim, wide gate/up tiles>; the prefill's 128-row chunks run before them,
+    # as another instance when the tree has fewer rows): take that
+    # instance's last launches.
     import workloads
 
     wl = workloads.get_workload(workload)
     n = len(workloads.make_tree(wl.tree, wl.shape.vocab, wl.seed)[0])
     mb = -(-n // 16)
     mb = 1 if mb <= 1 else 2 if mb <= 2 else 4 if mb <= 4 else 8
-    names = [k for k in fetch if f"pass_kernel<{mb}, {wl.shape.head_dim}>" in k]
+    inst = re.compile(rf"pass_kernel<{mb}, {wl.shape.head_dim}(, (true|false))?>")
+    names = [k for k in fetch if inst.search(k)]
     if len(names) != 1:
         raise SystemExit(f"pass kernel instance for {workload} not found: {sorted(fetch)}")
     passk = names[0]
