@@ -131,13 +131,22 @@ int pass_grid() {
   return G > kPassMaxGrid ? kPassMaxGrid : G;
 }
 
+// Runs of more than 8 gate/up blocks per workgroup at 16 or 32 rows (the
+// 30B shape: 8.75) take one tile of 9 instead of 8 + 1, whose lone block
+// re-reads the whole activation matrix (-2.5% per 30B pass): the pass then
+// runs the kernel instance with wide gate/up tiles.
+bool gate_up_wide(const Shape& s, int Mp, int G) {
+  return Mp <= 32 && !s.q4 && cdiv(step_blocks(s, STEP_GATE_UP), G) > 8;
+}
+
 int run_pass(const Pass& a, const TreeArgs& tree) {
   const Shape s(*a.cfg);
   const PackedLayout P(s);
   const int G = pass_grid();
   const WorkspaceLayout W(s, a.n, G);
   const int MB = W.Mp / 16;
-  const int occ = pass_occupancy(MB, s.Dh);
+  const bool wide = gate_up_wide(s, W.Mp, G);
+  const int occ = pass_occupancy(MB, s.Dh, wide);
   if (device_info().cus <= 0 || occ * device_info().cus < G) {
     g_last_error = hipErrorInvalidConfiguration;
     return LLMCAD_EHIP;
@@ -185,10 +194,7 @@ int run_pass(const Pass& a, const TreeArgs& tree) {
     sp.w_off = w_off[i];
     sp.s_off = sp.q4 ? w_off[i] + (long long)q4_codes_bytes(sp.nblocks, sp.ksteps) : 0;
     sp.split = 1;
-    // Runs of more than 8 blocks per workgroup at 16 or 32 rows (gate/up of
-    // the 30B shape: 8.75) take one tile of 9 instead of 8 + 1, whose lone
-    // block re-reads the whole activation matrix (-2.5% per 30B pass).
-    sp.wide = i == STEP_GATE_UP && W.Mp <= 32 && !sp.q4 && cdiv(sp.nblocks, G) > 8 ? 1 : 0;
+    sp.wide = i == STEP_GATE_UP && wide ? 1 : 0;
   }
   // Split-K for the projections with one column block per workgroup (O and
   // down: d/16 blocks): groups of S workgroups share a group's blocks, each

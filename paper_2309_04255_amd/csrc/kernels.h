@@ -117,7 +117,7 @@ struct PassParams {
 
 // mb16: 16-row blocks of the pass (Mp / 16: 1, 2, 4 or 8).
 hipError_t launch_pass(int mb16, const PassParams& p, const TreeArgs& tree, hipStream_t st);
-int pass_occupancy(int mb16, int dh);  // resident workgroups per CU (0 if unavailable)
+int pass_occupancy(int mb16, int dh, bool wide);  // resident workgroups per CU (0 if unavailable)
 size_t pass_lds_bytes(int mb16, int dh);
 
 

@@ -2283,9 +2283,9 @@ hipError_t launch_pass_mb(KParams& p, const TreeArgs& tree, hipStream_t st) {
   return hipLaunchCooperativeKernel(fn, dim3(p.G), dim3(kThreads), args, (unsigned)dyn_lds_bytes<DH>(), st);
 }
 
-template <int MB, int DH>
+template <int MB, int DH, bool WIDE>
 int occupancy_mb() {
-  const void* fn = (const void*)pass_kernel<MB, DH>;
+  const void* fn = (const void*)pass_kernel<MB, DH, WIDE>;
   if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_lds_bytes<DH>()) != hipSuccess)
     return 0;
   int blocks = 0;
@@ -2321,15 +2321,23 @@ hipError_t launch_pass(int mb16, KParams& p, const TreeArgs& tree, hipStream_t s
 #undef LLMCAD_PASS_CASE
 }
 
-int pass_occupancy(int mb16, int dh) {
-#define LLMCAD_OCC_CASE(M) \
-  case M:                  \
-    return dh == 128 ? occupancy_mb<M, 128>() : occupancy_mb<M, 64>();
+int pass_occupancy(int mb16, int dh, bool wide) {
+#define LLMCAD_OCC_CASE(M, W) \
+  case M:                     \
+    return dh == 128 ? occupancy_mb<M, 128, W>() : occupancy_mb<M, 64, W>();
+  if (!wide) {
+    switch (mb16) {
+      LLMCAD_OCC_CASE(1, false)
+      LLMCAD_OCC_CASE(2, false)
+      LLMCAD_OCC_CASE(4, false)
+      LLMCAD_OCC_CASE(8, false)
+      default:
+        return 0;
+    }
+  }
   switch (mb16) {
-    LLMCAD_OCC_CASE(1)
-    LLMCAD_OCC_CASE(2)
-    LLMCAD_OCC_CASE(4)
-    LLMCAD_OCC_CASE(8)
+    LLMCAD_OCC_CASE(1, true)
+    LLMCAD_OCC_CASE(2, true)
     default:
       return 0;
   }
