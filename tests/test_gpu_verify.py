@@ -124,6 +124,21 @@ def test_launch_shape_variants(model, monkeypatch):
             monkeypatch.delenv(k)
 
 
+def test_wide_gate_up_tiles(model, monkeypatch):
+    # Passes of up to 32 rows whose gate/up runs exceed 8 blocks per
+    # workgroup take tiles of up to 9 blocks (a separate kernel instance).
+    # Small grids force it on the test models: 9 blocks per workgroup (one
+    # tile), 10 (9 + 1) and ~43 (several tiles and a ragged last one).
+    parent = TREES["binary_d4_n31"]
+    tok = workloads.draw_tokens(len(parent), model.shape.vocab, seed=11)
+    Fp = -(-model.shape.d_ffn // 32) * 32
+    grids = sorted({-(-(Fp // 8) // 9), -(-(Fp // 8) // 10), 3})
+    for G in grids:
+        monkeypatch.setenv("LLMCAD_PASS_GRID", str(G))
+        _check_all(model, parent, tok, f"grid {G}")
+    monkeypatch.delenv("LLMCAD_PASS_GRID")
+
+
 @pytest.mark.parametrize("tree", ["binary_d4_n31", "b432_n41", "random_n77", "random_n128"])
 def test_split_k_variants(model, monkeypatch, tree):
     # Split-K for the O and down projections (passes of 32 or more rows):
